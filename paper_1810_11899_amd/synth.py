@@ -1,0 +1,286 @@
+"""Seeded synthetic inputs for the graph-sampling GCN layer (arXiv 1810.11899).
+
+This module only *draws* inputs: subgraph CSR patterns with their mean weights,
+vertex features, Glorot weights, labels.  It holds none of the layer's
+arithmetic, and it is the single source of inputs for both the HIP library and
+the CPU oracle, which never import each other.
+
+The paper trains on frontier-sampled subgraphs of PPI, Reddit, Yelp and Amazon
+(Sec. VI-A, Table I).  Those datasets are not available, so every workload here
+is synthetic and stands in for them: Erdos-Renyi or R-MAT subgraphs (R-MAT for
+the skewed, power-law degree mix that sampled social/product graphs have), with
+the attribute widths and class counts of Table I and the hidden width 512 of
+Sec. VI-C.  All graphs are undirected, without self-loops or duplicate edges;
+the stored CSR is symmetric in pattern and row-normalised in value
+(``vals[p] = 1/deg(row)``, the mean of Sec. II), which is how the per-subgraph
+aggregation matrix is handed to the layer.
+
+Random streams: ``np.random.SeedSequence([181011899, cfg, s, ...])`` spawned
+into children in a fixed order (graph, relabel, H, weights, labels, degree);
+PCG64 output is platform independent, so the same seed gives bitwise equal
+arrays on every machine.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import List, Optional, Tuple
+
+import numpy as np
+
+SEED_ROOT = 181011899
+RMAT_ABC = (0.57, 0.19, 0.19)  # d = 0.05
+
+
+# --------------------------------------------------------------------------
+# graphs
+# --------------------------------------------------------------------------
+@dataclass
+class Graph:
+    """CSR of the aggregation matrix: row i = destination vertex i."""
+    n: int
+    indptr: np.ndarray   # int32 [n+1]
+    indices: np.ndarray  # int32 [nnz], ascending within a row
+    vals: np.ndarray     # float32 [nnz]
+
+    @property
+    def nnz(self) -> int:
+        return int(self.indices.shape[0])
+
+    def degrees(self) -> np.ndarray:
+        return np.diff(self.indptr.astype(np.int64))
+
+
+def _mean_values(indptr: np.ndarray) -> np.ndarray:
+    """float32(1/deg(row)) for every stored entry, as an IEEE float32 quotient."""
+    deg = np.diff(indptr.astype(np.int64))
+    per_row = np.zeros(deg.shape[0], dtype=np.float32)
+    nz = deg > 0
+    per_row[nz] = np.float32(1.0) / deg[nz].astype(np.float32)
+    return np.repeat(per_row, deg)
+
+
+def csr_from_pairs(n: int, rows: np.ndarray, cols: np.ndarray,
+                   vals: Optional[np.ndarray] = None) -> Graph:
+    """Directed (row, col) pairs -> CSR sorted by (row, col).
+
+    With ``vals=None`` the values are the mean weights 1/deg(row); otherwise the
+    given values travel with their pairs.  Duplicates are kept as given.
+    """
+    rows = np.asarray(rows, dtype=np.int64)
+    cols = np.asarray(cols, dtype=np.int64)
+    order = np.lexsort((cols, rows))
+    rows, cols = rows[order], cols[order]
+    counts = np.bincount(rows, minlength=n) if rows.size else np.zeros(n, np.int64)
+    indptr = np.zeros(n + 1, dtype=np.int64)
+    np.cumsum(counts, out=indptr[1:])
+    if vals is None:
+        v = _mean_values(indptr)
+    else:
+        v = np.asarray(vals, dtype=np.float32)[order]
+    return Graph(n, indptr.astype(np.int32), cols.astype(np.int32), v.astype(np.float32))
+
+
+def csr_from_undirected(n: int, u: np.ndarray, v: np.ndarray) -> Graph:
+    """Undirected edge list (no self-loops, no duplicates) -> symmetric CSR."""
+    u = np.asarray(u, dtype=np.int64)
+    v = np.asarray(v, dtype=np.int64)
+    return csr_from_pairs(n, np.concatenate([u, v]), np.concatenate([v, u]))
+
+
+def _first_unique(keys: np.ndarray) -> np.ndarray:
+    """Distinct keys in order of first appearance."""
+    _, first = np.unique(keys, return_index=True)
+    return keys[np.sort(first)]
+
+
+def _fill_edges(draw, n: int, m: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Keep drawing canonical (min,max) pairs until m distinct ones exist."""
+    keys = np.zeros(0, dtype=np.int64)
+    while keys.size < m:
+        need = m - keys.size
+        u, v = draw(2 * need + 1024)
+        ok = (u < n) & (v < n) & (u != v)
+        u, v = u[ok], v[ok]
+        lo, hi = np.minimum(u, v), np.maximum(u, v)
+        keys = _first_unique(np.concatenate([keys, lo * n + hi]))
+    keys = keys[:m]
+    return keys // n, keys % n
+
+
+def erdos_renyi(rng: np.random.Generator, n: int, m: int):
+    """G(n, m): m distinct unordered pairs drawn uniformly."""
+    def draw(k):
+        return rng.integers(0, n, size=k), rng.integers(0, n, size=k)
+    return _fill_edges(draw, n, m)
+
+
+def rmat(rng: np.random.Generator, n: int, m: int, abc=RMAT_ABC):
+    """R-MAT with quadrant probabilities (a, b, c, 1-a-b-c), no noise."""
+    a, b, c = abc
+    scale = max(1, int(math.ceil(math.log2(max(n, 2)))))
+
+    def draw(k):
+        u = np.zeros(k, dtype=np.int64)
+        v = np.zeros(k, dtype=np.int64)
+        for _ in range(scale):
+            r = rng.random(k)
+            bu = (r >= a + b).astype(np.int64)            # quadrants c, d: lower half
+            bv = ((r >= a) & (r < a + b)) | (r >= a + b + c)  # quadrants b, d: right half
+            u = (u << 1) | bu
+            v = (v << 1) | bv.astype(np.int64)
+        return u, v
+    return _fill_edges(draw, n, m)
+
+
+def make_graph(kind: str, n: int, d: int, rng_graph: np.random.Generator,
+               rng_relabel: np.random.Generator) -> Graph:
+    """Undirected graph with exactly n*d/2 edges, vertex ids randomly relabelled."""
+    m = (n * d) // 2
+    if kind == "er":
+        u, v = erdos_renyi(rng_graph, n, m)
+    elif kind == "rmat":
+        u, v = rmat(rng_graph, n, m)
+    else:
+        raise ValueError(f"unknown graph kind {kind!r}")
+    perm = rng_relabel.permutation(n).astype(np.int64)
+    return csr_from_undirected(n, perm[u], perm[v])
+
+
+# special graphs used by tests --------------------------------------------
+def permutation_graph(n: int, rng: np.random.Generator) -> Graph:
+    """Each row holds exactly one entry, 1.0, at a random permuted column."""
+    p = rng.permutation(n)
+    return csr_from_pairs(n, np.arange(n), p, np.ones(n, np.float32))
+
+
+def complete_graph(n: int) -> Graph:
+    i, j = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    keep = i != j
+    return csr_from_pairs(n, i[keep], j[keep])
+
+
+def star_graph(n: int) -> Graph:
+    """Vertex 0 joined to all others: one row of length n-1, the rest of length 1."""
+    leaves = np.arange(1, n)
+    return csr_from_undirected(n, np.zeros(n - 1, np.int64), leaves)
+
+
+def empty_graph(n: int) -> Graph:
+    return Graph(n, np.zeros(n + 1, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+
+
+# --------------------------------------------------------------------------
+# workloads
+# --------------------------------------------------------------------------
+@dataclass
+class Spec:
+    """A GCN fwd+bwd workload on one sampled subgraph."""
+    name: str
+    n: int
+    graph: str                      # "er" | "rmat"
+    d: int                          # average degree (nnz = n*d)
+    layers: List[Tuple[int, int]]   # (f_in, h) per layer; output width 2h
+    head: Optional[str]             # None (dY given) | "ce" | "bce"
+    classes: int = 0
+    label_p: float = 0.1            # Bernoulli rate for BCE targets
+    d_range: Optional[Tuple[int, int]] = None  # per-subgraph degree draw (epoch stream)
+    subgraphs: int = 1
+
+
+@dataclass
+class Layer:
+    W_self: np.ndarray   # float32 [f_in, h]
+    W_neigh: np.ndarray  # float32 [f_in, h]
+    bias: np.ndarray     # float32 [2h]
+
+    @property
+    def f_in(self) -> int:
+        return self.W_self.shape[0]
+
+    @property
+    def h(self) -> int:
+        return self.W_self.shape[1]
+
+
+@dataclass
+class Workload:
+    spec: Spec
+    s: int
+    graph: Graph
+    H: np.ndarray                     # float32 [n, f_in(1)]
+    layers: List[Layer]
+    W_pred: Optional[np.ndarray] = None   # float32 [2h_L, C]
+    b_pred: Optional[np.ndarray] = None   # float32 [C]
+    labels: Optional[np.ndarray] = None   # int32 [n]           (ce)
+    targets: Optional[np.ndarray] = None  # float32 [n, C] {0,1} (bce)
+    dY: Optional[np.ndarray] = None       # float32 [n, 2h_L]    (no head)
+    d: int = 0
+
+    @property
+    def n(self) -> int:
+        return self.graph.n
+
+
+def glorot(rng: np.random.Generator, fan_in: int, fan_out: int) -> np.ndarray:
+    a = math.sqrt(6.0 / (fan_in + fan_out))
+    return rng.uniform(-a, a, size=(fan_in, fan_out)).astype(np.float32)
+
+
+def build(spec: Spec, s: int = 0, cfg_key: int = 99, n: Optional[int] = None) -> Workload:
+    """Draw one seeded workload.  ``n`` overrides the vertex count (same family)."""
+    n_eff = spec.n if n is None else int(n)
+    key = [SEED_ROOT, cfg_key, s] + ([n_eff] if n is not None else [])
+    children = np.random.SeedSequence(key).spawn(6)
+    rg_graph, rg_relabel, rg_h, rg_w, rg_lab, rg_deg = (
+        np.random.Generator(np.random.PCG64(c)) for c in children)
+    d = spec.d
+    if spec.d_range is not None:
+        d = int(rg_deg.integers(spec.d_range[0], spec.d_range[1] + 1))
+    g = make_graph(spec.graph, n_eff, d, rg_graph, rg_relabel)
+    f0 = spec.layers[0][0]
+    H = rg_h.standard_normal((n_eff, f0), dtype=np.float32)
+    layers = []
+    for (f_in, h) in spec.layers:
+        Ws = glorot(rg_w, f_in, h)
+        Wn = glorot(rg_w, f_in, h)
+        layers.append(Layer(Ws, Wn, np.zeros(2 * h, np.float32)))
+    wl = Workload(spec, s, g, H, layers, d=d)
+    hl2 = 2 * spec.layers[-1][1]
+    if spec.head is None:
+        wl.dY = rg_lab.standard_normal((n_eff, hl2), dtype=np.float32)
+    else:
+        C = spec.classes
+        wl.W_pred = glorot(rg_w, hl2, C)
+        wl.b_pred = np.zeros(C, np.float32)
+        if spec.head == "ce":
+            wl.labels = rg_lab.integers(0, C, size=n_eff).astype(np.int32)
+        elif spec.head == "bce":
+            wl.targets = (rg_lab.random((n_eff, C)) < spec.label_p).astype(np.float32)
+        else:
+            raise ValueError(spec.head)
+    return wl
+
+
+# The five workloads.  Attribute widths / class counts follow Table I
+# (PPI 50, Reddit 602/41 single-label, Yelp 300/100 multi-label, Amazon 200),
+# the hidden width 512 follows Sec. VI-C.
+CONFIGS = {
+    0: Spec("er2000_d15_50x64_givendY", 2000, "er", 15, [(50, 64)], None),
+    1: Spec("rmat8000_d20_602-128-128_ce41", 8000, "rmat", 20, [(602, 128), (256, 128)], "ce", 41),
+    2: Spec("rmat16000_d30_300-256x3_bce100", 16000, "rmat", 30,
+            [(300, 256), (512, 256), (512, 256)], "bce", 100),
+    3: Spec("rmat65536_d50_512-512-512_ce100", 65536, "rmat", 50, [(512, 512), (1024, 512)], "ce", 100),
+    4: Spec("stream200_rmat50000_d30-50_200-512x3_ce50", 50000, "rmat", 40,
+            [(200, 512), (1024, 512), (1024, 512)], "ce", 50, d_range=(30, 50), subgraphs=200),
+}
+
+
+def config(cfg: int, s: int = 0, n: Optional[int] = None) -> Workload:
+    return build(CONFIGS[cfg], s=s, cfg_key=cfg, n=n)
+
+
+def custom(n: int, graph: str, d: int, layers, head=None, classes=0, seed: int = 0) -> Workload:
+    """Small workloads for tests (ragged sizes spanning several tiles)."""
+    spec = Spec(f"custom_{graph}{n}_d{d}", n, graph, d, list(layers), head, classes)
+    return build(spec, s=seed, cfg_key=1000)

@@ -1,0 +1,329 @@
+"""Pins for the CPU oracle against what the paper and the mathematics fix.
+
+None of these re-types the oracle's own expressions: each checks a value that
+is fixed independently (exact rational brute force, closed forms, invariants,
+special cases that reduce to a library routine, finite differences), chosen so
+that a plausible slip in the oracle (a dropped term, a wrong sign or index, a
+transposed operand, a swapped concat half) fails at least one of them.
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.sparse as sp
+
+import oracle
+from oracle import bf16 as obf16
+from paper_1810_11899_amd import synth
+
+
+def rel(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    den = max(np.abs(b).max(), 1e-300) if b.size else 1.0
+    return float(np.abs(a - b).max() / den) if b.size else 0.0
+
+
+# ---------------------------------------------------------------- forward ----
+def test_exact_rational_layer_forward():
+    """Tiny graph, small-integer inputs: the layer of Sec. II in exact rationals."""
+    rng = np.random.default_rng(3)
+    n, f, h = 7, 3, 2
+    # a small directed pattern with varied degrees and one empty row
+    pairs = [(0, 1), (0, 2), (0, 5), (1, 0), (2, 3), (2, 4), (2, 6), (2, 1), (3, 2),
+             (5, 6), (5, 0), (6, 4)]
+    rows, cols = zip(*pairs)
+    g = synth.csr_from_pairs(n, np.array(rows), np.array(cols))
+    H = rng.integers(-4, 5, size=(n, f)).astype(np.float32)
+    Ws = rng.integers(-3, 4, size=(f, h)).astype(np.float32)
+    Wn = rng.integers(-3, 4, size=(f, h)).astype(np.float32)
+    b = np.array([1, -2, 0, 3], np.float32)
+    Y, cache = oracle.layer_fwd(g, H, Ws, Wn, b)
+    # the stored weights are float32(1/deg); the layer applies exactly those values
+    ent = {i: [(int(g.indices[p]), Fraction(float(g.vals[p])))
+               for p in range(g.indptr[i], g.indptr[i + 1])] for i in range(n)}
+    for i in range(n):
+        assert sorted(j for j, _ in ent[i]) == sorted(c for (r, c) in pairs if r == i)
+        agg = [sum((w * int(H[j, c]) for j, w in ent[i]), Fraction(0)) for c in range(f)]
+        for o in range(h):
+            s = sum(Fraction(int(H[i, c])) * int(Ws[c, o]) for c in range(f)) + int(b[o])
+            nn = sum(agg[c] * int(Wn[c, o]) for c in range(f)) + int(b[h + o])
+            assert abs(Y[i, o] - float(max(s, 0))) <= 1e-12 * (1 + abs(float(s)))
+            assert abs(Y[i, h + o] - float(max(nn, 0))) <= 1e-12 * (1 + abs(float(nn)))
+            assert abs(cache.AGG[i, 0] - float(agg[0])) <= 1e-12 * (1 + abs(float(agg[0])))
+
+
+def test_constant_features_mean_invariant():
+    """Mean aggregation of constant features returns the constant (0 on empty rows)."""
+    wl = synth.custom(3000, "rmat", 16, [(4, 4)])
+    g = wl.graph
+    c = np.array([1.5, -2.25, 1e3, 7.0])
+    X = np.tile(c, (g.n, 1))
+    out = oracle.aggregate(g.indptr, g.indices, g.vals, X)
+    deg = g.degrees()
+    assert np.all(out[deg == 0] == 0.0)
+    nz = deg > 0
+    err = np.abs(out[nz] - c[None, :]) / np.abs(c)[None, :]
+    # float32(1/d) carries a relative error <= 2^-24; d of them add up to within ~d 2^-24
+    assert np.all(err <= (deg[nz, None] + 4) * 2.0 ** -23)
+
+
+def test_permutation_graph_is_exact_gather():
+    rng = np.random.default_rng(5)
+    g = synth.permutation_graph(257, rng)
+    X = rng.standard_normal((257, 9))
+    out = oracle.aggregate(g.indptr, g.indices, g.vals, X)
+    assert np.array_equal(out, X[g.indices])
+
+
+def test_complete_graph_closed_form():
+    n = 23
+    g = synth.complete_graph(n)
+    X = np.random.default_rng(2).standard_normal((n, 5))
+    out = oracle.aggregate(g.indptr, g.indices, g.vals, X)
+    expect = (X.sum(axis=0)[None, :] - X) / (n - 1)
+    assert rel(out, expect) < 1e-6  # vals are float32(1/(n-1))
+
+
+def test_empty_graph_reduces_to_dense_layer():
+    rng = np.random.default_rng(7)
+    n, f, h = 40, 6, 5
+    g = synth.empty_graph(n)
+    H = rng.standard_normal((n, f)).astype(np.float32)
+    Ws = rng.standard_normal((f, h)).astype(np.float32)
+    Wn = rng.standard_normal((f, h)).astype(np.float32)
+    b = rng.standard_normal(2 * h).astype(np.float32)
+    Y, _ = oracle.layer_fwd(g, H, Ws, Wn, b)
+    import torch  # a library linear layer as the independent reference
+    lin = torch.nn.functional.linear(torch.tensor(H, dtype=torch.float64),
+                                     torch.tensor(Ws.T, dtype=torch.float64),
+                                     torch.tensor(b[:h], dtype=torch.float64))
+    assert rel(Y[:, :h], torch.relu(lin).numpy()) < 1e-14
+    assert np.array_equal(Y[:, h:], np.tile(np.maximum(b[h:], 0), (n, 1)).astype(np.float64))
+
+
+def test_dense_brute_force_small_graphs():
+    """Against a scipy dense product of the densified matrix, n <= 64."""
+    for seed in range(3):
+        wl = synth.custom(61, "rmat", 6, [(7, 5)], seed=seed)
+        g = wl.graph
+        A = sp.csr_matrix((g.vals.astype(np.float64), g.indices, g.indptr), shape=(g.n, g.n)).toarray()
+        lay = wl.layers[0]
+        b = np.random.default_rng(seed).standard_normal(10).astype(np.float32)
+        Y, cache = oracle.layer_fwd(g, wl.H, lay.W_self, lay.W_neigh, b)
+        N = np.linalg.multi_dot([A, wl.H.astype(np.float64), lay.W_neigh.astype(np.float64)])
+        S = wl.H.astype(np.float64) @ lay.W_self.astype(np.float64)
+        assert rel(Y[:, 5:], np.maximum(N + b[5:], 0)) < 1e-12
+        assert rel(Y[:, :5], np.maximum(S + b[:5], 0)) < 1e-12
+
+
+def test_linearity_of_aggregation():
+    wl = synth.custom(500, "rmat", 10, [(3, 3)])
+    g = wl.graph
+    rng = np.random.default_rng(1)
+    X, Z = rng.standard_normal((500, 6)), rng.standard_normal((500, 6))
+    lhs = oracle.aggregate(g.indptr, g.indices, g.vals, 2.5 * X - 0.75 * Z)
+    rhs = 2.5 * oracle.aggregate(g.indptr, g.indices, g.vals, X) - 0.75 * oracle.aggregate(
+        g.indptr, g.indices, g.vals, Z)
+    assert rel(lhs, rhs) < 1e-13
+
+
+def test_permutation_equivariance_of_step():
+    wl = synth.custom(120, "rmat", 8, [(6, 4), (8, 3)], head="ce", classes=5, seed=4)
+    base = oracle.step(wl, first_layer_dH=True)
+    rng = np.random.default_rng(11)
+    P = rng.permutation(wl.n)          # new id of old vertex v is P[v]
+    inv = np.argsort(P)
+    g = wl.graph
+    rows = np.repeat(np.arange(wl.n), g.degrees())
+    g2 = synth.csr_from_pairs(wl.n, P[rows], P[g.indices], g.vals)
+    import copy
+    wl2 = copy.deepcopy(wl)
+    wl2.graph = g2
+    wl2.H = wl.H[inv]
+    wl2.labels = wl.labels[inv]
+    r2 = oracle.step(wl2, first_layer_dH=True)
+    for a, b in zip(base.Y, r2.Y):
+        assert rel(b, a[inv]) < 1e-12
+    for li in range(2):
+        assert rel(r2.dW_self[li], base.dW_self[li]) < 1e-11
+        assert rel(r2.dW_neigh[li], base.dW_neigh[li]) < 1e-11
+        assert rel(r2.dH[li], base.dH[li][inv]) < 1e-11
+    assert abs(r2.loss - base.loss) < 1e-12
+
+
+# -------------------------------------------------------------- transpose ----
+def test_transpose_matches_scipy_and_is_an_involution():
+    wl = synth.custom(700, "rmat", 9, [(2, 2)])
+    g = wl.graph
+    # non-symmetric values (row-normalised) make the value check meaningful
+    ti, tj, tv = oracle.csr_transpose(g.n, g.n, g.indptr, g.indices, g.vals)
+    ref = sp.csr_matrix((g.vals, g.indices, g.indptr), shape=(g.n, g.n)).T.tocsr()
+    assert np.array_equal(ti, ref.indptr) and np.array_equal(tj, ref.indices)
+    assert np.array_equal(tv.view(np.uint32), ref.data.astype(np.float32).view(np.uint32))
+    bi, bj, bv = oracle.csr_transpose(g.n, g.n, ti, tj, tv)
+    assert np.array_equal(bi, g.indptr) and np.array_equal(bj, g.indices)
+    assert np.array_equal(bv.view(np.uint32), g.vals.view(np.uint32))
+    # undirected graph: same pattern; row lengths of A^T are column counts of A
+    assert np.array_equal(ti, g.indptr) and np.array_equal(tj, g.indices)
+    assert np.array_equal(np.diff(ti), np.bincount(g.indices, minlength=g.n))
+
+
+def test_transpose_rectangular_and_empty():
+    rows = np.array([0, 0, 2, 2, 2])
+    cols = np.array([4, 1, 0, 1, 3])
+    g = synth.csr_from_pairs(3, rows, cols, np.arange(5, dtype=np.float32))
+    ti, tj, tv = oracle.csr_transpose(3, 6, g.indptr, g.indices, g.vals)
+    assert ti.tolist() == [0, 1, 3, 3, 4, 5, 5]
+    assert tj.tolist() == [2, 0, 2, 2, 0]
+    # values: original order after (row, col) sort is (0,1)=1 (0,4)=0 (2,0)=2 (2,1)=3 (2,3)=4
+    assert tv.tolist() == [2.0, 1.0, 3.0, 4.0, 0.0]
+    e = synth.empty_graph(4)
+    ti, tj, tv = oracle.csr_transpose(4, 4, e.indptr, e.indices, e.vals)
+    assert ti.tolist() == [0] * 5 and tj.size == 0
+
+
+def test_adjoint_identity():
+    wl = synth.custom(900, "rmat", 12, [(2, 2)], seed=1)
+    g = wl.graph
+    ti, tj, tv = oracle.csr_transpose(g.n, g.n, g.indptr, g.indices, g.vals)
+    rng = np.random.default_rng(9)
+    X, Y = rng.standard_normal((g.n, 4)), rng.standard_normal((g.n, 4))
+    lhs = np.sum(oracle.aggregate(g.indptr, g.indices, g.vals, X) * Y)
+    rhs = np.sum(X * oracle.aggregate(ti, tj, tv, Y))
+    assert abs(lhs - rhs) <= 1e-12 * (abs(lhs) + 1)
+
+
+# ------------------------------------------------------------------- head ----
+def test_ce_closed_forms():
+    n, f, C = 50, 6, 7
+    rng = np.random.default_rng(0)
+    HL = rng.standard_normal((n, f))
+    lab = rng.integers(0, C, n)
+    loss, dWp, dbp, dHL, _ = oracle.loss_grad("ce", HL, np.zeros((f, C)), np.zeros(C), labels=lab)
+    assert abs(loss - math.log(C)) < 1e-14
+    G = np.full((n, C), 1.0 / C)
+    G[np.arange(n), lab] -= 1.0
+    G /= n
+    assert rel(dbp, G.sum(axis=0)) < 1e-13
+    assert np.all(dHL == 0.0)
+    # a row whose logit for the true class dominates has ~zero loss
+    Wp = np.zeros((f, C))
+    bp = np.zeros(C)
+    bp[3] = 60.0
+    loss2, *_ = oracle.loss_grad("ce", HL, Wp, bp, labels=np.full(n, 3))
+    assert loss2 < 1e-20
+    loss3, *_ = oracle.loss_grad("ce", HL, Wp, bp, labels=np.full(n, 0))
+    assert abs(loss3 - 60.0) < 1e-12
+
+
+def test_ce_gradient_rows_sum_to_zero_and_bce_closed_form():
+    rng = np.random.default_rng(1)
+    HL = rng.standard_normal((30, 5))
+    Wp = rng.standard_normal((5, 4))
+    _, _, dbp, _, X = oracle.loss_grad("ce", HL, Wp, np.zeros(4), labels=rng.integers(0, 4, 30))
+    assert abs(dbp.sum()) < 1e-15
+    t = (rng.random((30, 4)) < 0.3).astype(np.float64)
+    loss, _, dbp, dHL, _ = oracle.loss_grad("bce", HL, np.zeros((5, 4)), np.zeros(4), targets=t)
+    assert abs(loss - math.log(2.0)) < 1e-15
+    assert rel(dbp, (0.5 - t).sum(axis=0) / 120) < 1e-14
+    # large |x| stays finite (the log1p(exp(-|x|)) form)
+    big = np.full((2, 1), 800.0)
+    loss_big, *_ = oracle.loss_grad("bce", big, np.ones((1, 1)), np.zeros(1), targets=np.zeros((2, 1)))
+    assert abs(loss_big - 800.0) < 1e-9
+
+
+# ---------------------------------------------------- finite differences ----
+def _fd_workload(head, seed):
+    """A 2-layer float64 workload whose pre-activations keep away from the ReLU kink."""
+    for s in range(seed, seed + 50):
+        wl = synth.custom(14, "er", 4, [(5, 4), (8, 3)], head=head, classes=4, seed=s)
+        for lay in wl.layers:
+            lay.W_self = lay.W_self.astype(np.float64)
+            lay.W_neigh = lay.W_neigh.astype(np.float64)
+            lay.bias = np.random.default_rng(s).standard_normal(lay.bias.shape) * 0.1
+        wl.H = wl.H.astype(np.float64)
+        if wl.W_pred is not None:
+            wl.W_pred = wl.W_pred.astype(np.float64)
+            wl.b_pred = np.random.default_rng(s + 1).standard_normal(wl.b_pred.shape) * 0.1
+        else:
+            wl.dY = wl.dY.astype(np.float64)
+        H = wl.H
+        ok = True
+        for lay in wl.layers:
+            Y, c = oracle.layer_fwd(wl.graph, H, lay.W_self, lay.W_neigh, lay.bias)
+            ok &= np.abs(c.Z).min() > 1e-3
+            H = Y
+        if ok:
+            return wl
+    raise RuntimeError("no kink-free seed")
+
+
+def _objective(wl):
+    H = wl.H
+    for lay in wl.layers:
+        H, _ = oracle.layer_fwd(wl.graph, H, lay.W_self, lay.W_neigh, lay.bias)
+    if wl.spec.head is None:
+        return float(np.sum(H * wl.dY))
+    loss, *_ = oracle.loss_grad(wl.spec.head, H, wl.W_pred, wl.b_pred, labels=wl.labels,
+                                targets=wl.targets)
+    return loss
+
+
+@pytest.mark.parametrize("head", ["ce", "bce", None])
+def test_finite_difference_gradients(head):
+    wl = _fd_workload(head, 100)
+    r = oracle.step(wl, first_layer_dH=True)
+    eps = 1e-6
+    rng = np.random.default_rng(0)
+    checks = []
+    for li, lay in enumerate(wl.layers):
+        checks += [(lay.W_self, r.dW_self[li]), (lay.W_neigh, r.dW_neigh[li]), (lay.bias, r.db[li])]
+    checks.append((wl.H, r.dH[0]))
+    if head is not None:
+        checks += [(wl.W_pred, r.dW_pred), (wl.b_pred, r.db_pred)]
+    for arr, grad in checks:
+        flat = arr.reshape(-1)
+        gflat = np.asarray(grad).reshape(-1)
+        for idx in rng.choice(flat.size, size=min(8, flat.size), replace=False):
+            old = flat[idx]
+            flat[idx] = old + eps
+            jp = _objective(wl)
+            flat[idx] = old - eps
+            jm = _objective(wl)
+            flat[idx] = old
+            fd = (jp - jm) / (2 * eps)
+            scale = max(np.abs(gflat).max(), 1e-12)
+            assert abs(fd - gflat[idx]) <= 1e-6 * scale + 1e-9, (arr.shape, idx, fd, gflat[idx])
+
+
+def test_relu_derivative_at_zero_is_zero():
+    """An isolated vertex with zero bias has Z == 0 exactly on its neighbour half."""
+    g = synth.csr_from_undirected(3, np.array([0]), np.array([1]))  # vertex 2 isolated
+    H = np.ones((3, 2))
+    Y, cache = oracle.layer_fwd(g, H, np.ones((2, 1)), np.ones((2, 1)), np.zeros(2))
+    assert cache.Z[2, 1] == 0.0
+    gT = type("T", (), {})()
+    gT.indptr, gT.indices, gT.vals = oracle.csr_transpose(3, 3, g.indptr, g.indices, g.vals)
+    _, _, db, _ = oracle.layer_bwd(gT, cache, np.ones((2, 1)), np.ones((2, 1)), np.ones((3, 2)), False)
+    assert db[1] == 2.0  # only the two connected vertices pass gradient
+
+
+# ------------------------------------------------------------------- bf16 ----
+def test_bf16_rounding_against_torch_and_special_values():
+    import torch
+    rng = np.random.default_rng(0)
+    x = np.concatenate([
+        rng.standard_normal(10000).astype(np.float32),
+        np.array([0.0, -0.0, 1.0, np.inf, -np.inf, 3.4e38, 1e-40, -1e-45], np.float32),
+        # exact ties: 1 + 2^-8 (ties down to even), 1 + 3*2^-8 (ties up to even)
+        np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8], np.float32),
+    ])
+    ours = obf16.f32_to_bf16_bits(x)
+    ref = torch.tensor(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, ref)
+    assert obf16.round_bf16(np.float32(1.0 + 2.0 ** -8))[()] == 1.0
+    assert obf16.round_bf16(np.float32(1.0 + 3 * 2.0 ** -8))[()] == np.float32(1.0 + 2 ** -6)
+    nan = obf16.round_bf16(np.array([np.nan], np.float32))
+    assert np.isnan(nan[0])
