@@ -1,0 +1,281 @@
+"""ctypes binding of libgcnlayer (include/gcn_layer.h), same names as the C ABI.
+
+Argument marshalling only: torch tensors provide device memory and the current
+HIP stream; every step of the computation runs in the library's kernels.  The
+library must be built (``paper_1810_11899_amd.build``); without it every call
+raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+from .build import LIB_PATH
+
+GCN_OK, GCN_EINVAL, GCN_ESHAPE, GCN_EWORKSPACE, GCN_EHIP, GCN_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+GCN_F32, GCN_BF16 = 0, 1
+GCN_AGGREGATE_FIRST, GCN_TRANSFORM_FIRST = 0, 1
+GCN_SOFTMAX_CE, GCN_SIGMOID_BCE = 0, 1
+LOSS_KIND = {"ce": GCN_SOFTMAX_CE, "bce": GCN_SIGMOID_BCE}
+PREC = {"f32": GCN_F32, "fp32": GCN_F32, "bf16": GCN_BF16}
+
+
+class GcnError(RuntimeError):
+    def __init__(self, code: int, where: str, msg: str):
+        super().__init__(f"{where} failed with {code}: {msg}")
+        self.code = code
+
+
+class gcn_csr(ctypes.Structure):
+    _fields_ = [("n_rows", ctypes.c_int32), ("n_cols", ctypes.c_int32), ("nnz", ctypes.c_int32),
+                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p), ("vals", ctypes.c_void_p)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+_CSRP = ctypes.POINTER(gcn_csr)
+
+_SIGNATURES = {
+    "gcn_last_error": (ctypes.c_char_p, []),
+    "gcn_version": (ctypes.c_int, []),
+    "gcn_csr_validate_host": (ctypes.c_int, [_I32, _I32, _I32, _P, _P, ctypes.c_int]),
+    "gcn_csr_transpose_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
+    "gcn_csr_transpose": (ctypes.c_int, [_CSRP, _P, _P, _P, _P, _SZ, _P]),
+    "gcn_aggregate_workspace_bytes": (_SZ, [_I32, _I32, _I32, ctypes.c_int]),
+    "gcn_aggregate": (ctypes.c_int, [_CSRP, _P, _I32, _I32, _P, _I32, ctypes.c_int, _P, _SZ, _P]),
+    "gcn_layer_pick_order": (ctypes.c_int, [_I32, _I32, ctypes.c_int]),
+    "gcn_layer_saved_bytes": (_SZ, [_I32, _I32, _I32, ctypes.c_int, ctypes.c_int]),
+    "gcn_layer_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, ctypes.c_int, ctypes.c_int]),
+    "gcn_layer_fwd": (ctypes.c_int, [_CSRP, _P, _I32, _I32, _P, _P, _P, _I32, _P, _I32, _P, _SZ,
+                                     ctypes.c_int, ctypes.c_int, _P, _SZ, _P]),
+    "gcn_layer_bwd": (ctypes.c_int, [_CSRP, _CSRP, _P, _I32, _I32, _P, _P, _I32, _P, _I32, _P, _SZ,
+                                     _P, _I32, _P, _I32, _P, _P, _P, ctypes.c_int, ctypes.c_int, _P, _SZ,
+                                     _P]),
+    "gcn_loss_workspace_bytes": (_SZ, [_I32, _I32, _I32, ctypes.c_int]),
+    "gcn_loss_grad": (ctypes.c_int, [_P, _I32, _I32, _I32, _P, _P, _I32, ctypes.c_int, _P, _P, _P, _P,
+                                     _I32, _P, _P, ctypes.c_int, _P, _SZ, _P]),
+    "gcn_f32_to_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
+    "gcn_profile_enable": (ctypes.c_int, [ctypes.c_int]),
+    "gcn_profile_reset": (ctypes.c_int, []),
+    "gcn_profile_class_count": (ctypes.c_int, []),
+    "gcn_profile_class_name": (ctypes.c_char_p, [ctypes.c_int]),
+    "gcn_profile_read": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_double)]),
+}
+
+
+def lib():
+    """Load libgcnlayer.so; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_1810_11899_amd.build "
+                               f"(__graft_entry__.build()); there is no fallback path")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGNATURES)
+
+
+def _check(rc: int, where: str):
+    if rc != GCN_OK:
+        raise GcnError(rc, where, lib().gcn_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _ld(t: torch.Tensor) -> int:
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError("expected a row-major 2-D tensor with unit column stride")
+    return int(t.stride(0)) if t.shape[0] > 1 else max(int(t.stride(0)), int(t.shape[1]))
+
+
+def _dev_f32(t: torch.Tensor, name: str):
+    if not (t.is_cuda and t.dtype == torch.float32):
+        raise TypeError(f"{name} must be a float32 CUDA/HIP tensor")
+
+
+# --------------------------------------------------------------------------
+class Workspace:
+    """Grow-only device scratch handed to the library."""
+
+    def __init__(self, device="cuda"):
+        self.device = torch.device(device)
+        self.buf = torch.empty(0, dtype=torch.uint8, device=self.device)
+
+    def get(self, nbytes: int) -> torch.Tensor:
+        nbytes = max(int(nbytes), 256)
+        if self.buf.numel() < nbytes:
+            self.buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        return self.buf
+
+    def args(self, nbytes: int):
+        b = self.get(nbytes)
+        return ctypes.c_void_p(b.data_ptr()), ctypes.c_size_t(b.numel())
+
+
+class DeviceCSR:
+    """CSR arrays resident on the device (int32 indptr/indices, float32 vals)."""
+
+    def __init__(self, n_rows, n_cols, indptr, indices, vals):
+        self.n_rows, self.n_cols = int(n_rows), int(n_cols)
+        self.indptr, self.indices, self.vals = indptr, indices, vals
+        self.nnz = int(indices.numel())
+
+    @classmethod
+    def from_host(cls, n_rows, n_cols, indptr, indices, vals, device="cuda"):
+        d = torch.device(device)
+        ip = torch.as_tensor(indptr, dtype=torch.int32).to(d)
+        ix = torch.as_tensor(indices, dtype=torch.int32).to(d)
+        vv = torch.as_tensor(vals, dtype=torch.float32).to(d)
+        return cls(n_rows, n_cols, ip, ix, vv)
+
+    def struct(self) -> gcn_csr:
+        return gcn_csr(self.n_rows, self.n_cols, self.nnz, self.indptr.data_ptr(),
+                       self.indices.data_ptr() if self.nnz else None,
+                       self.vals.data_ptr() if self.nnz else None)
+
+
+# ------------------------------------------------------------------- calls
+def gcn_csr_validate_host(n_rows, n_cols, indptr, indices, require_sorted=True) -> int:
+    import numpy as np
+    ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    ix = np.ascontiguousarray(indices, dtype=np.int32)
+    return lib().gcn_csr_validate_host(n_rows, n_cols, int(ix.size), ip.ctypes.data,
+                                       ix.ctypes.data if ix.size else None, int(require_sorted))
+
+
+def gcn_csr_transpose(A: DeviceCSR, ws: Workspace, stream=None) -> DeviceCSR:
+    d = A.indptr.device
+    t_indptr = torch.empty(A.n_cols + 1, dtype=torch.int32, device=d)
+    t_indices = torch.empty(max(A.nnz, 1), dtype=torch.int32, device=d)[:A.nnz]
+    t_vals = torch.empty(max(A.nnz, 1), dtype=torch.float32, device=d)[:A.nnz]
+    gcn_csr_transpose_into(A, t_indptr, t_indices, t_vals, ws, stream)
+    return DeviceCSR(A.n_cols, A.n_rows, t_indptr, t_indices, t_vals)
+
+
+def gcn_csr_transpose_into(A: DeviceCSR, t_indptr, t_indices, t_vals, ws: Workspace, stream=None):
+    L = lib()
+    need = L.gcn_csr_transpose_workspace_bytes(A.n_rows, A.n_cols, A.nnz)
+    w, wb = ws.args(need)
+    s = A.struct()
+    _check(L.gcn_csr_transpose(ctypes.byref(s), _ptr(t_indptr), _ptr(t_indices), _ptr(t_vals), w, wb,
+                               _stream(stream)), "gcn_csr_transpose")
+
+
+def gcn_aggregate(A: DeviceCSR, X: torch.Tensor, out: torch.Tensor, ws: Workspace, prec=GCN_F32, stream=None):
+    _dev_f32(X, "X")
+    _dev_f32(out, "out")
+    L = lib()
+    k = int(X.shape[1])
+    need = L.gcn_aggregate_workspace_bytes(A.n_rows, A.nnz, k, prec)
+    w, wb = ws.args(need)
+    s = A.struct()
+    _check(L.gcn_aggregate(ctypes.byref(s), _ptr(X), k, _ld(X), _ptr(out), _ld(out), prec, w, wb,
+                           _stream(stream)), "gcn_aggregate")
+    return out
+
+
+def gcn_layer_pick_order(f_in, h, need_dH) -> int:
+    return lib().gcn_layer_pick_order(f_in, h, int(bool(need_dH)))
+
+
+def gcn_layer_saved_bytes(n, f_in, h, order, prec=GCN_F32) -> int:
+    return int(lib().gcn_layer_saved_bytes(n, f_in, h, order, prec))
+
+
+def gcn_layer_workspace_bytes(n, nnz, f_in, h, order, prec=GCN_F32) -> int:
+    return int(lib().gcn_layer_workspace_bytes(n, nnz, f_in, h, order, prec))
+
+
+def gcn_layer_fwd(A: DeviceCSR, H, W_self, W_neigh, bias, Y, saved, order, ws: Workspace, prec=GCN_F32,
+                  stream=None):
+    for t, nm in ((H, "H"), (W_self, "W_self"), (W_neigh, "W_neigh"), (bias, "bias"), (Y, "Y")):
+        _dev_f32(t, nm)
+    L = lib()
+    f_in, h = int(W_self.shape[0]), int(W_self.shape[1])
+    need = L.gcn_layer_workspace_bytes(A.n_rows, A.nnz, f_in, h, order, prec)
+    w, wb = ws.args(need)
+    s = A.struct()
+    sv = saved.numel() * saved.element_size() if saved is not None else 0
+    _check(L.gcn_layer_fwd(ctypes.byref(s), _ptr(H), f_in, _ld(H), _ptr(W_self), _ptr(W_neigh), _ptr(bias), h,
+                           _ptr(Y), _ld(Y), _ptr(saved), sv, order, prec, w, wb, _stream(stream)),
+           "gcn_layer_fwd")
+    return Y
+
+
+def gcn_layer_bwd(A: DeviceCSR, AT: DeviceCSR, H, W_self, W_neigh, Y, saved, dY, dH, dW_self, dW_neigh, dbias,
+                  order, ws: Workspace, prec=GCN_F32, stream=None):
+    L = lib()
+    f_in, h = int(W_self.shape[0]), int(W_self.shape[1])
+    need = L.gcn_layer_workspace_bytes(A.n_rows, A.nnz, f_in, h, order, prec)
+    w, wb = ws.args(need)
+    s, st = A.struct(), AT.struct()
+    sv = saved.numel() * saved.element_size() if saved is not None else 0
+    _check(L.gcn_layer_bwd(ctypes.byref(s), ctypes.byref(st), _ptr(H), f_in, _ld(H), _ptr(W_self),
+                           _ptr(W_neigh), h, _ptr(Y), _ld(Y), _ptr(saved), sv, _ptr(dY), _ld(dY), _ptr(dH),
+                           _ld(dH) if dH is not None else 0, _ptr(dW_self), _ptr(dW_neigh), _ptr(dbias), order,
+                           prec, w, wb, _stream(stream)), "gcn_layer_bwd")
+
+
+def gcn_loss_grad(HL, W_pred, b_pred, kind, labels, targets, loss, dHL, dW_pred, db_pred, ws: Workspace,
+                  prec=GCN_F32, stream=None):
+    L = lib()
+    n, f = int(HL.shape[0]), int(HL.shape[1])
+    C = int(W_pred.shape[1])
+    need = L.gcn_loss_workspace_bytes(n, f, C, prec)
+    w, wb = ws.args(need)
+    _check(L.gcn_loss_grad(_ptr(HL), n, f, _ld(HL), _ptr(W_pred), _ptr(b_pred), C, kind, _ptr(labels),
+                           _ptr(targets), _ptr(loss), _ptr(dHL), _ld(dHL), _ptr(dW_pred), _ptr(db_pred), prec,
+                           w, wb, _stream(stream)), "gcn_loss_grad")
+
+
+def gcn_f32_to_bf16(x: torch.Tensor, stream=None) -> torch.Tensor:
+    _dev_f32(x, "x")
+    x = x.contiguous()
+    y = torch.empty(x.shape, dtype=torch.int16, device=x.device)
+    _check(lib().gcn_f32_to_bf16(_ptr(x), _ptr(y), x.numel(), _stream(stream)), "gcn_f32_to_bf16")
+    return y
+
+
+# ---------------------------------------------------------------- profiling
+def gcn_profile_enable(on: bool):
+    _check(lib().gcn_profile_enable(int(bool(on))), "gcn_profile_enable")
+
+
+def gcn_profile_reset():
+    _check(lib().gcn_profile_reset(), "gcn_profile_reset")
+
+
+def gcn_profile_read_all():
+    """{class name: (ms, launches, flops, bytes)} since the last reset."""
+    L = lib()
+    out = {}
+    for c in range(L.gcn_profile_class_count()):
+        ms, n = ctypes.c_double(), ctypes.c_int64()
+        fl, by = ctypes.c_double(), ctypes.c_double()
+        _check(L.gcn_profile_read(c, ctypes.byref(ms), ctypes.byref(n), ctypes.byref(fl), ctypes.byref(by)),
+               "gcn_profile_read")
+        out[L.gcn_profile_class_name(c).decode()] = (ms.value, n.value, fl.value, by.value)
+    return out

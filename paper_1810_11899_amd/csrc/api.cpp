@@ -1,0 +1,578 @@
+// Host side of libgcnlayer: the C ABI of gcn_layer.h.  Validates arguments,
+// carves the caller's workspace, picks the kernels and enqueues them on the
+// caller's stream.  No device memory is allocated here.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace gcn {
+
+// ------------------------------------------------------------------ errors
+static thread_local std::string g_last_error;
+
+void set_error(const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    set_error("HIP error in %s: %s", what, hipGetErrorString(e));
+    return GCN_EHIP;
+}
+
+// --------------------------------------------------------------- profiling
+static const char *kClassNames[K_CLASS_COUNT] = {
+    "spmm", "spmm_fixup", "gemm_nn", "gemm_tn", "gemm_nt", "splitk_reduce", "relu_bwd",
+    "colsum", "loss_rows", "loss_reduce", "transpose_count", "transpose_scan", "transpose_scatter",
+    "transpose_sort", "transpose_final", "cvt_bf16"};
+
+const char *class_name(int cls) {
+    return (cls >= 0 && cls < K_CLASS_COUNT) ? kClassNames[cls] : "";
+}
+
+namespace {
+struct Record {
+    int cls;
+    hipEvent_t a, b;
+    double flops, bytes;
+};
+struct Totals {
+    double ms = 0.0, flops = 0.0, bytes = 0.0;
+    int64_t launches = 0;
+};
+struct Profiler {
+    std::mutex mu;
+    bool on = false;
+    std::vector<hipEvent_t> pool;
+    std::vector<Record> pending;
+    Totals tot[K_CLASS_COUNT];
+
+    hipEvent_t get() {
+        if (!pool.empty()) {
+            hipEvent_t e = pool.back();
+            pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+    int drain() {
+        int rc = GCN_OK;
+        for (Record &r : pending) {
+            float ms = 0.0f;
+            hipError_t e = hipEventSynchronize(r.b);
+            if (e == hipSuccess) e = hipEventElapsedTime(&ms, r.a, r.b);
+            if (e != hipSuccess) rc = hip_fail(e, "profiler event");
+            Totals &t = tot[r.cls];
+            t.ms += ms;
+            t.flops += r.flops;
+            t.bytes += r.bytes;
+            t.launches += 1;
+            pool.push_back(r.a);
+            pool.push_back(r.b);
+        }
+        pending.clear();
+        return rc;
+    }
+};
+Profiler &prof() {
+    static Profiler *p = new Profiler();  // never destroyed: events may outlive static teardown
+    return *p;
+}
+}  // namespace
+
+ProfScope::ProfScope(int cls, hipStream_t s, double flops, double bytes) : cls_(cls), s_(s), slot_(-1) {
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    if (!p.on) return;
+    Record r{cls, p.get(), p.get(), flops, bytes};
+    if (!r.a || !r.b) return;
+    if (hipEventRecord(r.a, s) != hipSuccess) return;
+    p.pending.push_back(r);
+    slot_ = (int)p.pending.size() - 1;
+}
+
+ProfScope::~ProfScope() {
+    if (slot_ < 0) return;
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    if (slot_ < (int)p.pending.size()) hipEventRecord(p.pending[slot_].b, s_);
+}
+
+}  // namespace gcn
+
+using namespace gcn;
+
+// =================================================================== helpers
+namespace {
+
+hipStream_t as_stream(void *s) { return (hipStream_t)s; }
+
+#define REQUIRE(cond, code, ...)       \
+    do {                               \
+        if (!(cond)) {                 \
+            set_error(__VA_ARGS__);    \
+            return (code);             \
+        }                              \
+    } while (0)
+
+int check_csr(const gcn_csr *A, const char *name) {
+    REQUIRE(A, GCN_EINVAL, "%s: null CSR", name);
+    REQUIRE(A->n_rows >= 0 && A->n_cols >= 0 && A->nnz >= 0, GCN_ESHAPE, "%s: negative size", name);
+    REQUIRE(A->n_rows == 0 || A->indptr, GCN_EINVAL, "%s: null indptr", name);
+    REQUIRE(A->nnz == 0 || (A->indices && A->vals), GCN_EINVAL, "%s: null indices/vals", name);
+    return GCN_OK;
+}
+
+// ----------------------------------------------------------- layer planning
+struct LayerPlan {
+    bool need_G;        // backward forms G = A^T dZ_n
+    size_t fwd_T;       // TRANSFORM_FIRST: n x h
+    size_t fwd_spmm;
+    size_t bwd_P, bwd_D, bwd_T2, bwd_relu, bwd_spmm, bwd_gemm;
+    size_t fwd_total, bwd_total, total;
+};
+
+bool bwd_uses_G(int order, bool dH, int32_t f_in, int32_t h) {
+    return order == GCN_TRANSFORM_FIRST || (dH && h <= f_in);
+}
+
+GemmProblem dw_problem(int32_t f_in, int32_t h, int32_t n) {
+    GemmProblem g{};
+    g.M = f_in;
+    g.N = h;
+    g.seg[0].K = n;
+    g.seg[0].lda = f_in;
+    g.seg[0].ldb = h;
+    return g;
+}
+
+LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order, bool dH) {
+    LayerPlan p{};
+    p.need_G = bwd_uses_G(order, dH, f_in, h);
+    const size_t F = sizeof(float);
+    if (order == GCN_TRANSFORM_FIRST) {
+        p.fwd_T = align256((size_t)n * h * F);
+        p.fwd_spmm = spmm_workspace_bytes(n, nnz, h);
+    } else {
+        p.fwd_spmm = spmm_workspace_bytes(n, nnz, f_in);
+    }
+    p.fwd_total = p.fwd_T + p.fwd_spmm + 512;
+
+    p.bwd_P = align256((size_t)n * 2 * h * F);
+    if (p.need_G) {
+        p.bwd_D = align256((size_t)n * h * F);
+        p.bwd_spmm = spmm_workspace_bytes(n, nnz, h);
+    }
+    if (dH && !p.need_G) {
+        p.bwd_T2 = align256((size_t)n * f_in * F);
+        p.bwd_spmm = std::max(p.bwd_spmm, spmm_workspace_bytes(n, nnz, f_in));
+    }
+    p.bwd_relu = relu_bwd_workspace_bytes(n, h);
+    GemmProblem pr[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
+    p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr));
+    p.bwd_total = p.bwd_P + p.bwd_D + p.bwd_T2 + p.bwd_relu + p.bwd_spmm + p.bwd_gemm + 2048;
+    p.total = std::max(p.fwd_total, p.bwd_total);
+    return p;
+}
+
+size_t saved_bytes(int32_t n, int32_t f_in, int32_t h, int order, int prec) {
+    (void)h;
+    (void)prec;
+    if (order == GCN_AGGREGATE_FIRST) return align256((size_t)n * f_in * sizeof(float));
+    return 0;
+}
+
+int check_layer_common(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, const float *W_self,
+                       const float *W_neigh, int32_t h, int order, int prec, const char *who) {
+    int rc = check_csr(A, who);
+    if (rc) return rc;
+    REQUIRE(A->n_rows == A->n_cols, GCN_ESHAPE, "%s: aggregation matrix must be square (%d x %d)", who,
+            A->n_rows, A->n_cols);
+    REQUIRE(f_in > 0 && h > 0, GCN_ESHAPE, "%s: f_in=%d h=%d must be positive", who, f_in, h);
+    REQUIRE(ldh >= f_in, GCN_ESHAPE, "%s: ldh=%d < f_in=%d", who, ldh, f_in);
+    REQUIRE(order == GCN_AGGREGATE_FIRST || order == GCN_TRANSFORM_FIRST, GCN_EINVAL, "%s: bad order %d",
+            who, order);
+    REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "%s: bad precision %d", who, prec);
+    REQUIRE(prec == GCN_F32, GCN_EUNSUPPORTED, "%s: the bfloat16 path is not built yet", who);
+    REQUIRE(A->n_rows == 0 || (H && W_self && W_neigh), GCN_EINVAL, "%s: null H or weights", who);
+    return GCN_OK;
+}
+
+}  // namespace
+
+// ==================================================================== ABI
+extern "C" {
+
+const char *gcn_last_error(void) { return g_last_error.c_str(); }
+
+int gcn_version(void) { return 100; }
+
+int gcn_csr_validate_host(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
+                          const int32_t *indices, int require_sorted) {
+    REQUIRE(n_rows >= 0 && n_cols >= 0 && nnz >= 0, GCN_EINVAL, "csr: negative size");
+    REQUIRE(indptr, GCN_EINVAL, "csr: null indptr");
+    REQUIRE(nnz == 0 || indices, GCN_EINVAL, "csr: null indices");
+    REQUIRE(indptr[0] == 0, GCN_EINVAL, "csr: indptr[0] = %d, expected 0", indptr[0]);
+    REQUIRE(indptr[n_rows] == nnz, GCN_EINVAL, "csr: indptr[n_rows] = %d, expected nnz = %d",
+            indptr[n_rows], nnz);
+    for (int32_t i = 0; i < n_rows; ++i) {
+        const int32_t b = indptr[i], e = indptr[i + 1];
+        REQUIRE(b <= e, GCN_EINVAL, "csr: indptr decreases at row %d", i);
+        for (int32_t p = b; p < e; ++p) {
+            REQUIRE(indices[p] >= 0 && indices[p] < n_cols, GCN_EINVAL,
+                    "csr: row %d holds column %d outside [0, %d)", i, indices[p], n_cols);
+            if (require_sorted && p > b)
+                REQUIRE(indices[p] > indices[p - 1], GCN_EINVAL,
+                        "csr: row %d is not strictly ascending at entry %d", i, p);
+        }
+    }
+    return GCN_OK;
+}
+
+// -------------------------------------------------------------- transpose
+size_t gcn_csr_transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz) {
+    return transpose_workspace_bytes(n_rows, n_cols, nnz);
+}
+
+int gcn_csr_transpose(const gcn_csr *A, int32_t *t_indptr, int32_t *t_indices, float *t_vals, void *ws,
+                      size_t ws_bytes, void *stream) {
+    int rc = check_csr(A, "gcn_csr_transpose");
+    if (rc) return rc;
+    REQUIRE(t_indptr, GCN_EINVAL, "gcn_csr_transpose: null t_indptr");
+    REQUIRE(A->nnz == 0 || (t_indices && t_vals), GCN_EINVAL, "gcn_csr_transpose: null outputs");
+    const size_t need = transpose_workspace_bytes(A->n_rows, A->n_cols, A->nnz);
+    REQUIRE(A->nnz == 0 || (ws && ws_bytes >= need), GCN_EWORKSPACE,
+            "gcn_csr_transpose: workspace %zu < %zu bytes", ws_bytes, need);
+    return csr_transpose(A->n_rows, A->n_cols, A->nnz, A->indptr, A->indices, A->vals, t_indptr, t_indices,
+                         t_vals, ws, ws_bytes, as_stream(stream));
+}
+
+// ------------------------------------------------------------- aggregate
+size_t gcn_aggregate_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k, gcn_prec prec) {
+    (void)prec;
+    return spmm_workspace_bytes(n_rows, nnz, k);
+}
+
+int gcn_aggregate(const gcn_csr *A, const float *X, int32_t k, int32_t ldx, float *out, int32_t ldo,
+                  gcn_prec prec, void *ws, size_t ws_bytes, void *stream) {
+    int rc = check_csr(A, "gcn_aggregate");
+    if (rc) return rc;
+    REQUIRE(k >= 0 && ldx >= k && ldo >= k, GCN_ESHAPE, "gcn_aggregate: k=%d ldx=%d ldo=%d", k, ldx, ldo);
+    REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "gcn_aggregate: bad precision");
+    REQUIRE(prec == GCN_F32, GCN_EUNSUPPORTED, "gcn_aggregate: the bfloat16 path is not built yet");
+    if (A->n_rows == 0 || k == 0) return GCN_OK;
+    REQUIRE(out && (A->nnz == 0 || X), GCN_EINVAL, "gcn_aggregate: null X or out");
+    const size_t need = spmm_workspace_bytes(A->n_rows, A->nnz, k);
+    REQUIRE(ws && ws_bytes >= need, GCN_EWORKSPACE, "gcn_aggregate: workspace %zu < %zu bytes", ws_bytes,
+            need);
+    return spmm_f32(A->n_rows, A->nnz, A->indptr, A->indices, A->vals, X, k, ldx, out, ldo, EPI_STORE,
+                    nullptr, ws, ws_bytes, as_stream(stream));
+}
+
+// ----------------------------------------------------------------- layer
+int gcn_layer_pick_order(int32_t f_in, int32_t h, int need_dH) {
+    // cheaper total aggregation width: forward at f_in (aggregate-first) or h
+    // (transform-first); the backward pass adds min(f_in, h) for the input
+    // gradient under aggregate-first, h under transform-first
+    if (need_dH) return f_in < h ? GCN_AGGREGATE_FIRST : GCN_TRANSFORM_FIRST;
+    return f_in <= 2 * h ? GCN_AGGREGATE_FIRST : GCN_TRANSFORM_FIRST;
+}
+
+size_t gcn_layer_saved_bytes(int32_t n, int32_t f_in, int32_t h, gcn_order order, gcn_prec prec) {
+    return saved_bytes(n, f_in, h, order, prec);
+}
+
+size_t gcn_layer_workspace_bytes(int32_t n, int32_t nnz, int32_t f_in, int32_t h, gcn_order order,
+                                 gcn_prec prec) {
+    (void)prec;
+    return plan_layer(n, nnz, f_in, h, order, true).total;
+}
+
+int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, const float *W_self,
+                  const float *W_neigh, const float *bias, int32_t h, float *Y, int32_t ldy, void *saved,
+                  size_t saved_bytes_, gcn_order order, gcn_prec prec, void *ws, size_t ws_bytes,
+                  void *stream) {
+    int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_fwd");
+    if (rc) return rc;
+    const int32_t n = A->n_rows;
+    REQUIRE(ldy >= 2 * h, GCN_ESHAPE, "gcn_layer_fwd: ldy=%d < 2h=%d", ldy, 2 * h);
+    if (n == 0) return GCN_OK;
+    REQUIRE(Y && bias, GCN_EINVAL, "gcn_layer_fwd: null Y or bias");
+    const size_t sneed = saved_bytes(n, f_in, h, order, prec);
+    REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
+            "gcn_layer_fwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
+    const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, true);
+    REQUIRE(ws && ws_bytes >= pl.fwd_total, GCN_EWORKSPACE, "gcn_layer_fwd: workspace %zu < %zu bytes",
+            ws_bytes, pl.fwd_total);
+    hipStream_t s = as_stream(stream);
+    Arena ar(ws, ws_bytes);
+
+    GemmProblem g[2] = {};
+    g[0].M = g[1].M = n;
+    g[0].N = g[1].N = h;
+    g[0].seg[0] = GemmSeg{H, ldh, W_self, h, f_in};
+    g[0].C = Y;
+    g[0].ldc = ldy;
+    g[0].bias = bias;
+    g[0].relu = 1;
+    if (order == GCN_AGGREGATE_FIRST) {
+        float *AGG = (float *)saved;
+        void *sw = ar.take<char>(pl.fwd_spmm);
+        rc = spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE, nullptr,
+                      sw, pl.fwd_spmm, s);
+        if (rc) return rc;
+        g[1].seg[0] = GemmSeg{AGG, f_in, W_neigh, h, f_in};
+        g[1].C = Y + h;
+        g[1].ldc = ldy;
+        g[1].bias = bias + h;
+        g[1].relu = 1;
+        return gemm(L_NN, 2, g, 0, 1, nullptr, 0, s);
+    }
+    float *T = ar.take<float>((size_t)n * h);
+    void *sw = ar.take<char>(pl.fwd_spmm);
+    g[1].seg[0] = GemmSeg{H, ldh, W_neigh, h, f_in};
+    g[1].C = T;
+    g[1].ldc = h;
+    rc = gemm(L_NN, 2, g, 0, 1, nullptr, 0, s);
+    if (rc) return rc;
+    return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, T, h, h, Y + h, ldy, EPI_BIAS_RELU, bias + h, sw,
+                    pl.fwd_spmm, s);
+}
+
+int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f_in, int32_t ldh,
+                  const float *W_self, const float *W_neigh, int32_t h, const float *Y, int32_t ldy,
+                  const void *saved, size_t saved_bytes_, const float *dY, int32_t lddy, float *dH, int32_t lddh,
+                  float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec, void *ws,
+                  size_t ws_bytes, void *stream) {
+    int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_bwd");
+    if (rc) return rc;
+    rc = check_csr(AT, "gcn_layer_bwd (transpose)");
+    if (rc) return rc;
+    const int32_t n = A->n_rows;
+    REQUIRE(AT->n_rows == n && AT->n_cols == n && AT->nnz == A->nnz, GCN_ESHAPE,
+            "gcn_layer_bwd: transpose is %d x %d with %d entries, expected %d x %d with %d", AT->n_rows,
+            AT->n_cols, AT->nnz, n, n, A->nnz);
+    REQUIRE(ldy >= 2 * h && lddy >= 2 * h, GCN_ESHAPE, "gcn_layer_bwd: ldy=%d lddy=%d < 2h=%d", ldy, lddy,
+            2 * h);
+    REQUIRE(!dH || lddh >= f_in, GCN_ESHAPE, "gcn_layer_bwd: lddh=%d < f_in=%d", lddh, f_in);
+    REQUIRE(dW_self && dW_neigh && dbias, GCN_EINVAL, "gcn_layer_bwd: null weight/bias gradient");
+    REQUIRE(n == 0 || (Y && dY), GCN_EINVAL, "gcn_layer_bwd: null Y or dY");
+    const size_t sneed = saved_bytes(n, f_in, h, order, prec);
+    REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
+            "gcn_layer_bwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
+    const bool want_dH = dH != nullptr;
+    const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, want_dH);
+    REQUIRE(ws && ws_bytes >= pl.bwd_total, GCN_EWORKSPACE, "gcn_layer_bwd: workspace %zu < %zu bytes",
+            ws_bytes, pl.bwd_total);
+    hipStream_t s = as_stream(stream);
+    Arena ar(ws, ws_bytes);
+    float *P = ar.take<float>((size_t)n * 2 * h);
+    float *D = pl.need_G ? ar.take<float>((size_t)n * h) : nullptr;
+    float *T2 = (want_dH && !pl.need_G) ? ar.take<float>((size_t)n * f_in) : nullptr;
+    void *rw = ar.take<char>(pl.bwd_relu);
+    void *sw = pl.bwd_spmm ? ar.take<char>(pl.bwd_spmm) : nullptr;
+    void *gw = pl.bwd_gemm ? ar.take<char>(pl.bwd_gemm) : nullptr;
+    const int64_t ldP = 2 * (int64_t)h;
+
+    // a6: dZ = dY * [Y > 0], dbias
+    float *dZn = pl.need_G ? D : P + h;
+    const int64_t ldZn = pl.need_G ? h : ldP;
+    rc = relu_bwd(n, h, dY, lddy, Y, ldy, P, ldP, dZn, ldZn, nullptr, nullptr, dbias, rw, pl.bwd_relu, s);
+    if (rc) return rc;
+    // G = A^T dZ_n into the second half of P
+    if (pl.need_G) {
+        rc = spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, D, h, h, P + h, ldP, EPI_STORE,
+                      nullptr, sw, pl.bwd_spmm, s);
+        if (rc) return rc;
+    }
+    // a7: weight gradients, K = n, split-K
+    GemmProblem g[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
+    g[0].seg[0] = GemmSeg{H, ldh, P, ldP, n};
+    g[0].C = dW_self;
+    g[0].ldc = h;
+    if (order == GCN_TRANSFORM_FIRST) {
+        g[1].seg[0] = GemmSeg{H, ldh, P + h, ldP, n};                       // H^T (A^T dZ_n)
+    } else {
+        const float *AGG = (const float *)saved;
+        g[1].seg[0] = pl.need_G ? GemmSeg{AGG, f_in, D, h, n} : GemmSeg{AGG, f_in, P + h, ldP, n};
+    }
+    g[1].C = dW_neigh;
+    g[1].ldc = h;
+    if (n == 0) {
+        // empty subgraph: zero gradients
+        rc = fill_zero(dW_self, (int64_t)f_in * h, s);
+        return rc ? rc : fill_zero(dW_neigh, (int64_t)f_in * h, s);
+    }
+    const int split = gemm_pick_split(2, g);
+    rc = gemm(L_TN, 2, g, 0, split, gw, pl.bwd_gemm, s);
+    if (rc) return rc;
+    if (!want_dH) return GCN_OK;
+    // a8: input gradient
+    if (pl.need_G) {
+        GemmProblem d{};
+        d.M = n;
+        d.N = f_in;
+        d.seg[0] = GemmSeg{P, ldP, W_self, h, h};
+        d.seg[1] = GemmSeg{P + h, ldP, W_neigh, h, h};
+        d.C = dH;
+        d.ldc = lddh;
+        return gemm(L_NT, 1, &d, 0, 1, nullptr, 0, s);
+    }
+    GemmProblem d[2] = {};
+    d[0].M = d[1].M = n;
+    d[0].N = d[1].N = f_in;
+    d[0].seg[0] = GemmSeg{P, ldP, W_self, h, h};
+    d[0].C = dH;
+    d[0].ldc = lddh;
+    d[1].seg[0] = GemmSeg{P + h, ldP, W_neigh, h, h};
+    d[1].C = T2;
+    d[1].ldc = f_in;
+    rc = gemm(L_NT, 2, d, 0, 1, nullptr, 0, s);
+    if (rc) return rc;
+    return spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, T2, f_in, f_in, dH, lddh,
+                    EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s);
+}
+
+// ------------------------------------------------------------------ loss
+namespace {
+struct LossPlan {
+    size_t X, rows, gemm, colsum, total;
+    int split;
+};
+LossPlan plan_loss(int32_t n, int32_t f, int32_t C) {
+    LossPlan p{};
+    p.X = align256((size_t)n * C * sizeof(float));
+    p.rows = align256((size_t)n * sizeof(float) + 4);
+    GemmProblem g = dw_problem(f, C, n);
+    p.split = gemm_pick_split(1, &g);
+    p.gemm = gemm_workspace_bytes(1, &g, p.split);
+    p.colsum = colsum_workspace_bytes(n, C);
+    p.total = p.X + p.rows + p.gemm + p.colsum + 1024;
+    return p;
+}
+}  // namespace
+
+size_t gcn_loss_workspace_bytes(int32_t n, int32_t f, int32_t C, gcn_prec prec) {
+    (void)prec;
+    return plan_loss(n, f, C).total;
+}
+
+int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const float *W_pred, const float *b_pred,
+                  int32_t C, gcn_loss_kind kind, const int32_t *labels, const float *targets, float *loss,
+                  float *dHL, int32_t lddhl, float *dW_pred, float *db_pred, gcn_prec prec, void *ws,
+                  size_t ws_bytes, void *stream) {
+    REQUIRE(n >= 0 && f > 0 && C > 0, GCN_ESHAPE, "gcn_loss_grad: n=%d f=%d C=%d", n, f, C);
+    REQUIRE(ldhl >= f && lddhl >= f, GCN_ESHAPE, "gcn_loss_grad: ldhl=%d lddhl=%d < f=%d", ldhl, lddhl, f);
+    REQUIRE(kind == GCN_SOFTMAX_CE || kind == GCN_SIGMOID_BCE, GCN_EINVAL, "gcn_loss_grad: bad kind %d",
+            kind);
+    REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "gcn_loss_grad: bad precision");
+    REQUIRE(prec == GCN_F32, GCN_EUNSUPPORTED, "gcn_loss_grad: the bfloat16 path is not built yet");
+    REQUIRE(W_pred && b_pred && loss && dHL && dW_pred && db_pred, GCN_EINVAL, "gcn_loss_grad: null pointer");
+    REQUIRE(n == 0 || HL, GCN_EINVAL, "gcn_loss_grad: null HL");
+    REQUIRE(n == 0 || (kind == GCN_SOFTMAX_CE ? labels != nullptr : targets != nullptr), GCN_EINVAL,
+            "gcn_loss_grad: null labels/targets");
+    const LossPlan pl = plan_loss(n, f, C);
+    REQUIRE(ws && ws_bytes >= pl.total, GCN_EWORKSPACE, "gcn_loss_grad: workspace %zu < %zu bytes", ws_bytes,
+            pl.total);
+    hipStream_t s = as_stream(stream);
+    Arena ar(ws, ws_bytes);
+    float *X = ar.take<float>((size_t)n * C);
+    float *rows = ar.take<float>((size_t)n + 1);
+    void *gw = pl.gemm ? ar.take<char>(pl.gemm) : nullptr;
+    void *cw = ar.take<char>(pl.colsum);
+    int rc;
+    if (n == 0) {
+        rc = fill_zero(dW_pred, (int64_t)f * C, s);
+        if (!rc) rc = fill_zero(db_pred, C, s);
+        return rc ? rc : fill_zero(loss, 1, s);
+    }
+    // a4: logits X = HL W_pred + b_pred
+    GemmProblem g{};
+    g.M = n;
+    g.N = C;
+    g.seg[0] = GemmSeg{HL, ldhl, W_pred, C, f};
+    g.C = X;
+    g.ldc = C;
+    g.bias = b_pred;
+    rc = gemm(L_NN, 1, &g, 0, 1, nullptr, 0, s);
+    if (rc) return rc;
+    // row losses; X <- G in place
+    rc = loss_rows(kind, n, C, X, labels, targets, rows, s);
+    if (rc) return rc;
+    const double scale = kind == GCN_SOFTMAX_CE ? 1.0 / (double)n : 1.0 / ((double)n * (double)C);
+    rc = loss_reduce(n, rows, scale, loss, s);
+    if (rc) return rc;
+    // a5: dW_pred = HL^T G, db_pred = sum_i G, dHL = G W_pred^T
+    GemmProblem w = dw_problem(f, C, n);
+    w.seg[0] = GemmSeg{HL, ldhl, X, C, n};
+    w.C = dW_pred;
+    w.ldc = C;
+    rc = gemm(L_TN, 1, &w, 0, pl.split, gw, pl.gemm, s);
+    if (rc) return rc;
+    rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s);
+    if (rc) return rc;
+    GemmProblem d{};
+    d.M = n;
+    d.N = f;
+    d.seg[0] = GemmSeg{X, C, W_pred, C, C};
+    d.C = dHL;
+    d.ldc = lddhl;
+    return gemm(L_NT, 1, &d, 0, 1, nullptr, 0, s);
+}
+
+// ------------------------------------------------------------------ bf16
+int gcn_f32_to_bf16(const float *x, uint16_t *y, int64_t count, void *stream) {
+    REQUIRE(count >= 0, GCN_ESHAPE, "gcn_f32_to_bf16: negative count");
+    if (count == 0) return GCN_OK;
+    REQUIRE(x && y, GCN_EINVAL, "gcn_f32_to_bf16: null pointer");
+    return cvt_bf16(1, count, x, count, y, count, as_stream(stream));
+}
+
+// ------------------------------------------------------------- profiling
+int gcn_profile_enable(int on) {
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    p.on = on != 0;
+    return GCN_OK;
+}
+
+int gcn_profile_reset(void) {
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    int rc = p.drain();
+    for (auto &t : p.tot) t = Totals{};
+    return rc;
+}
+
+int gcn_profile_class_count(void) { return K_CLASS_COUNT; }
+
+const char *gcn_profile_class_name(int cls) { return class_name(cls); }
+
+int gcn_profile_read(int cls, double *ms, int64_t *launches, double *flops, double *bytes) {
+    REQUIRE(cls >= 0 && cls < K_CLASS_COUNT, GCN_EINVAL, "gcn_profile_read: class %d", cls);
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lk(p.mu);
+    int rc = p.drain();
+    const Totals &t = p.tot[cls];
+    if (ms) *ms = t.ms;
+    if (launches) *launches = t.launches;
+    if (flops) *flops = t.flops;
+    if (bytes) *bytes = t.bytes;
+    return rc;
+}
+
+}  // extern "C"

@@ -1,0 +1,150 @@
+// Internal declarations shared by the HIP sources of libgcnlayer (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "gcn_layer.h"
+
+namespace gcn {
+
+constexpr int kWave = 64;  // CDNA wavefront width
+
+// ------------------------------------------------------------------ errors
+void set_error(const char *fmt, ...);
+int hip_fail(hipError_t e, const char *what);
+#define GCN_HIP_CHECK(expr)                                   \
+    do {                                                      \
+        hipError_t e_ = (expr);                               \
+        if (e_ != hipSuccess) return ::gcn::hip_fail(e_, #expr); \
+    } while (0)
+#define GCN_LAUNCH_CHECK(what)                                \
+    do {                                                      \
+        hipError_t e_ = hipGetLastError();                    \
+        if (e_ != hipSuccess) return ::gcn::hip_fail(e_, what); \
+    } while (0)
+
+// ---------------------------------------------------------------- profiling
+enum KernelClass {
+    K_SPMM = 0,
+    K_SPMM_FIXUP,
+    K_GEMM_NN,
+    K_GEMM_TN,
+    K_GEMM_NT,
+    K_SPLITK_REDUCE,
+    K_RELU_MASK,
+    K_COLSUM_REDUCE,
+    K_LOSS_ROWS,
+    K_LOSS_REDUCE,
+    K_T_COUNT,
+    K_T_SCAN,
+    K_T_FILL,
+    K_T_SORT,
+    K_T_FINAL,
+    K_CVT_BF16,
+    K_CLASS_COUNT
+};
+const char *class_name(int cls);
+// Recorded around one launch when profiling is on; no-ops otherwise.
+struct ProfScope {
+    ProfScope(int cls, hipStream_t s, double flops, double bytes);
+    ~ProfScope();
+    int cls_;
+    hipStream_t s_;
+    int slot_;
+};
+
+// --------------------------------------------------------------- workspace
+// Bump allocator over the caller's workspace; every carve is 256-byte aligned.
+struct Arena {
+    char *base;
+    size_t cap;
+    size_t used;
+    Arena(void *b, size_t c) : base((char *)b), cap(c), used(0) {}
+    template <class T> T *take(size_t count) {
+        size_t off = (used + 255) & ~(size_t)255;
+        used = off + ((count * sizeof(T) + 255) & ~(size_t)255);
+        return (base && used <= cap) ? (T *)(base + off) : nullptr;
+    }
+};
+inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// --------------------------------------------------------------- launchers
+// SpMM (feature propagation) -------------------------------------------------
+enum SpmmEpilogue { EPI_STORE = 0, EPI_BIAS_RELU = 1, EPI_ACCUMULATE = 2 };
+struct SpmmPlan {
+    int64_t items;      // n_rows + nnz (merge-path length)
+    int ipw;            // merge items per wavefront
+    int64_t waves;      // wavefronts in the main kernel
+};
+SpmmPlan spmm_plan(int32_t n_rows, int32_t nnz);
+size_t spmm_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k);
+// out[i, c] (epilogue) sum_p vals[p] * X[indices[p], c]
+int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+             const float *vals, const float *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s);
+// same with bfloat16 rows of X (uint16 bits), float32 accumulation
+int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+              const float *vals, const uint16_t *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s);
+
+// GEMM on the matrix cores -----------------------------------------------------
+// C[M x N] = sum over up to two K-segments of op(A_s) op(B_s), then epilogue.
+//   layout NN: A_s is M x K_s (lda), B_s is K_s x N (ldb)
+//   layout TN: A_s is stored K_s x M (A^T is used), B_s is K_s x N
+//   layout NT: A_s is M x K_s, B_s is stored N x K_s (B^T is used)
+enum GemmLayout { L_NN = 0, L_TN = 1, L_NT = 2 };
+struct GemmSeg {
+    const void *A;
+    int64_t lda;
+    const void *B;
+    int64_t ldb;
+    int32_t K;
+};
+struct GemmProblem {
+    int32_t M, N;
+    GemmSeg seg[2];   // seg[1].K == 0 when unused
+    float *C;
+    int64_t ldc;
+    const float *bias;  // [N] or null
+    int relu;
+};
+// Up to two problems of equal layout in one launch (grouped).  `bf16` selects
+// bfloat16 operands (uint16 bits) instead of float32.  split_k > 1 is only
+// supported for layout TN and needs workspace (gemm_workspace_bytes).
+int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
+         void *ws, size_t ws_bytes, hipStream_t s);
+size_t gemm_workspace_bytes(int nprob, const GemmProblem *probs, int split_k);
+int gemm_pick_split(int nprob, const GemmProblem *probs);
+
+// elementwise / reductions ----------------------------------------------------
+// dZ = dY * [Y > 0]; columns [0,h) -> outS (ldS), [h,2h) -> outN (ldN);
+// optional bf16 copies of the same values (outS16/outN16, same leading dims).
+// dbias[c] = sum_i dZ[i, c] in a fixed order.
+size_t relu_bwd_workspace_bytes(int32_t n, int32_t h);
+int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y, int64_t ldy,
+             float *outS, int64_t ldS, float *outN, int64_t ldN,
+             uint16_t *outS16, uint16_t *outN16, float *dbias,
+             void *ws, size_t ws_bytes, hipStream_t s);
+// column sums of an n x C matrix, fixed order
+size_t colsum_workspace_bytes(int32_t n, int32_t C);
+int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *ws, size_t ws_bytes,
+           hipStream_t s);
+// Row-wise loss on logits X (n x C, ldx == C), in place: X <- G.  rowloss[n].
+int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
+              float *rowloss, hipStream_t s);
+int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, hipStream_t s);
+// x[0..count) = 0 with a kernel (no memset nodes, so callers may capture it)
+int fill_zero(float *x, int64_t count, hipStream_t s);
+// float32 -> bfloat16 bits (RNE), 2-D with leading dimensions
+int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
+             hipStream_t s);
+
+// CSR transpose --------------------------------------------------------------
+size_t transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz);
+int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
+                  const int32_t *indices, const float *vals, int32_t *t_indptr, int32_t *t_indices,
+                  float *t_vals, void *ws, size_t ws_bytes, hipStream_t s);
+
+}  // namespace gcn

@@ -1,0 +1,301 @@
+// Streaming kernels around the two training kernels: the ReLU derivative with
+// the bias gradient, column sums, the PREDICT/LOSS rows of Alg. 1, and the
+// float32 -> bfloat16 rounding.  All are HBM-bound; reductions run in a fixed
+// order (per-chunk partial sums, then one pass over the chunks), so results
+// are bitwise reproducible.
+#include "common.h"
+
+namespace gcn {
+namespace {
+
+constexpr int kRowsPerChunk = 64;
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x0040u);  // NaN stays NaN
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// dZ = dY * [Y > 0] for a chunk of rows; one thread per VEC columns.
+// Writes the two halves to their destinations and the chunk's column sums.
+template <int VEC>
+__global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, const float *__restrict__ dY,
+                                                       int64_t lddy, const float *__restrict__ Y, int64_t ldy,
+                                                       float *__restrict__ outS, int64_t ldS,
+                                                       float *__restrict__ outN, int64_t ldN,
+                                                       uint16_t *__restrict__ outS16,
+                                                       uint16_t *__restrict__ outN16,
+                                                       float *__restrict__ part) {
+    const int c = (blockIdx.x * 256 + threadIdx.x) * VEC;
+    const int w = 2 * h;
+    if (c >= w) return;
+    const int chunk = blockIdx.y;
+    const int r0 = chunk * kRowsPerChunk;
+    const int r1 = min(r0 + kRowsPerChunk, n);
+    const bool self = c < h;  // VEC divides h, so a vector never straddles
+    float *dst = self ? outS : outN;
+    uint16_t *dst16 = self ? outS16 : outN16;
+    const int64_t ldd = self ? ldS : ldN;
+    const int cc = self ? c : c - h;
+    float sum[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) sum[v] = 0.0f;
+    for (int r = r0; r < r1; ++r) {
+        float g[VEC], y[VEC];
+        if (VEC == 4) {
+            const float4 a = *(const float4 *)(dY + (int64_t)r * lddy + c);
+            const float4 b = *(const float4 *)(Y + (int64_t)r * ldy + c);
+            g[0] = a.x; g[1] = a.y; g[2] = a.z; g[3] = a.w;
+            y[0] = b.x; y[1] = b.y; y[2] = b.z; y[3] = b.w;
+        } else {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                g[v] = dY[(int64_t)r * lddy + c + v];
+                y[v] = Y[(int64_t)r * ldy + c + v];
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            g[v] = y[v] > 0.0f ? g[v] : 0.0f;
+            sum[v] += g[v];
+        }
+        float *o = dst + (int64_t)r * ldd + cc;
+        if (VEC == 4) {
+            *(float4 *)o = make_float4(g[0], g[1], g[2], g[3]);
+        } else {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) o[v] = g[v];
+        }
+        if (dst16) {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) dst16[(int64_t)r * ldd + cc + v] = f32_to_bf16_rne(g[v]);
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) part[(int64_t)chunk * w + c + v] = sum[v];
+}
+
+// Column sums of a chunk of rows (generic matrix).
+__global__ __launch_bounds__(256) void colsum_part_kernel(int32_t n, int32_t C, const float *__restrict__ G,
+                                                          int64_t ldg, float *__restrict__ part) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c >= C) return;
+    const int chunk = blockIdx.y;
+    const int r0 = chunk * kRowsPerChunk;
+    const int r1 = min(r0 + kRowsPerChunk, n);
+    float s = 0.0f;
+    for (int r = r0; r < r1; ++r) s += G[(int64_t)r * ldg + c];
+    part[(int64_t)chunk * C + c] = s;
+}
+
+// out[c] = sum over chunks of part[chunk][c], in chunk order.
+__global__ __launch_bounds__(256) void colsum_reduce_kernel(int32_t chunks, int32_t C,
+                                                            const float *__restrict__ part,
+                                                            float *__restrict__ out) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c >= C) return;
+    float s = 0.0f;
+    for (int k = 0; k < chunks; ++k) s += part[(int64_t)k * C + c];
+    out[c] = s;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return v;
+}
+
+// One wavefront per row of logits.  In place: X[i, :] <- dLoss/dX[i, :].
+__global__ __launch_bounds__(256) void loss_rows_kernel(int kind, int32_t n, int32_t C, float *__restrict__ X,
+                                                        const int32_t *__restrict__ labels,
+                                                        const float *__restrict__ targets,
+                                                        float *__restrict__ rowloss) {
+    const int lane = threadIdx.x & 63;
+    const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (i >= n) return;
+    float *x = X + i * C;
+    if (kind == GCN_SOFTMAX_CE) {
+        float m = -INFINITY;
+        for (int c = lane; c < C; c += 64) m = fmaxf(m, x[c]);
+        m = wave_max(m);
+        float s = 0.0f;
+        for (int c = lane; c < C; c += 64) s += expf(x[c] - m);
+        s = wave_sum(s);
+        const float lse = m + logf(s);
+        const int y = labels[i];
+        const float inv_n = 1.0f / (float)n;
+        float xy = 0.0f;
+        for (int c = lane; c < C; c += 64) {
+            const float v = x[c];
+            if (c == y) xy = v;
+            const float p = expf(v - lse);
+            x[c] = (p - (c == y ? 1.0f : 0.0f)) * inv_n;
+        }
+        xy = wave_sum(xy);
+        if (lane == 0) rowloss[i] = lse - xy;
+    } else {
+        const float *t = targets + i * C;
+        const float inv = 1.0f / ((float)n * (float)C);
+        float s = 0.0f;
+        for (int c = lane; c < C; c += 64) {
+            const float v = x[c];
+            const float tv = t[c];
+            const float e = expf(-fabsf(v));
+            s += fmaxf(v, 0.0f) - v * tv + log1pf(e);
+            const float sg = v >= 0.0f ? 1.0f / (1.0f + e) : e / (1.0f + e);
+            x[c] = (sg - tv) * inv;
+        }
+        s = wave_sum(s);
+        if (lane == 0) rowloss[i] = s;
+    }
+}
+
+// loss = scale * sum_i rowloss[i]: one block, fixed strided partition, fixed tree.
+__global__ __launch_bounds__(256) void loss_reduce_kernel(int32_t n, const float *__restrict__ rowloss,
+                                                          double scale, float *__restrict__ loss) {
+    __shared__ double sh[256];
+    double s = 0.0;
+    for (int i = threadIdx.x; i < n; i += 256) s += (double)rowloss[i];
+    sh[threadIdx.x] = s;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = (float)(sh[0] * scale);
+}
+
+__global__ __launch_bounds__(256) void cvt_bf16_kernel(int64_t rows, int64_t cols, const float *__restrict__ x,
+                                                       int64_t ldx, uint16_t *__restrict__ y, int64_t ldy) {
+    const int64_t total = rows * cols;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
+        const int64_t r = e / cols, c = e % cols;
+        y[r * ldy + c] = f32_to_bf16_rne(x[r * ldx + c]);
+    }
+}
+
+__global__ __launch_bounds__(256) void fill_zero_f32_kernel(float *__restrict__ x, int64_t count) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) x[i] = 0.0f;
+}
+
+}  // namespace
+
+int fill_zero(float *x, int64_t count, hipStream_t s) {
+    if (count <= 0) return GCN_OK;
+    int64_t g = (count + 255) / 256;
+    if (g > 4096) g = 4096;
+    hipLaunchKernelGGL(fill_zero_f32_kernel, dim3((unsigned)g), dim3(256), 0, s, x, count);
+    GCN_LAUNCH_CHECK("fill_zero_f32_kernel");
+    return GCN_OK;
+}
+
+size_t relu_bwd_workspace_bytes(int32_t n, int32_t h) {
+    const int64_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
+    return align256((size_t)chunks * 2 * h * sizeof(float)) + 256;
+}
+
+int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y, int64_t ldy,
+             float *outS, int64_t ldS, float *outN, int64_t ldN, uint16_t *outS16, uint16_t *outN16,
+             float *dbias, void *ws, size_t ws_bytes, hipStream_t s) {
+    if (h <= 0) return GCN_OK;
+    const int w = 2 * h;
+    const int32_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
+    Arena ar(ws, ws_bytes);
+    float *part = ar.take<float>((size_t)chunks * w + 1);
+    if (!part) {
+        set_error("relu_bwd: workspace too small");
+        return GCN_EWORKSPACE;
+    }
+    if (n > 0) {
+        auto al = [](const void *p) { return ((uintptr_t)p & 15) == 0; };
+        const bool v4 = h % 4 == 0 && lddy % 4 == 0 && ldy % 4 == 0 && ldS % 4 == 0 && ldN % 4 == 0 &&
+                        al(dY) && al(Y) && al(outS) && al(outN);
+        const double bytes = (double)n * w * 4.0 * 3.0 + (outS16 ? (double)n * w * 2.0 : 0.0);
+        ProfScope ps(K_RELU_MASK, s, 0.0, bytes);
+        if (v4) {
+            dim3 g((unsigned)((w / 4 + 255) / 256), (unsigned)chunks);
+            hipLaunchKernelGGL(relu_bwd_kernel<4>, g, dim3(256), 0, s, n, h, dY, lddy, Y, ldy, outS, ldS,
+                               outN, ldN, outS16, outN16, part);
+        } else {
+            dim3 g((unsigned)((w + 255) / 256), (unsigned)chunks);
+            hipLaunchKernelGGL(relu_bwd_kernel<1>, g, dim3(256), 0, s, n, h, dY, lddy, Y, ldy, outS, ldS,
+                               outN, ldN, outS16, outN16, part);
+        }
+        GCN_LAUNCH_CHECK("relu_bwd_kernel");
+    }
+    {
+        ProfScope ps(K_COLSUM_REDUCE, s, 0.0, (double)chunks * w * 4.0);
+        hipLaunchKernelGGL(colsum_reduce_kernel, dim3((unsigned)((w + 255) / 256)), dim3(256), 0, s, chunks, w,
+                           part, dbias);
+        GCN_LAUNCH_CHECK("colsum_reduce_kernel");
+    }
+    return GCN_OK;
+}
+
+size_t colsum_workspace_bytes(int32_t n, int32_t C) {
+    const int64_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
+    return align256((size_t)chunks * C * sizeof(float)) + 256;
+}
+
+int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *ws, size_t ws_bytes,
+           hipStream_t s) {
+    if (C <= 0) return GCN_OK;
+    const int32_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
+    Arena ar(ws, ws_bytes);
+    float *part = ar.take<float>((size_t)chunks * C + 1);
+    if (!part) {
+        set_error("colsum: workspace too small");
+        return GCN_EWORKSPACE;
+    }
+    if (n > 0) {
+        ProfScope ps(K_COLSUM_REDUCE, s, 0.0, (double)n * C * 4.0);
+        hipLaunchKernelGGL(colsum_part_kernel, dim3((unsigned)((C + 255) / 256), (unsigned)chunks), dim3(256), 0,
+                           s, n, C, G, ldg, part);
+        GCN_LAUNCH_CHECK("colsum_part_kernel");
+    }
+    {
+        ProfScope ps(K_COLSUM_REDUCE, s, 0.0, (double)chunks * C * 4.0);
+        hipLaunchKernelGGL(colsum_reduce_kernel, dim3((unsigned)((C + 255) / 256)), dim3(256), 0, s, chunks, C,
+                           part, out);
+        GCN_LAUNCH_CHECK("colsum_reduce_kernel");
+    }
+    return GCN_OK;
+}
+
+int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
+              float *rowloss, hipStream_t s) {
+    if (n <= 0) return GCN_OK;
+    ProfScope ps(K_LOSS_ROWS, s, 0.0, (double)n * C * 4.0 * (kind == GCN_SIGMOID_BCE ? 3.0 : 2.0));
+    hipLaunchKernelGGL(loss_rows_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, kind, n, C, X, labels,
+                       targets, rowloss);
+    GCN_LAUNCH_CHECK("loss_rows_kernel");
+    return GCN_OK;
+}
+
+int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, hipStream_t s) {
+    ProfScope ps(K_LOSS_REDUCE, s, 0.0, (double)n * 4.0);
+    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, n, rowloss, scale, loss);
+    GCN_LAUNCH_CHECK("loss_reduce_kernel");
+    return GCN_OK;
+}
+
+int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
+             hipStream_t s) {
+    const int64_t total = rows * cols;
+    if (total <= 0) return GCN_OK;
+    int64_t g = (total + 255) / 256;
+    if (g > 8192) g = 8192;
+    ProfScope ps(K_CVT_BF16, s, 0.0, (double)total * 6.0);
+    hipLaunchKernelGGL(cvt_bf16_kernel, dim3((unsigned)g), dim3(256), 0, s, rows, cols, x, ldx, y, ldy);
+    GCN_LAUNCH_CHECK("cvt_bf16_kernel");
+    return GCN_OK;
+}
+
+}  // namespace gcn

@@ -1,0 +1,414 @@
+// Weight application: dense products on the matrix cores (the second training
+// kernel of Sec. V-A, which the paper runs with a BLAS dgemm).
+//
+// One kernel family covers every dense product of the layer:
+//   NN  C = A B        forward:   H W_self, AGG W_neigh, H [W_self W_neigh], HL W_pred
+//   TN  C = A^T B      weights:   H^T dZ_s, AGG^T dZ_n, HL^T G     (K = n, split-K)
+//   NT  C = A B^T      inputs:    dZ_s W_self^T + G W_neigh^T, G W_pred^T
+// Each problem may sum two K-segments with their own operands (the concat of
+// the layer turns into a K-concat in the backward pass), and two problems of
+// one layout share a launch.
+//
+// Tiles: 256 threads = 4 wavefronts in a 2 x 2 grid; block tile 128 x 128,
+// wavefront tile 64 x 64 = 2 x 2 blocks of v_mfma_f32_32x32x2f32 (float32
+// operands, float32 accumulate) or v_mfma_f32_32x32x16_bf16 (bfloat16
+// operands).  K advances by BK per step through a double-buffered LDS tile
+// stored k-major, so that the matrix-core operand reads (32 consecutive m or n
+// per half-wavefront) hit 32 distinct banks.  Split-K partial tiles go to the
+// workspace and a second kernel adds them in split order (no atomics).
+#include <type_traits>
+
+#include "common.h"
+
+namespace gcn {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 128;
+constexpr int BN = 128;
+constexpr int PAD = 4;
+constexpr int kThreads = 256;
+
+struct Segs {
+    const void *A[2];
+    int64_t lda[2];
+    const void *B[2];
+    int64_t ldb[2];
+    int32_t K[2];
+    int32_t kt[2];  // k-tiles per segment
+};
+
+struct DevProblem {
+    int32_t M, N;
+    int32_t tiles_m, tiles_n;
+    int32_t split;      // number of K splits
+    int32_t kt_per_split;
+    int32_t kt_total;
+    int64_t block_begin;  // first flat block of this problem
+    Segs s;
+    float *C;
+    int64_t ldc;
+    const float *bias;
+    int relu;
+    float *partial;     // split x M x N when split > 1
+};
+
+struct DevArgs {
+    DevProblem p[2];
+    int nprob;
+};
+
+// ------------------------------------------------------------------ loading
+// Element type: float (fp32 path) or uint16_t (bf16 bits).
+template <typename T> __device__ __forceinline__ T zero_elem() { return T(0); }
+
+// Tile of one operand, BK x 128 elements, kept k-major in LDS: lds[k][x].
+//   KMAJOR: element (x, k) sits at ptr[k*ld + x]   (contiguous along x)
+//   else  : element (x, k) sits at ptr[x*ld + k]   (contiguous along k)
+template <typename T, int BK, bool KMAJOR, bool VEC>
+struct TileLoader {
+    // 16-byte vectors of T
+    static constexpr int E = 16 / sizeof(T);
+    static constexpr int kElems = BK * 128;
+    static constexpr int kVecs = kElems / E;
+    static constexpr int kPer = kVecs / kThreads;  // vectors per thread
+    static_assert(kPer >= 1, "tile too small");
+    typedef typename std::conditional<sizeof(T) == 4, float4, uint4>::type V;
+    V reg[kPer];
+
+    __device__ __forceinline__ void coords(int i, int &x, int &k) const {
+        const int v = threadIdx.x + i * kThreads;
+        if (KMAJOR) {            // vectors along x
+            constexpr int per_row = 128 / E;
+            k = v / per_row;
+            x = (v % per_row) * E;
+        } else {                 // vectors along k
+            constexpr int per_row = BK / E;
+            x = v / per_row;
+            k = (v % per_row) * E;
+        }
+    }
+
+    __device__ __forceinline__ void load(const T *__restrict__ ptr, int64_t ld, int x0, int xlim,
+                                         int k0, int klim) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            int x, k;
+            coords(i, x, k);
+            const int gx = x0 + x, gk = k0 + k;
+            if (VEC) {
+                // xlim / klim are multiples of E on the vector path
+                if (gx < xlim && gk < klim) {
+                    const T *p = KMAJOR ? ptr + (int64_t)gk * ld + gx : ptr + (int64_t)gx * ld + gk;
+                    reg[i] = *(const V *)p;
+                } else {
+                    reg[i] = V{};
+                }
+            } else {
+                T tmp[E];
+#pragma unroll
+                for (int e = 0; e < E; ++e) {
+                    const int ex = KMAJOR ? gx + e : gx;
+                    const int ek = KMAJOR ? gk : gk + e;
+                    tmp[e] = (ex < xlim && ek < klim)
+                                 ? (KMAJOR ? ptr[(int64_t)ek * ld + ex] : ptr[(int64_t)ex * ld + ek])
+                                 : zero_elem<T>();
+                }
+                reg[i] = *(V *)tmp;
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(T (*lds)[128 + PAD]) const {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            int x, k;
+            coords(i, x, k);
+            const T *t = (const T *)&reg[i];
+            if (KMAJOR) {
+                *(V *)&lds[k][x] = reg[i];
+            } else {
+#pragma unroll
+                for (int e = 0; e < E; ++e) lds[k + e][x] = t[e];
+            }
+        }
+    }
+};
+
+// -------------------------------------------------------------- main kernel
+template <int LAYOUT, bool VEC>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
+    using T = float;
+    constexpr int BK = 16;
+    constexpr bool A_KMAJOR = (LAYOUT == L_TN);
+    constexpr bool B_KMAJOR = (LAYOUT != L_NT);
+    __shared__ __attribute__((aligned(16))) T As[2][BK][128 + PAD];
+    __shared__ __attribute__((aligned(16))) T Bs[2][BK][128 + PAD];
+
+    // ---- which problem / split / tile
+    int64_t blk = blockIdx.x;
+    const int pi = (args.nprob > 1 && blk >= args.p[1].block_begin) ? 1 : 0;
+    const DevProblem &P = args.p[pi];
+    blk -= P.block_begin;
+    const int64_t tiles = (int64_t)P.tiles_m * P.tiles_n;
+    const int split = (int)(blk / tiles);
+    const int64_t t = blk % tiles;
+    const int tm = (int)(t / P.tiles_n);
+    const int tn = (int)(t % P.tiles_n);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kt_begin = split * P.kt_per_split;
+    int kt_end = kt_begin + P.kt_per_split;
+    if (kt_end > P.kt_total) kt_end = P.kt_total;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    TileLoader<T, BK, A_KMAJOR, VEC> la;
+    TileLoader<T, BK, B_KMAJOR, VEC> lb;
+
+    auto load = [&](int kt) {
+        const int sg = kt < P.s.kt[0] ? 0 : 1;
+        const int kk = (sg == 0 ? kt : kt - P.s.kt[0]) * BK;
+        const T *A = (const T *)P.s.A[sg];
+        const T *B = (const T *)P.s.B[sg];
+        la.load(A, P.s.lda[sg], m0, P.M, kk, P.s.K[sg]);
+        lb.load(B, P.s.ldb[sg], n0, P.N, kk, P.s.K[sg]);
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    if (kt_begin < kt_end) load(kt_begin);
+    int buf = 0;
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
+        la.store(As[buf]);
+        lb.store(Bs[buf]);
+        __syncthreads();
+        if (kt + 1 < kt_end) load(kt + 1);
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            const int kr = kk + (lane >> 5);
+            float a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) a[i] = As[buf][kr][wm * 64 + i * 32 + (lane & 31)];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) b[j] = Bs[buf][kr][wn * 64 + j * 32 + (lane & 31)];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        buf ^= 1;
+    }
+
+    // ---- epilogue: 32x32 accumulator layout, column = lane % 32,
+    //      row = 8*(r/4) + 4*(lane/32) + r%4
+    const bool to_partial = P.split > 1;
+    float *dst = to_partial ? P.partial + (int64_t)split * P.M * P.N : P.C;
+    const int64_t ldd = to_partial ? P.N : P.ldc;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+            if (col >= P.N) continue;
+            const float bv = (!to_partial && P.bias) ? P.bias[col] : 0.0f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row < P.M) {
+                    float v = acc[i][j][r];
+                    if (!to_partial) {
+                        v += bv;
+                        if (P.relu) v = fmaxf(v, 0.0f);
+                    }
+                    dst[(int64_t)row * ldd + col] = v;
+                }
+            }
+        }
+}
+
+// C = sum over splits of the partial tiles, in split order.
+__global__ __launch_bounds__(256) void splitk_reduce(DevArgs args) {
+    const int pi = blockIdx.y;
+    const DevProblem &P = args.p[pi];
+    const int64_t total = (int64_t)P.M * P.N;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
+        float acc = P.partial[e];
+        for (int s = 1; s < P.split; ++s) acc += P.partial[(int64_t)s * total + e];
+        const int row = (int)(e / P.N), col = (int)(e % P.N);
+        if (P.bias) acc += P.bias[col];
+        if (P.relu) acc = fmaxf(acc, 0.0f);
+        P.C[(int64_t)row * P.ldc + col] = acc;
+    }
+}
+
+bool al(const void *p, int b) { return ((uintptr_t)p % (uintptr_t)b) == 0; }
+
+// Vector loads need every contiguous extent, leading dimension and base
+// pointer to be a multiple of the 16-byte vector.
+bool vec_ok(int layout, const GemmProblem &g, int esz) {
+    const int E = 16 / esz;
+    const bool a_km = layout == L_TN, b_km = layout != L_NT;
+    for (int s = 0; s < 2; ++s) {
+        const GemmSeg &sg = g.seg[s];
+        if (sg.K == 0) continue;
+        if (sg.lda % E || sg.ldb % E || !al(sg.A, 16) || !al(sg.B, 16)) return false;
+        if (a_km ? (g.M % E) : (sg.K % E)) return false;
+        if (b_km ? (g.N % E) : (sg.K % E)) return false;
+    }
+    return true;
+}
+
+int bk_of(int bf16) { return bf16 ? 32 : 16; }
+
+void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k, float *partial,
+              DevArgs &a, int64_t &blocks) {
+    const int BK = bk_of(bf16);
+    blocks = 0;
+    a.nprob = nprob;
+    size_t poff = 0;
+    for (int i = 0; i < nprob; ++i) {
+        const GemmProblem &g = probs[i];
+        DevProblem &d = a.p[i];
+        d.M = g.M;
+        d.N = g.N;
+        d.tiles_m = (g.M + BM - 1) / BM;
+        d.tiles_n = (g.N + BN - 1) / BN;
+        d.kt_total = 0;
+        for (int s = 0; s < 2; ++s) {
+            d.s.A[s] = g.seg[s].A;
+            d.s.B[s] = g.seg[s].B;
+            d.s.lda[s] = g.seg[s].lda;
+            d.s.ldb[s] = g.seg[s].ldb;
+            d.s.K[s] = g.seg[s].K;
+            d.s.kt[s] = (g.seg[s].K + BK - 1) / BK;
+            d.kt_total += d.s.kt[s];
+        }
+        int sp = split_k < 1 ? 1 : split_k;
+        if (sp > d.kt_total) sp = d.kt_total > 0 ? d.kt_total : 1;
+        d.kt_per_split = d.kt_total > 0 ? (d.kt_total + sp - 1) / sp : 0;
+        // recompute so that no split is empty
+        d.split = d.kt_per_split > 0 ? (d.kt_total + d.kt_per_split - 1) / d.kt_per_split : 1;
+        d.block_begin = blocks;
+        blocks += (int64_t)d.tiles_m * d.tiles_n * d.split;
+        d.C = g.C;
+        d.ldc = g.ldc;
+        d.bias = g.bias;
+        d.relu = g.relu;
+        d.partial = nullptr;
+        if (d.split > 1) {
+            d.partial = partial ? (float *)((char *)partial + poff) : nullptr;
+            poff += align256((size_t)d.split * g.M * g.N * sizeof(float));
+        }
+    }
+    if (nprob < 2) a.p[1] = a.p[0];
+}
+
+template <int LAYOUT>
+void launch(bool vec, dim3 grid, hipStream_t s, const DevArgs &a) {
+    if (vec)
+        hipLaunchKernelGGL((gemm_kernel<LAYOUT, true>), grid, dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL((gemm_kernel<LAYOUT, false>), grid, dim3(kThreads), 0, s, a);
+}
+
+}  // namespace
+
+int gemm_pick_split(int nprob, const GemmProblem *probs) {
+    int64_t tiles = 0, kt = 0;
+    for (int i = 0; i < nprob; ++i) {
+        tiles += (int64_t)((probs[i].M + BM - 1) / BM) * ((probs[i].N + BN - 1) / BN);
+        int64_t k = 0;
+        for (int s = 0; s < 2; ++s) k += (probs[i].seg[s].K + 15) / 16;
+        if (k > kt) kt = k;
+    }
+    if (tiles <= 0) return 1;
+    int64_t sp = 1024 / tiles;          // about four blocks per CU in total
+    const int64_t max_sp = kt / 8;      // keep >= 8 k-tiles per split
+    if (sp > max_sp) sp = max_sp;
+    if (sp < 1) sp = 1;
+    return (int)sp;
+}
+
+size_t gemm_workspace_bytes(int nprob, const GemmProblem *probs, int split_k) {
+    if (split_k <= 1) return 0;
+    size_t b = 0;
+    for (int i = 0; i < nprob; ++i)
+        b += align256((size_t)split_k * probs[i].M * probs[i].N * sizeof(float));
+    return b + 256;
+}
+
+int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k, void *ws,
+         size_t ws_bytes, hipStream_t s) {
+    if (nprob < 1 || nprob > 2) {
+        set_error("gemm: nprob %d", nprob);
+        return GCN_EINVAL;
+    }
+    if (bf16) {
+        set_error("gemm: bfloat16 operands are not built yet");
+        return GCN_EUNSUPPORTED;
+    }
+    if (split_k > 1 && layout != L_TN) {
+        set_error("gemm: split-K only for the TN layout");
+        return GCN_EINVAL;
+    }
+    bool vec = true;
+    double flops = 0.0;
+    for (int i = 0; i < nprob; ++i) {
+        vec = vec && vec_ok(layout, probs[i], bf16 ? 2 : 4);
+        flops += 2.0 * probs[i].M * probs[i].N * ((double)probs[i].seg[0].K + probs[i].seg[1].K);
+    }
+    float *partial = nullptr;
+    if (split_k > 1) {
+        if (!ws || ws_bytes < gemm_workspace_bytes(nprob, probs, split_k)) {
+            set_error("gemm: split-K workspace too small");
+            return GCN_EWORKSPACE;
+        }
+        partial = (float *)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
+    }
+    DevArgs a;
+    int64_t blocks = 0;
+    fill_dev(layout, nprob, probs, bf16, split_k, partial, a, blocks);
+    if (blocks == 0) return GCN_OK;
+    bool any_split = false;
+    for (int i = 0; i < nprob; ++i) any_split = any_split || a.p[i].split > 1;
+    const int cls = layout == L_NN ? K_GEMM_NN : (layout == L_TN ? K_GEMM_TN : K_GEMM_NT);
+    {
+        ProfScope ps(cls, s, flops, 0.0);
+        dim3 grid((unsigned)blocks);
+        if (layout == L_NN) launch<L_NN>(vec, grid, s, a);
+        else if (layout == L_TN) launch<L_TN>(vec, grid, s, a);
+        else launch<L_NT>(vec, grid, s, a);
+        GCN_LAUNCH_CHECK("gemm_kernel");
+    }
+    if (any_split) {
+        double bytes = 0.0;
+        for (int i = 0; i < nprob; ++i)
+            bytes += (double)a.p[i].M * a.p[i].N * 4.0 * (a.p[i].split + 1);
+        ProfScope ps(K_SPLITK_REDUCE, s, 0.0, bytes);
+        int64_t maxe = 0;
+        for (int i = 0; i < nprob; ++i) maxe = std::max<int64_t>(maxe, (int64_t)a.p[i].M * a.p[i].N);
+        int64_t g = (maxe + 255) / 256;
+        if (g > 4096) g = 4096;
+        // a problem without splits is written by the main kernel already; the
+        // reduce skips it by running over zero elements
+        DevArgs r = a;
+        for (int i = 0; i < nprob; ++i)
+            if (r.p[i].split <= 1) { r.p[i].M = 0; }
+        hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r);
+        GCN_LAUNCH_CHECK("splitk_reduce");
+    }
+    return GCN_OK;
+}
+
+}  // namespace gcn

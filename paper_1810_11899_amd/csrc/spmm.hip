@@ -1,0 +1,364 @@
+// Feature propagation within the sampled subgraph: out = A X for CSR A.
+//
+// This is the first of the two training kernels of Sec. V-A.  The paper's
+// 40-core Xeon schedule (Alg. 6) slices the feature dimension so that each
+// slice of X stays in a core's cache; on gfx950 the same idea becomes the
+// column slice of one wavefront, while the graph dimension is balanced with a
+// merge path over (rows + edges):
+//
+//   * the merge sequence lists, row by row, the row's edges followed by one
+//     "row end" item; a wavefront owns `ipw` consecutive items, so a vertex of
+//     degree 14,000 is spread over many wavefronts and empty rows cost one item;
+//   * for every edge the wavefront reads the source row of X, k contiguous
+//     values, with each lane loading VEC consecutive columns (one coalesced
+//     row read per wavefront per edge); the edge index and weight are
+//     wave-uniform scalar loads;
+//   * a row completed inside one wavefront is written once, with the
+//     epilogue (store / +bias and ReLU / accumulate) fused;
+//   * a row cut by wavefront boundaries leaves float32 partial sums in the
+//     workspace, and a fix-up pass owned by the wavefront that completes the
+//     row adds them in wavefront order.  No atomics: the result is bitwise
+//     reproducible.
+//
+// Accumulation is float32 in increasing edge order within each piece.
+#include <type_traits>
+
+#include "common.h"
+
+namespace gcn {
+namespace {
+
+constexpr int kWavesPerBlock = 4;
+constexpr int kUnroll = 4;
+
+// Smallest r in [0, n_rows] whose row-end item sits at merge position >= d,
+// i.e. indptr[r+1] + r >= d (n_rows when none does).  64-ary search: every
+// lane probes one point of the current interval per round.
+__device__ __forceinline__ int merge_search(const int32_t *__restrict__ indptr, int32_t n_rows,
+                                            int64_t d, int lane) {
+    int64_t lo = 0, hi = n_rows;
+    while (lo < hi) {
+        const int64_t step = (hi - lo + 63) / 64;
+        const int64_t q = lo + (int64_t)lane * step;
+        bool pred = false;
+        if (q < hi) pred = (int64_t)indptr[q + 1] + q >= d;
+        const unsigned long long mask = __ballot(pred);
+        if (mask) {
+            const int l = __ffsll(mask) - 1;
+            const int64_t qs = lo + (int64_t)l * step;
+            lo = (l == 0) ? lo : qs - step + 1;
+            hi = qs;
+        } else {
+            const int64_t last = (hi - 1 - lo) / step;
+            lo = lo + last * step + 1;
+        }
+    }
+    return (int)lo;
+}
+
+template <int VEC, bool BF16> struct Row;
+template <> struct Row<1, false> {
+    float v[1];
+    __device__ void load(const float *p) { v[0] = *p; }
+};
+template <> struct Row<2, false> {
+    float v[2];
+    __device__ void load(const float *p) {
+        const float2 t = *(const float2 *)p;
+        v[0] = t.x; v[1] = t.y;
+    }
+};
+template <> struct Row<4, false> {
+    float v[4];
+    __device__ void load(const float *p) {
+        const float4 t = *(const float4 *)p;
+        v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+    }
+};
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+template <> struct Row<2, true> {
+    float v[2];
+    __device__ void load(const uint16_t *p) {
+        const uint32_t w = *(const uint32_t *)p;
+        v[0] = bf16_lo(w); v[1] = bf16_hi(w);
+    }
+};
+template <> struct Row<4, true> {
+    float v[4];
+    __device__ void load(const uint16_t *p) {
+        const uint2 w = *(const uint2 *)p;
+        v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x); v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
+    }
+};
+template <> struct Row<8, true> {
+    float v[8];
+    __device__ void load(const uint16_t *p) {
+        const uint4 w = *(const uint4 *)p;
+        v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x); v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
+        v[4] = bf16_lo(w.z); v[5] = bf16_hi(w.z); v[6] = bf16_lo(w.w); v[7] = bf16_hi(w.w);
+    }
+};
+template <> struct Row<1, true> {
+    float v[1];
+    __device__ void load(const uint16_t *p) { v[0] = __uint_as_float((uint32_t)(*p) << 16); }
+};
+
+template <int VEC>
+__device__ __forceinline__ void emit(float *__restrict__ out, const float (&acc)[VEC], int epi,
+                                     const float *__restrict__ bias, int c) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) {
+        float r = acc[v];
+        if (epi == EPI_BIAS_RELU) r = fmaxf(r + bias[c + v], 0.0f);
+        else if (epi == EPI_ACCUMULATE) r = out[v] + r;
+        out[v] = r;
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_raw(float *__restrict__ out, const float (&acc)[VEC]) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) out[v] = acc[v];
+}
+
+// One wavefront = `ipw` merge items x one column slice of width 64*VEC*CT.
+template <int VEC, int CT, bool BF16>
+__global__ __launch_bounds__(256) void spmm_main(
+    int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
+    const float *__restrict__ vals, const void *__restrict__ Xv, int32_t k, int64_t ldx,
+    float *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
+    int64_t items, int ipw, int64_t waves, float *__restrict__ carry,
+    int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
+    using Elem = typename std::conditional<BF16, uint16_t, float>::type;
+    const Elem *__restrict__ X = (const Elem *)Xv;
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (wave >= waves) return;
+    const int64_t d0 = wave * ipw;
+    const int64_t d1 = d0 + ipw < items ? d0 + ipw : items;
+    const int r0 = merge_search(indptr, n_rows, d0, lane);
+    const int r1 = merge_search(indptr, n_rows, d1, lane);
+    const int64_t p0 = d0 - r0, p1 = d1 - r1;
+
+    constexpr int SW = 64 * VEC * CT;
+    const int cbase = blockIdx.y * SW + lane * VEC;
+    bool cok[CT];
+#pragma unroll
+    for (int t = 0; t < CT; ++t) cok[t] = cbase + t * 64 * VEC < k;
+
+    int32_t hrow = -1, trow = -1;
+    for (int r = r0; r <= r1 && r < n_rows; ++r) {
+        const int64_t rb = indptr[r], re = indptr[r + 1];
+        const bool complete = r < r1;
+        const int64_t pb = p0 > rb ? p0 : rb;
+        const int64_t pe = complete ? re : p1;
+        float acc[CT][VEC];
+#pragma unroll
+        for (int t = 0; t < CT; ++t)
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) acc[t][v] = 0.0f;
+
+        int64_t p = pb;
+        for (; p + kUnroll <= pe; p += kUnroll) {
+            int32_t j[kUnroll];
+            float w[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) { j[u] = indices[p + u]; w[u] = vals[p + u]; }
+            Row<VEC, BF16> x[kUnroll][CT];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                for (int t = 0; t < CT; ++t)
+                    if (cok[t]) x[u][t].load(X + (int64_t)j[u] * ldx + cbase + t * 64 * VEC);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+                for (int t = 0; t < CT; ++t)
+                    if (cok[t])
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(w[u], x[u][t].v[v], acc[t][v]);
+        }
+        for (; p < pe; ++p) {
+            const int32_t j = indices[p];
+            const float w = vals[p];
+#pragma unroll
+            for (int t = 0; t < CT; ++t)
+                if (cok[t]) {
+                    Row<VEC, BF16> x;
+                    x.load(X + (int64_t)j * ldx + cbase + t * 64 * VEC);
+#pragma unroll
+                    for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(w, x.v[v], acc[t][v]);
+                }
+        }
+
+        const bool started = (r > r0) || (p0 == rb);
+        if (complete && started) {
+#pragma unroll
+            for (int t = 0; t < CT; ++t)
+                if (cok[t]) {
+                    const int c = cbase + t * 64 * VEC;
+                    emit<VEC>(out + (int64_t)r * ldo + c, acc[t], epi, bias, c);
+                }
+        } else if (complete || pe > pb) {
+            // a piece of a row cut by wavefront boundaries: head (the piece
+            // that completes the row) or tail (a piece that does not)
+            const int slot = complete ? 0 : 1;
+            float *dst = carry + (2 * wave + slot) * (int64_t)k;
+#pragma unroll
+            for (int t = 0; t < CT; ++t)
+                if (cok[t]) store_raw<VEC>(dst + cbase + t * 64 * VEC, acc[t]);
+            if (complete) hrow = r; else trow = r;
+        }
+    }
+    if (blockIdx.y == 0 && lane == 0) {
+        head_row[wave] = hrow;
+        tail_row[wave] = trow;
+    }
+}
+
+// Completes every row cut by wavefront boundaries: the wavefront w holding the
+// row's head piece sums the tail pieces of the preceding wavefronts in order,
+// then its own head piece, and applies the epilogue.
+__global__ __launch_bounds__(256) void spmm_fixup(int32_t k, float *__restrict__ out, int64_t ldo,
+                                                  int epi, const float *__restrict__ bias,
+                                                  int64_t waves, const float *__restrict__ carry,
+                                                  const int32_t *__restrict__ head_row,
+                                                  const int32_t *__restrict__ tail_row) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (w >= waves) return;
+    const int32_t r = head_row[w];
+    if (r < 0) return;
+    int64_t ws = w;
+    while (ws > 0 && tail_row[ws - 1] == r) --ws;
+    for (int c = blockIdx.y * 256 + lane; c < k && c < (int)(blockIdx.y + 1) * 256; c += 64) {
+        float acc = 0.0f;
+        bool first = true;
+        for (int64_t q = ws; q < w; ++q) {
+            const float v = carry[(2 * q + 1) * (int64_t)k + c];
+            acc = first ? v : acc + v;
+            first = false;
+        }
+        const float hv = carry[(2 * w) * (int64_t)k + c];
+        acc = first ? hv : acc + hv;
+        float *o = out + (int64_t)r * ldo + c;
+        if (epi == EPI_BIAS_RELU) acc = fmaxf(acc + bias[c], 0.0f);
+        else if (epi == EPI_ACCUMULATE) acc = *o + acc;
+        *o = acc;
+    }
+}
+
+template <int VEC, int CT, bool BF16>
+void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr,
+                 const int32_t *indices, const float *vals, const void *X, int32_t k, int64_t ldx,
+                 float *out, int64_t ldo, int epi, const float *bias, const SpmmPlan &pl,
+                 float *carry, int32_t *hr, int32_t *tr) {
+    hipLaunchKernelGGL((spmm_main<VEC, CT, BF16>), grid, dim3(256), 0, s, n_rows, indptr, indices,
+                       vals, X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw, pl.waves, carry, hr,
+                       tr);
+}
+
+bool aligned(const void *p, int bytes) { return ((uintptr_t)p % (uintptr_t)bytes) == 0; }
+
+int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+             const float *vals, const void *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+             int epi, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
+    if (n_rows <= 0 || k <= 0) return GCN_OK;
+    const SpmmPlan pl = spmm_plan(n_rows, nnz);
+    Arena ar(ws, ws_bytes);
+    float *carry = ar.take<float>((size_t)2 * pl.waves * k);
+    int32_t *hr = ar.take<int32_t>(pl.waves);
+    int32_t *tr = ar.take<int32_t>(pl.waves);
+    if (!carry || !hr || !tr) {
+        set_error("spmm: workspace too small (%zu < %zu bytes)", ws_bytes,
+                  spmm_workspace_bytes(n_rows, nnz, k));
+        return GCN_EWORKSPACE;
+    }
+    const int esz = bf16 ? 2 : 4;
+    // widest per-lane vector that divides k, the leading dimensions and the
+    // base pointers
+    int vec = bf16 ? 8 : 4;
+    while (vec > 1 && !(k % vec == 0 && ldx % vec == 0 && aligned(X, vec * esz))) vec /= 2;
+    // narrow rows: keep lanes busy by lowering the vector width
+    while (vec > 1 && 64 * (vec / 2) >= k) vec /= 2;
+    int ct = (k + 64 * vec - 1) / (64 * vec);
+    if (ct > 2) ct = 2;
+    const int sw = 64 * vec * ct;
+    dim3 grid((unsigned)((pl.waves + kWavesPerBlock - 1) / kWavesPerBlock), (unsigned)((k + sw - 1) / sw));
+    const double bytes = (double)nnz * k * esz + (double)nnz * 8.0 + (double)(n_rows + 1) * 4.0 +
+                         (double)n_rows * k * 4.0 * (epi == EPI_ACCUMULATE ? 2.0 : 1.0);
+    {
+        ProfScope ps(K_SPMM, s, 2.0 * nnz * k, bytes);
+#define GCN_SPMM_CASE(V, C, B)                                                                   \
+    if (vec == V && ct == C && bf16 == B) {                                                      \
+        launch_main<V, C, B>(grid, s, n_rows, indptr, indices, vals, X, k, ldx, out, ldo, epi,   \
+                             bias, pl, carry, hr, tr);                                           \
+    } else
+        GCN_SPMM_CASE(4, 1, false)
+        GCN_SPMM_CASE(4, 2, false)
+        GCN_SPMM_CASE(2, 1, false)
+        GCN_SPMM_CASE(2, 2, false)
+        GCN_SPMM_CASE(1, 1, false)
+        GCN_SPMM_CASE(1, 2, false)
+        GCN_SPMM_CASE(8, 1, true)
+        GCN_SPMM_CASE(8, 2, true)
+        GCN_SPMM_CASE(4, 1, true)
+        GCN_SPMM_CASE(4, 2, true)
+        GCN_SPMM_CASE(2, 1, true)
+        GCN_SPMM_CASE(2, 2, true)
+        GCN_SPMM_CASE(1, 1, true)
+        GCN_SPMM_CASE(1, 2, true) {
+            set_error("spmm: no kernel for vec=%d ct=%d", vec, ct);
+            return GCN_EUNSUPPORTED;
+        }
+#undef GCN_SPMM_CASE
+        GCN_LAUNCH_CHECK("spmm_main");
+    }
+    {
+        ProfScope ps(K_SPMM_FIXUP, s, 0.0, 0.0);
+        dim3 g2((unsigned)((pl.waves + kWavesPerBlock - 1) / kWavesPerBlock), (unsigned)((k + 255) / 256));
+        hipLaunchKernelGGL(spmm_fixup, g2, dim3(256), 0, s, k, out, ldo, epi, bias, pl.waves, carry,
+                           hr, tr);
+        GCN_LAUNCH_CHECK("spmm_fixup");
+    }
+    return GCN_OK;
+}
+
+}  // namespace
+
+SpmmPlan spmm_plan(int32_t n_rows, int32_t nnz) {
+    SpmmPlan p;
+    p.items = (int64_t)n_rows + (int64_t)nnz;
+    // aim for >= 8192 wavefronts (32 per CU) before growing the per-wave share
+    int64_t ipw = (p.items + 8191) / 8192;
+    ipw = (ipw + 31) / 32 * 32;
+    if (ipw < 32) ipw = 32;
+    if (ipw > 256) ipw = 256;
+    p.ipw = (int)ipw;
+    p.waves = (p.items + ipw - 1) / ipw;
+    if (p.waves == 0) p.waves = 1;
+    return p;
+}
+
+size_t spmm_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k) {
+    if (n_rows <= 0 || k <= 0) return 0;
+    const SpmmPlan pl = spmm_plan(n_rows, nnz);
+    return align256((size_t)2 * pl.waves * k * sizeof(float)) + 2 * align256(pl.waves * sizeof(int32_t)) + 256;
+}
+
+int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+             const float *vals, const float *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
+    return spmm_any(false, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
+                    ws, ws_bytes, s);
+}
+
+int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+              const float *vals, const uint16_t *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
+    return spmm_any(true, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
+                    ws, ws_bytes, s);
+}
+
+}  // namespace gcn

@@ -1,0 +1,252 @@
+// CSR of A^T for the backward propagation.
+//
+// Row j of A^T lists the rows i of A that hold column j, in ascending i, with
+// equal entries in their CSR order.  The CSR entries are already in row-major
+// order, so A^T is exactly a *stable* sort of the entries by column.  This is
+// done as an LSD radix sort of (key = column, value = entry position p) with
+// 8-bit digits:
+//   1. per-tile digit histograms (integer LDS atomics: counts do not depend on
+//      the order of the increments);
+//   2. one exclusive scan over (digit, tile) in digit-major order;
+//   3. a stable scatter: each tile walks its keys in order, 256 at a time, and
+//      ranks equal digits with wavefront ballots (lane order) and per-wavefront
+//      counts (wavefront order), so every key lands at a position that only
+//      depends on the input.
+// Then t_indptr[j] = lower_bound(sorted keys, j), and each output entry looks
+// up its source row (upper_bound of p in indptr, minus one) and copies vals[p]
+// bit for bit.  The integer output is unique, hence bit-exact.
+#include "common.h"
+
+namespace gcn {
+namespace {
+
+constexpr int kTB = 256;            // threads per tile block
+constexpr int kItems = 8;           // keys per thread per tile
+constexpr int kTile = kTB * kItems; // keys per tile
+constexpr int kRadix = 256;
+
+__global__ __launch_bounds__(kTB) void iota_kernel(int32_t nnz, const int32_t *__restrict__ indices,
+                                                   uint32_t *__restrict__ keys, int32_t *__restrict__ vals) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < nnz; p += stride) {
+        keys[p] = (uint32_t)indices[p];
+        vals[p] = (int32_t)p;
+    }
+}
+
+__global__ __launch_bounds__(kTB) void hist_kernel(int32_t nnz, const uint32_t *__restrict__ keys, int shift,
+                                                   int32_t ntiles, int32_t *__restrict__ hist) {
+    __shared__ int32_t cnt[kRadix];
+    cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kTile;
+    for (int it = 0; it < kItems; ++it) {
+        const int64_t p = base + it * kTB + threadIdx.x;
+        if (p < nnz) atomicAdd(&cnt[(keys[p] >> shift) & 0xFF], 1);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// Exclusive scan of `len` ints by one block of 1024 threads (contiguous chunk
+// per thread, then a scan of the chunk totals).
+__global__ __launch_bounds__(1024) void scan_kernel(int64_t len, const int32_t *__restrict__ in,
+                                                    int32_t *__restrict__ out, int32_t *__restrict__ total) {
+    __shared__ int32_t sh[1024];
+    const int t = threadIdx.x;
+    const int64_t per = (len + 1023) / 1024;
+    const int64_t b = t * per;
+    const int64_t e = b + per < len ? b + per : len;
+    int32_t s = 0;
+    for (int64_t i = b; i < e; ++i) s += in[i];
+    sh[t] = s;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+        const int32_t v = t >= o ? sh[t - o] : 0;
+        __syncthreads();
+        sh[t] += v;
+        __syncthreads();
+    }
+    int32_t run = sh[t] - s;  // exclusive prefix of this chunk
+    for (int64_t i = b; i < e; ++i) {
+        const int32_t v = in[i];
+        out[i] = run;
+        run += v;
+    }
+    if (t == 1023 && total) *total = sh[1023];
+}
+
+__global__ __launch_bounds__(kTB) void scatter_kernel(int32_t nnz, const uint32_t *__restrict__ keys_in,
+                                                      const int32_t *__restrict__ vals_in, int shift,
+                                                      int32_t ntiles, const int32_t *__restrict__ offs,
+                                                      uint32_t *__restrict__ keys_out,
+                                                      int32_t *__restrict__ vals_out) {
+    __shared__ int32_t run[kRadix];          // keys of each digit placed so far by this tile
+    __shared__ int32_t wcnt[kTB / 64][kRadix];
+    const int t = threadIdx.x;
+    const int lane = t & 63, wave = t >> 6;
+    run[t] = offs[(int64_t)t * ntiles + blockIdx.x];
+    const int64_t base = (int64_t)blockIdx.x * kTile;
+    const unsigned long long below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int it = 0; it < kItems; ++it) {
+        for (int w = 0; w < kTB / 64; ++w) wcnt[w][t] = 0;
+        __syncthreads();
+        const int64_t p = base + it * kTB + t;
+        const bool valid = p < nnz;
+        uint32_t key = 0;
+        int32_t val = 0;
+        int digit = 0;
+        if (valid) {
+            key = keys_in[p];
+            val = vals_in[p];
+            digit = (key >> shift) & 0xFF;
+        }
+        // lanes of this wavefront holding the same digit
+        unsigned long long match = __ballot(valid);
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+            const unsigned long long bb = __ballot((digit >> bit) & 1);
+            match &= ((digit >> bit) & 1) ? bb : ~bb;
+        }
+        const int wrank = __popcll(match & below);
+        if (valid && wrank == 0) wcnt[wave][digit] = __popcll(match);
+        __syncthreads();
+        if (valid) {
+            int pos = run[digit] + wrank;
+            for (int w = 0; w < wave; ++w) pos += wcnt[w][digit];
+            keys_out[pos] = key;
+            vals_out[pos] = val;
+        }
+        __syncthreads();
+        int32_t add = 0;
+        for (int w = 0; w < kTB / 64; ++w) add += wcnt[w][t];
+        run[t] += add;
+        __syncthreads();
+    }
+}
+
+// t_indptr[j] = number of sorted keys < j, for j in [0, n_cols]
+__global__ __launch_bounds__(kTB) void bounds_kernel(int32_t n_cols, int32_t nnz,
+                                                     const uint32_t *__restrict__ keys,
+                                                     int32_t *__restrict__ t_indptr) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j > n_cols) return;
+    int64_t lo = 0, hi = nnz;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if ((int64_t)keys[mid] < j) lo = mid + 1; else hi = mid;
+    }
+    t_indptr[j] = (int32_t)lo;
+}
+
+// t_indices[q] = row of entry perm[q] in A;  t_vals[q] = vals[perm[q]]
+__global__ __launch_bounds__(kTB) void finalize_kernel(int32_t n_rows, int32_t nnz,
+                                                       const int32_t *__restrict__ indptr,
+                                                       const float *__restrict__ vals,
+                                                       const int32_t *__restrict__ perm,
+                                                       int32_t *__restrict__ t_indices,
+                                                       float *__restrict__ t_vals) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nnz; q += stride) {
+        const int32_t p = perm[q];
+        // last row i with indptr[i] <= p
+        int64_t lo = 0, hi = n_rows;  // answer in [0, n_rows)
+        while (lo < hi) {
+            const int64_t mid = (lo + hi + 1) >> 1;
+            if (indptr[mid] <= p) lo = mid; else hi = mid - 1;
+        }
+        t_indices[q] = (int32_t)lo;
+        t_vals[q] = vals[p];
+    }
+}
+
+__global__ void fill_zero_kernel(int32_t *__restrict__ x, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) x[i] = 0;
+}
+
+int key_bits(int32_t n_cols) {
+    int b = 0;
+    while (b < 31 && ((int64_t)1 << b) < (int64_t)n_cols) ++b;
+    return b;  // keys are < n_cols <= 2^b
+}
+
+}  // namespace
+
+size_t transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz) {
+    (void)n_rows;
+    (void)n_cols;
+    const int64_t ntiles = ((int64_t)nnz + kTile - 1) / kTile;
+    size_t b = 0;
+    b += 2 * align256((size_t)nnz * 4);          // keys ping-pong
+    b += 2 * align256((size_t)nnz * 4);          // values ping-pong
+    b += 2 * align256((size_t)ntiles * kRadix * 4);  // hist, offsets
+    return b + 256;
+}
+
+int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+                  const float *vals, int32_t *t_indptr, int32_t *t_indices, float *t_vals, void *ws,
+                  size_t ws_bytes, hipStream_t s) {
+    if (nnz == 0) {
+        ProfScope ps(K_T_FINAL, s, 0.0, (double)(n_cols + 1) * 4.0);
+        hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n_cols + 1 + 255) / 256)), dim3(256), 0, s,
+                           t_indptr, (int64_t)n_cols + 1);
+        GCN_LAUNCH_CHECK("fill_zero_kernel");
+        return GCN_OK;
+    }
+    const int32_t ntiles = (int32_t)(((int64_t)nnz + kTile - 1) / kTile);
+    Arena ar(ws, ws_bytes);
+    uint32_t *ka = ar.take<uint32_t>(nnz), *kb = ar.take<uint32_t>(nnz);
+    int32_t *va = ar.take<int32_t>(nnz), *vb = ar.take<int32_t>(nnz);
+    int32_t *hist = ar.take<int32_t>((size_t)ntiles * kRadix);
+    int32_t *offs = ar.take<int32_t>((size_t)ntiles * kRadix);
+    if (!ka || !kb || !va || !vb || !hist || !offs) {
+        set_error("csr_transpose: workspace too small (%zu < %zu bytes)", ws_bytes,
+                  transpose_workspace_bytes(n_rows, n_cols, nnz));
+        return GCN_EWORKSPACE;
+    }
+    unsigned g = (unsigned)((nnz + kTB - 1) / kTB);
+    if (g > 16384) g = 16384;
+    {
+        ProfScope ps(K_T_COUNT, s, 0.0, (double)nnz * 12.0);
+        hipLaunchKernelGGL(iota_kernel, dim3(g), dim3(kTB), 0, s, nnz, indices, ka, va);
+        GCN_LAUNCH_CHECK("iota_kernel");
+    }
+    const int bits = key_bits(n_cols);
+    for (int shift = 0; shift < bits || shift == 0; shift += 8) {
+        {
+            ProfScope ps(K_T_COUNT, s, 0.0, (double)nnz * 4.0);
+            hipLaunchKernelGGL(hist_kernel, dim3(ntiles), dim3(kTB), 0, s, nnz, ka, shift, ntiles, hist);
+            GCN_LAUNCH_CHECK("hist_kernel");
+        }
+        {
+            ProfScope ps(K_T_SCAN, s, 0.0, (double)ntiles * kRadix * 8.0);
+            hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, (int64_t)ntiles * kRadix, hist, offs,
+                               (int32_t *)nullptr);
+            GCN_LAUNCH_CHECK("scan_kernel");
+        }
+        {
+            ProfScope ps(K_T_FILL, s, 0.0, (double)nnz * 16.0);
+            hipLaunchKernelGGL(scatter_kernel, dim3(ntiles), dim3(kTB), 0, s, nnz, ka, va, shift, ntiles, offs,
+                               kb, vb);
+            GCN_LAUNCH_CHECK("scatter_kernel");
+        }
+        std::swap(ka, kb);
+        std::swap(va, vb);
+    }
+    {
+        ProfScope ps(K_T_FINAL, s, 0.0, (double)(n_cols + 1) * 4.0);
+        hipLaunchKernelGGL(bounds_kernel, dim3((unsigned)((n_cols + 1 + kTB - 1) / kTB)), dim3(kTB), 0, s,
+                           n_cols, nnz, ka, t_indptr);
+        GCN_LAUNCH_CHECK("bounds_kernel");
+    }
+    {
+        ProfScope ps(K_T_FINAL, s, 0.0, (double)nnz * 16.0);
+        hipLaunchKernelGGL(finalize_kernel, dim3(g), dim3(kTB), 0, s, n_rows, nnz, indptr, vals, va, t_indices,
+                           t_vals);
+        GCN_LAUNCH_CHECK("finalize_kernel");
+    }
+    return GCN_OK;
+}
+
+}  // namespace gcn

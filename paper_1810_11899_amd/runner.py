@@ -1,0 +1,170 @@
+"""One fwd+bwd training step of an L-layer GCN on a sampled subgraph.
+
+Holds the device buffers of a workload (sized once, reused across steps and
+across the subgraphs of an epoch stream) and issues the C-ABI calls of one
+step on one stream: CSR transpose, the layers' forward, PREDICT/LOSS (or a
+given output gradient), the layers' backward (Alg. 1, forward loop, PREDICT,
+LOSS and the backward pass that ADAM consumes).  No arithmetic happens here.
+"""
+from __future__ import annotations
+
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+from . import binding as B
+
+
+class StepRunner:
+    def __init__(self, wl, prec: int = B.GCN_F32, device: str = "cuda",
+                 first_layer_dH: Optional[bool] = None, nnz_capacity: int = 0,
+                 orders: Optional[List[int]] = None):
+        self.dev = torch.device(device)
+        self.prec = prec
+        self.spec = wl.spec
+        self.L = len(wl.layers)
+        self.first_layer_dH = (self.L == 1) if first_layer_dH is None else bool(first_layer_dH)
+        self.ws = B.Workspace(self.dev)
+        self.n = wl.n
+        self._alloc_graph(max(nnz_capacity, wl.graph.nnz))
+        f = lambda a: torch.as_tensor(a, dtype=torch.float32).to(self.dev)
+        self.W = [(f(l.W_self), f(l.W_neigh), f(l.bias)) for l in wl.layers]
+        self.dims = [(l.f_in, l.h) for l in wl.layers]
+        self.orders = []
+        for li, (f_in, h) in enumerate(self.dims):
+            need = li > 0 or self.first_layer_dH
+            self.orders.append(orders[li] if orders is not None else B.gcn_layer_pick_order(f_in, h, need))
+        n = self.n
+        self.H0 = torch.empty((n, self.dims[0][0]), dtype=torch.float32, device=self.dev)
+        self.Y = [torch.empty((n, 2 * h), dtype=torch.float32, device=self.dev) for (_, h) in self.dims]
+        self.saved = []
+        for (f_in, h), o in zip(self.dims, self.orders):
+            nb = B.gcn_layer_saved_bytes(n, f_in, h, o, prec)
+            self.saved.append(torch.empty(max(nb, 256), dtype=torch.uint8, device=self.dev) if nb else None)
+        self.dH = []
+        for li, (f_in, _) in enumerate(self.dims):
+            need = li > 0 or self.first_layer_dH
+            self.dH.append(torch.empty((n, f_in), dtype=torch.float32, device=self.dev) if need else None)
+        self.dWs = [torch.empty((f_in, h), dtype=torch.float32, device=self.dev) for (f_in, h) in self.dims]
+        self.dWn = [torch.empty((f_in, h), dtype=torch.float32, device=self.dev) for (f_in, h) in self.dims]
+        self.db = [torch.empty(2 * h, dtype=torch.float32, device=self.dev) for (_, h) in self.dims]
+        self.head = self.spec.head
+        hl2 = 2 * self.dims[-1][1]
+        if self.head is None:
+            self.dY = torch.empty((n, hl2), dtype=torch.float32, device=self.dev)
+        else:
+            C = self.spec.classes
+            self.W_pred = f(wl.W_pred)
+            self.b_pred = f(wl.b_pred)
+            self.kind = B.LOSS_KIND[self.head]
+            self.labels = torch.empty(n, dtype=torch.int32, device=self.dev) if self.head == "ce" else None
+            self.targets = torch.empty((n, C), dtype=torch.float32, device=self.dev) if self.head == "bce" else None
+            self.loss = torch.empty(1, dtype=torch.float32, device=self.dev)
+            self.dHL = torch.empty((n, hl2), dtype=torch.float32, device=self.dev)
+            self.dW_pred = torch.empty((hl2, C), dtype=torch.float32, device=self.dev)
+            self.db_pred = torch.empty(C, dtype=torch.float32, device=self.dev)
+        self.load(wl)
+
+    # ------------------------------------------------------------ buffers
+    def _alloc_graph(self, cap: int):
+        n, d = self.n, self.dev
+        self.cap = max(int(cap), 1)
+        self.indptr = torch.empty(n + 1, dtype=torch.int32, device=d)
+        self.indices = torch.empty(self.cap, dtype=torch.int32, device=d)
+        self.vals = torch.empty(self.cap, dtype=torch.float32, device=d)
+        self.t_indptr = torch.empty(n + 1, dtype=torch.int32, device=d)
+        self.t_indices = torch.empty(self.cap, dtype=torch.int32, device=d)
+        self.t_vals = torch.empty(self.cap, dtype=torch.float32, device=d)
+
+    def load(self, wl, non_blocking: bool = False):
+        """Copy a subgraph's CSR, features and labels into the resident buffers."""
+        g = wl.graph
+        if g.n != self.n:
+            raise ValueError("subgraph size differs from the buffers")
+        if g.nnz > self.cap:
+            self._alloc_graph(g.nnz)
+        self.nnz = g.nnz
+        self.indptr.copy_(torch.from_numpy(g.indptr), non_blocking=non_blocking)
+        if g.nnz:
+            self.indices[:g.nnz].copy_(torch.from_numpy(g.indices), non_blocking=non_blocking)
+            self.vals[:g.nnz].copy_(torch.from_numpy(g.vals), non_blocking=non_blocking)
+        self.H0.copy_(torch.from_numpy(wl.H), non_blocking=non_blocking)
+        if self.head is None:
+            self.dY.copy_(torch.from_numpy(wl.dY), non_blocking=non_blocking)
+        else:
+            if self.labels is not None:
+                self.labels.copy_(torch.from_numpy(wl.labels), non_blocking=non_blocking)
+            if self.targets is not None:
+                self.targets.copy_(torch.from_numpy(wl.targets), non_blocking=non_blocking)
+        self.A = B.DeviceCSR(self.n, self.n, self.indptr, self.indices[:self.nnz], self.vals[:self.nnz])
+        self.AT = B.DeviceCSR(self.n, self.n, self.t_indptr, self.t_indices[:self.nnz], self.t_vals[:self.nnz])
+
+    # --------------------------------------------------------------- step
+    def step(self, stream=None):
+        B.gcn_csr_transpose_into(self.A, self.AT.indptr, self.AT.indices, self.AT.vals, self.ws, stream)
+        H = self.H0
+        for li in range(self.L):
+            Ws, Wn, b = self.W[li]
+            B.gcn_layer_fwd(self.A, H, Ws, Wn, b, self.Y[li], self.saved[li], self.orders[li], self.ws,
+                            self.prec, stream)
+            H = self.Y[li]
+        if self.head is None:
+            dY = self.dY
+        else:
+            B.gcn_loss_grad(self.Y[-1], self.W_pred, self.b_pred, self.kind, self.labels, self.targets,
+                            self.loss, self.dHL, self.dW_pred, self.db_pred, self.ws, self.prec, stream)
+            dY = self.dHL
+        for li in range(self.L - 1, -1, -1):
+            Ws, Wn, _ = self.W[li]
+            Hin = self.H0 if li == 0 else self.Y[li - 1]
+            B.gcn_layer_bwd(self.A, self.AT, Hin, Ws, Wn, self.Y[li], self.saved[li], dY, self.dH[li],
+                            self.dWs[li], self.dWn[li], self.db[li], self.orders[li], self.ws, self.prec,
+                            stream)
+            dY = self.dH[li]
+
+    # ------------------------------------------------------------ results
+    def results(self) -> dict:
+        c = lambda t: None if t is None else t.detach().cpu().numpy()
+        r = {"Y": [c(y) for y in self.Y], "dW_self": [c(t) for t in self.dWs],
+             "dW_neigh": [c(t) for t in self.dWn], "db": [c(t) for t in self.db],
+             "dH": [c(t) for t in self.dH],
+             "t_indptr": c(self.AT.indptr), "t_indices": c(self.AT.indices), "t_vals": c(self.AT.vals)}
+        if self.head is not None:
+            r.update(loss=float(self.loss.item()), dW_pred=c(self.dW_pred), db_pred=c(self.db_pred),
+                     dHL=c(self.dHL))
+        return r
+
+    # ---------------------------------------------------- work accounting
+    def work(self) -> dict:
+        return step_work(self.n, self.nnz, self.dims, self.orders,
+                         [d is not None for d in self.dH],
+                         self.spec.classes if self.head is not None else 0)
+
+
+def step_work(n: int, nnz: int, dims, orders, need_dH, classes: int = 0) -> dict:
+    """Algorithmic work of one fwd+bwd step.
+
+    edge-features: sum over the aggregation passes of nnz x (aggregated width);
+    GEMM flops: 2*M*N*K summed over every dense product of the step.
+    Aggregate-first aggregates H at f_in in the forward pass and, for the input
+    gradient, A^T at min(f_in, h); transform-first aggregates at h forward and
+    h backward (A^T dZ_n, shared by dW_neigh and dH).
+    """
+    ef = 0
+    fl = 0.0
+    for (f_in, h), o, dH in zip(dims, orders, need_dH):
+        fl += 2.0 * n * f_in * h * 2          # forward: two n x f_in x h products
+        fl += 2.0 * n * f_in * h * 2          # weight gradients (K = n)
+        if dH:
+            fl += 2.0 * n * f_in * h * 2      # input gradient
+        if o == B.GCN_AGGREGATE_FIRST:
+            ef += nnz * f_in
+            if dH:
+                ef += nnz * min(f_in, h)
+        else:
+            ef += nnz * h * 2
+    if classes:
+        f2 = 2 * dims[-1][1]
+        fl += 3 * 2.0 * n * f2 * classes      # logits, dW_pred, dH_L
+    return {"edge_features": float(ef), "gemm_flops": fl, "spmm_flops": 2.0 * ef}

@@ -1,0 +1,140 @@
+"""The C-ABI library on the host: it loads, exports every declared symbol, and
+rejects malformed arguments before launching anything (no GPU needed)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1810_11899_amd import binding as B
+from paper_1810_11899_amd import build as pkg_build
+from paper_1810_11899_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(pkg_build.LIB_PATH):
+        pkg_build.build_library()
+    return B.lib()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "gcn_layer.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gcn_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 18
+    for nm in names:
+        assert hasattr(L, nm), nm
+    assert set(names) == set(B.exported_symbols())
+
+
+def test_version(L):
+    assert L.gcn_version() >= 100
+
+
+def test_validate_host_accepts_generated_graph(L):
+    g = synth.config(0).graph
+    assert B.gcn_csr_validate_host(g.n, g.n, g.indptr, g.indices) == B.GCN_OK
+
+
+@pytest.mark.parametrize("mutate, msg", [
+    (lambda ip, ix: (ip, np.where(np.arange(ix.size) == 3, 10 ** 6, ix)), "outside"),
+    (lambda ip, ix: (np.where(np.arange(ip.size) == 5, ip[4] - 1, ip), ix), "decreases"),
+    (lambda ip, ix: (ip, np.concatenate([ix[:1], ix[:1], ix[2:]])), "ascending"),
+])
+def test_validate_host_rejects(L, mutate, msg):
+    g = synth.custom(50, "er", 6, [(2, 2)]).graph
+    ip, ix = mutate(g.indptr.copy(), g.indices.copy())
+    rc = B.gcn_csr_validate_host(g.n, g.n, ip, ix)
+    assert rc == B.GCN_EINVAL
+    assert msg in L.gcn_last_error().decode()
+
+
+def test_validate_host_bad_endpoints(L):
+    ip = np.array([1, 2, 3], np.int32)
+    assert B.gcn_csr_validate_host(2, 2, ip, np.array([0, 1], np.int32)) == B.GCN_EINVAL
+    ip = np.array([0, 1, 1], np.int32)
+    assert B.gcn_csr_validate_host(2, 2, ip, np.array([0, 1], np.int32)) == B.GCN_EINVAL  # nnz mismatch
+
+
+def _fake_csr(n, nnz):
+    # non-null placeholder addresses: validation must fail before they are used
+    return B.gcn_csr(n, n, nnz, 0x1000, 0x2000 if nnz else None, 0x3000 if nnz else None)
+
+
+def test_layer_fwd_argument_errors(L):
+    A = _fake_csr(100, 400)
+    P = ctypes.c_void_p
+    fake = P(0x4000)
+
+    def fwd(f_in=8, ldh=8, h=4, ldy=8, order=0, prec=0, ws_bytes=1 << 30, saved_bytes=1 << 30, A=A):
+        return L.gcn_layer_fwd(ctypes.byref(A), fake, f_in, ldh, fake, fake, fake, h, fake, ldy, fake,
+                               saved_bytes, order, prec, fake, ws_bytes, None)
+
+    assert fwd(ldh=7) == B.GCN_ESHAPE
+    assert fwd(ldy=7) == B.GCN_ESHAPE
+    assert fwd(h=0) == B.GCN_ESHAPE
+    assert fwd(order=7) == B.GCN_EINVAL
+    assert fwd(prec=9) == B.GCN_EINVAL
+    assert fwd(ws_bytes=16) == B.GCN_EWORKSPACE
+    assert fwd(saved_bytes=16) == B.GCN_EWORKSPACE
+    rect = B.gcn_csr(100, 90, 400, 0x1000, 0x2000, 0x3000)
+    assert fwd(A=rect) == B.GCN_ESHAPE
+    nullcsr = B.gcn_csr(100, 100, 400, 0x1000, None, 0x3000)
+    assert fwd(A=nullcsr) == B.GCN_EINVAL
+    assert "null" in L.gcn_last_error().decode()
+
+
+def test_layer_bwd_transpose_mismatch(L):
+    A = _fake_csr(100, 400)
+    AT = _fake_csr(100, 399)
+    fake = ctypes.c_void_p(0x4000)
+    rc = L.gcn_layer_bwd(ctypes.byref(A), ctypes.byref(AT), fake, 8, 8, fake, fake, 4, fake, 8, fake,
+                         1 << 30, fake, 8, None, 0, fake, fake, fake, 0, 0, fake, 1 << 30, None)
+    assert rc == B.GCN_ESHAPE
+
+
+def test_loss_argument_errors(L):
+    fake = ctypes.c_void_p(0x4000)
+
+    def loss(n=10, f=8, ld=8, C=5, kind=0, labels=fake, targets=None, ws=1 << 30):
+        return L.gcn_loss_grad(fake, n, f, ld, fake, fake, C, kind, labels, targets, fake, fake, ld, fake,
+                               fake, 0, fake, ws, None)
+
+    assert loss(ld=7) == B.GCN_ESHAPE
+    assert loss(kind=5) == B.GCN_EINVAL
+    assert loss(labels=None) == B.GCN_EINVAL
+    assert loss(kind=1, targets=None) == B.GCN_EINVAL
+    assert loss(ws=8) == B.GCN_EWORKSPACE
+
+
+def test_workspace_queries_are_monotone(L):
+    a = L.gcn_layer_workspace_bytes(1000, 10000, 64, 64, 0, 0)
+    b = L.gcn_layer_workspace_bytes(2000, 20000, 64, 64, 0, 0)
+    assert 0 < a < b
+    assert L.gcn_layer_saved_bytes(1000, 64, 32, B.GCN_AGGREGATE_FIRST, 0) >= 1000 * 64 * 4
+    assert L.gcn_layer_saved_bytes(1000, 64, 32, B.GCN_TRANSFORM_FIRST, 0) == 0
+    assert L.gcn_csr_transpose_workspace_bytes(1000, 1000, 5000) >= 4 * 5000 * 4
+
+
+def test_pick_order_minimises_aggregation_width(L):
+    # first layer (no input gradient): aggregate at f_in when f_in <= 2h
+    assert L.gcn_layer_pick_order(512, 512, 0) == B.GCN_AGGREGATE_FIRST
+    assert L.gcn_layer_pick_order(602, 128, 0) == B.GCN_TRANSFORM_FIRST
+    # with the input gradient: aggregate-first only when f_in < h
+    assert L.gcn_layer_pick_order(1024, 512, 1) == B.GCN_TRANSFORM_FIRST
+    assert L.gcn_layer_pick_order(50, 64, 1) == B.GCN_AGGREGATE_FIRST
+
+
+def test_profile_classes(L):
+    n = L.gcn_profile_class_count()
+    names = [L.gcn_profile_class_name(i).decode() for i in range(n)]
+    assert "spmm" in names and "gemm_nn" in names and "gemm_tn" in names
+    assert L.gcn_profile_read(n, None, None, None, None) == B.GCN_EINVAL

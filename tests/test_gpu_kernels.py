@@ -1,0 +1,156 @@
+"""Kernel-level parity on the GPU, through the C ABI, against the CPU oracle.
+
+Sizes span several tiles / wavefront work units and leave ragged tails.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import bf16 as obf16
+from paper_1810_11899_amd import binding as B
+from paper_1810_11899_amd import synth
+
+from gpu_util import TOL_F32, dev, rel_inf, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.fixture(scope="module")
+def ws():
+    return B.Workspace("cuda")
+
+
+def dcsr(g, n_cols=None):
+    return B.DeviceCSR.from_host(g.n, g.n if n_cols is None else n_cols, g.indptr, g.indices, g.vals)
+
+
+# ------------------------------------------------------------- transpose ----
+@pytest.mark.parametrize("case", ["cfg1", "rmat3000", "star", "empty", "dup", "rect"])
+def test_transpose_bit_exact(case, ws):
+    n_cols = None
+    if case == "cfg1":
+        g = synth.config(1).graph
+    elif case == "rmat3000":
+        g = synth.custom(3001, "rmat", 13, [(2, 2)], seed=5).graph
+    elif case == "star":
+        g = synth.star_graph(70000)
+    elif case == "empty":
+        g = synth.empty_graph(333)
+    elif case == "dup":   # duplicated entries must keep their CSR order
+        rows = np.array([0, 0, 0, 1, 2, 2, 3, 3, 3, 3])
+        cols = np.array([2, 2, 1, 2, 0, 2, 3, 3, 2, 0])
+        g = synth.csr_from_pairs(4, rows, cols, np.arange(10, dtype=np.float32))
+    else:                 # rectangular: 500 rows, 1300 columns
+        rng = np.random.default_rng(0)
+        rows = rng.integers(0, 500, 4000)
+        cols = rng.integers(0, 1300, 4000)
+        key = np.unique(rows * 1300 + cols)
+        g = synth.csr_from_pairs(500, key // 1300, key % 1300)
+        n_cols = 1300
+    nc = g.n if n_cols is None else n_cols
+    A = dcsr(g, nc)
+    AT = B.gcn_csr_transpose(A, ws)
+    ti, tj, tv = oracle.csr_transpose(g.n, nc, g.indptr, g.indices, g.vals)
+    torch.cuda.synchronize()
+    assert np.array_equal(AT.indptr.cpu().numpy(), ti)
+    assert np.array_equal(AT.indices.cpu().numpy(), tj)
+    assert np.array_equal(AT.vals.cpu().numpy().view(np.uint32), np.asarray(tv, np.float32).view(np.uint32))
+
+
+# ------------------------------------------------------------- aggregate ----
+@pytest.mark.parametrize("k", [1, 50, 64, 100, 128, 130, 256, 300, 512, 602, 1024])
+def test_aggregate_parity_widths(k, ws):
+    wl = synth.custom(3001, "rmat", 13, [(2, 2)], seed=k)
+    g = wl.graph
+    X = np.random.default_rng(k).standard_normal((g.n, k)).astype(np.float32)
+    out = torch.empty((g.n, k), dtype=torch.float32, device="cuda")
+    B.gcn_aggregate(dcsr(g), dev(X), out, ws)
+    ref = oracle.aggregate(g.indptr, g.indices, g.vals, X)
+    assert rel_inf(out.cpu().numpy(), ref) <= TOL_F32 / 10
+
+
+def test_aggregate_leading_dimensions(ws):
+    g = synth.custom(2000, "rmat", 9, [(2, 2)], seed=3).graph
+    Xbig = np.random.default_rng(1).standard_normal((g.n, 200)).astype(np.float32)
+    X = dev(Xbig)[:, 10:138]                    # k = 128 inside a 200-wide buffer
+    outbuf = torch.full((g.n, 300), 7.0, device="cuda")
+    out = outbuf[:, 50:178]
+    B.gcn_aggregate(dcsr(g), X, out, ws)
+    ref = oracle.aggregate(g.indptr, g.indices, g.vals, Xbig[:, 10:138])
+    o = outbuf.cpu().numpy()
+    assert rel_inf(o[:, 50:178], ref) <= TOL_F32 / 10
+    assert np.all(o[:, :50] == 7.0) and np.all(o[:, 178:] == 7.0)  # nothing outside the view
+
+
+def test_aggregate_permutation_is_bit_exact(ws):
+    rng = np.random.default_rng(2)
+    g = synth.permutation_graph(5001, rng)
+    X = rng.standard_normal((g.n, 512)).astype(np.float32)
+    out = torch.empty((g.n, 512), dtype=torch.float32, device="cuda")
+    B.gcn_aggregate(dcsr(g), dev(X), out, ws)
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), X[g.indices].view(np.uint32))
+
+
+def test_aggregate_constant_features_mean(ws):
+    g = synth.custom(4000, "rmat", 20, [(2, 2)], seed=9).graph
+    c = np.array([1.5, -3.25, 1000.0, 0.1], np.float32)
+    X = np.tile(np.tile(c, 64), (g.n, 1))   # k = 256
+    out = torch.empty((g.n, 256), dtype=torch.float32, device="cuda")
+    B.gcn_aggregate(dcsr(g), dev(X), out, ws)
+    o = out.cpu().numpy()
+    deg = g.degrees()
+    assert np.all(o[deg == 0] == 0.0)
+    nz = deg > 0
+    err = np.abs(o[nz] - X[nz]) / np.abs(X[nz])
+    assert np.all(err <= (2.0 * deg[nz, None] + 4) * 2.0 ** -23)
+
+
+@pytest.mark.parametrize("n", [70000, 5])
+def test_aggregate_long_row_split_over_wavefronts(n, ws):
+    g = synth.star_graph(n)
+    X = np.random.default_rng(4).standard_normal((g.n, 96)).astype(np.float32)
+    out = torch.empty((g.n, 96), dtype=torch.float32, device="cuda")
+    B.gcn_aggregate(dcsr(g), dev(X), out, ws)
+    ref = oracle.aggregate(g.indptr, g.indices, g.vals, X)
+    assert rel_inf(out.cpu().numpy(), ref) <= TOL_F32 / 10
+
+
+def test_aggregate_empty_graph_and_zero_rows(ws):
+    g = synth.empty_graph(1000)
+    out = torch.full((1000, 64), 3.0, device="cuda")
+    B.gcn_aggregate(dcsr(g), torch.ones((1000, 64), device="cuda"), out, ws)
+    assert torch.count_nonzero(out).item() == 0
+    g0 = synth.empty_graph(0)
+    A0 = B.DeviceCSR(0, 0, torch.zeros(1, dtype=torch.int32, device="cuda"),
+                     torch.zeros(0, dtype=torch.int32, device="cuda"),
+                     torch.zeros(0, dtype=torch.float32, device="cuda"))
+    B.gcn_aggregate(A0, torch.ones((0, 8), device="cuda"), torch.ones((0, 8), device="cuda"), ws)
+
+
+def test_aggregate_is_deterministic(ws):
+    g = synth.custom(20000, "rmat", 30, [(2, 2)], seed=1).graph
+    X = dev(np.random.default_rng(0).standard_normal((g.n, 256)).astype(np.float32))
+    A = dcsr(g)
+    o1 = torch.empty((g.n, 256), device="cuda")
+    o2 = torch.empty((g.n, 256), device="cuda")
+    B.gcn_aggregate(A, X, o1, ws)
+    B.gcn_aggregate(A, X, o2, ws)
+    assert torch.equal(o1.view(torch.int32), o2.view(torch.int32))
+
+
+# ------------------------------------------------------------------ bf16 ----
+def test_bf16_conversion_bit_exact():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(100003).astype(np.float32) * 1e3,
+                        np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 3.4e38, 1e-40, -1e-45,
+                                  1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8], np.float32)])
+    y = B.gcn_f32_to_bf16(dev(x)).cpu().numpy().view(np.uint16)
+    assert np.array_equal(y, obf16.f32_to_bf16_bits(x))

@@ -1,0 +1,163 @@
+"""Layer, loss and whole-step parity on the GPU, through the C ABI, against the
+CPU oracle on the same seeded inputs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1810_11899_amd import binding as B
+from paper_1810_11899_amd import synth
+from paper_1810_11899_amd.runner import StepRunner
+
+from gpu_util import TOL_F32, dev, rel_inf, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.fixture(scope="module")
+def ws():
+    return B.Workspace("cuda")
+
+
+def dcsr(g):
+    return B.DeviceCSR.from_host(g.n, g.n, g.indptr, g.indices, g.vals)
+
+
+def _bias(h, seed):
+    return (np.random.default_rng(seed).standard_normal(2 * h) * 0.3).astype(np.float32)
+
+
+SHAPES = [(777, "rmat", 9, 37, 24), (1500, "er", 12, 64, 48), (2049, "rmat", 15, 130, 100),
+          (1000, "rmat", 11, 256, 128)]
+
+
+@pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_layer_forward(order, shape, ws):
+    n, kind, d, f_in, h = shape
+    wl = synth.custom(n, kind, d, [(f_in, h)], seed=f_in)
+    lay = wl.layers[0]
+    b = _bias(h, n)
+    A = dcsr(wl.graph)
+    Y = torch.empty((n, 2 * h), device="cuda")
+    nb = B.gcn_layer_saved_bytes(n, f_in, h, order)
+    saved = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda") if nb else None
+    B.gcn_layer_fwd(A, dev(wl.H), dev(lay.W_self), dev(lay.W_neigh), dev(b), Y, saved, order, ws)
+    Yref, _ = oracle.layer_fwd(wl.graph, wl.H, lay.W_self, lay.W_neigh, b)
+    assert rel_inf(Y.cpu().numpy(), Yref) <= TOL_F32
+
+
+@pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
+@pytest.mark.parametrize("want_dH", [True, False])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_layer_backward(order, want_dH, shape, ws):
+    n, kind, d, f_in, h = shape
+    wl = synth.custom(n, kind, d, [(f_in, h)], seed=f_in + 1)
+    lay = wl.layers[0]
+    b = _bias(h, n + 1)
+    g = wl.graph
+    A = dcsr(g)
+    AT = B.gcn_csr_transpose(A, ws)
+    H = dev(wl.H)
+    Ws, Wn = dev(lay.W_self), dev(lay.W_neigh)
+    Y = torch.empty((n, 2 * h), device="cuda")
+    nb = B.gcn_layer_saved_bytes(n, f_in, h, order)
+    saved = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda") if nb else None
+    B.gcn_layer_fwd(A, H, Ws, Wn, dev(b), Y, saved, order, ws)
+    dY = np.random.default_rng(n).standard_normal((n, 2 * h)).astype(np.float32)
+    dH = torch.empty((n, f_in), device="cuda") if want_dH else None
+    dWs = torch.empty((f_in, h), device="cuda")
+    dWn = torch.empty((f_in, h), device="cuda")
+    db = torch.empty(2 * h, device="cuda")
+    B.gcn_layer_bwd(A, AT, H, Ws, Wn, Y, saved, dev(dY), dH, dWs, dWn, db, order, ws)
+    _, cache = oracle.layer_fwd(g, wl.H, lay.W_self, lay.W_neigh, b)
+    ti, tj, tv = oracle.csr_transpose(g.n, g.n, g.indptr, g.indices, g.vals)
+    gT = synth.Graph(g.n, ti, tj, tv)
+    rWs, rWn, rdb, rdH = oracle.layer_bwd(gT, cache, lay.W_self, lay.W_neigh, dY, want_dH)
+    assert rel_inf(dWs.cpu().numpy(), rWs) <= TOL_F32
+    assert rel_inf(dWn.cpu().numpy(), rWn) <= TOL_F32
+    assert rel_inf(db.cpu().numpy(), rdb) <= TOL_F32
+    if want_dH:
+        assert rel_inf(dH.cpu().numpy(), rdH) <= TOL_F32
+
+
+@pytest.mark.parametrize("kind", ["ce", "bce"])
+@pytest.mark.parametrize("n, f, C", [(3000, 256, 41), (1001, 130, 100), (257, 64, 7)])
+def test_loss_grad(kind, n, f, C, ws):
+    rng = np.random.default_rng(n + C)
+    HL = np.maximum(rng.standard_normal((n, f)), 0).astype(np.float32)
+    Wp = (rng.standard_normal((f, C)) * 0.2).astype(np.float32)
+    bp = (rng.standard_normal(C) * 0.1).astype(np.float32)
+    labels = rng.integers(0, C, n).astype(np.int32)
+    targets = (rng.random((n, C)) < 0.1).astype(np.float32)
+    loss = torch.empty(1, device="cuda")
+    dHL = torch.empty((n, f), device="cuda")
+    dWp = torch.empty((f, C), device="cuda")
+    dbp = torch.empty(C, device="cuda")
+    B.gcn_loss_grad(dev(HL), dev(Wp), dev(bp), B.LOSS_KIND[kind], dev(labels, torch.int32),
+                    dev(targets) if kind == "bce" else None, loss, dHL, dWp, dbp, ws)
+    rl, rdWp, rdbp, rdHL, _ = oracle.loss_grad(kind, HL, Wp, bp, labels=labels, targets=targets)
+    assert abs(loss.item() - rl) / abs(rl) <= TOL_F32
+    assert rel_inf(dWp.cpu().numpy(), rdWp) <= TOL_F32
+    assert rel_inf(dbp.cpu().numpy(), rdbp) <= TOL_F32
+    assert rel_inf(dHL.cpu().numpy(), rdHL) <= TOL_F32
+
+
+# ------------------------------------------------------------ whole steps ----
+def compare_step(run: dict, ref: oracle.StepResult, tol=TOL_F32):
+    errs = {}
+    assert np.array_equal(run["t_indptr"], ref.t_indptr)
+    assert np.array_equal(run["t_indices"], ref.t_indices)
+    for li in range(len(ref.Y)):
+        errs[f"Y{li}"] = rel_inf(run["Y"][li], ref.Y[li])
+        errs[f"dW_self{li}"] = rel_inf(run["dW_self"][li], ref.dW_self[li])
+        errs[f"dW_neigh{li}"] = rel_inf(run["dW_neigh"][li], ref.dW_neigh[li])
+        errs[f"db{li}"] = rel_inf(run["db"][li], ref.db[li])
+        if ref.dH[li] is not None:
+            errs[f"dH{li}"] = rel_inf(run["dH"][li], ref.dH[li])
+    if ref.loss is not None:
+        errs["loss"] = abs(run["loss"] - ref.loss) / abs(ref.loss)
+        errs["dW_pred"] = rel_inf(run["dW_pred"], ref.dW_pred)
+        errs["db_pred"] = rel_inf(run["db_pred"], ref.db_pred)
+        errs["dHL"] = rel_inf(run["dHL"], ref.dHL)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, f"over tolerance {tol}: {bad}"
+    return errs
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_config_step_parity(cfg):
+    wl = synth.config(cfg)
+    r = StepRunner(wl)
+    r.step()
+    torch.cuda.synchronize()
+    compare_step(r.results(), oracle.step(wl))
+
+
+def test_step_is_deterministic():
+    wl = synth.config(1)
+    r = StepRunner(wl)
+    r.step()
+    a = r.results()
+    r.step()
+    b = r.results()
+    for key in ("Y", "dW_self", "dW_neigh", "db"):
+        for x, y in zip(a[key], b[key]):
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), key
+    assert a["loss"] == b["loss"]
+
+
+@pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
+def test_forced_orders_agree_with_oracle(order):
+    wl = synth.custom(3000, "rmat", 12, [(96, 64), (128, 64)], head="bce", classes=30, seed=2)
+    r = StepRunner(wl, orders=[order, order], first_layer_dH=True)
+    r.step()
+    torch.cuda.synchronize()
+    compare_step(r.results(), oracle.step(wl, first_layer_dH=True))
