@@ -23,6 +23,16 @@ Readings of points the paper leaves open (all also listed in the design doc):
   * PREDICT is linear, ``X = H_L W_pred + b_pred``;
   * LOSS is the mean softmax cross-entropy over all n nodes, or the mean sigmoid
     binary cross-entropy over all n*C entries.
+
+ReLU kinks.  The derivative of max(z, 0) switches at z = 0, so an output
+computed in float32 may take the other branch wherever z lies within float32
+rounding of zero; both branches are then correct results of a float32
+computation.  With ``envelope=True`` the oracle marks every pre-activation with
+|z| < C_AMB * u32 * (the sum of the magnitudes of its terms) as ambiguous and
+propagates, with absolute values through the backward pass, a per-entry bound
+on how far any choice of those branches can move each gradient.  Comparisons
+allow that bound on top of the float32 tolerance; everywhere else they are
+strict.
 """
 from __future__ import annotations
 
@@ -66,6 +76,10 @@ def _load():
 
 def num_threads() -> int:
     return int(_load().gcnref_num_threads())
+
+
+U32 = 2.0 ** -24      # unit roundoff of float32
+C_AMB = 16.0          # safety factor on u32 * sum|terms| (covers upstream float32 error too)
 
 
 def f64(a) -> np.ndarray:
@@ -117,31 +131,46 @@ class LayerCache:
     H: np.ndarray     # layer input, float64
     AGG: np.ndarray   # A H
     Z: np.ndarray     # pre-activation [S || N] + b
+    amb: Optional[np.ndarray] = None     # |Z| within float32 rounding of 0
+    absAGG: Optional[np.ndarray] = None  # |A| |H|
 
 
-def layer_fwd(g, H, W_self, W_neigh, bias):
+def layer_fwd(g, H, W_self, W_neigh, bias, ambiguity: bool = False):
     """Forward of one layer (Sec. II; Alg. 1 forward loop), float64.
 
     S = H W_self, N = (A H) W_neigh, Z = [S || N] + b, Y = max(Z, 0).
+    With ``ambiguity`` the cache also marks the ReLU kinks that float32 cannot
+    resolve: |Z| < C_AMB u32 (|b| + |H| |W_self|) on the self half and
+    |Z| < C_AMB u32 (|b| + |A| |H| |W_neigh|) on the neighbour half.
     """
     H = f64(H)
     AGG = aggregate(g.indptr, g.indices, g.vals, H)
     S = H @ f64(W_self)
     N = AGG @ f64(W_neigh)
-    Z = np.concatenate([S, N], axis=1) + f64(bias)[None, :]
+    b = f64(bias)
+    Z = np.concatenate([S, N], axis=1) + b[None, :]
     Y = np.maximum(Z, 0.0)
-    return Y, LayerCache(H, AGG, Z)
+    cache = LayerCache(H, AGG, Z)
+    if ambiguity:
+        absAGG = aggregate(g.indptr, g.indices, np.abs(f64(g.vals)), np.abs(H))
+        mag = np.concatenate([np.abs(H) @ np.abs(f64(W_self)), absAGG @ np.abs(f64(W_neigh))], axis=1)
+        mag += np.abs(b)[None, :]
+        cache.amb = np.abs(Z) < C_AMB * U32 * mag
+        cache.absAGG = absAGG
+    return Y, cache
 
 
-def layer_bwd(gT, cache: LayerCache, W_self, W_neigh, dY, need_dH: bool):
+def layer_bwd(gT, cache: LayerCache, W_self, W_neigh, dY, need_dH: bool, mask=None):
     """Backward of one layer: the same two kernels, transposed (Sec. III-B).
 
     dZ = dY * [Z > 0]; db = sum_i dZ; dW_self = H^T dZ_s; dW_neigh = (A H)^T dZ_n;
     dH = dZ_s W_self^T + A^T (dZ_n W_neigh^T).  ``gT`` is the CSR of A^T.
+    ``mask`` overrides [Z > 0] (used to enumerate kink choices).
     """
     Ws, Wn = f64(W_self), f64(W_neigh)
     h = Ws.shape[1]
-    dZ = f64(dY) * (cache.Z > 0.0)
+    m = (cache.Z > 0.0) if mask is None else mask
+    dZ = f64(dY) * m
     db = dZ.sum(axis=0)
     dZs, dZn = dZ[:, :h], dZ[:, h:]
     dWs = cache.H.T @ dZs
@@ -150,6 +179,27 @@ def layer_bwd(gT, cache: LayerCache, W_self, W_neigh, dY, need_dH: bool):
     if need_dH:
         dH = dZs @ Ws.T + aggregate(gT.indptr, gT.indices, gT.vals, dZn @ Wn.T)
     return dWs, dWn, db, dH
+
+
+def layer_bwd_envelope(gT, cache: LayerCache, W_self, W_neigh, dY, E_dY, need_dH: bool):
+    """Bound on how far the layer's gradients can move over the ReLU kinks.
+
+    An ambiguous entry of dZ may be 0 or dY (plus the upstream bound E_dY);
+    any other entry is dY * [Z > 0] up to E_dY.  The bound is carried through
+    the same products with absolute values: |H|^T, (|A||H|)^T, |W|^T, |A^T|.
+    """
+    Ws, Wn = np.abs(f64(W_self)), np.abs(f64(W_neigh))
+    h = Ws.shape[1]
+    E_dY = np.zeros_like(cache.Z) if E_dY is None else E_dY
+    E = np.where(cache.amb, np.abs(f64(dY)) + E_dY, (cache.Z > 0.0) * E_dY)
+    Es, En = E[:, :h], E[:, h:]
+    E_db = E.sum(axis=0)
+    E_dWs = np.abs(cache.H).T @ Es
+    E_dWn = cache.absAGG.T @ En
+    E_dH = None
+    if need_dH:
+        E_dH = Es @ Ws.T + aggregate(gT.indptr, gT.indices, np.abs(f64(gT.vals)), En @ Wn.T)
+    return E_dWs, E_dWn, E_db, E_dH
 
 
 # --------------------------------------------------------------------------
@@ -199,6 +249,12 @@ class StepResult:
     t_indptr: Optional[np.ndarray] = None
     t_indices: Optional[np.ndarray] = None
     t_vals: Optional[np.ndarray] = None
+    # per-entry kink envelopes of the gradients (envelope=True), same shapes
+    E_dW_self: Optional[List[np.ndarray]] = None
+    E_dW_neigh: Optional[List[np.ndarray]] = None
+    E_db: Optional[List[np.ndarray]] = None
+    E_dH: Optional[List[Optional[np.ndarray]]] = None
+    ambiguous: Optional[List[int]] = None
 
 
 class _CSR:
@@ -206,11 +262,12 @@ class _CSR:
         self.indptr, self.indices, self.vals = indptr, indices, vals
 
 
-def step(wl, first_layer_dH: Optional[bool] = None) -> StepResult:
+def step(wl, first_layer_dH: Optional[bool] = None, envelope: bool = False) -> StepResult:
     """Forward through every layer, PREDICT/LOSS (or the given dY), backward.
 
     The layer-1 input gradient is computed only for single-layer workloads
     unless ``first_layer_dH`` says otherwise (training never needs it).
+    ``envelope`` adds the ReLU-kink bounds of every gradient.
     """
     g = wl.graph
     L = len(wl.layers)
@@ -221,7 +278,7 @@ def step(wl, first_layer_dH: Optional[bool] = None) -> StepResult:
     H = wl.H
     caches, Ys = [], []
     for lay in wl.layers:
-        Y, cache = layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias)
+        Y, cache = layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=envelope)
         caches.append(cache)
         Ys.append(Y)
         H = Y
@@ -234,10 +291,18 @@ def step(wl, first_layer_dH: Optional[bool] = None) -> StepResult:
                                            labels=wl.labels, targets=wl.targets)
         res.loss, res.dW_pred, res.db_pred, res.dHL = loss, dWp, dbp, dHL
         dY = dHL
+    if envelope:
+        res.E_dW_self, res.E_dW_neigh, res.E_db, res.E_dH = [None] * L, [None] * L, [None] * L, [None] * L
+        res.ambiguous = [int(c.amb.sum()) for c in caches]
+    E_dY = None
     for li in range(L - 1, -1, -1):
         lay = wl.layers[li]
         need = li > 0 or first_layer_dH
         dWs, dWn, db, dH = layer_bwd(gT, caches[li], lay.W_self, lay.W_neigh, dY, need)
         res.dW_self[li], res.dW_neigh[li], res.db[li], res.dH[li] = dWs, dWn, db, dH
+        if envelope:
+            e = layer_bwd_envelope(gT, caches[li], lay.W_self, lay.W_neigh, dY, E_dY, need)
+            res.E_dW_self[li], res.E_dW_neigh[li], res.E_db[li], res.E_dH[li] = e
+            E_dY = e[3]
         dY = dH
     return res

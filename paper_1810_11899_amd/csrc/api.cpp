@@ -450,7 +450,7 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
 // ------------------------------------------------------------------ loss
 namespace {
 struct LossPlan {
-    size_t X, rows, gemm, colsum, total;
+    size_t X, rows, gemm, colsum, red, total;
     int split;
 };
 LossPlan plan_loss(int32_t n, int32_t f, int32_t C) {
@@ -461,7 +461,8 @@ LossPlan plan_loss(int32_t n, int32_t f, int32_t C) {
     p.split = gemm_pick_split(1, &g);
     p.gemm = gemm_workspace_bytes(1, &g, p.split);
     p.colsum = colsum_workspace_bytes(n, C);
-    p.total = p.X + p.rows + p.gemm + p.colsum + 1024;
+    p.red = loss_reduce_workspace_bytes(n);
+    p.total = p.X + p.rows + p.gemm + p.colsum + p.red + 1280;
     return p;
 }
 }  // namespace
@@ -494,6 +495,7 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
     float *rows = ar.take<float>((size_t)n + 1);
     void *gw = pl.gemm ? ar.take<char>(pl.gemm) : nullptr;
     void *cw = ar.take<char>(pl.colsum);
+    void *lw = ar.take<char>(pl.red);
     int rc;
     if (n == 0) {
         rc = fill_zero(dW_pred, (int64_t)f * C, s);
@@ -514,7 +516,7 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
     rc = loss_rows(kind, n, C, X, labels, targets, rows, s);
     if (rc) return rc;
     const double scale = kind == GCN_SOFTMAX_CE ? 1.0 / (double)n : 1.0 / ((double)n * (double)C);
-    rc = loss_reduce(n, rows, scale, loss, s);
+    rc = loss_reduce(n, rows, scale, loss, lw, pl.red, s);
     if (rc) return rc;
     // a5: dW_pred = HL^T G, db_pred = sum_i G, dHL = G W_pred^T
     GemmProblem w = dw_problem(f, C, n);

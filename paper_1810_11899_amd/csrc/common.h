@@ -134,7 +134,9 @@ int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *
 // Row-wise loss on logits X (n x C, ldx == C), in place: X <- G.  rowloss[n].
 int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
               float *rowloss, hipStream_t s);
-int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, hipStream_t s);
+size_t loss_reduce_workspace_bytes(int32_t n);
+int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void *ws, size_t ws_bytes,
+                hipStream_t s);
 // x[0..count) = 0 with a kernel (no memset nodes, so callers may capture it)
 int fill_zero(float *x, int64_t count, hipStream_t s);
 // float32 -> bfloat16 bits (RNE), 2-D with leading dimensions

@@ -88,15 +88,19 @@ __global__ __launch_bounds__(256) void colsum_part_kernel(int32_t n, int32_t C, 
     part[(int64_t)chunk * C + c] = s;
 }
 
-// out[c] = sum over chunks of part[chunk][c], in chunk order.
+// out[c] = sum over chunks of part[chunk][c]: one wavefront per column; lane
+// l adds chunks l, l+64, ... in order, then a fixed xor-shuffle tree.
 __global__ __launch_bounds__(256) void colsum_reduce_kernel(int32_t chunks, int32_t C,
                                                             const float *__restrict__ part,
                                                             float *__restrict__ out) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (c >= C) return;
     float s = 0.0f;
-    for (int k = 0; k < chunks; ++k) s += part[(int64_t)k * C + c];
-    out[c] = s;
+    for (int k = lane; k < chunks; k += 64) s += part[(int64_t)k * C + c];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if (lane == 0) out[c] = s;
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -155,12 +159,31 @@ __global__ __launch_bounds__(256) void loss_rows_kernel(int kind, int32_t n, int
     }
 }
 
-// loss = scale * sum_i rowloss[i]: one block, fixed strided partition, fixed tree.
-__global__ __launch_bounds__(256) void loss_reduce_kernel(int32_t n, const float *__restrict__ rowloss,
+// loss = scale * sum_i rowloss[i] in two fixed-order stages: blocks of
+// kLossSeg rows reduce to one double each, then one block adds those.
+constexpr int kLossSeg = 2048;
+
+__global__ __launch_bounds__(256) void loss_partial_kernel(int32_t n, const float *__restrict__ rowloss,
+                                                           double *__restrict__ part) {
+    __shared__ double sh[256];
+    const int64_t base = (int64_t)blockIdx.x * kLossSeg;
+    double s = 0.0;
+    for (int i = threadIdx.x; i < kLossSeg; i += 256)
+        if (base + i < n) s += (double)rowloss[base + i];
+    sh[threadIdx.x] = s;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) part[blockIdx.x] = sh[0];
+}
+
+__global__ __launch_bounds__(256) void loss_reduce_kernel(int32_t nparts, const double *__restrict__ part,
                                                           double scale, float *__restrict__ loss) {
     __shared__ double sh[256];
     double s = 0.0;
-    for (int i = threadIdx.x; i < n; i += 256) s += (double)rowloss[i];
+    for (int i = threadIdx.x; i < nparts; i += 256) s += part[i];
     sh[threadIdx.x] = s;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) {
@@ -232,7 +255,7 @@ int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y
     }
     {
         ProfScope ps(K_COLSUM_REDUCE, s, 0.0, (double)chunks * w * 4.0);
-        hipLaunchKernelGGL(colsum_reduce_kernel, dim3((unsigned)((w + 255) / 256)), dim3(256), 0, s, chunks, w,
+        hipLaunchKernelGGL(colsum_reduce_kernel, dim3((unsigned)((w + 3) / 4)), dim3(256), 0, s, chunks, w,
                            part, dbias);
         GCN_LAUNCH_CHECK("colsum_reduce_kernel");
     }
@@ -262,7 +285,7 @@ int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *
     }
     {
         ProfScope ps(K_COLSUM_REDUCE, s, 0.0, (double)chunks * C * 4.0);
-        hipLaunchKernelGGL(colsum_reduce_kernel, dim3((unsigned)((C + 255) / 256)), dim3(256), 0, s, chunks, C,
+        hipLaunchKernelGGL(colsum_reduce_kernel, dim3((unsigned)((C + 3) / 4)), dim3(256), 0, s, chunks, C,
                            part, out);
         GCN_LAUNCH_CHECK("colsum_reduce_kernel");
     }
@@ -279,9 +302,23 @@ int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, c
     return GCN_OK;
 }
 
-int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, hipStream_t s) {
+size_t loss_reduce_workspace_bytes(int32_t n) {
+    return align256((size_t)((n + kLossSeg - 1) / kLossSeg + 1) * sizeof(double)) + 256;
+}
+
+int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void *ws, size_t ws_bytes,
+                hipStream_t s) {
+    const int32_t nparts = (n + kLossSeg - 1) / kLossSeg;
+    Arena ar(ws, ws_bytes);
+    double *part = ar.take<double>((size_t)nparts + 1);
+    if (!part) {
+        set_error("loss_reduce: workspace too small");
+        return GCN_EWORKSPACE;
+    }
     ProfScope ps(K_LOSS_REDUCE, s, 0.0, (double)n * 4.0);
-    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, n, rowloss, scale, loss);
+    if (nparts > 0)
+        hipLaunchKernelGGL(loss_partial_kernel, dim3((unsigned)nparts), dim3(256), 0, s, n, rowloss, part);
+    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, nparts, part, scale, loss);
     GCN_LAUNCH_CHECK("loss_reduce_kernel");
     return GCN_OK;
 }

@@ -232,20 +232,48 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, float *__restrict__
     if (r < 0) return;
     int64_t ws = w;
     while (ws > 0 && tail_row[ws - 1] == r) --ws;
-    for (int c = blockIdx.y * 256 + lane; c < k && c < (int)(blockIdx.y + 1) * 256; c += 64) {
-        float acc = 0.0f;
-        bool first = true;
-        for (int64_t q = ws; q < w; ++q) {
-            const float v = carry[(2 * q + 1) * (int64_t)k + c];
-            acc = first ? v : acc + v;
-            first = false;
+    // four columns per lane; the pieces are added in wavefront order, eight
+    // loads in flight per column
+    const int c0 = blockIdx.y * 256 + lane;
+    float acc[4];
+    bool any = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = 0.0f;
+    int64_t q = ws;
+    for (; q + 8 <= w; q += 8) {
+        float v[8][4];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int c = c0 + 64 * j;
+                v[u][j] = c < k ? carry[(2 * (q + u) + 1) * (int64_t)k + c] : 0.0f;
+            }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[j] = (any || u > 0) ? acc[j] + v[u][j] : v[u][j];
+        any = true;
+    }
+    for (; q < w; ++q) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int c = c0 + 64 * j;
+            const float v = c < k ? carry[(2 * q + 1) * (int64_t)k + c] : 0.0f;
+            acc[j] = any ? acc[j] + v : v;
         }
+        any = true;
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int c = c0 + 64 * j;
+        if (c >= k) continue;
         const float hv = carry[(2 * w) * (int64_t)k + c];
-        acc = first ? hv : acc + hv;
+        float a = any ? acc[j] + hv : hv;
         float *o = out + (int64_t)r * ldo + c;
-        if (epi == EPI_BIAS_RELU) acc = fmaxf(acc + bias[c], 0.0f);
-        else if (epi == EPI_ACCUMULATE) acc = *o + acc;
-        *o = acc;
+        if (epi == EPI_BIAS_RELU) a = fmaxf(a + bias[c], 0.0f);
+        else if (epi == EPI_ACCUMULATE) a = *o + a;
+        *o = a;
     }
 }
 

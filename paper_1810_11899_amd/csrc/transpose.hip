@@ -48,10 +48,33 @@ __global__ __launch_bounds__(kTB) void hist_kernel(int32_t nnz, const uint32_t *
     hist[(int64_t)threadIdx.x * ntiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
-// Exclusive scan of `len` ints by one block of 1024 threads (contiguous chunk
-// per thread, then a scan of the chunk totals).
-__global__ __launch_bounds__(1024) void scan_kernel(int64_t len, const int32_t *__restrict__ in,
-                                                    int32_t *__restrict__ out, int32_t *__restrict__ total) {
+// Exclusive scan of `len` ints in three phases: per-segment sums, a scan of
+// the segment sums (one block), and a per-segment scan plus its offset.
+// Integer sums, so the result does not depend on the schedule.
+constexpr int kScanPer = 16;                   // ints per thread
+constexpr int kScanSeg = kTB * kScanPer;       // ints per block segment
+
+__global__ __launch_bounds__(kTB) void scan_reduce_kernel(int64_t len, const int32_t *__restrict__ in,
+                                                          int32_t *__restrict__ seg_sums) {
+    __shared__ int32_t sh[kTB];
+    const int64_t base = (int64_t)blockIdx.x * kScanSeg;
+    int32_t s = 0;
+    for (int i = 0; i < kScanPer; ++i) {
+        const int64_t e = base + (int64_t)i * kTB + threadIdx.x;
+        if (e < len) s += in[e];
+    }
+    sh[threadIdx.x] = s;
+    __syncthreads();
+    for (int o = kTB / 2; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) seg_sums[blockIdx.x] = sh[0];
+}
+
+// exclusive scan of a short array by one block of 1024 threads
+__global__ __launch_bounds__(1024) void scan_small_kernel(int64_t len, const int32_t *__restrict__ in,
+                                                          int32_t *__restrict__ out) {
     __shared__ int32_t sh[1024];
     const int t = threadIdx.x;
     const int64_t per = (len + 1023) / 1024;
@@ -67,13 +90,41 @@ __global__ __launch_bounds__(1024) void scan_kernel(int64_t len, const int32_t *
         sh[t] += v;
         __syncthreads();
     }
-    int32_t run = sh[t] - s;  // exclusive prefix of this chunk
+    int32_t run = sh[t] - s;
     for (int64_t i = b; i < e; ++i) {
         const int32_t v = in[i];
         out[i] = run;
         run += v;
     }
-    if (t == 1023 && total) *total = sh[1023];
+}
+
+__global__ __launch_bounds__(kTB) void scan_down_kernel(int64_t len, const int32_t *__restrict__ in,
+                                                        const int32_t *__restrict__ seg_offs,
+                                                        int32_t *__restrict__ out) {
+    __shared__ int32_t sh[kTB];
+    const int t = threadIdx.x;
+    const int64_t base = (int64_t)blockIdx.x * kScanSeg + (int64_t)t * kScanPer;
+    int32_t v[kScanPer];
+    int32_t s = 0;
+#pragma unroll
+    for (int i = 0; i < kScanPer; ++i) {
+        v[i] = base + i < len ? in[base + i] : 0;
+        s += v[i];
+    }
+    sh[t] = s;
+    __syncthreads();
+    for (int o = 1; o < kTB; o <<= 1) {
+        const int32_t x = t >= o ? sh[t - o] : 0;
+        __syncthreads();
+        sh[t] += x;
+        __syncthreads();
+    }
+    int32_t run = seg_offs[blockIdx.x] + sh[t] - s;
+#pragma unroll
+    for (int i = 0; i < kScanPer; ++i) {
+        if (base + i < len) out[base + i] = run;
+        run += v[i];
+    }
 }
 
 __global__ __launch_bounds__(kTB) void scatter_kernel(int32_t nnz, const uint32_t *__restrict__ keys_in,
@@ -181,6 +232,8 @@ size_t transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz) {
     b += 2 * align256((size_t)nnz * 4);          // keys ping-pong
     b += 2 * align256((size_t)nnz * 4);          // values ping-pong
     b += 2 * align256((size_t)ntiles * kRadix * 4);  // hist, offsets
+    const int64_t segs = (ntiles * kRadix + kScanSeg - 1) / kScanSeg;
+    b += 2 * align256((size_t)(segs + 1) * 4);        // segment sums, segment offsets
     return b + 256;
 }
 
@@ -200,7 +253,11 @@ int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *in
     int32_t *va = ar.take<int32_t>(nnz), *vb = ar.take<int32_t>(nnz);
     int32_t *hist = ar.take<int32_t>((size_t)ntiles * kRadix);
     int32_t *offs = ar.take<int32_t>((size_t)ntiles * kRadix);
-    if (!ka || !kb || !va || !vb || !hist || !offs) {
+    const int64_t scan_len = (int64_t)ntiles * kRadix;
+    const int64_t segs = (scan_len + kScanSeg - 1) / kScanSeg;
+    int32_t *seg_sums = ar.take<int32_t>((size_t)segs + 1);
+    int32_t *seg_offs = ar.take<int32_t>((size_t)segs + 1);
+    if (!ka || !kb || !va || !vb || !hist || !offs || !seg_sums || !seg_offs) {
         set_error("csr_transpose: workspace too small (%zu < %zu bytes)", ws_bytes,
                   transpose_workspace_bytes(n_rows, n_cols, nnz));
         return GCN_EWORKSPACE;
@@ -220,10 +277,13 @@ int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *in
             GCN_LAUNCH_CHECK("hist_kernel");
         }
         {
-            ProfScope ps(K_T_SCAN, s, 0.0, (double)ntiles * kRadix * 8.0);
-            hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(1024), 0, s, (int64_t)ntiles * kRadix, hist, offs,
-                               (int32_t *)nullptr);
-            GCN_LAUNCH_CHECK("scan_kernel");
+            ProfScope ps(K_T_SCAN, s, 0.0, (double)scan_len * 8.0);
+            hipLaunchKernelGGL(scan_reduce_kernel, dim3((unsigned)segs), dim3(kTB), 0, s, scan_len, hist,
+                               seg_sums);
+            hipLaunchKernelGGL(scan_small_kernel, dim3(1), dim3(1024), 0, s, segs, seg_sums, seg_offs);
+            hipLaunchKernelGGL(scan_down_kernel, dim3((unsigned)segs), dim3(kTB), 0, s, scan_len, hist, seg_offs,
+                               offs);
+            GCN_LAUNCH_CHECK("scan kernels");
         }
         {
             ProfScope ps(K_T_FILL, s, 0.0, (double)nnz * 16.0);

@@ -16,9 +16,11 @@ the stored CSR is symmetric in pattern and row-normalised in value
 aggregation matrix is handed to the layer.
 
 Random streams: ``np.random.SeedSequence([181011899, cfg, s, ...])`` spawned
-into children in a fixed order (graph, relabel, H, weights, labels, degree);
-PCG64 output is platform independent, so the same seed gives bitwise equal
-arrays on every machine.
+into children in a fixed order (graph, relabel, H, unused, labels, degree) for
+everything that belongs to subgraph s; the model weights come from
+``SeedSequence([181011899, cfg, WEIGHT_KEY])`` so that every subgraph of an
+epoch stream trains the same model.  PCG64 output is platform independent, so
+the same seed gives bitwise equal arrays on every machine.
 """
 from __future__ import annotations
 
@@ -29,6 +31,7 @@ from typing import List, Optional, Tuple
 import numpy as np
 
 SEED_ROOT = 181011899
+WEIGHT_KEY = 0x5EED
 RMAT_ABC = (0.57, 0.19, 0.19)  # d = 0.05
 
 
@@ -232,8 +235,9 @@ def build(spec: Spec, s: int = 0, cfg_key: int = 99, n: Optional[int] = None) ->
     n_eff = spec.n if n is None else int(n)
     key = [SEED_ROOT, cfg_key, s] + ([n_eff] if n is not None else [])
     children = np.random.SeedSequence(key).spawn(6)
-    rg_graph, rg_relabel, rg_h, rg_w, rg_lab, rg_deg = (
+    rg_graph, rg_relabel, rg_h, _, rg_lab, rg_deg = (
         np.random.Generator(np.random.PCG64(c)) for c in children)
+    rg_w = np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED_ROOT, cfg_key, WEIGHT_KEY])))
     d = spec.d
     if spec.d_range is not None:
         d = int(rg_deg.integers(spec.d_range[0], spec.d_range[1] + 1))

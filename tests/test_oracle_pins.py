@@ -327,3 +327,60 @@ def test_bf16_rounding_against_torch_and_special_values():
     assert obf16.round_bf16(np.float32(1.0 + 3 * 2.0 ** -8))[()] == np.float32(1.0 + 2 ** -6)
     nan = obf16.round_bf16(np.array([np.nan], np.float32))
     assert np.isnan(nan[0])
+
+
+# ------------------------------------------------------------ kink envelope ----
+def test_kink_envelope_bounds_every_branch_choice(monkeypatch):
+    """Brute force: with an enlarged ambiguity band, every assignment of the
+    ambiguous ReLU branches moves each gradient by at most the envelope."""
+    import itertools
+    from oracle import gcnref
+    monkeypatch.setattr(gcnref, "C_AMB", 1.0e6)   # widen the band to a handful of entries
+    checked = 0
+    for seed in range(8):
+        wl = synth.custom(9, "er", 4, [(4, 3), (6, 2)], head="ce", classes=3, seed=seed)
+        for lay in wl.layers:
+            lay.bias = np.random.default_rng(seed).standard_normal(lay.bias.shape).astype(np.float32) * 0.05
+        res = oracle.step(wl, first_layer_dH=True, envelope=True)
+        g = wl.graph
+        gT = synth.Graph(g.n, res.t_indptr, res.t_indices, res.t_vals)
+        H = wl.H
+        caches = []
+        for lay in wl.layers:
+            H, c = oracle.layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=True)
+            caches.append(c)
+        amb = [np.argwhere(c.amb) for c in caches]
+        total = sum(a.shape[0] for a in amb)
+        if total == 0 or total > 10:
+            continue
+        attained = 0.0
+        for bits in itertools.product([0, 1], repeat=total):
+            masks = [(c.Z > 0).astype(np.float64) for c in caches]
+            k = 0
+            for li, a in enumerate(amb):
+                for (i, j) in a:
+                    masks[li][i, j] = bits[k]
+                    k += 1
+            dY = res.dHL
+            for li in range(1, -1, -1):
+                lay = wl.layers[li]
+                dWs, dWn, db, dH = oracle.layer_bwd(gT, caches[li], lay.W_self, lay.W_neigh, dY, True,
+                                                    mask=masks[li])
+                for got, ref, E in ((dWs, res.dW_self[li], res.E_dW_self[li]),
+                                    (dWn, res.dW_neigh[li], res.E_dW_neigh[li]),
+                                    (db, res.db[li], res.E_db[li]), (dH, res.dH[li], res.E_dH[li])):
+                    dev_ = np.abs(got - ref)
+                    assert np.all(dev_ <= E + 1e-12), (seed, li, (dev_ - E).max())
+                    attained = max(attained, float(dev_.max()))
+                dY = dH
+        assert attained > 0.0  # some branch choice really moves a gradient
+        checked += 1
+    assert checked >= 2, "too few seeds with a small ambiguous set"
+
+
+def test_kink_envelope_is_zero_without_ambiguity():
+    wl = synth.custom(40, "er", 5, [(6, 4)], head="bce", classes=3, seed=1)
+    res = oracle.step(wl, first_layer_dH=True, envelope=True)
+    if res.ambiguous == [0]:
+        for E in res.E_dW_self + res.E_dW_neigh + res.E_db + res.E_dH:
+            assert not np.any(E)

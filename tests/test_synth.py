@@ -92,3 +92,12 @@ def test_special_graphs():
     assert s.degrees()[0] == 99
     e = synth.empty_graph(5)
     assert e.nnz == 0 and e.indptr.shape == (6,)
+
+
+def test_epoch_stream_shares_model_weights():
+    a = synth.config(4, s=0)
+    b = synth.config(4, s=7)
+    for la, lb in zip(a.layers, b.layers):
+        assert np.array_equal(la.W_self, lb.W_self) and np.array_equal(la.W_neigh, lb.W_neigh)
+    assert np.array_equal(a.W_pred, b.W_pred)
+    assert not np.array_equal(a.H, b.H)
