@@ -115,7 +115,7 @@ int gcn_csr_transpose(const gcn_csr *A, int32_t *t_indptr, int32_t *t_indices, f
  * X is n_cols x k (ldx), out is n_rows x k (ldo); out must not overlap X.
  * An empty row gives 0.  In GCN_BF16 the gathered X values are rounded to
  * bfloat16 first (accumulation stays float32). */
-size_t gcn_aggregate_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k, gcn_prec prec);
+size_t gcn_aggregate_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz, int32_t k, gcn_prec prec);
 int gcn_aggregate(const gcn_csr *A, const float *X, int32_t k, int32_t ldx,
                   float *out, int32_t ldo, gcn_prec prec,
                   void *ws, size_t ws_bytes, void *stream);

@@ -47,7 +47,7 @@ _SIGNATURES = {
     "gcn_csr_validate_host": (ctypes.c_int, [_I32, _I32, _I32, _P, _P, ctypes.c_int]),
     "gcn_csr_transpose_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
     "gcn_csr_transpose": (ctypes.c_int, [_CSRP, _P, _P, _P, _P, _SZ, _P]),
-    "gcn_aggregate_workspace_bytes": (_SZ, [_I32, _I32, _I32, ctypes.c_int]),
+    "gcn_aggregate_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, ctypes.c_int]),
     "gcn_aggregate": (ctypes.c_int, [_CSRP, _P, _I32, _I32, _P, _I32, ctypes.c_int, _P, _SZ, _P]),
     "gcn_layer_pick_order": (ctypes.c_int, [_I32, _I32, ctypes.c_int]),
     "gcn_layer_saved_bytes": (_SZ, [_I32, _I32, _I32, ctypes.c_int, ctypes.c_int]),
@@ -189,7 +189,7 @@ def gcn_aggregate(A: DeviceCSR, X: torch.Tensor, out: torch.Tensor, ws: Workspac
     _dev_f32(out, "out")
     L = lib()
     k = int(X.shape[1])
-    need = L.gcn_aggregate_workspace_bytes(A.n_rows, A.nnz, k, prec)
+    need = L.gcn_aggregate_workspace_bytes(A.n_rows, A.n_cols, A.nnz, k, prec)
     w, wb = ws.args(need)
     s = A.struct()
     _check(L.gcn_aggregate(ctypes.byref(s), _ptr(X), k, _ld(X), _ptr(out), _ld(out), prec, w, wb,

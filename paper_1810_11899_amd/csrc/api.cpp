@@ -36,7 +36,8 @@ int hip_fail(hipError_t e, const char *what) {
 static const char *kClassNames[K_CLASS_COUNT] = {
     "spmm", "spmm_fixup", "gemm_nn", "gemm_tn", "gemm_nt", "splitk_reduce", "relu_bwd",
     "colsum", "loss_rows", "loss_reduce", "transpose_count", "transpose_scan", "transpose_scatter",
-    "transpose_sort", "transpose_final", "cvt_bf16"};
+    "transpose_sort", "transpose_final", "cvt_bf16", "gemm_nn_bf16", "gemm_tn_bf16", "gemm_nt_bf16",
+    "spmm_bf16"};
 
 const char *class_name(int cls) {
     return (cls >= 0 && cls < K_CLASS_COUNT) ? kClassNames[cls] : "";
@@ -140,9 +141,9 @@ int check_csr(const gcn_csr *A, const char *name) {
 // ----------------------------------------------------------- layer planning
 struct LayerPlan {
     bool need_G;        // backward forms G = A^T dZ_n
-    size_t fwd_T;       // TRANSFORM_FIRST: n x h
-    size_t fwd_spmm;
-    size_t bwd_P, bwd_D, bwd_T2, bwd_relu, bwd_spmm, bwd_gemm;
+    bool bf16;
+    size_t fwd_T, fwd_W16, fwd_spmm;
+    size_t bwd_P, bwd_D, bwd_T2, bwd_W16, bwd_relu, bwd_spmm, bwd_gemm;
     size_t fwd_total, bwd_total, total;
 };
 
@@ -160,38 +161,46 @@ GemmProblem dw_problem(int32_t f_in, int32_t h, int32_t n) {
     return g;
 }
 
-LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order, bool dH) {
+LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order, bool dH, int prec) {
     LayerPlan p{};
     p.need_G = bwd_uses_G(order, dH, f_in, h);
-    const size_t F = sizeof(float);
+    p.bf16 = prec == GCN_BF16;
+    const size_t E = p.bf16 ? 2 : 4;  // bytes per stored intermediate element
+    const size_t W16 = p.bf16 ? 2 * align256((size_t)f_in * h * 2) : 0;
     if (order == GCN_TRANSFORM_FIRST) {
-        p.fwd_T = align256((size_t)n * h * F);
+        p.fwd_T = align256((size_t)n * h * E);
         p.fwd_spmm = spmm_workspace_bytes(n, nnz, h);
     } else {
         p.fwd_spmm = spmm_workspace_bytes(n, nnz, f_in);
     }
-    p.fwd_total = p.fwd_T + p.fwd_spmm + 512;
+    p.fwd_W16 = W16;
+    p.fwd_total = p.fwd_T + p.fwd_W16 + p.fwd_spmm + 768;
 
-    p.bwd_P = align256((size_t)n * 2 * h * F);
+    p.bwd_P = align256((size_t)n * 2 * h * E);
     if (p.need_G) {
-        p.bwd_D = align256((size_t)n * h * F);
+        p.bwd_D = align256((size_t)n * h * E);
         p.bwd_spmm = spmm_workspace_bytes(n, nnz, h);
     }
     if (dH && !p.need_G) {
-        p.bwd_T2 = align256((size_t)n * f_in * F);
+        p.bwd_T2 = align256((size_t)n * f_in * E);
         p.bwd_spmm = std::max(p.bwd_spmm, spmm_workspace_bytes(n, nnz, f_in));
     }
+    p.bwd_W16 = dH ? W16 : 0;
     p.bwd_relu = relu_bwd_workspace_bytes(n, h);
     GemmProblem pr[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
     p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr));
-    p.bwd_total = p.bwd_P + p.bwd_D + p.bwd_T2 + p.bwd_relu + p.bwd_spmm + p.bwd_gemm + 2048;
+    p.bwd_total = p.bwd_P + p.bwd_D + p.bwd_T2 + p.bwd_W16 + p.bwd_relu + p.bwd_spmm + p.bwd_gemm + 2304;
     p.total = std::max(p.fwd_total, p.bwd_total);
     return p;
 }
 
+// float32: AGG (aggregate-first only).  bfloat16: H16, then AGG16 (aggregate-first).
 size_t saved_bytes(int32_t n, int32_t f_in, int32_t h, int order, int prec) {
     (void)h;
-    (void)prec;
+    if (prec == GCN_BF16) {
+        const size_t one = align256((size_t)n * f_in * 2);
+        return order == GCN_AGGREGATE_FIRST ? 2 * one : one;
+    }
     if (order == GCN_AGGREGATE_FIRST) return align256((size_t)n * f_in * sizeof(float));
     return 0;
 }
@@ -207,7 +216,6 @@ int check_layer_common(const gcn_csr *A, const float *H, int32_t f_in, int32_t l
     REQUIRE(order == GCN_AGGREGATE_FIRST || order == GCN_TRANSFORM_FIRST, GCN_EINVAL, "%s: bad order %d",
             who, order);
     REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "%s: bad precision %d", who, prec);
-    REQUIRE(prec == GCN_F32, GCN_EUNSUPPORTED, "%s: the bfloat16 path is not built yet", who);
     REQUIRE(A->n_rows == 0 || (H && W_self && W_neigh), GCN_EINVAL, "%s: null H or weights", who);
     return GCN_OK;
 }
@@ -262,9 +270,9 @@ int gcn_csr_transpose(const gcn_csr *A, int32_t *t_indptr, int32_t *t_indices, f
 }
 
 // ------------------------------------------------------------- aggregate
-size_t gcn_aggregate_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k, gcn_prec prec) {
-    (void)prec;
-    return spmm_workspace_bytes(n_rows, nnz, k);
+size_t gcn_aggregate_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz, int32_t k, gcn_prec prec) {
+    return spmm_workspace_bytes(n_rows, nnz, k) +
+           (prec == GCN_BF16 ? align256((size_t)n_cols * k * 2) + 256 : 0);
 }
 
 int gcn_aggregate(const gcn_csr *A, const float *X, int32_t k, int32_t ldx, float *out, int32_t ldo,
@@ -273,14 +281,25 @@ int gcn_aggregate(const gcn_csr *A, const float *X, int32_t k, int32_t ldx, floa
     if (rc) return rc;
     REQUIRE(k >= 0 && ldx >= k && ldo >= k, GCN_ESHAPE, "gcn_aggregate: k=%d ldx=%d ldo=%d", k, ldx, ldo);
     REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "gcn_aggregate: bad precision");
-    REQUIRE(prec == GCN_F32, GCN_EUNSUPPORTED, "gcn_aggregate: the bfloat16 path is not built yet");
     if (A->n_rows == 0 || k == 0) return GCN_OK;
     REQUIRE(out && (A->nnz == 0 || X), GCN_EINVAL, "gcn_aggregate: null X or out");
-    const size_t need = spmm_workspace_bytes(A->n_rows, A->nnz, k);
+    const size_t need = gcn_aggregate_workspace_bytes(A->n_rows, A->n_cols, A->nnz, k, prec);
     REQUIRE(ws && ws_bytes >= need, GCN_EWORKSPACE, "gcn_aggregate: workspace %zu < %zu bytes", ws_bytes,
             need);
+    hipStream_t s = as_stream(stream);
+    if (prec == GCN_BF16) {
+        // the source rows of X are the gathered operand: round them (all n_cols rows)
+        Arena ar(ws, ws_bytes);
+        uint16_t *X16 = ar.take<uint16_t>((size_t)A->n_cols * k);
+        const size_t sw = spmm_workspace_bytes(A->n_rows, A->nnz, k);
+        void *w = ar.take<char>(sw);
+        int rc = cvt_bf16(A->n_cols, k, X, ldx, X16, k, s);
+        if (rc) return rc;
+        return spmm_bf16(A->n_rows, A->nnz, A->indptr, A->indices, A->vals, X16, k, k, out, ldo, EPI_STORE,
+                         nullptr, w, sw, s);
+    }
     return spmm_f32(A->n_rows, A->nnz, A->indptr, A->indices, A->vals, X, k, ldx, out, ldo, EPI_STORE,
-                    nullptr, ws, ws_bytes, as_stream(stream));
+                    nullptr, ws, ws_bytes, s);
 }
 
 // ----------------------------------------------------------------- layer
@@ -298,8 +317,7 @@ size_t gcn_layer_saved_bytes(int32_t n, int32_t f_in, int32_t h, gcn_order order
 
 size_t gcn_layer_workspace_bytes(int32_t n, int32_t nnz, int32_t f_in, int32_t h, gcn_order order,
                                  gcn_prec prec) {
-    (void)prec;
-    return plan_layer(n, nnz, f_in, h, order, true).total;
+    return plan_layer(n, nnz, f_in, h, order, true, prec).total;
 }
 
 int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, const float *W_self,
@@ -315,42 +333,71 @@ int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, c
     const size_t sneed = saved_bytes(n, f_in, h, order, prec);
     REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
             "gcn_layer_fwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
-    const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, true);
+    const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, true, prec);
     REQUIRE(ws && ws_bytes >= pl.fwd_total, GCN_EWORKSPACE, "gcn_layer_fwd: workspace %zu < %zu bytes",
             ws_bytes, pl.fwd_total);
     hipStream_t s = as_stream(stream);
     Arena ar(ws, ws_bytes);
+    const bool bf = prec == GCN_BF16;
+    const bool af = order == GCN_AGGREGATE_FIRST;
 
+    // operands of the products: float32 as given, or their bfloat16 roundings
+    const void *Hop = H, *Wsop = W_self, *Wnop = W_neigh;
+    int64_t ldHop = ldh;
+    uint16_t *H16 = nullptr, *AGG16 = nullptr;
+    if (bf) {
+        H16 = (uint16_t *)saved;
+        AGG16 = af ? (uint16_t *)((char *)saved + align256((size_t)n * f_in * 2)) : nullptr;
+        uint16_t *Ws16 = ar.take<uint16_t>((size_t)f_in * h);
+        uint16_t *Wn16 = ar.take<uint16_t>((size_t)f_in * h);
+        if ((rc = cvt_bf16(n, f_in, H, ldh, H16, f_in, s))) return rc;
+        if ((rc = cvt_bf16(f_in, h, W_self, h, Ws16, h, s))) return rc;
+        if ((rc = cvt_bf16(f_in, h, W_neigh, h, Wn16, h, s))) return rc;
+        Hop = H16;
+        ldHop = f_in;
+        Wsop = Ws16;
+        Wnop = Wn16;
+    }
     GemmProblem g[2] = {};
     g[0].M = g[1].M = n;
     g[0].N = g[1].N = h;
-    g[0].seg[0] = GemmSeg{H, ldh, W_self, h, f_in};
+    g[0].seg[0] = GemmSeg{Hop, ldHop, Wsop, h, f_in};
     g[0].C = Y;
     g[0].ldc = ldy;
     g[0].bias = bias;
     g[0].relu = 1;
-    if (order == GCN_AGGREGATE_FIRST) {
-        float *AGG = (float *)saved;
+    if (af) {
         void *sw = ar.take<char>(pl.fwd_spmm);
-        rc = spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE, nullptr,
-                      sw, pl.fwd_spmm, s);
+        if (bf) {
+            rc = spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, H16, f_in, f_in, AGG16, f_in,
+                           EPI_STORE_BF16, nullptr, sw, pl.fwd_spmm, s);
+            g[1].seg[0] = GemmSeg{AGG16, f_in, Wnop, h, f_in};
+        } else {
+            float *AGG = (float *)saved;
+            rc = spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE,
+                          nullptr, sw, pl.fwd_spmm, s);
+            g[1].seg[0] = GemmSeg{AGG, f_in, Wnop, h, f_in};
+        }
         if (rc) return rc;
-        g[1].seg[0] = GemmSeg{AGG, f_in, W_neigh, h, f_in};
         g[1].C = Y + h;
         g[1].ldc = ldy;
         g[1].bias = bias + h;
         g[1].relu = 1;
-        return gemm(L_NN, 2, g, 0, 1, nullptr, 0, s);
+        return gemm(L_NN, 2, g, bf, 1, nullptr, 0, s);
     }
-    float *T = ar.take<float>((size_t)n * h);
+    // transform-first: T = H W_neigh, then the neighbour half of Y = ReLU(A T + b)
+    void *T = ar.take<char>(pl.fwd_T);
     void *sw = ar.take<char>(pl.fwd_spmm);
-    g[1].seg[0] = GemmSeg{H, ldh, W_neigh, h, f_in};
-    g[1].C = T;
+    g[1].seg[0] = GemmSeg{Hop, ldHop, Wnop, h, f_in};
     g[1].ldc = h;
-    rc = gemm(L_NN, 2, g, 0, 1, nullptr, 0, s);
-    if (rc) return rc;
-    return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, T, h, h, Y + h, ldy, EPI_BIAS_RELU, bias + h, sw,
-                    pl.fwd_spmm, s);
+    if (bf) g[1].C16 = (uint16_t *)T;
+    else g[1].C = (float *)T;
+    if ((rc = gemm(L_NN, 2, g, bf, 1, nullptr, 0, s))) return rc;
+    if (bf)
+        return spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, (const uint16_t *)T, h, h, Y + h, ldy,
+                         EPI_BIAS_RELU, bias + h, sw, pl.fwd_spmm, s);
+    return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, (const float *)T, h, h, Y + h, ldy,
+                    EPI_BIAS_RELU, bias + h, sw, pl.fwd_spmm, s);
 }
 
 int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f_in, int32_t ldh,
@@ -375,101 +422,127 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
     REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
             "gcn_layer_bwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
     const bool want_dH = dH != nullptr;
-    const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, want_dH);
+    const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, want_dH, prec);
     REQUIRE(ws && ws_bytes >= pl.bwd_total, GCN_EWORKSPACE, "gcn_layer_bwd: workspace %zu < %zu bytes",
             ws_bytes, pl.bwd_total);
     hipStream_t s = as_stream(stream);
     Arena ar(ws, ws_bytes);
-    float *P = ar.take<float>((size_t)n * 2 * h);
-    float *D = pl.need_G ? ar.take<float>((size_t)n * h) : nullptr;
-    float *T2 = (want_dH && !pl.need_G) ? ar.take<float>((size_t)n * f_in) : nullptr;
+    const bool bf = prec == GCN_BF16;
+    const bool af = order == GCN_AGGREGATE_FIRST;
+    const size_t E = bf ? 2 : 4;
+    char *P = ar.take<char>(pl.bwd_P);                      // [dZ_s || G or dZ_n], n x 2h
+    char *D = pl.need_G ? ar.take<char>(pl.bwd_D) : nullptr;  // dZ_n, n x h
+    char *T2 = (want_dH && !pl.need_G) ? ar.take<char>(pl.bwd_T2) : nullptr;
+    uint16_t *Ws16 = pl.bwd_W16 ? ar.take<uint16_t>((size_t)f_in * h) : nullptr;
+    uint16_t *Wn16 = pl.bwd_W16 ? ar.take<uint16_t>((size_t)f_in * h) : nullptr;
     void *rw = ar.take<char>(pl.bwd_relu);
     void *sw = pl.bwd_spmm ? ar.take<char>(pl.bwd_spmm) : nullptr;
     void *gw = pl.bwd_gemm ? ar.take<char>(pl.bwd_gemm) : nullptr;
     const int64_t ldP = 2 * (int64_t)h;
-
-    // a6: dZ = dY * [Y > 0], dbias
-    float *dZn = pl.need_G ? D : P + h;
+    char *Pn = P + (size_t)h * E;                              // second half of P
+    char *Zn = pl.need_G ? D : Pn;                             // where dZ_n goes
     const int64_t ldZn = pl.need_G ? h : ldP;
-    rc = relu_bwd(n, h, dY, lddy, Y, ldy, P, ldP, dZn, ldZn, nullptr, nullptr, dbias, rw, pl.bwd_relu, s);
+
+    // a6: dZ = dY * [Y > 0] and dbias
+    if (bf)
+        rc = relu_bwd(n, h, dY, lddy, Y, ldy, nullptr, ldP, nullptr, ldZn, (uint16_t *)P, (uint16_t *)Zn, dbias,
+                      rw, pl.bwd_relu, s);
+    else
+        rc = relu_bwd(n, h, dY, lddy, Y, ldy, (float *)P, ldP, (float *)Zn, ldZn, nullptr, nullptr, dbias, rw,
+                      pl.bwd_relu, s);
     if (rc) return rc;
-    // G = A^T dZ_n into the second half of P
-    if (pl.need_G) {
-        rc = spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, D, h, h, P + h, ldP, EPI_STORE,
-                      nullptr, sw, pl.bwd_spmm, s);
-        if (rc) return rc;
-    }
-    // a7: weight gradients, K = n, split-K
-    GemmProblem g[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
-    g[0].seg[0] = GemmSeg{H, ldh, P, ldP, n};
-    g[0].C = dW_self;
-    g[0].ldc = h;
-    if (order == GCN_TRANSFORM_FIRST) {
-        g[1].seg[0] = GemmSeg{H, ldh, P + h, ldP, n};                       // H^T (A^T dZ_n)
-    } else {
-        const float *AGG = (const float *)saved;
-        g[1].seg[0] = pl.need_G ? GemmSeg{AGG, f_in, D, h, n} : GemmSeg{AGG, f_in, P + h, ldP, n};
-    }
-    g[1].C = dW_neigh;
-    g[1].ldc = h;
     if (n == 0) {
-        // empty subgraph: zero gradients
         rc = fill_zero(dW_self, (int64_t)f_in * h, s);
         return rc ? rc : fill_zero(dW_neigh, (int64_t)f_in * h, s);
     }
+    // G = A^T dZ_n into the second half of P
+    if (pl.need_G) {
+        rc = bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)D, h, h, Pn,
+                            ldP, EPI_STORE_BF16, nullptr, sw, pl.bwd_spmm, s)
+                : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)D, h, h, Pn,
+                           ldP, EPI_STORE, nullptr, sw, pl.bwd_spmm, s);
+        if (rc) return rc;
+    }
+    // a7: weight gradients, K = n, split-K
+    const void *Hop = bf ? saved : (const void *)H;
+    const int64_t ldHop = bf ? f_in : ldh;
+    const void *AGGop = af ? (bf ? (const void *)((const char *)saved + align256((size_t)n * f_in * 2)) : saved)
+                           : nullptr;
+    GemmProblem g[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
+    g[0].seg[0] = GemmSeg{Hop, ldHop, P, ldP, n};
+    g[0].C = dW_self;
+    g[0].ldc = h;
+    if (!af)
+        g[1].seg[0] = GemmSeg{Hop, ldHop, Pn, ldP, n};                 // H^T (A^T dZ_n)
+    else
+        g[1].seg[0] = pl.need_G ? GemmSeg{AGGop, f_in, D, h, n} : GemmSeg{AGGop, f_in, Pn, ldP, n};
+    g[1].C = dW_neigh;
+    g[1].ldc = h;
     const int split = gemm_pick_split(2, g);
-    rc = gemm(L_TN, 2, g, 0, split, gw, pl.bwd_gemm, s);
-    if (rc) return rc;
+    if ((rc = gemm(L_TN, 2, g, bf, split, gw, pl.bwd_gemm, s))) return rc;
     if (!want_dH) return GCN_OK;
     // a8: input gradient
+    const void *Wsop = W_self, *Wnop = W_neigh;
+    if (bf) {
+        if ((rc = cvt_bf16(f_in, h, W_self, h, Ws16, h, s))) return rc;
+        if ((rc = cvt_bf16(f_in, h, W_neigh, h, Wn16, h, s))) return rc;
+        Wsop = Ws16;
+        Wnop = Wn16;
+    }
     if (pl.need_G) {
         GemmProblem d{};
         d.M = n;
         d.N = f_in;
-        d.seg[0] = GemmSeg{P, ldP, W_self, h, h};
-        d.seg[1] = GemmSeg{P + h, ldP, W_neigh, h, h};
+        d.seg[0] = GemmSeg{P, ldP, Wsop, h, h};
+        d.seg[1] = GemmSeg{Pn, ldP, Wnop, h, h};
         d.C = dH;
         d.ldc = lddh;
-        return gemm(L_NT, 1, &d, 0, 1, nullptr, 0, s);
+        return gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s);
     }
     GemmProblem d[2] = {};
     d[0].M = d[1].M = n;
     d[0].N = d[1].N = f_in;
-    d[0].seg[0] = GemmSeg{P, ldP, W_self, h, h};
+    d[0].seg[0] = GemmSeg{P, ldP, Wsop, h, h};
     d[0].C = dH;
     d[0].ldc = lddh;
-    d[1].seg[0] = GemmSeg{P + h, ldP, W_neigh, h, h};
-    d[1].C = T2;
+    d[1].seg[0] = GemmSeg{Pn, ldP, Wnop, h, h};
     d[1].ldc = f_in;
-    rc = gemm(L_NT, 2, d, 0, 1, nullptr, 0, s);
-    if (rc) return rc;
-    return spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, T2, f_in, f_in, dH, lddh,
-                    EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s);
+    if (bf) d[1].C16 = (uint16_t *)T2;
+    else d[1].C = (float *)T2;
+    if ((rc = gemm(L_NT, 2, d, bf, 1, nullptr, 0, s))) return rc;
+    return bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)T2, f_in,
+                          f_in, dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s)
+              : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)T2, f_in, f_in,
+                         dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s);
 }
 
 // ------------------------------------------------------------------ loss
 namespace {
 struct LossPlan {
-    size_t X, rows, gemm, colsum, red, total;
+    size_t X, rows, HL16, Wp16, G16, gemm, colsum, red, total;
     int split;
 };
-LossPlan plan_loss(int32_t n, int32_t f, int32_t C) {
+LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
     LossPlan p{};
     p.X = align256((size_t)n * C * sizeof(float));
     p.rows = align256((size_t)n * sizeof(float) + 4);
+    if (prec == GCN_BF16) {
+        p.HL16 = align256((size_t)n * f * 2);
+        p.Wp16 = align256((size_t)f * C * 2);
+        p.G16 = align256((size_t)n * C * 2);
+    }
     GemmProblem g = dw_problem(f, C, n);
     p.split = gemm_pick_split(1, &g);
     p.gemm = gemm_workspace_bytes(1, &g, p.split);
     p.colsum = colsum_workspace_bytes(n, C);
     p.red = loss_reduce_workspace_bytes(n);
-    p.total = p.X + p.rows + p.gemm + p.colsum + p.red + 1280;
+    p.total = p.X + p.rows + p.HL16 + p.Wp16 + p.G16 + p.gemm + p.colsum + p.red + 2304;
     return p;
 }
 }  // namespace
 
 size_t gcn_loss_workspace_bytes(int32_t n, int32_t f, int32_t C, gcn_prec prec) {
-    (void)prec;
-    return plan_loss(n, f, C).total;
+    return plan_loss(n, f, C, prec).total;
 }
 
 int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const float *W_pred, const float *b_pred,
@@ -481,18 +554,21 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
     REQUIRE(kind == GCN_SOFTMAX_CE || kind == GCN_SIGMOID_BCE, GCN_EINVAL, "gcn_loss_grad: bad kind %d",
             kind);
     REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "gcn_loss_grad: bad precision");
-    REQUIRE(prec == GCN_F32, GCN_EUNSUPPORTED, "gcn_loss_grad: the bfloat16 path is not built yet");
     REQUIRE(W_pred && b_pred && loss && dHL && dW_pred && db_pred, GCN_EINVAL, "gcn_loss_grad: null pointer");
     REQUIRE(n == 0 || HL, GCN_EINVAL, "gcn_loss_grad: null HL");
     REQUIRE(n == 0 || (kind == GCN_SOFTMAX_CE ? labels != nullptr : targets != nullptr), GCN_EINVAL,
             "gcn_loss_grad: null labels/targets");
-    const LossPlan pl = plan_loss(n, f, C);
+    const LossPlan pl = plan_loss(n, f, C, prec);
     REQUIRE(ws && ws_bytes >= pl.total, GCN_EWORKSPACE, "gcn_loss_grad: workspace %zu < %zu bytes", ws_bytes,
             pl.total);
     hipStream_t s = as_stream(stream);
     Arena ar(ws, ws_bytes);
+    const bool bf = prec == GCN_BF16;
     float *X = ar.take<float>((size_t)n * C);
     float *rows = ar.take<float>((size_t)n + 1);
+    uint16_t *HL16 = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
+    uint16_t *Wp16 = bf ? ar.take<uint16_t>((size_t)f * C) : nullptr;
+    uint16_t *G16 = bf ? ar.take<uint16_t>((size_t)n * C) : nullptr;
     void *gw = pl.gemm ? ar.take<char>(pl.gemm) : nullptr;
     void *cw = ar.take<char>(pl.colsum);
     void *lw = ar.take<char>(pl.red);
@@ -502,38 +578,47 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
         if (!rc) rc = fill_zero(db_pred, C, s);
         return rc ? rc : fill_zero(loss, 1, s);
     }
+    const void *HLop = HL, *Wpop = W_pred;
+    int64_t ldHLop = ldhl;
+    if (bf) {
+        if ((rc = cvt_bf16(n, f, HL, ldhl, HL16, f, s))) return rc;
+        if ((rc = cvt_bf16(f, C, W_pred, C, Wp16, C, s))) return rc;
+        HLop = HL16;
+        ldHLop = f;
+        Wpop = Wp16;
+    }
     // a4: logits X = HL W_pred + b_pred
     GemmProblem g{};
     g.M = n;
     g.N = C;
-    g.seg[0] = GemmSeg{HL, ldhl, W_pred, C, f};
+    g.seg[0] = GemmSeg{HLop, ldHLop, Wpop, C, f};
     g.C = X;
     g.ldc = C;
     g.bias = b_pred;
-    rc = gemm(L_NN, 1, &g, 0, 1, nullptr, 0, s);
-    if (rc) return rc;
+    if ((rc = gemm(L_NN, 1, &g, bf, 1, nullptr, 0, s))) return rc;
     // row losses; X <- G in place
-    rc = loss_rows(kind, n, C, X, labels, targets, rows, s);
-    if (rc) return rc;
+    if ((rc = loss_rows(kind, n, C, X, labels, targets, rows, s))) return rc;
     const double scale = kind == GCN_SOFTMAX_CE ? 1.0 / (double)n : 1.0 / ((double)n * (double)C);
-    rc = loss_reduce(n, rows, scale, loss, lw, pl.red, s);
-    if (rc) return rc;
+    if ((rc = loss_reduce(n, rows, scale, loss, lw, pl.red, s))) return rc;
+    const void *Gop = X;
+    if (bf) {
+        if ((rc = cvt_bf16(n, C, X, C, G16, C, s))) return rc;
+        Gop = G16;
+    }
     // a5: dW_pred = HL^T G, db_pred = sum_i G, dHL = G W_pred^T
     GemmProblem w = dw_problem(f, C, n);
-    w.seg[0] = GemmSeg{HL, ldhl, X, C, n};
+    w.seg[0] = GemmSeg{HLop, ldHLop, Gop, C, n};
     w.C = dW_pred;
     w.ldc = C;
-    rc = gemm(L_TN, 1, &w, 0, pl.split, gw, pl.gemm, s);
-    if (rc) return rc;
-    rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s);
-    if (rc) return rc;
+    if ((rc = gemm(L_TN, 1, &w, bf, pl.split, gw, pl.gemm, s))) return rc;
+    if ((rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s))) return rc;
     GemmProblem d{};
     d.M = n;
     d.N = f;
-    d.seg[0] = GemmSeg{X, C, W_pred, C, C};
+    d.seg[0] = GemmSeg{Gop, C, Wpop, C, C};
     d.C = dHL;
     d.ldc = lddhl;
-    return gemm(L_NT, 1, &d, 0, 1, nullptr, 0, s);
+    return gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s);
 }
 
 // ------------------------------------------------------------------ bf16

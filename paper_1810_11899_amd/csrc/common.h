@@ -43,6 +43,10 @@ enum KernelClass {
     K_T_SORT,
     K_T_FINAL,
     K_CVT_BF16,
+    K_GEMM_NN_BF16,
+    K_GEMM_TN_BF16,
+    K_GEMM_NT_BF16,
+    K_SPMM_BF16,
     K_CLASS_COUNT
 };
 const char *class_name(int cls);
@@ -72,7 +76,8 @@ inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 // --------------------------------------------------------------- launchers
 // SpMM (feature propagation) -------------------------------------------------
-enum SpmmEpilogue { EPI_STORE = 0, EPI_BIAS_RELU = 1, EPI_ACCUMULATE = 2 };
+// out is float for the first three, bfloat16 bits for EPI_STORE_BF16
+enum SpmmEpilogue { EPI_STORE = 0, EPI_BIAS_RELU = 1, EPI_ACCUMULATE = 2, EPI_STORE_BF16 = 3 };
 struct SpmmPlan {
     int64_t items;      // n_rows + nnz (merge-path length)
     int ipw;            // merge items per wavefront
@@ -82,11 +87,11 @@ SpmmPlan spmm_plan(int32_t n_rows, int32_t nnz);
 size_t spmm_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k);
 // out[i, c] (epilogue) sum_p vals[p] * X[indices[p], c]
 int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
-             const float *vals, const float *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+             const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s);
 // same with bfloat16 rows of X (uint16 bits), float32 accumulation
 int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
-              const float *vals, const uint16_t *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+              const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
               int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s);
 
 // GEMM on the matrix cores -----------------------------------------------------
@@ -109,6 +114,7 @@ struct GemmProblem {
     int64_t ldc;
     const float *bias;  // [N] or null
     int relu;
+    uint16_t *C16;      // when set: write bfloat16 (RNE) here instead of C (leading dim ldc)
 };
 // Up to two problems of equal layout in one launch (grouped).  `bf16` selects
 // bfloat16 operands (uint16 bits) instead of float32.  split_k > 1 is only

@@ -59,16 +59,25 @@ __global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, con
             g[v] = y[v] > 0.0f ? g[v] : 0.0f;
             sum[v] += g[v];
         }
-        float *o = dst + (int64_t)r * ldd + cc;
-        if (VEC == 4) {
-            *(float4 *)o = make_float4(g[0], g[1], g[2], g[3]);
-        } else {
+        if (dst) {
+            float *o = dst + (int64_t)r * ldd + cc;
+            if (VEC == 4) {
+                *(float4 *)o = make_float4(g[0], g[1], g[2], g[3]);
+            } else {
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) o[v] = g[v];
+                for (int v = 0; v < VEC; ++v) o[v] = g[v];
+            }
         }
         if (dst16) {
+            uint16_t *o16 = dst16 + (int64_t)r * ldd + cc;
+            if (VEC == 4) {
+                const uint32_t lo = (uint32_t)f32_to_bf16_rne(g[0]) | ((uint32_t)f32_to_bf16_rne(g[1]) << 16);
+                const uint32_t hi = (uint32_t)f32_to_bf16_rne(g[2]) | ((uint32_t)f32_to_bf16_rne(g[3]) << 16);
+                *(uint2 *)o16 = make_uint2(lo, hi);
+            } else {
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) dst16[(int64_t)r * ldd + cc + v] = f32_to_bf16_rne(g[v]);
+                for (int v = 0; v < VEC; ++v) o16[v] = f32_to_bf16_rne(g[v]);
+            }
         }
     }
 #pragma unroll
@@ -237,10 +246,12 @@ int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y
         return GCN_EWORKSPACE;
     }
     if (n > 0) {
-        auto al = [](const void *p) { return ((uintptr_t)p & 15) == 0; };
+        auto al = [](const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; };
         const bool v4 = h % 4 == 0 && lddy % 4 == 0 && ldy % 4 == 0 && ldS % 4 == 0 && ldN % 4 == 0 &&
-                        al(dY) && al(Y) && al(outS) && al(outN);
-        const double bytes = (double)n * w * 4.0 * 3.0 + (outS16 ? (double)n * w * 2.0 : 0.0);
+                        al(dY, 16) && al(Y, 16) && al(outS, 16) && al(outN, 16) && al(outS16, 8) &&
+                        al(outN16, 8);
+        const double bytes = (double)n * w * 8.0 + (outS ? (double)n * w * 4.0 : 0.0) +
+                             (outS16 ? (double)n * w * 2.0 : 0.0);
         ProfScope ps(K_RELU_MASK, s, 0.0, bytes);
         if (v4) {
             dim3 g((unsigned)((w / 4 + 255) / 256), (unsigned)chunks);

@@ -52,6 +52,7 @@ struct DevProblem {
     const float *bias;
     int relu;
     float *partial;     // split x M x N when split > 1
+    uint16_t *C16;      // bfloat16 output instead of C (no split)
 };
 
 struct DevArgs {
@@ -137,10 +138,15 @@ struct TileLoader {
 };
 
 // -------------------------------------------------------------- main kernel
+#ifndef GCN_GEMM_BK
+#define GCN_GEMM_BK 16
+#endif
+constexpr int kBK = GCN_GEMM_BK;  // K depth of one LDS stage
+
 template <int LAYOUT, bool VEC>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
     using T = float;
-    constexpr int BK = 16;
+    constexpr int BK = kBK;
     constexpr bool A_KMAJOR = (LAYOUT == L_TN);
     constexpr bool B_KMAJOR = (LAYOUT != L_NT);
     __shared__ __attribute__((aligned(16))) T As[2][BK][128 + PAD];
@@ -192,19 +198,32 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
         lb.store(Bs[buf]);
         __syncthreads();
         if (kt + 1 < kt_end) load(kt + 1);
+        // operands of the next k-step are read from LDS while the matrix
+        // cores work on the current one
+        float a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = As[buf][(lane >> 5)][wm * 64 + i * 32 + (lane & 31)];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = Bs[buf][(lane >> 5)][wn * 64 + j * 32 + (lane & 31)];
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 2) {
-            const int kr = kk + (lane >> 5);
-            float a[2], b[2];
+            float an[2], bn[2];
+            if (kk + 2 < BK) {
+                const int kr = kk + 2 + (lane >> 5);
 #pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = As[buf][kr][wm * 64 + i * 32 + (lane & 31)];
+                for (int i = 0; i < 2; ++i) an[i] = As[buf][kr][wm * 64 + i * 32 + (lane & 31)];
 #pragma unroll
-            for (int j = 0; j < 2; ++j) b[j] = Bs[buf][kr][wn * 64 + j * 32 + (lane & 31)];
+                for (int j = 0; j < 2; ++j) bn[j] = Bs[buf][kr][wn * 64 + j * 32 + (lane & 31)];
+            }
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
+            if (kk + 2 < BK) {
+#pragma unroll
+                for (int i = 0; i < 2; ++i) { a[i] = an[i]; b[i] = bn[i]; }
+            }
         }
         buf ^= 1;
     }
@@ -229,6 +248,180 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
                     if (!to_partial) {
                         v += bv;
                         if (P.relu) v = fmaxf(v, 0.0f);
+                    }
+                    dst[(int64_t)row * ldd + col] = v;
+                }
+            }
+        }
+}
+
+// ------------------------------------------------------------ bf16 kernel
+// bfloat16 operands, float32 accumulation on v_mfma_f32_32x32x16_bf16.  Both
+// operand tiles sit in LDS as [row][k] with k contiguous (row stride BK16 + 8
+// elements = 80 bytes), so a lane's eight consecutive k values are one
+// ds_read_b128 and the eight lanes served per LDS cycle fall in distinct bank
+// groups.  Operands that are contiguous along k in memory are copied as
+// 16-byte vectors; operands contiguous along the row index are transposed on
+// the way into LDS.
+constexpr int BK16 = 32;
+constexpr int LDK16 = BK16 + 8;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+template <bool KMAJOR, bool VEC>
+struct TileLoader16 {
+    static constexpr int kPer = (BK16 * 128 / 8) / kThreads;  // 16-byte vectors per thread
+    uint4 reg[kPer];
+
+    __device__ __forceinline__ void coords(int i, int &x, int &k) const {
+        const int v = threadIdx.x + i * kThreads;
+        if (KMAJOR) {   // vectors along x
+            k = v / 16;
+            x = (v % 16) * 8;
+        } else {        // vectors along k
+            x = v / (BK16 / 8);
+            k = (v % (BK16 / 8)) * 8;
+        }
+    }
+    __device__ __forceinline__ void load(const uint16_t *__restrict__ ptr, int64_t ld, int x0, int xlim, int k0,
+                                         int klim) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            int x, k;
+            coords(i, x, k);
+            const int gx = x0 + x, gk = k0 + k;
+            if (VEC) {
+                if (gx < xlim && gk < klim) {
+                    const uint16_t *p = KMAJOR ? ptr + (int64_t)gk * ld + gx : ptr + (int64_t)gx * ld + gk;
+                    reg[i] = *(const uint4 *)p;
+                } else {
+                    reg[i] = uint4{0u, 0u, 0u, 0u};
+                }
+            } else {
+                uint16_t t[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int ex = KMAJOR ? gx + e : gx;
+                    const int ek = KMAJOR ? gk : gk + e;
+                    t[e] = (ex < xlim && ek < klim)
+                               ? (KMAJOR ? ptr[(int64_t)ek * ld + ex] : ptr[(int64_t)ex * ld + ek])
+                               : (uint16_t)0;
+                }
+                reg[i] = *(uint4 *)t;
+            }
+        }
+    }
+    __device__ __forceinline__ void store(uint16_t (*lds)[LDK16]) const {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            int x, k;
+            coords(i, x, k);
+            if (KMAJOR) {
+                const uint16_t *t = (const uint16_t *)&reg[i];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) lds[x + e][k] = t[e];
+            } else {
+                *(uint4 *)&lds[x][k] = reg[i];
+            }
+        }
+    }
+};
+
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x0040u);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+template <int LAYOUT, bool VEC>
+__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(DevArgs args) {
+    constexpr bool A_KMAJOR = (LAYOUT == L_TN);
+    constexpr bool B_KMAJOR = (LAYOUT != L_NT);
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][128][LDK16];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][128][LDK16];
+
+    int64_t blk = blockIdx.x;
+    const int pi = (args.nprob > 1 && blk >= args.p[1].block_begin) ? 1 : 0;
+    const DevProblem &P = args.p[pi];
+    blk -= P.block_begin;
+    const int64_t tiles = (int64_t)P.tiles_m * P.tiles_n;
+    const int split = (int)(blk / tiles);
+    const int64_t t = blk % tiles;
+    const int tm = (int)(t / P.tiles_n);
+    const int tn = (int)(t % P.tiles_n);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kt_begin = split * P.kt_per_split;
+    int kt_end = kt_begin + P.kt_per_split;
+    if (kt_end > P.kt_total) kt_end = P.kt_total;
+
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+
+    TileLoader16<A_KMAJOR, VEC> la;
+    TileLoader16<B_KMAJOR, VEC> lb;
+    auto load = [&](int kt) {
+        const int sg = kt < P.s.kt[0] ? 0 : 1;
+        const int kk = (sg == 0 ? kt : kt - P.s.kt[0]) * BK16;
+        la.load((const uint16_t *)P.s.A[sg], P.s.lda[sg], m0, P.M, kk, P.s.K[sg]);
+        lb.load((const uint16_t *)P.s.B[sg], P.s.ldb[sg], n0, P.N, kk, P.s.K[sg]);
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    if (kt_begin < kt_end) load(kt_begin);
+    int buf = 0;
+    const int koff = (lane >> 5) * 8;
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
+        la.store(As[buf]);
+        lb.store(Bs[buf]);
+        __syncthreads();
+        if (kt + 1 < kt_end) load(kt + 1);
+#pragma unroll
+        for (int kk = 0; kk < BK16; kk += 16) {
+            bf16x8 a[2], b[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                a[i] = *(const bf16x8 *)&As[buf][wm * 64 + i * 32 + (lane & 31)][kk + koff];
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                b[j] = *(const bf16x8 *)&Bs[buf][wn * 64 + j * 32 + (lane & 31)][kk + koff];
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        }
+        buf ^= 1;
+    }
+
+    const bool to_partial = P.split > 1;
+    float *dst = to_partial ? P.partial + (int64_t)split * P.M * P.N : P.C;
+    const int64_t ldd = to_partial ? P.N : P.ldc;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+            if (col >= P.N) continue;
+            const float bv = (!to_partial && P.bias) ? P.bias[col] : 0.0f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row < P.M) {
+                    float v = acc[i][j][r];
+                    if (!to_partial) {
+                        v += bv;
+                        if (P.relu) v = fmaxf(v, 0.0f);
+                        if (P.C16) {
+                            P.C16[(int64_t)row * P.ldc + col] = to_bf16(v);
+                            continue;
+                        }
                     }
                     dst[(int64_t)row * ldd + col] = v;
                 }
@@ -269,7 +462,7 @@ bool vec_ok(int layout, const GemmProblem &g, int esz) {
     return true;
 }
 
-int bk_of(int bf16) { return bf16 ? 32 : 16; }
+int bk_of(int bf16) { return bf16 ? 32 : kBK; }
 
 void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k, float *partial,
               DevArgs &a, int64_t &blocks) {
@@ -306,6 +499,7 @@ void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int spl
         d.bias = g.bias;
         d.relu = g.relu;
         d.partial = nullptr;
+        d.C16 = g.C16;
         if (d.split > 1) {
             d.partial = partial ? (float *)((char *)partial + poff) : nullptr;
             poff += align256((size_t)d.split * g.M * g.N * sizeof(float));
@@ -315,11 +509,17 @@ void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int spl
 }
 
 template <int LAYOUT>
-void launch(bool vec, dim3 grid, hipStream_t s, const DevArgs &a) {
-    if (vec)
+void launch(bool vec, bool bf16, dim3 grid, hipStream_t s, const DevArgs &a) {
+    if (bf16) {
+        if (vec)
+            hipLaunchKernelGGL((gemm_bf16_kernel<LAYOUT, true>), grid, dim3(kThreads), 0, s, a);
+        else
+            hipLaunchKernelGGL((gemm_bf16_kernel<LAYOUT, false>), grid, dim3(kThreads), 0, s, a);
+    } else if (vec) {
         hipLaunchKernelGGL((gemm_kernel<LAYOUT, true>), grid, dim3(kThreads), 0, s, a);
-    else
+    } else {
         hipLaunchKernelGGL((gemm_kernel<LAYOUT, false>), grid, dim3(kThreads), 0, s, a);
+    }
 }
 
 }  // namespace
@@ -329,7 +529,7 @@ int gemm_pick_split(int nprob, const GemmProblem *probs) {
     for (int i = 0; i < nprob; ++i) {
         tiles += (int64_t)((probs[i].M + BM - 1) / BM) * ((probs[i].N + BN - 1) / BN);
         int64_t k = 0;
-        for (int s = 0; s < 2; ++s) k += (probs[i].seg[s].K + 15) / 16;
+        for (int s = 0; s < 2; ++s) k += (probs[i].seg[s].K + kBK - 1) / kBK;
         if (k > kt) kt = k;
     }
     if (tiles <= 0) return 1;
@@ -353,10 +553,6 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     if (nprob < 1 || nprob > 2) {
         set_error("gemm: nprob %d", nprob);
         return GCN_EINVAL;
-    }
-    if (bf16) {
-        set_error("gemm: bfloat16 operands are not built yet");
-        return GCN_EUNSUPPORTED;
     }
     if (split_k > 1 && layout != L_TN) {
         set_error("gemm: split-K only for the TN layout");
@@ -382,13 +578,14 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     if (blocks == 0) return GCN_OK;
     bool any_split = false;
     for (int i = 0; i < nprob; ++i) any_split = any_split || a.p[i].split > 1;
-    const int cls = layout == L_NN ? K_GEMM_NN : (layout == L_TN ? K_GEMM_TN : K_GEMM_NT);
+    int cls = layout == L_NN ? K_GEMM_NN : (layout == L_TN ? K_GEMM_TN : K_GEMM_NT);
+    if (bf16) cls += K_GEMM_NN_BF16 - K_GEMM_NN;
     {
         ProfScope ps(cls, s, flops, 0.0);
         dim3 grid((unsigned)blocks);
-        if (layout == L_NN) launch<L_NN>(vec, grid, s, a);
-        else if (layout == L_TN) launch<L_TN>(vec, grid, s, a);
-        else launch<L_NT>(vec, grid, s, a);
+        if (layout == L_NN) launch<L_NN>(vec, bf16 != 0, grid, s, a);
+        else if (layout == L_TN) launch<L_TN>(vec, bf16 != 0, grid, s, a);
+        else launch<L_NT>(vec, bf16 != 0, grid, s, a);
         GCN_LAUNCH_CHECK("gemm_kernel");
     }
     if (any_split) {

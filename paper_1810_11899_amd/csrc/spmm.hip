@@ -104,15 +104,30 @@ template <> struct Row<1, true> {
     __device__ void load(const uint16_t *p) { v[0] = __uint_as_float((uint32_t)(*p) << 16); }
 };
 
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x0040u);
+    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
+// Final value of out[r, c .. c+VEC) under the epilogue; `out` is float, or
+// bfloat16 bits for EPI_STORE_BF16 (ldo counts elements of either type).
 template <int VEC>
-__device__ __forceinline__ void emit(float *__restrict__ out, const float (&acc)[VEC], int epi,
-                                     const float *__restrict__ bias, int c) {
+__device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_t r, int c,
+                                     const float (&acc)[VEC], int epi, const float *__restrict__ bias) {
+    if (epi == EPI_STORE_BF16) {
+        uint16_t *o = (uint16_t *)out + r * ldo + c;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) o[v] = to_bf16(acc[v]);
+        return;
+    }
+    float *o = (float *)out + r * ldo + c;
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
-        float r = acc[v];
-        if (epi == EPI_BIAS_RELU) r = fmaxf(r + bias[c + v], 0.0f);
-        else if (epi == EPI_ACCUMULATE) r = out[v] + r;
-        out[v] = r;
+        float x = acc[v];
+        if (epi == EPI_BIAS_RELU) x = fmaxf(x + bias[c + v], 0.0f);
+        else if (epi == EPI_ACCUMULATE) x = o[v] + x;
+        o[v] = x;
     }
 }
 
@@ -127,7 +142,7 @@ template <int VEC, int CT, bool BF16>
 __global__ __launch_bounds__(256) void spmm_main(
     int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
     const float *__restrict__ vals, const void *__restrict__ Xv, int32_t k, int64_t ldx,
-    float *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
+    void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
     int64_t items, int ipw, int64_t waves, float *__restrict__ carry,
     int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
     using Elem = typename std::conditional<BF16, uint16_t, float>::type;
@@ -198,7 +213,7 @@ __global__ __launch_bounds__(256) void spmm_main(
             for (int t = 0; t < CT; ++t)
                 if (cok[t]) {
                     const int c = cbase + t * 64 * VEC;
-                    emit<VEC>(out + (int64_t)r * ldo + c, acc[t], epi, bias, c);
+                    emit<VEC>(out, ldo, r, c, acc[t], epi, bias);
                 }
         } else if (complete || pe > pb) {
             // a piece of a row cut by wavefront boundaries: head (the piece
@@ -217,10 +232,145 @@ __global__ __launch_bounds__(256) void spmm_main(
     }
 }
 
+// XCD-sliced variant (float32, k % 4 == 0).  The feature dimension is cut
+// into 64-column slices and workgroups are numbered so that, under the
+// round-robin workgroup-to-XCD dispatch, each XCD keeps gathering the same
+// slice: its 4 MB L2 then holds the hot rows of one slice (256 B per row)
+// instead of whole rows, which raises the hit rate on skewed graphs.  This is
+// the feature-only partitioning of Sec. V-B / Alg. 6, with the XCD L2 in the
+// role of the per-core cache.  Inside a wavefront, lane group g = lane / 16
+// gathers edges g, g+4, g+8, ... of the row (16 lanes x float4 = 64 columns),
+// and the four partial sums are combined with a fixed xor-shuffle tree.
+struct SliceMap {
+    int32_t slices;      // ceil(k / 64)
+    int32_t chunks;      // block chunks of kWavesPerBlock wavefronts
+    int32_t mode;        // 0: slice-major multiple of 8, 1: slice divides 8, 2: plain
+    int32_t per_xcd;     // slices per XCD (mode 0) or XCDs per slice (mode 1)
+};
+
+__device__ __forceinline__ bool slice_of_block(const SliceMap &m, int64_t w, int &slice, int64_t &chunk) {
+    if (m.mode == 0) {
+        const int64_t x = w & 7, r = w >> 3;
+        slice = (int)(x + 8 * (r % m.per_xcd));
+        chunk = r / m.per_xcd;
+    } else if (m.mode == 1) {
+        const int64_t x = w & 7, r = w >> 3;
+        slice = (int)(x % m.slices);
+        chunk = r * m.per_xcd + x / m.slices;
+    } else {
+        slice = (int)(w % m.slices);
+        chunk = w / m.slices;
+    }
+    return chunk < m.chunks;
+}
+
+__global__ __launch_bounds__(256) void spmm_sliced(
+    int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
+    const float *__restrict__ vals, const float *__restrict__ X, int32_t k, int64_t ldx,
+    void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
+    int64_t items, int ipw, int64_t waves, SliceMap map, float *__restrict__ carry,
+    int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
+    int slice;
+    int64_t chunk;
+    if (!slice_of_block(map, blockIdx.x, slice, chunk)) return;
+    const int lane = threadIdx.x & 63;
+    const int64_t wave = chunk * kWavesPerBlock + (threadIdx.x >> 6);
+    if (wave >= waves) return;
+    const int64_t d0 = wave * ipw;
+    const int64_t d1 = d0 + ipw < items ? d0 + ipw : items;
+    const int r0 = merge_search(indptr, n_rows, d0, lane);
+    const int r1 = merge_search(indptr, n_rows, d1, lane);
+    const int64_t p0 = d0 - r0, p1 = d1 - r1;
+    const int g = lane >> 4;
+    const int col = slice * 64 + (lane & 15) * 4;
+    const bool cok = col < k;
+    constexpr int U = 4;  // edges per lane group in flight
+
+    int32_t hrow = -1, trow = -1;
+    for (int r = r0; r <= r1 && r < n_rows; ++r) {
+        const int64_t rb = indptr[r], re = indptr[r + 1];
+        const bool complete = r < r1;
+        const int64_t pb = p0 > rb ? p0 : rb;
+        const int64_t pe = complete ? re : p1;
+        float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+        int64_t p = pb + g;
+        for (; p + 4 * (U - 1) < pe; p += 4 * U) {
+            int32_t j[U];
+            float w[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) { j[u] = indices[p + 4 * u]; w[u] = vals[p + 4 * u]; }
+            float4 x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                x[u] = cok ? *(const float4 *)(X + (int64_t)j[u] * ldx + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                a0 = fmaf(w[u], x[u].x, a0);
+                a1 = fmaf(w[u], x[u].y, a1);
+                a2 = fmaf(w[u], x[u].z, a2);
+                a3 = fmaf(w[u], x[u].w, a3);
+            }
+        }
+        for (; p < pe; p += 4) {
+            const int32_t j = indices[p];
+            const float w = vals[p];
+            const float4 x = cok ? *(const float4 *)(X + (int64_t)j * ldx + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+            a0 = fmaf(w, x.x, a0);
+            a1 = fmaf(w, x.y, a1);
+            a2 = fmaf(w, x.z, a2);
+            a3 = fmaf(w, x.w, a3);
+        }
+        // groups (0,1) and (2,3), then the two pairs
+        a0 += __shfl_xor(a0, 16); a1 += __shfl_xor(a1, 16); a2 += __shfl_xor(a2, 16); a3 += __shfl_xor(a3, 16);
+        a0 += __shfl_xor(a0, 32); a1 += __shfl_xor(a1, 32); a2 += __shfl_xor(a2, 32); a3 += __shfl_xor(a3, 32);
+        const float acc[4] = {a0, a1, a2, a3};
+        const bool started = (r > r0) || (p0 == rb);
+        if (g == 0 && cok) {
+            if (complete && started) {
+                emit<4>(out, ldo, r, col, acc, epi, bias);
+            } else if (complete || pe > pb) {
+                const int slot = complete ? 0 : 1;
+                store_raw<4>(carry + (2 * wave + slot) * (int64_t)k + col, acc);
+            }
+        }
+        if (!(complete && started) && (complete || pe > pb)) {
+            if (complete) hrow = r; else trow = r;
+        }
+    }
+    if (slice == 0 && lane == 0) {
+        head_row[wave] = hrow;
+        tail_row[wave] = trow;
+    }
+}
+
+SliceMap make_slice_map(int32_t k, int64_t waves) {
+    SliceMap m;
+    m.slices = (k + 63) / 64;
+    const int64_t chunks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    m.chunks = (int32_t)chunks;
+    if (m.slices % 8 == 0) {
+        m.mode = 0;
+        m.per_xcd = m.slices / 8;
+    } else if (8 % m.slices == 0) {
+        m.mode = 1;
+        m.per_xcd = 8 / m.slices;
+    } else {
+        m.mode = 2;
+        m.per_xcd = 1;
+    }
+    return m;
+}
+
+int64_t slice_map_blocks(const SliceMap &m) {
+    if (m.mode == 0) return 8 * (int64_t)m.per_xcd * m.chunks;
+    if (m.mode == 1) return 8 * (((int64_t)m.chunks + m.per_xcd - 1) / m.per_xcd);
+    return (int64_t)m.slices * m.chunks;
+}
+
 // Completes every row cut by wavefront boundaries: the wavefront w holding the
 // row's head piece sums the tail pieces of the preceding wavefronts in order,
 // then its own head piece, and applies the epilogue.
-__global__ __launch_bounds__(256) void spmm_fixup(int32_t k, float *__restrict__ out, int64_t ldo,
+__global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ out, int64_t ldo,
                                                   int epi, const float *__restrict__ bias,
                                                   int64_t waves, const float *__restrict__ carry,
                                                   const int32_t *__restrict__ head_row,
@@ -269,18 +419,15 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, float *__restrict__
         const int c = c0 + 64 * j;
         if (c >= k) continue;
         const float hv = carry[(2 * w) * (int64_t)k + c];
-        float a = any ? acc[j] + hv : hv;
-        float *o = out + (int64_t)r * ldo + c;
-        if (epi == EPI_BIAS_RELU) a = fmaxf(a + bias[c], 0.0f);
-        else if (epi == EPI_ACCUMULATE) a = *o + a;
-        *o = a;
+        const float a[1] = {any ? acc[j] + hv : hv};
+        emit<1>(out, ldo, r, c, a, epi, bias);
     }
 }
 
 template <int VEC, int CT, bool BF16>
 void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr,
                  const int32_t *indices, const float *vals, const void *X, int32_t k, int64_t ldx,
-                 float *out, int64_t ldo, int epi, const float *bias, const SpmmPlan &pl,
+                 void *out, int64_t ldo, int epi, const float *bias, const SpmmPlan &pl,
                  float *carry, int32_t *hr, int32_t *tr) {
     hipLaunchKernelGGL((spmm_main<VEC, CT, BF16>), grid, dim3(256), 0, s, n_rows, indptr, indices,
                        vals, X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw, pl.waves, carry, hr,
@@ -290,7 +437,7 @@ void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr
 bool aligned(const void *p, int bytes) { return ((uintptr_t)p % (uintptr_t)bytes) == 0; }
 
 int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
-             const float *vals, const void *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+             const float *vals, const void *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
              int epi, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
     if (n_rows <= 0 || k <= 0) return GCN_OK;
     const SpmmPlan pl = spmm_plan(n_rows, nnz);
@@ -314,10 +461,20 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, cons
     if (ct > 2) ct = 2;
     const int sw = 64 * vec * ct;
     dim3 grid((unsigned)((pl.waves + kWavesPerBlock - 1) / kWavesPerBlock), (unsigned)((k + sw - 1) / sw));
+    const bool sliced = !bf16 && k % 4 == 0 && ldx % 4 == 0 && aligned(X, 16) && ldo % 4 == 0 &&
+                        aligned(out, 16) && k >= 128;
+    const double out_bytes = epi == EPI_STORE_BF16 ? 2.0 : (epi == EPI_ACCUMULATE ? 8.0 : 4.0);
     const double bytes = (double)nnz * k * esz + (double)nnz * 8.0 + (double)(n_rows + 1) * 4.0 +
-                         (double)n_rows * k * 4.0 * (epi == EPI_ACCUMULATE ? 2.0 : 1.0);
+                         (double)n_rows * k * out_bytes;
     {
-        ProfScope ps(K_SPMM, s, 2.0 * nnz * k, bytes);
+        ProfScope ps(bf16 ? K_SPMM_BF16 : K_SPMM, s, 2.0 * nnz * k, bytes);
+        if (sliced) {
+            const SliceMap m = make_slice_map(k, pl.waves);
+            hipLaunchKernelGGL(spmm_sliced, dim3((unsigned)slice_map_blocks(m)), dim3(256), 0, s, n_rows, indptr,
+                               indices, vals, (const float *)X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw,
+                               pl.waves, m, carry, hr, tr);
+            GCN_LAUNCH_CHECK("spmm_sliced");
+        } else
 #define GCN_SPMM_CASE(V, C, B)                                                                   \
     if (vec == V && ct == C && bf16 == B) {                                                      \
         launch_main<V, C, B>(grid, s, n_rows, indptr, indices, vals, X, k, ldx, out, ldo, epi,   \
@@ -376,14 +533,14 @@ size_t spmm_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k) {
 }
 
 int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
-             const float *vals, const float *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+             const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
     return spmm_any(false, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
                     ws, ws_bytes, s);
 }
 
 int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
-              const float *vals, const uint16_t *X, int32_t k, int64_t ldx, float *out, int64_t ldo,
+              const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
               int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
     return spmm_any(true, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
                     ws, ws_bytes, s);

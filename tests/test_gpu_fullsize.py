@@ -55,13 +55,16 @@ def _f32(a):
     return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4])
-def test_layerwise_strict(cfg):
+@pytest.mark.parametrize("cfg, prec", [(2, 0), (3, 0), (4, 0), (3, 1)])
+def test_layerwise_strict(cfg, prec):
     """Every layer of the full-size workload on the oracle's own (float32-
     rounded) layer inputs: forward Y, the loss head and every gradient within
-    1e-4 with no kink allowance.  The backward receives the oracle's Y, so the
-    ReLU branch is decided on the same sign on both sides."""
+    1e-4 (float32) or 2e-2 (bfloat16 operands) with no kink allowance.  The
+    backward receives the oracle's Y, so the ReLU branch is decided on the same
+    sign on both sides."""
     from paper_1810_11899_amd import binding as B
+    from gpu_util import TOL_BF16
+    tol = TOL_BF16 if prec == B.GCN_BF16 else TOL_F32
     wl = synth.config(cfg)
     g = wl.graph
     L = len(wl.layers)
@@ -98,7 +101,7 @@ def test_layerwise_strict(cfg):
     dbp_gpu = torch.empty(C, device="cuda")
     B.gcn_loss_grad(d(Ys[-1]), d(wl.W_pred), d(wl.b_pred), B.LOSS_KIND[wl.spec.head],
                     d(wl.labels.astype(np.int32), torch.int32) if wl.labels is not None else None,
-                    d(wl.targets) if wl.targets is not None else None, l_gpu, dHL_gpu, dWp_gpu, dbp_gpu, ws)
+                    d(wl.targets) if wl.targets is not None else None, l_gpu, dHL_gpu, dWp_gpu, dbp_gpu, ws, prec)
     errs["loss"] = abs(l_gpu.item() - loss) / abs(loss)
     errs["dW_pred"] = rel_inf(dWp_gpu.cpu().numpy(), dWp)
     errs["db_pred"] = rel_inf(dbp_gpu.cpu().numpy(), dbp)
@@ -110,9 +113,9 @@ def test_layerwise_strict(cfg):
         Hin = d(caches[li].H)
         Ws, Wn, b = d(lay.W_self), d(lay.W_neigh), d(lay.bias)
         Y_gpu = torch.empty((n, 2 * h), device="cuda")
-        nb = B.gcn_layer_saved_bytes(n, f_in, h, order)
+        nb = B.gcn_layer_saved_bytes(n, f_in, h, order, prec)
         saved = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda") if nb else None
-        B.gcn_layer_fwd(A, Hin, Ws, Wn, b, Y_gpu, saved, order, ws)
+        B.gcn_layer_fwd(A, Hin, Ws, Wn, b, Y_gpu, saved, order, ws, prec)
         errs[f"Y{li}"] = rel_inf(Y_gpu.cpu().numpy(), Ys[li])
         Y32 = _f32(Ys[li])
         assert np.array_equal(Y32 > 0, caches[li].Z > 0)  # same ReLU branch on both sides
@@ -120,7 +123,7 @@ def test_layerwise_strict(cfg):
         dWs = torch.empty((f_in, h), device="cuda")
         dWn = torch.empty((f_in, h), device="cuda")
         db = torch.empty(2 * h, device="cuda")
-        B.gcn_layer_bwd(A, AT, Hin, Ws, Wn, d(Y32), saved, d(dYs[li]), dH_gpu, dWs, dWn, db, order, ws)
+        B.gcn_layer_bwd(A, AT, Hin, Ws, Wn, d(Y32), saved, d(dYs[li]), dH_gpu, dWs, dWn, db, order, ws, prec)
         rWs, rWn, rdb, rdH = oracle.layer_bwd(gT, caches[li], lay.W_self, lay.W_neigh, dYs[li], need)
         errs[f"dW_self{li}"] = rel_inf(dWs.cpu().numpy(), rWs)
         errs[f"dW_neigh{li}"] = rel_inf(dWn.cpu().numpy(), rWn)
@@ -128,5 +131,5 @@ def test_layerwise_strict(cfg):
         if need:
             errs[f"dH{li}"] = rel_inf(dH_gpu.cpu().numpy(), rdH)
     print("max relative errors:", {k: f"{v:.1e}" for k, v in errs.items()})
-    bad = {k: v for k, v in errs.items() if not v <= TOL_F32}
+    bad = {k: v for k, v in errs.items() if not v <= tol}
     assert not bad, bad

@@ -66,7 +66,7 @@ def test_transpose_bit_exact(case, ws):
 
 
 # ------------------------------------------------------------- aggregate ----
-@pytest.mark.parametrize("k", [1, 50, 64, 100, 128, 130, 256, 300, 512, 602, 1024])
+@pytest.mark.parametrize("k", [1, 50, 64, 100, 128, 130, 192, 200, 256, 300, 512, 602, 1024])
 def test_aggregate_parity_widths(k, ws):
     wl = synth.custom(3001, "rmat", 13, [(2, 2)], seed=k)
     g = wl.graph
@@ -113,11 +113,11 @@ def test_aggregate_constant_features_mean(ws):
     assert np.all(err <= (2.0 * deg[nz, None] + 4) * 2.0 ** -23)
 
 
-@pytest.mark.parametrize("n", [70000, 5])
-def test_aggregate_long_row_split_over_wavefronts(n, ws):
+@pytest.mark.parametrize("n, k", [(70000, 96), (5, 96), (70000, 512), (3, 512)])
+def test_aggregate_long_row_split_over_wavefronts(n, k, ws):
     g = synth.star_graph(n)
-    X = np.random.default_rng(4).standard_normal((g.n, 96)).astype(np.float32)
-    out = torch.empty((g.n, 96), dtype=torch.float32, device="cuda")
+    X = np.random.default_rng(4).standard_normal((g.n, k)).astype(np.float32)
+    out = torch.empty((g.n, k), dtype=torch.float32, device="cuda")
     B.gcn_aggregate(dcsr(g), dev(X), out, ws)
     ref = oracle.aggregate(g.indptr, g.indices, g.vals, X)
     assert rel_inf(out.cpu().numpy(), ref) <= TOL_F32 / 10
@@ -147,6 +147,20 @@ def test_aggregate_is_deterministic(ws):
 
 
 # ------------------------------------------------------------------ bf16 ----
+@pytest.mark.parametrize("k", [64, 128, 200, 512, 602])
+def test_aggregate_bf16(k, ws):
+    """Against the oracle on the unrounded inputs (the 2e-2 gate) and, tighter,
+    on the bfloat16-rounded inputs (float32 accumulation only)."""
+    wl = synth.custom(3001, "rmat", 13, [(2, 2)], seed=k + 7)
+    g = wl.graph
+    X = np.random.default_rng(k).standard_normal((g.n, k)).astype(np.float32)
+    out = torch.empty((g.n, k), dtype=torch.float32, device="cuda")
+    B.gcn_aggregate(dcsr(g), dev(X), out, ws, prec=B.GCN_BF16)
+    o = out.cpu().numpy()
+    assert rel_inf(o, oracle.aggregate(g.indptr, g.indices, g.vals, X)) <= 2e-2
+    assert rel_inf(o, oracle.aggregate(g.indptr, g.indices, g.vals, obf16.round_bf16(X))) <= 1e-5
+
+
 def test_bf16_conversion_bit_exact():
     rng = np.random.default_rng(0)
     x = np.concatenate([rng.standard_normal(100003).astype(np.float32) * 1e3,

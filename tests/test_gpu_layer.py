@@ -9,7 +9,7 @@ from paper_1810_11899_amd import binding as B
 from paper_1810_11899_amd import synth
 from paper_1810_11899_amd.runner import StepRunner
 
-from gpu_util import TOL_F32, dev, rel_inf, require_gpu
+from gpu_util import TOL_BF16, TOL_F32, dev, rel_inf, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -38,26 +38,35 @@ SHAPES = [(777, "rmat", 9, 37, 24), (1500, "er", 12, 64, 48), (2049, "rmat", 15,
           (1000, "rmat", 11, 256, 128)]
 
 
+PRECS = [(B.GCN_F32, TOL_F32), (B.GCN_BF16, TOL_BF16)]
+
+
+@pytest.mark.parametrize("prec, tol", PRECS)
 @pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
 @pytest.mark.parametrize("shape", SHAPES)
-def test_layer_forward(order, shape, ws):
+def test_layer_forward(prec, tol, order, shape, ws):
     n, kind, d, f_in, h = shape
     wl = synth.custom(n, kind, d, [(f_in, h)], seed=f_in)
     lay = wl.layers[0]
     b = _bias(h, n)
     A = dcsr(wl.graph)
     Y = torch.empty((n, 2 * h), device="cuda")
-    nb = B.gcn_layer_saved_bytes(n, f_in, h, order)
+    nb = B.gcn_layer_saved_bytes(n, f_in, h, order, prec)
     saved = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda") if nb else None
-    B.gcn_layer_fwd(A, dev(wl.H), dev(lay.W_self), dev(lay.W_neigh), dev(b), Y, saved, order, ws)
+    B.gcn_layer_fwd(A, dev(wl.H), dev(lay.W_self), dev(lay.W_neigh), dev(b), Y, saved, order, ws, prec)
     Yref, _ = oracle.layer_fwd(wl.graph, wl.H, lay.W_self, lay.W_neigh, b)
-    assert rel_inf(Y.cpu().numpy(), Yref) <= TOL_F32
+    assert rel_inf(Y.cpu().numpy(), Yref) <= tol
 
 
+@pytest.mark.parametrize("prec, tol", PRECS)
 @pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
 @pytest.mark.parametrize("want_dH", [True, False])
 @pytest.mark.parametrize("shape", SHAPES)
-def test_layer_backward(order, want_dH, shape, ws):
+def test_layer_backward(prec, tol, order, want_dH, shape, ws):
+    """float32: the backward runs on the GPU's own forward output, with the
+    oracle's kink envelope.  bfloat16 (rounding far coarser than any kink
+    band worth modelling): the backward receives the oracle's Y, so both sides
+    take every ReLU branch on the same sign, and the gate is strict."""
     n, kind, d, f_in, h = shape
     wl = synth.custom(n, kind, d, [(f_in, h)], seed=f_in + 1)
     lay = wl.layers[0]
@@ -68,30 +77,38 @@ def test_layer_backward(order, want_dH, shape, ws):
     H = dev(wl.H)
     Ws, Wn = dev(lay.W_self), dev(lay.W_neigh)
     Y = torch.empty((n, 2 * h), device="cuda")
-    nb = B.gcn_layer_saved_bytes(n, f_in, h, order)
+    nb = B.gcn_layer_saved_bytes(n, f_in, h, order, prec)
     saved = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda") if nb else None
-    B.gcn_layer_fwd(A, H, Ws, Wn, dev(b), Y, saved, order, ws)
+    B.gcn_layer_fwd(A, H, Ws, Wn, dev(b), Y, saved, order, ws, prec)
+    Yref, cache = oracle.layer_fwd(g, wl.H, lay.W_self, lay.W_neigh, b, ambiguity=True)
+    if prec == B.GCN_BF16:
+        Y32 = Yref.astype(np.float32)
+        assert np.array_equal(Y32 > 0, cache.Z > 0)
+        Y = dev(Y32)
     dY = np.random.default_rng(n).standard_normal((n, 2 * h)).astype(np.float32)
     dH = torch.empty((n, f_in), device="cuda") if want_dH else None
     dWs = torch.empty((f_in, h), device="cuda")
     dWn = torch.empty((f_in, h), device="cuda")
     db = torch.empty(2 * h, device="cuda")
-    B.gcn_layer_bwd(A, AT, H, Ws, Wn, Y, saved, dev(dY), dH, dWs, dWn, db, order, ws)
-    _, cache = oracle.layer_fwd(g, wl.H, lay.W_self, lay.W_neigh, b, ambiguity=True)
+    B.gcn_layer_bwd(A, AT, H, Ws, Wn, Y, saved, dev(dY), dH, dWs, dWn, db, order, ws, prec)
     ti, tj, tv = oracle.csr_transpose(g.n, g.n, g.indptr, g.indices, g.vals)
     gT = synth.Graph(g.n, ti, tj, tv)
     rWs, rWn, rdb, rdH = oracle.layer_bwd(gT, cache, lay.W_self, lay.W_neigh, dY, want_dH)
-    eWs, eWn, edb, edH = oracle.layer_bwd_envelope(gT, cache, lay.W_self, lay.W_neigh, dY, None, want_dH)
-    assert rel_inf(dWs.cpu().numpy(), rWs, eWs) <= TOL_F32
-    assert rel_inf(dWn.cpu().numpy(), rWn, eWn) <= TOL_F32
-    assert rel_inf(db.cpu().numpy(), rdb, edb) <= TOL_F32
+    if prec == B.GCN_BF16:
+        eWs = eWn = edb = edH = None
+    else:
+        eWs, eWn, edb, edH = oracle.layer_bwd_envelope(gT, cache, lay.W_self, lay.W_neigh, dY, None, want_dH)
+    assert rel_inf(dWs.cpu().numpy(), rWs, eWs) <= tol
+    assert rel_inf(dWn.cpu().numpy(), rWn, eWn) <= tol
+    assert rel_inf(db.cpu().numpy(), rdb, edb) <= tol
     if want_dH:
-        assert rel_inf(dH.cpu().numpy(), rdH, edH) <= TOL_F32
+        assert rel_inf(dH.cpu().numpy(), rdH, edH) <= tol
 
 
+@pytest.mark.parametrize("prec, tol", PRECS)
 @pytest.mark.parametrize("kind", ["ce", "bce"])
 @pytest.mark.parametrize("n, f, C", [(3000, 256, 41), (1001, 130, 100), (257, 64, 7)])
-def test_loss_grad(kind, n, f, C, ws):
+def test_loss_grad(prec, tol, kind, n, f, C, ws):
     rng = np.random.default_rng(n + C)
     HL = np.maximum(rng.standard_normal((n, f)), 0).astype(np.float32)
     Wp = (rng.standard_normal((f, C)) * 0.2).astype(np.float32)
@@ -103,12 +120,12 @@ def test_loss_grad(kind, n, f, C, ws):
     dWp = torch.empty((f, C), device="cuda")
     dbp = torch.empty(C, device="cuda")
     B.gcn_loss_grad(dev(HL), dev(Wp), dev(bp), B.LOSS_KIND[kind], dev(labels, torch.int32),
-                    dev(targets) if kind == "bce" else None, loss, dHL, dWp, dbp, ws)
+                    dev(targets) if kind == "bce" else None, loss, dHL, dWp, dbp, ws, prec)
     rl, rdWp, rdbp, rdHL, _ = oracle.loss_grad(kind, HL, Wp, bp, labels=labels, targets=targets)
-    assert abs(loss.item() - rl) / abs(rl) <= TOL_F32
-    assert rel_inf(dWp.cpu().numpy(), rdWp) <= TOL_F32
-    assert rel_inf(dbp.cpu().numpy(), rdbp) <= TOL_F32
-    assert rel_inf(dHL.cpu().numpy(), rdHL) <= TOL_F32
+    assert abs(loss.item() - rl) / abs(rl) <= tol
+    assert rel_inf(dWp.cpu().numpy(), rdWp) <= tol
+    assert rel_inf(dbp.cpu().numpy(), rdbp) <= tol
+    assert rel_inf(dHL.cpu().numpy(), rdHL) <= tol
 
 
 # ------------------------------------------------------------ whole steps ----
