@@ -37,7 +37,7 @@ static const char *kClassNames[K_CLASS_COUNT] = {
     "spmm", "spmm_fixup", "gemm_nn", "gemm_tn", "gemm_nt", "splitk_reduce", "relu_bwd",
     "colsum", "loss_rows", "loss_reduce", "transpose_count", "transpose_scan", "transpose_scatter",
     "transpose_sort", "transpose_final", "cvt_bf16", "gemm_nn_bf16", "gemm_tn_bf16", "gemm_nt_bf16",
-    "spmm_bf16"};
+    "spmm_bf16", "transpose_bf16"};
 
 const char *class_name(int cls) {
     return (cls >= 0 && cls < K_CLASS_COUNT) ? kClassNames[cls] : "";
@@ -143,7 +143,7 @@ struct LayerPlan {
     bool need_G;        // backward forms G = A^T dZ_n
     bool bf16;
     size_t fwd_T, fwd_W16, fwd_spmm;
-    size_t bwd_P, bwd_D, bwd_T2, bwd_W16, bwd_relu, bwd_spmm, bwd_gemm;
+    size_t bwd_P, bwd_PT, bwd_D, bwd_DT, bwd_T2, bwd_W16, bwd_relu, bwd_spmm, bwd_gemm;
     size_t fwd_total, bwd_total, total;
 };
 
@@ -167,6 +167,10 @@ LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order,
     p.bf16 = prec == GCN_BF16;
     const size_t E = p.bf16 ? 2 : 4;  // bytes per stored intermediate element
     const size_t W16 = p.bf16 ? 2 * align256((size_t)f_in * h * 2) : 0;
+    // bfloat16 products run with both operands contiguous along K: the
+    // backward also keeps P^T (and dZ_n^T for aggregate-first with G)
+    p.bwd_PT = p.bf16 ? align256((size_t)n * 2 * h * 2) : 0;
+    p.bwd_DT = (p.bf16 && p.need_G && order == GCN_AGGREGATE_FIRST) ? align256((size_t)n * h * 2) : 0;
     if (order == GCN_TRANSFORM_FIRST) {
         p.fwd_T = align256((size_t)n * h * E);
         p.fwd_spmm = spmm_workspace_bytes(n, nnz, h);
@@ -189,17 +193,25 @@ LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order,
     p.bwd_relu = relu_bwd_workspace_bytes(n, h);
     GemmProblem pr[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
     p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr));
-    p.bwd_total = p.bwd_P + p.bwd_D + p.bwd_T2 + p.bwd_W16 + p.bwd_relu + p.bwd_spmm + p.bwd_gemm + 2304;
+    if (p.bf16) {  // weight gradients as NT products
+        pr[0].seg[0].lda = n;
+        pr[0].seg[0].ldb = n;
+        pr[1] = pr[0];
+        p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr));
+    }
+    p.bwd_total = p.bwd_P + p.bwd_PT + p.bwd_D + p.bwd_DT + p.bwd_T2 + p.bwd_W16 + p.bwd_relu + p.bwd_spmm +
+                  p.bwd_gemm + 2816;
     p.total = std::max(p.fwd_total, p.bwd_total);
     return p;
 }
 
-// float32: AGG (aggregate-first only).  bfloat16: H16, then AGG16 (aggregate-first).
+// float32: AGG (aggregate-first only).  bfloat16: H16, H16^T, then AGG16 and
+// AGG16^T (aggregate-first), each n x f_in.
 size_t saved_bytes(int32_t n, int32_t f_in, int32_t h, int order, int prec) {
     (void)h;
     if (prec == GCN_BF16) {
         const size_t one = align256((size_t)n * f_in * 2);
-        return order == GCN_AGGREGATE_FIRST ? 2 * one : one;
+        return order == GCN_AGGREGATE_FIRST ? 4 * one : 2 * one;
     }
     if (order == GCN_AGGREGATE_FIRST) return align256((size_t)n * f_in * sizeof(float));
     return 0;
@@ -341,63 +353,81 @@ int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, c
     const bool bf = prec == GCN_BF16;
     const bool af = order == GCN_AGGREGATE_FIRST;
 
-    // operands of the products: float32 as given, or their bfloat16 roundings
-    const void *Hop = H, *Wsop = W_self, *Wnop = W_neigh;
-    int64_t ldHop = ldh;
-    uint16_t *H16 = nullptr, *AGG16 = nullptr;
     if (bf) {
-        H16 = (uint16_t *)saved;
-        AGG16 = af ? (uint16_t *)((char *)saved + align256((size_t)n * f_in * 2)) : nullptr;
-        uint16_t *Ws16 = ar.take<uint16_t>((size_t)f_in * h);
-        uint16_t *Wn16 = ar.take<uint16_t>((size_t)f_in * h);
+        // bfloat16 operands, every product in NT form (both operands contiguous
+        // along K); saved = H16 | H16^T | AGG16 | AGG16^T
+        const size_t one = align256((size_t)n * f_in * 2);
+        uint16_t *H16 = (uint16_t *)saved;
+        uint16_t *H16T = (uint16_t *)((char *)saved + one);
+        uint16_t *AGG16 = af ? (uint16_t *)((char *)saved + 2 * one) : nullptr;
+        uint16_t *AGG16T = af ? (uint16_t *)((char *)saved + 3 * one) : nullptr;
+        uint16_t *WsT = ar.take<uint16_t>((size_t)f_in * h);
+        uint16_t *WnT = ar.take<uint16_t>((size_t)f_in * h);
         if ((rc = cvt_bf16(n, f_in, H, ldh, H16, f_in, s))) return rc;
-        if ((rc = cvt_bf16(f_in, h, W_self, h, Ws16, h, s))) return rc;
-        if ((rc = cvt_bf16(f_in, h, W_neigh, h, Wn16, h, s))) return rc;
-        Hop = H16;
-        ldHop = f_in;
-        Wsop = Ws16;
-        Wnop = Wn16;
+        if ((rc = transpose_bf16(n, f_in, H16, 1, f_in, H16T, n, s))) return rc;
+        if ((rc = transpose_bf16(f_in, h, W_self, 0, h, WsT, f_in, s))) return rc;
+        if ((rc = transpose_bf16(f_in, h, W_neigh, 0, h, WnT, f_in, s))) return rc;
+        GemmProblem g[2] = {};
+        g[0].M = g[1].M = n;
+        g[0].N = g[1].N = h;
+        g[0].seg[0] = GemmSeg{H16, f_in, WsT, f_in, f_in};
+        g[0].C = Y;
+        g[0].ldc = ldy;
+        g[0].bias = bias;
+        g[0].relu = 1;
+        if (af) {
+            void *sw = ar.take<char>(pl.fwd_spmm);
+            rc = spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, H16, f_in, f_in, AGG16, f_in,
+                           EPI_STORE_BF16, nullptr, sw, pl.fwd_spmm, s);
+            if (rc) return rc;
+            if ((rc = transpose_bf16(n, f_in, AGG16, 1, f_in, AGG16T, n, s))) return rc;
+            g[1].seg[0] = GemmSeg{AGG16, f_in, WnT, f_in, f_in};
+            g[1].C = Y + h;
+            g[1].ldc = ldy;
+            g[1].bias = bias + h;
+            g[1].relu = 1;
+            return gemm(L_NT, 2, g, 1, 1, nullptr, 0, s);
+        }
+        uint16_t *T16 = (uint16_t *)ar.take<char>(pl.fwd_T);
+        void *sw = ar.take<char>(pl.fwd_spmm);
+        g[1].seg[0] = GemmSeg{H16, f_in, WnT, f_in, f_in};
+        g[1].C16 = T16;
+        g[1].ldc = h;
+        if ((rc = gemm(L_NT, 2, g, 1, 1, nullptr, 0, s))) return rc;
+        return spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, T16, h, h, Y + h, ldy, EPI_BIAS_RELU,
+                         bias + h, sw, pl.fwd_spmm, s);
     }
+
     GemmProblem g[2] = {};
     g[0].M = g[1].M = n;
     g[0].N = g[1].N = h;
-    g[0].seg[0] = GemmSeg{Hop, ldHop, Wsop, h, f_in};
+    g[0].seg[0] = GemmSeg{H, ldh, W_self, h, f_in};
     g[0].C = Y;
     g[0].ldc = ldy;
     g[0].bias = bias;
     g[0].relu = 1;
     if (af) {
         void *sw = ar.take<char>(pl.fwd_spmm);
-        if (bf) {
-            rc = spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, H16, f_in, f_in, AGG16, f_in,
-                           EPI_STORE_BF16, nullptr, sw, pl.fwd_spmm, s);
-            g[1].seg[0] = GemmSeg{AGG16, f_in, Wnop, h, f_in};
-        } else {
-            float *AGG = (float *)saved;
-            rc = spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE,
-                          nullptr, sw, pl.fwd_spmm, s);
-            g[1].seg[0] = GemmSeg{AGG, f_in, Wnop, h, f_in};
-        }
+        float *AGG = (float *)saved;
+        rc = spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE, nullptr, sw,
+                      pl.fwd_spmm, s);
         if (rc) return rc;
+        g[1].seg[0] = GemmSeg{AGG, f_in, W_neigh, h, f_in};
         g[1].C = Y + h;
         g[1].ldc = ldy;
         g[1].bias = bias + h;
         g[1].relu = 1;
-        return gemm(L_NN, 2, g, bf, 1, nullptr, 0, s);
+        return gemm(L_NN, 2, g, 0, 1, nullptr, 0, s);
     }
     // transform-first: T = H W_neigh, then the neighbour half of Y = ReLU(A T + b)
-    void *T = ar.take<char>(pl.fwd_T);
+    float *T = (float *)ar.take<char>(pl.fwd_T);
     void *sw = ar.take<char>(pl.fwd_spmm);
-    g[1].seg[0] = GemmSeg{Hop, ldHop, Wnop, h, f_in};
+    g[1].seg[0] = GemmSeg{H, ldh, W_neigh, h, f_in};
+    g[1].C = T;
     g[1].ldc = h;
-    if (bf) g[1].C16 = (uint16_t *)T;
-    else g[1].C = (float *)T;
-    if ((rc = gemm(L_NN, 2, g, bf, 1, nullptr, 0, s))) return rc;
-    if (bf)
-        return spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, (const uint16_t *)T, h, h, Y + h, ldy,
-                         EPI_BIAS_RELU, bias + h, sw, pl.fwd_spmm, s);
-    return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, (const float *)T, h, h, Y + h, ldy,
-                    EPI_BIAS_RELU, bias + h, sw, pl.fwd_spmm, s);
+    if ((rc = gemm(L_NN, 2, g, 0, 1, nullptr, 0, s))) return rc;
+    return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, T, h, h, Y + h, ldy, EPI_BIAS_RELU, bias + h, sw,
+                    pl.fwd_spmm, s);
 }
 
 int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f_in, int32_t ldh,
@@ -464,22 +494,34 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
         if (rc) return rc;
     }
     // a7: weight gradients, K = n, split-K
-    const void *Hop = bf ? saved : (const void *)H;
-    const int64_t ldHop = bf ? f_in : ldh;
-    const void *AGGop = af ? (bf ? (const void *)((const char *)saved + align256((size_t)n * f_in * 2)) : saved)
-                           : nullptr;
     GemmProblem g[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
-    g[0].seg[0] = GemmSeg{Hop, ldHop, P, ldP, n};
+    int layout = L_TN;
+    if (bf) {
+        // NT form: dW = (H^T) (P^T)^T with H^T (f_in x n) and P^T (2h x n) contiguous along n
+        const size_t one = align256((size_t)n * f_in * 2);
+        const uint16_t *H16T = (const uint16_t *)((const char *)saved + one);
+        const uint16_t *AGG16T = af ? (const uint16_t *)((const char *)saved + 3 * one) : nullptr;
+        uint16_t *PT = (uint16_t *)ar.take<char>(pl.bwd_PT);
+        uint16_t *DT = pl.bwd_DT ? (uint16_t *)ar.take<char>(pl.bwd_DT) : nullptr;
+        if ((rc = transpose_bf16(n, 2 * h, P, 1, ldP, PT, n, s))) return rc;
+        if (DT && (rc = transpose_bf16(n, h, D, 1, h, DT, n, s))) return rc;
+        layout = L_NT;
+        g[0].seg[0] = GemmSeg{H16T, n, PT, n, n};
+        if (!af) g[1].seg[0] = GemmSeg{H16T, n, PT + (size_t)h * n, n, n};
+        else g[1].seg[0] = GemmSeg{AGG16T, n, DT ? DT : PT + (size_t)h * n, n, n};
+    } else {
+        g[0].seg[0] = GemmSeg{H, ldh, P, ldP, n};
+        if (!af)
+            g[1].seg[0] = GemmSeg{H, ldh, Pn, ldP, n};                 // H^T (A^T dZ_n)
+        else
+            g[1].seg[0] = pl.need_G ? GemmSeg{saved, f_in, D, h, n} : GemmSeg{saved, f_in, Pn, ldP, n};
+    }
     g[0].C = dW_self;
     g[0].ldc = h;
-    if (!af)
-        g[1].seg[0] = GemmSeg{Hop, ldHop, Pn, ldP, n};                 // H^T (A^T dZ_n)
-    else
-        g[1].seg[0] = pl.need_G ? GemmSeg{AGGop, f_in, D, h, n} : GemmSeg{AGGop, f_in, Pn, ldP, n};
     g[1].C = dW_neigh;
     g[1].ldc = h;
     const int split = gemm_pick_split(2, g);
-    if ((rc = gemm(L_TN, 2, g, bf, split, gw, pl.bwd_gemm, s))) return rc;
+    if ((rc = gemm(layout, 2, g, bf, split, gw, pl.bwd_gemm, s))) return rc;
     if (!want_dH) return GCN_OK;
     // a8: input gradient
     const void *Wsop = W_self, *Wnop = W_neigh;
@@ -519,7 +561,7 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
 // ------------------------------------------------------------------ loss
 namespace {
 struct LossPlan {
-    size_t X, rows, HL16, Wp16, G16, gemm, colsum, red, total;
+    size_t X, rows, HL16, HL16T, Wp16, Wp16T, G16, G16T, gemm, colsum, red, total;
     int split;
 };
 LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
@@ -527,16 +569,17 @@ LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
     p.X = align256((size_t)n * C * sizeof(float));
     p.rows = align256((size_t)n * sizeof(float) + 4);
     if (prec == GCN_BF16) {
-        p.HL16 = align256((size_t)n * f * 2);
-        p.Wp16 = align256((size_t)f * C * 2);
-        p.G16 = align256((size_t)n * C * 2);
+        p.HL16 = p.HL16T = align256((size_t)n * f * 2);
+        p.Wp16 = p.Wp16T = align256((size_t)f * C * 2);
+        p.G16 = p.G16T = align256((size_t)n * C * 2);
     }
     GemmProblem g = dw_problem(f, C, n);
     p.split = gemm_pick_split(1, &g);
     p.gemm = gemm_workspace_bytes(1, &g, p.split);
     p.colsum = colsum_workspace_bytes(n, C);
     p.red = loss_reduce_workspace_bytes(n);
-    p.total = p.X + p.rows + p.HL16 + p.Wp16 + p.G16 + p.gemm + p.colsum + p.red + 2304;
+    p.total = p.X + p.rows + p.HL16 + p.HL16T + p.Wp16 + p.Wp16T + p.G16 + p.G16T + p.gemm + p.colsum + p.red +
+              3328;
     return p;
 }
 }  // namespace
@@ -567,8 +610,11 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
     float *X = ar.take<float>((size_t)n * C);
     float *rows = ar.take<float>((size_t)n + 1);
     uint16_t *HL16 = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
+    uint16_t *HL16T = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
     uint16_t *Wp16 = bf ? ar.take<uint16_t>((size_t)f * C) : nullptr;
+    uint16_t *Wp16T = bf ? ar.take<uint16_t>((size_t)f * C) : nullptr;
     uint16_t *G16 = bf ? ar.take<uint16_t>((size_t)n * C) : nullptr;
+    uint16_t *G16T = bf ? ar.take<uint16_t>((size_t)n * C) : nullptr;
     void *gw = pl.gemm ? ar.take<char>(pl.gemm) : nullptr;
     void *cw = ar.take<char>(pl.colsum);
     void *lw = ar.take<char>(pl.red);
@@ -578,46 +624,51 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
         if (!rc) rc = fill_zero(db_pred, C, s);
         return rc ? rc : fill_zero(loss, 1, s);
     }
-    const void *HLop = HL, *Wpop = W_pred;
-    int64_t ldHLop = ldhl;
-    if (bf) {
-        if ((rc = cvt_bf16(n, f, HL, ldhl, HL16, f, s))) return rc;
-        if ((rc = cvt_bf16(f, C, W_pred, C, Wp16, C, s))) return rc;
-        HLop = HL16;
-        ldHLop = f;
-        Wpop = Wp16;
-    }
     // a4: logits X = HL W_pred + b_pred
     GemmProblem g{};
     g.M = n;
     g.N = C;
-    g.seg[0] = GemmSeg{HLop, ldHLop, Wpop, C, f};
     g.C = X;
     g.ldc = C;
     g.bias = b_pred;
-    if ((rc = gemm(L_NN, 1, &g, bf, 1, nullptr, 0, s))) return rc;
+    if (bf) {
+        // NT form: B = W_pred^T (C x f)
+        if ((rc = cvt_bf16(n, f, HL, ldhl, HL16, f, s))) return rc;
+        if ((rc = transpose_bf16(n, f, HL16, 1, f, HL16T, n, s))) return rc;
+        if ((rc = cvt_bf16(f, C, W_pred, C, Wp16, C, s))) return rc;
+        if ((rc = transpose_bf16(f, C, Wp16, 1, C, Wp16T, f, s))) return rc;
+        g.seg[0] = GemmSeg{HL16, f, Wp16T, f, f};
+        rc = gemm(L_NT, 1, &g, 1, 1, nullptr, 0, s);
+    } else {
+        g.seg[0] = GemmSeg{HL, ldhl, W_pred, C, f};
+        rc = gemm(L_NN, 1, &g, 0, 1, nullptr, 0, s);
+    }
+    if (rc) return rc;
     // row losses; X <- G in place
     if ((rc = loss_rows(kind, n, C, X, labels, targets, rows, s))) return rc;
     const double scale = kind == GCN_SOFTMAX_CE ? 1.0 / (double)n : 1.0 / ((double)n * (double)C);
     if ((rc = loss_reduce(n, rows, scale, loss, lw, pl.red, s))) return rc;
-    const void *Gop = X;
-    if (bf) {
-        if ((rc = cvt_bf16(n, C, X, C, G16, C, s))) return rc;
-        Gop = G16;
-    }
     // a5: dW_pred = HL^T G, db_pred = sum_i G, dHL = G W_pred^T
     GemmProblem w = dw_problem(f, C, n);
-    w.seg[0] = GemmSeg{HLop, ldHLop, Gop, C, n};
     w.C = dW_pred;
     w.ldc = C;
-    if ((rc = gemm(L_TN, 1, &w, bf, pl.split, gw, pl.gemm, s))) return rc;
-    if ((rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s))) return rc;
     GemmProblem d{};
     d.M = n;
     d.N = f;
-    d.seg[0] = GemmSeg{Gop, C, Wpop, C, C};
     d.C = dHL;
     d.ldc = lddhl;
+    if (bf) {
+        if ((rc = cvt_bf16(n, C, X, C, G16, C, s))) return rc;
+        if ((rc = transpose_bf16(n, C, G16, 1, C, G16T, n, s))) return rc;
+        w.seg[0] = GemmSeg{HL16T, n, G16T, n, n};
+        if ((rc = gemm(L_NT, 1, &w, 1, pl.split, gw, pl.gemm, s))) return rc;
+        d.seg[0] = GemmSeg{G16, C, Wp16, C, C};
+    } else {
+        w.seg[0] = GemmSeg{HL, ldhl, X, C, n};
+        if ((rc = gemm(L_TN, 1, &w, 0, pl.split, gw, pl.gemm, s))) return rc;
+        d.seg[0] = GemmSeg{X, C, W_pred, C, C};
+    }
+    if ((rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s))) return rc;
     return gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s);
 }
 

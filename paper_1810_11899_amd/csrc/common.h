@@ -47,6 +47,7 @@ enum KernelClass {
     K_GEMM_TN_BF16,
     K_GEMM_NT_BF16,
     K_SPMM_BF16,
+    K_TRANSPOSE_BF16,
     K_CLASS_COUNT
 };
 const char *class_name(int cls);
@@ -116,9 +117,9 @@ struct GemmProblem {
     int relu;
     uint16_t *C16;      // when set: write bfloat16 (RNE) here instead of C (leading dim ldc)
 };
-// Up to two problems of equal layout in one launch (grouped).  `bf16` selects
-// bfloat16 operands (uint16 bits) instead of float32.  split_k > 1 is only
-// supported for layout TN and needs workspace (gemm_workspace_bytes).
+// Up to two problems of equal layout and equal M, N, K in one launch
+// (grouped).  `bf16` selects bfloat16 operands (uint16 bits) instead of
+// float32.  split_k > 1 needs workspace (gemm_workspace_bytes).
 int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
          void *ws, size_t ws_bytes, hipStream_t s);
 size_t gemm_workspace_bytes(int nprob, const GemmProblem *probs, int split_k);
@@ -145,6 +146,10 @@ int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void
                 hipStream_t s);
 // x[0..count) = 0 with a kernel (no memset nodes, so callers may capture it)
 int fill_zero(float *x, int64_t count, hipStream_t s);
+// dst (cols x rows, ldd) = bf16 of src (rows x cols, lds) transposed; src is
+// float32 or (src_is_bf16) bfloat16 bits
+int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds, uint16_t *dst,
+                   int64_t ldd, hipStream_t s);
 // float32 -> bfloat16 bits (RNE), 2-D with leading dimensions
 int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
              hipStream_t s);

@@ -202,13 +202,80 @@ __global__ __launch_bounds__(256) void loss_reduce_kernel(int32_t nparts, const 
     if (threadIdx.x == 0) *loss = (float)(sh[0] * scale);
 }
 
+// rows on gridDim.y (strided), columns four per thread
 __global__ __launch_bounds__(256) void cvt_bf16_kernel(int64_t rows, int64_t cols, const float *__restrict__ x,
-                                                       int64_t ldx, uint16_t *__restrict__ y, int64_t ldy) {
-    const int64_t total = rows * cols;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
-        const int64_t r = e / cols, c = e % cols;
-        y[r * ldy + c] = f32_to_bf16_rne(x[r * ldx + c]);
+                                                       int64_t ldx, uint16_t *__restrict__ y, int64_t ldy, int vec4) {
+    const int64_t c = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (c >= cols) return;
+    for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
+        const float *xr = x + r * ldx;
+        uint16_t *yr = y + r * ldy;
+        if (vec4 && c + 4 <= cols) {
+            const float4 v = *(const float4 *)(xr + c);
+            const uint32_t lo = (uint32_t)f32_to_bf16_rne(v.x) | ((uint32_t)f32_to_bf16_rne(v.y) << 16);
+            const uint32_t hi = (uint32_t)f32_to_bf16_rne(v.z) | ((uint32_t)f32_to_bf16_rne(v.w) << 16);
+            *(uint2 *)(yr + c) = make_uint2(lo, hi);
+        } else {
+            for (int64_t e = c; e < c + 4 && e < cols; ++e) yr[e] = f32_to_bf16_rne(xr[e]);
+        }
+    }
+}
+
+// dst[c][r] = bf16(src[r][c]) through a 64 x 64 LDS tile.  Reads: each thread
+// takes 4 consecutive source columns of a row; writes: each thread emits 4
+// consecutive destination columns (8 bytes), so both sides stay coalesced.
+template <typename TIn>
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(int64_t rows, int64_t cols, const TIn *__restrict__ src,
+                                                             int64_t lds_, uint16_t *__restrict__ dst, int64_t ldd,
+                                                             int vec) {
+    __shared__ uint16_t tile[64][64 + 4];
+    const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
+    const int tq = threadIdx.x & 15, tr = threadIdx.x >> 4;  // 16 quads x 16 rows
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int rr = tr + 16 * i;
+        const int64_t r = r0 + rr, c = c0 + tq * 4;
+        uint16_t v[4] = {0, 0, 0, 0};
+        if (r < rows) {
+            if (vec && c + 4 <= cols) {
+                if constexpr (sizeof(TIn) == 4) {
+                    const float4 f = *(const float4 *)(src + r * lds_ + c);
+                    v[0] = f32_to_bf16_rne(f.x); v[1] = f32_to_bf16_rne(f.y);
+                    v[2] = f32_to_bf16_rne(f.z); v[3] = f32_to_bf16_rne(f.w);
+                } else {
+                    const uint2 u = *(const uint2 *)(src + r * lds_ + c);
+                    v[0] = (uint16_t)(u.x & 0xFFFF); v[1] = (uint16_t)(u.x >> 16);
+                    v[2] = (uint16_t)(u.y & 0xFFFF); v[3] = (uint16_t)(u.y >> 16);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (c + e < cols) {
+                        if constexpr (sizeof(TIn) == 4) v[e] = f32_to_bf16_rne(src[r * lds_ + c + e]);
+                        else v[e] = (uint16_t)src[r * lds_ + c + e];
+                    }
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tile[rr][tq * 4 + e] = v[e];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int cc = tr + 16 * i;            // destination row = source column
+        const int64_t c = c0 + cc, r = r0 + tq * 4;
+        if (c >= cols) continue;
+        uint16_t v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = tile[tq * 4 + e][cc];
+        uint16_t *o = dst + c * ldd + r;
+        if (vec && r + 4 <= rows) {
+            *(uint2 *)o = make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | ((uint32_t)v[3] << 16));
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (r + e < rows) o[e] = v[e];
+        }
     }
 }
 
@@ -334,14 +401,35 @@ int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void
     return GCN_OK;
 }
 
+int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds_, uint16_t *dst,
+                   int64_t ldd, hipStream_t s) {
+    if (rows <= 0 || cols <= 0) return GCN_OK;
+    ProfScope ps(K_TRANSPOSE_BF16, s, 0.0, (double)rows * cols * (src_is_bf16 ? 4.0 : 6.0));
+    dim3 g((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64));
+    const int esz = src_is_bf16 ? 2 : 4;
+    const int vec = (lds_ % 4 == 0 && ldd % 4 == 0 && ((uintptr_t)src % (4 * esz)) == 0 && ((uintptr_t)dst % 8) == 0)
+                        ? 1 : 0;
+    if (src_is_bf16)
+        hipLaunchKernelGGL(transpose_bf16_kernel<uint16_t>, g, dim3(256), 0, s, rows, cols, (const uint16_t *)src,
+                           lds_, dst, ldd, vec);
+    else
+        hipLaunchKernelGGL(transpose_bf16_kernel<float>, g, dim3(256), 0, s, rows, cols, (const float *)src, lds_,
+                           dst, ldd, vec);
+    GCN_LAUNCH_CHECK("transpose_bf16_kernel");
+    return GCN_OK;
+}
+
 int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
              hipStream_t s) {
     const int64_t total = rows * cols;
     if (total <= 0) return GCN_OK;
-    int64_t g = (total + 255) / 256;
-    if (g > 8192) g = 8192;
+    const int vec4 = (ldx % 4 == 0 && ldy % 4 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 7) == 0) ? 1 : 0;
+    const int64_t gx = (cols + 1023) / 1024;
+    int64_t gy = rows < 65535 ? rows : 65535;
+    if (gx * gy > 16384) gy = (16384 + gx - 1) / gx;
     ProfScope ps(K_CVT_BF16, s, 0.0, (double)total * 6.0);
-    hipLaunchKernelGGL(cvt_bf16_kernel, dim3((unsigned)g), dim3(256), 0, s, rows, cols, x, ldx, y, ldy);
+    hipLaunchKernelGGL(cvt_bf16_kernel, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, s, rows, cols, x, ldx, y,
+                       ldy, vec4);
     GCN_LAUNCH_CHECK("cvt_bf16_kernel");
     return GCN_OK;
 }

@@ -58,20 +58,47 @@ struct DevProblem {
 struct DevArgs {
     DevProblem p[2];
     int nprob;
+    int64_t total;     // logical blocks: splits x tiles_m x nprob x tiles_n
+    int64_t per_xcd;   // ceil(total / 8)
 };
+
+// Workgroups are dispatched round-robin over the 8 XCDs (workgroup b runs on
+// XCD b % 8).  Logical blocks are numbered XCD-major, so that the column tiles
+// of one row block, and the two problems of a grouped launch (which share
+// their row operand in the forward pass), run on the same XCD and its L2
+// serves the shared operand panel.  Order within an XCD: split, row tile,
+// problem, column tile.  Grouped problems have equal M, N and K.
+struct BlockCoord {
+    int pi, split, tm, tn;
+};
+__device__ __forceinline__ bool decode_block(const DevArgs &a, BlockCoord &c) {
+    const int64_t b = blockIdx.x;
+    const int64_t L = (b & 7) * a.per_xcd + (b >> 3);
+    if (L >= a.total) return false;
+    const DevProblem &P = a.p[0];
+    const int64_t row = (int64_t)a.nprob * P.tiles_n;   // logical blocks per row tile
+    const int64_t per_split = (int64_t)P.tiles_m * row;
+    c.split = (int)(L / per_split);
+    int64_t r = L % per_split;
+    c.tm = (int)(r / row);
+    r %= row;
+    c.pi = (int)(r / P.tiles_n);
+    c.tn = (int)(r % P.tiles_n);
+    return true;
+}
 
 // ------------------------------------------------------------------ loading
 // Element type: float (fp32 path) or uint16_t (bf16 bits).
 template <typename T> __device__ __forceinline__ T zero_elem() { return T(0); }
 
-// Tile of one operand, BK x 128 elements, kept k-major in LDS: lds[k][x].
+// Tile of one operand, BK x XT elements, kept k-major in LDS: lds[k][x].
 //   KMAJOR: element (x, k) sits at ptr[k*ld + x]   (contiguous along x)
 //   else  : element (x, k) sits at ptr[x*ld + k]   (contiguous along k)
-template <typename T, int BK, bool KMAJOR, bool VEC>
+template <typename T, int BK, bool KMAJOR, bool VEC, int XT = 128>
 struct TileLoader {
     // 16-byte vectors of T
     static constexpr int E = 16 / sizeof(T);
-    static constexpr int kElems = BK * 128;
+    static constexpr int kElems = BK * XT;
     static constexpr int kVecs = kElems / E;
     static constexpr int kPer = kVecs / kThreads;  // vectors per thread
     static_assert(kPer >= 1, "tile too small");
@@ -81,7 +108,7 @@ struct TileLoader {
     __device__ __forceinline__ void coords(int i, int &x, int &k) const {
         const int v = threadIdx.x + i * kThreads;
         if (KMAJOR) {            // vectors along x
-            constexpr int per_row = 128 / E;
+            constexpr int per_row = XT / E;
             k = v / per_row;
             x = (v % per_row) * E;
         } else {                 // vectors along k
@@ -121,7 +148,7 @@ struct TileLoader {
         }
     }
 
-    __device__ __forceinline__ void store(T (*lds)[128 + PAD]) const {
+    __device__ __forceinline__ void store(T (*lds)[XT + PAD]) const {
 #pragma unroll
         for (int i = 0; i < kPer; ++i) {
             int x, k;
@@ -142,27 +169,36 @@ struct TileLoader {
 #define GCN_GEMM_BK 16
 #endif
 constexpr int kBK = GCN_GEMM_BK;  // K depth of one LDS stage
+#ifndef GCN_GEMM_TBM
+#define GCN_GEMM_TBM 128
+#endif
+#ifndef GCN_GEMM_TBN
+#define GCN_GEMM_TBN 128
+#endif
+constexpr int kTBM = GCN_GEMM_TBM;  // float32 block tile (M x N), 2 x 2 wavefronts
+constexpr int kTBN = GCN_GEMM_TBN;
 
-template <int LAYOUT, bool VEC>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
+#ifndef GCN_GEMM_WAVES_PER_EU
+#define GCN_GEMM_WAVES_PER_EU 4
+#endif
+template <int LAYOUT, bool VEC, int TBM, int TBN>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(GCN_GEMM_WAVES_PER_EU)))
+void gemm_kernel(DevArgs args) {
     using T = float;
     constexpr int BK = kBK;
     constexpr bool A_KMAJOR = (LAYOUT == L_TN);
     constexpr bool B_KMAJOR = (LAYOUT != L_NT);
-    __shared__ __attribute__((aligned(16))) T As[2][BK][128 + PAD];
-    __shared__ __attribute__((aligned(16))) T Bs[2][BK][128 + PAD];
+    constexpr int WTM = TBM / 2, WTN = TBN / 2;     // wavefront tile (2 x 2 wavefronts)
+    constexpr int FM = WTM / 32, FN = WTN / 32;     // 32x32 accumulator blocks per wavefront
+    __shared__ __attribute__((aligned(16))) T As[2][BK][TBM + PAD];
+    __shared__ __attribute__((aligned(16))) T Bs[2][BK][TBN + PAD];
 
     // ---- which problem / split / tile
-    int64_t blk = blockIdx.x;
-    const int pi = (args.nprob > 1 && blk >= args.p[1].block_begin) ? 1 : 0;
-    const DevProblem &P = args.p[pi];
-    blk -= P.block_begin;
-    const int64_t tiles = (int64_t)P.tiles_m * P.tiles_n;
-    const int split = (int)(blk / tiles);
-    const int64_t t = blk % tiles;
-    const int tm = (int)(t / P.tiles_n);
-    const int tn = (int)(t % P.tiles_n);
-    const int m0 = tm * BM, n0 = tn * BN;
+    BlockCoord bc;
+    if (!decode_block(args, bc)) return;
+    const DevProblem &P = args.p[bc.pi];
+    const int split = bc.split;
+    const int m0 = bc.tm * TBM, n0 = bc.tn * TBN;
     const int kt_begin = split * P.kt_per_split;
     int kt_end = kt_begin + P.kt_per_split;
     if (kt_end > P.kt_total) kt_end = P.kt_total;
@@ -171,8 +207,8 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
     const int wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    TileLoader<T, BK, A_KMAJOR, VEC> la;
-    TileLoader<T, BK, B_KMAJOR, VEC> lb;
+    TileLoader<T, BK, A_KMAJOR, VEC, TBM> la;
+    TileLoader<T, BK, B_KMAJOR, VEC, TBN> lb;
 
     auto load = [&](int kt) {
         const int sg = kt < P.s.kt[0] ? 0 : 1;
@@ -183,11 +219,11 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
         lb.load(B, P.s.ldb[sg], n0, P.N, kk, P.s.K[sg]);
     };
 
-    floatx16 acc[2][2];
+    floatx16 acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
@@ -200,29 +236,31 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
         if (kt + 1 < kt_end) load(kt + 1);
         // operands of the next k-step are read from LDS while the matrix
         // cores work on the current one
-        float a[2], b[2];
+        float a[FM], b[FN];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = As[buf][(lane >> 5)][wm * 64 + i * 32 + (lane & 31)];
+        for (int i = 0; i < FM; ++i) a[i] = As[buf][(lane >> 5)][wm * WTM + i * 32 + (lane & 31)];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) b[j] = Bs[buf][(lane >> 5)][wn * 64 + j * 32 + (lane & 31)];
+        for (int j = 0; j < FN; ++j) b[j] = Bs[buf][(lane >> 5)][wn * WTN + j * 32 + (lane & 31)];
 #pragma unroll
         for (int kk = 0; kk < BK; kk += 2) {
-            float an[2], bn[2];
+            float an[FM], bn[FN];
             if (kk + 2 < BK) {
                 const int kr = kk + 2 + (lane >> 5);
 #pragma unroll
-                for (int i = 0; i < 2; ++i) an[i] = As[buf][kr][wm * 64 + i * 32 + (lane & 31)];
+                for (int i = 0; i < FM; ++i) an[i] = As[buf][kr][wm * WTM + i * 32 + (lane & 31)];
 #pragma unroll
-                for (int j = 0; j < 2; ++j) bn[j] = Bs[buf][kr][wn * 64 + j * 32 + (lane & 31)];
+                for (int j = 0; j < FN; ++j) bn[j] = Bs[buf][kr][wn * WTN + j * 32 + (lane & 31)];
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
             if (kk + 2 < BK) {
 #pragma unroll
-                for (int i = 0; i < 2; ++i) { a[i] = an[i]; b[i] = bn[i]; }
+                for (int i = 0; i < FM; ++i) a[i] = an[i];
+#pragma unroll
+                for (int j = 0; j < FN; ++j) b[j] = bn[j];
             }
         }
         buf ^= 1;
@@ -234,15 +272,15 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
     float *dst = to_partial ? P.partial + (int64_t)split * P.M * P.N : P.C;
     const int64_t ldd = to_partial ? P.N : P.ldc;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+        for (int j = 0; j < FN; ++j) {
+            const int col = n0 + wn * WTN + j * 32 + (lane & 31);
             if (col >= P.N) continue;
             const float bv = (!to_partial && P.bias) ? P.bias[col] : 0.0f;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                 if (row < P.M) {
                     float v = acc[i][j][r];
                     if (!to_partial) {
@@ -263,20 +301,35 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(DevArgs args) {
 // groups.  Operands that are contiguous along k in memory are copied as
 // 16-byte vectors; operands contiguous along the row index are transposed on
 // the way into LDS.
-constexpr int BK16 = 32;
+#ifndef GCN_BF16_BK
+#define GCN_BF16_BK 32
+#endif
+#ifndef GCN_BF16_TBM
+#define GCN_BF16_TBM 128
+#endif
+#ifndef GCN_BF16_TBN
+#define GCN_BF16_TBN 128
+#endif
+#ifndef GCN_BF16_WAVES_PER_EU
+#define GCN_BF16_WAVES_PER_EU 4
+#endif
+constexpr int BK16 = GCN_BF16_BK;
 constexpr int LDK16 = BK16 + 8;
+constexpr int kTBM16 = GCN_BF16_TBM;
+constexpr int kTBN16 = GCN_BF16_TBN;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-template <bool KMAJOR, bool VEC>
+template <bool KMAJOR, bool VEC, int XT>
 struct TileLoader16 {
-    static constexpr int kPer = (BK16 * 128 / 8) / kThreads;  // 16-byte vectors per thread
+    static constexpr int kPer = (BK16 * XT / 8) / kThreads;  // 16-byte vectors per thread
+    static_assert(kPer >= 1, "tile too small");
     uint4 reg[kPer];
 
     __device__ __forceinline__ void coords(int i, int &x, int &k) const {
         const int v = threadIdx.x + i * kThreads;
         if (KMAJOR) {   // vectors along x
-            k = v / 16;
-            x = (v % 16) * 8;
+            k = v / (XT / 8);
+            x = (v % (XT / 8)) * 8;
         } else {        // vectors along k
             x = v / (BK16 / 8);
             k = (v % (BK16 / 8)) * 8;
@@ -333,22 +386,20 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
 }
 
 template <int LAYOUT, bool VEC>
-__global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(DevArgs args) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(GCN_BF16_WAVES_PER_EU)))
+void gemm_bf16_kernel(DevArgs args) {
     constexpr bool A_KMAJOR = (LAYOUT == L_TN);
     constexpr bool B_KMAJOR = (LAYOUT != L_NT);
-    __shared__ __attribute__((aligned(16))) uint16_t As[2][128][LDK16];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][128][LDK16];
+    constexpr int WTM = kTBM16 / 2, WTN = kTBN16 / 2;
+    constexpr int FM = WTM / 32, FN = WTN / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t As[2][kTBM16][LDK16];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[2][kTBN16][LDK16];
 
-    int64_t blk = blockIdx.x;
-    const int pi = (args.nprob > 1 && blk >= args.p[1].block_begin) ? 1 : 0;
-    const DevProblem &P = args.p[pi];
-    blk -= P.block_begin;
-    const int64_t tiles = (int64_t)P.tiles_m * P.tiles_n;
-    const int split = (int)(blk / tiles);
-    const int64_t t = blk % tiles;
-    const int tm = (int)(t / P.tiles_n);
-    const int tn = (int)(t % P.tiles_n);
-    const int m0 = tm * BM, n0 = tn * BN;
+    BlockCoord bc;
+    if (!decode_block(args, bc)) return;
+    const DevProblem &P = args.p[bc.pi];
+    const int split = bc.split;
+    const int m0 = bc.tm * kTBM16, n0 = bc.tn * kTBN16;
     const int kt_begin = split * P.kt_per_split;
     int kt_end = kt_begin + P.kt_per_split;
     if (kt_end > P.kt_total) kt_end = P.kt_total;
@@ -357,8 +408,8 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(DevArgs args) {
     const int wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    TileLoader16<A_KMAJOR, VEC> la;
-    TileLoader16<B_KMAJOR, VEC> lb;
+    TileLoader16<A_KMAJOR, VEC, kTBM16> la;
+    TileLoader16<B_KMAJOR, VEC, kTBN16> lb;
     auto load = [&](int kt) {
         const int sg = kt < P.s.kt[0] ? 0 : 1;
         const int kk = (sg == 0 ? kt : kt - P.s.kt[0]) * BK16;
@@ -366,11 +417,11 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(DevArgs args) {
         lb.load((const uint16_t *)P.s.B[sg], P.s.ldb[sg], n0, P.N, kk, P.s.K[sg]);
     };
 
-    floatx16 acc[2][2];
+    floatx16 acc[FM][FN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
@@ -384,17 +435,17 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(DevArgs args) {
         if (kt + 1 < kt_end) load(kt + 1);
 #pragma unroll
         for (int kk = 0; kk < BK16; kk += 16) {
-            bf16x8 a[2], b[2];
+            bf16x8 a[FM], b[FN];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
-                a[i] = *(const bf16x8 *)&As[buf][wm * 64 + i * 32 + (lane & 31)][kk + koff];
+            for (int i = 0; i < FM; ++i)
+                a[i] = *(const bf16x8 *)&As[buf][wm * WTM + i * 32 + (lane & 31)][kk + koff];
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                b[j] = *(const bf16x8 *)&Bs[buf][wn * 64 + j * 32 + (lane & 31)][kk + koff];
+            for (int j = 0; j < FN; ++j)
+                b[j] = *(const bf16x8 *)&Bs[buf][wn * WTN + j * 32 + (lane & 31)][kk + koff];
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
         buf ^= 1;
@@ -404,15 +455,15 @@ __global__ __launch_bounds__(kThreads) void gemm_bf16_kernel(DevArgs args) {
     float *dst = to_partial ? P.partial + (int64_t)split * P.M * P.N : P.C;
     const int64_t ldd = to_partial ? P.N : P.ldc;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+        for (int j = 0; j < FN; ++j) {
+            const int col = n0 + wn * WTN + j * 32 + (lane & 31);
             if (col >= P.N) continue;
             const float bv = (!to_partial && P.bias) ? P.bias[col] : 0.0f;
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int row = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                const int row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                 if (row < P.M) {
                     float v = acc[i][j][r];
                     if (!to_partial) {
@@ -462,7 +513,9 @@ bool vec_ok(int layout, const GemmProblem &g, int esz) {
     return true;
 }
 
-int bk_of(int bf16) { return bf16 ? 32 : kBK; }
+int bk_of(int bf16) { return bf16 ? BK16 : kBK; }
+int tile_m_of(int bf16) { return bf16 ? kTBM16 : kTBM; }
+int tile_n_of(int bf16) { return bf16 ? kTBN16 : kTBN; }
 
 void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k, float *partial,
               DevArgs &a, int64_t &blocks) {
@@ -475,8 +528,8 @@ void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int spl
         DevProblem &d = a.p[i];
         d.M = g.M;
         d.N = g.N;
-        d.tiles_m = (g.M + BM - 1) / BM;
-        d.tiles_n = (g.N + BN - 1) / BN;
+        d.tiles_m = (g.M + tile_m_of(bf16) - 1) / tile_m_of(bf16);
+        d.tiles_n = (g.N + tile_n_of(bf16) - 1) / tile_n_of(bf16);
         d.kt_total = 0;
         for (int s = 0; s < 2; ++s) {
             d.s.A[s] = g.seg[s].A;
@@ -506,6 +559,9 @@ void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int spl
         }
     }
     if (nprob < 2) a.p[1] = a.p[0];
+    a.total = (int64_t)a.p[0].split * a.p[0].tiles_m * nprob * a.p[0].tiles_n;
+    a.per_xcd = (a.total + 7) / 8;
+    blocks = a.total > 0 ? 8 * a.per_xcd : 0;
 }
 
 template <int LAYOUT>
@@ -516,9 +572,9 @@ void launch(bool vec, bool bf16, dim3 grid, hipStream_t s, const DevArgs &a) {
         else
             hipLaunchKernelGGL((gemm_bf16_kernel<LAYOUT, false>), grid, dim3(kThreads), 0, s, a);
     } else if (vec) {
-        hipLaunchKernelGGL((gemm_kernel<LAYOUT, true>), grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<LAYOUT, true, kTBM, kTBN>), grid, dim3(kThreads), 0, s, a);
     } else {
-        hipLaunchKernelGGL((gemm_kernel<LAYOUT, false>), grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL((gemm_kernel<LAYOUT, false, kTBM, kTBN>), grid, dim3(kThreads), 0, s, a);
     }
 }
 
@@ -527,7 +583,7 @@ void launch(bool vec, bool bf16, dim3 grid, hipStream_t s, const DevArgs &a) {
 int gemm_pick_split(int nprob, const GemmProblem *probs) {
     int64_t tiles = 0, kt = 0;
     for (int i = 0; i < nprob; ++i) {
-        tiles += (int64_t)((probs[i].M + BM - 1) / BM) * ((probs[i].N + BN - 1) / BN);
+        tiles += (int64_t)((probs[i].M + kTBM - 1) / kTBM) * ((probs[i].N + kTBN - 1) / kTBN);
         int64_t k = 0;
         for (int s = 0; s < 2; ++s) k += (probs[i].seg[s].K + kBK - 1) / kBK;
         if (k > kt) kt = k;
@@ -554,8 +610,9 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         set_error("gemm: nprob %d", nprob);
         return GCN_EINVAL;
     }
-    if (split_k > 1 && layout != L_TN) {
-        set_error("gemm: split-K only for the TN layout");
+    if (nprob == 2 && (probs[0].M != probs[1].M || probs[0].N != probs[1].N ||
+                       probs[0].seg[0].K + probs[0].seg[1].K != probs[1].seg[0].K + probs[1].seg[1].K)) {
+        set_error("gemm: grouped problems must have equal M, N and K");
         return GCN_EINVAL;
     }
     bool vec = true;
@@ -576,6 +633,10 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     int64_t blocks = 0;
     fill_dev(layout, nprob, probs, bf16, split_k, partial, a, blocks);
     if (blocks == 0) return GCN_OK;
+    if (nprob == 2 && (a.p[0].kt_total != a.p[1].kt_total || a.p[0].split != a.p[1].split)) {
+        set_error("gemm: grouped problems must have the same K-tiling");
+        return GCN_EINVAL;
+    }
     bool any_split = false;
     for (int i = 0; i < nprob; ++i) any_split = any_split || a.p[i].split > 1;
     int cls = layout == L_NN ? K_GEMM_NN : (layout == L_TN ? K_GEMM_TN : K_GEMM_NT);

@@ -190,9 +190,17 @@ __global__ __launch_bounds__(kTB) void bounds_kernel(int32_t n_cols, int32_t nnz
     t_indptr[j] = (int32_t)lo;
 }
 
+// rowid[p] = the row of A that holds entry p (one wavefront per row)
+__global__ __launch_bounds__(kTB) void rowid_kernel(int32_t n_rows, const int32_t *__restrict__ indptr,
+                                                    int32_t *__restrict__ rowid) {
+    const int64_t r = (int64_t)blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
+    if (r >= n_rows) return;
+    const int32_t b = indptr[r], e = indptr[r + 1];
+    for (int32_t p = b + (int32_t)(threadIdx.x & 63); p < e; p += 64) rowid[p] = (int32_t)r;
+}
+
 // t_indices[q] = row of entry perm[q] in A;  t_vals[q] = vals[perm[q]]
-__global__ __launch_bounds__(kTB) void finalize_kernel(int32_t n_rows, int32_t nnz,
-                                                       const int32_t *__restrict__ indptr,
+__global__ __launch_bounds__(kTB) void finalize_kernel(int32_t nnz, const int32_t *__restrict__ rowid,
                                                        const float *__restrict__ vals,
                                                        const int32_t *__restrict__ perm,
                                                        int32_t *__restrict__ t_indices,
@@ -200,13 +208,7 @@ __global__ __launch_bounds__(kTB) void finalize_kernel(int32_t n_rows, int32_t n
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < nnz; q += stride) {
         const int32_t p = perm[q];
-        // last row i with indptr[i] <= p
-        int64_t lo = 0, hi = n_rows;  // answer in [0, n_rows)
-        while (lo < hi) {
-            const int64_t mid = (lo + hi + 1) >> 1;
-            if (indptr[mid] <= p) lo = mid; else hi = mid - 1;
-        }
-        t_indices[q] = (int32_t)lo;
+        t_indices[q] = rowid[p];
         t_vals[q] = vals[p];
     }
 }
@@ -301,9 +303,12 @@ int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *in
         GCN_LAUNCH_CHECK("bounds_kernel");
     }
     {
-        ProfScope ps(K_T_FINAL, s, 0.0, (double)nnz * 16.0);
-        hipLaunchKernelGGL(finalize_kernel, dim3(g), dim3(kTB), 0, s, n_rows, nnz, indptr, vals, va, t_indices,
-                           t_vals);
+        // the spare key buffer holds the row of every entry
+        int32_t *rowid = (int32_t *)kb;
+        ProfScope ps(K_T_FINAL, s, 0.0, (double)nnz * 20.0);
+        hipLaunchKernelGGL(rowid_kernel, dim3((unsigned)((n_rows + kTB / 64 - 1) / (kTB / 64))), dim3(kTB), 0, s,
+                           n_rows, indptr, rowid);
+        hipLaunchKernelGGL(finalize_kernel, dim3(g), dim3(kTB), 0, s, nnz, rowid, vals, va, t_indices, t_vals);
         GCN_LAUNCH_CHECK("finalize_kernel");
     }
     return GCN_OK;
