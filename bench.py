@@ -12,7 +12,8 @@ resident in HBM.  Prints one JSON line.
                nnz x width, divided by the step time)
   roofline     the kernel class with the most time in the timed region, timed
                with HIP events on its launch stream (library profiler)
-  cpu_baseline the CPU oracle on a bounded sample of the same workload family
+  cpu_baseline the CPU oracle on the same workload, whole steps timed for at
+               least --cpu-seconds on the host's cores
 """
 import argparse
 import hashlib
@@ -31,17 +32,22 @@ PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
 
-def kernel_source_hash() -> str:
+KERNEL_SOURCES = {"gemm": ["gemm.hip", "common.h"], "spmm": ["spmm.hip", "common.h"]}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    """Hash of the source files the kernel class is built from."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1810_11899_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".cpp", ".h")):
-            h.update(open(os.path.join(csrc, f), "rb").read())
+    for f in KERNEL_SOURCES["gemm" if kernel.startswith("gemm") else "spmm"]:
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 
-def traffic_for(kernel: str, config: str, launches_per_step: float):
-    """HBM bytes per launch from the committed counter runs, if still current."""
+def traffic_for(kernel: str, config: str):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated) from the
+    committed counter runs, or None when they are missing or the kernel's
+    source has changed since they were taken."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     try:
@@ -49,14 +55,16 @@ def traffic_for(kernel: str, config: str, launches_per_step: float):
     except (OSError, ValueError):
         return None
     e = t.get(config, {}).get(kernel)
-    if not e or e.get("source_hash") != kernel_source_hash():
+    if not e or e.get("source_hash") != kernel_source_hash(kernel):
         return None
     return e.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg: int, n_sample: int, synth, step_work, B):
+def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_reps: int = 20):
+    """The CPU oracle on the same workload: whole fwd+bwd steps, repeated until
+    at least `min_seconds` of CPU work have been timed (bounded by max_reps)."""
     import oracle
-    wl = synth.config(cfg, n=n_sample)
+    wl = synth.config(cfg)
     L = len(wl.layers)
     dims = [(l.f_in, l.h) for l in wl.layers]
     need = [li > 0 for li in range(L)] if L > 1 else [True]
@@ -64,14 +72,16 @@ def cpu_baseline(cfg: int, n_sample: int, synth, step_work, B):
     work = step_work(wl.n, wl.graph.nnz, dims, orders, need,
                      wl.spec.classes if wl.spec.head else 0)
     oracle.step(synth.config(cfg, n=1024))  # warm the thread pool on a tiny instance
-    t0 = time.perf_counter()
-    oracle.step(wl)
-    dt = time.perf_counter() - t0
-    return {"value": work["edge_features"] / dt, "unit": "edge-features/s", "cores": oracle.num_threads(),
+    reps, dt = 0, 0.0
+    while reps < max_reps and (reps == 0 or dt < min_seconds):
+        t0 = time.perf_counter()
+        oracle.step(wl)
+        dt += time.perf_counter() - t0
+        reps += 1
+    return {"value": work["edge_features"] * reps / dt, "unit": "edge-features/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"one full fwd+bwd step of the same workload family (generator, degree, widths, "
-                      f"head) at n={wl.n} vertices, nnz={wl.graph.nnz}; {dt:.2f} s; oracle work is "
-                      f"linear in n at fixed degree and widths"}
+            "sample": f"{reps} full fwd+bwd step(s) of the same workload (n={wl.n}, nnz={wl.graph.nnz}), "
+                      f"{dt:.1f} s in total; float64 oracle, OpenMP aggregation + BLAS dense products"}
 
 
 def main():
@@ -81,7 +91,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--prec", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--cpu-sample-n", type=int, default=32768)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event timing")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -140,7 +150,7 @@ def main():
 
     kernels = {}
     roof = None
-    config_name = spec.name
+    config_name = spec.name + ("" if args.prec == "f32" else "_bf16")
     if not args.no_profile:
         prof = B.gcn_profile_read_all()
         for name, (ms, launches, flops, bytes_) in prof.items():
@@ -166,7 +176,7 @@ def main():
                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
         roof["avg_launch_ms"] = round(per_launch_ms, 4)
         roof["launches_per_step"] = launches / args.steps
-        roof["traffic"] = traffic_for(name, config_name, launches / args.steps)
+        roof["traffic"] = traffic_for(name, config_name)
         spm = prof.get("spmm")
         if spm and spm[1]:
             kernels["spmm"]["hbm_frac_gather_model"] = round(spm[3] / (spm[0] / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
@@ -187,7 +197,7 @@ def main():
         "roofline": roof, "kernels": kernels,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_sample_n, synth, step_work, B)
+        out["cpu_baseline"] = cpu_baseline(args.config, synth, step_work, B, min_seconds=args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
