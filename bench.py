@@ -84,6 +84,51 @@ def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_r
                       f"{dt:.1f} s in total; float64 oracle, OpenMP aggregation + BLAS dense products"}
 
 
+def measure_peaks(B, torch) -> dict:
+    """Measured ceilings next to the datasheet ones: a streaming read of a
+    2 GiB array and back-to-back matrix-core products (gcn_peaks.h), each the
+    best of a few launch shapes, timed with events on the launch stream."""
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, reps):
+        fn()
+        a, b = ev(), ev()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    n = (2 << 30) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    sink = torch.empty(256 * 16384, dtype=torch.float32, device="cuda")
+    best_bw, best_blocks = 0.0, 0
+    for blocks in (2048, 4096, 8192, 16384):
+        ms = timed(lambda: B.gcn_peak_stream_read(x, sink, blocks), 5)
+        bw = n * 4 / (ms / 1e3) / 1e9
+        if bw > best_bw:
+            best_bw, best_blocks = bw, blocks
+    del x
+    out = {"stream_read_gbs": round(best_bw, 1), "stream_read_blocks": best_blocks}
+    for prec, iters in (("f32", 4000), ("bf16", 4000)):
+        best, bb = 0.0, 0
+        for blocks in (256, 512, 1024):
+            fl = [0.0]
+
+            def run():
+                fl[0] = B.gcn_peak_mfma(B.PREC[prec], blocks, iters, sink)
+            ms = timed(run, 3)
+            tf = fl[0] / (ms / 1e3) / 1e12
+            if tf > best:
+                best, bb = tf, blocks
+        out[f"mfma_{prec}_tflops"] = round(best, 1)
+        out[f"mfma_{prec}_blocks"] = bb
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -94,6 +139,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event timing")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured machine ceilings")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for counter calibration)")
     args = ap.parse_args()
@@ -196,6 +242,13 @@ def main():
         "edge_features_per_step": work["edge_features"], "gemm_gflop_per_step": work["gemm_flops"] / 1e9,
         "roofline": roof, "kernels": kernels,
     }
+    if not args.no_peaks:
+        peaks = measure_peaks(B, torch)
+        out["measured_peaks"] = peaks
+        if roof is not None:
+            key = "stream_read_gbs" if roof["bound"] == "hbm" else f"mfma_{args.prec}_tflops"
+            roof["measured_peak"] = peaks[key]
+            roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.config, synth, step_work, B, min_seconds=args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -1,0 +1,43 @@
+/*
+ * gcn_peaks.h -- machine-rate probes of libgcnlayer.
+ *
+ * These two calls do none of the method's arithmetic.  They measure what this
+ * GPU sustains for the two resources the layer's kernels are bound by:
+ * streaming reads from device memory (the aggregation of Sec. V-A/V-B is
+ * bandwidth bound) and the matrix cores (the weight application of Sec. V-A is
+ * a dense product).  Kernel rates are reported against both the datasheet peak
+ * and these measured ceilings.
+ *
+ * Both calls only enqueue one kernel on `stream` (a hipStream_t as void*,
+ * NULL = default stream); the caller times it with events on that stream.
+ * Errors follow gcn_layer.h: a negative gcn_status with a message for
+ * gcn_last_error(), nothing launched.
+ */
+#ifndef GCN_PEAKS_H_
+#define GCN_PEAKS_H_
+
+#include <stdint.h>
+
+#include "gcn_layer.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Reads every element of the device array x [count] once with 16-byte loads
+ * (count % 4 == 0, x 16-byte aligned) and writes one float per thread to the
+ * device array sink [blocks * 256].  Bytes moved: 4 * count read. */
+int gcn_peak_stream_read(const float *x, int64_t count, float *sink, int32_t blocks, void *stream);
+
+/* Runs `iters` x 4 independent matrix-core products per wavefront, 4
+ * wavefronts per block, on `blocks` blocks: v_mfma_f32_32x32x2f32 for GCN_F32,
+ * v_mfma_f32_32x32x16_bf16 for GCN_BF16.  Writes one float per thread to
+ * sink [blocks * 256] and the number of floating-point operations issued to
+ * *flops (host pointer, may be NULL). */
+int gcn_peak_mfma(gcn_prec prec, int32_t blocks, int32_t iters, float *sink, double *flops, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GCN_PEAKS_H_ */

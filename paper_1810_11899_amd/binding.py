@@ -68,6 +68,9 @@ _SIGNATURES = {
     "gcn_profile_read": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_double)]),
+    # gcn_peaks.h
+    "gcn_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _I32, _P]),
+    "gcn_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I32, _I32, _P, ctypes.POINTER(ctypes.c_double), _P]),
 }
 
 
@@ -279,3 +282,25 @@ def gcn_profile_read_all():
                "gcn_profile_read")
         out[L.gcn_profile_class_name(c).decode()] = (ms.value, n.value, fl.value, by.value)
     return out
+
+
+# ------------------------------------------------------------ peak probes
+def gcn_peak_stream_read(x: torch.Tensor, sink: torch.Tensor, blocks: int, stream=None):
+    """Enqueue one streaming read of every element of the float32 tensor x."""
+    _dev_f32(x, "x")
+    _dev_f32(sink, "sink")
+    if sink.numel() < blocks * 256:
+        raise ValueError("sink needs blocks * 256 floats")
+    _check(lib().gcn_peak_stream_read(_ptr(x), x.numel(), _ptr(sink), blocks, _stream(stream)),
+           "gcn_peak_stream_read")
+
+
+def gcn_peak_mfma(prec: int, blocks: int, iters: int, sink: torch.Tensor, stream=None) -> float:
+    """Enqueue the matrix-core probe; returns the floating-point operations it issues."""
+    _dev_f32(sink, "sink")
+    if sink.numel() < blocks * 256:
+        raise ValueError("sink needs blocks * 256 floats")
+    fl = ctypes.c_double(0.0)
+    _check(lib().gcn_peak_mfma(prec, blocks, iters, _ptr(sink), ctypes.byref(fl), _stream(stream)),
+           "gcn_peak_mfma")
+    return fl.value
