@@ -45,7 +45,7 @@ from typing import List, Optional
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "gcnref_aggregate.c")
+_SRCS = [os.path.join(_HERE, "gcnref_aggregate.c"), os.path.join(_HERE, "gcnref_sampler.c")]
 _LIB_PATH = os.path.join(_HERE, "libgcnref.so")
 _lib = None
 
@@ -55,7 +55,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared",
-                               "-o", tmp, _SRC])
+                               "-o", tmp] + _SRCS)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
 
