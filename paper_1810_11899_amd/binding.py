@@ -34,6 +34,13 @@ class gcn_csr(ctypes.Structure):
                 ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p), ("vals", ctypes.c_void_p)]
 
 
+class gcn_sampler_params(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int32), ("n", ctypes.c_int32), ("db_entries", ctypes.c_int32),
+                ("ia_slots", ctypes.c_int32), ("cap", ctypes.c_int32), ("seed", ctypes.c_uint64)]
+
+
+SAMPLE_STATUS = {0: "ok", 1: "exhausted", 2: "overflow", 3: "probe_limit", 4: "root_limit", 5: "bad_graph"}
+
 _lib = None
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -68,6 +75,15 @@ _SIGNATURES = {
     "gcn_profile_read": (ctypes.c_int, [ctypes.c_int, ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double),
                                         ctypes.POINTER(ctypes.c_double)]),
+    # gcn_sampler.h
+    "gcn_sampler_plan": (ctypes.c_int, [_I32, _P, _I32, _I32, ctypes.c_double, _I32, ctypes.c_uint64,
+                                        ctypes.POINTER(gcn_sampler_params)]),
+    "gcn_frontier_sample": (ctypes.c_int, [_CSRP, ctypes.POINTER(gcn_sampler_params), _I64, _I32, _P, _P, _P,
+                                           _P]),
+    "gcn_induce_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
+    "gcn_induce_subgraphs": (ctypes.c_int, [_CSRP, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P,
+                                            _SZ, _P]),
+    "gcn_gather_rows": (ctypes.c_int, [_P, _I32, _I32, _I64, _P, _I32, _P, _I64, _P]),
     # gcn_peaks.h
     "gcn_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _I32, _P]),
     "gcn_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I32, _I32, _P, ctypes.POINTER(ctypes.c_double), _P]),
@@ -260,6 +276,86 @@ def gcn_f32_to_bf16(x: torch.Tensor, stream=None) -> torch.Tensor:
     y = torch.empty(x.shape, dtype=torch.int16, device=x.device)
     _check(lib().gcn_f32_to_bf16(_ptr(x), _ptr(y), x.numel(), _stream(stream)), "gcn_f32_to_bf16")
     return y
+
+
+# ----------------------------------------------------------------- sampling
+def gcn_sampler_plan(indptr_host, m: int, n: int, eta: float = 2.0, cap: int = 0,
+                     seed: int = 0) -> gcn_sampler_params:
+    """Dashboard / Index-Array sizes for G's row pointer (host array)."""
+    import numpy as np
+    ip = np.ascontiguousarray(indptr_host, dtype=np.int32)
+    p = gcn_sampler_params()
+    _check(lib().gcn_sampler_plan(int(ip.size - 1), ip.ctypes.data, m, n, float(eta), cap,
+                                  seed & (2 ** 64 - 1), ctypes.byref(p)), "gcn_sampler_plan")
+    return p
+
+
+def gcn_frontier_sample(G: DeviceCSR, params: gcn_sampler_params, first_sampler: int, S: int,
+                        vertices=None, counts=None, status=None, stream=None):
+    """S frontier-sampling runs; returns (vertices [S x n], counts [S], status [S]) device tensors."""
+    d = G.indptr.device
+    n = params.n
+    if vertices is None:
+        vertices = torch.empty((max(S, 1), n), dtype=torch.int32, device=d)
+    if counts is None:
+        counts = torch.empty(max(S, 1), dtype=torch.int32, device=d)
+    if status is None:
+        status = torch.empty(max(S, 1), dtype=torch.int32, device=d)
+    if vertices.dtype != torch.int32 or vertices.numel() < S * n or counts.numel() < S or status.numel() < S:
+        raise ValueError("vertices [S x n], counts [S] and status [S] int32 tensors are needed")
+    g = G.struct()
+    _check(lib().gcn_frontier_sample(ctypes.byref(g), ctypes.byref(params), int(first_sampler), int(S),
+                                     _ptr(vertices), _ptr(counts), _ptr(status), _stream(stream)),
+           "gcn_frontier_sample")
+    return vertices, counts, status
+
+
+class InducedBatch:
+    """Device outputs of gcn_induce_subgraphs for S vertex lists of length n."""
+
+    def __init__(self, S: int, n: int, edge_capacity: int, device):
+        self.S, self.n = S, n
+        d = torch.device(device)
+        self.n_sub = torch.empty(max(S, 1), dtype=torch.int32, device=d)
+        self.vsub = torch.empty((max(S, 1), max(n, 1)), dtype=torch.int32, device=d)
+        self.indptr = torch.empty((max(S, 1), n + 1), dtype=torch.int32, device=d)
+        self.edge_offsets = torch.empty(S + 1, dtype=torch.int64, device=d)
+        self.edge_capacity = int(edge_capacity)
+        self.indices = torch.empty(max(self.edge_capacity, 1), dtype=torch.int32, device=d)
+        self.vals = torch.empty(max(self.edge_capacity, 1), dtype=torch.float32, device=d)
+        self.status = torch.empty(1, dtype=torch.int32, device=d)
+
+    def csr(self, s: int, n_sub: int, e0: int, e1: int) -> DeviceCSR:
+        """Subgraph s as a DeviceCSR (host copies of n_sub / edge offsets given)."""
+        return DeviceCSR(n_sub, n_sub, self.indptr[s, :n_sub + 1], self.indices[e0:e1], self.vals[e0:e1])
+
+
+def gcn_induce_subgraphs(G: DeviceCSR, vertices: torch.Tensor, counts: torch.Tensor, out: InducedBatch,
+                         ws: Workspace, stream=None):
+    L = lib()
+    S, n = out.S, out.n
+    need = L.gcn_induce_workspace_bytes(G.n_rows, n, S)
+    w, wb = ws.args(need)
+    g = G.struct()
+    _check(L.gcn_induce_subgraphs(ctypes.byref(g), S, n, _ptr(vertices), _ptr(counts), _ptr(out.n_sub),
+                                  _ptr(out.vsub), _ptr(out.indptr), _ptr(out.edge_offsets), _ptr(out.indices),
+                                  _ptr(out.vals), out.edge_capacity, _ptr(out.status), w, wb, _stream(stream)),
+           "gcn_induce_subgraphs")
+    return out
+
+
+def gcn_gather_rows(X: torch.Tensor, rows: torch.Tensor, count: int, out: torch.Tensor, stream=None):
+    """out[:count] = X[rows[:count]] for 4-byte tensors (float32 rows or int32 labels)."""
+    if X.element_size() != 4 or out.element_size() != 4 or rows.dtype != torch.int32:
+        raise TypeError("4-byte X / out and int32 rows are needed")
+    X2 = X if X.dim() == 2 else X.view(-1, 1)
+    o2 = out if out.dim() == 2 else out.view(-1, 1)
+    width = int(X2.shape[1])
+    if int(o2.shape[1]) != width or o2.shape[0] < count or rows.numel() < count:
+        raise ValueError("shape mismatch")
+    _check(lib().gcn_gather_rows(_ptr(X2), int(X2.shape[0]), width, _ld(X2), _ptr(rows), int(count), _ptr(o2),
+                                 _ld(o2), _stream(stream)), "gcn_gather_rows")
+    return out
 
 
 # ---------------------------------------------------------------- profiling

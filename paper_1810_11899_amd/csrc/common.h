@@ -48,6 +48,9 @@ enum KernelClass {
     K_GEMM_NT_BF16,
     K_SPMM_BF16,
     K_TRANSPOSE_BF16,
+    K_SAMPLE,
+    K_INDUCE,
+    K_GATHER,
     K_CLASS_COUNT
 };
 const char *class_name(int cls);

@@ -1,0 +1,687 @@
+// Graph sampling and GCN construction on the sample (Sec. IV; Alg. 1-5):
+//
+//   frontier_kernel  frontier sampling with the Dashboard (Sec. IV-A/IV-B,
+//                    Alg. 2-4); one wavefront per sampler instance, the 64
+//                    lanes are the p processors of the probing step and of
+//                    the Dashboard updates (intra-subgraph parallelism), one
+//                    workgroup per sampler (inter-subgraph parallelism,
+//                    Sec. IV-C)
+//   induce kernels   the subgraph of G induced by each sampled vertex list, as
+//                    a mean-normalised CSR with local ids, for a batch of
+//                    samples at once (the last step of Alg. 2 / Alg. 3)
+//   gather kernel    feature (or label) rows of the sampled vertices
+//
+// Dashboard layout (LDS, per sampler): db[entries] holds, for every entry, the
+// Index-Array slot it belongs to (16 bits); slot k holds its vertex and its
+// weight, with the live flag in bit 31.  Popping a vertex clears one flag,
+// which invalidates all of its entries at once; the paper's Alg. 4 writes INV
+// into each of them.  Random numbers: Philox4x64-10 (Salmon et al., SC 2011)
+// keyed by (seed, sampler id), counter (t, kind, 0, 0).
+#include <algorithm>
+#include <cmath>
+
+#include "common.h"
+#include "gcn_sampler.h"
+
+namespace gcn {
+namespace {
+
+constexpr size_t kSamplerMaxLds = 160 * 1024;  // LDS of one gfx950 CU
+
+constexpr int kSampThreads = 64;          // one wavefront per sampler
+constexpr uint32_t kLive = 0x80000000u;
+constexpr uint64_t kKindRoot = 1, kKindProbe = 2, kKindNeigh = 3;
+constexpr int64_t kProbeRoundLimit = 1 << 20;
+
+// ---------------------------------------------------------------- Philox
+__device__ __forceinline__ uint64_t philox_word0(uint64_t t, uint64_t kind, uint64_t seed, uint64_t sid) {
+    const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+    const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+    uint64_t c0 = t, c1 = kind, c2 = 0, c3 = 0, k0 = seed, k1 = sid;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
+        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
+        c0 = hi1 ^ c1 ^ k0;
+        c1 = lo1;
+        c2 = hi0 ^ c3 ^ k1;
+        c3 = lo0;
+        k0 += W0;
+        k1 += W1;
+    }
+    return c0;
+}
+// integer uniform on [0, n): high word of r * n
+__device__ __forceinline__ int64_t below(uint64_t r, int64_t n) { return (int64_t)__umul64hi(r, (uint64_t)n); }
+
+__device__ __forceinline__ int32_t weight_of(const int32_t *__restrict__ indptr, int32_t v, int32_t cap) {
+    const int32_t d = indptr[v + 1] - indptr[v];
+    return (cap > 0 && d > cap) ? cap : d;
+}
+
+// inclusive prefix sum over the 64 lanes
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t x) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    return x;
+}
+
+// ------------------------------------------------------- frontier sampling
+struct SampArgs {
+    int32_t nV;
+    const int32_t *indptr;
+    const int32_t *indices;
+    int32_t m, n, db_cap, ia_cap, cap;
+    uint64_t seed;
+    int64_t first_sampler;
+    int32_t *vertices;   // [S][n]
+    int32_t *counts;     // [S]
+    int32_t *status;     // [S]
+};
+
+// Cleanup (Alg. 4): keep the live slots in slot order, renumber them, and
+// rebuild the Dashboard from their weights.  Whole wavefront.
+__device__ void dashboard_cleanup(uint16_t *db, int32_t *sv, uint32_t *sw, int32_t &s, int64_t &used) {
+    const int lane = threadIdx.x;
+    int32_t ns = 0;
+    for (int32_t base = 0; base < s; base += 64) {
+        const int32_t k = base + lane;
+        const bool in = k < s;
+        const int32_t v = in ? sv[k] : 0;
+        const uint32_t w = in ? sw[k] : 0u;
+        const bool live = in && (w & kLive);
+        const uint64_t mask = __ballot(live);
+        const int rank = __popcll(mask & ((1ull << lane) - 1ull));
+        __syncthreads();            // every lane has read its slot before any moves
+        if (live) {
+            sv[ns + rank] = v;
+            sw[ns + rank] = w;
+        }
+        ns += __popcll(mask);
+        __syncthreads();
+    }
+    s = ns;
+    int64_t off = 0;
+    for (int32_t base = 0; base < ns; base += 64) {
+        const int32_t k = base + lane;
+        const int32_t w = k < ns ? (int32_t)(sw[k] & ~kLive) : 0;
+        const int64_t incl = wave_incl_scan(w);
+        const int64_t start = off + incl - w;
+        for (int32_t e = 0; e < w; ++e) db[start + e] = (uint16_t)k;
+        off += __shfl(incl, 63, 64);
+    }
+    used = off;
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(kSampThreads) void frontier_kernel(SampArgs a) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+    int32_t *sv = (int32_t *)lds;                       // slot vertex   [ia_cap]
+    uint32_t *sw = (uint32_t *)(sv + a.ia_cap);         // slot weight | live [ia_cap]
+    uint16_t *db = (uint16_t *)(sw + a.ia_cap);         // Dashboard     [db_cap]
+    const int lane = threadIdx.x;
+    const uint64_t sid = (uint64_t)(a.first_sampler + blockIdx.x);
+    int32_t *out = a.vertices + (int64_t)blockIdx.x * a.n;
+    int status = GCN_SAMPLE_OK;
+    int32_t count = 0;
+
+    // ---- roots: m distinct vertices; candidate t is kept unless it repeats an
+    // earlier root (the lanes of a round take candidates t = 64 r + lane in order)
+    {
+        const uint64_t limit = 64ull * (uint64_t)a.m + 65536ull;
+        int32_t got = 0;
+        for (uint64_t base = 0; got < a.m; base += 64) {
+            if (base >= limit) { status = GCN_SAMPLE_ROOT_LIMIT; break; }
+            const uint64_t t = base + lane;
+            const int32_t c = (int32_t)below(philox_word0(t, kKindRoot, a.seed, sid), a.nV);
+            bool dup = t >= limit;
+            for (int32_t k = 0; k < got && !dup; ++k) dup = (sv[k] == c);
+            for (int j = 0; j < 64; ++j) {
+                const int32_t cj = __shfl(c, j, 64);
+                if (j < lane && cj == c) dup = true;
+            }
+            const uint64_t mask = __ballot(!dup);
+            const int rank = __popcll(mask & ((1ull << lane) - 1ull));
+            if (!dup && got + rank < a.m) {
+                sv[got + rank] = c;
+                out[got + rank] = c;
+            }
+            got += min(__popcll(mask), a.m - got);
+            __syncthreads();
+        }
+        count = got;
+    }
+
+    int64_t used = 0, live_weight = 0;
+    int32_t s = 0;
+    if (status == GCN_SAMPLE_OK) {
+        // ---- Dashboard from the roots (Alg. 3, initialisation)
+        for (int32_t base = 0; base < a.m; base += 64) {
+            const int32_t k = base + lane;
+            const int32_t w = k < a.m ? weight_of(a.indptr, sv[k], a.cap) : 0;
+            const int64_t incl = wave_incl_scan(w);
+            const int64_t total = __shfl(incl, 63, 64);
+            if (used + total > a.db_cap) { status = GCN_SAMPLE_OVERFLOW; break; }
+            const int64_t start = used + incl - w;
+            if (k < a.m) {
+                sw[k] = (uint32_t)w | kLive;
+                for (int32_t e = 0; e < w; ++e) db[start + e] = (uint16_t)k;
+            }
+            used += total;
+        }
+        live_weight = used;
+        s = a.m;
+        __syncthreads();
+    }
+
+    // ---- main loop: pop a frontier vertex, step to a neighbour, add it
+    uint64_t round = 0;
+    for (int32_t i = a.m; status == GCN_SAMPLE_OK && i < a.n; ++i) {
+        if (live_weight == 0) { status = GCN_SAMPLE_EXHAUSTED; break; }
+        const uint64_t rn = philox_word0((uint64_t)(i - a.m), kKindNeigh, a.seed, sid);
+        int32_t k = -1;
+        for (int64_t rr = 0;; ++rr) {
+            if (rr >= kProbeRoundLimit) { status = GCN_SAMPLE_PROBE_LIMIT; break; }
+            const int64_t idx = below(philox_word0(round * 64 + lane, kKindProbe, a.seed, sid), used);
+            const int32_t slot = db[idx];
+            const uint64_t mask = __ballot((sw[slot] & kLive) != 0u);
+            ++round;
+            if (mask) {
+                k = __shfl(slot, __ffsll((unsigned long long)mask) - 1, 64);
+                break;
+            }
+        }
+        if (status != GCN_SAMPLE_OK) break;
+        const int32_t v_pop = sv[k];
+        const uint32_t w_pop = sw[k] & ~kLive;
+        __syncthreads();
+        if (lane == 0) sw[k] = w_pop;               // no longer in the frontier
+        live_weight -= w_pop;
+
+        const int32_t beg = a.indptr[v_pop];
+        const int32_t deg = a.indptr[v_pop + 1] - beg;   // >= 1: its weight was > 0
+        const int32_t v_new = a.indices[beg + below(rn, deg)];
+        if ((uint32_t)v_new >= (uint32_t)a.nV) { status = GCN_SAMPLE_BAD_GRAPH; break; }
+        const int32_t w = weight_of(a.indptr, v_new, a.cap);
+
+        __syncthreads();
+        if (used + w > a.db_cap || s == a.ia_cap) dashboard_cleanup(db, sv, sw, s, used);
+        if (used + w > a.db_cap) { status = GCN_SAMPLE_OVERFLOW; break; }
+        for (int32_t e = lane; e < w; e += 64) db[used + e] = (uint16_t)s;
+        if (lane == 0) {
+            sv[s] = v_new;
+            sw[s] = (uint32_t)w | kLive;
+            out[i] = v_new;
+        }
+        used += w;
+        live_weight += w;
+        ++s;
+        count = i + 1;
+        __syncthreads();
+    }
+    if (lane == 0) {
+        a.counts[blockIdx.x] = count;
+        a.status[blockIdx.x] = status;
+    }
+}
+
+// ------------------------------------------------------- induced subgraphs
+constexpr int kTB = 256;
+constexpr int kItems = 8;
+constexpr int kTile = kTB * kItems;   // elements per scan tile
+
+// exclusive scan of one value per thread over the block; returns the total
+__device__ __forceinline__ int64_t block_excl_scan(int64_t x, int64_t &total) {
+    __shared__ int64_t wsum[kTB / 64];
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const int64_t incl = wave_incl_scan(x);
+    if (lane == 63) wsum[wid] = incl;
+    __syncthreads();
+    int64_t before = 0;
+    total = 0;
+#pragma unroll
+    for (int w = 0; w < kTB / 64; ++w) {
+        if (w < wid) before += wsum[w];
+        total += wsum[w];
+    }
+    __syncthreads();
+    return before + incl - x;
+}
+
+__global__ __launch_bounds__(kTB) void fill_i32_kernel(int32_t *__restrict__ x, int64_t n, int32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * kTB + threadIdx.x; i < n; i += (int64_t)gridDim.x * kTB) x[i] = v;
+}
+
+// map[s][v] = 1 for every sampled v of subgraph s (duplicates collapse)
+__global__ __launch_bounds__(kTB) void mark_kernel(int32_t nV, int32_t n, const int32_t *__restrict__ vertices,
+                                                   const int32_t *__restrict__ counts, int32_t *__restrict__ map) {
+    const int s = blockIdx.y;
+    const int32_t cnt = min(counts[s], n);
+    for (int32_t i = blockIdx.x * kTB + threadIdx.x; i < cnt; i += gridDim.x * kTB) {
+        const int32_t v = vertices[(int64_t)s * n + i];
+        if ((uint32_t)v < (uint32_t)nV) map[(int64_t)s * nV + v] = 1;
+    }
+}
+
+// per (segment, tile): sum of the tile's values
+__global__ __launch_bounds__(kTB) void seg_tile_sum_kernel(const int32_t *__restrict__ x, int64_t len,
+                                                           int64_t stride, int64_t *__restrict__ tsum,
+                                                           int32_t tiles) {
+    const int s = blockIdx.y;
+    const int64_t t0 = (int64_t)blockIdx.x * kTile;
+    const int32_t *xs = x + (int64_t)s * stride;
+    int64_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int64_t i = t0 + (int64_t)threadIdx.x * kItems + j;
+        if (i < len) acc += xs[i];
+    }
+    int64_t total;
+    block_excl_scan(acc, total);
+    if (threadIdx.x == 0) tsum[(int64_t)s * tiles + blockIdx.x] = total;
+}
+
+// per segment: exclusive scan of its tile sums (in place), segment total
+__global__ __launch_bounds__(kTB) void seg_tile_scan_kernel(int64_t *__restrict__ tsum, int32_t tiles,
+                                                            int64_t *__restrict__ seg_total) {
+    const int s = blockIdx.x;
+    int64_t *t = tsum + (int64_t)s * tiles;
+    int64_t carry = 0;
+    for (int32_t base = 0; base < tiles; base += kTB) {
+        const int32_t i = base + threadIdx.x;
+        const int64_t v = i < tiles ? t[i] : 0;
+        int64_t total;
+        const int64_t ex = block_excl_scan(v, total);
+        if (i < tiles) t[i] = carry + ex;
+        carry += total;
+    }
+    if (threadIdx.x == 0) seg_total[s] = carry;
+}
+
+// map[s][v] <- marked ? local id + 1 : 0;  vsub[s][local id] = v
+__global__ __launch_bounds__(kTB) void rank_kernel(int32_t nV, int32_t n, int32_t *__restrict__ map,
+                                                   const int64_t *__restrict__ toff, int32_t tiles,
+                                                   int32_t *__restrict__ vsub) {
+    const int s = blockIdx.y;
+    const int64_t t0 = (int64_t)blockIdx.x * kTile;
+    int32_t *ms = map + (int64_t)s * nV;
+    int32_t vals[kItems];
+    int64_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int64_t i = t0 + (int64_t)threadIdx.x * kItems + j;
+        vals[j] = i < nV ? ms[i] : 0;
+        acc += vals[j];
+    }
+    int64_t total;
+    int64_t r = toff[(int64_t)s * tiles + blockIdx.x] + block_excl_scan(acc, total);
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int64_t i = t0 + (int64_t)threadIdx.x * kItems + j;
+        if (i < nV && vals[j]) {
+            ms[i] = (int32_t)(r + 1);
+            if (r < n) vsub[(int64_t)s * n + r] = (int32_t)i;
+            ++r;
+        }
+    }
+}
+
+// row length of every local row: neighbours of vsub[s][i] that are in the sample
+__global__ __launch_bounds__(kTB) void row_count_kernel(int32_t nV, int32_t n, const int32_t *__restrict__ indptr,
+                                                        const int32_t *__restrict__ indices,
+                                                        const int32_t *__restrict__ map,
+                                                        const int64_t *__restrict__ n_sub,
+                                                        const int32_t *__restrict__ vsub,
+                                                        int32_t *__restrict__ rowlen) {
+    const int s = blockIdx.y;
+    const int lane = threadIdx.x & 63;
+    const int32_t i = blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
+    if (i >= n) return;
+    int32_t cnt = 0;
+    if (i < n_sub[s]) {
+        const int32_t u = vsub[(int64_t)s * n + i];
+        const int32_t *ms = map + (int64_t)s * nV;
+        for (int32_t p = indptr[u] + lane; p < indptr[u + 1]; p += 64) {
+            const int32_t w = indices[p];
+            cnt += ((uint32_t)w < (uint32_t)nV && ms[w] > 0) ? 1 : 0;
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+    }
+    if (lane == 0) rowlen[(int64_t)s * n + i] = cnt;
+}
+
+// per subgraph: indptr = exclusive scan of the row lengths (one block each)
+__global__ __launch_bounds__(kTB) void row_scan_kernel(int32_t n, const int32_t *__restrict__ rowlen,
+                                                       int32_t *__restrict__ indptr_sub,
+                                                       int64_t *__restrict__ nnz_sub) {
+    const int s = blockIdx.x;
+    const int32_t *rl = rowlen + (int64_t)s * n;
+    int32_t *ip = indptr_sub + (int64_t)s * (n + 1);
+    int64_t carry = 0;
+    for (int32_t base = 0; base < n; base += kTB) {
+        const int32_t i = base + threadIdx.x;
+        const int64_t v = i < n ? rl[i] : 0;
+        int64_t total;
+        const int64_t ex = block_excl_scan(v, total);
+        if (i < n) ip[i] = (int32_t)(carry + ex);
+        carry += total;
+    }
+    if (threadIdx.x == 0) {
+        ip[n] = (int32_t)carry;
+        nnz_sub[s] = carry;
+    }
+}
+
+// edge offsets of the subgraphs in the packed edge arrays; overflow flag
+__global__ __launch_bounds__(kTB) void edge_offsets_kernel(int32_t S, const int64_t *__restrict__ nnz_sub,
+                                                           int64_t *__restrict__ off, int64_t e_cap,
+                                                           int32_t *__restrict__ status) {
+    int64_t carry = 0;
+    for (int32_t base = 0; base < S; base += kTB) {
+        const int32_t i = base + threadIdx.x;
+        const int64_t v = i < S ? nnz_sub[i] : 0;
+        int64_t total;
+        const int64_t ex = block_excl_scan(v, total);
+        if (i < S) off[i] = carry + ex;
+        carry += total;
+    }
+    if (threadIdx.x == 0) {
+        off[S] = carry;
+        *status = carry > e_cap ? 1 : 0;
+    }
+}
+
+// local column ids and mean weights of every row, in neighbour order
+__global__ __launch_bounds__(kTB) void fill_rows_kernel(int32_t nV, int32_t n, const int32_t *__restrict__ indptr,
+                                                        const int32_t *__restrict__ indices,
+                                                        const int32_t *__restrict__ map,
+                                                        const int64_t *__restrict__ n_sub,
+                                                        const int32_t *__restrict__ vsub,
+                                                        const int32_t *__restrict__ indptr_sub,
+                                                        const int64_t *__restrict__ off,
+                                                        const int32_t *__restrict__ status,
+                                                        int32_t *__restrict__ sub_indices,
+                                                        float *__restrict__ sub_vals) {
+    const int s = blockIdx.y;
+    const int lane = threadIdx.x & 63;
+    const int32_t i = blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
+    if (*status != 0 || i >= n || i >= n_sub[s]) return;
+    const int32_t u = vsub[(int64_t)s * n + i];
+    const int32_t *ms = map + (int64_t)s * nV;
+    const int32_t *ip = indptr_sub + (int64_t)s * (n + 1);
+    const int32_t len = ip[i + 1] - ip[i];
+    const float val = 1.0f / (float)len;
+    int64_t pos = off[s] + ip[i];
+    for (int32_t p0 = indptr[u]; p0 < indptr[u + 1]; p0 += 64) {
+        const int32_t p = p0 + lane;
+        int32_t loc = -1;
+        if (p < indptr[u + 1]) {
+            const int32_t w = indices[p];
+            if ((uint32_t)w < (uint32_t)nV) loc = ms[w] - 1;
+        }
+        const uint64_t mask = __ballot(loc >= 0);
+        if (loc >= 0) {
+            const int64_t q = pos + __popcll(mask & ((1ull << lane) - 1ull));
+            sub_indices[q] = loc;
+            sub_vals[q] = val;
+        }
+        pos += __popcll(mask);
+    }
+}
+
+__global__ __launch_bounds__(kTB) void copy_n_sub_kernel(int32_t S, const int64_t *__restrict__ a,
+                                                         int32_t *__restrict__ b) {
+    const int32_t i = blockIdx.x * kTB + threadIdx.x;
+    if (i < S) b[i] = (int32_t)a[i];
+}
+
+// ------------------------------------------------------------------ gather
+// out[i, :] = X[rows[i], :] for 4-byte elements; a row index outside
+// [0, n_rows_X) gives a row of zeros.  VEC: 16-byte moves.
+template <bool VEC>
+__global__ __launch_bounds__(kTB) void gather_kernel(const uint32_t *__restrict__ X, int32_t n_rows_X,
+                                                     int32_t width, int64_t ldx, const int32_t *__restrict__ rows,
+                                                     int32_t count, uint32_t *__restrict__ out, int64_t ldo) {
+    const int lane = threadIdx.x & 63;
+    const int64_t i = (int64_t)blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
+    if (i >= count) return;
+    const int32_t r = rows[i];
+    const bool ok = (uint32_t)r < (uint32_t)n_rows_X;
+    const uint32_t *src = X + (int64_t)(ok ? r : 0) * ldx;
+    uint32_t *dst = out + i * ldo;
+    if (VEC) {
+        for (int32_t c = lane * 4; c < width; c += 256) {
+            uint4 v = ok ? *(const uint4 *)(src + c) : uint4{0, 0, 0, 0};
+            *(uint4 *)(dst + c) = v;
+        }
+    } else {
+        for (int32_t c = lane; c < width; c += 64) dst[c] = ok ? src[c] : 0u;
+    }
+}
+
+int blocks_for(int64_t n, int per) { return (int)std::min<int64_t>((n + per - 1) / per, 65535); }
+
+}  // namespace
+
+size_t sampler_lds_bytes(int32_t db_cap, int32_t ia_cap) {
+    return align256((size_t)ia_cap * 8 + (size_t)db_cap * 2);
+}
+
+int frontier_sample(const SampArgs &a, int32_t S, size_t lds, hipStream_t s) {
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipFuncSetAttribute((const void *)frontier_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            kSamplerMaxLds);
+        attr_set = true;
+    }
+    frontier_kernel<<<S, kSampThreads, lds, s>>>(a);
+    GCN_LAUNCH_CHECK("frontier_kernel");
+    return GCN_OK;
+}
+
+}  // namespace gcn
+
+using namespace gcn;
+
+namespace {
+struct InduceWs {
+    int32_t *map;       // [S][nV]: 0, then local id + 1 of sampled vertices
+    int64_t *tsum;      // [S][tiles]: tile sums, then their exclusive scan
+    int64_t *n_sub64;   // [S]
+    int64_t *nnz_sub;   // [S]
+    int32_t *rowlen;    // [S][n]
+};
+InduceWs carve_induce(Arena &ar, int32_t nV, int32_t n, int32_t S) {
+    InduceWs w;
+    const int32_t tiles = (int32_t)((nV + kTile - 1) / kTile);
+    w.map = ar.take<int32_t>((size_t)S * nV);
+    w.tsum = ar.take<int64_t>((size_t)S * tiles);
+    w.n_sub64 = ar.take<int64_t>(S);
+    w.nnz_sub = ar.take<int64_t>(S);
+    w.rowlen = ar.take<int32_t>((size_t)S * n);
+    return w;
+}
+}  // namespace
+
+extern "C" {
+
+int gcn_sampler_plan(int32_t n_vertices, const int32_t *indptr_host, int32_t m, int32_t n, double eta,
+                     int32_t cap, uint64_t seed, gcn_sampler_params *out) {
+    if (!indptr_host || !out || n_vertices <= 0 || m <= 0 || m > n_vertices || n < m || !(eta > 1.0) ||
+        cap < 0) {
+        set_error("gcn_sampler_plan: need indptr_host, out, 0 < m <= n_vertices, n >= m, eta > 1, cap >= 0");
+        return GCN_EINVAL;
+    }
+    double sum_w = 0.0;
+    int64_t wmax = 0;
+    for (int32_t v = 0; v < n_vertices; ++v) {
+        int64_t d = (int64_t)indptr_host[v + 1] - indptr_host[v];
+        if (cap > 0 && d > cap) d = cap;
+        sum_w += (double)d;
+        wmax = std::max(wmax, d);
+    }
+    // Dashboard of eta * m * (mean entries per vertex) entries (Sec. IV-B), at
+    // least enough for a frontier of m vertices of the largest weight when that
+    // fits; Index Array from the LDS left over, up to 16-bit slot ids.
+    int64_t db = (int64_t)std::ceil(eta * (double)m * (sum_w / n_vertices));
+    db = std::max<int64_t>(db, std::min<int64_t>((int64_t)m * wmax, (int64_t)(kSamplerMaxLds / 2)));
+    db = std::max<int64_t>(db, 1);
+    const int64_t min_ia = (int64_t)m + 64;
+    if ((size_t)min_ia * 8 + (size_t)db * 2 > kSamplerMaxLds) {
+        db = ((int64_t)kSamplerMaxLds - min_ia * 8) / 2;
+    }
+    if (db < 1 || min_ia > 65535) {
+        set_error("gcn_sampler_plan: a frontier of m = %d does not fit the %zu bytes of LDS", m,
+                  (size_t)kSamplerMaxLds);
+        return GCN_EUNSUPPORTED;
+    }
+    int64_t ia = ((int64_t)kSamplerMaxLds - db * 2) / 8;
+    ia = std::min<int64_t>(ia, 65535);
+    ia = std::min<int64_t>(ia, std::max<int64_t>(min_ia, 4 * (int64_t)m + 64));
+    out->m = m;
+    out->n = n;
+    out->db_entries = (int32_t)db;
+    out->ia_slots = (int32_t)ia;
+    out->cap = cap;
+    out->seed = seed;
+    return GCN_OK;
+}
+
+int gcn_frontier_sample(const gcn_csr *G, const gcn_sampler_params *p, int64_t first_sampler, int32_t S,
+                        int32_t *vertices, int32_t *counts, int32_t *status, void *stream) {
+    if (!G || !p || !vertices || !counts || !status || S < 0 || first_sampler < 0) {
+        set_error("gcn_frontier_sample: null argument or negative count");
+        return GCN_EINVAL;
+    }
+    if (G->n_rows != G->n_cols || G->n_rows <= 0 || !G->indptr || (G->nnz > 0 && !G->indices)) {
+        set_error("gcn_frontier_sample: G must be a square CSR with at least one vertex");
+        return GCN_ESHAPE;
+    }
+    if (p->m <= 0 || p->m > G->n_rows || p->n < p->m || p->ia_slots <= p->m || p->ia_slots > 65535 ||
+        p->db_entries <= 0 || p->cap < 0) {
+        set_error("gcn_frontier_sample: need 0 < m <= n_vertices, n >= m, m < ia_slots <= 65535, db_entries > 0");
+        return GCN_EINVAL;
+    }
+    const size_t lds = sampler_lds_bytes(p->db_entries, p->ia_slots);
+    int dev = 0, max_lds = 0;
+    GCN_HIP_CHECK(hipGetDevice(&dev));
+    GCN_HIP_CHECK(hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev));
+    const size_t limit = std::min<size_t>((size_t)max_lds, kSamplerMaxLds);
+    if (lds > limit) {
+        set_error("gcn_frontier_sample: Dashboard of %d entries and %d slots needs %zu bytes of LDS (limit %zu)",
+                  p->db_entries, p->ia_slots, lds, limit);
+        return GCN_EUNSUPPORTED;
+    }
+    if (S == 0) return GCN_OK;
+    SampArgs a;
+    a.nV = G->n_rows;
+    a.indptr = G->indptr;
+    a.indices = G->indices;
+    a.m = p->m;
+    a.n = p->n;
+    a.db_cap = p->db_entries;
+    a.ia_cap = p->ia_slots;
+    a.cap = p->cap;
+    a.seed = p->seed;
+    a.first_sampler = first_sampler;
+    a.vertices = vertices;
+    a.counts = counts;
+    a.status = status;
+    hipStream_t s = (hipStream_t)stream;
+    ProfScope prof(K_SAMPLE, s, 0.0, 0.0);
+    return frontier_sample(a, S, lds, s);
+}
+
+size_t gcn_induce_workspace_bytes(int32_t n_vertices, int32_t n, int32_t S) {
+    if (n_vertices <= 0 || n < 0 || S <= 0) return 256;
+    Arena ar(nullptr, 0);
+    carve_induce(ar, n_vertices, n, S);
+    return ar.used;
+}
+
+int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *vertices, const int32_t *counts,
+                         int32_t *n_sub, int32_t *vsub, int32_t *indptr_sub, int64_t *edge_offsets,
+                         int32_t *sub_indices, float *sub_vals, int64_t edge_capacity, int32_t *status,
+                         void *ws, size_t ws_bytes, void *stream) {
+    if (!G || !vertices || !counts || !n_sub || !vsub || !indptr_sub || !edge_offsets || !status || S < 0 ||
+        n < 0 || edge_capacity < 0 || (edge_capacity > 0 && (!sub_indices || !sub_vals))) {
+        set_error("gcn_induce_subgraphs: null argument or negative size");
+        return GCN_EINVAL;
+    }
+    if (G->n_rows != G->n_cols || G->n_rows <= 0 || !G->indptr || (G->nnz > 0 && !G->indices)) {
+        set_error("gcn_induce_subgraphs: G must be a square CSR with at least one vertex");
+        return GCN_ESHAPE;
+    }
+    if (S == 0) return GCN_OK;
+    const int32_t nV = G->n_rows;
+    Arena ar(ws, ws_bytes);
+    InduceWs w = carve_induce(ar, nV, n, S);
+    if (!w.map || !w.rowlen || ((uintptr_t)ws & 255u)) {
+        set_error("gcn_induce_subgraphs: workspace of %zu bytes is too small or misaligned (need %zu)", ws_bytes,
+                  gcn_induce_workspace_bytes(nV, n, S));
+        return GCN_EWORKSPACE;
+    }
+    if (S > 65535) {
+        set_error("gcn_induce_subgraphs: at most 65535 subgraphs per call");
+        return GCN_EINVAL;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    ProfScope prof(K_INDUCE, s, 0.0, 0.0);
+    const int32_t tiles = (nV + kTile - 1) / kTile;
+    const int64_t mapn = (int64_t)S * nV;
+    fill_i32_kernel<<<blocks_for(mapn, kTB * 8), kTB, 0, s>>>(w.map, mapn, 0);
+    if (n > 0) {
+        mark_kernel<<<dim3(blocks_for(n, kTB), S), kTB, 0, s>>>(nV, n, vertices, counts, w.map);
+    }
+    seg_tile_sum_kernel<<<dim3(tiles, S), kTB, 0, s>>>(w.map, nV, nV, w.tsum, tiles);
+    seg_tile_scan_kernel<<<S, kTB, 0, s>>>(w.tsum, tiles, w.n_sub64);
+    rank_kernel<<<dim3(tiles, S), kTB, 0, s>>>(nV, n, w.map, w.tsum, tiles, vsub);
+    copy_n_sub_kernel<<<blocks_for(S, kTB), kTB, 0, s>>>(S, w.n_sub64, n_sub);
+    if (n > 0) {
+        const int rb = (n + kTB / 64 - 1) / (kTB / 64);
+        row_count_kernel<<<dim3(rb, S), kTB, 0, s>>>(nV, n, G->indptr, G->indices, w.map, w.n_sub64, vsub,
+                                                     w.rowlen);
+    }
+    row_scan_kernel<<<S, kTB, 0, s>>>(n, w.rowlen, indptr_sub, w.nnz_sub);
+    edge_offsets_kernel<<<1, kTB, 0, s>>>(S, w.nnz_sub, edge_offsets, edge_capacity, status);
+    if (n > 0) {
+        const int rb = (n + kTB / 64 - 1) / (kTB / 64);
+        fill_rows_kernel<<<dim3(rb, S), kTB, 0, s>>>(nV, n, G->indptr, G->indices, w.map, w.n_sub64, vsub,
+                                                     indptr_sub, edge_offsets, status, sub_indices, sub_vals);
+    }
+    GCN_LAUNCH_CHECK("induce kernels");
+    return GCN_OK;
+}
+
+int gcn_gather_rows(const void *X, int32_t n_rows_X, int32_t width, int64_t ldx, const int32_t *rows,
+                    int32_t count, void *out, int64_t ldo, void *stream) {
+    if (count < 0 || width < 0 || n_rows_X < 0 || (count > 0 && (!X || !rows || !out))) {
+        set_error("gcn_gather_rows: null argument or negative size");
+        return GCN_EINVAL;
+    }
+    if (ldx < width || ldo < width) {
+        set_error("gcn_gather_rows: leading dimensions must be >= width");
+        return GCN_ESHAPE;
+    }
+    if (count == 0 || width == 0) return GCN_OK;
+    hipStream_t s = (hipStream_t)stream;
+    ProfScope prof(K_GATHER, s, 0.0, 2.0 * 4.0 * (double)count * width);
+    const bool vec = width % 4 == 0 && ldx % 4 == 0 && ldo % 4 == 0 && ((uintptr_t)X & 15u) == 0 &&
+                     ((uintptr_t)out & 15u) == 0;
+    const int blocks = (int)(((int64_t)count + kTB / 64 - 1) / (kTB / 64));
+    if (vec)
+        gather_kernel<true><<<blocks, kTB, 0, s>>>((const uint32_t *)X, n_rows_X, width, ldx, rows, count,
+                                                   (uint32_t *)out, ldo);
+    else
+        gather_kernel<false><<<blocks, kTB, 0, s>>>((const uint32_t *)X, n_rows_X, width, ldx, rows, count,
+                                                    (uint32_t *)out, ldo);
+    GCN_LAUNCH_CHECK("gather_kernel");
+    return GCN_OK;
+}
+
+}  // extern "C"

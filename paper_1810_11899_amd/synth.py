@@ -288,3 +288,36 @@ def custom(n: int, graph: str, d: int, layers, head=None, classes=0, seed: int =
     """Small workloads for tests (ragged sizes spanning several tiles)."""
     spec = Spec(f"custom_{graph}{n}_d{d}", n, graph, d, list(layers), head, classes)
     return build(spec, s=seed, cfg_key=1000)
+
+
+# --------------------------------------------------------------------------
+# training graphs for the sampler (the graph G that subgraphs are drawn from)
+# --------------------------------------------------------------------------
+@dataclass
+class TrainingGraph:
+    """G with its vertex attributes H^(0) and labels (the input of Alg. 5)."""
+    name: str
+    graph: Graph
+    X: np.ndarray        # float32 [nV, f]
+    labels: np.ndarray   # int32 [nV] in [0, classes)
+    classes: int
+
+
+def training_graph(n: int, d: int, f: int, classes: int, seed: int = 0, kind: str = "rmat",
+                   name: Optional[str] = None) -> TrainingGraph:
+    """Undirected graph with n*d/2 edges (R-MAT by default), N(0,1) attributes,
+    uniform single-label classes.  Streams: SeedSequence([181011899, 2000,
+    seed, n]) spawned into graph, relabel, attributes, labels."""
+    children = np.random.SeedSequence([SEED_ROOT, 2000, seed, n]).spawn(4)
+    rg_graph, rg_relabel, rg_x, rg_lab = (np.random.Generator(np.random.PCG64(c)) for c in children)
+    g = make_graph(kind, n, d, rg_graph, rg_relabel)
+    X = rg_x.standard_normal((n, f), dtype=np.float32)
+    labels = rg_lab.integers(0, classes, size=n).astype(np.int32)
+    return TrainingGraph(name or f"{kind}{n}_d{d}_f{f}_c{classes}", g, X, labels, classes)
+
+
+# A Reddit-shaped training graph (Table I: 232,965 vertices, 602 attributes,
+# 41 classes), R-MAT with 50 stored edges per vertex on average.
+TRAINING_GRAPHS = {
+    "reddit_like": dict(n=232965, d=50, f=602, classes=41),
+}

@@ -142,3 +142,45 @@ def test_profile_classes(L):
     names = [L.gcn_profile_class_name(i).decode() for i in range(n)]
     assert "spmm" in names and "gemm_nn" in names and "gemm_tn" in names
     assert L.gcn_profile_read(n, None, None, None, None) == B.GCN_EINVAL
+
+
+# ------------------------------------------------------------ sampler ABI ----
+def test_sampler_plan_sizes_fit_lds(L):
+    g = synth.custom(5000, "rmat", 20, [(4, 4)], seed=1).graph
+    for m, cap in [(1000, 30), (200, 0), (64, 5)]:
+        p = B.gcn_sampler_plan(g.indptr, m, 4 * m, eta=2.0, cap=cap, seed=3)
+        w = np.minimum(g.degrees(), cap) if cap else g.degrees()
+        assert p.db_entries >= int(np.ceil(2.0 * m * w.mean())) or 8 * p.ia_slots + 2 * p.db_entries > 160 * 1024 - 256
+        assert 8 * p.ia_slots + 2 * p.db_entries <= 160 * 1024
+        assert m < p.ia_slots <= 65535 and p.m == m and p.n == 4 * m and p.cap == cap and p.seed == 3
+
+
+def test_sampler_plan_rejects_bad_arguments(L):
+    g = synth.custom(500, "rmat", 8, [(4, 4)], seed=1).graph
+    with pytest.raises(B.GcnError) as e:
+        B.gcn_sampler_plan(g.indptr, 501, 600)
+    assert e.value.code == B.GCN_EINVAL
+    with pytest.raises(B.GcnError) as e:
+        B.gcn_sampler_plan(g.indptr, 10, 100, eta=1.0)
+    assert e.value.code == B.GCN_EINVAL
+    big = synth.custom(40000, "er", 2, [(4, 4)], seed=1).graph
+    with pytest.raises(B.GcnError) as e:
+        B.gcn_sampler_plan(big.indptr, 30000, 30000)
+    assert e.value.code == B.GCN_EUNSUPPORTED
+
+
+def test_sampler_entry_points_check_arguments_before_launch(L):
+    p = B.gcn_sampler_params(10, 20, 100, 32, 0, 1)
+    csr = B.gcn_csr(100, 100, 0, None, None, None)
+    assert L.gcn_frontier_sample(ctypes.byref(csr), ctypes.byref(p), 0, 1, None, None, None, None) == B.GCN_EINVAL
+    fake = ctypes.c_void_p(256)   # never dereferenced: the shape check fails first
+    csr2 = B.gcn_csr(100, 90, 0, fake, None, None)
+    assert L.gcn_frontier_sample(ctypes.byref(csr2), ctypes.byref(p), 0, 1, fake, fake, fake, None) == B.GCN_ESHAPE
+    p_bad = B.gcn_sampler_params(10, 20, 100, 10, 0, 1)   # ia_slots must exceed m
+    csr3 = B.gcn_csr(100, 100, 0, fake, None, None)
+    assert L.gcn_frontier_sample(ctypes.byref(csr3), ctypes.byref(p_bad), 0, 1, fake, fake, fake, None) == B.GCN_EINVAL
+    assert L.gcn_induce_subgraphs(ctypes.byref(csr3), 1, 10, None, None, None, None, None, None, None, None, 0,
+                                  None, None, 0, None) == B.GCN_EINVAL
+    assert L.gcn_gather_rows(fake, 10, 8, 4, fake, 3, fake, 8, None) == B.GCN_ESHAPE
+    assert L.gcn_gather_rows(None, 10, 8, 8, None, 0, None, 8, None) == B.GCN_OK   # nothing to do
+    assert L.gcn_induce_workspace_bytes(1000, 100, 4) >= 4 * 1000 * 4
