@@ -84,6 +84,9 @@ _SIGNATURES = {
     "gcn_induce_subgraphs": (ctypes.c_int, [_CSRP, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P,
                                             _SZ, _P]),
     "gcn_gather_rows": (ctypes.c_int, [_P, _I32, _I32, _I64, _P, _I32, _P, _I64, _P]),
+    # gcn_optim.h
+    "gcn_adam_update": (ctypes.c_int, [_P, _P, _P, _P, _I64, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                       ctypes.c_double, _I32, _P]),
     # gcn_peaks.h
     "gcn_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _I32, _P]),
     "gcn_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I32, _I32, _P, ctypes.POINTER(ctypes.c_double), _P]),
@@ -356,6 +359,18 @@ def gcn_gather_rows(X: torch.Tensor, rows: torch.Tensor, count: int, out: torch.
     _check(lib().gcn_gather_rows(_ptr(X2), int(X2.shape[0]), width, _ld(X2), _ptr(rows), int(count), _ptr(o2),
                                  _ld(o2), _stream(stream)), "gcn_gather_rows")
     return out
+
+
+# ---------------------------------------------------------------- optimiser
+def gcn_adam_update(params, grads, m, v, lr: float, step: int, beta1: float = 0.9, beta2: float = 0.999,
+                    eps: float = 1e-8, stream=None):
+    """One Adam step over flat float32 tensors of equal length, in place."""
+    for t, nm in ((params, "params"), (grads, "grads"), (m, "m"), (v, "v")):
+        _dev_f32(t, nm)
+        if not t.is_contiguous() or t.numel() != params.numel():
+            raise ValueError(f"{nm} must be contiguous with as many elements as params")
+    _check(lib().gcn_adam_update(_ptr(params), _ptr(grads), _ptr(m), _ptr(v), params.numel(), lr, beta1, beta2,
+                                 eps, int(step), _stream(stream)), "gcn_adam_update")
 
 
 # ---------------------------------------------------------------- profiling

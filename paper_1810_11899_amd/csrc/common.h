@@ -51,6 +51,7 @@ enum KernelClass {
     K_SAMPLE,
     K_INDUCE,
     K_GATHER,
+    K_ADAM,
     K_CLASS_COUNT
 };
 const char *class_name(int cls);

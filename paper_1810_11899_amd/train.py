@@ -1,0 +1,271 @@
+"""GCN training with the parallel frontier sampler (Alg. 5), on one GPU.
+
+The scheduler keeps a pool of sampled subgraphs.  When the pool runs out it
+is refilled by S sampler runs launched at once (inter-subgraph parallelism,
+Sec. IV-C), and each training iteration pops one subgraph, builds the GCN on it
+and runs forward, loss, backward and the ADAM update (Alg. 1, Alg. 5).
+
+MI355X mapping:
+  - two pools are double-buffered: while the compute stream trains on one, a
+    second stream (default priority) samples and induces the next, so sampling
+    overlaps training;
+  - the training graph G, its attributes and labels stay resident in HBM; an
+    iteration gathers the subgraph's rows on the device;
+  - all trained tensors live in one flat buffer, so one kernel applies ADAM to
+    the whole model.
+Every step of the computation is a call into libgcnlayer; this module only
+sequences the calls and moves pool metadata (vertex and edge counts) to the
+host, which the layer calls take as sizes.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import List, Optional, Tuple
+
+import numpy as np
+import torch
+
+from . import binding as B
+from . import synth
+
+
+@dataclass
+class SamplerConfig:
+    m: int = 1000          # frontier size (Sec. IV-A uses 1000)
+    n: int = 8000          # vertex-list length per subgraph
+    eta: float = 2.0       # Dashboard enlargement factor
+    cap: int = 30          # Dashboard entries per vertex at most (Sec. VI-C-2)
+    pool: int = 256        # subgraphs per refill (p_inter)
+    seed: int = 1
+
+
+class FlatModel:
+    """Weights, biases and the prediction layer in one flat float32 buffer,
+    with gradient, first- and second-moment buffers of the same layout."""
+
+    def __init__(self, dims: List[Tuple[int, int]], classes: int, device, seed: int = 0):
+        self.dims = list(dims)
+        self.classes = classes
+        shapes = []
+        for (f_in, h) in dims:
+            shapes += [(f_in, h), (f_in, h), (2 * h,)]
+        shapes += [(2 * dims[-1][1], classes), (classes,)]
+        self.shapes = shapes
+        offs, o = [], 0
+        for sh in shapes:
+            offs.append(o)
+            o += (int(np.prod(sh)) + 63) // 64 * 64     # 256-byte aligned views
+        self.offsets, self.total = offs, o
+        d = torch.device(device)
+        self.params = torch.zeros(o, dtype=torch.float32, device=d)
+        self.grads = torch.zeros(o, dtype=torch.float32, device=d)
+        self.m = torch.zeros(o, dtype=torch.float32, device=d)
+        self.v = torch.zeros(o, dtype=torch.float32, device=d)
+        rg = np.random.Generator(np.random.PCG64(np.random.SeedSequence([synth.SEED_ROOT, 3000, seed])))
+        host = np.zeros(o, dtype=np.float32)
+        for i, sh in enumerate(shapes):
+            if len(sh) == 2:
+                host[offs[i]:offs[i] + sh[0] * sh[1]] = synth.glorot(rg, sh[0], sh[1]).ravel()
+        self.params.copy_(torch.from_numpy(host))
+        self.step_count = 0
+
+    def _view(self, buf, i):
+        sh = self.shapes[i]
+        return buf[self.offsets[i]:self.offsets[i] + int(np.prod(sh))].view(*sh)
+
+    def layer(self, li, buf=None):
+        buf = self.params if buf is None else buf
+        return tuple(self._view(buf, 3 * li + j) for j in range(3))
+
+    def head(self, buf=None):
+        buf = self.params if buf is None else buf
+        k = 3 * len(self.dims)
+        return self._view(buf, k), self._view(buf, k + 1)
+
+    def host_tensors(self):
+        """{name: numpy array} of the current parameters (for checks)."""
+        p = self.params.cpu().numpy()
+        out = {}
+        names = []
+        for li in range(len(self.dims)):
+            names += [f"W_self{li}", f"W_neigh{li}", f"bias{li}"]
+        names += ["W_pred", "b_pred"]
+        for nm, o, sh in zip(names, self.offsets, self.shapes):
+            out[nm] = p[o:o + int(np.prod(sh))].reshape(sh).copy()
+        return out
+
+
+class _Pool:
+    """Device buffers of S sampled subgraphs and their induced CSRs."""
+
+    def __init__(self, S: int, n: int, nV: int, edge_capacity: int, device):
+        d = torch.device(device)
+        self.S, self.n = S, n
+        self.vertices = torch.empty((S, n), dtype=torch.int32, device=d)
+        self.counts = torch.empty(S, dtype=torch.int32, device=d)
+        self.status = torch.empty(S, dtype=torch.int32, device=d)
+        self.batch = B.InducedBatch(S, n, edge_capacity, d)
+        self.ws = B.Workspace(d)
+        self.ws.get(B.lib().gcn_induce_workspace_bytes(nV, n, S))
+        self.h_nsub = torch.empty(S, dtype=torch.int32).pin_memory()
+        self.h_off = torch.empty(S + 1, dtype=torch.int64).pin_memory()
+        self.h_status = torch.empty(S, dtype=torch.int32).pin_memory()
+        self.h_istatus = torch.empty(1, dtype=torch.int32).pin_memory()
+        self.ready = torch.cuda.Event()
+        self.released = torch.cuda.Event()
+        self.first_id = 0
+        self.next = S       # nothing to pop until filled
+
+
+class Trainer:
+    """Alg. 5 on one GPU: pool refills on a side stream, iterations on the
+    current stream."""
+
+    def __init__(self, tg: "synth.TrainingGraph", dims: List[Tuple[int, int]], cfg: SamplerConfig,
+                 lr: float = 0.01, prec: int = B.GCN_F32, device: str = "cuda", model_seed: int = 0):
+        self.dev = torch.device(device)
+        self.cfg = cfg
+        self.prec = prec
+        self.lr = lr
+        g = tg.graph
+        if dims[0][0] != tg.X.shape[1]:
+            raise ValueError("the first layer's width must match the attributes")
+        self.G = B.DeviceCSR.from_host(g.n, g.n, g.indptr, g.indices, g.vals, device=self.dev)
+        self.X = torch.from_numpy(tg.X).to(self.dev)
+        self.labels_all = torch.from_numpy(tg.labels).to(self.dev)
+        self.classes = tg.classes
+        self.params = B.gcn_sampler_plan(g.indptr, cfg.m, cfg.n, eta=cfg.eta, cap=cfg.cap, seed=cfg.seed)
+        self.model = FlatModel(dims, tg.classes, self.dev, seed=model_seed)
+        self.dims = list(dims)
+        self.L = len(dims)
+        self.orders = [B.gcn_layer_pick_order(f, h, li > 0) for li, (f, h) in enumerate(dims)]
+        n = cfg.n
+        d = self.dev
+        mean_deg = g.nnz / max(g.n, 1)
+        self.edge_cap = int(cfg.n * max(mean_deg, 1.0) * 2) + 1024
+        self.side = torch.cuda.Stream(device=d)
+        self.pools = [_Pool(cfg.pool, n, g.n, cfg.pool * self.edge_cap // 4 + 1024, d) for _ in range(2)]
+        self.cur = 0
+        self.next_id = 0
+        # iteration buffers, sized for the largest subgraph (n vertices)
+        self.ws = B.Workspace(d)
+        self.H0 = torch.empty((n, dims[0][0]), dtype=torch.float32, device=d)
+        self.lab = torch.empty(n, dtype=torch.int32, device=d)
+        self.Y = [torch.empty((n, 2 * h), dtype=torch.float32, device=d) for (_, h) in dims]
+        self.dH = [None] + [torch.empty((n, f), dtype=torch.float32, device=d) for (f, _) in dims[1:]]
+        self.dHL = torch.empty((n, 2 * dims[-1][1]), dtype=torch.float32, device=d)
+        self.saved = []
+        for (f, h), o in zip(dims, self.orders):
+            nb = B.gcn_layer_saved_bytes(n, f, h, o, prec)
+            self.saved.append(torch.empty(max(nb, 256), dtype=torch.uint8, device=d) if nb else None)
+        self._alloc_edges(self.edge_cap)
+        self.losses = torch.zeros(1 << 16, dtype=torch.float32, device=d)
+        self.iteration = 0
+        self.subgraph_ids: List[int] = []
+        for p in self.pools:
+            self._refill(p)
+
+    def _alloc_edges(self, cap):
+        d = self.dev
+        self.t_indptr = torch.empty(self.cfg.n + 1, dtype=torch.int32, device=d)
+        self.t_indices = torch.empty(max(cap, 1), dtype=torch.int32, device=d)
+        self.t_vals = torch.empty(max(cap, 1), dtype=torch.float32, device=d)
+        self.t_cap = cap
+
+    # ---------------------------------------------------------------- pools
+    def _refill(self, p: _Pool):
+        """Sample and induce S subgraphs on the side stream (after the compute
+        stream has released the pool's buffers)."""
+        p.first_id = self.next_id
+        self.next_id += p.S
+        s = self.side
+        s.wait_event(p.released)
+        with torch.cuda.stream(s):
+            B.gcn_frontier_sample(self.G, self.params, p.first_id, p.S, p.vertices, p.counts, p.status, stream=s)
+            B.gcn_induce_subgraphs(self.G, p.vertices, p.counts, p.batch, p.ws, stream=s)
+            p.h_status.copy_(p.status, non_blocking=True)
+            p.h_nsub.copy_(p.batch.n_sub, non_blocking=True)
+            p.h_off.copy_(p.batch.edge_offsets, non_blocking=True)
+            p.h_istatus.copy_(p.batch.status, non_blocking=True)
+            p.ready.record(s)
+        p.next = -1   # filled, metadata not read yet
+
+    def _open(self, p: _Pool):
+        """Wait for a refill and read its metadata on the host."""
+        p.ready.synchronize()
+        if int(p.h_istatus[0]) != 0:       # edge arrays too small: grow and induce again
+            need = int(p.h_off[-1])
+            s = self.side
+            with torch.cuda.stream(s):
+                p.batch = B.InducedBatch(p.S, p.n, need + need // 8, self.dev)
+                B.gcn_induce_subgraphs(self.G, p.vertices, p.counts, p.batch, p.ws, stream=s)
+                p.h_nsub.copy_(p.batch.n_sub, non_blocking=True)
+                p.h_off.copy_(p.batch.edge_offsets, non_blocking=True)
+                p.ready.record(s)
+            p.ready.synchronize()
+        bad = [B.SAMPLE_STATUS[int(x)] for x in p.h_status.numpy() if int(x) not in (0, 1)]
+        if bad:
+            raise RuntimeError(f"sampler runs failed: {sorted(set(bad))}")
+        p.nsub = p.h_nsub.numpy().copy()
+        p.off = p.h_off.numpy().copy()
+        p.next = 0
+        torch.cuda.current_stream(self.dev).wait_event(p.ready)
+
+    def _pop(self):
+        p = self.pools[self.cur]
+        if p.next < 0:
+            self._open(p)
+        if p.next >= p.S:
+            p.released.record(torch.cuda.current_stream(self.dev))
+            self._refill(p)
+            self.cur ^= 1
+            p = self.pools[self.cur]
+            if p.next < 0:
+                self._open(p)
+        s = p.next
+        p.next += 1
+        return p, s
+
+    # ------------------------------------------------------------ iteration
+    def step(self):
+        """One training iteration on the next subgraph of the pool."""
+        p, s = self._pop()
+        ns, e0, e1 = int(p.nsub[s]), int(p.off[s]), int(p.off[s + 1])
+        self.subgraph_ids.append(p.first_id + s)
+        nnz = e1 - e0
+        if nnz > self.t_cap:
+            self._alloc_edges(nnz + nnz // 8)
+        A = p.batch.csr(s, ns, e0, e1)
+        AT = B.DeviceCSR(ns, ns, self.t_indptr[:ns + 1], self.t_indices[:nnz], self.t_vals[:nnz])
+        rows = p.batch.vsub[s]
+        B.gcn_gather_rows(self.X, rows, ns, self.H0)
+        B.gcn_gather_rows(self.labels_all, rows, ns, self.lab)
+        B.gcn_csr_transpose_into(A, AT.indptr, AT.indices, AT.vals, self.ws)
+        mdl = self.model
+        H = self.H0[:ns]
+        for li in range(self.L):
+            Ws, Wn, b = mdl.layer(li)
+            B.gcn_layer_fwd(A, H, Ws, Wn, b, self.Y[li][:ns], self.saved[li], self.orders[li], self.ws, self.prec)
+            H = self.Y[li][:ns]
+        Wp, bp = mdl.head()
+        dWp, dbp = mdl.head(mdl.grads)
+        t = self.iteration % self.losses.numel()
+        B.gcn_loss_grad(H, Wp, bp, B.GCN_SOFTMAX_CE, self.lab[:ns], None, self.losses[t:t + 1], self.dHL[:ns],
+                        dWp, dbp, self.ws, self.prec)
+        dY = self.dHL[:ns]
+        for li in range(self.L - 1, -1, -1):
+            Ws, Wn, _ = mdl.layer(li)
+            gWs, gWn, gb = mdl.layer(li, mdl.grads)
+            Hin = self.H0[:ns] if li == 0 else self.Y[li - 1][:ns]
+            dH = None if self.dH[li] is None else self.dH[li][:ns]
+            B.gcn_layer_bwd(A, AT, Hin, Ws, Wn, self.Y[li][:ns], self.saved[li], dY, dH, gWs, gWn, gb,
+                            self.orders[li], self.ws, self.prec)
+            dY = dH
+        mdl.step_count += 1
+        B.gcn_adam_update(mdl.params, mdl.grads, mdl.m, mdl.v, self.lr, mdl.step_count)
+        self.iteration += 1
+        return ns, nnz
+
+    def loss_history(self) -> np.ndarray:
+        k = min(self.iteration, self.losses.numel())
+        return self.losses[:k].cpu().numpy()

@@ -1,0 +1,105 @@
+"""The optimiser kernel and the training loop (Alg. 5) on the GPU against the
+CPU oracle: Adam step by step on the same float32 inputs, and a whole run of
+sampled-subgraph iterations replayed on the oracle (same sampler runs, same
+induced subgraphs, float64 layer and Adam)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import optim as OO
+from oracle import sampler as OS
+from paper_1810_11899_amd import binding as B
+from paper_1810_11899_amd import synth
+from paper_1810_11899_amd.train import SamplerConfig, Trainer
+
+from gpu_util import rel_inf, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+    yield
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("count, offset", [(100003, 0), (65536, 0), (4096, 1)])
+def test_adam_kernel_matches_oracle(count, offset):
+    """Several steps from zero moments, gradients of mixed magnitudes; the
+    oracle is fed the GPU's own float32 state each step."""
+    rng = np.random.default_rng(count)
+    buf = [torch.zeros(count + offset, dtype=torch.float32, device="cuda") for _ in range(4)]
+    p, g, m, v = (b[offset:] for b in buf)      # offset 1: misaligned, scalar path
+    p.copy_(torch.from_numpy(rng.standard_normal(count).astype(np.float32)))
+    for t in range(1, 5):
+        gh = (rng.standard_normal(count) * 10.0 ** rng.integers(-5, 1, count)).astype(np.float32)
+        g.copy_(torch.from_numpy(gh))
+        p0, m0, v0 = p.cpu().numpy(), m.cpu().numpy(), v.cpu().numpy()
+        B.gcn_adam_update(p, g, m, v, lr=0.01, step=t)
+        rp, rm, rv = OO.adam(p0, gh, m0, v0, t, 0.01)
+        assert rel_inf(p.cpu().numpy(), rp) <= 1e-6
+        assert rel_inf(m.cpu().numpy(), rm) <= 1e-6
+        assert rel_inf(v.cpu().numpy(), rv) <= 1e-6
+
+
+def replay_on_oracle(tg, dims, cfg, params, init, ids, lr):
+    """The training run re-done on the CPU oracle: same sampler runs (same
+    Philox streams), induced subgraphs, float64 fwd/bwd, float64 Adam."""
+    g = tg.graph
+    P = {k: v.astype(np.float64) for k, v in init.items()}
+    M = {k: np.zeros_like(v) for k, v in P.items()}
+    V = {k: np.zeros_like(v) for k, v in P.items()}
+    spec = synth.Spec("replay", 0, "rmat", 0, dims, "ce", tg.classes)
+    losses = []
+    for t, sid in enumerate(ids, start=1):
+        verts, st = OS.frontier_sample(g.indptr, g.indices, cfg.m, cfg.n, params.db_entries, params.ia_slots,
+                                       cap=cfg.cap, p=64, seed=cfg.seed, sampler_id=sid)
+        assert st in ("ok", "exhausted")
+        vsub, ip, ix, vals = OS.induce(g.indptr, g.indices, verts)
+        layers = [synth.Layer(P[f"W_self{li}"].astype(np.float32), P[f"W_neigh{li}"].astype(np.float32),
+                              P[f"bias{li}"].astype(np.float32)) for li in range(len(dims))]
+        wl = synth.Workload(spec, 0, synth.Graph(vsub.size, ip, ix, vals), OS.gather_rows(tg.X, vsub), layers,
+                            W_pred=P["W_pred"].astype(np.float32), b_pred=P["b_pred"].astype(np.float32),
+                            labels=OS.gather_rows(tg.labels, vsub))
+        r = oracle.step(wl)
+        losses.append(r.loss)
+        grads = {"W_pred": r.dW_pred, "b_pred": r.db_pred}
+        for li in range(len(dims)):
+            grads[f"W_self{li}"], grads[f"W_neigh{li}"], grads[f"bias{li}"] = r.dW_self[li], r.dW_neigh[li], r.db[li]
+        for k in P:
+            P[k], M[k], V[k] = OO.adam(P[k], grads[k], M[k], V[k], t, lr)
+    return np.array(losses), P
+
+
+def test_training_run_matches_oracle_replay():
+    tg = synth.training_graph(3000, 16, 24, 7, seed=3)
+    dims = [(24, 16), (32, 16)]
+    cfg = SamplerConfig(m=40, n=300, eta=2.0, cap=20, pool=3, seed=5)
+    tr = Trainer(tg, dims, cfg, lr=0.01)
+    init = tr.model.host_tensors()
+    iters = 8                                    # crosses two pool refills
+    for it in range(iters):
+        ns, nnz = tr.step()
+        print(f"iteration {it}: subgraph {tr.subgraph_ids[-1]} n={ns} nnz={nnz}", flush=True)
+    torch.cuda.synchronize()
+    assert tr.subgraph_ids == list(range(iters))
+    losses = tr.loss_history()
+    ref_losses, ref_P = replay_on_oracle(tg, dims, cfg, tr.params, init, tr.subgraph_ids, 0.01)
+    assert np.max(np.abs(losses - ref_losses) / np.abs(ref_losses)) <= 1e-4, (losses, ref_losses)
+    final = tr.model.host_tensors()
+    for k, v in final.items():
+        assert rel_inf(v, ref_P[k]) <= 1e-3, k
+
+
+def test_training_loss_decreases():
+    tg = synth.training_graph(2000, 12, 16, 4, seed=4)
+    dims = [(16, 32), (64, 32)]
+    cfg = SamplerConfig(m=50, n=600, eta=2.0, cap=20, pool=8, seed=2)
+    tr = Trainer(tg, dims, cfg, lr=0.01)
+    for _ in range(60):
+        tr.step()
+    h = tr.loss_history()
+    assert np.all(np.isfinite(h))
+    assert h[-10:].mean() < h[:10].mean() - 0.05, h

@@ -384,3 +384,35 @@ def test_kink_envelope_is_zero_without_ambiguity():
     if res.ambiguous == [0]:
         for E in res.E_dW_self + res.E_dW_neigh + res.E_db + res.E_dH:
             assert not np.any(E)
+
+
+# ----------------------------------------------------------------- Adam ----
+def test_adam_matches_torch_optim_adam_float64():
+    """Adam of Alg. 1 against torch.optim.Adam (an independent implementation),
+    both in float64, over several steps with changing gradients."""
+    import torch
+    from oracle import optim
+    rng = np.random.default_rng(0)
+    p0 = rng.standard_normal(1000)
+    tp = torch.tensor(p0.copy(), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([tp], lr=0.01, betas=(0.9, 0.999), eps=1e-8)
+    p, m, v = p0.copy(), np.zeros(1000), np.zeros(1000)
+    for t in range(1, 8):
+        g = rng.standard_normal(1000) * (10.0 ** rng.integers(-6, 2))
+        tp.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        p, m, v = optim.adam(p, g, m, v, t, 0.01)
+        assert np.max(np.abs(p - tp.detach().numpy())) <= 1e-12 * np.max(np.abs(p))
+
+
+def test_adam_closed_forms():
+    from oracle import optim
+    g = np.array([3.0, -2e-3, 0.0, 1e-12])
+    # first step from zero moments: lr * g / (|g| + eps)
+    p, m, v = optim.adam(np.zeros(4), g, np.zeros(4), np.zeros(4), 1, 0.1)
+    assert np.allclose(p, -0.1 * g / (np.abs(g) + 1e-8), rtol=1e-14, atol=0)
+    # a constant gradient keeps the bias-corrected moments equal to g and g^2
+    p, m, v = np.zeros(4), np.zeros(4), np.zeros(4)
+    for t in range(1, 6):
+        p, m, v = optim.adam(p, g, m, v, t, 0.1)
+    assert np.allclose(p, -5 * 0.1 * g / (np.abs(g) + 1e-8), rtol=1e-12, atol=1e-15)
