@@ -129,6 +129,128 @@ def measure_peaks(B, torch) -> dict:
     return out
 
 
+def chase_latency_ns(B, torch, n: int, chains: int, steps: int = 4000, seed: int = 0) -> float:
+    """Latency of one dependent load, ns, over an int32 random cycle of n
+    elements walked by `chains` wavefronts at once (gcn_peak_chase)."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    perm = rng.permutation(n).astype(np.int64)
+    nxt = np.empty(n, dtype=np.int32)
+    nxt[perm] = np.roll(perm, -1).astype(np.int32)
+    assert nxt.min() >= 0 and nxt.max() < n
+    d_next = torch.from_numpy(nxt).cuda()
+    sink = torch.empty(chains, dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    B.gcn_peak_chase(d_next, 200, chains, sink)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    B.gcn_peak_chase(d_next, steps, chains, sink)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e6 / steps
+
+
+def bench_sampler(args, B, torch):
+    """Frontier sampling (Sec. IV, Alg. 2-4) of S runs at once on a
+    Reddit-shaped R-MAT training graph, then the induced subgraphs of the batch
+    and one subgraph's feature gather.  One JSON line."""
+    import numpy as np
+    from paper_1810_11899_amd import synth
+    from oracle import sampler as OS  # cpu_baseline leg only
+    spec = synth.TRAINING_GRAPHS["reddit_like"]
+    t0 = time.perf_counter()
+    tg = synth.training_graph(**spec, seed=0)
+    gen_s = time.perf_counter() - t0
+    g = tg.graph
+    m, n, cap, eta = 1000, 8000, 30, 2.0
+    params = B.gcn_sampler_plan(g.indptr, m, n, eta=eta, cap=cap, seed=1)
+    S = args.sampler_runs
+    G = B.DeviceCSR.from_host(g.n, g.n, g.indptr, g.indices, g.vals)
+    X = torch.from_numpy(tg.X).cuda()
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    verts = torch.empty((S, n), dtype=torch.int32, device="cuda")
+    counts = torch.empty(S, dtype=torch.int32, device="cuda")
+    status = torch.empty(S, dtype=torch.int32, device="cuda")
+    for w in range(args.warmup):
+        B.gcn_frontier_sample(G, params, 10 ** 9 + w * S, S, verts, counts, status)
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    a.record(stream)
+    for k in range(args.steps):
+        B.gcn_frontier_sample(G, params, k * S, S, verts, counts, status)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    st = status.cpu().numpy()
+    c = counts.cpu().numpy()
+    sampled = float(c.sum())
+    # induced subgraphs of the last batch, and the feature gather of one of them
+    ws = B.Workspace("cuda")
+    ib = B.InducedBatch(S, n, int(S * n * 30), "cuda")
+    B.gcn_induce_subgraphs(G, verts, counts, ib, ws)
+    torch.cuda.synchronize()
+    if int(ib.status.item()) != 0:
+        ib = B.InducedBatch(S, n, int(ib.edge_offsets[-1].item()), "cuda")
+    a2, b2 = ev(), ev()
+    a2.record(stream)
+    B.gcn_induce_subgraphs(G, verts, counts, ib, ws)
+    b2.record(stream)
+    torch.cuda.synchronize()
+    induce_ms = a2.elapsed_time(b2)
+    n_sub = ib.n_sub.cpu().numpy()
+    nnz_sub = np.diff(ib.edge_offsets.cpu().numpy())
+    H0 = torch.empty((n, X.shape[1]), dtype=torch.float32, device="cuda")
+    a3, b3 = ev(), ev()
+    a3.record(stream)
+    for _ in range(10):
+        B.gcn_gather_rows(X, ib.vsub[0], int(n_sub[0]), H0)
+    b3.record(stream)
+    torch.cuda.synchronize()
+    gather_ms = a3.elapsed_time(b3) / 10
+    # latency bound: two dependent global loads per step, measured on a random
+    # cycle the size of G's neighbour array, at the same concurrency
+    lat = chase_latency_ns(B, torch, g.nnz, S)
+    steps_per_run_s = (n - m) / (ms / 1e3)
+    peak_steps = 1e9 / (2 * lat)
+    out = {
+        "metric": "frontier sampling (Dashboard, Alg. 2-4): sampled vertices/s",
+        "value": round(sampled / (ms / 1e3), 1), "unit": "sampled vertices/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int32", "data": "synthetic (seeded R-MAT training graph)",
+        "config": {"workload": f"frontier_{tg.name}_m{m}_n{n}_cap{cap}_runs{S}", "n_vertices": g.n, "nnz": g.nnz,
+                   "m": m, "n": n, "eta": eta, "cap": cap, "runs_per_launch": S,
+                   "db_entries": params.db_entries, "ia_slots": params.ia_slots,
+                   "lds_bytes_per_run": 12 * params.ia_slots + 2 * params.db_entries,
+                   "parallelism": "single GPU"},
+        "statuses": {B.SAMPLE_STATUS[int(k)]: int((st == k).sum()) for k in np.unique(st)},
+        "subgraphs_per_s": round(S / (ms / 1e3), 1),
+        "induce": {"ms_per_batch": round(induce_ms, 4), "subgraphs": S,
+                   "mean_vertices": float(n_sub.mean()), "mean_edges": float(nnz_sub.mean())},
+        "gather": {"ms_per_subgraph": round(gather_ms, 4), "rows": int(n_sub[0]), "width": int(X.shape[1]),
+                   "gbs": round(2 * 4 * int(n_sub[0]) * X.shape[1] / (gather_ms / 1e3) / 1e9, 1)},
+        "roofline": {"bound": "latency", "kernel": "frontier_sample", "achieved": round(steps_per_run_s, 1),
+                     "peak": round(peak_steps, 1), "unit": "steps/s per run", "frac": round(steps_per_run_s / peak_steps, 4),
+                     "dependent_load_ns": round(lat, 1), "traffic": None},
+        "graph_generation_s": round(gen_s, 1),
+    }
+    if not args.no_cpu_baseline:
+        reps, dt, tot = 0, 0.0, 0
+        while dt < args.cpu_seconds and reps < 100000:
+            t1 = time.perf_counter()
+            v, _ = OS.frontier_sample(g.indptr, g.indices, m, n, params.db_entries, params.ia_slots, cap=cap,
+                                      p=64, seed=1, sampler_id=reps)
+            dt += time.perf_counter() - t1
+            tot += v.size
+            reps += 1
+        out["cpu_baseline"] = {"value": round(tot / dt, 1), "unit": "sampled vertices/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": f"{reps} runs of the same sampler on the same graph, {dt:.1f} s; "
+                                         f"sequential C oracle (one thread)"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +262,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event timing")
     ap.add_argument("--no-peaks", action="store_true", help="skip the measured machine ceilings")
+    ap.add_argument("--workload", default="step", choices=["step", "sampler"],
+                    help="step: one fwd+bwd step of the layer (default); sampler: the frontier sampler")
+    ap.add_argument("--sampler-runs", type=int, default=512, help="sampler runs per launch")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for counter calibration)")
     args = ap.parse_args()
@@ -166,6 +291,9 @@ def main():
     from paper_1810_11899_amd.runner import StepRunner, step_work
 
     B.lib()
+    if args.workload == "sampler":
+        bench_sampler(args, B, torch)
+        return
     prec = B.PREC[args.prec]
     wl = synth.config(args.config)
     spec = synth.CONFIGS[args.config]

@@ -36,6 +36,15 @@ int gcn_peak_stream_read(const float *x, int64_t count, float *sink, int32_t blo
  * *flops (host pointer, may be NULL). */
 int gcn_peak_mfma(gcn_prec prec, int32_t blocks, int32_t iters, float *sink, double *flops, void *stream);
 
+/* Latency of dependent global loads: `chains` wavefronts each follow
+ * i <- next[i] for `steps` hops from their own start, one load in flight per
+ * wavefront; sink [chains] receives the last index.  next [n] must hold
+ * values in [0, n) (a random cycle measures the latency of the cache level
+ * that an array of n int32 lands in).  Time / steps is the latency per load
+ * at that concurrency: the bound of the frontier sampler, whose steps are
+ * chains of dependent loads (gcn_sampler.h). */
+int gcn_peak_chase(const int32_t *next, int64_t n, int32_t steps, int32_t chains, int32_t *sink, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

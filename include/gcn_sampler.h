@@ -32,10 +32,13 @@
  *   - a cleanup (Alg. 4) runs before an append that would overflow the
  *     Dashboard or the Index Array;
  *   - random numbers: Philox4x64-10 keyed by (seed, first_sampler + run
- *     index), counter (t, kind, 0, 0), word 0; an integer uniform on [0, N) is
- *     the high 64 bits of the word times N.  kind 1: root candidate t; kind 2:
- *     probe t = round * 64 + lane; kind 3: neighbour choice of step t.
- *     The same (seed, run id) gives the same subgraph on every device.
+ *     index); word w of the block with counter (c0, kind, c2, 0) gives an
+ *     integer uniform on [0, N) as the high 64 bits of the word times N.
+ *     Root candidate t: counter (t, 1, 0, 0), word 0.  Probe of lane j in
+ *     probing round r: counter (r / 4, 2, j, 0), word r % 4.  Neighbour
+ *     choice of step t (t = 0 for the first step after the roots): counter
+ *     (t / 4, 3, 0, 0), word t % 4.  The same (seed, run id) gives the same
+ *     subgraph on every device.
  */
 #ifndef GCN_SAMPLER_H_
 #define GCN_SAMPLER_H_
@@ -69,10 +72,10 @@ typedef struct {
 
 /* Sizes the Dashboard for enlargement factor eta > 1 (Sec. IV-B: eta * m *
  * the mean number of entries per vertex of G, and at least a frontier of m
- * vertices of the largest weight when that fits) and gives the Index Array
- * the LDS left over.  indptr_host is G's row pointer in HOST memory
- * [n_vertices + 1].  GCN_EUNSUPPORTED when a frontier of m vertices cannot fit
- * one CU's LDS (160 KB). */
+ * vertices of the largest weight, so that no run can overflow) with an Index
+ * Array of m + 512 slots, clamped to one CU's LDS (160 KB).  indptr_host is
+ * G's row pointer in HOST memory [n_vertices + 1].  GCN_EUNSUPPORTED when
+ * the Index Array alone cannot fit. */
 int gcn_sampler_plan(int32_t n_vertices, const int32_t *indptr_host, int32_t m, int32_t n, double eta,
                      int32_t cap, uint64_t seed, gcn_sampler_params *out);
 
@@ -81,7 +84,8 @@ int gcn_sampler_plan(int32_t n_vertices, const int32_t *indptr_host, int32_t m, 
  *   vertices [S x n]  run r's list in row r (entries past counts[r] untouched)
  *   counts   [S]      list length (n unless the status says otherwise)
  *   status   [S]      gcn_sample_status
- * Each run uses 8 ia_slots + 2 db_entries bytes of LDS (one CU's at most). */
+ * Each run uses 12 ia_slots + 2 db_entries bytes of LDS (one CU's at most);
+ * runs of at most 80 KB share a CU two at a time. */
 int gcn_frontier_sample(const gcn_csr *G, const gcn_sampler_params *p, int64_t first_sampler, int32_t S,
                         int32_t *vertices, int32_t *counts, int32_t *status, void *stream);
 

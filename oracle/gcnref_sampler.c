@@ -26,10 +26,12 @@
  *     Dashboard or the Index Array; it keeps the live slots in slot order;
  *   - the m roots are distinct: candidates are drawn one by one and a repeat
  *     is skipped.
- * Random draws: draw(kind, t) = word 0 of Philox4x64-10 with counter
- * (t, kind, 0, 0) and key (seed, sampler id); an integer uniform on [0, N) is
- * the high 64 bits of draw * N.  kind 1 = root candidates, 2 = probes (draw
- * t = round * p + processor), 3 = neighbour choice (t = step - m).
+ * Random draws: word w of the Philox4x64-10 block with counter (c0, kind, c2,
+ * 0) and key (seed, sampler id); an integer uniform on [0, N) is the high 64
+ * bits of the word times N.  Root candidate t: kind 1, counter (t, 1, 0, 0),
+ * word 0.  Probe of processor j in probing round r: kind 2, counter
+ * (r / 4, 2, j, 0), word r % 4.  Neighbour choice of step t = i - m: kind 3,
+ * counter (t / 4, 3, 0, 0), word t % 4.
  */
 #include <stdint.h>
 #include <stdlib.h>
@@ -71,11 +73,11 @@ void gcnref_philox4x64(const uint64_t ctr_in[4], const uint64_t key_in[2], uint6
     out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
 }
 
-static uint64_t draw(uint64_t seed, uint64_t sid, uint64_t kind, uint64_t t) {
-    const uint64_t ctr[4] = {t, kind, 0, 0}, key[2] = {seed, sid};
+static uint64_t draw(uint64_t seed, uint64_t sid, uint64_t kind, uint64_t c0, uint64_t c2, int word) {
+    const uint64_t ctr[4] = {c0, kind, c2, 0}, key[2] = {seed, sid};
     uint64_t out[4];
     gcnref_philox4x64(ctr, key, out);
-    return out[0];
+    return out[word];
 }
 
 static int64_t below(uint64_t r, int64_t n) {
@@ -126,7 +128,7 @@ int gcnref_frontier_sample(int64_t nV, const int32_t *indptr, const int32_t *ind
     const uint64_t root_limit = 64ull * (uint64_t)m + 65536ull;
     for (uint64_t t = 0; got < m; ++t) {
         if (t >= root_limit) { status = GCNREF_SAMPLE_ROOT_LIMIT; break; }
-        const int32_t v = (int32_t)below(draw(seed, sampler_id, KIND_ROOT, t), nV);
+        const int32_t v = (int32_t)below(draw(seed, sampler_id, KIND_ROOT, t, 0, 0), nV);
         if (is_root[v]) continue;
         is_root[v] = 1;
         out[got++] = v;
@@ -157,7 +159,8 @@ int gcnref_frontier_sample(int64_t nV, const int32_t *indptr, const int32_t *ind
         for (int64_t rr = 0; k < 0; ++rr, ++round) {
             if (rr >= PROBE_ROUND_LIMIT) { status = GCNREF_SAMPLE_PROBE_LIMIT; goto done; }
             for (int32_t j = 0; j < p; ++j) {
-                const int64_t idx = below(draw(seed, sampler_id, KIND_PROBE, round * (uint64_t)p + (uint64_t)j), used);
+                const int64_t idx = below(draw(seed, sampler_id, KIND_PROBE, round >> 2, (uint64_t)j, (int)(round & 3)),
+                                          used);
                 if (ia[db[idx]].live) { k = db[idx]; break; }
             }
         }
@@ -166,7 +169,8 @@ int gcnref_frontier_sample(int64_t nV, const int32_t *indptr, const int32_t *ind
         live_weight -= ia[k].weight;
 
         const int32_t deg = indptr[v_pop + 1] - indptr[v_pop];  /* >= 1: its weight was > 0 */
-        const int64_t pick = below(draw(seed, sampler_id, KIND_NEIGH, (uint64_t)(i - m)), deg);
+        const uint64_t t = (uint64_t)(i - m);
+        const int64_t pick = below(draw(seed, sampler_id, KIND_NEIGH, t >> 2, 0, (int)(t & 3)), deg);
         const int32_t v_new = indices[indptr[v_pop] + pick];
         const int32_t w = weight_of(indptr, v_new, cap);
 

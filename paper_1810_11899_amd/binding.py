@@ -90,6 +90,7 @@ _SIGNATURES = {
     # gcn_peaks.h
     "gcn_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _I32, _P]),
     "gcn_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I32, _I32, _P, ctypes.POINTER(ctypes.c_double), _P]),
+    "gcn_peak_chase": (ctypes.c_int, [_P, _I64, _I32, _I32, _P, _P]),
 }
 
 
@@ -415,3 +416,11 @@ def gcn_peak_mfma(prec: int, blocks: int, iters: int, sink: torch.Tensor, stream
     _check(lib().gcn_peak_mfma(prec, blocks, iters, _ptr(sink), ctypes.byref(fl), _stream(stream)),
            "gcn_peak_mfma")
     return fl.value
+
+
+def gcn_peak_chase(next_idx: torch.Tensor, steps: int, chains: int, sink: torch.Tensor, stream=None):
+    """Enqueue `chains` dependent-load walks of `steps` hops over next_idx (int32)."""
+    if next_idx.dtype != torch.int32 or sink.dtype != torch.int32 or sink.numel() < chains:
+        raise TypeError("int32 next_idx and an int32 sink of >= chains elements are needed")
+    _check(lib().gcn_peak_chase(_ptr(next_idx), next_idx.numel(), int(steps), int(chains), _ptr(sink),
+                                _stream(stream)), "gcn_peak_chase")

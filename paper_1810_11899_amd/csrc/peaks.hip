@@ -73,6 +73,18 @@ __global__ __launch_bounds__(kPeakThreads) void mfma_bf16_kernel(int32_t iters, 
     sink[(int64_t)blockIdx.x * kPeakThreads + threadIdx.x] = s;
 }
 
+// Dependent loads: each chain follows next[] for `steps` hops (one lane does
+// the walk, the wavefront waits on it as the sampler's wavefront waits on its
+// global loads).
+__global__ __launch_bounds__(64) void chase_kernel(const int32_t *__restrict__ next, int64_t n, int32_t steps,
+                                                   int32_t *__restrict__ sink) {
+    int64_t i = ((int64_t)blockIdx.x * 2654435761ll) % n;
+    if (threadIdx.x == 0) {
+        for (int32_t k = 0; k < steps; ++k) i = next[i];
+        sink[blockIdx.x] = (int32_t)i;
+    }
+}
+
 }  // namespace
 }  // namespace gcn
 
@@ -108,6 +120,17 @@ int gcn_peak_mfma(gcn_prec prec, int32_t blocks, int32_t iters, float *sink, dou
         mfma_bf16_kernel<<<blocks, kPeakThreads, 0, s>>>(iters, sink);
     GCN_LAUNCH_CHECK("mfma_kernel");
     if (flops) *flops = per_mfma * 4.0 * iters * (blocks * (kPeakThreads / kWave));
+    return GCN_OK;
+}
+
+int gcn_peak_chase(const int32_t *next, int64_t n, int32_t steps, int32_t chains, int32_t *sink, void *stream) {
+    if (!next || !sink || n <= 0 || steps < 0 || chains <= 0) {
+        set_error("gcn_peak_chase: null pointer or bad size");
+        return GCN_EINVAL;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    chase_kernel<<<chains, 64, 0, s>>>(next, n, steps, sink);
+    GCN_LAUNCH_CHECK("chase_kernel");
     return GCN_OK;
 }
 

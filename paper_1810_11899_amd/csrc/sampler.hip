@@ -12,11 +12,13 @@
 //   gather kernel    feature (or label) rows of the sampled vertices
 //
 // Dashboard layout (LDS, per sampler): db[entries] holds, for every entry, the
-// Index-Array slot it belongs to (16 bits); slot k holds its vertex and its
-// weight, with the live flag in bit 31.  Popping a vertex clears one flag,
-// which invalidates all of its entries at once; the paper's Alg. 4 writes INV
-// into each of them.  Random numbers: Philox4x64-10 (Salmon et al., SC 2011)
-// keyed by (seed, sampler id), counter (t, kind, 0, 0).
+// Index-Array slot it belongs to (16 bits); slot k holds its vertex, the start
+// of its neighbour list in G and its degree, with the live flag in bit 31.
+// Popping a vertex clears one flag, which invalidates all of its entries at
+// once (the paper's Alg. 4 writes INV into each of them), and reads no global
+// memory; a step then costs two dependent global loads (the chosen neighbour,
+// then its row bounds).  Random numbers: Philox4x64-10 (Salmon et al.,
+// SC 2011) keyed by (seed, sampler id); each block gives four draws.
 #include <algorithm>
 #include <cmath>
 
@@ -34,29 +36,35 @@ constexpr uint64_t kKindRoot = 1, kKindProbe = 2, kKindNeigh = 3;
 constexpr int64_t kProbeRoundLimit = 1 << 20;
 
 // ---------------------------------------------------------------- Philox
-__device__ __forceinline__ uint64_t philox_word0(uint64_t t, uint64_t kind, uint64_t seed, uint64_t sid) {
+// One Philox4x64-10 block: counter (c0, kind, c2, 0), key (seed, sampler id).
+struct Words {
+    uint64_t w0, w1, w2, w3;
+    __device__ __forceinline__ uint64_t get(uint32_t i) const {
+        return i == 0 ? w0 : (i == 1 ? w1 : (i == 2 ? w2 : w3));
+    }
+};
+__device__ __forceinline__ Words philox(uint64_t c0, uint64_t kind, uint64_t c2, uint64_t seed, uint64_t sid) {
     const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
     const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
-    uint64_t c0 = t, c1 = kind, c2 = 0, c3 = 0, k0 = seed, k1 = sid;
+    uint64_t x0 = c0, x1 = kind, x2 = c2, x3 = 0, k0 = seed, k1 = sid;
 #pragma unroll
     for (int r = 0; r < 10; ++r) {
-        const uint64_t lo0 = M0 * c0, hi0 = __umul64hi(M0, c0);
-        const uint64_t lo1 = M1 * c2, hi1 = __umul64hi(M1, c2);
-        c0 = hi1 ^ c1 ^ k0;
-        c1 = lo1;
-        c2 = hi0 ^ c3 ^ k1;
-        c3 = lo0;
+        const uint64_t lo0 = M0 * x0, hi0 = __umul64hi(M0, x0);
+        const uint64_t lo1 = M1 * x2, hi1 = __umul64hi(M1, x2);
+        x0 = hi1 ^ x1 ^ k0;
+        x1 = lo1;
+        x2 = hi0 ^ x3 ^ k1;
+        x3 = lo0;
         k0 += W0;
         k1 += W1;
     }
-    return c0;
+    return Words{x0, x1, x2, x3};
 }
 // integer uniform on [0, n): high word of r * n
 __device__ __forceinline__ int64_t below(uint64_t r, int64_t n) { return (int64_t)__umul64hi(r, (uint64_t)n); }
 
-__device__ __forceinline__ int32_t weight_of(const int32_t *__restrict__ indptr, int32_t v, int32_t cap) {
-    const int32_t d = indptr[v + 1] - indptr[v];
-    return (cap > 0 && d > cap) ? cap : d;
+__device__ __forceinline__ int32_t weight_of_deg(uint32_t d, int32_t cap) {
+    return (cap > 0 && (int32_t)d > cap) ? cap : (int32_t)d;
 }
 
 // inclusive prefix sum over the 64 lanes
@@ -83,23 +91,34 @@ struct SampArgs {
     int32_t *status;     // [S]
 };
 
+// Index-Array slots in LDS: vertex, start of its neighbour list in G, and
+// degree with the live flag (the slot keeps what a pop needs, so popping
+// reads no global memory).
+struct Slots {
+    int32_t *v;
+    int32_t *beg;
+    uint32_t *deg;   // degree | kLive
+};
+
 // Cleanup (Alg. 4): keep the live slots in slot order, renumber them, and
 // rebuild the Dashboard from their weights.  Whole wavefront.
-__device__ void dashboard_cleanup(uint16_t *db, int32_t *sv, uint32_t *sw, int32_t &s, int64_t &used) {
+__device__ void dashboard_cleanup(uint16_t *db, Slots sl, int32_t cap, int32_t &s, int64_t &used) {
     const int lane = threadIdx.x;
     int32_t ns = 0;
     for (int32_t base = 0; base < s; base += 64) {
         const int32_t k = base + lane;
         const bool in = k < s;
-        const int32_t v = in ? sv[k] : 0;
-        const uint32_t w = in ? sw[k] : 0u;
-        const bool live = in && (w & kLive);
+        const int32_t v = in ? sl.v[k] : 0;
+        const int32_t b = in ? sl.beg[k] : 0;
+        const uint32_t d = in ? sl.deg[k] : 0u;
+        const bool live = in && (d & kLive);
         const uint64_t mask = __ballot(live);
         const int rank = __popcll(mask & ((1ull << lane) - 1ull));
         __syncthreads();            // every lane has read its slot before any moves
         if (live) {
-            sv[ns + rank] = v;
-            sw[ns + rank] = w;
+            sl.v[ns + rank] = v;
+            sl.beg[ns + rank] = b;
+            sl.deg[ns + rank] = d;
         }
         ns += __popcll(mask);
         __syncthreads();
@@ -108,7 +127,7 @@ __device__ void dashboard_cleanup(uint16_t *db, int32_t *sv, uint32_t *sw, int32
     int64_t off = 0;
     for (int32_t base = 0; base < ns; base += 64) {
         const int32_t k = base + lane;
-        const int32_t w = k < ns ? (int32_t)(sw[k] & ~kLive) : 0;
+        const int32_t w = k < ns ? weight_of_deg(sl.deg[k] & ~kLive, cap) : 0;
         const int64_t incl = wave_incl_scan(w);
         const int64_t start = off + incl - w;
         for (int32_t e = 0; e < w; ++e) db[start + e] = (uint16_t)k;
@@ -120,9 +139,11 @@ __device__ void dashboard_cleanup(uint16_t *db, int32_t *sv, uint32_t *sw, int32
 
 __global__ __launch_bounds__(kSampThreads) void frontier_kernel(SampArgs a) {
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-    int32_t *sv = (int32_t *)lds;                       // slot vertex   [ia_cap]
-    uint32_t *sw = (uint32_t *)(sv + a.ia_cap);         // slot weight | live [ia_cap]
-    uint16_t *db = (uint16_t *)(sw + a.ia_cap);         // Dashboard     [db_cap]
+    Slots sl;
+    sl.v = (int32_t *)lds;                              // [ia_cap]
+    sl.beg = sl.v + a.ia_cap;                           // [ia_cap]
+    sl.deg = (uint32_t *)(sl.beg + a.ia_cap);           // [ia_cap]
+    uint16_t *db = (uint16_t *)(sl.deg + a.ia_cap);     // Dashboard [db_cap]
     const int lane = threadIdx.x;
     const uint64_t sid = (uint64_t)(a.first_sampler + blockIdx.x);
     int32_t *out = a.vertices + (int64_t)blockIdx.x * a.n;
@@ -137,9 +158,9 @@ __global__ __launch_bounds__(kSampThreads) void frontier_kernel(SampArgs a) {
         for (uint64_t base = 0; got < a.m; base += 64) {
             if (base >= limit) { status = GCN_SAMPLE_ROOT_LIMIT; break; }
             const uint64_t t = base + lane;
-            const int32_t c = (int32_t)below(philox_word0(t, kKindRoot, a.seed, sid), a.nV);
+            const int32_t c = (int32_t)below(philox(t, kKindRoot, 0, a.seed, sid).w0, a.nV);
             bool dup = t >= limit;
-            for (int32_t k = 0; k < got && !dup; ++k) dup = (sv[k] == c);
+            for (int32_t k = 0; k < got && !dup; ++k) dup = (sl.v[k] == c);
             for (int j = 0; j < 64; ++j) {
                 const int32_t cj = __shfl(c, j, 64);
                 if (j < lane && cj == c) dup = true;
@@ -147,7 +168,7 @@ __global__ __launch_bounds__(kSampThreads) void frontier_kernel(SampArgs a) {
             const uint64_t mask = __ballot(!dup);
             const int rank = __popcll(mask & ((1ull << lane) - 1ull));
             if (!dup && got + rank < a.m) {
-                sv[got + rank] = c;
+                sl.v[got + rank] = c;
                 out[got + rank] = c;
             }
             got += min(__popcll(mask), a.m - got);
@@ -162,13 +183,21 @@ __global__ __launch_bounds__(kSampThreads) void frontier_kernel(SampArgs a) {
         // ---- Dashboard from the roots (Alg. 3, initialisation)
         for (int32_t base = 0; base < a.m; base += 64) {
             const int32_t k = base + lane;
-            const int32_t w = k < a.m ? weight_of(a.indptr, sv[k], a.cap) : 0;
+            int32_t b = 0;
+            uint32_t d = 0;
+            if (k < a.m) {
+                const int32_t v = sl.v[k];
+                b = a.indptr[v];
+                d = (uint32_t)(a.indptr[v + 1] - b);
+            }
+            const int32_t w = weight_of_deg(d, a.cap);
             const int64_t incl = wave_incl_scan(w);
             const int64_t total = __shfl(incl, 63, 64);
             if (used + total > a.db_cap) { status = GCN_SAMPLE_OVERFLOW; break; }
             const int64_t start = used + incl - w;
             if (k < a.m) {
-                sw[k] = (uint32_t)w | kLive;
+                sl.beg[k] = b;
+                sl.deg[k] = d | kLive;
                 for (int32_t e = 0; e < w; ++e) db[start + e] = (uint16_t)k;
             }
             used += total;
@@ -178,17 +207,30 @@ __global__ __launch_bounds__(kSampThreads) void frontier_kernel(SampArgs a) {
         __syncthreads();
     }
 
-    // ---- main loop: pop a frontier vertex, step to a neighbour, add it
+    // ---- main loop: pop a frontier vertex, step to a neighbour, add it.
+    // Random blocks are drawn ahead, while the step's global loads are in
+    // flight: probe block r/4 of this lane, neighbour block t/4.
     uint64_t round = 0;
+    int64_t pblk = -1, nblk = -1;
+    Words pw{0, 0, 0, 0}, nw{0, 0, 0, 0};
     for (int32_t i = a.m; status == GCN_SAMPLE_OK && i < a.n; ++i) {
         if (live_weight == 0) { status = GCN_SAMPLE_EXHAUSTED; break; }
-        const uint64_t rn = philox_word0((uint64_t)(i - a.m), kKindNeigh, a.seed, sid);
+        const uint64_t t = (uint64_t)(i - a.m);
+        if ((int64_t)(t >> 2) != nblk) {
+            nw = philox(t >> 2, kKindNeigh, 0, a.seed, sid);
+            nblk = (int64_t)(t >> 2);
+        }
+        const uint64_t rn = nw.get((uint32_t)(t & 3));
         int32_t k = -1;
         for (int64_t rr = 0;; ++rr) {
             if (rr >= kProbeRoundLimit) { status = GCN_SAMPLE_PROBE_LIMIT; break; }
-            const int64_t idx = below(philox_word0(round * 64 + lane, kKindProbe, a.seed, sid), used);
+            if ((int64_t)(round >> 2) != pblk) {
+                pw = philox(round >> 2, kKindProbe, (uint64_t)lane, a.seed, sid);
+                pblk = (int64_t)(round >> 2);
+            }
+            const int64_t idx = below(pw.get((uint32_t)(round & 3)), used);
             const int32_t slot = db[idx];
-            const uint64_t mask = __ballot((sw[slot] & kLive) != 0u);
+            const uint64_t mask = __ballot((sl.deg[slot] & kLive) != 0u);
             ++round;
             if (mask) {
                 k = __shfl(slot, __ffsll((unsigned long long)mask) - 1, 64);
@@ -196,25 +238,35 @@ __global__ __launch_bounds__(kSampThreads) void frontier_kernel(SampArgs a) {
             }
         }
         if (status != GCN_SAMPLE_OK) break;
-        const int32_t v_pop = sv[k];
-        const uint32_t w_pop = sw[k] & ~kLive;
+        const int32_t beg = sl.beg[k];
+        const uint32_t deg = sl.deg[k] & ~kLive;    // >= 1: its weight was > 0
         __syncthreads();
-        if (lane == 0) sw[k] = w_pop;               // no longer in the frontier
-        live_weight -= w_pop;
+        if (lane == 0) sl.deg[k] = deg;             // no longer in the frontier
+        live_weight -= weight_of_deg(deg, a.cap);
 
-        const int32_t beg = a.indptr[v_pop];
-        const int32_t deg = a.indptr[v_pop + 1] - beg;   // >= 1: its weight was > 0
-        const int32_t v_new = a.indices[beg + below(rn, deg)];
+        const int32_t v_new = a.indices[beg + below(rn, (int64_t)deg)];
+        // draw ahead while the load is in flight
+        if ((int64_t)((t + 1) >> 2) != nblk) {
+            nw = philox((t + 1) >> 2, kKindNeigh, 0, a.seed, sid);
+            nblk = (int64_t)((t + 1) >> 2);
+        }
+        if ((int64_t)(round >> 2) != pblk) {
+            pw = philox(round >> 2, kKindProbe, (uint64_t)lane, a.seed, sid);
+            pblk = (int64_t)(round >> 2);
+        }
         if ((uint32_t)v_new >= (uint32_t)a.nV) { status = GCN_SAMPLE_BAD_GRAPH; break; }
-        const int32_t w = weight_of(a.indptr, v_new, a.cap);
+        const int32_t b2 = a.indptr[v_new];
+        const uint32_t d2 = (uint32_t)(a.indptr[v_new + 1] - b2);
+        const int32_t w = weight_of_deg(d2, a.cap);
 
         __syncthreads();
-        if (used + w > a.db_cap || s == a.ia_cap) dashboard_cleanup(db, sv, sw, s, used);
+        if (used + w > a.db_cap || s == a.ia_cap) dashboard_cleanup(db, sl, a.cap, s, used);
         if (used + w > a.db_cap) { status = GCN_SAMPLE_OVERFLOW; break; }
         for (int32_t e = lane; e < w; e += 64) db[used + e] = (uint16_t)s;
         if (lane == 0) {
-            sv[s] = v_new;
-            sw[s] = (uint32_t)w | kLive;
+            sl.v[s] = v_new;
+            sl.beg[s] = b2;
+            sl.deg[s] = d2 | kLive;
             out[i] = v_new;
         }
         used += w;
@@ -469,7 +521,7 @@ int blocks_for(int64_t n, int per) { return (int)std::min<int64_t>((n + per - 1)
 }  // namespace
 
 size_t sampler_lds_bytes(int32_t db_cap, int32_t ia_cap) {
-    return align256((size_t)ia_cap * 8 + (size_t)db_cap * 2);
+    return align256((size_t)ia_cap * 12 + (size_t)db_cap * 2);
 }
 
 int frontier_sample(const SampArgs &a, int32_t S, size_t lds, hipStream_t s) {
@@ -525,24 +577,20 @@ int gcn_sampler_plan(int32_t n_vertices, const int32_t *indptr_host, int32_t m, 
         sum_w += (double)d;
         wmax = std::max(wmax, d);
     }
-    // Dashboard of eta * m * (mean entries per vertex) entries (Sec. IV-B), at
-    // least enough for a frontier of m vertices of the largest weight when that
-    // fits; Index Array from the LDS left over, up to 16-bit slot ids.
-    int64_t db = (int64_t)std::ceil(eta * (double)m * (sum_w / n_vertices));
-    db = std::max<int64_t>(db, std::min<int64_t>((int64_t)m * wmax, (int64_t)(kSamplerMaxLds / 2)));
-    db = std::max<int64_t>(db, 1);
-    const int64_t min_ia = (int64_t)m + 64;
-    if ((size_t)min_ia * 8 + (size_t)db * 2 > kSamplerMaxLds) {
-        db = ((int64_t)kSamplerMaxLds - min_ia * 8) / 2;
-    }
-    if (db < 1 || min_ia > 65535) {
+    // Dashboard of eta * m * (mean entries per vertex) entries (Sec. IV-B), and
+    // at least a frontier of m vertices of the largest weight (no overflow is
+    // then possible); Index Array m + 512 slots.  Clamped to one CU's LDS;
+    // at <= 80 KB two samplers share a CU.
+    const int64_t ia = std::min<int64_t>((int64_t)m + 512, 65535);
+    if (ia <= m || (size_t)ia * 12 + 2 > kSamplerMaxLds) {
         set_error("gcn_sampler_plan: a frontier of m = %d does not fit the %zu bytes of LDS", m,
                   (size_t)kSamplerMaxLds);
         return GCN_EUNSUPPORTED;
     }
-    int64_t ia = ((int64_t)kSamplerMaxLds - db * 2) / 8;
-    ia = std::min<int64_t>(ia, 65535);
-    ia = std::min<int64_t>(ia, std::max<int64_t>(min_ia, 4 * (int64_t)m + 64));
+    int64_t db = (int64_t)std::ceil(eta * (double)m * (sum_w / n_vertices));
+    db = std::max<int64_t>(db, (int64_t)m * wmax);
+    db = std::max<int64_t>(db, 1);
+    db = std::min<int64_t>(db, ((int64_t)kSamplerMaxLds - ia * 12) / 2);
     out->m = m;
     out->n = n;
     out->db_entries = (int32_t)db;
