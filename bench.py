@@ -251,6 +251,114 @@ def bench_sampler(args, B, torch):
     print(json.dumps(out), flush=True)
 
 
+PHASES = {  # the time breakdown of Sec. VI-C (Fig. 3): sampling, propagation, weights
+    "sampling": ("frontier_sample", "induce_subgraphs"),
+    "feature_propagation": ("spmm", "spmm_fixup", "spmm_bf16"),
+    "weight_application": ("gemm_nn", "gemm_tn", "gemm_nt", "splitk_reduce", "gemm_nn_bf16", "gemm_tn_bf16",
+                           "gemm_nt_bf16"),
+}
+
+
+def bench_train(args, B, torch):
+    """Alg. 5 on one GPU: frontier-sampled subgraphs of a Reddit-shaped
+    training graph, 2-layer GCN (602 -> 2x128 -> 2x128, softmax-CE over 41
+    classes), ADAM; pools of subgraphs sampled on a side stream while the
+    compute stream trains.  One JSON line."""
+    import numpy as np
+    import oracle
+    from oracle import optim as OO
+    from oracle import sampler as OS
+    from paper_1810_11899_amd import synth
+    from paper_1810_11899_amd.train import SamplerConfig, Trainer
+    spec = synth.TRAINING_GRAPHS["reddit_like"]
+    tg = synth.training_graph(**spec, seed=0)
+    dims = [(602, 128), (256, 128)]
+    cfg = SamplerConfig(m=1000, n=8000, eta=2.0, cap=30, pool=args.pool, seed=1)
+    tr = Trainer(tg, dims, cfg, lr=0.01, prec=B.PREC[args.prec])
+    for _ in range(args.train_warmup):
+        tr.step()
+    torch.cuda.synchronize()
+    B.gcn_profile_reset()
+    B.gcn_profile_enable(not args.no_profile)
+    stream = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    verts = edges = 0
+    t0 = time.perf_counter()
+    a.record(stream)
+    for _ in range(args.train_iters):
+        ns, nnz = tr.step()
+        verts += ns
+        edges += nnz
+    b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    B.gcn_profile_enable(False)
+    K = args.train_iters
+    ms_it = wall * 1e3 / K
+    losses = tr.loss_history()
+    ef = 0.0   # edge-features of the iterations (aggregation widths of the orders used)
+    for (f_in, h), o, li in zip(dims, tr.orders, range(len(dims))):
+        if o == B.GCN_AGGREGATE_FIRST:
+            ef += f_in + (min(f_in, h) if li > 0 else 0)
+        else:
+            ef += 2 * h
+    phases, kernels = {}, {}
+    if not args.no_profile:
+        prof = B.gcn_profile_read_all()
+        for name, (ms, launches, flops, bytes_) in prof.items():
+            if launches:
+                kernels[name] = {"ms_per_iteration": round(ms / K, 4), "launches_per_iteration": launches / K}
+        for ph, names in PHASES.items():
+            phases[ph] = round(sum(prof[nm][0] for nm in names if nm in prof) / K, 4)
+        phases["other"] = round(sum(v["ms_per_iteration"] for v in kernels.values()) - sum(phases.values()), 4)
+    out = {
+        "metric": "GCN training with frontier sampling (Alg. 5): iterations/s",
+        "value": round(K / wall, 2), "unit": "iterations/s", "n_gpus": 1, "steps": K,
+        "warmup": args.train_warmup, "ms_per_step": round(ms_it, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": args.prec, "data": "synthetic (seeded R-MAT training graph, random labels)",
+        "config": {"workload": f"train_{tg.name}_602-128-128_ce41_m1000_n8000_pool{args.pool}",
+                   "n_vertices": tg.graph.n, "nnz": tg.graph.nnz, "layers": [list(d) for d in dims],
+                   "orders": ["aggregate_first" if o == B.GCN_AGGREGATE_FIRST else "transform_first"
+                              for o in tr.orders], "parallelism": "single GPU"},
+        "mean_subgraph_vertices": verts / K, "mean_subgraph_edges": edges / K,
+        "edge_features_per_s": round(edges * ef / wall, 1),
+        "compute_stream_ms_per_iteration": round(a.elapsed_time(b) / K, 4),
+        "phases_ms_per_iteration": phases, "kernels": kernels,
+        "loss_first_last": [float(losses[0]), float(losses[-1])],
+    }
+    if not args.no_cpu_baseline:
+        # the oracle pipeline on the same graph: sample, induce, fwd/bwd, ADAM
+        g = tg.graph
+        P = {k: v.astype(np.float64) for k, v in tr.model.host_tensors().items()}
+        M = {k: np.zeros_like(v) for k, v in P.items()}
+        V = {k: np.zeros_like(v) for k, v in P.items()}
+        sp = synth.Spec("train", 0, "rmat", 0, dims, "ce", tg.classes)
+        reps, dt = 0, 0.0
+        while dt < args.cpu_seconds and reps < 50:
+            t1 = time.perf_counter()
+            v, _ = OS.frontier_sample(g.indptr, g.indices, cfg.m, cfg.n, tr.params.db_entries, tr.params.ia_slots,
+                                      cap=cfg.cap, p=64, seed=cfg.seed, sampler_id=10 ** 6 + reps)
+            vs, ip, ix, vals = OS.induce(g.indptr, g.indices, v)
+            layers = [synth.Layer(P[f"W_self{i}"].astype(np.float32), P[f"W_neigh{i}"].astype(np.float32),
+                                  P[f"bias{i}"].astype(np.float32)) for i in range(len(dims))]
+            wl = synth.Workload(sp, 0, synth.Graph(vs.size, ip, ix, vals), OS.gather_rows(tg.X, vs), layers,
+                                W_pred=P["W_pred"].astype(np.float32), b_pred=P["b_pred"].astype(np.float32),
+                                labels=OS.gather_rows(tg.labels, vs))
+            r = oracle.step(wl)
+            grads = {"W_pred": r.dW_pred, "b_pred": r.db_pred}
+            for i in range(len(dims)):
+                grads[f"W_self{i}"], grads[f"W_neigh{i}"], grads[f"bias{i}"] = r.dW_self[i], r.dW_neigh[i], r.db[i]
+            for k in P:
+                P[k], M[k], V[k] = OO.adam(P[k], grads[k], M[k], V[k], reps + 1, 0.01)
+            dt += time.perf_counter() - t1
+            reps += 1
+        out["cpu_baseline"] = {"value": round(reps / dt, 4), "unit": "iterations/s", "cores": oracle.num_threads(),
+                               "kind": "oracle",
+                               "sample": f"{reps} iterations of the oracle pipeline (sampler, induced subgraph, "
+                                         f"float64 fwd/bwd, ADAM) on the same graph, {dt:.1f} s"}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -262,8 +370,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event timing")
     ap.add_argument("--no-peaks", action="store_true", help="skip the measured machine ceilings")
-    ap.add_argument("--workload", default="step", choices=["step", "sampler"],
-                    help="step: one fwd+bwd step of the layer (default); sampler: the frontier sampler")
+    ap.add_argument("--workload", default="step", choices=["step", "sampler", "train"],
+                    help="step: one fwd+bwd step of the layer (default); sampler: the frontier sampler; "
+                         "train: the sampled-subgraph training loop")
+    ap.add_argument("--pool", type=int, default=256, help="subgraphs per pool refill (train)")
+    ap.add_argument("--train-iters", type=int, default=600)
+    ap.add_argument("--train-warmup", type=int, default=40)
     ap.add_argument("--sampler-runs", type=int, default=512, help="sampler runs per launch")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this size (for counter calibration)")
@@ -293,6 +405,9 @@ def main():
     B.lib()
     if args.workload == "sampler":
         bench_sampler(args, B, torch)
+        return
+    if args.workload == "train":
+        bench_train(args, B, torch)
         return
     prec = B.PREC[args.prec]
     wl = synth.config(args.config)
