@@ -99,6 +99,14 @@ int gcn_frontier_sample(const gcn_csr *G, const gcn_sampler_params *p, int64_t f
  *                                 row i lists the local ids of the neighbours
  *                                 of vsub[i] in the set, ascending, with value
  *                                 1/(row length) (float32 quotient)
+ *   sub_vals_t (may be NULL)      entry p of row i, column j = sub_indices[p],
+ *                                 gets 1/(row length of j): when G's pattern
+ *                                 is symmetric (gcn_csr_pattern_symmetric_host)
+ *                                 so is each induced subgraph's, and
+ *                                 (indptr_sub, sub_indices, sub_vals_t) is then
+ *                                 the CSR of the transposed aggregation
+ *                                 matrix, equal bit for bit to what
+ *                                 gcn_csr_transpose returns
  *   edge_offsets [S+1]            int64 prefix of the subgraphs' edge counts
  *   status [1]                    0, or 1 when edge_offsets[S] > edge_capacity
  *                                 (then no edge is written; size the arrays
@@ -108,8 +116,13 @@ int gcn_frontier_sample(const gcn_csr *G, const gcn_sampler_params *p, int64_t f
 size_t gcn_induce_workspace_bytes(int32_t n_vertices, int32_t n, int32_t S);
 int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *vertices, const int32_t *counts,
                          int32_t *n_sub, int32_t *vsub, int32_t *indptr_sub, int64_t *edge_offsets,
-                         int32_t *sub_indices, float *sub_vals, int64_t edge_capacity, int32_t *status,
-                         void *ws, size_t ws_bytes, void *stream);
+                         int32_t *sub_indices, float *sub_vals, float *sub_vals_t, int64_t edge_capacity,
+                         int32_t *status, void *ws, size_t ws_bytes, void *stream);
+
+/* 1 when every stored (i, j) of the CSR in HOST memory has a stored (j, i),
+ * 0 when not; rows must hold ascending column indices (GCN_EINVAL if not, or
+ * if an index is out of range).  O(nnz log(max degree)). */
+int gcn_csr_pattern_symmetric_host(int32_t n, const int32_t *indptr_host, const int32_t *indices_host);
 
 /* out[i, 0:width] = X[rows[i], 0:width] for i < count, 4-byte elements (float
  * features or int32 labels), leading dimensions in elements.  A row index

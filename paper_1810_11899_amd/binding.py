@@ -81,8 +81,9 @@ _SIGNATURES = {
     "gcn_frontier_sample": (ctypes.c_int, [_CSRP, ctypes.POINTER(gcn_sampler_params), _I64, _I32, _P, _P, _P,
                                            _P]),
     "gcn_induce_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
-    "gcn_induce_subgraphs": (ctypes.c_int, [_CSRP, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P, _P,
-                                            _SZ, _P]),
+    "gcn_induce_subgraphs": (ctypes.c_int, [_CSRP, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _I64, _P,
+                                            _P, _SZ, _P]),
+    "gcn_csr_pattern_symmetric_host": (ctypes.c_int, [_I32, _P, _P]),
     "gcn_gather_rows": (ctypes.c_int, [_P, _I32, _I32, _I64, _P, _I32, _P, _I64, _P]),
     # gcn_optim.h
     "gcn_adam_update": (ctypes.c_int, [_P, _P, _P, _P, _I64, ctypes.c_double, ctypes.c_double, ctypes.c_double,
@@ -317,7 +318,7 @@ def gcn_frontier_sample(G: DeviceCSR, params: gcn_sampler_params, first_sampler:
 class InducedBatch:
     """Device outputs of gcn_induce_subgraphs for S vertex lists of length n."""
 
-    def __init__(self, S: int, n: int, edge_capacity: int, device):
+    def __init__(self, S: int, n: int, edge_capacity: int, device, with_transpose: bool = False):
         self.S, self.n = S, n
         d = torch.device(device)
         self.n_sub = torch.empty(max(S, 1), dtype=torch.int32, device=d)
@@ -327,11 +328,19 @@ class InducedBatch:
         self.edge_capacity = int(edge_capacity)
         self.indices = torch.empty(max(self.edge_capacity, 1), dtype=torch.int32, device=d)
         self.vals = torch.empty(max(self.edge_capacity, 1), dtype=torch.float32, device=d)
+        self.vals_t = (torch.empty(max(self.edge_capacity, 1), dtype=torch.float32, device=d)
+                       if with_transpose else None)
         self.status = torch.empty(1, dtype=torch.int32, device=d)
 
     def csr(self, s: int, n_sub: int, e0: int, e1: int) -> DeviceCSR:
         """Subgraph s as a DeviceCSR (host copies of n_sub / edge offsets given)."""
         return DeviceCSR(n_sub, n_sub, self.indptr[s, :n_sub + 1], self.indices[e0:e1], self.vals[e0:e1])
+
+    def csr_t(self, s: int, n_sub: int, e0: int, e1: int) -> DeviceCSR:
+        """The transposed aggregation matrix of subgraph s (symmetric G only)."""
+        if self.vals_t is None:
+            raise ValueError("built without the transposed values")
+        return DeviceCSR(n_sub, n_sub, self.indptr[s, :n_sub + 1], self.indices[e0:e1], self.vals_t[e0:e1])
 
 
 def gcn_induce_subgraphs(G: DeviceCSR, vertices: torch.Tensor, counts: torch.Tensor, out: InducedBatch,
@@ -343,9 +352,20 @@ def gcn_induce_subgraphs(G: DeviceCSR, vertices: torch.Tensor, counts: torch.Ten
     g = G.struct()
     _check(L.gcn_induce_subgraphs(ctypes.byref(g), S, n, _ptr(vertices), _ptr(counts), _ptr(out.n_sub),
                                   _ptr(out.vsub), _ptr(out.indptr), _ptr(out.edge_offsets), _ptr(out.indices),
-                                  _ptr(out.vals), out.edge_capacity, _ptr(out.status), w, wb, _stream(stream)),
+                                  _ptr(out.vals), _ptr(out.vals_t), out.edge_capacity, _ptr(out.status), w, wb,
+                                  _stream(stream)),
            "gcn_induce_subgraphs")
     return out
+
+
+def gcn_csr_pattern_symmetric_host(indptr, indices) -> bool:
+    import numpy as np
+    ip = np.ascontiguousarray(indptr, dtype=np.int32)
+    ix = np.ascontiguousarray(indices, dtype=np.int32)
+    r = lib().gcn_csr_pattern_symmetric_host(int(ip.size - 1), ip.ctypes.data, ix.ctypes.data if ix.size else None)
+    if r < 0:
+        _check(r, "gcn_csr_pattern_symmetric_host")
+    return bool(r)
 
 
 def gcn_gather_rows(X: torch.Tensor, rows: torch.Tensor, count: int, out: torch.Tensor, stream=None):

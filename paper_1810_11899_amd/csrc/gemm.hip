@@ -181,6 +181,18 @@ constexpr int kTBN = GCN_GEMM_TBN;
 #ifndef GCN_GEMM_WAVES_PER_EU
 #define GCN_GEMM_WAVES_PER_EU 4
 #endif
+// A wavefront issuing matrix-core products runs at raised priority, so that
+// the SIMD's arbiter feeds the matrix pipe before the other wavefronts' loads.
+#ifndef GCN_GEMM_SETPRIO
+#define GCN_GEMM_SETPRIO 1
+#endif
+#if GCN_GEMM_SETPRIO
+#define GCN_PRIO_UP() __builtin_amdgcn_s_setprio(1)
+#define GCN_PRIO_DOWN() __builtin_amdgcn_s_setprio(0)
+#else
+#define GCN_PRIO_UP() ((void)0)
+#define GCN_PRIO_DOWN() ((void)0)
+#endif
 template <int LAYOUT, bool VEC, int TBM, int TBN>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(GCN_GEMM_WAVES_PER_EU)))
 void gemm_kernel(DevArgs args) {
@@ -210,13 +222,20 @@ void gemm_kernel(DevArgs args) {
     TileLoader<T, BK, A_KMAJOR, VEC, TBM> la;
     TileLoader<T, BK, B_KMAJOR, VEC, TBN> lb;
 
+    // the two K-segments' descriptors, read once
+    const T *const A0 = (const T *)P.s.A[0], *const A1 = (const T *)P.s.A[1];
+    const T *const B0 = (const T *)P.s.B[0], *const B1 = (const T *)P.s.B[1];
+    const int64_t lda0 = P.s.lda[0], lda1 = P.s.lda[1], ldb0 = P.s.ldb[0], ldb1 = P.s.ldb[1];
+    const int K0 = P.s.K[0], K1 = P.s.K[1], kt0 = P.s.kt[0];
+    const int Mp = P.M, Np = P.N;
     auto load = [&](int kt) {
-        const int sg = kt < P.s.kt[0] ? 0 : 1;
-        const int kk = (sg == 0 ? kt : kt - P.s.kt[0]) * BK;
-        const T *A = (const T *)P.s.A[sg];
-        const T *B = (const T *)P.s.B[sg];
-        la.load(A, P.s.lda[sg], m0, P.M, kk, P.s.K[sg]);
-        lb.load(B, P.s.ldb[sg], n0, P.N, kk, P.s.K[sg]);
+        if (kt < kt0) {
+            la.load(A0, lda0, m0, Mp, kt * BK, K0);
+            lb.load(B0, ldb0, n0, Np, kt * BK, K0);
+        } else {
+            la.load(A1, lda1, m0, Mp, (kt - kt0) * BK, K1);
+            lb.load(B1, ldb1, n0, Np, (kt - kt0) * BK, K1);
+        }
     };
 
     floatx16 acc[FM][FN];
@@ -229,39 +248,46 @@ void gemm_kernel(DevArgs args) {
 
     if (kt_begin < kt_end) load(kt_begin);
     int buf = 0;
+    const int kh = lane >> 5;
     for (int kt = kt_begin; kt < kt_end; ++kt) {
         la.store(As[buf]);
         lb.store(Bs[buf]);
         __syncthreads();
         if (kt + 1 < kt_end) load(kt + 1);
-        // operands of the next k-step are read from LDS while the matrix
-        // cores work on the current one
-        float a[FM], b[FN];
+        // two register sets of operands: the LDS reads of k-step s + 1 are
+        // issued before the matrix-core products of k-step s
+        float a0[FM], b0[FN], a1[FM], b1[FN];
+        auto rd = [&](float *a, float *b, int kr) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i) a[i] = As[buf][(lane >> 5)][wm * WTM + i * 32 + (lane & 31)];
+            for (int i = 0; i < FM; ++i) a[i] = As[buf][kr][wm * WTM + i * 32 + (lane & 31)];
 #pragma unroll
-        for (int j = 0; j < FN; ++j) b[j] = Bs[buf][(lane >> 5)][wn * WTN + j * 32 + (lane & 31)];
-#pragma unroll
-        for (int kk = 0; kk < BK; kk += 2) {
-            float an[FM], bn[FN];
-            if (kk + 2 < BK) {
-                const int kr = kk + 2 + (lane >> 5);
-#pragma unroll
-                for (int i = 0; i < FM; ++i) an[i] = As[buf][kr][wm * WTM + i * 32 + (lane & 31)];
-#pragma unroll
-                for (int j = 0; j < FN; ++j) bn[j] = Bs[buf][kr][wn * WTN + j * 32 + (lane & 31)];
-            }
+            for (int j = 0; j < FN; ++j) b[j] = Bs[buf][kr][wn * WTN + j * 32 + (lane & 31)];
+        };
+        auto mma = [&](const float *a, const float *b) {
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-            if (kk + 2 < BK) {
+        };
+        // (scheduling barriers keep each group of reads ahead of the products
+        // that do not need it; without them the compiler sinks the reads
+        // below the products and waits on them at once)
+        rd(a0, b0, kh);
 #pragma unroll
-                for (int i = 0; i < FM; ++i) a[i] = an[i];
-#pragma unroll
-                for (int j = 0; j < FN; ++j) b[j] = bn[j];
-            }
+        for (int kk = 0; kk < BK; kk += 4) {
+            rd(a1, b1, kk + 2 + kh);
+            __builtin_amdgcn_sched_barrier(0);
+            GCN_PRIO_UP();
+            mma(a0, b0);
+            GCN_PRIO_DOWN();
+            __builtin_amdgcn_sched_barrier(0);
+            if (kk + 4 < BK) rd(a0, b0, kk + 4 + kh);
+            __builtin_amdgcn_sched_barrier(0);
+            GCN_PRIO_UP();
+            mma(a1, b1);
+            GCN_PRIO_DOWN();
+            __builtin_amdgcn_sched_barrier(0);
         }
         buf ^= 1;
     }

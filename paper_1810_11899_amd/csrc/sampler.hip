@@ -458,7 +458,8 @@ __global__ __launch_bounds__(kTB) void fill_rows_kernel(int32_t nV, int32_t n, c
                                                         const int64_t *__restrict__ off,
                                                         const int32_t *__restrict__ status,
                                                         int32_t *__restrict__ sub_indices,
-                                                        float *__restrict__ sub_vals) {
+                                                        float *__restrict__ sub_vals,
+                                                        float *__restrict__ sub_vals_t) {
     const int s = blockIdx.y;
     const int lane = threadIdx.x & 63;
     const int32_t i = blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
@@ -481,6 +482,7 @@ __global__ __launch_bounds__(kTB) void fill_rows_kernel(int32_t nV, int32_t n, c
             const int64_t q = pos + __popcll(mask & ((1ull << lane) - 1ull));
             sub_indices[q] = loc;
             sub_vals[q] = val;
+            if (sub_vals_t) sub_vals_t[q] = 1.0f / (float)(ip[loc + 1] - ip[loc]);
         }
         pos += __popcll(mask);
     }
@@ -654,8 +656,8 @@ size_t gcn_induce_workspace_bytes(int32_t n_vertices, int32_t n, int32_t S) {
 
 int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *vertices, const int32_t *counts,
                          int32_t *n_sub, int32_t *vsub, int32_t *indptr_sub, int64_t *edge_offsets,
-                         int32_t *sub_indices, float *sub_vals, int64_t edge_capacity, int32_t *status,
-                         void *ws, size_t ws_bytes, void *stream) {
+                         int32_t *sub_indices, float *sub_vals, float *sub_vals_t, int64_t edge_capacity,
+                         int32_t *status, void *ws, size_t ws_bytes, void *stream) {
     if (!G || !vertices || !counts || !n_sub || !vsub || !indptr_sub || !edge_offsets || !status || S < 0 ||
         n < 0 || edge_capacity < 0 || (edge_capacity > 0 && (!sub_indices || !sub_vals))) {
         set_error("gcn_induce_subgraphs: null argument or negative size");
@@ -700,7 +702,8 @@ int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *
     if (n > 0) {
         const int rb = (n + kTB / 64 - 1) / (kTB / 64);
         fill_rows_kernel<<<dim3(rb, S), kTB, 0, s>>>(nV, n, G->indptr, G->indices, w.map, w.n_sub64, vsub,
-                                                     indptr_sub, edge_offsets, status, sub_indices, sub_vals);
+                                                     indptr_sub, edge_offsets, status, sub_indices, sub_vals,
+                                                     sub_vals_t);
     }
     GCN_LAUNCH_CHECK("induce kernels");
     return GCN_OK;
@@ -733,3 +736,26 @@ int gcn_gather_rows(const void *X, int32_t n_rows_X, int32_t width, int64_t ldx,
 }
 
 }  // extern "C"
+
+extern "C" int gcn_csr_pattern_symmetric_host(int32_t n, const int32_t *indptr, const int32_t *indices) {
+    if (n < 0 || !indptr || (indptr[n] > 0 && !indices)) {
+        set_error("gcn_csr_pattern_symmetric_host: null pointer or negative size");
+        return GCN_EINVAL;
+    }
+    for (int32_t i = 0; i < n; ++i) {
+        for (int32_t p = indptr[i]; p < indptr[i + 1]; ++p) {
+            const int32_t j = indices[p];
+            if (j < 0 || j >= n || (p > indptr[i] && indices[p - 1] >= j)) {
+                set_error("gcn_csr_pattern_symmetric_host: row %d is not strictly ascending within [0, n)", i);
+                return GCN_EINVAL;
+            }
+        }
+    }
+    for (int32_t i = 0; i < n; ++i) {
+        for (int32_t p = indptr[i]; p < indptr[i + 1]; ++p) {
+            const int32_t j = indices[p];
+            if (!std::binary_search(indices + indptr[j], indices + indptr[j + 1], i)) return 0;
+        }
+    }
+    return 1;
+}

@@ -98,13 +98,14 @@ class FlatModel:
 class _Pool:
     """Device buffers of S sampled subgraphs and their induced CSRs."""
 
-    def __init__(self, S: int, n: int, nV: int, edge_capacity: int, device):
+    def __init__(self, S: int, n: int, nV: int, edge_capacity: int, device, with_transpose: bool):
         d = torch.device(device)
         self.S, self.n = S, n
+        self.with_transpose = with_transpose
         self.vertices = torch.empty((S, n), dtype=torch.int32, device=d)
         self.counts = torch.empty(S, dtype=torch.int32, device=d)
         self.status = torch.empty(S, dtype=torch.int32, device=d)
-        self.batch = B.InducedBatch(S, n, edge_capacity, d)
+        self.batch = B.InducedBatch(S, n, edge_capacity, d, with_transpose)
         self.ws = B.Workspace(d)
         self.ws.get(B.lib().gcn_induce_workspace_bytes(nV, n, S))
         self.h_nsub = torch.empty(S, dtype=torch.int32).pin_memory()
@@ -143,8 +144,12 @@ class Trainer:
         d = self.dev
         mean_deg = g.nnz / max(g.n, 1)
         self.edge_cap = int(cfg.n * max(mean_deg, 1.0) * 2) + 1024
+        # on a symmetric G the induce step also emits the transposed matrix's
+        # values, and the per-iteration CSR transpose is not needed
+        self.symmetric = B.gcn_csr_pattern_symmetric_host(g.indptr, g.indices)
         self.side = torch.cuda.Stream(device=d)
-        self.pools = [_Pool(cfg.pool, n, g.n, cfg.pool * self.edge_cap // 4 + 1024, d) for _ in range(2)]
+        self.pools = [_Pool(cfg.pool, n, g.n, cfg.pool * self.edge_cap // 4 + 1024, d, self.symmetric)
+                      for _ in range(2)]
         self.cur = 0
         self.next_id = 0
         # iteration buffers, sized for the largest subgraph (n vertices)
@@ -197,7 +202,7 @@ class Trainer:
             need = int(p.h_off[-1])
             s = self.side
             with torch.cuda.stream(s):
-                p.batch = B.InducedBatch(p.S, p.n, need + need // 8, self.dev)
+                p.batch = B.InducedBatch(p.S, p.n, need + need // 8, self.dev, p.with_transpose)
                 B.gcn_induce_subgraphs(self.G, p.vertices, p.counts, p.batch, p.ws, stream=s)
                 p.h_nsub.copy_(p.batch.n_sub, non_blocking=True)
                 p.h_off.copy_(p.batch.edge_offsets, non_blocking=True)
@@ -236,11 +241,14 @@ class Trainer:
         if nnz > self.t_cap:
             self._alloc_edges(nnz + nnz // 8)
         A = p.batch.csr(s, ns, e0, e1)
-        AT = B.DeviceCSR(ns, ns, self.t_indptr[:ns + 1], self.t_indices[:nnz], self.t_vals[:nnz])
         rows = p.batch.vsub[s]
         B.gcn_gather_rows(self.X, rows, ns, self.H0)
         B.gcn_gather_rows(self.labels_all, rows, ns, self.lab)
-        B.gcn_csr_transpose_into(A, AT.indptr, AT.indices, AT.vals, self.ws)
+        if self.symmetric:
+            AT = p.batch.csr_t(s, ns, e0, e1)
+        else:
+            AT = B.DeviceCSR(ns, ns, self.t_indptr[:ns + 1], self.t_indices[:nnz], self.t_vals[:nnz])
+            B.gcn_csr_transpose_into(A, AT.indptr, AT.indices, AT.vals, self.ws)
         mdl = self.model
         H = self.H0[:ns]
         for li in range(self.L):

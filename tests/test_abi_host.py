@@ -180,8 +180,18 @@ def test_sampler_entry_points_check_arguments_before_launch(L):
     p_bad = B.gcn_sampler_params(10, 20, 100, 10, 0, 1)   # ia_slots must exceed m
     csr3 = B.gcn_csr(100, 100, 0, fake, None, None)
     assert L.gcn_frontier_sample(ctypes.byref(csr3), ctypes.byref(p_bad), 0, 1, fake, fake, fake, None) == B.GCN_EINVAL
-    assert L.gcn_induce_subgraphs(ctypes.byref(csr3), 1, 10, None, None, None, None, None, None, None, None, 0,
-                                  None, None, 0, None) == B.GCN_EINVAL
+    assert L.gcn_induce_subgraphs(ctypes.byref(csr3), 1, 10, None, None, None, None, None, None, None, None, None,
+                                  0, None, None, 0, None) == B.GCN_EINVAL
     assert L.gcn_gather_rows(fake, 10, 8, 4, fake, 3, fake, 8, None) == B.GCN_ESHAPE
     assert L.gcn_gather_rows(None, 10, 8, 8, None, 0, None, 8, None) == B.GCN_OK   # nothing to do
     assert L.gcn_induce_workspace_bytes(1000, 100, 4) >= 4 * 1000 * 4
+
+
+def test_pattern_symmetry_check(L):
+    g = synth.custom(800, "rmat", 10, [(4, 4)], seed=2).graph
+    assert B.gcn_csr_pattern_symmetric_host(g.indptr, g.indices) is True
+    d = synth.csr_from_pairs(5, np.array([0, 1, 2]), np.array([1, 2, 0]))   # a directed cycle
+    assert B.gcn_csr_pattern_symmetric_host(d.indptr, d.indices) is False
+    assert B.gcn_csr_pattern_symmetric_host(synth.empty_graph(4).indptr, np.zeros(0, np.int32)) is True
+    with pytest.raises(B.GcnError):
+        B.gcn_csr_pattern_symmetric_host(np.array([0, 2], np.int32), np.array([0, 0], np.int32))

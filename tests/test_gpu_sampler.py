@@ -145,12 +145,24 @@ def test_induce_sampled_subgraphs_bit_exact(ws):
     p = params_for(g, 300, 2500, cap=30, seed=7)
     S = 5
     v, c, st = B.gcn_frontier_sample(dcsr(g), p, 0, S)
-    ib = B.InducedBatch(S, p.n, 4_000_000, "cuda")
+    ib = B.InducedBatch(S, p.n, 4_000_000, "cuda", with_transpose=True)
     print("induce: S=5 n=2500", flush=True)
     B.gcn_induce_subgraphs(dcsr(g), v, c, ib, ws)
     torch.cuda.synchronize()
     assert int(ib.status.item()) == 0
     check_induced(g, v.cpu().numpy(), c.cpu().numpy(), ib)
+    # G is symmetric, so the transposed values make the transpose of each
+    # subgraph's aggregation matrix: the same as the CSR transpose, bit for bit
+    assert B.gcn_csr_pattern_symmetric_host(g.indptr, g.indices)
+    n_sub = ib.n_sub.cpu().numpy()
+    off = ib.edge_offsets.cpu().numpy()
+    for s in range(S):
+        A = ib.csr(s, int(n_sub[s]), int(off[s]), int(off[s + 1]))
+        AT = B.gcn_csr_transpose(A, ws)
+        ATs = ib.csr_t(s, int(n_sub[s]), int(off[s]), int(off[s + 1]))
+        torch.cuda.synchronize()
+        assert torch.equal(AT.indptr, ATs.indptr) and torch.equal(AT.indices, ATs.indices)
+        assert torch.equal(AT.vals.view(torch.int32), ATs.vals.view(torch.int32))
 
 
 def test_induce_edge_cases_and_capacity(ws):
