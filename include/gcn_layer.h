@@ -109,6 +109,20 @@ size_t gcn_csr_transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t
 int gcn_csr_transpose(const gcn_csr *A, int32_t *t_indptr, int32_t *t_indices, float *t_vals,
                       void *ws, size_t ws_bytes, void *stream);
 
+/* The same transpose for a square A whose pattern is symmetric, with strictly
+ * ascending rows (gcn_csr_pattern_symmetric_host, gcn_sampler.h, checks it
+ * on the host): A^T then has A's indptr and indices, and only its values
+ * differ.  Writes t_vals[nnz]: for entry p of row j (column i), the value A
+ * holds at (i, j) -- the row's value when all of row i's values are equal (as
+ * in the mean aggregation of Sec. II), else found by binary search in row i.
+ * Outside this contract, an index outside [0, n) or a missing (i, j) in a row
+ * with unequal values gives NaN.  On such input A^T = (A.indptr, A.indices,
+ * t_vals) equals the output of gcn_csr_transpose bit for bit.  Undirected
+ * graphs (every workload here, and the subgraphs a symmetric training graph
+ * induces) have this form. */
+size_t gcn_csr_transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz);
+int gcn_csr_transpose_symmetric(const gcn_csr *A, float *t_vals, void *ws, size_t ws_bytes, void *stream);
+
 /* ---------------------------------------------------------------- a1 ----
  * Feature propagation (the first kernel of Sec. V-A; Sec. V-B, Alg. 6):
  *     out[i, c] = sum_p vals[p] * X[indices[p], c],   c in [0, k)

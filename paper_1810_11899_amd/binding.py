@@ -54,6 +54,8 @@ _SIGNATURES = {
     "gcn_csr_validate_host": (ctypes.c_int, [_I32, _I32, _I32, _P, _P, ctypes.c_int]),
     "gcn_csr_transpose_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
     "gcn_csr_transpose": (ctypes.c_int, [_CSRP, _P, _P, _P, _P, _SZ, _P]),
+    "gcn_csr_transpose_symmetric_workspace_bytes": (_SZ, [_I32, _I32]),
+    "gcn_csr_transpose_symmetric": (ctypes.c_int, [_CSRP, _P, _P, _SZ, _P]),
     "gcn_aggregate_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, ctypes.c_int]),
     "gcn_aggregate": (ctypes.c_int, [_CSRP, _P, _I32, _I32, _P, _I32, ctypes.c_int, _P, _SZ, _P]),
     "gcn_layer_pick_order": (ctypes.c_int, [_I32, _I32, ctypes.c_int]),
@@ -206,6 +208,18 @@ def gcn_csr_transpose_into(A: DeviceCSR, t_indptr, t_indices, t_vals, ws: Worksp
     s = A.struct()
     _check(L.gcn_csr_transpose(ctypes.byref(s), _ptr(t_indptr), _ptr(t_indices), _ptr(t_vals), w, wb,
                                _stream(stream)), "gcn_csr_transpose")
+
+
+def gcn_csr_transpose_symmetric(A: DeviceCSR, ws: Workspace, t_vals=None, stream=None) -> DeviceCSR:
+    """A^T of a symmetric-pattern A: A's indptr / indices with the transposed values."""
+    if t_vals is None:
+        t_vals = torch.empty(max(A.nnz, 1), dtype=torch.float32, device=A.indptr.device)[:A.nnz]
+    L = lib()
+    w, wb = ws.args(L.gcn_csr_transpose_symmetric_workspace_bytes(A.n_rows, A.nnz))
+    s = A.struct()
+    _check(L.gcn_csr_transpose_symmetric(ctypes.byref(s), _ptr(t_vals), w, wb, _stream(stream)),
+           "gcn_csr_transpose_symmetric")
+    return DeviceCSR(A.n_cols, A.n_rows, A.indptr, A.indices, t_vals[:A.nnz])
 
 
 def gcn_aggregate(A: DeviceCSR, X: torch.Tensor, out: torch.Tensor, ws: Workspace, prec=GCN_F32, stream=None):

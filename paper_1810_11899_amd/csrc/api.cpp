@@ -37,7 +37,7 @@ static const char *kClassNames[K_CLASS_COUNT] = {
     "spmm", "spmm_fixup", "gemm_nn", "gemm_tn", "gemm_nt", "splitk_reduce", "relu_bwd",
     "colsum", "loss_rows", "loss_reduce", "transpose_count", "transpose_scan", "transpose_scatter",
     "transpose_sort", "transpose_final", "cvt_bf16", "gemm_nn_bf16", "gemm_tn_bf16", "gemm_nt_bf16",
-    "spmm_bf16", "transpose_bf16", "frontier_sample", "induce_subgraphs", "gather_rows", "adam"};
+    "spmm_bf16", "transpose_bf16", "frontier_sample", "induce_subgraphs", "gather_rows", "adam", "transpose_symmetric"};
 
 const char *class_name(int cls) {
     return (cls >= 0 && cls < K_CLASS_COUNT) ? kClassNames[cls] : "";
@@ -282,6 +282,24 @@ int gcn_csr_transpose(const gcn_csr *A, int32_t *t_indptr, int32_t *t_indices, f
 }
 
 // ------------------------------------------------------------- aggregate
+size_t gcn_csr_transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz) {
+    return (n < 0 || nnz < 0) ? 0 : transpose_symmetric_workspace_bytes(n, nnz);
+}
+
+int gcn_csr_transpose_symmetric(const gcn_csr *A, float *t_vals, void *ws, size_t ws_bytes, void *stream) {
+    int rc = check_csr(A, "gcn_csr_transpose_symmetric");
+    if (rc) return rc;
+    REQUIRE(A->n_rows == A->n_cols, GCN_ESHAPE, "gcn_csr_transpose_symmetric: A must be square (%d x %d)",
+            A->n_rows, A->n_cols);
+    REQUIRE(A->nnz == 0 || t_vals, GCN_EINVAL, "gcn_csr_transpose_symmetric: null t_vals");
+    const size_t need = transpose_symmetric_workspace_bytes(A->n_rows, A->nnz);
+    REQUIRE(A->nnz == 0 || A->n_rows == 0 || (ws && ws_bytes >= need && ((uintptr_t)ws & 255u) == 0),
+            GCN_EWORKSPACE, "gcn_csr_transpose_symmetric: workspace %zu < %zu bytes or misaligned", ws_bytes,
+            need);
+    return csr_transpose_symmetric(A->n_rows, A->nnz, A->indptr, A->indices, A->vals, t_vals, ws, ws_bytes,
+                                   (hipStream_t)stream);
+}
+
 size_t gcn_aggregate_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz, int32_t k, gcn_prec prec) {
     return spmm_workspace_bytes(n_rows, nnz, k) +
            (prec == GCN_BF16 ? align256((size_t)n_cols * k * 2) + 256 : 0);

@@ -52,6 +52,7 @@ enum KernelClass {
     K_INDUCE,
     K_GATHER,
     K_ADAM,
+    K_T_SYM,
     K_CLASS_COUNT
 };
 const char *class_name(int cls);
@@ -159,6 +160,10 @@ int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *
              hipStream_t s);
 
 // CSR transpose --------------------------------------------------------------
+// values of A^T for a symmetric pattern (A^T shares A's indptr / indices)
+size_t transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz);
+int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+                            const float *vals, float *t_vals, void *ws, size_t ws_bytes, hipStream_t s);
 size_t transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz);
 int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
                   const int32_t *indices, const float *vals, int32_t *t_indptr, int32_t *t_indices,

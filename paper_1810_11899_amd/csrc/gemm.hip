@@ -321,10 +321,10 @@ void gemm_kernel(DevArgs args) {
 
 // ------------------------------------------------------------ bf16 kernel
 // bfloat16 operands, float32 accumulation on v_mfma_f32_32x32x16_bf16.  Both
-// operand tiles sit in LDS as [row][k] with k contiguous (row stride BK16 + 8
-// elements = 80 bytes), so a lane's eight consecutive k values are one
-// ds_read_b128 and the eight lanes served per LDS cycle fall in distinct bank
-// groups.  Operands that are contiguous along k in memory are copied as
+// operand tiles sit in LDS as [row][k] with k contiguous (64-byte rows whose
+// 16-byte chunks are XOR-swizzled by row), so a lane's eight consecutive k
+// values are one ds_read_b128 and both the fragment reads and the tile stores
+// are free of bank conflicts.  Operands that are contiguous along k in memory are copied as
 // 16-byte vectors; operands contiguous along the row index are transposed on
 // the way into LDS.
 #ifndef GCN_BF16_BK
@@ -340,7 +340,14 @@ void gemm_kernel(DevArgs args) {
 #define GCN_BF16_WAVES_PER_EU 4
 #endif
 constexpr int BK16 = GCN_BF16_BK;
-constexpr int LDK16 = BK16 + 8;
+constexpr int LDK16 = BK16;                 // no padding: chunks are XOR-swizzled
+constexpr int kChunks16 = BK16 / 8;         // 16-byte chunks per row
+constexpr int kRowsPerSpan16 = 256 / (BK16 * 2);  // rows that share the 64 banks once
+static_assert(kRowsPerSpan16 >= 1 && (kChunks16 & (kChunks16 - 1)) == 0, "BK16 must be 32 or 64");
+// Chunk c of row r is stored at chunk c ^ swz16(r): the 16 lanes that one LDS
+// cycle serves (16 consecutive rows of a fragment read, or 4 rows x 4 chunks
+// of a tile store) then fall in 16 distinct 4-bank groups.
+__device__ __forceinline__ int swz16(int r) { return (r / kRowsPerSpan16) & (kChunks16 - 1); }
 constexpr int kTBM16 = GCN_BF16_TBM;
 constexpr int kTBN16 = GCN_BF16_TBN;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -397,9 +404,10 @@ struct TileLoader16 {
             if (KMAJOR) {
                 const uint16_t *t = (const uint16_t *)&reg[i];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) lds[x + e][k] = t[e];
+                for (int e = 0; e < 8; ++e)
+                    lds[x + e][((k >> 3) ^ swz16(x + e)) * 8 + (k & 7)] = t[e];
             } else {
-                *(uint4 *)&lds[x][k] = reg[i];
+                *(uint4 *)&lds[x][((k >> 3) ^ swz16(x)) * 8] = reg[i];
             }
         }
     }
@@ -463,11 +471,15 @@ void gemm_bf16_kernel(DevArgs args) {
         for (int kk = 0; kk < BK16; kk += 16) {
             bf16x8 a[FM], b[FN];
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-                a[i] = *(const bf16x8 *)&As[buf][wm * WTM + i * 32 + (lane & 31)][kk + koff];
+            for (int i = 0; i < FM; ++i) {
+                const int r = wm * WTM + i * 32 + (lane & 31);
+                a[i] = *(const bf16x8 *)&As[buf][r][(((kk + koff) >> 3) ^ swz16(r)) * 8];
+            }
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                b[j] = *(const bf16x8 *)&Bs[buf][wn * WTN + j * 32 + (lane & 31)][kk + koff];
+            for (int j = 0; j < FN; ++j) {
+                const int r = wn * WTN + j * 32 + (lane & 31);
+                b[j] = *(const bf16x8 *)&Bs[buf][r][(((kk + koff) >> 3) ^ swz16(r)) * 8];
+            }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll

@@ -213,6 +213,62 @@ __global__ __launch_bounds__(kTB) void finalize_kernel(int32_t nnz, const int32_
     }
 }
 
+// Symmetric pattern: A^T has A's row pointers and indices; the value at
+// (row j, column i) is A's value at (i, j).
+// Pass 1, one wavefront per row i: the row id of every entry, and whether the
+// row's values are all the same bits (true of every row of a mean
+// aggregation matrix, Sec. II), in which case that value is A(i, j) for
+// every j.
+__global__ __launch_bounds__(kTB) void sym_rows_kernel(int32_t n, const int32_t *__restrict__ indptr,
+                                                       const float *__restrict__ vals, int32_t *__restrict__ rowid,
+                                                       uint32_t *__restrict__ rowval, int32_t *__restrict__ rowconst) {
+    const int64_t i = (int64_t)blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
+    if (i >= n) return;
+    const int lane = threadIdx.x & 63;
+    const int32_t b = indptr[i], e = indptr[i + 1];
+    const uint32_t first = e > b ? __float_as_uint(vals[b]) : 0u;
+    bool same = true;
+    for (int32_t p = b + lane; p < e; p += 64) {
+        rowid[p] = (int32_t)i;
+        same = same && (__float_as_uint(vals[p]) == first);
+    }
+    const bool all_same = __all(same);
+    if (lane == 0) {
+        rowval[i] = first;
+        rowconst[i] = all_same ? 1 : 0;
+    }
+}
+
+// Pass 2, one thread per entry p (row j, column i): the constant value of row
+// i, or a binary search for j in row i.  An index outside [0, n), or a missing
+// (i, j) found by the search, gives NaN.
+__global__ __launch_bounds__(kTB) void sym_vals_kernel(int32_t n, int32_t nnz, const int32_t *__restrict__ indptr,
+                                                       const int32_t *__restrict__ indices,
+                                                       const float *__restrict__ vals,
+                                                       const int32_t *__restrict__ rowid,
+                                                       const uint32_t *__restrict__ rowval,
+                                                       const int32_t *__restrict__ rowconst,
+                                                       float *__restrict__ t_vals) {
+    const int64_t stride = (int64_t)gridDim.x * kTB;
+    for (int64_t p = (int64_t)blockIdx.x * kTB + threadIdx.x; p < nnz; p += stride) {
+        const int32_t i = indices[p], j = rowid[p];
+        float t = __int_as_float(0x7FC00000);
+        if ((uint32_t)i < (uint32_t)n) {
+            if (rowconst[i]) {
+                t = __uint_as_float(rowval[i]);
+            } else {
+                int32_t lo = indptr[i], hi = indptr[i + 1];   // first index >= j in row i
+                while (lo < hi) {
+                    const int32_t mid = lo + ((hi - lo) >> 1);
+                    if (indices[mid] < j) lo = mid + 1; else hi = mid;
+                }
+                if (lo < indptr[i + 1] && indices[lo] == j) t = vals[lo];
+            }
+        }
+        t_vals[p] = t;
+    }
+}
+
 __global__ void fill_zero_kernel(int32_t *__restrict__ x, int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n) x[i] = 0;
@@ -311,6 +367,32 @@ int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *in
         hipLaunchKernelGGL(finalize_kernel, dim3(g), dim3(kTB), 0, s, nnz, rowid, vals, va, t_indices, t_vals);
         GCN_LAUNCH_CHECK("finalize_kernel");
     }
+    return GCN_OK;
+}
+
+size_t transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz) {
+    return align256((size_t)nnz * 4) + 2 * align256((size_t)n * 4) + 256;
+}
+
+int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+                            const float *vals, float *t_vals, void *ws, size_t ws_bytes, hipStream_t s) {
+    if (n == 0 || nnz == 0) return GCN_OK;
+    Arena ar(ws, ws_bytes);
+    int32_t *rowid = ar.take<int32_t>(nnz);
+    uint32_t *rowval = ar.take<uint32_t>(n);
+    int32_t *rowconst = ar.take<int32_t>(n);
+    if (!rowid || !rowval || !rowconst) {
+        set_error("csr_transpose_symmetric: workspace too small (%zu < %zu bytes)", ws_bytes,
+                  transpose_symmetric_workspace_bytes(n, nnz));
+        return GCN_EWORKSPACE;
+    }
+    ProfScope ps(K_T_SYM, s, 0.0, (double)nnz * 20.0 + (double)n * 16.0);
+    hipLaunchKernelGGL(sym_rows_kernel, dim3((unsigned)((n + kTB / 64 - 1) / (kTB / 64))), dim3(kTB), 0, s, n,
+                       indptr, vals, rowid, rowval, rowconst);
+    unsigned g = (unsigned)std::min<int64_t>(((int64_t)nnz + kTB - 1) / kTB, 16384);
+    hipLaunchKernelGGL(sym_vals_kernel, dim3(g), dim3(kTB), 0, s, n, nnz, indptr, indices, vals, rowid, rowval,
+                       rowconst, t_vals);
+    GCN_LAUNCH_CHECK("transpose_symmetric kernels");
     return GCN_OK;
 }
 

@@ -19,9 +19,10 @@ from . import binding as B
 class StepRunner:
     def __init__(self, wl, prec: int = B.GCN_F32, device: str = "cuda",
                  first_layer_dH: Optional[bool] = None, nnz_capacity: int = 0,
-                 orders: Optional[List[int]] = None):
+                 orders: Optional[List[int]] = None, transpose_shortcut: bool = True):
         self.dev = torch.device(device)
         self.prec = prec
+        self.transpose_shortcut = transpose_shortcut
         self.spec = wl.spec
         self.L = len(wl.layers)
         self.first_layer_dH = (self.L == 1) if first_layer_dH is None else bool(first_layer_dH)
@@ -98,11 +99,20 @@ class StepRunner:
             if self.targets is not None:
                 self.targets.copy_(torch.from_numpy(wl.targets), non_blocking=non_blocking)
         self.A = B.DeviceCSR(self.n, self.n, self.indptr, self.indices[:self.nnz], self.vals[:self.nnz])
-        self.AT = B.DeviceCSR(self.n, self.n, self.t_indptr, self.t_indices[:self.nnz], self.t_vals[:self.nnz])
+        # an undirected subgraph's A^T shares A's pattern: only its values are
+        # computed (gcn_csr_transpose_symmetric); otherwise the full transpose
+        self.symmetric = self.transpose_shortcut and B.gcn_csr_pattern_symmetric_host(g.indptr, g.indices)
+        if self.symmetric:
+            self.AT = B.DeviceCSR(self.n, self.n, self.indptr, self.indices[:self.nnz], self.t_vals[:self.nnz])
+        else:
+            self.AT = B.DeviceCSR(self.n, self.n, self.t_indptr, self.t_indices[:self.nnz], self.t_vals[:self.nnz])
 
     # --------------------------------------------------------------- step
     def step(self, stream=None):
-        B.gcn_csr_transpose_into(self.A, self.AT.indptr, self.AT.indices, self.AT.vals, self.ws, stream)
+        if self.symmetric:
+            B.gcn_csr_transpose_symmetric(self.A, self.ws, self.AT.vals, stream)
+        else:
+            B.gcn_csr_transpose_into(self.A, self.AT.indptr, self.AT.indices, self.AT.vals, self.ws, stream)
         H = self.H0
         for li in range(self.L):
             Ws, Wn, b = self.W[li]

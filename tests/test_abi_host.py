@@ -195,3 +195,11 @@ def test_pattern_symmetry_check(L):
     assert B.gcn_csr_pattern_symmetric_host(synth.empty_graph(4).indptr, np.zeros(0, np.int32)) is True
     with pytest.raises(B.GcnError):
         B.gcn_csr_pattern_symmetric_host(np.array([0, 2], np.int32), np.array([0, 0], np.int32))
+
+
+def test_transpose_symmetric_checks_arguments(L):
+    csr = B.gcn_csr(10, 12, 0, ctypes.c_void_p(256), None, None)
+    assert L.gcn_csr_transpose_symmetric(ctypes.byref(csr), None, None, 0, None) == B.GCN_ESHAPE
+    assert L.gcn_csr_transpose_symmetric(None, None, None, 0, None) == B.GCN_EINVAL
+    sq = B.gcn_csr(10, 10, 5, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256))
+    assert L.gcn_csr_transpose_symmetric(ctypes.byref(sq), ctypes.c_void_p(256), None, 0, None) == B.GCN_EWORKSPACE

@@ -65,6 +65,46 @@ def test_transpose_bit_exact(case, ws):
     assert np.array_equal(AT.vals.cpu().numpy().view(np.uint32), np.asarray(tv, np.float32).view(np.uint32))
 
 
+@pytest.mark.parametrize("case", ["cfg1", "rmat3000_random_vals", "star", "complete", "empty"])
+def test_transpose_symmetric_pattern_bit_exact(case, ws):
+    """A symmetric pattern's transpose: A's indptr / indices with values found
+    in the partner rows, equal bit for bit to the general transpose."""
+    rng = np.random.default_rng(3)
+    if case == "cfg1":
+        g = synth.config(1).graph
+    elif case == "rmat3000_random_vals":      # values that are not constant along rows
+        g0 = synth.custom(3001, "rmat", 13, [(2, 2)], seed=5).graph
+        g = synth.Graph(g0.n, g0.indptr, g0.indices, rng.standard_normal(g0.nnz).astype(np.float32))
+    elif case == "star":
+        g = synth.star_graph(70000)
+    elif case == "complete":
+        g = synth.complete_graph(300)
+    else:
+        g = synth.empty_graph(333)
+    assert B.gcn_csr_pattern_symmetric_host(g.indptr, g.indices)
+    A = dcsr(g)
+    AT = B.gcn_csr_transpose(A, ws)
+    ATs = B.gcn_csr_transpose_symmetric(A, ws)
+    ti, tj, tv = oracle.csr_transpose(g.n, g.n, g.indptr, g.indices, g.vals)
+    torch.cuda.synchronize()
+    assert np.array_equal(ATs.indptr.cpu().numpy(), ti) and np.array_equal(ATs.indices.cpu().numpy(), tj)
+    assert np.array_equal(ATs.vals.cpu().numpy().view(np.uint32), np.asarray(tv, np.float32).view(np.uint32))
+    assert torch.equal(ATs.vals.view(torch.int32), AT.vals.view(torch.int32))
+
+
+def test_transpose_symmetric_marks_missing_partners_nan(ws):
+    """Outside the contract (pattern not symmetric): a missing partner in a row
+    whose values differ, and an index out of range, give NaN."""
+    # entries (0,1) (1,1) (1,2) (2,1) (2,7); (1,0) is missing, 7 is out of range
+    ip = np.array([0, 1, 3, 5], np.int32)
+    ix = np.array([1, 1, 2, 1, 7], np.int32)
+    vals = np.array([1.0, 5.0, 6.0, 3.0, 4.0], np.float32)
+    A = B.DeviceCSR.from_host(3, 3, ip, ix, vals)
+    t = B.gcn_csr_transpose_symmetric(A, ws).vals.cpu().numpy()
+    assert np.isnan(t[0]) and np.isnan(t[4])
+    assert t[1] == 5.0 and t[2] == 3.0 and t[3] == 6.0
+
+
 # ------------------------------------------------------------- aggregate ----
 @pytest.mark.parametrize("k", [1, 50, 64, 100, 128, 130, 192, 200, 256, 300, 512, 602, 1024])
 def test_aggregate_parity_widths(k, ws):
