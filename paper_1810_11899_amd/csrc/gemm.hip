@@ -330,6 +330,9 @@ void gemm_kernel(DevArgs args) {
 #ifndef GCN_BF16_BK
 #define GCN_BF16_BK 32
 #endif
+#ifndef GCN_BF16_BIG
+#define GCN_BF16_BIG 1
+#endif
 #ifndef GCN_BF16_TBM
 #define GCN_BF16_TBM 128
 #endif
@@ -538,6 +541,189 @@ bool al(const void *p, int b) { return ((uintptr_t)p % (uintptr_t)b) == 0; }
 
 // Vector loads need every contiguous extent, leading dimension and base
 // pointer to be a multiple of the 16-byte vector.
+// ---------------------------------------------------- bf16, large tiles
+// The bf16 product of the layer (NT form, both operands contiguous along k):
+// 256 x 256 block tiles, four wavefronts each owning a 128 x 128 tile
+// (4 x 4 v_mfma_f32_32x32x16_bf16 blocks, accumulators in the AGPRs), one
+// block per CU.  Operand tiles of 256 rows x 32 k are copied from global
+// memory straight into LDS (16-byte global_load_lds, no staging registers)
+// through a ring of kBigStages stages, so three tiles are in flight while one
+// is multiplied: a 128 x 128 x 32 tile is too short to cover the load
+// latency with a single prefetch.  Rows are 64 bytes with their 16-byte
+// chunks XOR-swizzled by row (conflict-free fragment reads); a lane's
+// global address is chosen so that the chunk it deposits lands in its
+// swizzled place.  Requires every K-segment to be a multiple of 32 and
+// 16-byte aligned rows; rows past M or N are clamped to the last row and
+// their results dropped.
+constexpr int kBigT = 256;       // block tile, M and N
+constexpr int kBigBK = 32;       // k per stage
+#ifndef GCN_BIG_STAGES
+#define GCN_BIG_STAGES 4
+#endif
+constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU's LDS)
+#ifndef GCN_BIG_WAVES
+#define GCN_BIG_WAVES 8
+#endif
+constexpr int kBigWaves = GCN_BIG_WAVES;                 // 4 (2 x 2) or 8 (2 x 4)
+constexpr int kBigThreads = 64 * kBigWaves;
+constexpr int kBigWN = kBigWaves / 2;                     // wavefronts along N
+constexpr int kBigWTM = 128, kBigWTN = kBigT / kBigWN;   // wavefront tile
+constexpr int kBigFM = kBigWTM / 32, kBigFN = kBigWTN / 32;
+constexpr int kBigQ = 16 / kBigWaves;                     // 1 KB loads per operand per wavefront
+__device__ __forceinline__ int bigswz(int r) { return (r >> 2) & 3; }
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(kBigWaves / 4)))
+void gemm_bf16_big_kernel(DevArgs args) {
+    __shared__ __attribute__((aligned(16))) uint16_t lds[kBigStages][2][kBigT * kBigBK];
+
+    BlockCoord bc;
+    if (!decode_block(args, bc)) return;
+    const DevProblem &P = args.p[bc.pi];
+    const int m0 = bc.tm * kBigT, n0 = bc.tn * kBigT;
+    const int kt_begin = bc.split * P.kt_per_split;
+    const int kt_end = min(kt_begin + P.kt_per_split, P.kt_total);
+    const int ntiles = kt_end - kt_begin;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave / kBigWN, wn = wave % kBigWN;
+
+    const uint16_t *const A0 = (const uint16_t *)P.s.A[0], *const A1 = (const uint16_t *)P.s.A[1];
+    const uint16_t *const B0 = (const uint16_t *)P.s.B[0], *const B1 = (const uint16_t *)P.s.B[1];
+    const int64_t lda0 = P.s.lda[0], lda1 = P.s.lda[1], ldb0 = P.s.ldb[0], ldb1 = P.s.ldb[1];
+    const int kt0 = P.s.kt[0];
+    const int Mlast = P.M - 1, Nlast = P.N - 1;
+
+    // Lane `lane` of load q deposits chunk position (wave*Q + q)*64 + lane of
+    // the stage's operand tile: row pos/4, stored chunk pos%4, which holds
+    // global chunk (pos%4) ^ swizzle(row).
+    int rowA[kBigQ], rowB[kBigQ], chk[kBigQ];
+#pragma unroll
+    for (int q = 0; q < kBigQ; ++q) {
+        const int pos = (wave * kBigQ + q) * 64 + lane;
+        const int r = pos >> 2;
+        chk[q] = ((pos & 3) ^ bigswz(r)) * 8;
+        rowA[q] = min(m0 + r, Mlast);
+        rowB[q] = min(n0 + r, Nlast);
+    }
+    auto issue = [&](int kt, int stage) {
+        const bool s1 = kt >= kt0;
+        const uint16_t *A = s1 ? A1 : A0;
+        const uint16_t *Bm = s1 ? B1 : B0;
+        const int64_t lda = s1 ? lda1 : lda0, ldb = s1 ? ldb1 : ldb0;
+        const int k0 = (s1 ? kt - kt0 : kt) * kBigBK;
+#pragma unroll
+        for (int q = 0; q < kBigQ; ++q)
+            __builtin_amdgcn_global_load_lds((const void *)(A + (int64_t)rowA[q] * lda + k0 + chk[q]),
+                                             (void __attribute__((address_space(3))) *)&lds[stage][0][(wave * kBigQ + q) * 512],
+                                             16, 0, 0);
+#pragma unroll
+        for (int q = 0; q < kBigQ; ++q)
+            __builtin_amdgcn_global_load_lds((const void *)(Bm + (int64_t)rowB[q] * ldb + k0 + chk[q]),
+                                             (void __attribute__((address_space(3))) *)&lds[stage][1][(wave * kBigQ + q) * 512],
+                                             16, 0, 0);
+    };
+
+    floatx16 acc[kBigFM][kBigFN];
+#pragma unroll
+    for (int i = 0; i < kBigFM; ++i)
+#pragma unroll
+        for (int j = 0; j < kBigFN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+#pragma unroll
+    for (int st = 0; st < kBigStages - 1; ++st)
+        if (st < ntiles) issue(kt_begin + st, st);
+
+    constexpr int G = 2 * kBigQ;   // loads per tile per wavefront
+    for (int t = 0; t < ntiles; ++t) {
+        // the loads of tile t are done when at most the later tiles' loads
+        // are still outstanding
+        const int later = min(ntiles - 1 - t, kBigStages - 2);
+        if (later >= 3) wait_vmcnt<3 * G>();
+        else if (later == 2) wait_vmcnt<2 * G>();
+        else if (later == 1) wait_vmcnt<G>();
+        else wait_vmcnt<0>();
+        // every wavefront's part of tile t has landed and tile t-1's stage is
+        // free.  A bare s_barrier: the fence of __syncthreads would also wait
+        // for the later tiles' loads, which is the latency the ring hides.
+        // The empty asm statements keep the compiler from moving LDS accesses
+        // across it.
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+        if (t + kBigStages - 1 < ntiles) issue(kt_begin + t + kBigStages - 1, (t + kBigStages - 1) % kBigStages);
+        const uint16_t *As = lds[t % kBigStages][0];
+        const uint16_t *Bs = lds[t % kBigStages][1];
+#pragma unroll
+        for (int ks = 0; ks < kBigBK / 16; ++ks) {
+            const int c = 2 * ks + (lane >> 5);
+            bf16x8 a[kBigFM], b[kBigFN];
+#pragma unroll
+            for (int i = 0; i < kBigFM; ++i) {
+                const int r = wm * kBigWTM + i * 32 + (lane & 31);
+                a[i] = *(const bf16x8 *)&As[(r * 4 + (c ^ bigswz(r))) * 8];
+            }
+#pragma unroll
+            for (int j = 0; j < kBigFN; ++j) {
+                const int r = wn * kBigWTN + j * 32 + (lane & 31);
+                b[j] = *(const bf16x8 *)&Bs[(r * 4 + (c ^ bigswz(r))) * 8];
+            }
+            GCN_PRIO_UP();
+#pragma unroll
+            for (int i = 0; i < kBigFM; ++i)
+#pragma unroll
+                for (int j = 0; j < kBigFN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+            GCN_PRIO_DOWN();
+        }
+    }
+
+    // ---- epilogue (accumulator layout as in the other kernels); one call
+    // per accumulator block with constant indices, so that the accumulators
+    // stay in registers
+    const bool to_partial = P.split > 1;
+    float *dst = to_partial ? P.partial + (int64_t)bc.split * P.M * P.N : P.C;
+    const int64_t ldd = to_partial ? P.N : P.ldc;
+    auto epi = [&](const floatx16 &v, int i, int j) {
+        const int col = n0 + wn * kBigWTN + j * 32 + (lane & 31);
+        if (col < P.N) {
+            const float bv = (!to_partial && P.bias) ? P.bias[col] : 0.0f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm * kBigWTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row < P.M) {
+                    float x = v[r];
+                    if (to_partial) {
+                        dst[(int64_t)row * ldd + col] = x;
+                    } else {
+                        x += bv;
+                        if (P.relu) x = fmaxf(x, 0.0f);
+                        if (P.C16) P.C16[(int64_t)row * P.ldc + col] = to_bf16(x);
+                        else dst[(int64_t)row * ldd + col] = x;
+                    }
+                }
+            }
+        }
+    };
+    static_assert(kBigFM == 4 && (kBigFN == 4 || kBigFN == 2), "epilogue unrolled for 4 x 4 or 4 x 2 blocks");
+    epi(acc[0][0], 0, 0); epi(acc[0][1], 0, 1);
+    epi(acc[1][0], 1, 0); epi(acc[1][1], 1, 1);
+    epi(acc[2][0], 2, 0); epi(acc[2][1], 2, 1);
+    epi(acc[3][0], 3, 0); epi(acc[3][1], 3, 1);
+    if constexpr (kBigFN == 4) {
+        epi(acc[0][2], 0, 2); epi(acc[0][3], 0, 3);
+        epi(acc[1][2], 1, 2); epi(acc[1][3], 1, 3);
+        epi(acc[2][2], 2, 2); epi(acc[2][3], 2, 3);
+        epi(acc[3][2], 3, 2); epi(acc[3][3], 3, 3);
+    }
+}
+
 bool vec_ok(int layout, const GemmProblem &g, int esz) {
     const int E = 16 / esz;
     const bool a_km = layout == L_TN, b_km = layout != L_NT;
@@ -551,13 +737,27 @@ bool vec_ok(int layout, const GemmProblem &g, int esz) {
     return true;
 }
 
-int bk_of(int bf16) { return bf16 ? BK16 : kBK; }
-int tile_m_of(int bf16) { return bf16 ? kTBM16 : kTBM; }
-int tile_n_of(int bf16) { return bf16 ? kTBN16 : kTBN; }
+// mode 0: float32 kernel; 1: bf16 kernel; 2: bf16 large-tile kernel
+int bk_of(int mode) { return mode == 2 ? kBigBK : (mode ? BK16 : kBK); }
+int tile_m_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBM16 : kTBM); }
+int tile_n_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBN16 : kTBN); }
+
+// The large-tile bf16 kernel takes NT products whose K-segments are multiples
+// of its k-stage, with 16-byte aligned operand rows.
+bool big_ok(int layout, int nprob, const GemmProblem *probs) {
+    if (layout != L_NT || GCN_BF16_BIG == 0) return false;
+    for (int i = 0; i < nprob; ++i)
+        for (int s = 0; s < 2; ++s) {
+            const GemmSeg &sg = probs[i].seg[s];
+            if (sg.K == 0) continue;
+            if (sg.K % kBigBK || sg.lda % 8 || sg.ldb % 8 || !al(sg.A, 16) || !al(sg.B, 16)) return false;
+        }
+    return true;
+}
 
 void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k, float *partial,
               DevArgs &a, int64_t &blocks) {
-    const int BK = bk_of(bf16);
+    const int BK = bk_of(bf16);  // bf16 here is the kernel mode (0, 1, 2)
     blocks = 0;
     a.nprob = nprob;
     size_t poff = 0;
@@ -667,9 +867,10 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         }
         partial = (float *)(((uintptr_t)ws + 255) & ~(uintptr_t)255);
     }
+    const bool big = bf16 && big_ok(layout, nprob, probs);
     DevArgs a;
     int64_t blocks = 0;
-    fill_dev(layout, nprob, probs, bf16, split_k, partial, a, blocks);
+    fill_dev(layout, nprob, probs, big ? 2 : (bf16 ? 1 : 0), split_k, partial, a, blocks);
     if (blocks == 0) return GCN_OK;
     if (nprob == 2 && (a.p[0].kt_total != a.p[1].kt_total || a.p[0].split != a.p[1].split)) {
         set_error("gemm: grouped problems must have the same K-tiling");
@@ -682,7 +883,8 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     {
         ProfScope ps(cls, s, flops, 0.0);
         dim3 grid((unsigned)blocks);
-        if (layout == L_NN) launch<L_NN>(vec, bf16 != 0, grid, s, a);
+        if (big) hipLaunchKernelGGL(gemm_bf16_big_kernel, grid, dim3(kBigThreads), 0, s, a);
+        else if (layout == L_NN) launch<L_NN>(vec, bf16 != 0, grid, s, a);
         else if (layout == L_TN) launch<L_TN>(vec, bf16 != 0, grid, s, a);
         else launch<L_NT>(vec, bf16 != 0, grid, s, a);
         GCN_LAUNCH_CHECK("gemm_kernel");
