@@ -142,7 +142,7 @@ int check_csr(const gcn_csr *A, const char *name) {
 struct LayerPlan {
     bool need_G;        // backward forms G = A^T dZ_n
     bool bf16;
-    size_t fwd_T, fwd_W16, fwd_spmm;
+    size_t fwd_T, fwd_W16, fwd_spmm, fwd_gemm;
     size_t bwd_P, bwd_PT, bwd_D, bwd_DT, bwd_T2, bwd_W16, bwd_relu, bwd_spmm, bwd_gemm;
     size_t fwd_total, bwd_total, total;
 };
@@ -178,7 +178,16 @@ LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order,
         p.fwd_spmm = spmm_workspace_bytes(n, nnz, f_in);
     }
     p.fwd_W16 = W16;
-    p.fwd_total = p.fwd_T + p.fwd_W16 + p.fwd_spmm + 768;
+    // split-K partials of the forward products, when there are too few row
+    // tiles to fill the GPU (a few thousand vertices)
+    {
+        GemmProblem f[2] = {};
+        f[0].M = f[1].M = n;
+        f[0].N = f[1].N = h;
+        f[0].seg[0].K = f[1].seg[0].K = f_in;
+        p.fwd_gemm = gemm_workspace_bytes(2, f, gemm_pick_split(2, f, false));
+    }
+    p.fwd_total = p.fwd_T + p.fwd_W16 + p.fwd_spmm + p.fwd_gemm + 1024;
 
     p.bwd_P = align256((size_t)n * 2 * h * E);
     if (p.need_G) {
@@ -192,12 +201,20 @@ LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order,
     p.bwd_W16 = dH ? W16 : 0;
     p.bwd_relu = relu_bwd_workspace_bytes(n, h);
     GemmProblem pr[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
-    p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr));
+    p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr, true));
     if (p.bf16) {  // weight gradients as NT products
         pr[0].seg[0].lda = n;
         pr[0].seg[0].ldb = n;
         pr[1] = pr[0];
-        p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr));
+        p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr, true));
+    }
+    if (dH) {  // the input-gradient product reuses the weight-gradient partials' region
+        GemmProblem d[2] = {};
+        d[0].M = d[1].M = n;
+        d[0].N = d[1].N = f_in;
+        d[0].seg[0].K = d[1].seg[0].K = p.need_G ? 2 * h : h;
+        const int nd = p.need_G ? 1 : 2;
+        p.bwd_gemm = std::max(p.bwd_gemm, gemm_workspace_bytes(nd, d, gemm_pick_split(nd, d, false)));
     }
     p.bwd_total = p.bwd_P + p.bwd_PT + p.bwd_D + p.bwd_DT + p.bwd_T2 + p.bwd_W16 + p.bwd_relu + p.bwd_spmm +
                   p.bwd_gemm + 2816;
@@ -404,14 +421,16 @@ int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, c
             g[1].ldc = ldy;
             g[1].bias = bias + h;
             g[1].relu = 1;
-            return gemm(L_NT, 2, g, 1, 1, nullptr, 0, s);
+            void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
+            return gemm(L_NT, 2, g, 1, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s);
         }
         uint16_t *T16 = (uint16_t *)ar.take<char>(pl.fwd_T);
         void *sw = ar.take<char>(pl.fwd_spmm);
         g[1].seg[0] = GemmSeg{H16, f_in, WnT, f_in, f_in};
         g[1].C16 = T16;
         g[1].ldc = h;
-        if ((rc = gemm(L_NT, 2, g, 1, 1, nullptr, 0, s))) return rc;
+        void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
+        if ((rc = gemm(L_NT, 2, g, 1, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s))) return rc;
         return spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, T16, h, h, Y + h, ldy, EPI_BIAS_RELU,
                          bias + h, sw, pl.fwd_spmm, s);
     }
@@ -435,7 +454,8 @@ int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, c
         g[1].ldc = ldy;
         g[1].bias = bias + h;
         g[1].relu = 1;
-        return gemm(L_NN, 2, g, 0, 1, nullptr, 0, s);
+        void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
+        return gemm(L_NN, 2, g, 0, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s);
     }
     // transform-first: T = H W_neigh, then the neighbour half of Y = ReLU(A T + b)
     float *T = (float *)ar.take<char>(pl.fwd_T);
@@ -443,7 +463,8 @@ int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, c
     g[1].seg[0] = GemmSeg{H, ldh, W_neigh, h, f_in};
     g[1].C = T;
     g[1].ldc = h;
-    if ((rc = gemm(L_NN, 2, g, 0, 1, nullptr, 0, s))) return rc;
+    void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
+    if ((rc = gemm(L_NN, 2, g, 0, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s))) return rc;
     return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, T, h, h, Y + h, ldy, EPI_BIAS_RELU, bias + h, sw,
                     pl.fwd_spmm, s);
 }
@@ -538,7 +559,7 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
     g[0].ldc = h;
     g[1].C = dW_neigh;
     g[1].ldc = h;
-    const int split = gemm_pick_split(2, g);
+    const int split = gemm_pick_split(2, g, true);
     if ((rc = gemm(layout, 2, g, bf, split, gw, pl.bwd_gemm, s))) return rc;
     if (!want_dH) return GCN_OK;
     // a8: input gradient
@@ -557,7 +578,7 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
         d.seg[1] = GemmSeg{Pn, ldP, Wnop, h, h};
         d.C = dH;
         d.ldc = lddh;
-        return gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s);
+        return gemm(L_NT, 1, &d, bf, gemm_pick_split(1, &d, false), gw, pl.bwd_gemm, s);
     }
     GemmProblem d[2] = {};
     d[0].M = d[1].M = n;
@@ -569,7 +590,7 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
     d[1].ldc = f_in;
     if (bf) d[1].C16 = (uint16_t *)T2;
     else d[1].C = (float *)T2;
-    if ((rc = gemm(L_NT, 2, d, bf, 1, nullptr, 0, s))) return rc;
+    if ((rc = gemm(L_NT, 2, d, bf, gemm_pick_split(2, d, false), gw, pl.bwd_gemm, s))) return rc;
     return bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)T2, f_in,
                           f_in, dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s)
               : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)T2, f_in, f_in,
@@ -592,7 +613,7 @@ LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
         p.G16 = p.G16T = align256((size_t)n * C * 2);
     }
     GemmProblem g = dw_problem(f, C, n);
-    p.split = gemm_pick_split(1, &g);
+    p.split = gemm_pick_split(1, &g, true);
     p.gemm = gemm_workspace_bytes(1, &g, p.split);
     p.colsum = colsum_workspace_bytes(n, C);
     p.red = loss_reduce_workspace_bytes(n);

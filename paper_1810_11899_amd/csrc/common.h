@@ -128,7 +128,8 @@ struct GemmProblem {
 int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
          void *ws, size_t ws_bytes, hipStream_t s);
 size_t gemm_workspace_bytes(int nprob, const GemmProblem *probs, int split_k);
-int gemm_pick_split(int nprob, const GemmProblem *probs);
+// split-K count; k_is_rows: a weight gradient (K = vertices, few output tiles)
+int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows);
 
 // elementwise / reductions ----------------------------------------------------
 // dZ = dY * [Y > 0]; columns [0,h) -> outS (ldS), [h,2h) -> outN (ldN);

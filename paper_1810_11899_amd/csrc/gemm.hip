@@ -522,18 +522,48 @@ void gemm_bf16_kernel(DevArgs args) {
 }
 
 // C = sum over splits of the partial tiles, in split order.
+// Adds the split partials in split order and applies the epilogue.  VEC: four
+// consecutive columns per thread (N, ldc and the output 16-byte aligned).
+template <bool VEC>
 __global__ __launch_bounds__(256) void splitk_reduce(DevArgs args) {
     const int pi = blockIdx.y;
     const DevProblem &P = args.p[pi];
     const int64_t total = (int64_t)P.M * P.N;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    if (VEC) {
+        const int n4 = P.N / 4;
+        const int64_t total4 = (int64_t)P.M * n4;
+        for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += stride) {
+            float4 acc = ((const float4 *)P.partial)[e];
+            for (int s = 1; s < P.split; ++s) {
+                const float4 v = ((const float4 *)(P.partial + (int64_t)s * total))[e];
+                acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+            }
+            const int row = (int)(e / n4), col = (int)(e - (int64_t)row * n4) * 4;
+            float o[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (P.bias) o[j] += P.bias[col + j];
+                if (P.relu) o[j] = fmaxf(o[j], 0.0f);
+            }
+            if (P.C16) {
+                uint16_t *d = P.C16 + (int64_t)row * P.ldc + col;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) d[j] = to_bf16(o[j]);
+            } else {
+                *(float4 *)(P.C + (int64_t)row * P.ldc + col) = float4{o[0], o[1], o[2], o[3]};
+            }
+        }
+        return;
+    }
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
         float acc = P.partial[e];
         for (int s = 1; s < P.split; ++s) acc += P.partial[(int64_t)s * total + e];
         const int row = (int)(e / P.N), col = (int)(e % P.N);
         if (P.bias) acc += P.bias[col];
         if (P.relu) acc = fmaxf(acc, 0.0f);
-        P.C[(int64_t)row * P.ldc + col] = acc;
+        if (P.C16) P.C16[(int64_t)row * P.ldc + col] = to_bf16(acc);
+        else P.C[(int64_t)row * P.ldc + col] = acc;
     }
 }
 
@@ -543,13 +573,13 @@ bool al(const void *p, int b) { return ((uintptr_t)p % (uintptr_t)b) == 0; }
 // pointer to be a multiple of the 16-byte vector.
 // ---------------------------------------------------- bf16, large tiles
 // The bf16 product of the layer (NT form, both operands contiguous along k):
-// 256 x 256 block tiles, four wavefronts each owning a 128 x 128 tile
-// (4 x 4 v_mfma_f32_32x32x16_bf16 blocks, accumulators in the AGPRs), one
-// block per CU.  Operand tiles of 256 rows x 32 k are copied from global
+// 256 x 256 block tiles, eight wavefronts each owning a 128 x 64 tile
+// (4 x 2 v_mfma_f32_32x32x16_bf16 blocks), two wavefronts per SIMD, one block
+// per CU.  Operand tiles of 256 rows x 32 k are copied from global
 // memory straight into LDS (16-byte global_load_lds, no staging registers)
 // through a ring of kBigStages stages, so three tiles are in flight while one
-// is multiplied: a 128 x 128 x 32 tile is too short to cover the load
-// latency with a single prefetch.  Rows are 64 bytes with their 16-byte
+// is multiplied: a 128 x 128 x 32 tile of the smaller kernel is too short to
+// cover the load latency with a single prefetch.  Rows are 64 bytes with their 16-byte
 // chunks XOR-swizzled by row (conflict-free fragment reads); a lane's
 // global address is chosen so that the chunk it deposits lands in its
 // swizzled place.  Requires every K-segment to be a multiple of 32 and
@@ -818,7 +848,7 @@ void launch(bool vec, bool bf16, dim3 grid, hipStream_t s, const DevArgs &a) {
 
 }  // namespace
 
-int gemm_pick_split(int nprob, const GemmProblem *probs) {
+int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows) {
     int64_t tiles = 0, kt = 0;
     for (int i = 0; i < nprob; ++i) {
         tiles += (int64_t)((probs[i].M + kTBM - 1) / kTBM) * ((probs[i].N + kTBN - 1) / kTBN);
@@ -827,7 +857,13 @@ int gemm_pick_split(int nprob, const GemmProblem *probs) {
         if (k > kt) kt = k;
     }
     if (tiles <= 0) return 1;
-    int64_t sp = 1024 / tiles;          // about four blocks per CU in total
+    // Weight gradients (K = the subgraph's vertices, few output tiles): split
+    // to about four blocks per CU.  Other products: split only when the tiles
+    // do not give every CU a block, since the reduce pass costs a read of
+    // every partial.
+    int64_t sp;
+    if (k_is_rows) sp = 1024 / tiles;
+    else sp = tiles >= 256 ? 1 : 512 / tiles;
     const int64_t max_sp = kt / 8;      // keep >= 8 k-tiles per split
     if (sp > max_sp) sp = max_sp;
     if (sp < 1) sp = 1;
@@ -901,9 +937,20 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         // a problem without splits is written by the main kernel already; the
         // reduce skips it by running over zero elements
         DevArgs r = a;
-        for (int i = 0; i < nprob; ++i)
+        bool v4 = true;
+        for (int i = 0; i < nprob; ++i) {
             if (r.p[i].split <= 1) { r.p[i].M = 0; }
-        hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r);
+            const DevProblem &q = r.p[i];
+            v4 = v4 && q.N % 4 == 0 && q.ldc % 4 == 0 && (q.C16 || al(q.C, 16));
+        }
+        if (v4) {
+            g = (maxe / 4 + 255) / 256;
+            if (g > 4096) g = 4096;
+            if (g < 1) g = 1;
+            hipLaunchKernelGGL(splitk_reduce<true>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r);
+        } else {
+            hipLaunchKernelGGL(splitk_reduce<false>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r);
+        }
         GCN_LAUNCH_CHECK("splitk_reduce");
     }
     return GCN_OK;
