@@ -380,8 +380,20 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
     if (w >= waves) return;
     const int32_t r = head_row[w];
     if (r < 0) return;
+    // first wavefront of the run of wavefronts whose tail pieces belong to
+    // row r, 64 predecessors per step (a long row spans many wavefronts)
     int64_t ws = w;
-    while (ws > 0 && tail_row[ws - 1] == r) --ws;
+    for (;;) {
+        const int64_t q = ws - 1 - lane;
+        const bool same = q >= 0 && tail_row[q] == r;
+        const uint64_t brk = __ballot(!same);
+        if (brk == 0) {
+            ws -= 64;
+            continue;
+        }
+        ws -= __ffsll((unsigned long long)brk) - 1;
+        break;
+    }
     // four columns per lane; the pieces are added in wavefront order, eight
     // loads in flight per column
     const int c0 = blockIdx.y * 256 + lane;
