@@ -188,6 +188,49 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl,
                   float *loss, float *dHL, int32_t lddhl, float *dW_pred, float *db_pred,
                   gcn_prec prec, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------ whole step ----
+ * One fwd+bwd step of an L-layer model on one subgraph (Alg. 1: the forward
+ * loop, PREDICT, LOSS and the backward pass whose gradients ADAM consumes),
+ * as the sequence gcn_layer_fwd (l = 0..L-1), gcn_loss_grad, gcn_layer_bwd
+ * (l = L-1..0) with the same meaning for every buffer, in one call: the
+ * per-layer buffers are described once (gcn_layer_args) and reused for every
+ * subgraph.  Layer l's input is H0 for l = 0 and layer l-1's Y otherwise
+ * (f_in of layer l must be 2h of layer l-1); layer l's dH (NULL allowed for
+ * l = 0 only) is the output gradient of layer l-1.  With head == NULL the
+ * output gradient dY [n x 2h_L] (lddy) is given instead of PREDICT/LOSS.
+ * The workspace (gcn_model_workspace_bytes) is shared by the calls, which
+ * run in order on `stream`.  Errors are those of the calls it makes. */
+typedef struct {
+    int32_t f_in, h;
+    gcn_order order;
+    const float *W_self, *W_neigh, *bias;   /* f_in x h (leading dim h), f_in x h, [2h] */
+    float *Y;                               /* n x 2h (ldy) */
+    int32_t ldy;
+    void *saved;                            /* gcn_layer_saved_bytes */
+    size_t saved_bytes;
+    float *dH;                              /* n x f_in (lddh), NULL for layer 0 */
+    int32_t lddh;
+    float *dW_self, *dW_neigh, *dbias;      /* f_in x h, f_in x h, [2h] */
+} gcn_layer_args;
+
+typedef struct {
+    const float *W_pred, *b_pred;           /* 2h_L x C (leading dim C), [C] */
+    int32_t C;
+    gcn_loss_kind kind;
+    const int32_t *labels;                  /* CE: [n] */
+    const float *targets;                   /* BCE: n x C */
+    float *loss;                            /* [1] */
+    float *dHL;                             /* n x 2h_L (lddhl) */
+    int32_t lddhl;
+    float *dW_pred, *db_pred;               /* 2h_L x C, [C] */
+} gcn_head_args;
+
+size_t gcn_model_workspace_bytes(int32_t n, int32_t nnz, int32_t L, const gcn_layer_args *layers,
+                                 const gcn_head_args *head, gcn_prec prec);
+int gcn_model_step(const gcn_csr *A, const gcn_csr *AT, const float *H0, int32_t ldh0, int32_t L,
+                   const gcn_layer_args *layers, const gcn_head_args *head, const float *dY, int32_t lddy,
+                   gcn_prec prec, void *ws, size_t ws_bytes, void *stream);
+
 /* float32 -> bfloat16 bits, round to nearest even (NaN stays NaN): the
  * rounding every GCN_BF16 operand goes through.  x and y are device arrays of
  * `count` elements. */

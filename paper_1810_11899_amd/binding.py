@@ -39,6 +39,21 @@ class gcn_sampler_params(ctypes.Structure):
                 ("ia_slots", ctypes.c_int32), ("cap", ctypes.c_int32), ("seed", ctypes.c_uint64)]
 
 
+class gcn_layer_args(ctypes.Structure):
+    _fields_ = [("f_in", ctypes.c_int32), ("h", ctypes.c_int32), ("order", ctypes.c_int),
+                ("W_self", ctypes.c_void_p), ("W_neigh", ctypes.c_void_p), ("bias", ctypes.c_void_p),
+                ("Y", ctypes.c_void_p), ("ldy", ctypes.c_int32), ("saved", ctypes.c_void_p),
+                ("saved_bytes", ctypes.c_size_t), ("dH", ctypes.c_void_p), ("lddh", ctypes.c_int32),
+                ("dW_self", ctypes.c_void_p), ("dW_neigh", ctypes.c_void_p), ("dbias", ctypes.c_void_p)]
+
+
+class gcn_head_args(ctypes.Structure):
+    _fields_ = [("W_pred", ctypes.c_void_p), ("b_pred", ctypes.c_void_p), ("C", ctypes.c_int32),
+                ("kind", ctypes.c_int), ("labels", ctypes.c_void_p), ("targets", ctypes.c_void_p),
+                ("loss", ctypes.c_void_p), ("dHL", ctypes.c_void_p), ("lddhl", ctypes.c_int32),
+                ("dW_pred", ctypes.c_void_p), ("db_pred", ctypes.c_void_p)]
+
+
 SAMPLE_STATUS = {0: "ok", 1: "exhausted", 2: "overflow", 3: "probe_limit", 4: "root_limit", 5: "bad_graph"}
 
 _lib = None
@@ -69,6 +84,10 @@ _SIGNATURES = {
     "gcn_loss_workspace_bytes": (_SZ, [_I32, _I32, _I32, ctypes.c_int]),
     "gcn_loss_grad": (ctypes.c_int, [_P, _I32, _I32, _I32, _P, _P, _I32, ctypes.c_int, _P, _P, _P, _P,
                                      _I32, _P, _P, ctypes.c_int, _P, _SZ, _P]),
+    "gcn_model_workspace_bytes": (_SZ, [_I32, _I32, _I32, ctypes.POINTER(gcn_layer_args),
+                                        ctypes.POINTER(gcn_head_args), ctypes.c_int]),
+    "gcn_model_step": (ctypes.c_int, [_CSRP, _CSRP, _P, _I32, _I32, ctypes.POINTER(gcn_layer_args),
+                                      ctypes.POINTER(gcn_head_args), _P, _I32, ctypes.c_int, _P, _SZ, _P]),
     "gcn_f32_to_bf16": (ctypes.c_int, [_P, _P, _I64, _P]),
     "gcn_profile_enable": (ctypes.c_int, [ctypes.c_int]),
     "gcn_profile_reset": (ctypes.c_int, []),
@@ -287,6 +306,57 @@ def gcn_loss_grad(HL, W_pred, b_pred, kind, labels, targets, loss, dHL, dW_pred,
     _check(L.gcn_loss_grad(_ptr(HL), n, f, _ld(HL), _ptr(W_pred), _ptr(b_pred), C, kind, _ptr(labels),
                            _ptr(targets), _ptr(loss), _ptr(dHL), _ld(dHL), _ptr(dW_pred), _ptr(db_pred), prec,
                            w, wb, _stream(stream)), "gcn_loss_grad")
+
+
+class ModelStep:
+    """gcn_model_step with the per-layer descriptors built once.
+
+    layers: one dict per layer with the tensors W_self, W_neigh, bias, Y,
+    saved (uint8 or None), dH (or None), dW_self, dW_neigh, dbias and the int
+    order; head: None or a dict with W_pred, b_pred, kind, labels, targets,
+    loss, dHL, dW_pred, db_pred.  Buffers may hold more rows than a call's
+    subgraph (the row count is A's); they must stay alive and in place."""
+
+    def __init__(self, layers, head=None, prec=GCN_F32):
+        self.L = len(layers)
+        self.prec = prec
+        self.arr = (gcn_layer_args * self.L)()
+        self._keep = [layers, head]
+        for i, d in enumerate(layers):
+            for nm in ("W_self", "W_neigh", "bias", "Y", "dW_self", "dW_neigh", "dbias"):
+                _dev_f32(d[nm], nm)
+            f_in, h = int(d["W_self"].shape[0]), int(d["W_self"].shape[1])
+            sv, dH = d.get("saved"), d.get("dH")
+            self.arr[i] = gcn_layer_args(
+                f_in, h, int(d["order"]), d["W_self"].data_ptr(), d["W_neigh"].data_ptr(), d["bias"].data_ptr(),
+                d["Y"].data_ptr(), _ld(d["Y"]), None if sv is None else sv.data_ptr(),
+                0 if sv is None else sv.numel() * sv.element_size(), None if dH is None else dH.data_ptr(),
+                0 if dH is None else _ld(dH), d["dW_self"].data_ptr(), d["dW_neigh"].data_ptr(),
+                d["dbias"].data_ptr())
+        if head is None:
+            self.head = None
+        else:
+            p = lambda t: None if t is None else t.data_ptr()
+            self.head = gcn_head_args(p(head["W_pred"]), p(head["b_pred"]), int(head["W_pred"].shape[1]),
+                                      int(head["kind"]), p(head.get("labels")), p(head.get("targets")),
+                                      p(head["loss"]), p(head["dHL"]), _ld(head["dHL"]), p(head["dW_pred"]),
+                                      p(head["db_pred"]))
+        self._head_ref = None if self.head is None else ctypes.byref(self.head)
+
+    def set_loss(self, loss: torch.Tensor):
+        """Where the next call writes its loss (a 1-element float32 device tensor)."""
+        self.head.loss = loss.data_ptr()
+
+    def workspace_bytes(self, n: int, nnz: int) -> int:
+        return int(lib().gcn_model_workspace_bytes(n, nnz, self.L, self.arr, self._head_ref, self.prec))
+
+    def __call__(self, A: DeviceCSR, AT: DeviceCSR, H0: torch.Tensor, ws: Workspace, dY=None, stream=None):
+        L = lib()
+        w, wb = ws.args(self.workspace_bytes(A.n_rows, A.nnz))
+        s, st = A.struct(), AT.struct()
+        _check(L.gcn_model_step(ctypes.byref(s), ctypes.byref(st), H0.data_ptr(), _ld(H0), self.L, self.arr,
+                                self._head_ref, _ptr(dY), 0 if dY is None else _ld(dY), self.prec, w, wb,
+                                _stream(stream)), "gcn_model_step")
 
 
 def gcn_f32_to_bf16(x: torch.Tensor, stream=None) -> torch.Tensor:

@@ -367,10 +367,11 @@ size_t gcn_layer_workspace_bytes(int32_t n, int32_t nnz, int32_t f_in, int32_t h
     return plan_layer(n, nnz, f_in, h, order, true, prec).total;
 }
 
-int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, const float *W_self,
-                  const float *W_neigh, const float *bias, int32_t h, float *Y, int32_t ldy, void *saved,
-                  size_t saved_bytes_, gcn_order order, gcn_prec prec, void *ws, size_t ws_bytes,
-                  void *stream) {
+// launch == false: the argument checks only, nothing enqueued
+static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh,
+                     const float *W_self, const float *W_neigh, const float *bias, int32_t h, float *Y, int32_t ldy,
+                     void *saved, size_t saved_bytes_, gcn_order order, gcn_prec prec, void *ws, size_t ws_bytes,
+                     void *stream) {
     int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_fwd");
     if (rc) return rc;
     const int32_t n = A->n_rows;
@@ -383,6 +384,7 @@ int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, c
     const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, true, prec);
     REQUIRE(ws && ws_bytes >= pl.fwd_total, GCN_EWORKSPACE, "gcn_layer_fwd: workspace %zu < %zu bytes",
             ws_bytes, pl.fwd_total);
+    if (!launch) return GCN_OK;
     hipStream_t s = as_stream(stream);
     Arena ar(ws, ws_bytes);
     const bool bf = prec == GCN_BF16;
@@ -469,11 +471,11 @@ int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, c
                     pl.fwd_spmm, s);
 }
 
-int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f_in, int32_t ldh,
-                  const float *W_self, const float *W_neigh, int32_t h, const float *Y, int32_t ldy,
-                  const void *saved, size_t saved_bytes_, const float *dY, int32_t lddy, float *dH, int32_t lddh,
-                  float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec, void *ws,
-                  size_t ws_bytes, void *stream) {
+static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f_in,
+                     int32_t ldh, const float *W_self, const float *W_neigh, int32_t h, const float *Y, int32_t ldy,
+                     const void *saved, size_t saved_bytes_, const float *dY, int32_t lddy, float *dH,
+                     int32_t lddh, float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec,
+                     void *ws, size_t ws_bytes, void *stream) {
     int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_bwd");
     if (rc) return rc;
     rc = check_csr(AT, "gcn_layer_bwd (transpose)");
@@ -494,6 +496,7 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
     const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, want_dH, prec);
     REQUIRE(ws && ws_bytes >= pl.bwd_total, GCN_EWORKSPACE, "gcn_layer_bwd: workspace %zu < %zu bytes",
             ws_bytes, pl.bwd_total);
+    if (!launch) return GCN_OK;
     hipStream_t s = as_stream(stream);
     Arena ar(ws, ws_bytes);
     const bool bf = prec == GCN_BF16;
@@ -627,10 +630,10 @@ size_t gcn_loss_workspace_bytes(int32_t n, int32_t f, int32_t C, gcn_prec prec) 
     return plan_loss(n, f, C, prec).total;
 }
 
-int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const float *W_pred, const float *b_pred,
-                  int32_t C, gcn_loss_kind kind, const int32_t *labels, const float *targets, float *loss,
-                  float *dHL, int32_t lddhl, float *dW_pred, float *db_pred, gcn_prec prec, void *ws,
-                  size_t ws_bytes, void *stream) {
+static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t ldhl, const float *W_pred,
+                     const float *b_pred, int32_t C, gcn_loss_kind kind, const int32_t *labels,
+                     const float *targets, float *loss, float *dHL, int32_t lddhl, float *dW_pred, float *db_pred,
+                     gcn_prec prec, void *ws, size_t ws_bytes, void *stream) {
     REQUIRE(n >= 0 && f > 0 && C > 0, GCN_ESHAPE, "gcn_loss_grad: n=%d f=%d C=%d", n, f, C);
     REQUIRE(ldhl >= f && lddhl >= f, GCN_ESHAPE, "gcn_loss_grad: ldhl=%d lddhl=%d < f=%d", ldhl, lddhl, f);
     REQUIRE(kind == GCN_SOFTMAX_CE || kind == GCN_SIGMOID_BCE, GCN_EINVAL, "gcn_loss_grad: bad kind %d",
@@ -643,6 +646,7 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
     const LossPlan pl = plan_loss(n, f, C, prec);
     REQUIRE(ws && ws_bytes >= pl.total, GCN_EWORKSPACE, "gcn_loss_grad: workspace %zu < %zu bytes", ws_bytes,
             pl.total);
+    if (!launch) return GCN_OK;
     hipStream_t s = as_stream(stream);
     Arena ar(ws, ws_bytes);
     const bool bf = prec == GCN_BF16;
@@ -750,6 +754,102 @@ int gcn_profile_read(int cls, double *ms, int64_t *launches, double *flops, doub
     if (flops) *flops = t.flops;
     if (bytes) *bytes = t.bytes;
     return rc;
+}
+
+// ------------------------------------------------------------ entry points
+int gcn_layer_fwd(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, const float *W_self,
+                  const float *W_neigh, const float *bias, int32_t h, float *Y, int32_t ldy, void *saved,
+                  size_t saved_bytes_, gcn_order order, gcn_prec prec, void *ws, size_t ws_bytes, void *stream) {
+    return layer_fwd(true, A, H, f_in, ldh, W_self, W_neigh, bias, h, Y, ldy, saved, saved_bytes_, order, prec,
+                     ws, ws_bytes, stream);
+}
+
+int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f_in, int32_t ldh,
+                  const float *W_self, const float *W_neigh, int32_t h, const float *Y, int32_t ldy,
+                  const void *saved, size_t saved_bytes_, const float *dY, int32_t lddy, float *dH, int32_t lddh,
+                  float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec, void *ws,
+                  size_t ws_bytes, void *stream) {
+    return layer_bwd(true, A, AT, H, f_in, ldh, W_self, W_neigh, h, Y, ldy, saved, saved_bytes_, dY, lddy, dH,
+                     lddh, dW_self, dW_neigh, dbias, order, prec, ws, ws_bytes, stream);
+}
+
+int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const float *W_pred, const float *b_pred,
+                  int32_t C, gcn_loss_kind kind, const int32_t *labels, const float *targets, float *loss,
+                  float *dHL, int32_t lddhl, float *dW_pred, float *db_pred, gcn_prec prec, void *ws,
+                  size_t ws_bytes, void *stream) {
+    return loss_grad(true, HL, n, f, ldhl, W_pred, b_pred, C, kind, labels, targets, loss, dHL, lddhl, dW_pred,
+                     db_pred, prec, ws, ws_bytes, stream);
+}
+
+// ------------------------------------------------------------ model step
+size_t gcn_model_workspace_bytes(int32_t n, int32_t nnz, int32_t L, const gcn_layer_args *layers,
+                                 const gcn_head_args *head, gcn_prec prec) {
+    if (n < 0 || nnz < 0 || L < 1 || !layers) return 0;
+    size_t b = 0;
+    for (int32_t l = 0; l < L; ++l)
+        b = std::max(b, plan_layer(n, nnz, layers[l].f_in, layers[l].h, layers[l].order, true, prec).total);
+    if (head) b = std::max(b, plan_loss(n, 2 * layers[L - 1].h, head->C, prec).total);
+    return b;
+}
+
+namespace {
+// The step's calls in order; with launch == false only their argument checks
+// run, so that a bad descriptor is reported before anything is enqueued.
+int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0, int32_t ldh0, int32_t L,
+               const gcn_layer_args *layers, const gcn_head_args *head, const float *dY, int32_t lddy,
+               gcn_prec prec, void *ws, size_t ws_bytes, void *stream) {
+    const int32_t n = A->n_rows;
+    int rc;
+    const float *H = H0;  // forward: layer l reads layer l-1's output
+    int32_t ldh = ldh0;
+    for (int32_t l = 0; l < L; ++l) {
+        const gcn_layer_args &a = layers[l];
+        if ((rc = layer_fwd(launch, A, H, a.f_in, ldh, a.W_self, a.W_neigh, a.bias, a.h, a.Y, a.ldy, a.saved,
+                            a.saved_bytes, a.order, prec, ws, ws_bytes, stream)))
+            return rc;
+        H = a.Y;
+        ldh = a.ldy;
+    }
+    const float *g = dY;  // PREDICT + LOSS, or the given output gradient
+    int32_t ldg = lddy;
+    if (head) {
+        const gcn_layer_args &last = layers[L - 1];
+        if ((rc = loss_grad(launch, last.Y, n, 2 * last.h, last.ldy, head->W_pred, head->b_pred, head->C,
+                            head->kind, head->labels, head->targets, head->loss, head->dHL, head->lddhl,
+                            head->dW_pred, head->db_pred, prec, ws, ws_bytes, stream)))
+            return rc;
+        g = head->dHL;
+        ldg = head->lddhl;
+    }
+    for (int32_t l = L - 1; l >= 0; --l) {  // backward: layer l's dH is layer l-1's output gradient
+        const gcn_layer_args &a = layers[l];
+        const float *Hin = l == 0 ? H0 : layers[l - 1].Y;
+        const int32_t ldin = l == 0 ? ldh0 : layers[l - 1].ldy;
+        if ((rc = layer_bwd(launch, A, AT, Hin, a.f_in, ldin, a.W_self, a.W_neigh, a.h, a.Y, a.ldy, a.saved,
+                            a.saved_bytes, g, ldg, a.dH, a.lddh, a.dW_self, a.dW_neigh, a.dbias, a.order, prec, ws,
+                            ws_bytes, stream)))
+            return rc;
+        g = a.dH;
+        ldg = a.lddh;
+    }
+    return GCN_OK;
+}
+}  // namespace
+
+int gcn_model_step(const gcn_csr *A, const gcn_csr *AT, const float *H0, int32_t ldh0, int32_t L,
+                   const gcn_layer_args *layers, const gcn_head_args *head, const float *dY, int32_t lddy,
+                   gcn_prec prec, void *ws, size_t ws_bytes, void *stream) {
+    REQUIRE(A && AT && layers && L >= 1, GCN_EINVAL, "gcn_model_step: null argument or L < 1");
+    REQUIRE(head || dY, GCN_EINVAL, "gcn_model_step: neither a head nor an output gradient dY");
+    for (int32_t l = 1; l < L; ++l) {
+        REQUIRE(layers[l].f_in == 2 * layers[l - 1].h, GCN_ESHAPE,
+                "gcn_model_step: layer %d takes %d features, layer %d gives %d", l, layers[l].f_in, l - 1,
+                2 * layers[l - 1].h);
+        REQUIRE(layers[l].dH, GCN_EINVAL, "gcn_model_step: layer %d needs dH (the gradient of layer %d)", l,
+                l - 1);
+    }
+    int rc = model_step(false, A, AT, H0, ldh0, L, layers, head, dY, lddy, prec, ws, ws_bytes, stream);
+    return rc ? rc : model_step(true, A, AT, H0, ldh0, L, layers, head, dY, lddy, prec, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

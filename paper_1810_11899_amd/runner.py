@@ -66,6 +66,13 @@ class StepRunner:
             self.dW_pred = torch.empty((hl2, C), dtype=torch.float32, device=self.dev)
             self.db_pred = torch.empty(C, dtype=torch.float32, device=self.dev)
         self.load(wl)
+        layers = [dict(W_self=Ws, W_neigh=Wn, bias=b, Y=self.Y[li], saved=self.saved[li], dH=self.dH[li],
+                       dW_self=self.dWs[li], dW_neigh=self.dWn[li], dbias=self.db[li], order=self.orders[li])
+                  for li, (Ws, Wn, b) in enumerate(self.W)]
+        head = None if self.head is None else dict(
+            W_pred=self.W_pred, b_pred=self.b_pred, kind=self.kind, labels=self.labels, targets=self.targets,
+            loss=self.loss, dHL=self.dHL, dW_pred=self.dW_pred, db_pred=self.db_pred)
+        self.model = B.ModelStep(layers, head, prec)
 
     # ------------------------------------------------------------ buffers
     def _alloc_graph(self, cap: int):
@@ -108,11 +115,20 @@ class StepRunner:
             self.AT = B.DeviceCSR(self.n, self.n, self.t_indptr, self.t_indices[:self.nnz], self.t_vals[:self.nnz])
 
     # --------------------------------------------------------------- step
-    def step(self, stream=None):
+    def _transpose(self, stream):
         if self.symmetric:
             B.gcn_csr_transpose_symmetric(self.A, self.ws, self.AT.vals, stream)
         else:
             B.gcn_csr_transpose_into(self.A, self.AT.indptr, self.AT.indices, self.AT.vals, self.ws, stream)
+
+    def step(self, stream=None):
+        """The transpose, then the whole fwd+bwd in one gcn_model_step call."""
+        self._transpose(stream)
+        self.model(self.A, self.AT, self.H0, self.ws, dY=self.dY if self.head is None else None, stream=stream)
+
+    def step_calls(self, stream=None):
+        """The same step as separate gcn_layer_fwd / gcn_loss_grad / gcn_layer_bwd calls."""
+        self._transpose(stream)
         H = self.H0
         for li in range(self.L):
             Ws, Wn, b = self.W[li]

@@ -165,6 +165,19 @@ class Trainer:
             self.saved.append(torch.empty(max(nb, 256), dtype=torch.uint8, device=d) if nb else None)
         self._alloc_edges(self.edge_cap)
         self.losses = torch.zeros(1 << 16, dtype=torch.float32, device=d)
+        # every step is one gcn_model_step call over these buffers
+        mdl = self.model
+        layers = []
+        for li in range(self.L):
+            Ws, Wn, b = mdl.layer(li)
+            gWs, gWn, gb = mdl.layer(li, mdl.grads)
+            layers.append(dict(W_self=Ws, W_neigh=Wn, bias=b, Y=self.Y[li], saved=self.saved[li], dH=self.dH[li],
+                               dW_self=gWs, dW_neigh=gWn, dbias=gb, order=self.orders[li]))
+        Wp, bp = mdl.head()
+        dWp, dbp = mdl.head(mdl.grads)
+        self.fused = B.ModelStep(layers, dict(W_pred=Wp, b_pred=bp, kind=B.GCN_SOFTMAX_CE, labels=self.lab,
+                                              targets=None, loss=self.losses[:1], dHL=self.dHL, dW_pred=dWp,
+                                              db_pred=dbp), prec)
         self.iteration = 0
         self.subgraph_ids: List[int] = []
         for p in self.pools:
@@ -250,25 +263,9 @@ class Trainer:
             AT = B.DeviceCSR(ns, ns, self.t_indptr[:ns + 1], self.t_indices[:nnz], self.t_vals[:nnz])
             B.gcn_csr_transpose_into(A, AT.indptr, AT.indices, AT.vals, self.ws)
         mdl = self.model
-        H = self.H0[:ns]
-        for li in range(self.L):
-            Ws, Wn, b = mdl.layer(li)
-            B.gcn_layer_fwd(A, H, Ws, Wn, b, self.Y[li][:ns], self.saved[li], self.orders[li], self.ws, self.prec)
-            H = self.Y[li][:ns]
-        Wp, bp = mdl.head()
-        dWp, dbp = mdl.head(mdl.grads)
         t = self.iteration % self.losses.numel()
-        B.gcn_loss_grad(H, Wp, bp, B.GCN_SOFTMAX_CE, self.lab[:ns], None, self.losses[t:t + 1], self.dHL[:ns],
-                        dWp, dbp, self.ws, self.prec)
-        dY = self.dHL[:ns]
-        for li in range(self.L - 1, -1, -1):
-            Ws, Wn, _ = mdl.layer(li)
-            gWs, gWn, gb = mdl.layer(li, mdl.grads)
-            Hin = self.H0[:ns] if li == 0 else self.Y[li - 1][:ns]
-            dH = None if self.dH[li] is None else self.dH[li][:ns]
-            B.gcn_layer_bwd(A, AT, Hin, Ws, Wn, self.Y[li][:ns], self.saved[li], dY, dH, gWs, gWn, gb,
-                            self.orders[li], self.ws, self.prec)
-            dY = dH
+        self.fused.set_loss(self.losses[t:t + 1])
+        self.fused(A, AT, self.H0, self.ws)
         mdl.step_count += 1
         B.gcn_adam_update(mdl.params, mdl.grads, mdl.m, mdl.v, self.lr, mdl.step_count)
         self.iteration += 1

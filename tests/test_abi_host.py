@@ -203,3 +203,49 @@ def test_transpose_symmetric_checks_arguments(L):
     assert L.gcn_csr_transpose_symmetric(None, None, None, 0, None) == B.GCN_EINVAL
     sq = B.gcn_csr(10, 10, 5, ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.c_void_p(256))
     assert L.gcn_csr_transpose_symmetric(ctypes.byref(sq), ctypes.c_void_p(256), None, 0, None) == B.GCN_EWORKSPACE
+
+
+def _layer_args(f_in, h, ld_extra=0, dH=True):
+    f = 0x4000
+    return B.gcn_layer_args(f_in, h, B.GCN_AGGREGATE_FIRST, f, f, f, f, 2 * h + ld_extra, f, 1 << 30,
+                            f if dH else None, f_in, f, f, f)
+
+
+def test_model_step_checks_every_call_before_launch(L):
+    A = _fake_csr(100, 400)
+    fake = ctypes.c_void_p(0x4000)
+    head = B.gcn_head_args(0x4000, 0x4000, 5, B.GCN_SOFTMAX_CE, 0x4000, None, 0x4000, 0x4000, 16, 0x4000,
+                           0x4000)
+
+    def step(layers, head=head, dY=None, lddy=0, ws=1 << 30):
+        arr = (B.gcn_layer_args * len(layers))(*layers)
+        hp = None if head is None else ctypes.byref(head)
+        return L.gcn_model_step(ctypes.byref(A), ctypes.byref(A), fake, 8, len(layers), arr, hp, dY, lddy, 0,
+                                fake, ws, None)
+
+    ok = [_layer_args(8, 4, dH=False), _layer_args(8, 8)]
+    assert step([_layer_args(8, 4, dH=False), _layer_args(6, 8)]) == B.GCN_ESHAPE      # 2h != next f_in
+    assert "layer 1" in L.gcn_last_error().decode()
+    assert step([ok[0], _layer_args(8, 8, dH=False)]) == B.GCN_EINVAL                 # no dH for layer 0
+    assert step(ok, head=None) == B.GCN_EINVAL                                         # no head, no dY
+    assert step([ok[0], _layer_args(8, 8, ld_extra=-1)]) == B.GCN_ESHAPE               # layer 1's ldy
+    assert "gcn_layer_fwd" in L.gcn_last_error().decode()
+    bad_head = B.gcn_head_args(0x4000, 0x4000, 5, 7, 0x4000, None, 0x4000, 0x4000, 16, 0x4000, 0x4000)
+    assert step(ok, head=bad_head) == B.GCN_EINVAL                                     # the head's kind
+    assert step(ok, head=None, dY=fake, lddy=15) == B.GCN_ESHAPE                       # dY narrower than 2h
+    assert "gcn_layer_bwd" in L.gcn_last_error().decode()
+    assert step(ok, ws=4096) == B.GCN_EWORKSPACE
+    assert L.gcn_model_step(ctypes.byref(A), ctypes.byref(A), fake, 8, 0, (B.gcn_layer_args * 1)(), None, fake,
+                            8, 0, fake, 1 << 30, None) == B.GCN_EINVAL                # L = 0
+
+
+def test_model_workspace_is_the_largest_call(L):
+    layers = (B.gcn_layer_args * 2)(_layer_args(602, 128, dH=False), _layer_args(256, 128))
+    head = B.gcn_head_args(0x4000, 0x4000, 41, B.GCN_SOFTMAX_CE, 0x4000, None, 0x4000, 0x4000, 256, 0x4000,
+                           0x4000)
+    for prec in (B.GCN_F32, B.GCN_BF16):
+        need = L.gcn_model_workspace_bytes(8000, 120000, 2, layers, ctypes.byref(head), prec)
+        parts = [L.gcn_layer_workspace_bytes(8000, 120000, 602, 128, B.GCN_AGGREGATE_FIRST, prec),
+                 L.gcn_layer_workspace_bytes(8000, 120000, 256, 128, B.GCN_AGGREGATE_FIRST, prec),
+                 L.gcn_loss_workspace_bytes(8000, 256, 41, prec)]
+        assert need == max(parts)

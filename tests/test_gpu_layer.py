@@ -185,3 +185,33 @@ def test_forced_orders_agree_with_oracle(order):
     r.step()
     torch.cuda.synchronize()
     compare_step(r.results(), oracle.step(wl, first_layer_dH=True, envelope=True))
+
+
+@pytest.mark.parametrize("case", ["cfg1-f32", "cfg1-bf16", "dY-f32", "bce-transform-first"])
+def test_model_step_matches_separate_calls(case):
+    """gcn_model_step enqueues the same kernels as the separate calls, in the
+    same order: results must be identical bit for bit."""
+    if case.startswith("cfg1"):
+        wl = synth.config(1)
+        r = StepRunner(wl, prec=B.GCN_BF16 if case.endswith("bf16") else B.GCN_F32)
+    elif case == "dY-f32":
+        wl = synth.custom(2500, "rmat", 10, [(64, 32), (64, 48)], head=None, seed=4)
+        r = StepRunner(wl, first_layer_dH=True)
+    else:
+        wl = synth.custom(3000, "rmat", 12, [(96, 64), (128, 64)], head="bce", classes=30, seed=2)
+        r = StepRunner(wl, orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
+    print(f"model step vs calls: {case}", flush=True)
+    r.step_calls()
+    a = r.results()
+    r.step()
+    b = r.results()
+    for key in ("Y", "dW_self", "dW_neigh", "db", "dH"):
+        for i, (x, y) in enumerate(zip(a[key], b[key])):
+            if x is None:
+                assert y is None
+                continue
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), (key, i)
+    if "loss" in a:
+        assert a["loss"] == b["loss"]
+        for key in ("dW_pred", "db_pred", "dHL"):
+            assert np.array_equal(a[key].view(np.uint32), b[key].view(np.uint32)), key
