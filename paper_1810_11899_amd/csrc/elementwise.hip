@@ -8,7 +8,27 @@
 namespace gcn {
 namespace {
 
-constexpr int kRowsPerChunk = 64;
+// Column sums run in two fixed-order stages.  A block of kRowWaves
+// wavefronts covers a chunk of rows: its lanes span 64 x VEC adjacent columns
+// (coalesced rows), each wavefront adds every kRowWaves-th row of the chunk,
+// and the wavefronts' sums are added in order into one partial row per chunk;
+// a second pass adds the chunks' partial rows in order.
+constexpr int kRowWaves = 4;
+
+// Rows per chunk: enough chunks for about 2048 blocks, at least 16 rows, a
+// multiple of kRowWaves.  `width` is the row width in floats.
+__host__ __device__ inline int32_t chunk_rows(int32_t n, int32_t width) {
+    const int64_t xblocks = ((int64_t)width + 255) / 256;
+    int64_t r = ((int64_t)n * xblocks + 2047) / 2048;
+    if (r < 16) r = 16;
+    r = (r + kRowWaves - 1) / kRowWaves * kRowWaves;
+    return (int32_t)(r > 0x40000000 ? 0x40000000 : r);
+}
+
+inline int32_t chunk_count(int32_t n, int32_t width) {
+    const int32_t r = chunk_rows(n, width);
+    return (int32_t)(((int64_t)n + r - 1) / r);
+}
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -16,22 +36,46 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
-// dZ = dY * [Y > 0] for a chunk of rows; one thread per VEC columns.
-// Writes the two halves to their destinations and the chunk's column sums.
+// Adds the block's kRowWaves per-wavefront sums in wavefront order and writes
+// the chunk's partial row.  Every thread of the block must call it.
 template <int VEC>
-__global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, const float *__restrict__ dY,
-                                                       int64_t lddy, const float *__restrict__ Y, int64_t ldy,
+__device__ __forceinline__ void block_col_partial(const float (&sum)[VEC], int lane, int wv, int c, int width,
+                                                  bool active, float *__restrict__ part_row) {
+    __shared__ float red[kRowWaves - 1][64 * VEC];
+    if (wv > 0) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) red[wv - 1][lane * VEC + v] = sum[v];
+    }
+    __syncthreads();
+    if (wv == 0 && active) {
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            float t = sum[v];
+#pragma unroll
+            for (int k = 0; k < kRowWaves - 1; ++k) t += red[k][lane * VEC + v];
+            if (c + v < width) part_row[c + v] = t;
+        }
+    }
+}
+
+// dZ = dY * [Y > 0] for a chunk of rows, VEC columns per lane.  Writes the two
+// halves to their destinations and the chunk's column sums (the bias gradient).
+template <int VEC>
+__global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, int32_t rpc,
+                                                       const float *__restrict__ dY, int64_t lddy,
+                                                       const float *__restrict__ Y, int64_t ldy,
                                                        float *__restrict__ outS, int64_t ldS,
                                                        float *__restrict__ outN, int64_t ldN,
                                                        uint16_t *__restrict__ outS16,
                                                        uint16_t *__restrict__ outN16,
                                                        float *__restrict__ part) {
-    const int c = (blockIdx.x * 256 + threadIdx.x) * VEC;
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int c = (blockIdx.x * 64 + lane) * VEC;
     const int w = 2 * h;
-    if (c >= w) return;
+    const bool active = c < w;
     const int chunk = blockIdx.y;
-    const int r0 = chunk * kRowsPerChunk;
-    const int r1 = min(r0 + kRowsPerChunk, n);
+    const int r0 = chunk * rpc;
+    const int r1 = min(r0 + rpc, n);
     const bool self = c < h;  // VEC divides h, so a vector never straddles
     float *dst = self ? outS : outN;
     uint16_t *dst16 = self ? outS16 : outN16;
@@ -40,61 +84,68 @@ __global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, con
     float sum[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) sum[v] = 0.0f;
-    for (int r = r0; r < r1; ++r) {
-        float g[VEC], y[VEC];
-        if (VEC == 4) {
-            const float4 a = *(const float4 *)(dY + (int64_t)r * lddy + c);
-            const float4 b = *(const float4 *)(Y + (int64_t)r * ldy + c);
-            g[0] = a.x; g[1] = a.y; g[2] = a.z; g[3] = a.w;
-            y[0] = b.x; y[1] = b.y; y[2] = b.z; y[3] = b.w;
-        } else {
+    if (active) {
+#pragma unroll 2
+        for (int r = r0 + wv; r < r1; r += kRowWaves) {
+            float g[VEC], y[VEC];
+            if (VEC == 4) {
+                const float4 a = *(const float4 *)(dY + (int64_t)r * lddy + c);
+                const float4 b = *(const float4 *)(Y + (int64_t)r * ldy + c);
+                g[0] = a.x; g[1] = a.y; g[2] = a.z; g[3] = a.w;
+                y[0] = b.x; y[1] = b.y; y[2] = b.z; y[3] = b.w;
+            } else {
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    g[v] = dY[(int64_t)r * lddy + c + v];
+                    y[v] = Y[(int64_t)r * ldy + c + v];
+                }
+            }
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                g[v] = dY[(int64_t)r * lddy + c + v];
-                y[v] = Y[(int64_t)r * ldy + c + v];
+                g[v] = y[v] > 0.0f ? g[v] : 0.0f;
+                sum[v] += g[v];
             }
-        }
+            if (dst) {
+                float *o = dst + (int64_t)r * ldd + cc;
+                if (VEC == 4) {
+                    *(float4 *)o = make_float4(g[0], g[1], g[2], g[3]);
+                } else {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) {
-            g[v] = y[v] > 0.0f ? g[v] : 0.0f;
-            sum[v] += g[v];
-        }
-        if (dst) {
-            float *o = dst + (int64_t)r * ldd + cc;
-            if (VEC == 4) {
-                *(float4 *)o = make_float4(g[0], g[1], g[2], g[3]);
-            } else {
-#pragma unroll
-                for (int v = 0; v < VEC; ++v) o[v] = g[v];
+                    for (int v = 0; v < VEC; ++v) o[v] = g[v];
+                }
             }
-        }
-        if (dst16) {
-            uint16_t *o16 = dst16 + (int64_t)r * ldd + cc;
-            if (VEC == 4) {
-                const uint32_t lo = (uint32_t)f32_to_bf16_rne(g[0]) | ((uint32_t)f32_to_bf16_rne(g[1]) << 16);
-                const uint32_t hi = (uint32_t)f32_to_bf16_rne(g[2]) | ((uint32_t)f32_to_bf16_rne(g[3]) << 16);
-                *(uint2 *)o16 = make_uint2(lo, hi);
-            } else {
+            if (dst16) {
+                uint16_t *o16 = dst16 + (int64_t)r * ldd + cc;
+                if (VEC == 4) {
+                    const uint32_t lo = (uint32_t)f32_to_bf16_rne(g[0]) | ((uint32_t)f32_to_bf16_rne(g[1]) << 16);
+                    const uint32_t hi = (uint32_t)f32_to_bf16_rne(g[2]) | ((uint32_t)f32_to_bf16_rne(g[3]) << 16);
+                    *(uint2 *)o16 = make_uint2(lo, hi);
+                } else {
 #pragma unroll
-                for (int v = 0; v < VEC; ++v) o16[v] = f32_to_bf16_rne(g[v]);
+                    for (int v = 0; v < VEC; ++v) o16[v] = f32_to_bf16_rne(g[v]);
+                }
             }
         }
     }
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) part[(int64_t)chunk * w + c + v] = sum[v];
+    block_col_partial<VEC>(sum, lane, wv, c, w, active, part + (int64_t)chunk * w);
 }
 
 // Column sums of a chunk of rows (generic matrix).
-__global__ __launch_bounds__(256) void colsum_part_kernel(int32_t n, int32_t C, const float *__restrict__ G,
-                                                          int64_t ldg, float *__restrict__ part) {
-    const int c = blockIdx.x * 256 + threadIdx.x;
-    if (c >= C) return;
+__global__ __launch_bounds__(256) void colsum_part_kernel(int32_t n, int32_t C, int32_t rpc,
+                                                          const float *__restrict__ G, int64_t ldg,
+                                                          float *__restrict__ part) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int c = blockIdx.x * 64 + lane;
+    const bool active = c < C;
     const int chunk = blockIdx.y;
-    const int r0 = chunk * kRowsPerChunk;
-    const int r1 = min(r0 + kRowsPerChunk, n);
-    float s = 0.0f;
-    for (int r = r0; r < r1; ++r) s += G[(int64_t)r * ldg + c];
-    part[(int64_t)chunk * C + c] = s;
+    const int r0 = chunk * rpc;
+    const int r1 = min(r0 + rpc, n);
+    float sum[1] = {0.0f};
+    if (active) {
+#pragma unroll 4
+        for (int r = r0 + wv; r < r1; r += kRowWaves) sum[0] += G[(int64_t)r * ldg + c];
+    }
+    block_col_partial<1>(sum, lane, wv, c, C, active, part + (int64_t)chunk * C);
 }
 
 // out[c] = sum over chunks of part[chunk][c]: one wavefront per column; lane
@@ -168,24 +219,29 @@ __global__ __launch_bounds__(256) void loss_rows_kernel(int kind, int32_t n, int
     }
 }
 
-// loss = scale * sum_i rowloss[i] in two fixed-order stages: blocks of
-// kLossSeg rows reduce to one double each, then one block adds those.
-constexpr int kLossSeg = 2048;
+// loss = scale * sum_i rowloss[i] in fixed order: blocks of kLossSeg rows
+// reduce to one double each, then one block adds those; a single segment
+// (n <= kLossSeg) writes the loss directly.
+constexpr int kLossSeg = 16384;
 
 __global__ __launch_bounds__(256) void loss_partial_kernel(int32_t n, const float *__restrict__ rowloss,
-                                                           double *__restrict__ part) {
+                                                           double *__restrict__ part, double scale,
+                                                           float *__restrict__ loss) {
     __shared__ double sh[256];
     const int64_t base = (int64_t)blockIdx.x * kLossSeg;
+    const int64_t end = min((int64_t)n, base + kLossSeg);
     double s = 0.0;
-    for (int i = threadIdx.x; i < kLossSeg; i += 256)
-        if (base + i < n) s += (double)rowloss[base + i];
+    for (int64_t i = base + threadIdx.x; i < end; i += 256) s += (double)rowloss[i];
     sh[threadIdx.x] = s;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) {
         if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
         __syncthreads();
     }
-    if (threadIdx.x == 0) part[blockIdx.x] = sh[0];
+    if (threadIdx.x == 0) {
+        if (loss) *loss = (float)(sh[0] * scale);
+        else part[blockIdx.x] = sh[0];
+    }
 }
 
 __global__ __launch_bounds__(256) void loss_reduce_kernel(int32_t nparts, const double *__restrict__ part,
@@ -296,8 +352,7 @@ int fill_zero(float *x, int64_t count, hipStream_t s) {
 }
 
 size_t relu_bwd_workspace_bytes(int32_t n, int32_t h) {
-    const int64_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
-    return align256((size_t)chunks * 2 * h * sizeof(float)) + 256;
+    return align256((size_t)chunk_count(n, 2 * h) * 2 * h * sizeof(float)) + 256;
 }
 
 int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y, int64_t ldy,
@@ -305,7 +360,8 @@ int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y
              float *dbias, void *ws, size_t ws_bytes, hipStream_t s) {
     if (h <= 0) return GCN_OK;
     const int w = 2 * h;
-    const int32_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
+    const int32_t rpc = chunk_rows(n, w);
+    const int32_t chunks = chunk_count(n, w);
     Arena ar(ws, ws_bytes);
     float *part = ar.take<float>((size_t)chunks * w + 1);
     if (!part) {
@@ -321,12 +377,12 @@ int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y
                              (outS16 ? (double)n * w * 2.0 : 0.0);
         ProfScope ps(K_RELU_MASK, s, 0.0, bytes);
         if (v4) {
-            dim3 g((unsigned)((w / 4 + 255) / 256), (unsigned)chunks);
-            hipLaunchKernelGGL(relu_bwd_kernel<4>, g, dim3(256), 0, s, n, h, dY, lddy, Y, ldy, outS, ldS,
+            dim3 g((unsigned)((w / 4 + 63) / 64), (unsigned)chunks);
+            hipLaunchKernelGGL(relu_bwd_kernel<4>, g, dim3(256), 0, s, n, h, rpc, dY, lddy, Y, ldy, outS, ldS,
                                outN, ldN, outS16, outN16, part);
         } else {
-            dim3 g((unsigned)((w + 255) / 256), (unsigned)chunks);
-            hipLaunchKernelGGL(relu_bwd_kernel<1>, g, dim3(256), 0, s, n, h, dY, lddy, Y, ldy, outS, ldS,
+            dim3 g((unsigned)((w + 63) / 64), (unsigned)chunks);
+            hipLaunchKernelGGL(relu_bwd_kernel<1>, g, dim3(256), 0, s, n, h, rpc, dY, lddy, Y, ldy, outS, ldS,
                                outN, ldN, outS16, outN16, part);
         }
         GCN_LAUNCH_CHECK("relu_bwd_kernel");
@@ -341,14 +397,14 @@ int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y
 }
 
 size_t colsum_workspace_bytes(int32_t n, int32_t C) {
-    const int64_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
-    return align256((size_t)chunks * C * sizeof(float)) + 256;
+    return align256((size_t)chunk_count(n, C) * C * sizeof(float)) + 256;
 }
 
 int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *ws, size_t ws_bytes,
            hipStream_t s) {
     if (C <= 0) return GCN_OK;
-    const int32_t chunks = (n + kRowsPerChunk - 1) / kRowsPerChunk;
+    const int32_t rpc = chunk_rows(n, C);
+    const int32_t chunks = chunk_count(n, C);
     Arena ar(ws, ws_bytes);
     float *part = ar.take<float>((size_t)chunks * C + 1);
     if (!part) {
@@ -357,8 +413,8 @@ int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *
     }
     if (n > 0) {
         ProfScope ps(K_COLSUM_REDUCE, s, 0.0, (double)n * C * 4.0);
-        hipLaunchKernelGGL(colsum_part_kernel, dim3((unsigned)((C + 255) / 256), (unsigned)chunks), dim3(256), 0,
-                           s, n, C, G, ldg, part);
+        hipLaunchKernelGGL(colsum_part_kernel, dim3((unsigned)((C + 63) / 64), (unsigned)chunks), dim3(256), 0,
+                           s, n, C, rpc, G, ldg, part);
         GCN_LAUNCH_CHECK("colsum_part_kernel");
     }
     {
@@ -394,9 +450,14 @@ int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void
         return GCN_EWORKSPACE;
     }
     ProfScope ps(K_LOSS_REDUCE, s, 0.0, (double)n * 4.0);
-    if (nparts > 0)
-        hipLaunchKernelGGL(loss_partial_kernel, dim3((unsigned)nparts), dim3(256), 0, s, n, rowloss, part);
-    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, nparts, part, scale, loss);
+    if (nparts == 1) {
+        hipLaunchKernelGGL(loss_partial_kernel, dim3(1), dim3(256), 0, s, n, rowloss, part, scale, loss);
+    } else {
+        if (nparts > 1)
+            hipLaunchKernelGGL(loss_partial_kernel, dim3((unsigned)nparts), dim3(256), 0, s, n, rowloss, part,
+                               0.0, (float *)nullptr);
+        hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, nparts, part, scale, loss);
+    }
     GCN_LAUNCH_CHECK("loss_reduce_kernel");
     return GCN_OK;
 }
