@@ -606,14 +606,21 @@ struct LossPlan {
     size_t X, rows, HL16, HL16T, Wp16, Wp16T, G16, G16T, gemm, colsum, red, total;
     int split;
 };
+// bfloat16 class dimension padded with zero columns to a multiple of 32, so
+// that dHL = G W_pred^T (K = classes) runs on the large-tile product
+int32_t pad_classes(int32_t C) { return (C + 31) / 32 * 32; }
+
 LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
     LossPlan p{};
     p.X = align256((size_t)n * C * sizeof(float));
     p.rows = align256((size_t)n * sizeof(float) + 4);
     if (prec == GCN_BF16) {
+        const size_t Cp = pad_classes(C);
         p.HL16 = p.HL16T = align256((size_t)n * f * 2);
-        p.Wp16 = p.Wp16T = align256((size_t)f * C * 2);
-        p.G16 = p.G16T = align256((size_t)n * C * 2);
+        p.Wp16 = align256((size_t)f * Cp * 2);
+        p.Wp16T = align256((size_t)f * C * 2);
+        p.G16 = align256((size_t)n * Cp * 2);
+        p.G16T = align256((size_t)n * C * 2);
     }
     GemmProblem g = dw_problem(f, C, n);
     p.split = gemm_pick_split(1, &g, true);
@@ -654,9 +661,10 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     float *rows = ar.take<float>((size_t)n + 1);
     uint16_t *HL16 = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
     uint16_t *HL16T = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
-    uint16_t *Wp16 = bf ? ar.take<uint16_t>((size_t)f * C) : nullptr;
+    const int32_t Cp = pad_classes(C);
+    uint16_t *Wp16 = bf ? ar.take<uint16_t>((size_t)f * Cp) : nullptr;
     uint16_t *Wp16T = bf ? ar.take<uint16_t>((size_t)f * C) : nullptr;
-    uint16_t *G16 = bf ? ar.take<uint16_t>((size_t)n * C) : nullptr;
+    uint16_t *G16 = bf ? ar.take<uint16_t>((size_t)n * Cp) : nullptr;
     uint16_t *G16T = bf ? ar.take<uint16_t>((size_t)n * C) : nullptr;
     void *gw = pl.gemm ? ar.take<char>(pl.gemm) : nullptr;
     void *cw = ar.take<char>(pl.colsum);
@@ -678,8 +686,8 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
         // NT form: B = W_pred^T (C x f)
         if ((rc = cvt_bf16(n, f, HL, ldhl, HL16, f, s))) return rc;
         if ((rc = transpose_bf16(n, f, HL16, 1, f, HL16T, n, s))) return rc;
-        if ((rc = cvt_bf16(f, C, W_pred, C, Wp16, C, s))) return rc;
-        if ((rc = transpose_bf16(f, C, Wp16, 1, C, Wp16T, f, s))) return rc;
+        if ((rc = cvt_bf16_pad(f, C, W_pred, C, Wp16, Cp, Cp, s))) return rc;
+        if ((rc = transpose_bf16(f, C, Wp16, 1, Cp, Wp16T, f, s))) return rc;
         g.seg[0] = GemmSeg{HL16, f, Wp16T, f, f};
         rc = gemm(L_NT, 1, &g, 1, 1, nullptr, 0, s);
     } else {
@@ -701,11 +709,12 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     d.C = dHL;
     d.ldc = lddhl;
     if (bf) {
-        if ((rc = cvt_bf16(n, C, X, C, G16, C, s))) return rc;
-        if ((rc = transpose_bf16(n, C, G16, 1, C, G16T, n, s))) return rc;
+        if ((rc = cvt_bf16_pad(n, C, X, C, G16, Cp, Cp, s))) return rc;
+        if ((rc = transpose_bf16(n, C, G16, 1, Cp, G16T, n, s))) return rc;
         w.seg[0] = GemmSeg{HL16T, n, G16T, n, n};
         if ((rc = gemm(L_NT, 1, &w, 1, pl.split, gw, pl.gemm, s))) return rc;
-        d.seg[0] = GemmSeg{G16, C, Wp16, C, C};
+        d.seg[0] = GemmSeg{G16, Cp, Wp16, Cp, Cp};   // the zero columns add nothing
+        d.k_pad = Cp - C;
     } else {
         w.seg[0] = GemmSeg{HL, ldhl, X, C, n};
         if ((rc = gemm(L_TN, 1, &w, 0, pl.split, gw, pl.gemm, s))) return rc;

@@ -121,6 +121,7 @@ struct GemmProblem {
     const float *bias;  // [N] or null
     int relu;
     uint16_t *C16;      // when set: write bfloat16 (RNE) here instead of C (leading dim ldc)
+    int32_t k_pad;      // trailing K columns that are zero padding (left out of the flop count)
 };
 // Up to two problems of equal layout and equal M, N, K in one launch
 // (grouped).  `bf16` selects bfloat16 operands (uint16 bits) instead of
@@ -159,6 +160,9 @@ int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16,
 // float32 -> bfloat16 bits (RNE), 2-D with leading dimensions
 int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
              hipStream_t s);
+// the same, and columns cols .. ycols-1 of y set to zero (K padding)
+int cvt_bf16_pad(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
+                 int64_t ycols, hipStream_t s);
 
 // CSR transpose --------------------------------------------------------------
 // values of A^T for a symmetric pattern (A^T shares A's indptr / indices)

@@ -219,22 +219,24 @@ __global__ __launch_bounds__(256) void loss_rows_kernel(int kind, int32_t n, int
     }
 }
 
-// loss = scale * sum_i rowloss[i] in fixed order: blocks of kLossSeg rows
-// reduce to one double each, then one block adds those; a single segment
-// (n <= kLossSeg) writes the loss directly.
-constexpr int kLossSeg = 16384;
+// loss = scale * sum_i rowloss[i] in fixed order.  Up to kLossOne rows: one
+// block of 1024 threads writes the loss directly.  Beyond: blocks of kLossSeg
+// rows reduce to one double each, then one block adds those.
+constexpr int kLossSeg = 2048;
+constexpr int kLossOne = 16384;
 
-__global__ __launch_bounds__(256) void loss_partial_kernel(int32_t n, const float *__restrict__ rowloss,
-                                                           double *__restrict__ part, double scale,
-                                                           float *__restrict__ loss) {
-    __shared__ double sh[256];
-    const int64_t base = (int64_t)blockIdx.x * kLossSeg;
-    const int64_t end = min((int64_t)n, base + kLossSeg);
+template <int T>
+__global__ __launch_bounds__(T) void loss_partial_kernel(int32_t n, int64_t seg, const float *__restrict__ rowloss,
+                                                         double *__restrict__ part, double scale,
+                                                         float *__restrict__ loss) {
+    __shared__ double sh[T];
+    const int64_t base = (int64_t)blockIdx.x * seg;
+    const int64_t end = min((int64_t)n, base + seg);
     double s = 0.0;
-    for (int64_t i = base + threadIdx.x; i < end; i += 256) s += (double)rowloss[i];
+    for (int64_t i = base + threadIdx.x; i < end; i += T) s += (double)rowloss[i];
     sh[threadIdx.x] = s;
     __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
+    for (int o = T / 2; o > 0; o >>= 1) {
         if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
         __syncthreads();
     }
@@ -259,10 +261,11 @@ __global__ __launch_bounds__(256) void loss_reduce_kernel(int32_t nparts, const 
 }
 
 // rows on gridDim.y (strided), columns four per thread
-__global__ __launch_bounds__(256) void cvt_bf16_kernel(int64_t rows, int64_t cols, const float *__restrict__ x,
-                                                       int64_t ldx, uint16_t *__restrict__ y, int64_t ldy, int vec4) {
+__global__ __launch_bounds__(256) void cvt_bf16_kernel(int64_t rows, int64_t cols, int64_t ycols,
+                                                       const float *__restrict__ x, int64_t ldx,
+                                                       uint16_t *__restrict__ y, int64_t ldy, int vec4) {
     const int64_t c = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
-    if (c >= cols) return;
+    if (c >= ycols) return;
     for (int64_t r = blockIdx.y; r < rows; r += gridDim.y) {
         const float *xr = x + r * ldx;
         uint16_t *yr = y + r * ldy;
@@ -272,7 +275,7 @@ __global__ __launch_bounds__(256) void cvt_bf16_kernel(int64_t rows, int64_t col
             const uint32_t hi = (uint32_t)f32_to_bf16_rne(v.z) | ((uint32_t)f32_to_bf16_rne(v.w) << 16);
             *(uint2 *)(yr + c) = make_uint2(lo, hi);
         } else {
-            for (int64_t e = c; e < c + 4 && e < cols; ++e) yr[e] = f32_to_bf16_rne(xr[e]);
+            for (int64_t e = c; e < c + 4 && e < ycols; ++e) yr[e] = e < cols ? f32_to_bf16_rne(xr[e]) : 0;
         }
     }
 }
@@ -450,12 +453,12 @@ int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void
         return GCN_EWORKSPACE;
     }
     ProfScope ps(K_LOSS_REDUCE, s, 0.0, (double)n * 4.0);
-    if (nparts == 1) {
-        hipLaunchKernelGGL(loss_partial_kernel, dim3(1), dim3(256), 0, s, n, rowloss, part, scale, loss);
+    if (n <= kLossOne) {
+        hipLaunchKernelGGL(loss_partial_kernel<1024>, dim3(1), dim3(1024), 0, s, n, (int64_t)kLossOne, rowloss,
+                           part, scale, loss);
     } else {
-        if (nparts > 1)
-            hipLaunchKernelGGL(loss_partial_kernel, dim3((unsigned)nparts), dim3(256), 0, s, n, rowloss, part,
-                               0.0, (float *)nullptr);
+        hipLaunchKernelGGL(loss_partial_kernel<256>, dim3((unsigned)nparts), dim3(256), 0, s, n, (int64_t)kLossSeg,
+                           rowloss, part, 0.0, (float *)nullptr);
         hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(256), 0, s, nparts, part, scale, loss);
     }
     GCN_LAUNCH_CHECK("loss_reduce_kernel");
@@ -480,19 +483,23 @@ int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16,
     return GCN_OK;
 }
 
-int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
-             hipStream_t s) {
-    const int64_t total = rows * cols;
-    if (total <= 0) return GCN_OK;
+int cvt_bf16_pad(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
+                 int64_t ycols, hipStream_t s) {
+    if (rows <= 0 || ycols <= 0) return GCN_OK;
     const int vec4 = (ldx % 4 == 0 && ldy % 4 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)y & 7) == 0) ? 1 : 0;
-    const int64_t gx = (cols + 1023) / 1024;
+    const int64_t gx = (ycols + 1023) / 1024;
     int64_t gy = rows < 65535 ? rows : 65535;
     if (gx * gy > 16384) gy = (16384 + gx - 1) / gx;
-    ProfScope ps(K_CVT_BF16, s, 0.0, (double)total * 6.0);
-    hipLaunchKernelGGL(cvt_bf16_kernel, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, s, rows, cols, x, ldx, y,
-                       ldy, vec4);
+    ProfScope ps(K_CVT_BF16, s, 0.0, (double)rows * cols * 4.0 + (double)rows * ycols * 2.0);
+    hipLaunchKernelGGL(cvt_bf16_kernel, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, s, rows, cols, ycols, x,
+                       ldx, y, ldy, vec4);
     GCN_LAUNCH_CHECK("cvt_bf16_kernel");
     return GCN_OK;
+}
+
+int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
+             hipStream_t s) {
+    return cvt_bf16_pad(rows, cols, x, ldx, y, ldy, cols, s);
 }
 
 }  // namespace gcn

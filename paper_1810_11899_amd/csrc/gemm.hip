@@ -521,49 +521,74 @@ void gemm_bf16_kernel(DevArgs args) {
         }
 }
 
-// C = sum over splits of the partial tiles, in split order.
-// Adds the split partials in split order and applies the epilogue.  VEC: four
-// consecutive columns per thread (N, ldc and the output 16-byte aligned).
+// C = sum over splits of the partial tiles, then the epilogue.  A block
+// covers 256 / G output elements (float4 groups when VEC: N, ldc and the
+// output 16-byte aligned) with G threads each: thread group g adds splits g,
+// g + G, g + 2G, ... in increasing order, and the G group sums are added in
+// group order.  The order is fixed, so results are bitwise reproducible; G > 1
+// gives small outputs with many splits (weight gradients) enough threads.
 template <bool VEC>
-__global__ __launch_bounds__(256) void splitk_reduce(DevArgs args) {
+__global__ __launch_bounds__(256) void splitk_reduce(DevArgs args, int G) {
+    using V = typename std::conditional<VEC, float4, float>::type;
+    __shared__ V sh[256];
     const int pi = blockIdx.y;
     const DevProblem &P = args.p[pi];
     const int64_t total = (int64_t)P.M * P.N;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    if (VEC) {
-        const int n4 = P.N / 4;
-        const int64_t total4 = (int64_t)P.M * n4;
-        for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total4; e += stride) {
-            float4 acc = ((const float4 *)P.partial)[e];
-            for (int s = 1; s < P.split; ++s) {
-                const float4 v = ((const float4 *)(P.partial + (int64_t)s * total))[e];
-                acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    const int W = VEC ? 4 : 1;
+    const int nw = P.N / W;                     // vectors per row
+    const int64_t count = (int64_t)P.M * nw;    // vectors in the output
+    const int epb = 256 / G;
+    const int el = threadIdx.x % epb, g = threadIdx.x / epb;
+    const V *part = (const V *)P.partial;
+    const int64_t pstride = total / W;          // one split's partials, in vectors
+    for (int64_t base = (int64_t)blockIdx.x * epb; base < count; base += (int64_t)gridDim.x * epb) {
+        const int64_t e = base + el;
+        V acc{};
+        if (e < count && g < P.split) {
+            acc = part[(int64_t)g * pstride + e];
+            for (int s = g + G; s < P.split; s += G) {
+                const V v = part[(int64_t)s * pstride + e];
+                if constexpr (VEC) {
+                    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+                } else {
+                    acc += v;
+                }
             }
-            const int row = (int)(e / n4), col = (int)(e - (int64_t)row * n4) * 4;
-            float o[4] = {acc.x, acc.y, acc.z, acc.w};
+        }
+        sh[threadIdx.x] = acc;
+        __syncthreads();
+        if (g == 0 && e < count) {
+            for (int q = 1; q < G && q < P.split; ++q) {
+                const V v = sh[q * epb + el];
+                if constexpr (VEC) {
+                    acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+                } else {
+                    acc += v;
+                }
+            }
+            const int row = (int)(e / nw), col = (int)(e - (int64_t)row * nw) * W;
+            float o[W];
+            if constexpr (VEC) {
+                o[0] = acc.x; o[1] = acc.y; o[2] = acc.z; o[3] = acc.w;
+            } else {
+                o[0] = acc;
+            }
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int j = 0; j < W; ++j) {
                 if (P.bias) o[j] += P.bias[col + j];
                 if (P.relu) o[j] = fmaxf(o[j], 0.0f);
             }
             if (P.C16) {
                 uint16_t *d = P.C16 + (int64_t)row * P.ldc + col;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) d[j] = to_bf16(o[j]);
-            } else {
+                for (int j = 0; j < W; ++j) d[j] = to_bf16(o[j]);
+            } else if constexpr (VEC) {
                 *(float4 *)(P.C + (int64_t)row * P.ldc + col) = float4{o[0], o[1], o[2], o[3]};
+            } else {
+                P.C[(int64_t)row * P.ldc + col] = o[0];
             }
         }
-        return;
-    }
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total; e += stride) {
-        float acc = P.partial[e];
-        for (int s = 1; s < P.split; ++s) acc += P.partial[(int64_t)s * total + e];
-        const int row = (int)(e / P.N), col = (int)(e % P.N);
-        if (P.bias) acc += P.bias[col];
-        if (P.relu) acc = fmaxf(acc, 0.0f);
-        if (P.C16) P.C16[(int64_t)row * P.ldc + col] = to_bf16(acc);
-        else P.C[(int64_t)row * P.ldc + col] = acc;
+        __syncthreads();
     }
 }
 
@@ -594,7 +619,10 @@ constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU
 #ifndef GCN_BIG_WAVES
 #define GCN_BIG_WAVES 8
 #endif
-constexpr int kBigWaves = GCN_BIG_WAVES;                 // 4 (2 x 2) or 8 (2 x 4)
+constexpr int kBigWaves = GCN_BIG_WAVES;
+#ifndef GCN_BIG_EPI_LDS
+#define GCN_BIG_EPI_LDS 1
+#endif                 // 4 (2 x 2) or 8 (2 x 4)
 constexpr int kBigThreads = 64 * kBigWaves;
 constexpr int kBigWN = kBigWaves / 2;                     // wavefronts along N
 constexpr int kBigWTM = 128, kBigWTN = kBigT / kBigWN;   // wavefront tile
@@ -714,12 +742,85 @@ void gemm_bf16_big_kernel(DevArgs args) {
         }
     }
 
-    // ---- epilogue (accumulator layout as in the other kernels); one call
-    // per accumulator block with constant indices, so that the accumulators
-    // stay in registers
     const bool to_partial = P.split > 1;
     float *dst = to_partial ? P.partial + (int64_t)bc.split * P.M * P.N : P.C;
     const int64_t ldd = to_partial ? P.N : P.ldc;
+#if GCN_BIG_EPI_LDS
+    // ---- epilogue through LDS, in two passes of 128 rows: the wavefronts
+    // holding those rows deposit their accumulators row-major in the (now
+    // idle) operand ring, then every wavefront writes whole 256-column rows,
+    // 16 bytes per lane.  Accumulator blocks are moved by calls with constant
+    // indices, so that they stay in registers.
+    static_assert(kBigStages >= 4, "the epilogue stages 128 x 256 floats in the operand ring");
+    float *stg = (float *)&lds[0][0][0];
+    auto put = [&](const floatx16 &v, int i, int j) {
+        const int lc = wn * kBigWTN + j * 32 + (lane & 31);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int lr = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            stg[lr * kBigT + lc] = v[r];
+        }
+    };
+    const bool c16 = !to_partial && P.C16 != nullptr;
+    const bool vec = c16 ? (P.ldc % 4 == 0 && ((uintptr_t)P.C16 & 7) == 0)
+                         : (ldd % 4 == 0 && ((uintptr_t)dst & 15) == 0);
+    const int col = n0 + 4 * lane;
+    float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (!to_partial && P.bias)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bv[e] = col + e < P.N ? P.bias[col + e] : 0.0f;
+    const bool relu = !to_partial && P.relu;
+    __syncthreads();   // every wavefront is done reading the ring
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        if (wm == h) {
+            put(acc[0][0], 0, 0); put(acc[0][1], 0, 1);
+            put(acc[1][0], 1, 0); put(acc[1][1], 1, 1);
+            put(acc[2][0], 2, 0); put(acc[2][1], 2, 1);
+            put(acc[3][0], 3, 0); put(acc[3][1], 3, 1);
+            if constexpr (kBigFN == 4) {
+                put(acc[0][2], 0, 2); put(acc[0][3], 0, 3);
+                put(acc[1][2], 1, 2); put(acc[1][3], 1, 3);
+                put(acc[2][2], 2, 2); put(acc[2][3], 2, 3);
+                put(acc[3][2], 3, 2); put(acc[3][3], 3, 3);
+            }
+        }
+        __syncthreads();
+        for (int rr = wave; rr < 128; rr += kBigWaves) {
+            const int row = m0 + h * 128 + rr;
+            if (row > Mlast || col > Nlast) continue;
+            const float4 q = *(const float4 *)&stg[rr * kBigT + 4 * lane];
+            float o[4] = {q.x + bv[0], q.y + bv[1], q.z + bv[2], q.w + bv[3]};
+            if (relu)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
+            if (c16) {
+                uint16_t *d = P.C16 + (int64_t)row * P.ldc + col;
+                if (vec && col + 3 <= Nlast) {
+                    *(uint2 *)d = make_uint2((uint32_t)to_bf16(o[0]) | ((uint32_t)to_bf16(o[1]) << 16),
+                                             (uint32_t)to_bf16(o[2]) | ((uint32_t)to_bf16(o[3]) << 16));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (col + e <= Nlast) d[e] = to_bf16(o[e]);
+                }
+            } else {
+                float *d = dst + (int64_t)row * ldd + col;
+                if (vec && col + 3 <= Nlast) {
+                    *(float4 *)d = make_float4(o[0], o[1], o[2], o[3]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (col + e <= Nlast) d[e] = o[e];
+                }
+            }
+        }
+        __syncthreads();
+    }
+#else
+    // ---- epilogue (accumulator layout as in the other kernels); one call
+    // per accumulator block with constant indices, so that the accumulators
+    // stay in registers
     auto epi = [&](const floatx16 &v, int i, int j) {
         const int col = n0 + wn * kBigWTN + j * 32 + (lane & 31);
         if (col < P.N) {
@@ -752,6 +853,7 @@ void gemm_bf16_big_kernel(DevArgs args) {
         epi(acc[2][2], 2, 2); epi(acc[2][3], 2, 3);
         epi(acc[3][2], 3, 2); epi(acc[3][3], 3, 3);
     }
+#endif
 }
 
 bool vec_ok(int layout, const GemmProblem &g, int esz) {
@@ -776,12 +878,15 @@ int tile_n_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBN16 : kTBN); }
 // of its k-stage, with 16-byte aligned operand rows.
 bool big_ok(int layout, int nprob, const GemmProblem *probs) {
     if (layout != L_NT || GCN_BF16_BIG == 0) return false;
-    for (int i = 0; i < nprob; ++i)
+    for (int i = 0; i < nprob; ++i) {
+        // a side of 128 or less would leave most of a 256-wide tile idle
+        if (probs[i].M <= 128 || probs[i].N <= 128) return false;
         for (int s = 0; s < 2; ++s) {
             const GemmSeg &sg = probs[i].seg[s];
             if (sg.K == 0) continue;
             if (sg.K % kBigBK || sg.lda % 8 || sg.ldb % 8 || !al(sg.A, 16) || !al(sg.B, 16)) return false;
         }
+    }
     return true;
 }
 
@@ -866,6 +971,7 @@ int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows) {
     else sp = tiles >= 256 ? 1 : 512 / tiles;
     const int64_t max_sp = kt / 8;      // keep >= 8 k-tiles per split
     if (sp > max_sp) sp = max_sp;
+    if (sp > 64) sp = 64;               // partials are written and read once each
     if (sp < 1) sp = 1;
     return (int)sp;
 }
@@ -893,7 +999,8 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     double flops = 0.0;
     for (int i = 0; i < nprob; ++i) {
         vec = vec && vec_ok(layout, probs[i], bf16 ? 2 : 4);
-        flops += 2.0 * probs[i].M * probs[i].N * ((double)probs[i].seg[0].K + probs[i].seg[1].K);
+        flops += 2.0 * probs[i].M * probs[i].N *
+                 ((double)probs[i].seg[0].K + probs[i].seg[1].K - probs[i].k_pad);
     }
     float *partial = nullptr;
     if (split_k > 1) {
@@ -931,9 +1038,11 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
             bytes += (double)a.p[i].M * a.p[i].N * 4.0 * (a.p[i].split + 1);
         ProfScope ps(K_SPLITK_REDUCE, s, 0.0, bytes);
         int64_t maxe = 0;
-        for (int i = 0; i < nprob; ++i) maxe = std::max<int64_t>(maxe, (int64_t)a.p[i].M * a.p[i].N);
-        int64_t g = (maxe + 255) / 256;
-        if (g > 4096) g = 4096;
+        int maxsplit = 1;
+        for (int i = 0; i < nprob; ++i) {
+            maxe = std::max<int64_t>(maxe, (int64_t)a.p[i].M * a.p[i].N);
+            maxsplit = std::max(maxsplit, a.p[i].split);
+        }
         // a problem without splits is written by the main kernel already; the
         // reduce skips it by running over zero elements
         DevArgs r = a;
@@ -943,14 +1052,15 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
             const DevProblem &q = r.p[i];
             v4 = v4 && q.N % 4 == 0 && q.ldc % 4 == 0 && (q.C16 || al(q.C, 16));
         }
-        if (v4) {
-            g = (maxe / 4 + 255) / 256;
-            if (g > 4096) g = 4096;
-            if (g < 1) g = 1;
-            hipLaunchKernelGGL(splitk_reduce<true>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r);
-        } else {
-            hipLaunchKernelGGL(splitk_reduce<false>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r);
-        }
+        const int64_t vecs = v4 ? maxe / 4 : maxe;
+        // threads per output vector: up to 8, for about 2^18 threads in all
+        int G = 1;
+        while (G < 8 && 2 * G <= maxsplit && vecs * nprob * G < (1 << 18)) G *= 2;
+        int64_t g = (vecs + 256 / G - 1) / (256 / G);
+        if (g > 4096) g = 4096;
+        if (g < 1) g = 1;
+        if (v4) hipLaunchKernelGGL(splitk_reduce<true>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r, G);
+        else hipLaunchKernelGGL(splitk_reduce<false>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r, G);
         GCN_LAUNCH_CHECK("splitk_reduce");
     }
     return GCN_OK;

@@ -187,7 +187,7 @@ def test_aggregate_is_deterministic(ws):
 
 
 # ------------------------------------------------------------------ bf16 ----
-@pytest.mark.parametrize("k", [64, 128, 200, 512, 602])
+@pytest.mark.parametrize("k", [64, 128, 200, 256, 264, 384, 512, 602, 1024])
 def test_aggregate_bf16(k, ws):
     """Against the oracle on the unrounded inputs (the 2e-2 gate) and, tighter,
     on the bfloat16-rounded inputs (float32 accumulation only)."""
