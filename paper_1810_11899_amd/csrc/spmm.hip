@@ -30,6 +30,11 @@ namespace {
 
 constexpr int kWavesPerBlock = 4;
 constexpr int kUnroll = 4;
+constexpr int kMaxIpw = 256;   // merge items per wavefront, at most
+#ifndef GCN_SPMM_U
+#define GCN_SPMM_U 4
+#endif
+
 
 // Smallest r in [0, n_rows] whose row-end item sits at merge position >= d,
 // i.e. indptr[r+1] + r >= d (n_rows when none does).  64-ary search: every
@@ -54,6 +59,46 @@ __device__ __forceinline__ int merge_search(const int32_t *__restrict__ indptr, 
         }
     }
     return (int)lo;
+}
+
+// The merge range of one wavefront: rows r0..r1 (r1 may be cut or n_rows)
+// and edge positions [p0, p1).  Its edges (at most kMaxIpw) and row pointers
+// are copied into LDS with coalesced loads, so that the gather loop waits on
+// one global load per edge, the feature row, instead of three dependent ones
+// (row pointer, edge index, feature row).
+struct EdgeStage {
+    int32_t idx[kWavesPerBlock][kMaxIpw];
+    float val[kWavesPerBlock][kMaxIpw];
+    int32_t ptr[kWavesPerBlock][kMaxIpw + 2];
+};
+struct WaveRange {
+    int r0, r1;
+    int64_t p0, p1;
+};
+// Every thread of the block calls it (it ends with a block barrier); `live`
+// is false for wavefronts past the last merge range.
+__device__ __forceinline__ WaveRange stage_wave(EdgeStage &st, int wv, int lane, bool live, int64_t wave,
+                                                int ipw, int64_t items, int32_t n_rows,
+                                                const int32_t *__restrict__ indptr,
+                                                const int32_t *__restrict__ indices,
+                                                const float *__restrict__ vals) {
+    WaveRange w{0, 0, 0, 0};
+    if (live) {
+        const int64_t d0 = wave * ipw;
+        const int64_t d1 = d0 + ipw < items ? d0 + ipw : items;
+        w.r0 = merge_search(indptr, n_rows, d0, lane);
+        w.r1 = merge_search(indptr, n_rows, d1, lane);
+        w.p0 = d0 - w.r0;
+        w.p1 = d1 - w.r1;
+        for (int i = lane; i < (int)(w.p1 - w.p0); i += 64) {
+            st.idx[wv][i] = indices[w.p0 + i];
+            st.val[wv][i] = vals[w.p0 + i];
+        }
+        const int nr = min(w.r1, n_rows - 1) - w.r0 + 2;   // pointers r0 .. min(r1, n_rows - 1) + 1
+        for (int i = lane; i < nr; i += 64) st.ptr[wv][i] = indptr[w.r0 + i];
+    }
+    __syncthreads();
+    return w;
 }
 
 template <int VEC, bool BF16> struct Row;
@@ -148,13 +193,17 @@ __global__ __launch_bounds__(256) void spmm_main(
     using Elem = typename std::conditional<BF16, uint16_t, float>::type;
     const Elem *__restrict__ X = (const Elem *)Xv;
     const int lane = threadIdx.x & 63;
-    const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    if (wave >= waves) return;
-    const int64_t d0 = wave * ipw;
-    const int64_t d1 = d0 + ipw < items ? d0 + ipw : items;
-    const int r0 = merge_search(indptr, n_rows, d0, lane);
-    const int r1 = merge_search(indptr, n_rows, d1, lane);
-    const int64_t p0 = d0 - r0, p1 = d1 - r1;
+    const int wv = threadIdx.x >> 6;
+    const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + wv;
+    __shared__ EdgeStage st;
+    const bool live = wave < waves;
+    const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, indptr, indices, vals);
+    if (!live) return;
+    const int r0 = wr.r0, r1 = wr.r1;
+    const int64_t p0 = wr.p0, p1 = wr.p1;
+    const int32_t *const e_idx = st.idx[wv];
+    const float *const e_val = st.val[wv];
+    const int32_t *const r_ptr = st.ptr[wv];
 
     constexpr int SW = 64 * VEC * CT;
     const int cbase = blockIdx.y * SW + lane * VEC;
@@ -164,7 +213,7 @@ __global__ __launch_bounds__(256) void spmm_main(
 
     int32_t hrow = -1, trow = -1;
     for (int r = r0; r <= r1 && r < n_rows; ++r) {
-        const int64_t rb = indptr[r], re = indptr[r + 1];
+        const int64_t rb = r_ptr[r - r0], re = r_ptr[r - r0 + 1];
         const bool complete = r < r1;
         const int64_t pb = p0 > rb ? p0 : rb;
         const int64_t pe = complete ? re : p1;
@@ -179,7 +228,7 @@ __global__ __launch_bounds__(256) void spmm_main(
             int32_t j[kUnroll];
             float w[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) { j[u] = indices[p + u]; w[u] = vals[p + u]; }
+            for (int u = 0; u < kUnroll; ++u) { j[u] = e_idx[p + u - p0]; w[u] = e_val[p + u - p0]; }
             Row<VEC, BF16> x[kUnroll][CT];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
@@ -195,8 +244,8 @@ __global__ __launch_bounds__(256) void spmm_main(
                         for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(w[u], x[u][t].v[v], acc[t][v]);
         }
         for (; p < pe; ++p) {
-            const int32_t j = indices[p];
-            const float w = vals[p];
+            const int32_t j = e_idx[p - p0];
+            const float w = e_val[p - p0];
 #pragma unroll
             for (int t = 0; t < CT; ++t)
                 if (cok[t]) {
@@ -274,21 +323,25 @@ __global__ __launch_bounds__(256) void spmm_sliced(
     int64_t chunk;
     if (!slice_of_block(map, blockIdx.x, slice, chunk)) return;
     const int lane = threadIdx.x & 63;
-    const int64_t wave = chunk * kWavesPerBlock + (threadIdx.x >> 6);
-    if (wave >= waves) return;
-    const int64_t d0 = wave * ipw;
-    const int64_t d1 = d0 + ipw < items ? d0 + ipw : items;
-    const int r0 = merge_search(indptr, n_rows, d0, lane);
-    const int r1 = merge_search(indptr, n_rows, d1, lane);
-    const int64_t p0 = d0 - r0, p1 = d1 - r1;
+    const int wv = threadIdx.x >> 6;
+    const int64_t wave = chunk * kWavesPerBlock + wv;
+    __shared__ EdgeStage st;
+    const bool live = wave < waves;
+    const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, indptr, indices, vals);
+    if (!live) return;
+    const int r0 = wr.r0, r1 = wr.r1;
+    const int64_t p0 = wr.p0, p1 = wr.p1;
+    const int32_t *const e_idx = st.idx[wv];
+    const float *const e_val = st.val[wv];
+    const int32_t *const r_ptr = st.ptr[wv];
     const int g = lane >> 4;
     const int col = slice * 64 + (lane & 15) * 4;
     const bool cok = col < k;
-    constexpr int U = 4;  // edges per lane group in flight
+    constexpr int U = GCN_SPMM_U;  // edges per lane group in flight
 
     int32_t hrow = -1, trow = -1;
     for (int r = r0; r <= r1 && r < n_rows; ++r) {
-        const int64_t rb = indptr[r], re = indptr[r + 1];
+        const int64_t rb = r_ptr[r - r0], re = r_ptr[r - r0 + 1];
         const bool complete = r < r1;
         const int64_t pb = p0 > rb ? p0 : rb;
         const int64_t pe = complete ? re : p1;
@@ -298,7 +351,7 @@ __global__ __launch_bounds__(256) void spmm_sliced(
             int32_t j[U];
             float w[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) { j[u] = indices[p + 4 * u]; w[u] = vals[p + 4 * u]; }
+            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + 4 * u - p0]; w[u] = e_val[p + 4 * u - p0]; }
             float4 x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
@@ -312,8 +365,8 @@ __global__ __launch_bounds__(256) void spmm_sliced(
             }
         }
         for (; p < pe; p += 4) {
-            const int32_t j = indices[p];
-            const float w = vals[p];
+            const int32_t j = e_idx[p - p0];
+            const float w = e_val[p - p0];
             const float4 x = cok ? *(const float4 *)(X + (int64_t)j * ldx + col) : make_float4(0.f, 0.f, 0.f, 0.f);
             a0 = fmaf(w, x.x, a0);
             a1 = fmaf(w, x.y, a1);
@@ -531,7 +584,7 @@ SpmmPlan spmm_plan(int32_t n_rows, int32_t nnz) {
     int64_t ipw = (p.items + 8191) / 8192;
     ipw = (ipw + 31) / 32 * 32;
     if (ipw < 32) ipw = 32;
-    if (ipw > 256) ipw = 256;
+    if (ipw > kMaxIpw) ipw = kMaxIpw;
     p.ipw = (int)ipw;
     p.waves = (p.items + ipw - 1) / ipw;
     if (p.waves == 0) p.waves = 1;
