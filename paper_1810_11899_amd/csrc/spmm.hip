@@ -76,9 +76,11 @@ struct WaveRange {
     int64_t p0, p1;
 };
 // Every thread of the block calls it (it ends with a block barrier); `live`
-// is false for wavefronts past the last merge range.
+// is false for wavefronts past the last merge range.  bnd[w] is the first row
+// of merge range w (spmm_bounds_kernel).
 __device__ __forceinline__ WaveRange stage_wave(EdgeStage &st, int wv, int lane, bool live, int64_t wave,
                                                 int ipw, int64_t items, int32_t n_rows,
+                                                const int32_t *__restrict__ bnd,
                                                 const int32_t *__restrict__ indptr,
                                                 const int32_t *__restrict__ indices,
                                                 const float *__restrict__ vals) {
@@ -86,8 +88,8 @@ __device__ __forceinline__ WaveRange stage_wave(EdgeStage &st, int wv, int lane,
     if (live) {
         const int64_t d0 = wave * ipw;
         const int64_t d1 = d0 + ipw < items ? d0 + ipw : items;
-        w.r0 = merge_search(indptr, n_rows, d0, lane);
-        w.r1 = merge_search(indptr, n_rows, d1, lane);
+        w.r0 = bnd[wave];
+        w.r1 = bnd[wave + 1];
         w.p0 = d0 - w.r0;
         w.p1 = d1 - w.r1;
         for (int i = lane; i < (int)(w.p1 - w.p0); i += 64) {
@@ -99,6 +101,20 @@ __device__ __forceinline__ WaveRange stage_wave(EdgeStage &st, int wv, int lane,
     }
     __syncthreads();
     return w;
+}
+
+// bnd[w] = the row holding merge position min(w * ipw, items), w = 0 ..
+// waves (n_rows for the end): the row ranges of all wavefronts, searched once
+// per product rather than by every wavefront of every column slice.
+__global__ __launch_bounds__(256) void spmm_bounds_kernel(int32_t n_rows, const int32_t *__restrict__ indptr,
+                                                          int64_t items, int ipw, int64_t waves,
+                                                          int32_t *__restrict__ bnd) {
+    const int lane = threadIdx.x & 63;
+    const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    if (w > waves) return;
+    const int64_t d = w * ipw < items ? w * ipw : items;
+    const int r = merge_search(indptr, n_rows, d, lane);
+    if (lane == 0) bnd[w] = r;
 }
 
 template <int VEC, bool BF16> struct Row;
@@ -188,7 +204,7 @@ __global__ __launch_bounds__(256) void spmm_main(
     int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
     const float *__restrict__ vals, const void *__restrict__ Xv, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
-    int64_t items, int ipw, int64_t waves, float *__restrict__ carry,
+    int64_t items, int ipw, int64_t waves, const int32_t *__restrict__ bnd, float *__restrict__ carry,
     int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
     using Elem = typename std::conditional<BF16, uint16_t, float>::type;
     const Elem *__restrict__ X = (const Elem *)Xv;
@@ -197,7 +213,7 @@ __global__ __launch_bounds__(256) void spmm_main(
     const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + wv;
     __shared__ EdgeStage st;
     const bool live = wave < waves;
-    const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, indptr, indices, vals);
+    const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, bnd, indptr, indices, vals);
     if (!live) return;
     const int r0 = wr.r0, r1 = wr.r1;
     const int64_t p0 = wr.p0, p1 = wr.p1;
@@ -317,8 +333,8 @@ __global__ __launch_bounds__(256) void spmm_sliced(
     int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
     const float *__restrict__ vals, const float *__restrict__ X, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
-    int64_t items, int ipw, int64_t waves, SliceMap map, float *__restrict__ carry,
-    int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
+    int64_t items, int ipw, int64_t waves, SliceMap map, const int32_t *__restrict__ bnd,
+    float *__restrict__ carry, int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
     int slice;
     int64_t chunk;
     if (!slice_of_block(map, blockIdx.x, slice, chunk)) return;
@@ -327,7 +343,7 @@ __global__ __launch_bounds__(256) void spmm_sliced(
     const int64_t wave = chunk * kWavesPerBlock + wv;
     __shared__ EdgeStage st;
     const bool live = wave < waves;
-    const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, indptr, indices, vals);
+    const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, bnd, indptr, indices, vals);
     if (!live) return;
     const int r0 = wr.r0, r1 = wr.r1;
     const int64_t p0 = wr.p0, p1 = wr.p1;
@@ -493,9 +509,9 @@ template <int VEC, int CT, bool BF16>
 void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr,
                  const int32_t *indices, const float *vals, const void *X, int32_t k, int64_t ldx,
                  void *out, int64_t ldo, int epi, const float *bias, const SpmmPlan &pl,
-                 float *carry, int32_t *hr, int32_t *tr) {
+                 const int32_t *bnd, float *carry, int32_t *hr, int32_t *tr) {
     hipLaunchKernelGGL((spmm_main<VEC, CT, BF16>), grid, dim3(256), 0, s, n_rows, indptr, indices,
-                       vals, X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw, pl.waves, carry, hr,
+                       vals, X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw, pl.waves, bnd, carry, hr,
                        tr);
 }
 
@@ -510,7 +526,8 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, cons
     float *carry = ar.take<float>((size_t)2 * pl.waves * k);
     int32_t *hr = ar.take<int32_t>(pl.waves);
     int32_t *tr = ar.take<int32_t>(pl.waves);
-    if (!carry || !hr || !tr) {
+    int32_t *bnd = ar.take<int32_t>(pl.waves + 1);
+    if (!carry || !hr || !tr || !bnd) {
         set_error("spmm: workspace too small (%zu < %zu bytes)", ws_bytes,
                   spmm_workspace_bytes(n_rows, nnz, k));
         return GCN_EWORKSPACE;
@@ -533,17 +550,20 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, cons
                          (double)n_rows * k * out_bytes;
     {
         ProfScope ps(bf16 ? K_SPMM_BF16 : K_SPMM, s, 2.0 * nnz * k, bytes);
+        hipLaunchKernelGGL(spmm_bounds_kernel, dim3((unsigned)((pl.waves + kWavesPerBlock) / kWavesPerBlock)),
+                           dim3(256), 0, s, n_rows, indptr, pl.items, pl.ipw, pl.waves, bnd);
+        GCN_LAUNCH_CHECK("spmm_bounds_kernel");
         if (sliced) {
             const SliceMap m = make_slice_map(k, pl.waves);
             hipLaunchKernelGGL(spmm_sliced, dim3((unsigned)slice_map_blocks(m)), dim3(256), 0, s, n_rows, indptr,
                                indices, vals, (const float *)X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw,
-                               pl.waves, m, carry, hr, tr);
+                               pl.waves, m, bnd, carry, hr, tr);
             GCN_LAUNCH_CHECK("spmm_sliced");
         } else
 #define GCN_SPMM_CASE(V, C, B)                                                                   \
     if (vec == V && ct == C && bf16 == B) {                                                      \
         launch_main<V, C, B>(grid, s, n_rows, indptr, indices, vals, X, k, ldx, out, ldo, epi,   \
-                             bias, pl, carry, hr, tr);                                           \
+                             bias, pl, bnd, carry, hr, tr);                                      \
     } else
         GCN_SPMM_CASE(4, 1, false)
         GCN_SPMM_CASE(4, 2, false)
@@ -594,7 +614,8 @@ SpmmPlan spmm_plan(int32_t n_rows, int32_t nnz) {
 size_t spmm_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k) {
     if (n_rows <= 0 || k <= 0) return 0;
     const SpmmPlan pl = spmm_plan(n_rows, nnz);
-    return align256((size_t)2 * pl.waves * k * sizeof(float)) + 2 * align256(pl.waves * sizeof(int32_t)) + 256;
+    return align256((size_t)2 * pl.waves * k * sizeof(float)) + 2 * align256(pl.waves * sizeof(int32_t)) +
+           align256((pl.waves + 1) * sizeof(int32_t)) + 256;
 }
 
 int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
