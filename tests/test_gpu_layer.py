@@ -35,7 +35,8 @@ def _bias(h, seed):
 
 
 SHAPES = [(777, "rmat", 9, 37, 24), (1500, "er", 12, 64, 48), (2049, "rmat", 15, 130, 100),
-          (1000, "rmat", 11, 256, 128), (900, "rmat", 10, 264, 256)]
+          (1000, "rmat", 11, 256, 128), (900, "rmat", 10, 264, 256), (1024, "rmat", 9, 96, 64),
+          (2048, "er", 8, 128, 100)]
 
 
 PRECS = [(B.GCN_F32, TOL_F32), (B.GCN_BF16, TOL_BF16)]
