@@ -202,8 +202,10 @@ void gemm_kernel(DevArgs args) {
     constexpr bool B_KMAJOR = (LAYOUT != L_NT);
     constexpr int WTM = TBM / 2, WTN = TBN / 2;     // wavefront tile (2 x 2 wavefronts)
     constexpr int FM = WTM / 32, FN = WTN / 32;     // 32x32 accumulator blocks per wavefront
-    __shared__ __attribute__((aligned(16))) T As[2][BK][TBM + PAD];
-    __shared__ __attribute__((aligned(16))) T Bs[2][BK][TBN + PAD];
+    // one LDS block: the two operand double buffers, reused by the epilogue
+    __shared__ __attribute__((aligned(16))) T smem[2 * BK * (TBM + PAD) + 2 * BK * (TBN + PAD)];
+    T(*As)[BK][TBM + PAD] = (T(*)[BK][TBM + PAD])smem;
+    T(*Bs)[BK][TBN + PAD] = (T(*)[BK][TBN + PAD])(smem + 2 * BK * (TBM + PAD));
 
     // ---- which problem / split / tile
     BlockCoord bc;
@@ -292,31 +294,60 @@ void gemm_kernel(DevArgs args) {
         buf ^= 1;
     }
 
-    // ---- epilogue: 32x32 accumulator layout, column = lane % 32,
-    //      row = 8*(r/4) + 4*(lane/32) + r%4
     const bool to_partial = P.split > 1;
     float *dst = to_partial ? P.partial + (int64_t)split * P.M * P.N : P.C;
     const int64_t ldd = to_partial ? P.N : P.ldc;
+    // ---- epilogue through LDS, 32 rows per pass: the two wavefronts holding
+    // those rows deposit their accumulator blocks row-major (row stride 136
+    // floats: the two half-wavefronts' rows, four apart, land 32 banks apart),
+    // then all four wavefronts write whole 128-column rows, 16 bytes per lane.
+    static_assert(FM == 2 && FN == 2 && TBN == 128, "epilogue written for 2 x 2 blocks of a 128-wide tile");
+    constexpr int SLD = 136;
+    static_assert(32 * SLD <= 2 * BK * (TBM + PAD) + 2 * BK * (TBN + PAD), "staging fits the operand buffers");
+    float *stg = smem;
+    const int ecol = n0 + 4 * (lane & 31);
+    float ebv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (!to_partial && P.bias)
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+        for (int e = 0; e < 4; ++e) ebv[e] = ecol + e < P.N ? P.bias[ecol + e] : 0.0f;
+    const bool erelu = !to_partial && P.relu;
+    const bool evec = ldd % 4 == 0 && ((uintptr_t)dst & 15) == 0;
+    auto put = [&](const floatx16 &v, int jb) {
+        const int lc = wn * WTN + jb * 32 + (lane & 31);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int col = n0 + wn * WTN + j * 32 + (lane & 31);
-            if (col >= P.N) continue;
-            const float bv = (!to_partial && P.bias) ? P.bias[col] : 0.0f;
+        for (int r = 0; r < 16; ++r) stg[(8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * SLD + lc] = v[r];
+    };
+    __syncthreads();   // the last tile's operand reads are done
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = m0 + wm * WTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if (row < P.M) {
-                    float v = acc[i][j][r];
-                    if (!to_partial) {
-                        v += bv;
-                        if (P.relu) v = fmaxf(v, 0.0f);
-                    }
-                    dst[(int64_t)row * ldd + col] = v;
+    for (int h = 0; h < 4; ++h) {
+        if (wm == (h >> 1)) {
+            put(acc[h & 1][0], 0);
+            put(acc[h & 1][1], 1);
+        }
+        __syncthreads();
+        // rows 32h .. 32h+31 of the tile; a wavefront writes two rows per store
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int lr = wave * 8 + q * 2 + (lane >> 5);
+            const int row = m0 + 32 * h + lr;
+            if (row < P.M && ecol < P.N) {
+                const float4 x = *(const float4 *)&stg[lr * SLD + 4 * (lane & 31)];
+                float o[4] = {x.x + ebv[0], x.y + ebv[1], x.z + ebv[2], x.w + ebv[3]};
+                if (erelu)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
+                float *d = dst + (int64_t)row * ldd + ecol;
+                if (evec && ecol + 3 < P.N) {
+                    *(float4 *)d = make_float4(o[0], o[1], o[2], o[3]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (ecol + e < P.N) d[e] = o[e];
                 }
             }
         }
+        __syncthreads();
+    }
 }
 
 // ------------------------------------------------------------ bf16 kernel
@@ -620,9 +651,7 @@ constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU
 #define GCN_BIG_WAVES 8
 #endif
 constexpr int kBigWaves = GCN_BIG_WAVES;
-#ifndef GCN_BIG_EPI_LDS
-#define GCN_BIG_EPI_LDS 1
-#endif                 // 4 (2 x 2) or 8 (2 x 4)
+                 // 4 (2 x 2) or 8 (2 x 4)
 constexpr int kBigThreads = 64 * kBigWaves;
 constexpr int kBigWN = kBigWaves / 2;                     // wavefronts along N
 constexpr int kBigWTM = 128, kBigWTN = kBigT / kBigWN;   // wavefront tile
@@ -745,13 +774,13 @@ void gemm_bf16_big_kernel(DevArgs args) {
     const bool to_partial = P.split > 1;
     float *dst = to_partial ? P.partial + (int64_t)bc.split * P.M * P.N : P.C;
     const int64_t ldd = to_partial ? P.N : P.ldc;
-#if GCN_BIG_EPI_LDS
     // ---- epilogue through LDS, in two passes of 128 rows: the wavefronts
     // holding those rows deposit their accumulators row-major in the (now
     // idle) operand ring, then every wavefront writes whole 256-column rows,
     // 16 bytes per lane.  Accumulator blocks are moved by calls with constant
     // indices, so that they stay in registers.
     static_assert(kBigStages >= 4, "the epilogue stages 128 x 256 floats in the operand ring");
+    static_assert(kBigFM == 4 && (kBigFN == 4 || kBigFN == 2), "epilogue unrolled for 4 x 4 or 4 x 2 blocks");
     float *stg = (float *)&lds[0][0][0];
     auto put = [&](const floatx16 &v, int i, int j) {
         const int lc = wn * kBigWTN + j * 32 + (lane & 31);
@@ -817,43 +846,6 @@ void gemm_bf16_big_kernel(DevArgs args) {
         }
         __syncthreads();
     }
-#else
-    // ---- epilogue (accumulator layout as in the other kernels); one call
-    // per accumulator block with constant indices, so that the accumulators
-    // stay in registers
-    auto epi = [&](const floatx16 &v, int i, int j) {
-        const int col = n0 + wn * kBigWTN + j * 32 + (lane & 31);
-        if (col < P.N) {
-            const float bv = (!to_partial && P.bias) ? P.bias[col] : 0.0f;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = m0 + wm * kBigWTM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if (row < P.M) {
-                    float x = v[r];
-                    if (to_partial) {
-                        dst[(int64_t)row * ldd + col] = x;
-                    } else {
-                        x += bv;
-                        if (P.relu) x = fmaxf(x, 0.0f);
-                        if (P.C16) P.C16[(int64_t)row * P.ldc + col] = to_bf16(x);
-                        else dst[(int64_t)row * ldd + col] = x;
-                    }
-                }
-            }
-        }
-    };
-    static_assert(kBigFM == 4 && (kBigFN == 4 || kBigFN == 2), "epilogue unrolled for 4 x 4 or 4 x 2 blocks");
-    epi(acc[0][0], 0, 0); epi(acc[0][1], 0, 1);
-    epi(acc[1][0], 1, 0); epi(acc[1][1], 1, 1);
-    epi(acc[2][0], 2, 0); epi(acc[2][1], 2, 1);
-    epi(acc[3][0], 3, 0); epi(acc[3][1], 3, 1);
-    if constexpr (kBigFN == 4) {
-        epi(acc[0][2], 0, 2); epi(acc[0][3], 0, 3);
-        epi(acc[1][2], 1, 2); epi(acc[1][3], 1, 3);
-        epi(acc[2][2], 2, 2); epi(acc[2][3], 2, 3);
-        epi(acc[3][2], 3, 2); epi(acc[3][3], 3, 3);
-    }
-#endif
 }
 
 bool vec_ok(int layout, const GemmProblem &g, int esz) {
@@ -953,6 +945,15 @@ void launch(bool vec, bool bf16, dim3 grid, hipStream_t s, const DevArgs &a) {
 
 }  // namespace
 
+#ifndef GCN_SPLIT_MIN_TILES
+#define GCN_SPLIT_MIN_TILES 256
+#endif
+#ifndef GCN_SPLIT_TARGET
+#define GCN_SPLIT_TARGET 512
+#endif
+#ifndef GCN_SPLIT_CAP
+#define GCN_SPLIT_CAP 64
+#endif
 int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows) {
     int64_t tiles = 0, kt = 0;
     for (int i = 0; i < nprob; ++i) {
@@ -968,10 +969,10 @@ int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows) {
     // every partial.
     int64_t sp;
     if (k_is_rows) sp = 1024 / tiles;
-    else sp = tiles >= 256 ? 1 : 512 / tiles;
+    else sp = tiles >= GCN_SPLIT_MIN_TILES ? 1 : GCN_SPLIT_TARGET / tiles;
     const int64_t max_sp = kt / 8;      // keep >= 8 k-tiles per split
     if (sp > max_sp) sp = max_sp;
-    if (sp > 64) sp = 64;               // partials are written and read once each
+    if (sp > GCN_SPLIT_CAP) sp = GCN_SPLIT_CAP;   // partials are written and read once each
     if (sp < 1) sp = 1;
     return (int)sp;
 }
