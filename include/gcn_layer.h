@@ -97,6 +97,19 @@ int gcn_csr_validate_host(int32_t n_rows, int32_t n_cols, int32_t nnz,
                           const int32_t *indptr_host, const int32_t *indices_host,
                           int require_sorted);
 
+/* The same checks on a CSR held in DEVICE memory, enqueued on `stream`; for
+ * callers whose graphs never visit the host (the sampled subgraphs of
+ * gcn_induce_subgraphs).  Writes status[0] = 0 if the CSR is valid, else the
+ * kind of the first violation in row order (1 indptr[0] != 0 or
+ * indptr[n_rows] != nnz, checked before the rows; 2 indptr decreases at row
+ * status[1]; 3 an index outside [0, n_cols) in row status[1]; 4 row status[1]
+ * not strictly ascending, with require_sorted), and status[1] = that row (0 or
+ * n_rows for the endpoints).  status: device int32[2], 8-byte aligned, valid
+ * after the stream is synchronized.  Rows whose indptr bounds leave [0, nnz]
+ * are not read (a decrease or an endpoint violation is then reported).
+ * Returns GCN_EINVAL for null or misaligned arguments, before any launch. */
+int gcn_csr_validate(const gcn_csr *A, int require_sorted, int32_t *status, void *stream);
+
 /* ---------------------------------------------------------------- a0 ----
  * CSR of A^T, the transposed aggregation used by the backward propagation
  * (Alg. 1 propagates with the transpose of the bi-adjacency matrix; the

@@ -67,6 +67,7 @@ _SIGNATURES = {
     "gcn_last_error": (ctypes.c_char_p, []),
     "gcn_version": (ctypes.c_int, []),
     "gcn_csr_validate_host": (ctypes.c_int, [_I32, _I32, _I32, _P, _P, ctypes.c_int]),
+    "gcn_csr_validate": (ctypes.c_int, [_CSRP, ctypes.c_int, _P, _P]),
     "gcn_csr_transpose_workspace_bytes": (_SZ, [_I32, _I32, _I32]),
     "gcn_csr_transpose": (ctypes.c_int, [_CSRP, _P, _P, _P, _P, _SZ, _P]),
     "gcn_csr_transpose_symmetric_workspace_bytes": (_SZ, [_I32, _I32]),
@@ -209,6 +210,20 @@ def gcn_csr_validate_host(n_rows, n_cols, indptr, indices, require_sorted=True) 
     ix = np.ascontiguousarray(indices, dtype=np.int32)
     return lib().gcn_csr_validate_host(n_rows, n_cols, int(ix.size), ip.ctypes.data,
                                        ix.ctypes.data if ix.size else None, int(require_sorted))
+
+
+CSR_VIOLATION = {0: "ok", 1: "endpoints", 2: "indptr decreases", 3: "index out of range", 4: "not ascending"}
+
+
+def gcn_csr_validate(A: DeviceCSR, require_sorted=True, status: Optional[torch.Tensor] = None, stream=None):
+    """Enqueue the device-side CSR check; returns the int32[2] status tensor
+    (kind of the first violation, its row), valid after synchronization."""
+    if status is None:
+        status = torch.empty(2, dtype=torch.int32, device=A.indptr.device)
+    s = A.struct()
+    _check(lib().gcn_csr_validate(ctypes.byref(s), int(bool(require_sorted)), _ptr(status), _stream(stream)),
+           "gcn_csr_validate")
+    return status
 
 
 def gcn_csr_transpose(A: DeviceCSR, ws: Workspace, stream=None) -> DeviceCSR:

@@ -280,6 +280,15 @@ int gcn_csr_validate_host(int32_t n_rows, int32_t n_cols, int32_t nnz, const int
     return GCN_OK;
 }
 
+int gcn_csr_validate(const gcn_csr *A, int require_sorted, int32_t *status, void *stream) {
+    REQUIRE(A && status, GCN_EINVAL, "gcn_csr_validate: null argument");
+    REQUIRE(A->n_rows >= 0 && A->n_cols >= 0 && A->nnz >= 0, GCN_EINVAL, "gcn_csr_validate: negative size");
+    REQUIRE(A->indptr && (A->nnz == 0 || A->indices), GCN_EINVAL, "gcn_csr_validate: null indptr or indices");
+    REQUIRE(((uintptr_t)status & 7u) == 0, GCN_EINVAL, "gcn_csr_validate: status must be 8-byte aligned");
+    return csr_validate_device(A->n_rows, A->n_cols, A->nnz, A->indptr, A->indices, require_sorted != 0, status,
+                               as_stream(stream));
+}
+
 // -------------------------------------------------------------- transpose
 size_t gcn_csr_transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz) {
     return transpose_workspace_bytes(n_rows, n_cols, nnz);

@@ -167,6 +167,9 @@ int cvt_bf16_pad(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16
 // CSR transpose --------------------------------------------------------------
 // values of A^T for a symmetric pattern (A^T shares A's indptr / indices)
 size_t transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz);
+// device-side CSR content check; status: 8-byte aligned int32[2]
+int csr_validate_device(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
+                        const int32_t *indices, int sorted, int32_t *status, hipStream_t s);
 int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, const int32_t *indices,
                             const float *vals, float *t_vals, void *ws, size_t ws_bytes, hipStream_t s);
 size_t transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz);

@@ -396,4 +396,90 @@ int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, const
     return GCN_OK;
 }
 
+// ------------------------------------------------------- content check
+// The first violation in row order, as a 64-bit key for an integer atomicMin
+// (the minimum is unique, so the result does not depend on timing):
+//   endpoints:        key = which (0: indptr[0] != 0, 1: indptr[n_rows] != nnz)
+//   row r decreasing: key = (r + 1) << 32
+//   row r, entry q (q-th of the row) out of range / not ascending:
+//                     key = (r + 1) << 32 | (1 + 2q + (not ascending))
+namespace {
+constexpr int64_t kValidKey = 0x7fffffffffffffffLL;
+
+__global__ void validate_init_kernel(int64_t *key) { *key = kValidKey; }
+
+__global__ __launch_bounds__(256) void validate_rows_kernel(int32_t n_rows, int32_t n_cols, int32_t nnz,
+                                                            const int32_t *__restrict__ indptr,
+                                                            const int32_t *__restrict__ indices, int sorted,
+                                                            int64_t *__restrict__ key) {
+    const int lane = threadIdx.x & 63;
+    const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r == 0 && lane == 0) {
+        if (indptr[0] != 0) atomicMin((long long *)key, 0LL);
+        if (indptr[n_rows] != nnz) atomicMin((long long *)key, 1LL);
+    }
+    if (r >= n_rows) return;
+    const int32_t b = indptr[r], e = indptr[r + 1];
+    const int64_t base = (r + 1) << 32;
+    if (e < b) {
+        if (lane == 0) atomicMin((long long *)key, (long long)base);
+        return;
+    }
+    if (b < 0 || e > nnz) return;   // then an endpoint or a decrease is reported elsewhere
+    // the row's first bad entry: lanes take entries b + lane, b + lane + 64, ...
+    int64_t mine = kValidKey;
+    for (int32_t p = b + lane; p < e; p += 64) {
+        const int32_t j = indices[p];
+        int bad = -1;
+        if (j < 0 || j >= n_cols) bad = 0;
+        else if (sorted && p > b && indices[p - 1] >= j) bad = 1;
+        if (bad >= 0) {
+            mine = base | (int64_t)(1 + 2 * (int64_t)(p - b) + bad);
+            break;
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const int64_t other = __shfl_xor(mine, o);
+        mine = other < mine ? other : mine;
+    }
+    if (lane == 0 && mine != kValidKey) atomicMin((long long *)key, (long long)mine);
+}
+
+// status[0] = code (0 valid, 1 endpoints, 2 indptr decreases, 3 index out of
+// range, 4 not ascending), status[1] = row (0 or n_rows for endpoints)
+__global__ void validate_final_kernel(int32_t n_rows, int64_t *key_status) {
+    const int64_t key = *key_status;
+    int32_t code = 0, row = 0;
+    if (key != kValidKey) {
+        const int64_t r = (key >> 32) - 1;
+        const int64_t sub = key & 0xffffffffLL;
+        if (r < 0) {
+            code = 1;
+            row = sub == 0 ? 0 : n_rows;
+        } else {
+            row = (int32_t)r;
+            code = sub == 0 ? 2 : (((sub - 1) & 1) ? 4 : 3);
+        }
+    }
+    int32_t *st = (int32_t *)key_status;
+    st[0] = code;
+    st[1] = row;
+}
+}  // namespace
+
+int csr_validate_device(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
+                        const int32_t *indices, int sorted, int32_t *status, hipStream_t s) {
+    int64_t *key = (int64_t *)status;
+    hipLaunchKernelGGL(validate_init_kernel, dim3(1), dim3(1), 0, s, key);
+    GCN_LAUNCH_CHECK("validate_init_kernel");
+    const int64_t blocks = ((int64_t)n_rows + 3) / 4;
+    hipLaunchKernelGGL(validate_rows_kernel, dim3((unsigned)(blocks > 0 ? blocks : 1)), dim3(256), 0, s, n_rows,
+                       n_cols, nnz, indptr, indices, sorted, key);
+    GCN_LAUNCH_CHECK("validate_rows_kernel");
+    hipLaunchKernelGGL(validate_final_kernel, dim3(1), dim3(1), 0, s, n_rows, key);
+    GCN_LAUNCH_CHECK("validate_final_kernel");
+    return GCN_OK;
+}
+
 }  // namespace gcn

@@ -249,3 +249,14 @@ def test_model_workspace_is_the_largest_call(L):
                  L.gcn_layer_workspace_bytes(8000, 120000, 256, 128, B.GCN_AGGREGATE_FIRST, prec),
                  L.gcn_loss_workspace_bytes(8000, 256, 41, prec)]
         assert need == max(parts)
+
+
+def test_device_validate_checks_arguments_before_launch(L):
+    A = _fake_csr(10, 20)
+    st = ctypes.c_void_p(0x4000)
+    assert L.gcn_csr_validate(None, 1, st, None) == B.GCN_EINVAL
+    assert L.gcn_csr_validate(ctypes.byref(A), 1, None, None) == B.GCN_EINVAL
+    assert L.gcn_csr_validate(ctypes.byref(A), 1, ctypes.c_void_p(0x4004), None) == B.GCN_EINVAL
+    assert "aligned" in L.gcn_last_error().decode()
+    bad = B.gcn_csr(10, 10, 20, 0x1000, None, 0x3000)
+    assert L.gcn_csr_validate(ctypes.byref(bad), 1, st, None) == B.GCN_EINVAL

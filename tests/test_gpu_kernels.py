@@ -208,3 +208,72 @@ def test_bf16_conversion_bit_exact():
                                   1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8], np.float32)])
     y = B.gcn_f32_to_bf16(dev(x)).cpu().numpy().view(np.uint16)
     assert np.array_equal(y, obf16.f32_to_bf16_bits(x))
+
+
+# ----------------------------------------------------- device CSR check ----
+def first_violation(n_rows, n_cols, nnz, indptr, indices, sorted_):
+    """The documented result of gcn_csr_validate, written out row by row."""
+    if indptr[0] != 0:
+        return 1, 0
+    if indptr[n_rows] != nnz:
+        return 1, n_rows
+    for r in range(n_rows):
+        b, e = int(indptr[r]), int(indptr[r + 1])
+        if e < b:
+            return 2, r
+        if b < 0 or e > nnz:
+            continue
+        for p in range(b, e):
+            if not 0 <= indices[p] < n_cols:
+                return 3, r
+            if sorted_ and p > b and indices[p - 1] >= indices[p]:
+                return 4, r
+    return 0, 0
+
+
+@pytest.mark.parametrize("case", ["valid", "unsorted", "duplicate_unsorted_ok", "out_of_range", "negative",
+                                  "decreasing", "bad_start", "bad_end", "empty", "no_rows", "two_faults"])
+def test_device_validate_matches_row_order_semantics(case):
+    g = synth.custom(3000, "rmat", 12, [(4, 4)], seed=5).graph
+    n, ip, ix = g.n, g.indptr.copy(), g.indices.copy()
+    sorted_ = True
+    hub = int(np.argmax(np.diff(ip)))                     # the longest row: many wavefront strides
+    if case == "unsorted":
+        b = ip[hub]
+        ix[b + 100], ix[b + 101] = ix[b + 101], ix[b + 100]
+    elif case == "duplicate_unsorted_ok":
+        b = ip[hub]
+        ix[b + 1] = ix[b]
+        sorted_ = False
+    elif case == "out_of_range":
+        ix[ip[hub] + 70] = n
+    elif case == "negative":
+        ix[ip[7] if ip[8] > ip[7] else 0] = -3
+    elif case == "decreasing":
+        ip[1234] = ip[1235] + 1
+    elif case == "bad_start":
+        ip[0] = 1
+    elif case == "bad_end":
+        ip[-1] -= 1
+    elif case == "empty":
+        ip = np.zeros(n + 1, np.int32)
+        ix = np.zeros(0, np.int32)
+    elif case == "no_rows":
+        n, ip, ix = 0, np.zeros(1, np.int32), np.zeros(0, np.int32)
+    elif case == "two_faults":                             # the earlier row wins
+        ix[ip[hub] + 5] = n + 7
+        r = max(0, hub - 3)
+        while r > 0 and ip[r + 1] - ip[r] < 2:
+            r -= 1
+        ix[ip[r] + 1] = ix[ip[r]]
+    nnz = int(ix.size)
+    want = first_violation(n, max(n, 1) if case == "no_rows" else n, nnz, ip, ix, sorted_)
+    A = B.DeviceCSR(n, n, torch.from_numpy(ip).cuda(), torch.from_numpy(ix).cuda(),
+                    torch.ones(nnz, dtype=torch.float32, device="cuda"))
+    print(f"validate: {case}", flush=True)
+    st = B.gcn_csr_validate(A, require_sorted=sorted_)
+    got = tuple(int(x) for x in st.cpu())
+    assert got == want, (case, got, want)
+    if case not in ("decreasing",):   # the host check reads out of range on a decreasing indptr
+        host_ok = B.gcn_csr_validate_host(n, n, ip, ix, require_sorted=sorted_) == B.GCN_OK
+        assert host_ok == (want[0] == 0)
