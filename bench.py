@@ -66,6 +66,16 @@ def traffic_for(kernel: str, config: str):
     return e.get("bytes_per_launch")
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_reps: int = 20):
     """The CPU oracle on the same workload: whole fwd+bwd steps, repeated until
     at least `min_seconds` of CPU work have been timed (bounded by max_reps)."""
@@ -85,7 +95,7 @@ def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_r
         dt += time.perf_counter() - t0
         reps += 1
     return {"value": work["edge_features"] * reps / dt, "unit": "edge-features/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": f"{reps} full fwd+bwd step(s) of the same workload (n={wl.n}, nnz={wl.graph.nnz}), "
                       f"{dt:.1f} s in total; float64 oracle, OpenMP aggregation + BLAS dense products"}
 
@@ -251,6 +261,7 @@ def bench_sampler(args, B, torch):
             tot += v.size
             reps += 1
         out["cpu_baseline"] = {"value": round(tot / dt, 1), "unit": "sampled vertices/s", "cores": 1,
+                               "cpu_model": cpu_model(),
                                "kind": "oracle",
                                "sample": f"{reps} runs of the same sampler on the same graph, {dt:.1f} s; "
                                          f"sequential C oracle (one thread)"}
@@ -344,7 +355,7 @@ def bench_stream(args, torch):
             ef_c += step_work(wl.n, wl.graph.nnz, dims, orders, need, spec.classes)["edge_features"]
             reps += 1
         out["cpu_baseline"] = {"value": round(ef_c / dt, 1), "unit": "edge-features/s",
-                               "cores": oracle.num_threads(), "kind": "oracle",
+                               "cores": oracle.num_threads(), "kind": "oracle", "cpu_model": cpu_model(),
                                "sample": f"{reps} subgraph(s) of the stream (the last ones), {dt:.1f} s; the "
                                          f"whole stream would take about {dt / reps * S:.0f} s (extrapolated)"}
     print(json.dumps(out), flush=True)
@@ -462,6 +473,7 @@ def bench_train(args, B, torch):
             dt += time.perf_counter() - t1
             reps += 1
         out["cpu_baseline"] = {"value": round(reps / dt, 4), "unit": "iterations/s", "cores": oracle.num_threads(),
+                               "cpu_model": cpu_model(),
                                "kind": "oracle",
                                "sample": f"{reps} iterations of the oracle pipeline (sampler, induced subgraph, "
                                          f"float64 fwd/bwd, ADAM) on the same graph, {dt:.1f} s"}
@@ -540,13 +552,17 @@ def main():
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     host = 0.0
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     start.record(stream)
-    for _ in range(args.steps):
+    for i in range(args.steps):
         th = time.perf_counter()
         runner.step()
         host += time.perf_counter() - th
+        marks[i].record(stream)   # per-step times (no synchronization in the loop)
     stop.record(stream)
     torch.cuda.synchronize()
+    step_ms = sorted([start.elapsed_time(marks[0])] +
+                     [marks[i - 1].elapsed_time(marks[i]) for i in range(1, args.steps)])
     if not args.no_profile:
         B.gcn_profile_reset()
         B.gcn_profile_enable(True)
@@ -588,9 +604,17 @@ def main():
         roof["avg_launch_ms"] = round(per_launch_ms, 4)
         roof["launches_per_step"] = launches / args.steps
         roof["traffic"] = traffic_for(name, config_name)
-        spm = prof.get("spmm")
-        if spm and spm[1]:
-            kernels["spmm"]["hbm_frac_gather_model"] = round(spm[3] / (spm[0] / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
+        for cls, esz in (("spmm", 4), ("spmm_bf16", 2)):
+            spm = prof.get(cls)
+            if not (spm and spm[1]):
+                continue
+            t_s = spm[0] / 1e3
+            kernels[cls]["hbm_frac_gather_model"] = round(spm[3] / t_s / 1e9 / PEAK_HBM_GBS, 4)
+            # compulsory model: every feature row read once, plus CSR and output
+            passes = spm[1] / args.steps
+            k_sum = work["edge_features"] / max(wl.graph.nnz, 1)
+            comp = args.steps * (wl.n * k_sum * (esz + 4) + passes * (8.0 * wl.graph.nnz + 4.0 * (wl.n + 1)))
+            kernels[cls]["hbm_frac_compulsory_model"] = round(comp / t_s / 1e9 / PEAK_HBM_GBS, 4)
 
     out = {
         "metric": METRIC, "value": round(ef_per_s, 1), "unit": "edge-features/s",
@@ -604,6 +628,7 @@ def main():
                               for o in runner.orders],
                    "head": spec.head, "classes": spec.classes, "parallelism": "single GPU"},
         "gflops": round(gflops, 1),
+        "step_ms_min_median": [round(step_ms[0], 4), round(step_ms[len(step_ms) // 2], 4)],
         "host_issue_ms_per_step": round(host * 1e3 / args.steps, 4),
         "edge_features_per_step": work["edge_features"], "gemm_gflop_per_step": work["gemm_flops"] / 1e9,
         "roofline": roof, "kernels": kernels,

@@ -228,7 +228,21 @@ __global__ __launch_bounds__(kTB) void sym_rows_kernel(int32_t n, const int32_t 
     const int32_t b = indptr[i], e = indptr[i + 1];
     const uint32_t first = e > b ? __float_as_uint(vals[b]) : 0u;
     bool same = true;
-    for (int32_t p = b + lane; p < e; p += 64) {
+    // eight loads in flight per lane: a hub row of 14,000 entries is one
+    // wavefront's serial walk
+    constexpr int U = 8;
+    int32_t p = b + lane;
+    for (; p + 64 * (U - 1) < e; p += 64 * U) {
+        uint32_t v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = __float_as_uint(vals[p + 64 * u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            rowid[p + 64 * u] = (int32_t)i;
+            same = same && (v[u] == first);
+        }
+    }
+    for (; p < e; p += 64) {
         rowid[p] = (int32_t)i;
         same = same && (__float_as_uint(vals[p]) == first);
     }
