@@ -287,7 +287,7 @@ def bench_stream(args, torch):
     from paper_1810_11899_amd import synth
     from paper_1810_11899_amd.runner import StepRunner
     S = args.stream_subgraphs
-    spec = synth.CONFIGS[4]
+    spec = synth.WORKLOADS[4]
     workers = max(1, min(16, len(os.sched_getaffinity(0))))
     # the worker processes are forked before this process first touches the
     # GPU; they only draw subgraphs with numpy
@@ -505,7 +505,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+        print(f"bench.py measures one GPU only: the library has no multi-GPU path "
               f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
         sys.exit(2)
 
@@ -536,7 +536,7 @@ def main():
         return
     prec = B.PREC[args.prec]
     wl = synth.config(args.config)
-    spec = synth.CONFIGS[args.config]
+    spec = synth.WORKLOADS[args.config]
     runner = StepRunner(wl, prec=prec)
     work = runner.work()
     stream = torch.cuda.current_stream()

@@ -50,7 +50,7 @@ typedef enum {
     GCN_ESHAPE = -2,        /* inconsistent sizes or leading dimensions           */
     GCN_EWORKSPACE = -3,    /* workspace or saved buffer too small / misaligned   */
     GCN_EHIP = -4,          /* a HIP runtime call or kernel launch failed         */
-    GCN_EUNSUPPORTED = -5   /* valid request that this build does not implement   */
+    GCN_EUNSUPPORTED = -5   /* valid request that the library does not implement */
 } gcn_status;
 
 /* Arithmetic of the dense transforms and the gather.

@@ -14,7 +14,7 @@ products (the paper uses a BLAS ``dgemm``, Sec. V-A / VI-C-4) and numpy's stable
 sort for the transpose; the sparse aggregation is a plain C loop
 (``gcnref_aggregate.c``).
 
-Readings of points the paper leaves open (all also listed in the design doc):
+Readings of points the paper leaves open:
   * concat order self-first: ``[H W_self || A H W_neigh]``;
   * no self-loops are added to A (the self term is W_self's);
   * A is row-normalised (the mean of Sec. II): ``A[i, j] = 1/deg(i)``;

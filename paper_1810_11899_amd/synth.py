@@ -269,7 +269,7 @@ def build(spec: Spec, s: int = 0, cfg_key: int = 99, n: Optional[int] = None) ->
 # The five workloads.  Attribute widths / class counts follow Table I
 # (PPI 50, Reddit 602/41 single-label, Yelp 300/100 multi-label, Amazon 200),
 # the hidden width 512 follows Sec. VI-C.
-CONFIGS = {
+WORKLOADS = {
     0: Spec("er2000_d15_50x64_givendY", 2000, "er", 15, [(50, 64)], None),
     1: Spec("rmat8000_d20_602-128-128_ce41", 8000, "rmat", 20, [(602, 128), (256, 128)], "ce", 41),
     2: Spec("rmat16000_d30_300-256x3_bce100", 16000, "rmat", 30,
@@ -281,7 +281,7 @@ CONFIGS = {
 
 
 def config(cfg: int, s: int = 0, n: Optional[int] = None) -> Workload:
-    return build(CONFIGS[cfg], s=s, cfg_key=cfg, n=n)
+    return build(WORKLOADS[cfg], s=s, cfg_key=cfg, n=n)
 
 
 def custom(n: int, graph: str, d: int, layers, head=None, classes=0, seed: int = 0) -> Workload:

@@ -37,7 +37,7 @@ def test_rmat65536_two_layer_f32_step():
 def test_epoch_stream_subgraphs_reuse_buffers():
     """Several subgraphs of the stream through one runner (buffers sized for
     the largest nnz, reused); each checked against the oracle."""
-    spec = synth.CONFIGS[4]
+    spec = synth.WORKLOADS[4]
     subs = [0, 1, 199]
     wls = [synth.config(4, s=s) for s in subs]
     cap = max(w.graph.nnz for w in wls)

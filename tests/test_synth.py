@@ -27,7 +27,7 @@ def _check_csr(g: synth.Graph, symmetric=True):
 @pytest.mark.parametrize("cfg", [0, 1])
 def test_config_graph_well_formed(cfg):
     wl = synth.config(cfg)
-    spec = synth.CONFIGS[cfg]
+    spec = synth.WORKLOADS[cfg]
     _check_csr(wl.graph)
     assert wl.graph.nnz == spec.n * spec.d
     assert wl.H.shape == (spec.n, spec.layers[0][0]) and wl.H.dtype == np.float32
