@@ -409,8 +409,8 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         uint16_t *AGG16T = af ? (uint16_t *)((char *)saved + 3 * one) : nullptr;
         uint16_t *WsT = ar.take<uint16_t>((size_t)f_in * h);
         uint16_t *WnT = ar.take<uint16_t>((size_t)f_in * h);
-        if ((rc = cvt_bf16(n, f_in, H, ldh, H16, f_in, s))) return rc;
-        if ((rc = transpose_bf16(n, f_in, H16, 1, f_in, H16T, n, s))) return rc;
+        // H16T and H16 in one pass over H
+        if ((rc = transpose_bf16_copy(n, f_in, H, 0, ldh, H16T, n, H16, f_in, s))) return rc;
         if ((rc = transpose_bf16(f_in, h, W_self, 0, h, WsT, f_in, s))) return rc;
         if ((rc = transpose_bf16(f_in, h, W_neigh, 0, h, WnT, f_in, s))) return rc;
         GemmProblem g[2] = {};
@@ -693,8 +693,7 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     g.bias = b_pred;
     if (bf) {
         // NT form: B = W_pred^T (C x f)
-        if ((rc = cvt_bf16(n, f, HL, ldhl, HL16, f, s))) return rc;
-        if ((rc = transpose_bf16(n, f, HL16, 1, f, HL16T, n, s))) return rc;
+        if ((rc = transpose_bf16_copy(n, f, HL, 0, ldhl, HL16T, n, HL16, f, s))) return rc;
         if ((rc = cvt_bf16_pad(f, C, W_pred, C, Wp16, Cp, Cp, s))) return rc;
         if ((rc = transpose_bf16(f, C, Wp16, 1, Cp, Wp16T, f, s))) return rc;
         g.seg[0] = GemmSeg{HL16, f, Wp16T, f, f};

@@ -157,6 +157,9 @@ int fill_zero(float *x, int64_t count, hipStream_t s);
 // float32 or (src_is_bf16) bfloat16 bits
 int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds, uint16_t *dst,
                    int64_t ldd, hipStream_t s);
+// the same, and (copy non-null) the untransposed bfloat16 rows into copy (ldc)
+int transpose_bf16_copy(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds, uint16_t *dst,
+                        int64_t ldd, uint16_t *copy, int64_t ldc, hipStream_t s);
 // float32 -> bfloat16 bits (RNE), 2-D with leading dimensions
 int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
              hipStream_t s);

@@ -286,7 +286,7 @@ __global__ __launch_bounds__(256) void cvt_bf16_kernel(int64_t rows, int64_t col
 template <typename TIn>
 __global__ __launch_bounds__(256) void transpose_bf16_kernel(int64_t rows, int64_t cols, const TIn *__restrict__ src,
                                                              int64_t lds_, uint16_t *__restrict__ dst, int64_t ldd,
-                                                             int vec) {
+                                                             uint16_t *__restrict__ copy, int64_t ldc, int vec) {
     __shared__ uint16_t tile[64][64 + 4];
     const int64_t r0 = (int64_t)blockIdx.y * 64, c0 = (int64_t)blockIdx.x * 64;
     const int tq = threadIdx.x & 15, tr = threadIdx.x >> 4;  // 16 quads x 16 rows
@@ -317,6 +317,16 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(int64_t rows, int64
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) tile[rr][tq * 4 + e] = v[e];
+        if (copy && r < rows) {   // the untransposed bfloat16 copy, from the same registers
+            uint16_t *o = copy + r * ldc + c;
+            if (vec && c + 4 <= cols) {
+                *(uint2 *)o = make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | ((uint32_t)v[3] << 16));
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (c + e < cols) o[e] = v[e];
+            }
+        }
     }
     __syncthreads();
 #pragma unroll
@@ -465,22 +475,29 @@ int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void
     return GCN_OK;
 }
 
-int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds_, uint16_t *dst,
-                   int64_t ldd, hipStream_t s) {
+int transpose_bf16_copy(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds_, uint16_t *dst,
+                        int64_t ldd, uint16_t *copy, int64_t ldc, hipStream_t s) {
     if (rows <= 0 || cols <= 0) return GCN_OK;
-    ProfScope ps(K_TRANSPOSE_BF16, s, 0.0, (double)rows * cols * (src_is_bf16 ? 4.0 : 6.0));
+    ProfScope ps(K_TRANSPOSE_BF16, s, 0.0,
+                 (double)rows * cols * ((src_is_bf16 ? 4.0 : 6.0) + (copy ? 2.0 : 0.0)));
     dim3 g((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64));
     const int esz = src_is_bf16 ? 2 : 4;
-    const int vec = (lds_ % 4 == 0 && ldd % 4 == 0 && ((uintptr_t)src % (4 * esz)) == 0 && ((uintptr_t)dst % 8) == 0)
+    const int vec = (lds_ % 4 == 0 && ldd % 4 == 0 && ((uintptr_t)src % (4 * esz)) == 0 && ((uintptr_t)dst % 8) == 0 &&
+                     (!copy || (ldc % 4 == 0 && ((uintptr_t)copy % 8) == 0)))
                         ? 1 : 0;
     if (src_is_bf16)
         hipLaunchKernelGGL(transpose_bf16_kernel<uint16_t>, g, dim3(256), 0, s, rows, cols, (const uint16_t *)src,
-                           lds_, dst, ldd, vec);
+                           lds_, dst, ldd, copy, ldc, vec);
     else
         hipLaunchKernelGGL(transpose_bf16_kernel<float>, g, dim3(256), 0, s, rows, cols, (const float *)src, lds_,
-                           dst, ldd, vec);
+                           dst, ldd, copy, ldc, vec);
     GCN_LAUNCH_CHECK("transpose_bf16_kernel");
     return GCN_OK;
+}
+
+int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds_, uint16_t *dst,
+                   int64_t ldd, hipStream_t s) {
+    return transpose_bf16_copy(rows, cols, src, src_is_bf16, lds_, dst, ldd, nullptr, 0, s);
 }
 
 int cvt_bf16_pad(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
