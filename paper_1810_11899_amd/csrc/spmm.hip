@@ -34,6 +34,15 @@ constexpr int kMaxIpw = 256;   // merge items per wavefront, at most
 #ifndef GCN_SPMM_U
 #define GCN_SPMM_U 4
 #endif
+// wavefronts per SIMD the register allocation must allow: the gathers are
+// latency-bound, so the bytes in flight per CU (wavefronts x loads each) set
+// the rate; the sliced kernel fits 8 without spilling (64 VGPRs)
+#ifndef GCN_SPMM_MAIN_WPE
+#define GCN_SPMM_MAIN_WPE 1
+#endif
+#ifndef GCN_SPMM_SLICED_WPE
+#define GCN_SPMM_SLICED_WPE 8
+#endif
 
 
 // Smallest r in [0, n_rows] whose row-end item sits at merge position >= d,
@@ -200,7 +209,8 @@ __device__ __forceinline__ void store_raw(float *__restrict__ out, const float (
 
 // One wavefront = `ipw` merge items x one column slice of width 64*VEC*CT.
 template <int VEC, int CT, bool BF16>
-__global__ __launch_bounds__(256) void spmm_main(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_MAIN_WPE)))
+void spmm_main(
     int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
     const float *__restrict__ vals, const void *__restrict__ Xv, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
@@ -329,7 +339,8 @@ __device__ __forceinline__ bool slice_of_block(const SliceMap &m, int64_t w, int
     return chunk < m.chunks;
 }
 
-__global__ __launch_bounds__(256) void spmm_sliced(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_SLICED_WPE)))
+void spmm_sliced(
     int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
     const float *__restrict__ vals, const float *__restrict__ X, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
