@@ -148,6 +148,27 @@ struct TileLoader {
         }
     }
 
+    // Fast path of the vector loader, for k-tiles wholly inside a K-segment:
+    // per-thread element offsets of the vectors (at k = 0), computed once per
+    // segment, with rows / column chunks past the extent clamped to the last
+    // valid ones (their products land in outputs the epilogue drops).  A
+    // k-tile is then one add and one load per vector, with no bounds branches.
+    int64_t off[kPer];
+    __device__ __forceinline__ void prepare(int64_t ld, int x0, int xlim) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            int x, k;
+            coords(i, x, k);
+            if (KMAJOR) off[i] = (int64_t)k * ld + min(x0 + x, xlim - E);
+            else off[i] = (int64_t)min(x0 + x, xlim - 1) * ld + k;
+        }
+    }
+    // kofs: k0 (operand contiguous along k) or k0 * ld (contiguous along x)
+    __device__ __forceinline__ void load_fast(const T *__restrict__ ptr, int64_t kofs) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) reg[i] = *(const V *)(ptr + off[i] + kofs);
+    }
+
     __device__ __forceinline__ void store(T (*lds)[XT + PAD]) const {
 #pragma unroll
         for (int i = 0; i < kPer; ++i) {
@@ -230,13 +251,27 @@ void gemm_kernel(DevArgs args) {
     const int64_t lda0 = P.s.lda[0], lda1 = P.s.lda[1], ldb0 = P.s.ldb[0], ldb1 = P.s.ldb[1];
     const int K0 = P.s.K[0], K1 = P.s.K[1], kt0 = P.s.kt[0];
     const int Mp = P.M, Np = P.N;
+    // the clamped fast loads need M (TN) and N (NN, TN) of at least one vector
+    const bool fast = VEC && (!A_KMAJOR || Mp >= 4) && (!B_KMAJOR || Np >= 4);
+    int ready = -1;   // the K-segment whose offsets are prepared
     auto load = [&](int kt) {
-        if (kt < kt0) {
-            la.load(A0, lda0, m0, Mp, kt * BK, K0);
-            lb.load(B0, ldb0, n0, Np, kt * BK, K0);
+        const int sg = kt < kt0 ? 0 : 1;
+        const int kk = (sg ? kt - kt0 : kt) * BK;
+        const T *A = sg ? A1 : A0;
+        const T *Bm = sg ? B1 : B0;
+        const int64_t lda = sg ? lda1 : lda0, ldb = sg ? ldb1 : ldb0;
+        const int K = sg ? K1 : K0;
+        if (fast && kk + BK <= K) {
+            if (ready != sg) {
+                la.prepare(lda, m0, Mp);
+                lb.prepare(ldb, n0, Np);
+                ready = sg;
+            }
+            la.load_fast(A, A_KMAJOR ? (int64_t)kk * lda : (int64_t)kk);
+            lb.load_fast(Bm, B_KMAJOR ? (int64_t)kk * ldb : (int64_t)kk);
         } else {
-            la.load(A1, lda1, m0, Mp, (kt - kt0) * BK, K1);
-            lb.load(B1, ldb1, n0, Np, (kt - kt0) * BK, K1);
+            la.load(A, lda, m0, Mp, kk, K);
+            lb.load(Bm, ldb, n0, Np, kk, K);
         }
     };
 
