@@ -76,9 +76,29 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_reps: int = 20):
+def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_reps: int = 20,
+                 threads: int = 0):
     """The CPU oracle on the same workload: whole fwd+bwd steps, repeated until
-    at least `min_seconds` of CPU work have been timed (bounded by max_reps)."""
+    at least `min_seconds` of CPU work have been timed (bounded by max_reps).
+    threads > 0: that many threads for the oracle's aggregation and BLAS (a
+    serial run is the analogue of the paper's single-core baseline)."""
+    import contextlib
+    import oracle
+    limit = contextlib.nullcontext()
+    prev = oracle.num_threads()
+    if threads > 0:
+        from threadpoolctl import threadpool_limits
+        limit = threadpool_limits(limits=threads)
+        oracle.set_num_threads(threads)
+    try:
+        with limit:
+            return _cpu_baseline(cfg, synth, step_work, B, min_seconds, max_reps)
+    finally:
+        if threads > 0:
+            oracle.set_num_threads(prev)
+
+
+def _cpu_baseline(cfg, synth, step_work, B, min_seconds, max_reps):
     import oracle
     wl = synth.config(cfg)
     L = len(wl.layers)
@@ -642,6 +662,9 @@ def main():
             roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.config, synth, step_work, B, min_seconds=args.cpu_seconds)
+        if args.config in (0, 1, 2):   # the serial oracle as well (small workloads only)
+            out["cpu_baseline_serial"] = cpu_baseline(args.config, synth, step_work, B,
+                                                      min_seconds=args.cpu_seconds, max_reps=5, threads=1)
     print(json.dumps(out), flush=True)
 
 

@@ -70,12 +70,19 @@ def _load():
         lib.gcnref_aggregate.argtypes = [i64, i64, p, p, p, p, i64, p, i64]
         lib.gcnref_aggregate.restype = None
         lib.gcnref_num_threads.restype = ctypes.c_int
+        lib.gcnref_set_num_threads.argtypes = [ctypes.c_int]
+        lib.gcnref_set_num_threads.restype = None
         _lib = lib
     return _lib
 
 
 def num_threads() -> int:
     return int(_load().gcnref_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the C aggregation (for timing a serial run)."""
+    _load().gcnref_set_num_threads(int(n))
 
 
 U32 = 2.0 ** -24      # unit roundoff of float32

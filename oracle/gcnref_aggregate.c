@@ -40,6 +40,17 @@ void gcnref_aggregate(int64_t n_rows, int64_t k,
     }
 }
 
+/* Threads for the following aggregations (timing of a serial run); n < 1
+ * leaves the setting alone.  Not part of the arithmetic. */
+void gcnref_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 int gcnref_num_threads(void)
 {
     int t = 1;
