@@ -188,12 +188,12 @@ def test_forced_orders_agree_with_oracle(order):
     compare_step(r.results(), oracle.step(wl, first_layer_dH=True, envelope=True))
 
 
-@pytest.mark.parametrize("case", ["cfg1-f32", "cfg1-bf16", "dY-f32", "bce-transform-first"])
+@pytest.mark.parametrize("case", ["cfg1-f32", "cfg1-bf16", "cfg2-bf16", "dY-f32", "bce-transform-first"])
 def test_model_step_matches_separate_calls(case):
     """gcn_model_step enqueues the same kernels as the separate calls, in the
     same order: results must be identical bit for bit."""
-    if case.startswith("cfg1"):
-        wl = synth.config(1)
+    if case.startswith("cfg"):
+        wl = synth.config(int(case[3]))
         r = StepRunner(wl, prec=B.GCN_BF16 if case.endswith("bf16") else B.GCN_F32)
     elif case == "dY-f32":
         wl = synth.custom(2500, "rmat", 10, [(64, 32), (64, 48)], head=None, seed=4)
@@ -216,3 +216,19 @@ def test_model_step_matches_separate_calls(case):
         assert a["loss"] == b["loss"]
         for key in ("dW_pred", "db_pred", "dHL"):
             assert np.array_equal(a[key].view(np.uint32), b[key].view(np.uint32)), key
+
+
+@pytest.mark.parametrize("graph", ["empty", "star"])
+def test_model_step_degenerate_graphs_match_oracle(graph):
+    """The whole step through gcn_model_step on a graph without edges (every
+    aggregation is zero, so the neighbour halves are ReLU(bias)) and on a star
+    (one hub row over every vertex)."""
+    import dataclasses
+    wl = synth.custom(777, "er", 6, [(48, 32), (64, 40)], head="ce", classes=9, seed=3)
+    g = synth.empty_graph(wl.n) if graph == "empty" else synth.star_graph(wl.n)
+    wl = dataclasses.replace(wl, graph=g)
+    r = StepRunner(wl, first_layer_dH=True)
+    print(f"model step on {graph} graph: n={wl.n} nnz={g.nnz}", flush=True)
+    r.step()
+    torch.cuda.synchronize()
+    compare_step(r.results(), oracle.step(wl, first_layer_dH=True, envelope=True))
