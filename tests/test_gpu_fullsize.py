@@ -38,7 +38,7 @@ def test_epoch_stream_subgraphs_reuse_buffers():
     """Several subgraphs of the stream through one runner (buffers sized for
     the largest nnz, reused); each checked against the oracle."""
     spec = synth.WORKLOADS[4]
-    subs = [0, 1, 199]
+    subs = [0, 1, 2, 50, 100, 150, 198, 199]
     wls = [synth.config(4, s=s) for s in subs]
     cap = max(w.graph.nnz for w in wls)
     r = StepRunner(wls[0], nnz_capacity=cap)
@@ -55,7 +55,7 @@ def _f32(a):
     return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
 
 
-@pytest.mark.parametrize("cfg, prec", [(2, 0), (3, 0), (4, 0), (3, 1)])
+@pytest.mark.parametrize("cfg, prec", [(2, 0), (3, 0), (4, 0), (2, 1), (3, 1)])
 def test_layerwise_strict(cfg, prec):
     """Every layer of the full-size workload on the oracle's own (float32-
     rounded) layer inputs: forward Y, the loss head and every gradient within
