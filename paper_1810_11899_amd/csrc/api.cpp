@@ -143,13 +143,32 @@ struct LayerPlan {
     bool need_G;        // backward forms G = A^T dZ_n
     bool bf16;
     size_t fwd_T, fwd_W16, fwd_spmm, fwd_gemm;
-    size_t bwd_P, bwd_PT, bwd_D, bwd_DT, bwd_T2, bwd_W16, bwd_relu, bwd_spmm, bwd_gemm;
+    size_t bwd_P, bwd_PT, bwd_D, bwd_DT, bwd_T2, bwd_W16, bwd_relu, bwd_spmm, bwd_gemm, bwd_cp;
     size_t fwd_total, bwd_total, total;
 };
 
 bool bwd_uses_G(int order, bool dH, int32_t f_in, int32_t h) {
     return order == GCN_TRANSFORM_FIRST || (dH && h <= f_in);
 }
+
+// The float32 input-gradient product of a layer whose backward forms G:
+// dH = [dZ_s || G] [W_self || W_neigh]^T, one product with K = 2h.  When it
+// runs unsplit, a model step has its epilogue multiply dH by the ReLU
+// derivative of the layer below, [H > 0] (H = that layer's output Y), and sum
+// the columns of the result: the layer below then receives its dZ and bias
+// gradient ready (Sec. III-A's backward pass, with the mask of the layer
+// below applied where its input gradient is written).
+bool dH_mask_fusable(int32_t n, int32_t f_in, int32_t h, int order, int prec) {
+    if (prec != GCN_F32 || n <= 0 || !bwd_uses_G(order, true, f_in, h)) return false;
+    GemmProblem d{};
+    d.M = n;
+    d.N = f_in;
+    d.seg[0].K = h;
+    d.seg[1].K = h;
+    return gemm_pick_split(1, &d, false) == 1;
+}
+
+size_t colpart_bytes(int32_t n, int32_t N) { return align256((size_t)gemm_colpart_rows(n) * N * sizeof(float)); }
 
 GemmProblem dw_problem(int32_t f_in, int32_t h, int32_t n) {
     GemmProblem g{};
@@ -216,8 +235,9 @@ LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order,
         const int nd = p.need_G ? 1 : 2;
         p.bwd_gemm = std::max(p.bwd_gemm, gemm_workspace_bytes(nd, d, gemm_pick_split(nd, d, false)));
     }
+    p.bwd_cp = (dH && dH_mask_fusable(n, f_in, h, order, prec)) ? colpart_bytes(n, f_in) : 0;
     p.bwd_total = p.bwd_P + p.bwd_PT + p.bwd_D + p.bwd_DT + p.bwd_T2 + p.bwd_W16 + p.bwd_relu + p.bwd_spmm +
-                  p.bwd_gemm + 2816;
+                  p.bwd_gemm + p.bwd_cp + 3072;
     p.total = std::max(p.fwd_total, p.bwd_total);
     return p;
 }
@@ -484,7 +504,11 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
                      int32_t ldh, const float *W_self, const float *W_neigh, int32_t h, const float *Y, int32_t ldy,
                      const void *saved, size_t saved_bytes_, const float *dY, int32_t lddy, float *dH,
                      int32_t lddh, float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec,
-                     void *ws, size_t ws_bytes, void *stream) {
+                     void *ws, size_t ws_bytes, void *stream, bool dz_ready = false,
+                     float *below_dbias = nullptr) {
+    // dz_ready: dY already holds dZ = dY * [Y > 0] and dbias is already
+    // written (by the producer of dY).  below_dbias: write dH multiplied by
+    // [H > 0] and its column sums to below_dbias (dH_mask_fusable only).
     int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_bwd");
     if (rc) return rc;
     rc = check_csr(AT, "gcn_layer_bwd (transpose)");
@@ -502,6 +526,9 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
             "gcn_layer_bwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
     const bool want_dH = dH != nullptr;
+    REQUIRE(!dz_ready || (prec == GCN_F32 && n > 0), GCN_EINVAL, "gcn_layer_bwd: masked dY needs float32, n > 0");
+    REQUIRE(!below_dbias || (want_dH && dH_mask_fusable(n, f_in, h, order, prec)), GCN_EINVAL,
+            "gcn_layer_bwd: the masked input gradient needs an unsplit float32 product");
     const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, want_dH, prec);
     REQUIRE(ws && ws_bytes >= pl.bwd_total, GCN_EWORKSPACE, "gcn_layer_bwd: workspace %zu < %zu bytes",
             ws_bytes, pl.bwd_total);
@@ -519,29 +546,39 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     void *rw = ar.take<char>(pl.bwd_relu);
     void *sw = pl.bwd_spmm ? ar.take<char>(pl.bwd_spmm) : nullptr;
     void *gw = pl.bwd_gemm ? ar.take<char>(pl.bwd_gemm) : nullptr;
+    float *cp = pl.bwd_cp ? ar.take<float>(pl.bwd_cp / sizeof(float)) : nullptr;
     const int64_t ldP = 2 * (int64_t)h;
     char *Pn = P + (size_t)h * E;                              // second half of P
-    char *Zn = pl.need_G ? D : Pn;                             // where dZ_n goes
-    const int64_t ldZn = pl.need_G ? h : ldP;
+    // where dZ_s, dZ_n and G = A^T dZ_n live: in the workspace, or, with dZ
+    // given, dZ in dY and G at the start of P
+    const char *Zs = dz_ready ? (const char *)dY : P;
+    const int64_t ldZs = dz_ready ? lddy : ldP;
+    char *ZnW = pl.need_G ? D : Pn;
+    const char *Zn = dz_ready ? (const char *)(dY + h) : ZnW;
+    const int64_t ldZn = dz_ready ? lddy : (pl.need_G ? h : ldP);
+    char *Gp = dz_ready ? P : Pn;
+    const int64_t ldG = dz_ready ? h : ldP;
 
     // a6: dZ = dY * [Y > 0] and dbias
-    if (bf)
-        rc = relu_bwd(n, h, dY, lddy, Y, ldy, nullptr, ldP, nullptr, ldZn, (uint16_t *)P, (uint16_t *)Zn, dbias,
-                      rw, pl.bwd_relu, s);
-    else
-        rc = relu_bwd(n, h, dY, lddy, Y, ldy, (float *)P, ldP, (float *)Zn, ldZn, nullptr, nullptr, dbias, rw,
-                      pl.bwd_relu, s);
-    if (rc) return rc;
+    if (!dz_ready) {
+        if (bf)
+            rc = relu_bwd(n, h, dY, lddy, Y, ldy, nullptr, ldP, nullptr, ldZn, (uint16_t *)P, (uint16_t *)ZnW,
+                          dbias, rw, pl.bwd_relu, s);
+        else
+            rc = relu_bwd(n, h, dY, lddy, Y, ldy, (float *)P, ldP, (float *)ZnW, ldZn, nullptr, nullptr, dbias, rw,
+                          pl.bwd_relu, s);
+        if (rc) return rc;
+    }
     if (n == 0) {
         rc = fill_zero(dW_self, (int64_t)f_in * h, s);
         return rc ? rc : fill_zero(dW_neigh, (int64_t)f_in * h, s);
     }
     // G = A^T dZ_n into the second half of P
     if (pl.need_G) {
-        rc = bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)D, h, h, Pn,
-                            ldP, EPI_STORE_BF16, nullptr, sw, pl.bwd_spmm, s)
-                : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)D, h, h, Pn,
-                           ldP, EPI_STORE, nullptr, sw, pl.bwd_spmm, s);
+        rc = bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)Zn, h, ldZn,
+                            Gp, ldG, EPI_STORE_BF16, nullptr, sw, pl.bwd_spmm, s)
+                : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)Zn, h, ldZn, Gp,
+                           ldG, EPI_STORE, nullptr, sw, pl.bwd_spmm, s);
         if (rc) return rc;
     }
     // a7: weight gradients, K = n, split-K
@@ -561,11 +598,11 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
         if (!af) g[1].seg[0] = GemmSeg{H16T, n, PT + (size_t)h * n, n, n};
         else g[1].seg[0] = GemmSeg{AGG16T, n, DT ? DT : PT + (size_t)h * n, n, n};
     } else {
-        g[0].seg[0] = GemmSeg{H, ldh, P, ldP, n};
+        g[0].seg[0] = GemmSeg{H, ldh, Zs, ldZs, n};
         if (!af)
-            g[1].seg[0] = GemmSeg{H, ldh, Pn, ldP, n};                 // H^T (A^T dZ_n)
+            g[1].seg[0] = GemmSeg{H, ldh, Gp, ldG, n};                 // H^T (A^T dZ_n)
         else
-            g[1].seg[0] = pl.need_G ? GemmSeg{saved, f_in, D, h, n} : GemmSeg{saved, f_in, Pn, ldP, n};
+            g[1].seg[0] = GemmSeg{saved, f_in, Zn, ldZn, n};           // AGG^T dZ_n
     }
     g[0].C = dW_self;
     g[0].ldc = h;
@@ -586,19 +623,25 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
         GemmProblem d{};
         d.M = n;
         d.N = f_in;
-        d.seg[0] = GemmSeg{P, ldP, Wsop, h, h};
-        d.seg[1] = GemmSeg{Pn, ldP, Wnop, h, h};
+        d.seg[0] = GemmSeg{Zs, ldZs, Wsop, h, h};
+        d.seg[1] = GemmSeg{Gp, ldG, Wnop, h, h};
         d.C = dH;
         d.ldc = lddh;
-        return gemm(L_NT, 1, &d, bf, gemm_pick_split(1, &d, false), gw, pl.bwd_gemm, s);
+        if (below_dbias) {  // dZ of the layer below, and its bias gradient
+            d.mask = H;
+            d.ldm = ldh;
+            d.colpart = cp;
+        }
+        if ((rc = gemm(L_NT, 1, &d, bf, gemm_pick_split(1, &d, false), gw, pl.bwd_gemm, s))) return rc;
+        return below_dbias ? colsum_reduce_rows(gemm_colpart_rows(n), f_in, cp, below_dbias, s) : GCN_OK;
     }
     GemmProblem d[2] = {};
     d[0].M = d[1].M = n;
     d[0].N = d[1].N = f_in;
-    d[0].seg[0] = GemmSeg{P, ldP, Wsop, h, h};
+    d[0].seg[0] = GemmSeg{Zs, ldZs, Wsop, h, h};
     d[0].C = dH;
     d[0].ldc = lddh;
-    d[1].seg[0] = GemmSeg{Pn, ldP, Wnop, h, h};
+    d[1].seg[0] = GemmSeg{Zn, ldZn, Wnop, h, h};
     d[1].ldc = f_in;
     if (bf) d[1].C16 = (uint16_t *)T2;
     else d[1].C = (float *)T2;
@@ -612,7 +655,7 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
 // ------------------------------------------------------------------ loss
 namespace {
 struct LossPlan {
-    size_t X, rows, HL16, HL16T, Wp16, Wp16T, G16, G16T, gemm, colsum, red, total;
+    size_t X, rows, HL16, HL16T, Wp16, Wp16T, G16, G16T, gemm, colsum, red, cp, total;
     int split;
 };
 // bfloat16 class dimension padded with zero columns to a multiple of 32, so
@@ -636,8 +679,9 @@ LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
     p.gemm = gemm_workspace_bytes(1, &g, p.split);
     p.colsum = colsum_workspace_bytes(n, C);
     p.red = loss_reduce_workspace_bytes(n);
+    p.cp = prec == GCN_F32 ? colpart_bytes(n, f) : 0;
     p.total = p.X + p.rows + p.HL16 + p.HL16T + p.Wp16 + p.Wp16T + p.G16 + p.G16T + p.gemm + p.colsum + p.red +
-              3328;
+              p.cp + 3584;
     return p;
 }
 }  // namespace
@@ -649,8 +693,12 @@ size_t gcn_loss_workspace_bytes(int32_t n, int32_t f, int32_t C, gcn_prec prec) 
 static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t ldhl, const float *W_pred,
                      const float *b_pred, int32_t C, gcn_loss_kind kind, const int32_t *labels,
                      const float *targets, float *loss, float *dHL, int32_t lddhl, float *dW_pred, float *db_pred,
-                     gcn_prec prec, void *ws, size_t ws_bytes, void *stream) {
+                     gcn_prec prec, void *ws, size_t ws_bytes, void *stream, float *below_dbias = nullptr) {
+    // below_dbias: write dHL multiplied by [HL > 0] (HL is the last layer's
+    // ReLU output), i.e. that layer's dZ, and its column sums to below_dbias
     REQUIRE(n >= 0 && f > 0 && C > 0, GCN_ESHAPE, "gcn_loss_grad: n=%d f=%d C=%d", n, f, C);
+    REQUIRE(!below_dbias || (prec == GCN_F32 && n > 0), GCN_EINVAL,
+            "gcn_loss_grad: the masked gradient needs float32, n > 0");
     REQUIRE(ldhl >= f && lddhl >= f, GCN_ESHAPE, "gcn_loss_grad: ldhl=%d lddhl=%d < f=%d", ldhl, lddhl, f);
     REQUIRE(kind == GCN_SOFTMAX_CE || kind == GCN_SIGMOID_BCE, GCN_EINVAL, "gcn_loss_grad: bad kind %d",
             kind);
@@ -678,6 +726,7 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     void *gw = pl.gemm ? ar.take<char>(pl.gemm) : nullptr;
     void *cw = ar.take<char>(pl.colsum);
     void *lw = ar.take<char>(pl.red);
+    float *cp = pl.cp ? ar.take<float>(pl.cp / sizeof(float)) : nullptr;
     int rc;
     if (n == 0) {
         rc = fill_zero(dW_pred, (int64_t)f * C, s);
@@ -729,7 +778,13 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
         d.seg[0] = GemmSeg{X, C, W_pred, C, C};
     }
     if ((rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s))) return rc;
-    return gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s);
+    if (below_dbias) {
+        d.mask = HL;
+        d.ldm = ldhl;
+        d.colpart = cp;
+    }
+    if ((rc = gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s))) return rc;
+    return below_dbias ? colsum_reduce_rows(gemm_colpart_rows(n), f, cp, below_dbias, s) : GCN_OK;
 }
 
 // ------------------------------------------------------------------ bf16
@@ -829,25 +884,33 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
     }
     const float *g = dY;  // PREDICT + LOSS, or the given output gradient
     int32_t ldg = lddy;
+    // float32: the head, and a layer whose input-gradient product runs
+    // unsplit, write the next layer down its dZ and bias gradient directly
+    bool ready = false;
     if (head) {
         const gcn_layer_args &last = layers[L - 1];
+        const bool fuse = prec == GCN_F32 && n > 0;
         if ((rc = loss_grad(launch, last.Y, n, 2 * last.h, last.ldy, head->W_pred, head->b_pred, head->C,
                             head->kind, head->labels, head->targets, head->loss, head->dHL, head->lddhl,
-                            head->dW_pred, head->db_pred, prec, ws, ws_bytes, stream)))
+                            head->dW_pred, head->db_pred, prec, ws, ws_bytes, stream,
+                            fuse ? last.dbias : nullptr)))
             return rc;
         g = head->dHL;
         ldg = head->lddhl;
+        ready = fuse;
     }
     for (int32_t l = L - 1; l >= 0; --l) {  // backward: layer l's dH is layer l-1's output gradient
         const gcn_layer_args &a = layers[l];
         const float *Hin = l == 0 ? H0 : layers[l - 1].Y;
         const int32_t ldin = l == 0 ? ldh0 : layers[l - 1].ldy;
+        const bool fuse = l > 0 && dH_mask_fusable(n, a.f_in, a.h, a.order, prec);
         if ((rc = layer_bwd(launch, A, AT, Hin, a.f_in, ldin, a.W_self, a.W_neigh, a.h, a.Y, a.ldy, a.saved,
                             a.saved_bytes, g, ldg, a.dH, a.lddh, a.dW_self, a.dW_neigh, a.dbias, a.order, prec, ws,
-                            ws_bytes, stream)))
+                            ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr)))
             return rc;
         g = a.dH;
         ldg = a.lddh;
+        ready = fuse;
     }
     return GCN_OK;
 }

@@ -122,6 +122,13 @@ struct GemmProblem {
     int relu;
     uint16_t *C16;      // when set: write bfloat16 (RNE) here instead of C (leading dim ldc)
     int32_t k_pad;      // trailing K columns that are zero padding (left out of the flop count)
+    // float32 kernel, unsplit only: C[i][j] is kept where mask[i][j] > 0 and
+    // set to 0 elsewhere (leading dim ldm), after bias and ReLU
+    const float *mask;
+    int64_t ldm;
+    // float32 kernel, unsplit only: colpart[t][j] = sum of the stored C[i][j]
+    // over the rows i of row tile t (gemm_colpart_rows(M) x N, leading dim N)
+    float *colpart;
 };
 // Up to two problems of equal layout and equal M, N, K in one launch
 // (grouped).  `bf16` selects bfloat16 operands (uint16 bits) instead of
@@ -131,6 +138,8 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
 size_t gemm_workspace_bytes(int nprob, const GemmProblem *probs, int split_k);
 // split-K count; k_is_rows: a weight gradient (K = vertices, few output tiles)
 int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows);
+// row tiles of a float32 product with M rows (the rows of colpart)
+int32_t gemm_colpart_rows(int32_t M);
 
 // elementwise / reductions ----------------------------------------------------
 // dZ = dY * [Y > 0]; columns [0,h) -> outS (ldS), [h,2h) -> outN (ldN);
@@ -141,6 +150,8 @@ int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y
              float *outS, int64_t ldS, float *outN, int64_t ldN,
              uint16_t *outS16, uint16_t *outN16, float *dbias,
              void *ws, size_t ws_bytes, hipStream_t s);
+// out[c] = sum over r < rows of part[r * C + c], in a fixed order
+int colsum_reduce_rows(int32_t rows, int32_t C, const float *part, float *out, hipStream_t s);
 // column sums of an n x C matrix, fixed order
 size_t colsum_workspace_bytes(int32_t n, int32_t C);
 int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *ws, size_t ws_bytes,

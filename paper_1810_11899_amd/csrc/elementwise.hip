@@ -439,6 +439,14 @@ int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *
     return GCN_OK;
 }
 
+int colsum_reduce_rows(int32_t rows, int32_t C, const float *part, float *out, hipStream_t s) {
+    if (C <= 0) return GCN_OK;
+    ProfScope ps(K_COLSUM_REDUCE, s, 0.0, (double)rows * C * 4.0);
+    hipLaunchKernelGGL(colsum_reduce_kernel, dim3((unsigned)((C + 3) / 4)), dim3(256), 0, s, rows, C, part, out);
+    GCN_LAUNCH_CHECK("colsum_reduce_kernel");
+    return GCN_OK;
+}
+
 int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
               float *rowloss, hipStream_t s) {
     if (n <= 0) return GCN_OK;

@@ -53,6 +53,9 @@ struct DevProblem {
     int relu;
     float *partial;     // split x M x N when split > 1
     uint16_t *C16;      // bfloat16 output instead of C (no split)
+    const float *mask;  // float32, no split: keep C where mask > 0 (leading dim ldm)
+    int64_t ldm;
+    float *colpart;     // float32, no split: per-row-tile column sums of C
 };
 
 struct DevArgs {
@@ -349,6 +352,14 @@ void gemm_kernel(DevArgs args) {
         for (int e = 0; e < 4; ++e) ebv[e] = ecol + e < P.N ? P.bias[ecol + e] : 0.0f;
     const bool erelu = !to_partial && P.relu;
     const bool evec = ldd % 4 == 0 && ((uintptr_t)dst & 15) == 0;
+    // optional mask operand (a [mask > 0] factor on every stored value), read
+    // for a pass's four rows before that pass's barrier; optional column sums
+    // of the stored values over this thread's 16 rows of the tile
+    const float *const emask = to_partial ? nullptr : P.mask;
+    const bool mvec = emask && P.ldm % 4 == 0 && ((uintptr_t)emask & 15) == 0 && ecol + 3 < P.N;
+    const bool ecs = !to_partial && P.colpart;
+    float4 mk[4];
+    float cs[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     auto put = [&](const floatx16 &v, int jb) {
         const int lc = wn * WTN + jb * 32 + (lane & 31);
 #pragma unroll
@@ -357,6 +368,24 @@ void gemm_kernel(DevArgs args) {
     __syncthreads();   // the last tile's operand reads are done
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
+        if (emask) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int row = m0 + 32 * h + wave * 8 + q * 2 + (lane >> 5);
+                mk[q] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                if (row < P.M && ecol < P.N) {
+                    const float *mp = emask + (int64_t)row * P.ldm + ecol;
+                    if (mvec) {
+                        mk[q] = *(const float4 *)mp;
+                    } else {
+                        mk[q].x = mp[0];
+                        if (ecol + 1 < P.N) mk[q].y = mp[1];
+                        if (ecol + 2 < P.N) mk[q].z = mp[2];
+                        if (ecol + 3 < P.N) mk[q].w = mp[3];
+                    }
+                }
+            }
+        }
         if (wm == (h >> 1)) {
             put(acc[h & 1][0], 0);
             put(acc[h & 1][1], 1);
@@ -373,6 +402,15 @@ void gemm_kernel(DevArgs args) {
                 if (erelu)
 #pragma unroll
                     for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
+                if (emask) {
+                    o[0] = mk[q].x > 0.0f ? o[0] : 0.0f;
+                    o[1] = mk[q].y > 0.0f ? o[1] : 0.0f;
+                    o[2] = mk[q].z > 0.0f ? o[2] : 0.0f;
+                    o[3] = mk[q].w > 0.0f ? o[3] : 0.0f;
+                }
+                if (ecs)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) cs[e] += o[e];
                 float *d = dst + (int64_t)row * ldd + ecol;
                 if (evec && ecol + 3 < P.N) {
                     *(float4 *)d = make_float4(o[0], o[1], o[2], o[3]);
@@ -384,6 +422,20 @@ void gemm_kernel(DevArgs args) {
             }
         }
         __syncthreads();
+    }
+    if (ecs) {
+        // the 8 row groups (wavefront, half) of each column, added in order
+        const int grp = wave * 2 + (lane >> 5);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) stg[grp * 128 + 4 * (lane & 31) + e] = cs[e];
+        __syncthreads();
+        if (threadIdx.x < 128) {
+            float t = 0.0f;
+#pragma unroll
+            for (int g = 0; g < 8; ++g) t += stg[g * 128 + threadIdx.x];
+            const int col = n0 + (int)threadIdx.x;
+            if (col < P.N) P.colpart[(int64_t)bc.tm * P.N + col] = t;
+        }
     }
 }
 
@@ -955,6 +1007,9 @@ void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int spl
         d.relu = g.relu;
         d.partial = nullptr;
         d.C16 = g.C16;
+        d.mask = g.mask;
+        d.ldm = g.ldm;
+        d.colpart = g.colpart;
         if (d.split > 1) {
             d.partial = partial ? (float *)((char *)partial + poff) : nullptr;
             poff += align256((size_t)d.split * g.M * g.N * sizeof(float));
@@ -1014,6 +1069,8 @@ int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows) {
     return (int)sp;
 }
 
+int32_t gemm_colpart_rows(int32_t M) { return M > 0 ? (M + kTBM - 1) / kTBM : 0; }
+
 size_t gemm_workspace_bytes(int nprob, const GemmProblem *probs, int split_k) {
     if (split_k <= 1) return 0;
     size_t b = 0;
@@ -1058,7 +1115,17 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         return GCN_EINVAL;
     }
     bool any_split = false;
-    for (int i = 0; i < nprob; ++i) any_split = any_split || a.p[i].split > 1;
+    for (int i = 0; i < nprob; ++i) {
+        any_split = any_split || a.p[i].split > 1;
+        if ((probs[i].mask || probs[i].colpart) && (bf16 || a.p[i].split > 1 || !probs[i].C || probs[i].C16)) {
+            set_error("gemm: the mask and column-sum epilogue needs an unsplit float32 product");
+            return GCN_EINVAL;
+        }
+        if (probs[i].mask && probs[i].ldm < probs[i].N) {
+            set_error("gemm: mask leading dimension %lld < N=%d", (long long)probs[i].ldm, probs[i].N);
+            return GCN_ESHAPE;
+        }
+    }
     int cls = layout == L_NN ? K_GEMM_NN : (layout == L_TN ? K_GEMM_TN : K_GEMM_NT);
     if (bf16) cls += K_GEMM_NN_BF16 - K_GEMM_NN;
     {

@@ -125,6 +125,7 @@ class StepRunner:
         """The transpose, then the whole fwd+bwd in one gcn_model_step call."""
         self._transpose(stream)
         self.model(self.A, self.AT, self.H0, self.ws, dY=self.dY if self.head is None else None, stream=stream)
+        self._last = "step"
 
     def step_calls(self, stream=None):
         """The same step as separate gcn_layer_fwd / gcn_loss_grad / gcn_layer_bwd calls."""
@@ -148,17 +149,22 @@ class StepRunner:
                             self.dWs[li], self.dWn[li], self.db[li], self.orders[li], self.ws, self.prec,
                             stream)
             dY = self.dH[li]
+        self._last = "calls"
 
     # ------------------------------------------------------------ results
     def results(self) -> dict:
+        """Host copies of the last step's outputs.  After ``step()`` the
+        inter-layer gradient buffers (dHL, dH of layers 1..L-1) hold
+        intermediate values and are reported as None."""
         c = lambda t: None if t is None else t.detach().cpu().numpy()
+        inner = getattr(self, "_last", "calls") == "step"
         r = {"Y": [c(y) for y in self.Y], "dW_self": [c(t) for t in self.dWs],
              "dW_neigh": [c(t) for t in self.dWn], "db": [c(t) for t in self.db],
-             "dH": [c(t) for t in self.dH],
+             "dH": [None if (inner and li > 0) else c(t) for li, t in enumerate(self.dH)],
              "t_indptr": c(self.AT.indptr), "t_indices": c(self.AT.indices), "t_vals": c(self.AT.vals)}
         if self.head is not None:
             r.update(loss=float(self.loss.item()), dW_pred=c(self.dW_pred), db_pred=c(self.db_pred),
-                     dHL=c(self.dHL))
+                     dHL=None if inner else c(self.dHL))
         return r
 
     # ---------------------------------------------------- work accounting
