@@ -215,13 +215,14 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl,
  * run in order on `stream`.  Errors are those of the calls it makes.
  * Buffers between the calls: head->dHL and the dH of layers 1..L-1 carry the
  * gradient from one call to the next, and their contents on return are
- * unspecified.  With float32 the step multiplies such a gradient by the
- * ReLU derivative of the layer that consumes it as the gradient is written
- * (the head's dHL, and a layer's dH when its input-gradient product runs
- * unsplit), and that layer's bias gradient is summed in the same pass; every
- * other output equals the separate calls' bit for bit, and those bias
- * gradients equal theirs up to the order of the sum.  Layer 0's dH, when
- * given, is the gradient with respect to H0 as in gcn_layer_bwd. */
+ * unspecified.  The step multiplies such a gradient by the ReLU derivative
+ * of the layer that consumes it as the gradient is written (the head's dHL,
+ * and a layer's dH when its input-gradient product runs unsplit; with
+ * GCN_BF16 the buffer then holds that layer's bfloat16 operand rows), and
+ * that layer's bias gradient is summed in the same pass; every other output
+ * equals the separate calls' bit for bit, and those bias gradients equal
+ * theirs up to the order of the sum.  Layer 0's dH, when given, is the
+ * gradient with respect to H0 as in gcn_layer_bwd. */
 typedef struct {
     int32_t f_in, h;
     gcn_order order;

@@ -151,15 +151,18 @@ bool bwd_uses_G(int order, bool dH, int32_t f_in, int32_t h) {
     return order == GCN_TRANSFORM_FIRST || (dH && h <= f_in);
 }
 
-// The float32 input-gradient product of a layer whose backward forms G:
+// The input-gradient product of a layer whose backward forms G:
 // dH = [dZ_s || G] [W_self || W_neigh]^T, one product with K = 2h.  When it
 // runs unsplit, a model step has its epilogue multiply dH by the ReLU
 // derivative of the layer below, [H > 0] (H = that layer's output Y), and sum
 // the columns of the result: the layer below then receives its dZ and bias
 // gradient ready (Sec. III-A's backward pass, with the mask of the layer
-// below applied where its input gradient is written).
+// below applied where its input gradient is written).  With bfloat16
+// operands the epilogue stores dZ as the bfloat16 rows the layer below
+// multiplies with (n x f_in, leading dimension f_in, in the dH buffer).
 bool dH_mask_fusable(int32_t n, int32_t f_in, int32_t h, int order, int prec) {
-    if (prec != GCN_F32 || n <= 0 || !bwd_uses_G(order, true, f_in, h)) return false;
+    (void)prec;
+    if (n <= 0 || !bwd_uses_G(order, true, f_in, h)) return false;
     GemmProblem d{};
     d.M = n;
     d.N = f_in;
@@ -506,9 +509,11 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
                      int32_t lddh, float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec,
                      void *ws, size_t ws_bytes, void *stream, bool dz_ready = false,
                      float *below_dbias = nullptr) {
-    // dz_ready: dY already holds dZ = dY * [Y > 0] and dbias is already
-    // written (by the producer of dY).  below_dbias: write dH multiplied by
-    // [H > 0] and its column sums to below_dbias (dH_mask_fusable only).
+    // dz_ready: dY already holds dZ = dY * [Y > 0] (float32 with leading
+    // dimension lddy, or bfloat16 n x 2h with leading dimension 2h) and dbias
+    // is already written (by the producer of dY).  below_dbias: write dH
+    // multiplied by [H > 0] (bfloat16 n x f_in rows with bfloat16 operands)
+    // and its column sums to below_dbias (dH_mask_fusable only).
     int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_bwd");
     if (rc) return rc;
     rc = check_csr(AT, "gcn_layer_bwd (transpose)");
@@ -526,9 +531,9 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
             "gcn_layer_bwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
     const bool want_dH = dH != nullptr;
-    REQUIRE(!dz_ready || (prec == GCN_F32 && n > 0), GCN_EINVAL, "gcn_layer_bwd: masked dY needs float32, n > 0");
+    REQUIRE(!dz_ready || n > 0, GCN_EINVAL, "gcn_layer_bwd: masked dY needs n > 0");
     REQUIRE(!below_dbias || (want_dH && dH_mask_fusable(n, f_in, h, order, prec)), GCN_EINVAL,
-            "gcn_layer_bwd: the masked input gradient needs an unsplit float32 product");
+            "gcn_layer_bwd: the masked input gradient needs an unsplit product");
     const LayerPlan pl = plan_layer(n, A->nnz, f_in, h, order, want_dH, prec);
     REQUIRE(ws && ws_bytes >= pl.bwd_total, GCN_EWORKSPACE, "gcn_layer_bwd: workspace %zu < %zu bytes",
             ws_bytes, pl.bwd_total);
@@ -552,10 +557,10 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     // where dZ_s, dZ_n and G = A^T dZ_n live: in the workspace, or, with dZ
     // given, dZ in dY and G at the start of P
     const char *Zs = dz_ready ? (const char *)dY : P;
-    const int64_t ldZs = dz_ready ? lddy : ldP;
+    const int64_t ldZs = dz_ready ? (bf ? ldP : lddy) : ldP;
     char *ZnW = pl.need_G ? D : Pn;
-    const char *Zn = dz_ready ? (const char *)(dY + h) : ZnW;
-    const int64_t ldZn = dz_ready ? lddy : (pl.need_G ? h : ldP);
+    const char *Zn = dz_ready ? Zs + (size_t)h * E : ZnW;
+    const int64_t ldZn = dz_ready ? ldZs : (pl.need_G ? h : ldP);
     char *Gp = dz_ready ? P : Pn;
     const int64_t ldG = dz_ready ? h : ldP;
 
@@ -591,8 +596,16 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
         const uint16_t *AGG16T = af ? (const uint16_t *)((const char *)saved + 3 * one) : nullptr;
         uint16_t *PT = (uint16_t *)ar.take<char>(pl.bwd_PT);
         uint16_t *DT = pl.bwd_DT ? (uint16_t *)ar.take<char>(pl.bwd_DT) : nullptr;
-        if ((rc = transpose_bf16(n, 2 * h, P, 1, ldP, PT, n, s))) return rc;
-        if (DT && (rc = transpose_bf16(n, h, D, 1, h, DT, n, s))) return rc;
+        if (!dz_ready) {
+            if ((rc = transpose_bf16(n, 2 * h, P, 1, ldP, PT, n, s))) return rc;
+            if (DT && (rc = transpose_bf16(n, h, D, 1, h, DT, n, s))) return rc;
+        } else if (af) {   // PT = [dZ_s || dZ_n]^T
+            if ((rc = transpose_bf16(n, 2 * h, Zs, 1, ldZs, PT, n, s))) return rc;
+            DT = nullptr;
+        } else {           // PT = [dZ_s || G]^T
+            if ((rc = transpose_bf16(n, h, Zs, 1, ldZs, PT, n, s))) return rc;
+            if ((rc = transpose_bf16(n, h, Gp, 1, ldG, PT + (size_t)h * n, n, s))) return rc;
+        }
         layout = L_NT;
         g[0].seg[0] = GemmSeg{H16T, n, PT, n, n};
         if (!af) g[1].seg[0] = GemmSeg{H16T, n, PT + (size_t)h * n, n, n};
@@ -631,6 +644,11 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
             d.mask = H;
             d.ldm = ldh;
             d.colpart = cp;
+            if (bf) {
+                d.C = nullptr;
+                d.C16 = (uint16_t *)dH;
+                d.ldc = f_in;
+            }
         }
         if ((rc = gemm(L_NT, 1, &d, bf, gemm_pick_split(1, &d, false), gw, pl.bwd_gemm, s))) return rc;
         return below_dbias ? colsum_reduce_rows(gemm_colpart_rows(n), f_in, cp, below_dbias, s) : GCN_OK;
@@ -679,7 +697,7 @@ LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
     p.gemm = gemm_workspace_bytes(1, &g, p.split);
     p.colsum = colsum_workspace_bytes(n, C);
     p.red = loss_reduce_workspace_bytes(n);
-    p.cp = prec == GCN_F32 ? colpart_bytes(n, f) : 0;
+    p.cp = colpart_bytes(n, f);
     p.total = p.X + p.rows + p.HL16 + p.HL16T + p.Wp16 + p.Wp16T + p.G16 + p.G16T + p.gemm + p.colsum + p.red +
               p.cp + 3584;
     return p;
@@ -695,10 +713,10 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
                      const float *targets, float *loss, float *dHL, int32_t lddhl, float *dW_pred, float *db_pred,
                      gcn_prec prec, void *ws, size_t ws_bytes, void *stream, float *below_dbias = nullptr) {
     // below_dbias: write dHL multiplied by [HL > 0] (HL is the last layer's
-    // ReLU output), i.e. that layer's dZ, and its column sums to below_dbias
+    // ReLU output), i.e. that layer's dZ (bfloat16 n x f rows, leading
+    // dimension f, with bfloat16 operands), and its column sums to below_dbias
     REQUIRE(n >= 0 && f > 0 && C > 0, GCN_ESHAPE, "gcn_loss_grad: n=%d f=%d C=%d", n, f, C);
-    REQUIRE(!below_dbias || (prec == GCN_F32 && n > 0), GCN_EINVAL,
-            "gcn_loss_grad: the masked gradient needs float32, n > 0");
+    REQUIRE(!below_dbias || n > 0, GCN_EINVAL, "gcn_loss_grad: the masked gradient needs n > 0");
     REQUIRE(ldhl >= f && lddhl >= f, GCN_ESHAPE, "gcn_loss_grad: ldhl=%d lddhl=%d < f=%d", ldhl, lddhl, f);
     REQUIRE(kind == GCN_SOFTMAX_CE || kind == GCN_SIGMOID_BCE, GCN_EINVAL, "gcn_loss_grad: bad kind %d",
             kind);
@@ -782,6 +800,11 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
         d.mask = HL;
         d.ldm = ldhl;
         d.colpart = cp;
+        if (bf) {
+            d.C = nullptr;
+            d.C16 = (uint16_t *)dHL;
+            d.ldc = f;
+        }
     }
     if ((rc = gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s))) return rc;
     return below_dbias ? colsum_reduce_rows(gemm_colpart_rows(n), f, cp, below_dbias, s) : GCN_OK;
@@ -884,12 +907,12 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
     }
     const float *g = dY;  // PREDICT + LOSS, or the given output gradient
     int32_t ldg = lddy;
-    // float32: the head, and a layer whose input-gradient product runs
-    // unsplit, write the next layer down its dZ and bias gradient directly
+    // the head, and a layer whose input-gradient product runs unsplit, write
+    // the next layer down its dZ and bias gradient directly
     bool ready = false;
     if (head) {
         const gcn_layer_args &last = layers[L - 1];
-        const bool fuse = prec == GCN_F32 && n > 0;
+        const bool fuse = n > 0;
         if ((rc = loss_grad(launch, last.Y, n, 2 * last.h, last.ldy, head->W_pred, head->b_pred, head->C,
                             head->kind, head->labels, head->targets, head->loss, head->dHL, head->lddhl,
                             head->dW_pred, head->db_pred, prec, ws, ws_bytes, stream,

@@ -615,6 +615,13 @@ void gemm_bf16_kernel(DevArgs args) {
     const bool to_partial = P.split > 1;
     float *dst = to_partial ? P.partial + (int64_t)split * P.M * P.N : P.C;
     const int64_t ldd = to_partial ? P.N : P.ldc;
+    // optional [mask > 0] factor and per-row-tile column sums, as in the
+    // float32 kernel
+    const float *const emask = to_partial ? nullptr : P.mask;
+    const bool ecs = !to_partial && P.colpart;
+    float cs[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) cs[j] = 0.0f;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -630,6 +637,8 @@ void gemm_bf16_kernel(DevArgs args) {
                     if (!to_partial) {
                         v += bv;
                         if (P.relu) v = fmaxf(v, 0.0f);
+                        if (emask) v = emask[(int64_t)row * P.ldm + col] > 0.0f ? v : 0.0f;
+                        if (ecs) cs[j] += v;
                         if (P.C16) {
                             P.C16[(int64_t)row * P.ldc + col] = to_bf16(v);
                             continue;
@@ -639,6 +648,24 @@ void gemm_bf16_kernel(DevArgs args) {
                 }
             }
         }
+    if (ecs) {
+        // the 4 row groups (wavefront row, half) of each column, in order
+        static_assert(kTBM16 == 128, "column-sum rows are 128-row tiles");
+        float *red = (float *)&As[0][0][0];
+        static_assert(4 * kTBN16 * sizeof(float) <= sizeof(As), "column sums fit the operand buffer");
+        __syncthreads();   // operand reads done
+        const int grp = wm * 2 + (lane >> 5);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) red[grp * kTBN16 + wn * WTN + j * 32 + (lane & 31)] = cs[j];
+        __syncthreads();
+        if (threadIdx.x < kTBN16) {
+            float t = 0.0f;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) t += red[g * kTBN16 + threadIdx.x];
+            const int col = n0 + (int)threadIdx.x;
+            if (col < P.N) P.colpart[(int64_t)bc.tm * P.N + col] = t;
+        }
+    }
 }
 
 // C = sum over splits of the partial tiles, then the epilogue.  A block
@@ -736,6 +763,12 @@ constexpr int kBigBK = 32;       // k per stage
 #define GCN_BIG_STAGES 4
 #endif
 constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU's LDS)
+#ifndef GCN_BIG_MASKED
+#define GCN_BIG_MASKED 1
+#endif
+#ifndef GCN_BIG_MASK_PREFETCH
+#define GCN_BIG_MASK_PREFETCH 4
+#endif
 #ifndef GCN_BIG_WAVES
 #define GCN_BIG_WAVES 8
 #endif
@@ -888,9 +921,40 @@ void gemm_bf16_big_kernel(DevArgs args) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) bv[e] = col + e < P.N ? P.bias[col + e] : 0.0f;
     const bool relu = !to_partial && P.relu;
+    // optional [mask > 0] factor and column sums per 128-row half of the tile
+    const float *const emask = to_partial ? nullptr : P.mask;
+    const bool mvec = emask && P.ldm % 4 == 0 && ((uintptr_t)emask & 15) == 0 && col + 3 <= Nlast;
+    const bool ecs = !to_partial && P.colpart;
+    float cs[2][4] = {{0.0f, 0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f, 0.0f}};
+    // the mask of a pass's rows is loaded in batches of kMaskBatch rows: the
+    // first batch before that pass's deposit and barrier (its latency
+    // overlaps them), each later one as the previous batch is used up
+    constexpr int kRowsPerWave = 128 / kBigWaves;
+    constexpr int kMaskBatch = GCN_BIG_MASK_PREFETCH;
+    static_assert(kRowsPerWave % kMaskBatch == 0, "whole mask batches");
+    float4 mk[kMaskBatch];
+    auto load_mask = [&](int h, int k0) {
+#pragma unroll
+        for (int k = 0; k < kMaskBatch; ++k) {
+            const int row = m0 + h * 128 + wave + (k0 + k) * kBigWaves;
+            mk[k] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (row <= Mlast && col <= Nlast) {
+                const float *mp = emask + (int64_t)row * P.ldm + col;
+                if (mvec) {
+                    mk[k] = *(const float4 *)mp;
+                } else {
+                    mk[k].x = mp[0];
+                    if (col + 1 <= Nlast) mk[k].y = mp[1];
+                    if (col + 2 <= Nlast) mk[k].z = mp[2];
+                    if (col + 3 <= Nlast) mk[k].w = mp[3];
+                }
+            }
+        }
+    };
     __syncthreads();   // every wavefront is done reading the ring
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
+        if (emask) load_mask(h, 0);
         if (wm == h) {
             put(acc[0][0], 0, 0); put(acc[0][1], 0, 1);
             put(acc[1][0], 1, 0); put(acc[1][1], 1, 1);
@@ -904,7 +968,10 @@ void gemm_bf16_big_kernel(DevArgs args) {
             }
         }
         __syncthreads();
-        for (int rr = wave; rr < 128; rr += kBigWaves) {
+#pragma unroll
+        for (int k = 0; k < kRowsPerWave; ++k) {
+            if (emask && k > 0 && k % kMaskBatch == 0) load_mask(h, k);
+            const int rr = wave + k * kBigWaves;
             const int row = m0 + h * 128 + rr;
             if (row > Mlast || col > Nlast) continue;
             const float4 q = *(const float4 *)&stg[rr * kBigT + 4 * lane];
@@ -912,6 +979,16 @@ void gemm_bf16_big_kernel(DevArgs args) {
             if (relu)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
+            if (emask) {
+                const float4 m = mk[k % kMaskBatch];
+                o[0] = m.x > 0.0f ? o[0] : 0.0f;
+                o[1] = m.y > 0.0f ? o[1] : 0.0f;
+                o[2] = m.z > 0.0f ? o[2] : 0.0f;
+                o[3] = m.w > 0.0f ? o[3] : 0.0f;
+            }
+            if (ecs)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) cs[h][e] += o[e];
             if (c16) {
                 uint16_t *d = P.C16 + (int64_t)row * P.ldc + col;
                 if (vec && col + 3 <= Nlast) {
@@ -934,6 +1011,22 @@ void gemm_bf16_big_kernel(DevArgs args) {
             }
         }
         __syncthreads();
+    }
+    if (ecs) {
+        // per half: the 8 wavefronts' sums of each column, in order; the
+        // half's rows are column-sum row 2 * tm + h (128-row tiles)
+        static_assert(16 * kBigT * sizeof(float) <= sizeof(lds), "column sums fit the ring");
+        static_assert(kBigThreads == 2 * kBigT, "one thread per (half, column)");
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) stg[(h * kBigWaves + wave) * kBigT + 4 * lane + e] = cs[h][e];
+        __syncthreads();
+        const int h = (int)threadIdx.x / kBigT, c = (int)threadIdx.x % kBigT;
+        float t = 0.0f;
+#pragma unroll
+        for (int w = 0; w < kBigWaves; ++w) t += stg[(h * kBigWaves + w) * kBigT + c];
+        if (m0 + h * 128 <= Mlast && n0 + c <= Nlast) P.colpart[(int64_t)(2 * bc.tm + h) * P.N + n0 + c] = t;
     }
 }
 
@@ -960,6 +1053,7 @@ int tile_n_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBN16 : kTBN); }
 bool big_ok(int layout, int nprob, const GemmProblem *probs) {
     if (layout != L_NT || GCN_BF16_BIG == 0) return false;
     for (int i = 0; i < nprob; ++i) {
+        if (!GCN_BIG_MASKED && probs[i].mask) return false;
         // a side of 128 or less would leave most of a 256-wide tile idle
         if (probs[i].M <= 128 || probs[i].N <= 128) return false;
         for (int s = 0; s < 2; ++s) {
@@ -1117,8 +1211,8 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     bool any_split = false;
     for (int i = 0; i < nprob; ++i) {
         any_split = any_split || a.p[i].split > 1;
-        if ((probs[i].mask || probs[i].colpart) && (bf16 || a.p[i].split > 1 || !probs[i].C || probs[i].C16)) {
-            set_error("gemm: the mask and column-sum epilogue needs an unsplit float32 product");
+        if ((probs[i].mask || probs[i].colpart) && (a.p[i].split > 1 || (probs[i].C16 != nullptr) == (probs[i].C != nullptr))) {
+            set_error("gemm: the mask and column-sum epilogue needs an unsplit product with one output");
             return GCN_EINVAL;
         }
         if (probs[i].mask && probs[i].ldm < probs[i].N) {

@@ -190,23 +190,24 @@ def test_forced_orders_agree_with_oracle(order):
 
 
 @pytest.mark.parametrize("case", ["cfg1-f32", "cfg1-bf16", "cfg2-bf16", "dY-f32", "bce-transform-first",
-                                  "f32-odd-widths"])
+                                  "f32-odd-widths", "bf16-odd-widths"])
 def test_model_step_matches_separate_calls(case):
     """gcn_model_step computes what the separate calls compute: every output
-    bit for bit, except that with float32 a layer whose dZ arrives from the
-    head or from an unsplit input-gradient product (masked in that product's
-    epilogue) has its bias gradient summed there, in another order.  The
-    inter-layer gradient buffers then hold the separate calls' gradient
-    times [input > 0], or that gradient itself."""
+    bit for bit, except that a layer whose dZ arrives from the head or from an
+    unsplit input-gradient product (masked in that product's epilogue) has its
+    bias gradient summed there, in another order.  The inter-layer gradient
+    buffers then hold the separate calls' gradient times [input > 0] (as
+    packed bfloat16 rows with bfloat16 operands), or that gradient itself."""
     if case.startswith("cfg"):
         wl = synth.config(int(case[3]))
         r = StepRunner(wl, prec=B.GCN_BF16 if case.endswith("bf16") else B.GCN_F32)
     elif case == "dY-f32":
         wl = synth.custom(2500, "rmat", 10, [(64, 32), (64, 48)], head=None, seed=4)
         r = StepRunner(wl, first_layer_dH=True)
-    elif case == "f32-odd-widths":   # ragged tiles, widths not a multiple of 4 (scalar mask loads)
+    elif case.endswith("odd-widths"):   # ragged tiles, widths not a multiple of 4 (scalar mask loads)
         wl = synth.custom(2999, "rmat", 9, [(70, 51), (102, 50)], head="ce", classes=13, seed=5)
-        r = StepRunner(wl, orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
+        r = StepRunner(wl, prec=B.GCN_BF16 if case.startswith("bf16") else B.GCN_F32,
+                       orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
     else:
         wl = synth.custom(3000, "rmat", 12, [(96, 64), (128, 64)], head="bce", classes=30, seed=2)
         r = StepRunner(wl, orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
@@ -224,10 +225,7 @@ def test_model_step_matches_separate_calls(case):
             assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), (key, i)
     fp32 = r.prec == B.GCN_F32
     for i, (x, y) in enumerate(zip(a["db"], b["db"])):
-        if fp32:
-            assert rel_inf(y, x) <= 1e-6, i
-        else:
-            assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), ("db", i)
+        assert rel_inf(y, x) <= 1e-6, i
     if "loss" in a:
         assert a["loss"] == b["loss"]
         for key in ("dW_pred", "db_pred"):
@@ -239,11 +237,17 @@ def test_model_step_matches_separate_calls(case):
     for i, (g, got, y) in enumerate(zip(sep, inner, below)):
         masked = np.where(y > 0, g, np.float32(0))
         same = np.array_equal(got.view(np.uint32), g.view(np.uint32))
-        fused = np.array_equal(got.view(np.uint32), masked.view(np.uint32))
-        assert same or (fp32 and fused), ("inter-layer gradient", i)
-        if fp32 and r.head is not None and i == 0:
-            assert fused, "float32 head writes the last layer's dZ"
-        if case in ("bce-transform-first", "f32-odd-widths"):
+        if fp32:
+            fused = np.array_equal(got.view(np.uint32), masked.view(np.uint32))
+        else:
+            rows, cols = masked.shape
+            packed = got.view(np.uint16).reshape(-1)[: rows * cols].reshape(rows, cols)
+            bits = torch.from_numpy(np.ascontiguousarray(masked)).to(torch.bfloat16).view(torch.int16).numpy()
+            fused = np.array_equal(packed, bits.view(np.uint16))
+        assert same or fused, ("inter-layer gradient", i)
+        if r.head is not None and i == 0:
+            assert fused, "the head writes the last layer's dZ"
+        if case in ("bce-transform-first", "f32-odd-widths", "bf16-odd-widths"):
             assert fused and not same, ("unsplit input-gradient product writes dZ", i)
 
 
