@@ -366,19 +366,21 @@ void spmm_sliced(
     const bool cok = col < k;
     constexpr int U = GCN_SPMM_U;  // edges per lane group in flight
 
+    // edge positions relative to p0 (32-bit: nnz < 2^31), as staged in LDS
+    const int q0 = (int)p0;
     int32_t hrow = -1, trow = -1;
     for (int r = r0; r <= r1 && r < n_rows; ++r) {
-        const int64_t rb = r_ptr[r - r0], re = r_ptr[r - r0 + 1];
+        const int rb = r_ptr[r - r0], re = r_ptr[r - r0 + 1];
         const bool complete = r < r1;
-        const int64_t pb = p0 > rb ? p0 : rb;
-        const int64_t pe = complete ? re : p1;
+        const int pb = (q0 > rb ? q0 : rb) - q0;
+        const int pe = (complete ? re : (int)p1) - q0;
         float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
-        int64_t p = pb + g;
+        int p = pb + g;
         for (; p + 4 * (U - 1) < pe; p += 4 * U) {
             int32_t j[U];
             float w[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + 4 * u - p0]; w[u] = e_val[p + 4 * u - p0]; }
+            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + 4 * u]; w[u] = e_val[p + 4 * u]; }
             float4 x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
@@ -392,8 +394,8 @@ void spmm_sliced(
             }
         }
         for (; p < pe; p += 4) {
-            const int32_t j = e_idx[p - p0];
-            const float w = e_val[p - p0];
+            const int32_t j = e_idx[p];
+            const float w = e_val[p];
             const float4 x = cok ? *(const float4 *)(X + (int64_t)j * ldx + col) : make_float4(0.f, 0.f, 0.f, 0.f);
             a0 = fmaf(w, x.x, a0);
             a1 = fmaf(w, x.y, a1);
@@ -404,7 +406,7 @@ void spmm_sliced(
         a0 += __shfl_xor(a0, 16); a1 += __shfl_xor(a1, 16); a2 += __shfl_xor(a2, 16); a3 += __shfl_xor(a3, 16);
         a0 += __shfl_xor(a0, 32); a1 += __shfl_xor(a1, 32); a2 += __shfl_xor(a2, 32); a3 += __shfl_xor(a3, 32);
         const float acc[4] = {a0, a1, a2, a3};
-        const bool started = (r > r0) || (p0 == rb);
+        const bool started = (r > r0) || (q0 == rb);
         if (g == 0 && cok) {
             if (complete && started) {
                 emit<4>(out, ldo, r, col, acc, epi, bias);

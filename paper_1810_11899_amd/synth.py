@@ -157,6 +157,19 @@ def permutation_graph(n: int, rng: np.random.Generator) -> Graph:
     return csr_from_pairs(n, np.arange(n), p, np.ones(n, np.float32))
 
 
+def circulant_graph(n: int, offsets) -> Graph:
+    """Row i holds columns (i + o) mod n and (i - o) mod n for each offset o
+    (distinct, 0 < o < n/2): an undirected graph of degree 2 * len(offsets)
+    whose rows reach across the whole vertex range."""
+    o = np.asarray(offsets, dtype=np.int64)
+    i = np.arange(n, dtype=np.int64)[:, None]
+    cols = np.sort(np.concatenate([(i + o) % n, (i - o) % n], axis=1), axis=1)
+    deg = cols.shape[1]
+    indptr = (np.arange(n + 1, dtype=np.int64) * deg).astype(np.int32)
+    vals = np.full(n * deg, np.float32(1.0) / np.float32(deg), dtype=np.float32)
+    return Graph(n, indptr, cols.reshape(-1).astype(np.int32), vals)
+
+
 def complete_graph(n: int) -> Graph:
     i, j = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
     keep = i != j
@@ -223,6 +236,24 @@ class Workload:
     @property
     def n(self) -> int:
         return self.graph.n
+
+
+def periodic_normal(rng: np.random.Generator, n: int, f: int, period: int = 65537):
+    """An n x f float32 matrix described by parts, for matrices too large to
+    draw entry by entry in seconds (billions of entries): row i is
+    2^e_i * R[i mod period] with R ~ N(0, 1) (period x f) and e_i uniform on
+    {-1, 0, 1}.  The scaling is exact in float32, and no two rows 2^k rows
+    apart are equal (the period is odd).  Returns (R, e); periodic_rows
+    gives rows of the matrix."""
+    R = rng.standard_normal((min(period, n), f), dtype=np.float32)
+    e = rng.integers(-1, 2, size=n).astype(np.int8)
+    return R, e
+
+
+def periodic_rows(R: np.ndarray, e: np.ndarray, rows) -> np.ndarray:
+    """Rows `rows` of the matrix described by periodic_normal's parts."""
+    rows = np.asarray(rows, dtype=np.int64)
+    return np.ldexp(R[rows % R.shape[0]], e[rows].astype(np.int32)[:, None]).astype(np.float32)
 
 
 def glorot(rng: np.random.Generator, fan_in: int, fan_out: int) -> np.ndarray:
