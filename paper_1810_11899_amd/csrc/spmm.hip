@@ -182,16 +182,45 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
 
 // Final value of out[r, c .. c+VEC) under the epilogue; `out` is float, or
 // bfloat16 bits for EPI_STORE_BF16 (ldo counts elements of either type).
+// ovec: the VEC elements are one aligned vector (ldo a multiple of VEC and
+// `out` aligned to min(16, VEC * element size) bytes), moved with 16-, 8- or
+// 4-byte accesses instead of one access per element.
 template <int VEC>
 __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_t r, int c,
-                                     const float (&acc)[VEC], int epi, const float *__restrict__ bias) {
+                                     const float (&acc)[VEC], int epi, const float *__restrict__ bias,
+                                     bool ovec) {
     if (epi == EPI_STORE_BF16) {
         uint16_t *o = (uint16_t *)out + r * ldo + c;
+        if (VEC >= 2 && ovec) {
+            uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
+#pragma unroll
+            for (int i = 0; i < VEC / 2; ++i)
+                w[i] = (uint32_t)to_bf16(acc[2 * i]) | ((uint32_t)to_bf16(acc[2 * i + 1]) << 16);
+            if constexpr (VEC == 8) *(uint4 *)o = make_uint4(w[0], w[1], w[2], w[3]);
+            else if constexpr (VEC == 4) *(uint2 *)o = make_uint2(w[0], w[1]);
+            else *(uint32_t *)o = w[0];
+            return;
+        }
 #pragma unroll
         for (int v = 0; v < VEC; ++v) o[v] = to_bf16(acc[v]);
         return;
     }
     float *o = (float *)out + r * ldo + c;
+    if (VEC >= 4 && ovec) {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+            float x[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+            if (epi == EPI_BIAS_RELU) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) x[e] = fmaxf(x[e] + bias[c + 4 * q + e], 0.0f);
+            } else if (epi == EPI_ACCUMULATE) {
+                const float4 p = *(const float4 *)(o + 4 * q);
+                x[0] = p.x + x[0]; x[1] = p.y + x[1]; x[2] = p.z + x[2]; x[3] = p.w + x[3];
+            }
+            *(float4 *)(o + 4 * q) = make_float4(x[0], x[1], x[2], x[3]);
+        }
+        return;
+    }
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
         float x = acc[v];
@@ -213,7 +242,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_MA
 void spmm_main(
     int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
     const float *__restrict__ vals, const void *__restrict__ Xv, int32_t k, int64_t ldx,
-    void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
+    void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias, int ovec,
     int64_t items, int ipw, int64_t waves, const int32_t *__restrict__ bnd, float *__restrict__ carry,
     int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
     using Elem = typename std::conditional<BF16, uint16_t, float>::type;
@@ -288,7 +317,7 @@ void spmm_main(
             for (int t = 0; t < CT; ++t)
                 if (cok[t]) {
                     const int c = cbase + t * 64 * VEC;
-                    emit<VEC>(out, ldo, r, c, acc[t], epi, bias);
+                    emit<VEC>(out, ldo, r, c, acc[t], epi, bias, ovec != 0);
                 }
         } else if (complete || pe > pb) {
             // a piece of a row cut by wavefront boundaries: head (the piece
@@ -409,7 +438,7 @@ void spmm_sliced(
         const bool started = (r > r0) || (q0 == rb);
         if (g == 0 && cok) {
             if (complete && started) {
-                emit<4>(out, ldo, r, col, acc, epi, bias);
+                emit<4>(out, ldo, r, col, acc, epi, bias, true);   // ldo % 4 == 0, 16-byte aligned
             } else if (complete || pe > pb) {
                 const int slot = complete ? 0 : 1;
                 store_raw<4>(carry + (2 * wave + slot) * (int64_t)k + col, acc);
@@ -514,7 +543,7 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
         if (c >= k) continue;
         const float hv = carry[(2 * w) * (int64_t)k + c];
         const float a[1] = {any ? acc[j] + hv : hv};
-        emit<1>(out, ldo, r, c, a, epi, bias);
+        emit<1>(out, ldo, r, c, a, epi, bias, false);
     }
 }
 
@@ -523,8 +552,11 @@ void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr
                  const int32_t *indices, const float *vals, const void *X, int32_t k, int64_t ldx,
                  void *out, int64_t ldo, int epi, const float *bias, const SpmmPlan &pl,
                  const int32_t *bnd, float *carry, int32_t *hr, int32_t *tr) {
+    // the epilogue's per-lane VEC outputs as one vector store when aligned
+    const size_t chunk = std::min<size_t>(16, (size_t)VEC * (epi == EPI_STORE_BF16 ? 2 : 4));
+    const int ovec = ldo % VEC == 0 && (uintptr_t)out % chunk == 0;
     hipLaunchKernelGGL((spmm_main<VEC, CT, BF16>), grid, dim3(256), 0, s, n_rows, indptr, indices,
-                       vals, X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw, pl.waves, bnd, carry, hr,
+                       vals, X, k, ldx, out, ldo, epi, bias, ovec, pl.items, pl.ipw, pl.waves, bnd, carry, hr,
                        tr);
 }
 
