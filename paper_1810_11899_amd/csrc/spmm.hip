@@ -29,7 +29,10 @@ namespace gcn {
 namespace {
 
 constexpr int kWavesPerBlock = 4;
-constexpr int kUnroll = 4;
+#ifndef GCN_SPMM_MAIN_U
+#define GCN_SPMM_MAIN_U 4
+#endif
+constexpr int kUnroll = GCN_SPMM_MAIN_U;   // edges in flight per wavefront (spmm_main)
 constexpr int kMaxIpw = 256;   // merge items per wavefront, at most
 #ifndef GCN_SPMM_U
 #define GCN_SPMM_U 4
@@ -126,52 +129,47 @@ __global__ __launch_bounds__(256) void spmm_bounds_kernel(int32_t n_rows, const 
     if (lane == 0) bnd[w] = r;
 }
 
+// One lane's VEC consecutive elements of a gathered row.  bfloat16 rows keep
+// the loaded words and widen an element when it is used, so a gather in
+// flight holds VEC/2 registers rather than VEC.
 template <int VEC, bool BF16> struct Row;
-template <> struct Row<1, false> {
-    float v[1];
-    __device__ void load(const float *p) { v[0] = *p; }
-};
-template <> struct Row<2, false> {
-    float v[2];
+template <int VEC> struct Row<VEC, false> {
+    float v[VEC];
     __device__ void load(const float *p) {
-        const float2 t = *(const float2 *)p;
-        v[0] = t.x; v[1] = t.y;
+        if constexpr (VEC == 4) {
+            const float4 t = *(const float4 *)p;
+            v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+        } else if constexpr (VEC == 2) {
+            const float2 t = *(const float2 *)p;
+            v[0] = t.x; v[1] = t.y;
+        } else {
+            v[0] = *p;
+        }
     }
-};
-template <> struct Row<4, false> {
-    float v[4];
-    __device__ void load(const float *p) {
-        const float4 t = *(const float4 *)p;
-        v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-    }
+    __device__ float get(int i) const { return v[i]; }
 };
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-template <> struct Row<2, true> {
-    float v[2];
+template <int VEC> struct Row<VEC, true> {
+    static constexpr int W = VEC >= 2 ? VEC / 2 : 1;
+    uint32_t w[W];
     __device__ void load(const uint16_t *p) {
-        const uint32_t w = *(const uint32_t *)p;
-        v[0] = bf16_lo(w); v[1] = bf16_hi(w);
+        if constexpr (VEC == 8) {
+            const uint4 t = *(const uint4 *)p;
+            w[0] = t.x; w[1] = t.y; w[2] = t.z; w[3] = t.w;
+        } else if constexpr (VEC == 4) {
+            const uint2 t = *(const uint2 *)p;
+            w[0] = t.x; w[1] = t.y;
+        } else if constexpr (VEC == 2) {
+            w[0] = *(const uint32_t *)p;
+        } else {
+            w[0] = (uint32_t)(*p);
+        }
     }
-};
-template <> struct Row<4, true> {
-    float v[4];
-    __device__ void load(const uint16_t *p) {
-        const uint2 w = *(const uint2 *)p;
-        v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x); v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
+    __device__ float get(int i) const {
+        if constexpr (VEC == 1) return __uint_as_float(w[0] << 16);
+        return (i & 1) ? bf16_hi(w[i >> 1]) : bf16_lo(w[i >> 1]);
     }
-};
-template <> struct Row<8, true> {
-    float v[8];
-    __device__ void load(const uint16_t *p) {
-        const uint4 w = *(const uint4 *)p;
-        v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x); v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
-        v[4] = bf16_lo(w.z); v[5] = bf16_hi(w.z); v[6] = bf16_lo(w.w); v[7] = bf16_hi(w.w);
-    }
-};
-template <> struct Row<1, true> {
-    float v[1];
-    __device__ void load(const uint16_t *p) { v[0] = __uint_as_float((uint32_t)(*p) << 16); }
 };
 
 __device__ __forceinline__ uint16_t to_bf16(float f) {
@@ -266,24 +264,26 @@ void spmm_main(
 #pragma unroll
     for (int t = 0; t < CT; ++t) cok[t] = cbase + t * 64 * VEC < k;
 
+    // edge positions relative to p0 (32-bit: nnz < 2^31), as staged in LDS
+    const int q0 = (int)p0;
     int32_t hrow = -1, trow = -1;
     for (int r = r0; r <= r1 && r < n_rows; ++r) {
-        const int64_t rb = r_ptr[r - r0], re = r_ptr[r - r0 + 1];
+        const int rb = r_ptr[r - r0], re = r_ptr[r - r0 + 1];
         const bool complete = r < r1;
-        const int64_t pb = p0 > rb ? p0 : rb;
-        const int64_t pe = complete ? re : p1;
+        const int pb = (q0 > rb ? q0 : rb) - q0;
+        const int pe = (complete ? re : (int)p1) - q0;
         float acc[CT][VEC];
 #pragma unroll
         for (int t = 0; t < CT; ++t)
 #pragma unroll
             for (int v = 0; v < VEC; ++v) acc[t][v] = 0.0f;
 
-        int64_t p = pb;
+        int p = pb;
         for (; p + kUnroll <= pe; p += kUnroll) {
             int32_t j[kUnroll];
             float w[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) { j[u] = e_idx[p + u - p0]; w[u] = e_val[p + u - p0]; }
+            for (int u = 0; u < kUnroll; ++u) { j[u] = e_idx[p + u]; w[u] = e_val[p + u]; }
             Row<VEC, BF16> x[kUnroll][CT];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
@@ -296,22 +296,22 @@ void spmm_main(
                 for (int t = 0; t < CT; ++t)
                     if (cok[t])
 #pragma unroll
-                        for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(w[u], x[u][t].v[v], acc[t][v]);
+                        for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(w[u], x[u][t].get(v), acc[t][v]);
         }
         for (; p < pe; ++p) {
-            const int32_t j = e_idx[p - p0];
-            const float w = e_val[p - p0];
+            const int32_t j = e_idx[p];
+            const float w = e_val[p];
 #pragma unroll
             for (int t = 0; t < CT; ++t)
                 if (cok[t]) {
                     Row<VEC, BF16> x;
                     x.load(X + (int64_t)j * ldx + cbase + t * 64 * VEC);
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(w, x.v[v], acc[t][v]);
+                    for (int v = 0; v < VEC; ++v) acc[t][v] = fmaf(w, x.get(v), acc[t][v]);
                 }
         }
 
-        const bool started = (r > r0) || (p0 == rb);
+        const bool started = (r > r0) || (q0 == rb);
         if (complete && started) {
 #pragma unroll
             for (int t = 0; t < CT; ++t)
