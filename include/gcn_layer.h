@@ -193,7 +193,9 @@ int gcn_layer_bwd(const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f
  *                    G = (sigmoid(X) - targets) / (nC)
  *   loss [1] (device scalar), dHL = G W_pred^T [n x f] (lddhl),
  *   dW_pred = HL^T G [f x C], db_pred = sum_i G [C].
- * The pointer not used by `kind` may be NULL. */
+ * The pointer not used by `kind` may be NULL.  With n = 0 the loss, dW_pred
+ * and db_pred are written as 0 (sums over no rows), and HL, dHL, labels and
+ * targets may be NULL. */
 size_t gcn_loss_workspace_bytes(int32_t n, int32_t f, int32_t C, gcn_prec prec);
 int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl,
                   const float *W_pred, const float *b_pred, int32_t C,

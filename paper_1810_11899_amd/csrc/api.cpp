@@ -721,8 +721,8 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     REQUIRE(kind == GCN_SOFTMAX_CE || kind == GCN_SIGMOID_BCE, GCN_EINVAL, "gcn_loss_grad: bad kind %d",
             kind);
     REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "gcn_loss_grad: bad precision");
-    REQUIRE(W_pred && b_pred && loss && dHL && dW_pred && db_pred, GCN_EINVAL, "gcn_loss_grad: null pointer");
-    REQUIRE(n == 0 || HL, GCN_EINVAL, "gcn_loss_grad: null HL");
+    REQUIRE(W_pred && b_pred && loss && dW_pred && db_pred, GCN_EINVAL, "gcn_loss_grad: null pointer");
+    REQUIRE(n == 0 || (HL && dHL), GCN_EINVAL, "gcn_loss_grad: null HL or dHL");
     REQUIRE(n == 0 || (kind == GCN_SOFTMAX_CE ? labels != nullptr : targets != nullptr), GCN_EINVAL,
             "gcn_loss_grad: null labels/targets");
     const LossPlan pl = plan_loss(n, f, C, prec);

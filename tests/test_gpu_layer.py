@@ -158,6 +158,36 @@ def compare_step(run: dict, ref: oracle.StepResult, tol=TOL_F32):
     return errs
 
 
+@pytest.mark.parametrize("prec", [B.GCN_F32, B.GCN_BF16])
+@pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
+def test_zero_vertex_subgraph(prec, order, ws):
+    """n = 0: every call succeeds; the gradients and the loss are sums over no
+    rows, so they come out as zeros (written over NaN-filled buffers)."""
+    f_in, h, C = 48, 32, 9
+    rng = np.random.default_rng(5)
+    A = B.DeviceCSR.from_host(0, 0, np.zeros(1, np.int32), np.zeros(0, np.int32), np.zeros(0, np.float32))
+    AT = B.gcn_csr_transpose(A, ws)
+    assert AT.nnz == 0 and AT.indptr.cpu().tolist() == [0]
+    e = lambda *shape: torch.empty(shape, device="cuda")
+    nan = lambda *shape: torch.full(shape, float("nan"), device="cuda")
+    Ws, Wn = dev(rng.standard_normal((f_in, h)) * 0.1), dev(rng.standard_normal((f_in, h)) * 0.1)
+    b = dev(_bias(h, 1))
+    H, Y = e(0, f_in), e(0, 2 * h)
+    nb = B.gcn_layer_saved_bytes(0, f_in, h, order, prec)
+    saved = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda") if nb else None
+    B.gcn_layer_fwd(A, H, Ws, Wn, b, Y, saved, order, ws, prec)
+    dWs, dWn, db = nan(f_in, h), nan(f_in, h), nan(2 * h)
+    B.gcn_layer_bwd(A, AT, H, Ws, Wn, Y, saved, e(0, 2 * h), e(0, f_in), dWs, dWn, db, order, ws, prec)
+    Wp, bp = dev(rng.standard_normal((2 * h, C)) * 0.1), dev(np.zeros(C, np.float32))
+    loss, dWp, dbp = nan(1), nan(2 * h, C), nan(C)
+    B.gcn_loss_grad(Y, Wp, bp, B.GCN_SOFTMAX_CE, torch.empty(0, dtype=torch.int32, device="cuda"), None, loss,
+                    e(0, 2 * h), dWp, dbp, ws, prec)
+    torch.cuda.synchronize()
+    for name, t in (("dW_self", dWs), ("dW_neigh", dWn), ("dbias", db), ("loss", loss), ("dW_pred", dWp),
+                    ("db_pred", dbp)):
+        assert torch.count_nonzero(t).item() == 0 and not torch.isnan(t).any().item(), name
+
+
 @pytest.mark.parametrize("cfg", [0, 1, 2])
 def test_config_step_parity(cfg):
     wl = synth.config(cfg)
