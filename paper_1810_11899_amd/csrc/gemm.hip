@@ -94,6 +94,17 @@ __device__ __forceinline__ bool decode_block(const DevArgs &a, BlockCoord &c) {
 // Element type: float (fp32 path) or uint16_t (bf16 bits).
 template <typename T> __device__ __forceinline__ T zero_elem() { return T(0); }
 
+#ifndef GCN_GEMM_SWZ
+#define GCN_GEMM_SWZ 1
+#endif
+// Column swizzle of the float32 operand tiles: row k of lds[k][x] holds
+// element x at x ^ kswz(k).  The transposing store of an operand contiguous
+// along k (four consecutive k of one x per thread, eight consecutive x per
+// half-wavefront) then puts the half-wavefront's 32 values in 32 distinct
+// banks: with rows 132 floats apart, k-groups 0/8 and 4/12 would otherwise
+// share banks.  Reads of 32 consecutive x in one row stay conflict-free.
+__device__ __forceinline__ int kswz(int k) { return GCN_GEMM_SWZ ? ((k >> 3) & 1) << 3 : 0; }
+
 // Tile of one operand, BK x XT elements, kept k-major in LDS: lds[k][x].
 //   KMAJOR: element (x, k) sits at ptr[k*ld + x]   (contiguous along x)
 //   else  : element (x, k) sits at ptr[x*ld + k]   (contiguous along k)
@@ -179,10 +190,10 @@ struct TileLoader {
             coords(i, x, k);
             const T *t = (const T *)&reg[i];
             if (KMAJOR) {
-                *(V *)&lds[k][x] = reg[i];
+                *(V *)&lds[k][sizeof(T) == 4 ? x ^ kswz(k) : x] = reg[i];
             } else {
 #pragma unroll
-                for (int e = 0; e < E; ++e) lds[k + e][x] = t[e];
+                for (int e = 0; e < E; ++e) lds[k + e][sizeof(T) == 4 ? x ^ kswz(k + e) : x] = t[e];
             }
         }
     }
@@ -301,9 +312,9 @@ void gemm_kernel(DevArgs args) {
         float a0[FM], b0[FN], a1[FM], b1[FN];
         auto rd = [&](float *a, float *b, int kr) {
 #pragma unroll
-            for (int i = 0; i < FM; ++i) a[i] = As[buf][kr][wm * WTM + i * 32 + (lane & 31)];
+            for (int i = 0; i < FM; ++i) a[i] = As[buf][kr][(wm * WTM + i * 32 + (lane & 31)) ^ kswz(kr)];
 #pragma unroll
-            for (int j = 0; j < FN; ++j) b[j] = Bs[buf][kr][wn * WTN + j * 32 + (lane & 31)];
+            for (int j = 0; j < FN; ++j) b[j] = Bs[buf][kr][(wn * WTN + j * 32 + (lane & 31)) ^ kswz(kr)];
         };
         auto mma = [&](const float *a, const float *b) {
 #pragma unroll
