@@ -231,10 +231,14 @@ LayerPlan plan_layer(int32_t n, int32_t nnz, int32_t f_in, int32_t h, int order,
         p.bwd_gemm = gemm_workspace_bytes(2, pr, gemm_pick_split(2, pr, true));
     }
     if (dH) {  // the input-gradient product reuses the weight-gradient partials' region
+        // the same problems gcn_layer_bwd forms: with G one product of two
+        // K = h segments ([dZ_s || G] [W_self || W_neigh]^T), else two of K = h
+        // (the split count depends on the segments' k-tiles)
         GemmProblem d[2] = {};
         d[0].M = d[1].M = n;
         d[0].N = d[1].N = f_in;
-        d[0].seg[0].K = d[1].seg[0].K = p.need_G ? 2 * h : h;
+        d[0].seg[0].K = d[1].seg[0].K = h;
+        if (p.need_G) d[0].seg[1].K = h;
         const int nd = p.need_G ? 1 : 2;
         p.bwd_gemm = std::max(p.bwd_gemm, gemm_workspace_bytes(nd, d, gemm_pick_split(nd, d, false)));
     }

@@ -281,6 +281,50 @@ def test_model_step_matches_separate_calls(case):
             assert fused and not same, ("unsplit input-gradient product writes dZ", i)
 
 
+def _random_model(seed):
+    """A seeded random model and subgraph: 1-3 layers, widths 8-300 (odd ones
+    included), random orders, head and precision."""
+    r = np.random.default_rng(1000 + seed)
+    n = int(r.integers(200, 5000))
+    L = int(r.integers(1, 4))
+    dims, f = [], int(r.integers(8, 301))
+    for _ in range(L):
+        h = int(r.integers(4, 151))
+        dims.append((f, h))
+        f = 2 * h
+    head = [None, "ce", "bce"][int(r.integers(0, 3))]
+    classes = int(r.integers(2, 120)) if head else 0
+    wl = synth.custom(n, ["er", "rmat"][int(r.integers(0, 2))], int(r.integers(2, 30)), dims, head=head,
+                      classes=classes, seed=seed)
+    orders = [int(r.integers(0, 2)) for _ in range(L)]
+    prec = B.GCN_BF16 if r.random() < 0.4 else B.GCN_F32
+    return wl, orders, prec
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_model_step_random_models(seed):
+    """Seeded random models through gcn_model_step (fused mask epilogues where
+    they apply, split and unsplit products, ragged tiles): float32 against the
+    oracle (kink envelope), both precisions against the separate calls."""
+    wl, orders, prec = _random_model(seed)
+    r = StepRunner(wl, prec=prec, orders=orders, first_layer_dH=True)
+    print(f"seed {seed}: n={wl.n} nnz={wl.graph.nnz} dims={[l for l in wl.spec.layers]} head={wl.spec.head} "
+          f"C={wl.spec.classes} orders={orders} prec={prec}", flush=True)
+    r.step_calls()
+    a = r.results()
+    r.step()
+    torch.cuda.synchronize()
+    b = r.results()
+    for key in ("Y", "dW_self", "dW_neigh"):
+        for i, (x, y) in enumerate(zip(a[key], b[key])):
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), (key, i)
+    assert np.array_equal(a["dH"][0].view(np.uint32), b["dH"][0].view(np.uint32))
+    for i, (x, y) in enumerate(zip(a["db"], b["db"])):
+        assert rel_inf(y, x) <= 1e-6, ("db", i)
+    if prec == B.GCN_F32:
+        compare_step(b, oracle.step(wl, first_layer_dH=True, envelope=True))
+
+
 @pytest.mark.parametrize("graph", ["empty", "star"])
 def test_model_step_degenerate_graphs_match_oracle(graph):
     """The whole step through gcn_model_step on a graph without edges (every
