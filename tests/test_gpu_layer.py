@@ -301,11 +301,13 @@ def _random_model(seed):
     return wl, orders, prec
 
 
-@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("seed", range(48))
 def test_model_step_random_models(seed):
     """Seeded random models through gcn_model_step (fused mask epilogues where
     they apply, split and unsplit products, ragged tiles): float32 against the
-    oracle (kink envelope), both precisions against the separate calls."""
+    oracle (kink envelope), both precisions against the separate calls.
+    (Seed 12 found a split-K workspace that the input-gradient plan sized for
+    one split too few.)"""
     wl, orders, prec = _random_model(seed)
     r = StepRunner(wl, prec=prec, orders=orders, first_layer_dH=True)
     print(f"seed {seed}: n={wl.n} nnz={wl.graph.nnz} dims={[l for l in wl.spec.layers]} head={wl.spec.head} "
