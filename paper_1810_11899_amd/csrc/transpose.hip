@@ -215,12 +215,11 @@ __global__ __launch_bounds__(kTB) void finalize_kernel(int32_t nnz, const int32_
 
 // Symmetric pattern: A^T has A's row pointers and indices; the value at
 // (row j, column i) is A's value at (i, j).
-// Pass 1, one wavefront per row i: the row id of every entry, and whether the
-// row's values are all the same bits (true of every row of a mean
-// aggregation matrix, Sec. II), in which case that value is A(i, j) for
-// every j.
+// Pass 1, one wavefront per row i: whether the row's values are all the same
+// bits (true of every row of a mean aggregation matrix, Sec. II), in which
+// case that value is A(i, j) for every j.
 __global__ __launch_bounds__(kTB) void sym_rows_kernel(int32_t n, const int32_t *__restrict__ indptr,
-                                                       const float *__restrict__ vals, int32_t *__restrict__ rowid,
+                                                       const float *__restrict__ vals,
                                                        uint32_t *__restrict__ rowval, int32_t *__restrict__ rowconst) {
     const int64_t i = (int64_t)blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
     if (i >= n) return;
@@ -237,15 +236,9 @@ __global__ __launch_bounds__(kTB) void sym_rows_kernel(int32_t n, const int32_t 
 #pragma unroll
         for (int u = 0; u < U; ++u) v[u] = __float_as_uint(vals[p + 64 * u]);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            rowid[p + 64 * u] = (int32_t)i;
-            same = same && (v[u] == first);
-        }
+        for (int u = 0; u < U; ++u) same = same && (v[u] == first);
     }
-    for (; p < e; p += 64) {
-        rowid[p] = (int32_t)i;
-        same = same && (__float_as_uint(vals[p]) == first);
-    }
+    for (; p < e; p += 64) same = same && (__float_as_uint(vals[p]) == first);
     const bool all_same = __all(same);
     if (lane == 0) {
         rowval[i] = first;
@@ -254,23 +247,29 @@ __global__ __launch_bounds__(kTB) void sym_rows_kernel(int32_t n, const int32_t 
 }
 
 // Pass 2, one thread per entry p (row j, column i): the constant value of row
-// i, or a binary search for j in row i.  An index outside [0, n), or a missing
-// (i, j) found by the search, gives NaN.
+// i, or else j (the row holding p, by a search of indptr) and a binary search
+// for j in row i.  An index outside [0, n), or a missing (i, j) found by the
+// search, gives NaN.
 __global__ __launch_bounds__(kTB) void sym_vals_kernel(int32_t n, int32_t nnz, const int32_t *__restrict__ indptr,
                                                        const int32_t *__restrict__ indices,
                                                        const float *__restrict__ vals,
-                                                       const int32_t *__restrict__ rowid,
                                                        const uint32_t *__restrict__ rowval,
                                                        const int32_t *__restrict__ rowconst,
                                                        float *__restrict__ t_vals) {
     const int64_t stride = (int64_t)gridDim.x * kTB;
     for (int64_t p = (int64_t)blockIdx.x * kTB + threadIdx.x; p < nnz; p += stride) {
-        const int32_t i = indices[p], j = rowid[p];
+        const int32_t i = indices[p];
         float t = __int_as_float(0x7FC00000);
         if ((uint32_t)i < (uint32_t)n) {
             if (rowconst[i]) {
                 t = __uint_as_float(rowval[i]);
             } else {
+                int32_t a = 0, b = n;   // the last row r with indptr[r] <= p
+                while (a < b) {
+                    const int32_t mid = a + ((b - a + 1) >> 1);
+                    if (indptr[mid] <= p) a = mid; else b = mid - 1;
+                }
+                const int32_t j = a;
                 int32_t lo = indptr[i], hi = indptr[i + 1];   // first index >= j in row i
                 while (lo < hi) {
                     const int32_t mid = lo + ((hi - lo) >> 1);
@@ -385,26 +384,26 @@ int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *in
 }
 
 size_t transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz) {
-    return align256((size_t)nnz * 4) + 2 * align256((size_t)n * 4) + 256;
+    (void)nnz;
+    return 2 * align256((size_t)n * 4) + 256;
 }
 
 int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, const int32_t *indices,
                             const float *vals, float *t_vals, void *ws, size_t ws_bytes, hipStream_t s) {
     if (n == 0 || nnz == 0) return GCN_OK;
     Arena ar(ws, ws_bytes);
-    int32_t *rowid = ar.take<int32_t>(nnz);
     uint32_t *rowval = ar.take<uint32_t>(n);
     int32_t *rowconst = ar.take<int32_t>(n);
-    if (!rowid || !rowval || !rowconst) {
+    if (!rowval || !rowconst) {
         set_error("csr_transpose_symmetric: workspace too small (%zu < %zu bytes)", ws_bytes,
                   transpose_symmetric_workspace_bytes(n, nnz));
         return GCN_EWORKSPACE;
     }
-    ProfScope ps(K_T_SYM, s, 0.0, (double)nnz * 20.0 + (double)n * 16.0);
+    ProfScope ps(K_T_SYM, s, 0.0, (double)nnz * 12.0 + (double)n * 16.0);
     hipLaunchKernelGGL(sym_rows_kernel, dim3((unsigned)((n + kTB / 64 - 1) / (kTB / 64))), dim3(kTB), 0, s, n,
-                       indptr, vals, rowid, rowval, rowconst);
+                       indptr, vals, rowval, rowconst);
     unsigned g = (unsigned)std::min<int64_t>(((int64_t)nnz + kTB - 1) / kTB, 16384);
-    hipLaunchKernelGGL(sym_vals_kernel, dim3(g), dim3(kTB), 0, s, n, nnz, indptr, indices, vals, rowid, rowval,
+    hipLaunchKernelGGL(sym_vals_kernel, dim3(g), dim3(kTB), 0, s, n, nnz, indptr, indices, vals, rowval,
                        rowconst, t_vals);
     GCN_LAUNCH_CHECK("transpose_symmetric kernels");
     return GCN_OK;
