@@ -407,7 +407,8 @@ size_t gcn_layer_workspace_bytes(int32_t n, int32_t nnz, int32_t f_in, int32_t h
 static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh,
                      const float *W_self, const float *W_neigh, const float *bias, int32_t h, float *Y, int32_t ldy,
                      void *saved, size_t saved_bytes_, gcn_order order, gcn_prec prec, void *ws, size_t ws_bytes,
-                     void *stream) {
+                     void *stream, const int32_t *bA = nullptr) {
+    // bA: A's merge-path row ranges (spmm_bounds), or NULL
     int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_fwd");
     if (rc) return rc;
     const int32_t n = A->n_rows;
@@ -451,7 +452,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         if (af) {
             void *sw = ar.take<char>(pl.fwd_spmm);
             rc = spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, H16, f_in, f_in, AGG16, f_in,
-                           EPI_STORE_BF16, nullptr, sw, pl.fwd_spmm, s);
+                           EPI_STORE_BF16, nullptr, sw, pl.fwd_spmm, s, bA);
             if (rc) return rc;
             if ((rc = transpose_bf16(n, f_in, AGG16, 1, f_in, AGG16T, n, s))) return rc;
             g[1].seg[0] = GemmSeg{AGG16, f_in, WnT, f_in, f_in};
@@ -470,7 +471,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
         if ((rc = gemm(L_NT, 2, g, 1, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s))) return rc;
         return spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, T16, h, h, Y + h, ldy, EPI_BIAS_RELU,
-                         bias + h, sw, pl.fwd_spmm, s);
+                         bias + h, sw, pl.fwd_spmm, s, bA);
     }
 
     GemmProblem g[2] = {};
@@ -485,7 +486,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         void *sw = ar.take<char>(pl.fwd_spmm);
         float *AGG = (float *)saved;
         rc = spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE, nullptr, sw,
-                      pl.fwd_spmm, s);
+                      pl.fwd_spmm, s, bA);
         if (rc) return rc;
         g[1].seg[0] = GemmSeg{AGG, f_in, W_neigh, h, f_in};
         g[1].C = Y + h;
@@ -504,7 +505,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
     void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
     if ((rc = gemm(L_NN, 2, g, 0, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s))) return rc;
     return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, T, h, h, Y + h, ldy, EPI_BIAS_RELU, bias + h, sw,
-                    pl.fwd_spmm, s);
+                    pl.fwd_spmm, s, bA);
 }
 
 static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H, int32_t f_in,
@@ -512,7 +513,8 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
                      const void *saved, size_t saved_bytes_, const float *dY, int32_t lddy, float *dH,
                      int32_t lddh, float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec,
                      void *ws, size_t ws_bytes, void *stream, bool dz_ready = false,
-                     float *below_dbias = nullptr) {
+                     float *below_dbias = nullptr, const int32_t *bAT = nullptr) {
+    // bAT: A^T's merge-path row ranges (spmm_bounds), or NULL
     // dz_ready: dY already holds dZ = dY * [Y > 0] (float32 with leading
     // dimension lddy, or bfloat16 n x 2h with leading dimension 2h) and dbias
     // is already written (by the producer of dY).  below_dbias: write dH
@@ -585,9 +587,9 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     // G = A^T dZ_n into the second half of P
     if (pl.need_G) {
         rc = bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)Zn, h, ldZn,
-                            Gp, ldG, EPI_STORE_BF16, nullptr, sw, pl.bwd_spmm, s)
+                            Gp, ldG, EPI_STORE_BF16, nullptr, sw, pl.bwd_spmm, s, bAT)
                 : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)Zn, h, ldZn, Gp,
-                           ldG, EPI_STORE, nullptr, sw, pl.bwd_spmm, s);
+                           ldG, EPI_STORE, nullptr, sw, pl.bwd_spmm, s, bAT);
         if (rc) return rc;
     }
     // a7: weight gradients, K = n, split-K
@@ -669,9 +671,9 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     else d[1].C = (float *)T2;
     if ((rc = gemm(L_NT, 2, d, bf, gemm_pick_split(2, d, false), gw, pl.bwd_gemm, s))) return rc;
     return bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)T2, f_in,
-                          f_in, dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s)
+                          f_in, dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s, bAT)
               : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)T2, f_in, f_in,
-                         dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s);
+                         dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s, bAT);
 }
 
 // ------------------------------------------------------------------ loss
@@ -888,7 +890,7 @@ size_t gcn_model_workspace_bytes(int32_t n, int32_t nnz, int32_t L, const gcn_la
     for (int32_t l = 0; l < L; ++l)
         b = std::max(b, plan_layer(n, nnz, layers[l].f_in, layers[l].h, layers[l].order, true, prec).total);
     if (head) b = std::max(b, plan_loss(n, 2 * layers[L - 1].h, head->C, prec).total);
-    return b;
+    return b + 2 * spmm_bounds_bytes(n, nnz);   // the row ranges of A and A^T, shared by the calls
 }
 
 namespace {
@@ -899,12 +901,32 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
                gcn_prec prec, void *ws, size_t ws_bytes, void *stream) {
     const int32_t n = A->n_rows;
     int rc;
+    // the merge-path row ranges of A and A^T, computed once for every SpMM of
+    // the step (they depend only on the row pointers; A^T shares A's when it
+    // shares A's row pointers), ahead of the calls' workspace
+    const size_t rb = spmm_bounds_bytes(n, A->nnz);
+    const int32_t *bA = nullptr, *bAT = nullptr;
+    if (rb) {
+        REQUIRE(ws && ws_bytes >= 2 * rb, GCN_EWORKSPACE, "gcn_model_step: workspace %zu bytes too small",
+                ws_bytes);
+        int32_t *ra = (int32_t *)ws;
+        int32_t *rt = AT->indptr == A->indptr ? ra : (int32_t *)((char *)ws + rb);
+        ws = (char *)ws + 2 * rb;
+        ws_bytes -= 2 * rb;
+        if (launch) {
+            hipStream_t s = as_stream(stream);
+            if ((rc = spmm_bounds(n, A->nnz, A->indptr, ra, s))) return rc;
+            if (rt != ra && (rc = spmm_bounds(n, AT->nnz, AT->indptr, rt, s))) return rc;
+        }
+        bA = ra;
+        bAT = rt;
+    }
     const float *H = H0;  // forward: layer l reads layer l-1's output
     int32_t ldh = ldh0;
     for (int32_t l = 0; l < L; ++l) {
         const gcn_layer_args &a = layers[l];
         if ((rc = layer_fwd(launch, A, H, a.f_in, ldh, a.W_self, a.W_neigh, a.bias, a.h, a.Y, a.ldy, a.saved,
-                            a.saved_bytes, a.order, prec, ws, ws_bytes, stream)))
+                            a.saved_bytes, a.order, prec, ws, ws_bytes, stream, bA)))
             return rc;
         H = a.Y;
         ldh = a.ldy;
@@ -933,7 +955,7 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         const bool fuse = l > 0 && dH_mask_fusable(n, a.f_in, a.h, a.order, prec);
         if ((rc = layer_bwd(launch, A, AT, Hin, a.f_in, ldin, a.W_self, a.W_neigh, a.h, a.Y, a.ldy, a.saved,
                             a.saved_bytes, g, ldg, a.dH, a.lddh, a.dW_self, a.dW_neigh, a.dbias, a.order, prec, ws,
-                            ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr)))
+                            ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr, bAT)))
             return rc;
         g = a.dH;
         ldg = a.lddh;

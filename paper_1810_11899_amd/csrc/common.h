@@ -91,14 +91,21 @@ struct SpmmPlan {
 };
 SpmmPlan spmm_plan(int32_t n_rows, int32_t nnz);
 size_t spmm_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k);
-// out[i, c] (epilogue) sum_p vals[p] * X[indices[p], c]
+// the merge-path row ranges of a CSR (first row of every wavefront's range,
+// spmm_plan(n_rows, nnz).waves + 1 entries), which depend only on indptr
+size_t spmm_bounds_bytes(int32_t n_rows, int32_t nnz);
+int spmm_bounds(int32_t n_rows, int32_t nnz, const int32_t *indptr, int32_t *bounds, hipStream_t s);
+// out[i, c] (epilogue) sum_p vals[p] * X[indices[p], c].  `bounds`: the row
+// ranges from spmm_bounds for this indptr, or NULL to compute them here.
 int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
              const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s);
+             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s,
+             const int32_t *bounds = nullptr);
 // same with bfloat16 rows of X (uint16 bits), float32 accumulation
 int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
               const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s);
+              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s,
+              const int32_t *bounds = nullptr);
 
 // GEMM on the matrix cores -----------------------------------------------------
 // C[M x N] = sum over up to two K-segments of op(A_s) op(B_s), then epilogue.

@@ -564,15 +564,15 @@ bool aligned(const void *p, int bytes) { return ((uintptr_t)p % (uintptr_t)bytes
 
 int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
              const float *vals, const void *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-             int epi, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
+             int epi, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
     if (n_rows <= 0 || k <= 0) return GCN_OK;
     const SpmmPlan pl = spmm_plan(n_rows, nnz);
     Arena ar(ws, ws_bytes);
     float *carry = ar.take<float>((size_t)2 * pl.waves * k);
     int32_t *hr = ar.take<int32_t>(pl.waves);
     int32_t *tr = ar.take<int32_t>(pl.waves);
-    int32_t *bnd = ar.take<int32_t>(pl.waves + 1);
-    if (!carry || !hr || !tr || !bnd) {
+    int32_t *bnd_ws = ar.take<int32_t>(pl.waves + 1);
+    if (!carry || !hr || !tr || !bnd_ws) {
         set_error("spmm: workspace too small (%zu < %zu bytes)", ws_bytes,
                   spmm_workspace_bytes(n_rows, nnz, k));
         return GCN_EWORKSPACE;
@@ -595,9 +595,13 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, cons
                          (double)n_rows * k * out_bytes;
     {
         ProfScope ps(bf16 ? K_SPMM_BF16 : K_SPMM, s, 2.0 * nnz * k, bytes);
-        hipLaunchKernelGGL(spmm_bounds_kernel, dim3((unsigned)((pl.waves + kWavesPerBlock) / kWavesPerBlock)),
-                           dim3(256), 0, s, n_rows, indptr, pl.items, pl.ipw, pl.waves, bnd);
-        GCN_LAUNCH_CHECK("spmm_bounds_kernel");
+        const int32_t *bnd = bounds;
+        if (!bnd) {
+            hipLaunchKernelGGL(spmm_bounds_kernel, dim3((unsigned)((pl.waves + kWavesPerBlock) / kWavesPerBlock)),
+                               dim3(256), 0, s, n_rows, indptr, pl.items, pl.ipw, pl.waves, bnd_ws);
+            GCN_LAUNCH_CHECK("spmm_bounds_kernel");
+            bnd = bnd_ws;
+        }
         if (sliced) {
             const SliceMap m = make_slice_map(k, pl.waves);
             hipLaunchKernelGGL(spmm_sliced, dim3((unsigned)slice_map_blocks(m)), dim3(256), 0, s, n_rows, indptr,
@@ -663,18 +667,33 @@ size_t spmm_workspace_bytes(int32_t n_rows, int32_t nnz, int32_t k) {
            align256((pl.waves + 1) * sizeof(int32_t)) + 256;
 }
 
+size_t spmm_bounds_bytes(int32_t n_rows, int32_t nnz) {
+    if (n_rows <= 0) return 0;
+    return align256((spmm_plan(n_rows, nnz).waves + 1) * sizeof(int32_t));
+}
+
+int spmm_bounds(int32_t n_rows, int32_t nnz, const int32_t *indptr, int32_t *bounds, hipStream_t s) {
+    if (n_rows <= 0) return GCN_OK;
+    const SpmmPlan pl = spmm_plan(n_rows, nnz);
+    ProfScope ps(K_SPMM_FIXUP, s, 0.0, (double)(pl.waves + 1) * 4.0);
+    hipLaunchKernelGGL(spmm_bounds_kernel, dim3((unsigned)((pl.waves + kWavesPerBlock) / kWavesPerBlock)),
+                       dim3(256), 0, s, n_rows, indptr, pl.items, pl.ipw, pl.waves, bounds);
+    GCN_LAUNCH_CHECK("spmm_bounds_kernel");
+    return GCN_OK;
+}
+
 int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
              const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
+             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
     return spmm_any(false, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
-                    ws, ws_bytes, s);
+                    ws, ws_bytes, s, bounds);
 }
 
 int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
               const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s) {
+              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
     return spmm_any(true, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
-                    ws, ws_bytes, s);
+                    ws, ws_bytes, s, bounds);
 }
 
 }  // namespace gcn
