@@ -39,16 +39,29 @@ class SamplerConfig:
     seed: int = 1
 
 
+def pad4(f: int) -> int:
+    return (f + 3) // 4 * 4
+
+
 class FlatModel:
     """Weights, biases and the prediction layer in one flat float32 buffer,
-    with gradient, first- and second-moment buffers of the same layout."""
+    with gradient, first- and second-moment buffers of the same layout.
+
+    The first layer's weights are stored with pad4(f_in) rows, the rows past
+    f_in zero: the features are stored with zero columns to the same width,
+    so those rows only ever meet zeros, get zero gradients and stay zero under
+    ADAM, and the model is the f_in-wide one exactly.  The padded width lets
+    the products take 16-byte loads (a width such as 602 is not a multiple of
+    four floats)."""
 
     def __init__(self, dims: List[Tuple[int, int]], classes: int, device, seed: int = 0):
         self.dims = list(dims)
         self.classes = classes
+        self.f0 = dims[0][0]
         shapes = []
-        for (f_in, h) in dims:
-            shapes += [(f_in, h), (f_in, h), (2 * h,)]
+        for li, (f_in, h) in enumerate(dims):
+            fs = pad4(f_in) if li == 0 else f_in
+            shapes += [(fs, h), (fs, h), (2 * h,)]
         shapes += [(2 * dims[-1][1], classes), (classes,)]
         self.shapes = shapes
         offs, o = [], 0
@@ -65,7 +78,10 @@ class FlatModel:
         host = np.zeros(o, dtype=np.float32)
         for i, sh in enumerate(shapes):
             if len(sh) == 2:
-                host[offs[i]:offs[i] + sh[0] * sh[1]] = synth.glorot(rg, sh[0], sh[1]).ravel()
+                rows = self.f0 if i < 2 else sh[0]      # the first layer's real rows
+                w = np.zeros(sh, np.float32)
+                w[:rows] = synth.glorot(rg, rows, sh[1])
+                host[offs[i]:offs[i] + sh[0] * sh[1]] = w.ravel()
         self.params.copy_(torch.from_numpy(host))
         self.step_count = 0
 
@@ -82,16 +98,23 @@ class FlatModel:
         k = 3 * len(self.dims)
         return self._view(buf, k), self._view(buf, k + 1)
 
+    def padding_rows(self):
+        """The first layer's padding rows of W_self and W_neigh (host copies)."""
+        p = self.params.cpu().numpy()
+        return [p[o:o + int(np.prod(sh))].reshape(sh)[self.f0:] for o, sh in zip(self.offsets[:2], self.shapes[:2])]
+
     def host_tensors(self):
-        """{name: numpy array} of the current parameters (for checks)."""
+        """{name: numpy array} of the current parameters (for checks), the first
+        layer's weights at their f_in rows."""
         p = self.params.cpu().numpy()
         out = {}
         names = []
         for li in range(len(self.dims)):
             names += [f"W_self{li}", f"W_neigh{li}", f"bias{li}"]
         names += ["W_pred", "b_pred"]
-        for nm, o, sh in zip(names, self.offsets, self.shapes):
-            out[nm] = p[o:o + int(np.prod(sh))].reshape(sh).copy()
+        for i, (nm, o, sh) in enumerate(zip(names, self.offsets, self.shapes)):
+            a = p[o:o + int(np.prod(sh))].reshape(sh)
+            out[nm] = (a[:self.f0] if i < 2 else a).copy()
         return out
 
 
@@ -132,7 +155,10 @@ class Trainer:
         if dims[0][0] != tg.X.shape[1]:
             raise ValueError("the first layer's width must match the attributes")
         self.G = B.DeviceCSR.from_host(g.n, g.n, g.indptr, g.indices, g.vals, device=self.dev)
-        self.X = torch.from_numpy(tg.X).to(self.dev)
+        # attributes stored pad4(f_in) wide, the extra columns zero (see FlatModel)
+        f0p = pad4(dims[0][0])
+        self.X = torch.zeros((g.n, f0p), dtype=torch.float32, device=self.dev)
+        self.X[:, :dims[0][0]].copy_(torch.from_numpy(tg.X))
         self.labels_all = torch.from_numpy(tg.labels).to(self.dev)
         self.classes = tg.classes
         self.params = B.gcn_sampler_plan(g.indptr, cfg.m, cfg.n, eta=cfg.eta, cap=cfg.cap, seed=cfg.seed)
@@ -154,14 +180,14 @@ class Trainer:
         self.next_id = 0
         # iteration buffers, sized for the largest subgraph (n vertices)
         self.ws = B.Workspace(d)
-        self.H0 = torch.empty((n, dims[0][0]), dtype=torch.float32, device=d)
+        self.H0 = torch.empty((n, f0p), dtype=torch.float32, device=d)
         self.lab = torch.empty(n, dtype=torch.int32, device=d)
         self.Y = [torch.empty((n, 2 * h), dtype=torch.float32, device=d) for (_, h) in dims]
         self.dH = [None] + [torch.empty((n, f), dtype=torch.float32, device=d) for (f, _) in dims[1:]]
         self.dHL = torch.empty((n, 2 * dims[-1][1]), dtype=torch.float32, device=d)
         self.saved = []
-        for (f, h), o in zip(dims, self.orders):
-            nb = B.gcn_layer_saved_bytes(n, f, h, o, prec)
+        for li, ((f, h), o) in enumerate(zip(dims, self.orders)):
+            nb = B.gcn_layer_saved_bytes(n, f0p if li == 0 else f, h, o, prec)
             self.saved.append(torch.empty(max(nb, 256), dtype=torch.uint8, device=d) if nb else None)
         self._alloc_edges(self.edge_cap)
         self.losses = torch.zeros(1 << 16, dtype=torch.float32, device=d)

@@ -73,9 +73,13 @@ def replay_on_oracle(tg, dims, cfg, params, init, ids, lr):
     return np.array(losses), P
 
 
-def test_training_run_matches_oracle_replay():
-    tg = synth.training_graph(3000, 16, 24, 7, seed=3)
-    dims = [(24, 16), (32, 16)]
+@pytest.mark.parametrize("f", [24, 23])
+def test_training_run_matches_oracle_replay(f):
+    """f = 23: the trainer stores the attributes and the first layer's weights
+    24 wide (zero padding); the padding rows must stay zero and the run must
+    replay the 23-wide model."""
+    tg = synth.training_graph(3000, 16, f, 7, seed=3)
+    dims = [(f, 16), (32, 16)]
     cfg = SamplerConfig(m=40, n=300, eta=2.0, cap=20, pool=3, seed=5)
     tr = Trainer(tg, dims, cfg, lr=0.01)
     init = tr.model.host_tensors()
@@ -91,6 +95,8 @@ def test_training_run_matches_oracle_replay():
     final = tr.model.host_tensors()
     for k, v in final.items():
         assert rel_inf(v, ref_P[k]) <= 1e-3, k
+    for pad in tr.model.padding_rows():
+        assert pad.size == (24 - f) * 16 and not np.any(pad), "padding rows stay zero"
 
 
 def test_training_loss_decreases():
