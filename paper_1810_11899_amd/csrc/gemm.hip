@@ -783,6 +783,9 @@ constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU
 #ifndef GCN_BIG_WAVES
 #define GCN_BIG_WAVES 8
 #endif
+#ifndef GCN_BIG_READS_PER_MFMA
+#define GCN_BIG_READS_PER_MFMA 3
+#endif
 constexpr int kBigWaves = GCN_BIG_WAVES;
                  // 4 (2 x 2) or 8 (2 x 4)
 constexpr int kBigThreads = 64 * kBigWaves;
@@ -795,6 +798,17 @@ __device__ __forceinline__ int bigswz(int r) { return (r >> 2) & 3; }
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// scheduling groups: one matrix instruction, then PER LDS reads (the last
+// group takes the remainder of TOT), for groups Q .. NG-1
+template <int Q, int NG, int PER, int TOT>
+__device__ __forceinline__ void sched_reads() {
+    if constexpr (Q < NG) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, Q + 1 < NG ? PER : TOT - Q * PER, 0);
+        sched_reads<Q + 1, NG, PER, TOT>();
+    }
 }
 
 __global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(kBigWaves / 4)))
@@ -856,52 +870,114 @@ void gemm_bf16_big_kernel(DevArgs args) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
+    // tile t goes to stage t % kBigStages
+    auto issue_tile = [&](int t) { issue(kt_begin + t, t % kBigStages); };
 #pragma unroll
     for (int st = 0; st < kBigStages - 1; ++st)
-        if (st < ntiles) issue(kt_begin + st, st);
+        if (st < ntiles) issue_tile(st);
 
     constexpr int G = 2 * kBigQ;   // loads per tile per wavefront
-    for (int t = 0; t < ntiles; ++t) {
-        // the loads of tile t are done when at most the later tiles' loads
-        // are still outstanding
-        const int later = min(ntiles - 1 - t, kBigStages - 2);
+    // Software pipeline over the two 16-k steps of a stage.  The operand
+    // fragments of one k-step are read from LDS while the products of the
+    // other run (the reads are interleaved with the matrix instructions), so
+    // the LDS reads and the tile copies overlap the matrix-core time instead
+    // of adding to it.  The barrier that publishes tile t+1 sits between
+    // tile t's two k-steps:
+    //   f0 = k-step 0 of tile t (in registers)
+    //   products(f0) while f1 <- k-step 1 of tile t
+    //   wait for tile t+1, barrier, copy tile t+3
+    //   products(f1) while f0 <- k-step 0 of tile t+1
+    // A stage is refilled only after every wavefront has consumed (not just
+    // issued) its last read of that stage: stage (t+3) % 4 held tile t-1,
+    // whose reads fed tile t-1's products.
+    constexpr int KS = kBigBK / 16;
+    static_assert(KS == 2, "the pipeline alternates two k-steps per stage");
+    static_assert(kBigStages >= 3, "tile t+1 must be in flight behind tile t");
+    bf16x8 fa[2][kBigFM], fb[2][kBigFN];
+    auto read_frags = [&](int stage, int ks, bf16x8 (&a)[kBigFM], bf16x8 (&b)[kBigFN]) {
+        const uint16_t *As = lds[stage][0];
+        const uint16_t *Bs = lds[stage][1];
+        const int c = 2 * ks + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < kBigFM; ++i) {
+            const int r = wm * kBigWTM + i * 32 + (lane & 31);
+            a[i] = *(const bf16x8 *)&As[(r * 4 + (c ^ bigswz(r))) * 8];
+        }
+#pragma unroll
+        for (int j = 0; j < kBigFN; ++j) {
+            const int r = wn * kBigWTN + j * 32 + (lane & 31);
+            b[j] = *(const bf16x8 *)&Bs[(r * 4 + (c ^ bigswz(r))) * 8];
+        }
+    };
+    auto products = [&](const bf16x8 (&a)[kBigFM], const bf16x8 (&b)[kBigFN]) {
+#pragma unroll
+        for (int i = 0; i < kBigFM; ++i)
+#pragma unroll
+            for (int j = 0; j < kBigFN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+    // the next k-step's LDS reads go out behind the first few products, so
+    // they have the rest of the k-step to land
+    constexpr int kReads = kBigFM + kBigFN;
+    constexpr int kReadsPer = GCN_BIG_READS_PER_MFMA;
+    constexpr int kReadGroups = (kReads + kReadsPer - 1) / kReadsPer;
+    static_assert(kReadGroups <= kBigFM * kBigFN, "a product ahead of every read group");
+    auto interleave = [&]() {
+        sched_reads<0, kReadGroups, kReadsPer, kReads>();
+        __builtin_amdgcn_sched_group_barrier(0x008, kBigFM * kBigFN - kReadGroups, 0);
+    };
+    // the loads of a tile are done when at most `later` tiles' loads issued
+    // after it are still outstanding; then a bare s_barrier: the fence of
+    // __syncthreads would also wait for those later loads, which is the
+    // latency the ring hides.  The empty asm statements keep the compiler
+    // from moving LDS accesses across it.
+    auto barrier_after_vmcnt = [&]() {
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    };
+    // wait until at most `later` tiles' copies (issued after the awaited
+    // tile) are outstanding
+    auto wait_tile = [&](int later) {
         if (later >= 3) wait_vmcnt<3 * G>();
         else if (later == 2) wait_vmcnt<2 * G>();
         else if (later == 1) wait_vmcnt<G>();
         else wait_vmcnt<0>();
-        // every wavefront's part of tile t has landed and tile t-1's stage is
-        // free.  A bare s_barrier: the fence of __syncthreads would also wait
-        // for the later tiles' loads, which is the latency the ring hides.
-        // The empty asm statements keep the compiler from moving LDS accesses
-        // across it.
-        asm volatile("" ::: "memory");
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");
-        if (t + kBigStages - 1 < ntiles) issue(kt_begin + t + kBigStages - 1, (t + kBigStages - 1) % kBigStages);
-        const uint16_t *As = lds[t % kBigStages][0];
-        const uint16_t *Bs = lds[t % kBigStages][1];
-#pragma unroll
-        for (int ks = 0; ks < kBigBK / 16; ++ks) {
-            const int c = 2 * ks + (lane >> 5);
-            bf16x8 a[kBigFM], b[kBigFN];
-#pragma unroll
-            for (int i = 0; i < kBigFM; ++i) {
-                const int r = wm * kBigWTM + i * 32 + (lane & 31);
-                a[i] = *(const bf16x8 *)&As[(r * 4 + (c ^ bigswz(r))) * 8];
-            }
-#pragma unroll
-            for (int j = 0; j < kBigFN; ++j) {
-                const int r = wn * kBigWTN + j * 32 + (lane & 31);
-                b[j] = *(const bf16x8 *)&Bs[(r * 4 + (c ^ bigswz(r))) * 8];
-            }
-            GCN_PRIO_UP();
-#pragma unroll
-            for (int i = 0; i < kBigFM; ++i)
-#pragma unroll
-                for (int j = 0; j < kBigFN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-            GCN_PRIO_DOWN();
+    };
+    auto half0 = [&](int t) {   // products of k-step 0 of tile t, reads of its k-step 1
+        read_frags(t % kBigStages, 1, fa[1], fb[1]);
+        products(fa[0], fb[0]);
+        interleave();
+    };
+    auto half1 = [&](int t) {   // products of k-step 1 of tile t, reads of k-step 0 of tile t+1
+        // (on the last tile the read is of a stale stage, in bounds and unused)
+        read_frags((t + 1) % kBigStages, 0, fa[0], fb[0]);
+        products(fa[1], fb[1]);
+        interleave();
+    };
+    if (ntiles > 0) {
+        wait_tile(min(ntiles - 1, kBigStages - 2));   // tile 0
+        barrier_after_vmcnt();
+        read_frags(0, 0, fa[0], fb[0]);
+    }
+    // Steady state: tile t+1 is awaited with tiles t+2 .. t+stages-2 still in
+    // flight, then tile t+stages-1 is copied.  No branches in this loop.
+    int t = 0;
+    for (; t < ntiles - kBigStages + 1; ++t) {
+        half0(t);
+        wait_vmcnt<(kBigStages - 3) * G>();
+        barrier_after_vmcnt();
+        issue_tile(t + kBigStages - 1);
+        half1(t);
+    }
+    // The last tiles: nothing left to copy, fewer copies in flight.
+    for (; t < ntiles; ++t) {
+        half0(t);
+        if (t + 1 < ntiles) {
+            wait_tile(min(ntiles - 2 - t, kBigStages - 3));
+            barrier_after_vmcnt();
         }
+        half1(t);
     }
 
     const bool to_partial = P.split > 1;
@@ -1027,17 +1103,20 @@ void gemm_bf16_big_kernel(DevArgs args) {
         // per half: the 8 wavefronts' sums of each column, in order; the
         // half's rows are column-sum row 2 * tm + h (128-row tiles)
         static_assert(16 * kBigT * sizeof(float) <= sizeof(lds), "column sums fit the ring");
-        static_assert(kBigThreads == 2 * kBigT, "one thread per (half, column)");
+        static_assert((2 * kBigT) % kBigThreads == 0, "whole (half, column) sweeps");
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int e = 0; e < 4; ++e) stg[(h * kBigWaves + wave) * kBigT + 4 * lane + e] = cs[h][e];
         __syncthreads();
-        const int h = (int)threadIdx.x / kBigT, c = (int)threadIdx.x % kBigT;
-        float t = 0.0f;
 #pragma unroll
-        for (int w = 0; w < kBigWaves; ++w) t += stg[(h * kBigWaves + w) * kBigT + c];
-        if (m0 + h * 128 <= Mlast && n0 + c <= Nlast) P.colpart[(int64_t)(2 * bc.tm + h) * P.N + n0 + c] = t;
+        for (int idx = (int)threadIdx.x; idx < 2 * kBigT; idx += kBigThreads) {
+            const int h = idx / kBigT, c = idx % kBigT;
+            float t = 0.0f;
+#pragma unroll
+            for (int w = 0; w < kBigWaves; ++w) t += stg[(h * kBigWaves + w) * kBigT + c];
+            if (m0 + h * 128 <= Mlast && n0 + c <= Nlast) P.colpart[(int64_t)(2 * bc.tm + h) * P.N + n0 + c] = t;
+        }
     }
 }
 
