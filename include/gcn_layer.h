@@ -56,7 +56,11 @@ typedef enum {
 /* Arithmetic of the dense transforms and the gather.
  * GCN_F32 : float32 operands, float32 accumulation.
  * GCN_BF16: operands rounded to bfloat16 (round-to-nearest-even), float32
- *           accumulation; inputs and outputs at the boundary stay float32.  */
+ *           accumulation; inputs and outputs at the boundary stay float32.
+ *           The ReLU derivative is taken on the bfloat16-rounded layer
+ *           output, the operand the next layer reads: dZ = dY * [bf16(Y) > 0],
+ *           which is dY * [Y > 2^-134] (it drops only outputs below half the
+ *           smallest bfloat16 subnormal).  */
 typedef enum { GCN_F32 = 0, GCN_BF16 = 1 } gcn_prec;
 
 /* Grouping of the neighbour branch, (A H) W_neigh vs A (H W_neigh).  Equal in

@@ -574,7 +574,7 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     if (!dz_ready) {
         if (bf)
             rc = relu_bwd(n, h, dY, lddy, Y, ldy, nullptr, ldP, nullptr, ldZn, (uint16_t *)P, (uint16_t *)ZnW,
-                          dbias, rw, pl.bwd_relu, s);
+                          dbias, rw, pl.bwd_relu, s, kBf16ReluThreshold);
         else
             rc = relu_bwd(n, h, dY, lddy, Y, ldy, (float *)P, ldP, (float *)ZnW, ldZn, nullptr, nullptr, dbias, rw,
                           pl.bwd_relu, s);
@@ -647,13 +647,19 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
         d.C = dH;
         d.ldc = lddh;
         if (below_dbias) {  // dZ of the layer below, and its bias gradient
-            d.mask = H;
-            d.ldm = ldh;
             d.colpart = cp;
             if (bf) {
+                // the layer's bfloat16 input rows (saved by the forward pass)
+                // are the mask: [bf16(H) > 0] is the relu_bwd rule of the
+                // bfloat16 path, [H > 2^-134]
+                d.mask16 = (const uint16_t *)saved;
+                d.ldm = f_in;
                 d.C = nullptr;
                 d.C16 = (uint16_t *)dH;
                 d.ldc = f_in;
+            } else {
+                d.mask = H;
+                d.ldm = ldh;
             }
         }
         if ((rc = gemm(L_NT, 1, &d, bf, gemm_pick_split(1, &d, false), gw, pl.bwd_gemm, s))) return rc;
@@ -803,13 +809,16 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     }
     if ((rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s))) return rc;
     if (below_dbias) {
-        d.mask = HL;
-        d.ldm = ldhl;
         d.colpart = cp;
         if (bf) {
+            d.mask16 = HL16;   // [bf16(HL) > 0], as in relu_bwd's bfloat16 rule
+            d.ldm = f;
             d.C = nullptr;
             d.C16 = (uint16_t *)dHL;
             d.ldc = f;
+        } else {
+            d.mask = HL;
+            d.ldm = ldhl;
         }
     }
     if ((rc = gemm(L_NT, 1, &d, bf, 1, nullptr, 0, s))) return rc;

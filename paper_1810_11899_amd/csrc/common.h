@@ -132,6 +132,9 @@ struct GemmProblem {
     // float32 kernel, unsplit only: C[i][j] is kept where mask[i][j] > 0 and
     // set to 0 elsewhere (leading dim ldm), after bias and ReLU
     const float *mask;
+    // bfloat16 kernels: the mask as bfloat16 bits, same rule and leading dim
+    // (a bfloat16 product takes only this one, a float32 product only mask)
+    const uint16_t *mask16;
     int64_t ldm;
     // float32 kernel, unsplit only: colpart[t][j] = sum of the stored C[i][j]
     // over the rows i of row tile t (gemm_colpart_rows(M) x N, leading dim N)
@@ -149,14 +152,19 @@ int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows);
 int32_t gemm_colpart_rows(int32_t M);
 
 // elementwise / reductions ----------------------------------------------------
-// dZ = dY * [Y > 0]; columns [0,h) -> outS (ldS), [h,2h) -> outN (ldN);
+// dZ = dY * [Y > thr] (thr = 0, or kBf16ReluThreshold on the bfloat16 path);
+// columns [0,h) -> outS (ldS), [h,2h) -> outN (ldN);
 // optional bf16 copies of the same values (outS16/outN16, same leading dims).
 // dbias[c] = sum_i dZ[i, c] in a fixed order.
 size_t relu_bwd_workspace_bytes(int32_t n, int32_t h);
+// The bfloat16 path takes the ReLU derivative on the bfloat16-rounded layer
+// output (the operand the next layer reads): bf16_rne(y) > 0 exactly when
+// y > 2^-134, half the smallest bfloat16 subnormal (the tie rounds to 0).
+constexpr float kBf16ReluThreshold = 0x1p-134f;
 int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y, int64_t ldy,
              float *outS, int64_t ldS, float *outN, int64_t ldN,
              uint16_t *outS16, uint16_t *outN16, float *dbias,
-             void *ws, size_t ws_bytes, hipStream_t s);
+             void *ws, size_t ws_bytes, hipStream_t s, float thr = 0.0f);
 // out[c] = sum over r < rows of part[r * C + c], in a fixed order
 int colsum_reduce_rows(int32_t rows, int32_t C, const float *part, float *out, hipStream_t s);
 // column sums of an n x C matrix, fixed order

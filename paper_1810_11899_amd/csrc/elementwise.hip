@@ -58,7 +58,7 @@ __device__ __forceinline__ void block_col_partial(const float (&sum)[VEC], int l
     }
 }
 
-// dZ = dY * [Y > 0] for a chunk of rows, VEC columns per lane.  Writes the two
+// dZ = dY * [Y > thr] for a chunk of rows, VEC columns per lane.  Writes the two
 // halves to their destinations and the chunk's column sums (the bias gradient).
 template <int VEC>
 __global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, int32_t rpc,
@@ -68,7 +68,7 @@ __global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, int
                                                        float *__restrict__ outN, int64_t ldN,
                                                        uint16_t *__restrict__ outS16,
                                                        uint16_t *__restrict__ outN16,
-                                                       float *__restrict__ part) {
+                                                       float *__restrict__ part, float thr) {
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int c = (blockIdx.x * 64 + lane) * VEC;
     const int w = 2 * h;
@@ -102,7 +102,7 @@ __global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, int
             }
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                g[v] = y[v] > 0.0f ? g[v] : 0.0f;
+                g[v] = y[v] > thr ? g[v] : 0.0f;
                 sum[v] += g[v];
             }
             if (dst) {
@@ -370,7 +370,7 @@ size_t relu_bwd_workspace_bytes(int32_t n, int32_t h) {
 
 int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y, int64_t ldy,
              float *outS, int64_t ldS, float *outN, int64_t ldN, uint16_t *outS16, uint16_t *outN16,
-             float *dbias, void *ws, size_t ws_bytes, hipStream_t s) {
+             float *dbias, void *ws, size_t ws_bytes, hipStream_t s, float thr) {
     if (h <= 0) return GCN_OK;
     const int w = 2 * h;
     const int32_t rpc = chunk_rows(n, w);
@@ -392,11 +392,11 @@ int relu_bwd(int32_t n, int32_t h, const float *dY, int64_t lddy, const float *Y
         if (v4) {
             dim3 g((unsigned)((w / 4 + 63) / 64), (unsigned)chunks);
             hipLaunchKernelGGL(relu_bwd_kernel<4>, g, dim3(256), 0, s, n, h, rpc, dY, lddy, Y, ldy, outS, ldS,
-                               outN, ldN, outS16, outN16, part);
+                               outN, ldN, outS16, outN16, part, thr);
         } else {
             dim3 g((unsigned)((w + 63) / 64), (unsigned)chunks);
             hipLaunchKernelGGL(relu_bwd_kernel<1>, g, dim3(256), 0, s, n, h, rpc, dY, lddy, Y, ldy, outS, ldS,
-                               outN, ldN, outS16, outN16, part);
+                               outN, ldN, outS16, outN16, part, thr);
         }
         GCN_LAUNCH_CHECK("relu_bwd_kernel");
     }

@@ -53,7 +53,8 @@ struct DevProblem {
     int relu;
     float *partial;     // split x M x N when split > 1
     uint16_t *C16;      // bfloat16 output instead of C (no split)
-    const float *mask;  // float32, no split: keep C where mask > 0 (leading dim ldm)
+    const float *mask;  // float32 kernel, no split: keep C where mask > 0 (leading dim ldm)
+    const uint16_t *mask16;  // bfloat16 kernels: the same rule on bfloat16 bits
     int64_t ldm;
     float *colpart;     // float32, no split: per-row-tile column sums of C
 };
@@ -553,6 +554,9 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+// a bfloat16 value (raw bits) compares > 0 exactly when its float32 widening does
+__device__ __forceinline__ bool bf16_bits_positive(uint32_t b) { return __uint_as_float(b << 16) > 0.0f; }
+
 template <int LAYOUT, bool VEC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(GCN_BF16_WAVES_PER_EU)))
 void gemm_bf16_kernel(DevArgs args) {
@@ -626,9 +630,9 @@ void gemm_bf16_kernel(DevArgs args) {
     const bool to_partial = P.split > 1;
     float *dst = to_partial ? P.partial + (int64_t)split * P.M * P.N : P.C;
     const int64_t ldd = to_partial ? P.N : P.ldc;
-    // optional [mask > 0] factor and per-row-tile column sums, as in the
-    // float32 kernel
-    const float *const emask = to_partial ? nullptr : P.mask;
+    // optional [mask > 0] factor (bfloat16 mask) and per-row-tile column
+    // sums, as in the float32 kernel
+    const uint16_t *const emask = to_partial ? nullptr : P.mask16;
     const bool ecs = !to_partial && P.colpart;
     float cs[FN];
 #pragma unroll
@@ -648,7 +652,7 @@ void gemm_bf16_kernel(DevArgs args) {
                     if (!to_partial) {
                         v += bv;
                         if (P.relu) v = fmaxf(v, 0.0f);
-                        if (emask) v = emask[(int64_t)row * P.ldm + col] > 0.0f ? v : 0.0f;
+                        if (emask) v = bf16_bits_positive(emask[(int64_t)row * P.ldm + col]) ? v : 0.0f;
                         if (ecs) cs[j] += v;
                         if (P.C16) {
                             P.C16[(int64_t)row * P.ldc + col] = to_bf16(v);
@@ -778,7 +782,7 @@ constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU
 #define GCN_BIG_MASKED 1
 #endif
 #ifndef GCN_BIG_MASK_PREFETCH
-#define GCN_BIG_MASK_PREFETCH 4
+#define GCN_BIG_MASK_PREFETCH 8
 #endif
 #ifndef GCN_BIG_WAVES
 #define GCN_BIG_WAVES 8
@@ -1008,9 +1012,10 @@ void gemm_bf16_big_kernel(DevArgs args) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) bv[e] = col + e < P.N ? P.bias[col + e] : 0.0f;
     const bool relu = !to_partial && P.relu;
-    // optional [mask > 0] factor and column sums per 128-row half of the tile
-    const float *const emask = to_partial ? nullptr : P.mask;
-    const bool mvec = emask && P.ldm % 4 == 0 && ((uintptr_t)emask & 15) == 0 && col + 3 <= Nlast;
+    // optional [mask > 0] factor (bfloat16 mask) and column sums per 128-row
+    // half of the tile
+    const uint16_t *const emask = to_partial ? nullptr : P.mask16;
+    const bool mvec = emask && P.ldm % 4 == 0 && ((uintptr_t)emask & 7) == 0 && col + 3 <= Nlast;
     const bool ecs = !to_partial && P.colpart;
     float cs[2][4] = {{0.0f, 0.0f, 0.0f, 0.0f}, {0.0f, 0.0f, 0.0f, 0.0f}};
     // the mask of a pass's rows is loaded in batches of kMaskBatch rows: the
@@ -1019,21 +1024,21 @@ void gemm_bf16_big_kernel(DevArgs args) {
     constexpr int kRowsPerWave = 128 / kBigWaves;
     constexpr int kMaskBatch = GCN_BIG_MASK_PREFETCH;
     static_assert(kRowsPerWave % kMaskBatch == 0, "whole mask batches");
-    float4 mk[kMaskBatch];
+    uint2 mk[kMaskBatch];   // 4 bfloat16 mask values per row
     auto load_mask = [&](int h, int k0) {
 #pragma unroll
         for (int k = 0; k < kMaskBatch; ++k) {
             const int row = m0 + h * 128 + wave + (k0 + k) * kBigWaves;
-            mk[k] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            mk[k] = make_uint2(0u, 0u);
             if (row <= Mlast && col <= Nlast) {
-                const float *mp = emask + (int64_t)row * P.ldm + col;
+                const uint16_t *mp = emask + (int64_t)row * P.ldm + col;
                 if (mvec) {
-                    mk[k] = *(const float4 *)mp;
+                    mk[k] = *(const uint2 *)mp;
                 } else {
                     mk[k].x = mp[0];
-                    if (col + 1 <= Nlast) mk[k].y = mp[1];
-                    if (col + 2 <= Nlast) mk[k].z = mp[2];
-                    if (col + 3 <= Nlast) mk[k].w = mp[3];
+                    if (col + 1 <= Nlast) mk[k].x |= (uint32_t)mp[1] << 16;
+                    if (col + 2 <= Nlast) mk[k].y = mp[2];
+                    if (col + 3 <= Nlast) mk[k].y |= (uint32_t)mp[3] << 16;
                 }
             }
         }
@@ -1067,11 +1072,11 @@ void gemm_bf16_big_kernel(DevArgs args) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
             if (emask) {
-                const float4 m = mk[k % kMaskBatch];
-                o[0] = m.x > 0.0f ? o[0] : 0.0f;
-                o[1] = m.y > 0.0f ? o[1] : 0.0f;
-                o[2] = m.z > 0.0f ? o[2] : 0.0f;
-                o[3] = m.w > 0.0f ? o[3] : 0.0f;
+                const uint2 m = mk[k % kMaskBatch];
+                o[0] = bf16_bits_positive(m.x & 0xFFFFu) ? o[0] : 0.0f;
+                o[1] = bf16_bits_positive(m.x >> 16) ? o[1] : 0.0f;
+                o[2] = bf16_bits_positive(m.y & 0xFFFFu) ? o[2] : 0.0f;
+                o[3] = bf16_bits_positive(m.y >> 16) ? o[3] : 0.0f;
             }
             if (ecs)
 #pragma unroll
@@ -1143,7 +1148,7 @@ int tile_n_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBN16 : kTBN); }
 bool big_ok(int layout, int nprob, const GemmProblem *probs) {
     if (layout != L_NT || GCN_BF16_BIG == 0) return false;
     for (int i = 0; i < nprob; ++i) {
-        if (!GCN_BIG_MASKED && probs[i].mask) return false;
+        if (!GCN_BIG_MASKED && probs[i].mask16) return false;
         // a side of 128 or less would leave most of a 256-wide tile idle
         if (probs[i].M <= 128 || probs[i].N <= 128) return false;
         for (int s = 0; s < 2; ++s) {
@@ -1192,6 +1197,7 @@ void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int spl
         d.partial = nullptr;
         d.C16 = g.C16;
         d.mask = g.mask;
+        d.mask16 = g.mask16;
         d.ldm = g.ldm;
         d.colpart = g.colpart;
         if (d.split > 1) {
@@ -1301,11 +1307,16 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     bool any_split = false;
     for (int i = 0; i < nprob; ++i) {
         any_split = any_split || a.p[i].split > 1;
-        if ((probs[i].mask || probs[i].colpart) && (a.p[i].split > 1 || (probs[i].C16 != nullptr) == (probs[i].C != nullptr))) {
+        const bool masked = probs[i].mask || probs[i].mask16;
+        if ((masked || probs[i].colpart) && (a.p[i].split > 1 || (probs[i].C16 != nullptr) == (probs[i].C != nullptr))) {
             set_error("gemm: the mask and column-sum epilogue needs an unsplit product with one output");
             return GCN_EINVAL;
         }
-        if (probs[i].mask && probs[i].ldm < probs[i].N) {
+        if (bf16 ? probs[i].mask != nullptr : probs[i].mask16 != nullptr) {
+            set_error("gemm: bfloat16 products take a bfloat16 mask (mask16), float32 products a float32 one");
+            return GCN_EINVAL;
+        }
+        if (masked && probs[i].ldm < probs[i].N) {
             set_error("gemm: mask leading dimension %lld < N=%d", (long long)probs[i].ldm, probs[i].N);
             return GCN_ESHAPE;
         }
