@@ -787,6 +787,9 @@ constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU
 #ifndef GCN_BIG_WAVES
 #define GCN_BIG_WAVES 8
 #endif
+#ifndef GCN_BIG_NARROW_TILES
+#define GCN_BIG_NARROW_TILES 256
+#endif
 #ifndef GCN_BIG_READS_PER_MFMA
 #define GCN_BIG_READS_PER_MFMA 3
 #endif
@@ -1149,8 +1152,13 @@ bool big_ok(int layout, int nprob, const GemmProblem *probs) {
     if (layout != L_NT || GCN_BF16_BIG == 0) return false;
     for (int i = 0; i < nprob; ++i) {
         if (!GCN_BIG_MASKED && probs[i].mask16) return false;
-        // a side of 128 or less would leave most of a 256-wide tile idle
-        if (probs[i].M <= 128 || probs[i].N <= 128) return false;
+        // A side of 128 or less leaves most of a 256-wide tile idle.  Still
+        // worth it for a side of 64+ when the other one alone gives every CU
+        // a tile (the logits of a large subgraph): the product is then bound
+        // by its operand and output traffic, not by the idle matrix work.
+        const int lo = min(probs[i].M, probs[i].N);
+        const int64_t tiles = (int64_t)((probs[i].M + kBigT - 1) / kBigT) * ((probs[i].N + kBigT - 1) / kBigT);
+        if (lo <= 128 && !(lo >= 64 && tiles >= GCN_BIG_NARROW_TILES)) return false;
         for (int s = 0; s < 2; ++s) {
             const GemmSeg &sg = probs[i].seg[s];
             if (sg.K == 0) continue;

@@ -416,3 +416,18 @@ def test_adam_closed_forms():
     for t in range(1, 6):
         p, m, v = optim.adam(p, g, m, v, t, 0.1)
     assert np.allclose(p, -5 * 0.1 * g / (np.abs(g) + 1e-8), rtol=1e-12, atol=1e-15)
+
+
+def test_bf16_relu_threshold_is_the_rounding_rule():
+    """The bfloat16 path's ReLU derivative [bf16(y) > 0] equals [y > 2^-134]
+    (half the smallest bfloat16 subnormal; the tie rounds to even, i.e. 0)."""
+    import numpy as np
+    from oracle.bf16 import f32_to_bf16_bits
+    t = np.float32(2.0 ** -134)
+    ys = [0.0, -0.0, 2.0 ** -149, 2.0 ** -135, 2.0 ** -134, 2.0 ** -133, 2.0 ** -126, 1e-30, 1.0,
+          -(2.0 ** -133), float("inf"), float("-inf")]
+    ys = np.array(ys, dtype=np.float32)
+    ys = np.concatenate([ys, np.nextafter(t, np.float32(1)), np.nextafter(t, np.float32(0))], axis=None)
+    bits = f32_to_bf16_bits(ys).astype(np.uint32)
+    positive = ((bits & 0x8000) == 0) & (bits != 0) & ((bits & 0x7FFF) <= 0x7F80)
+    assert np.array_equal(positive, ys > t)
