@@ -36,7 +36,10 @@ def _bias(h, seed):
 
 SHAPES = [(777, "rmat", 9, 37, 24), (1500, "er", 12, 64, 48), (2049, "rmat", 15, 130, 100),
           (1000, "rmat", 11, 256, 128), (900, "rmat", 10, 264, 256), (1024, "rmat", 9, 96, 64),
-          (2048, "er", 8, 128, 100)]
+          (2048, "er", 8, 128, 100),
+          # bf16 forward products on the large-tile kernel with 1, 2 and 3
+          # k-tiles of 32 (the pipeline's prologue and tail without a steady state)
+          (1100, "rmat", 9, 32, 160), (700, "er", 8, 64, 200), (600, "rmat", 7, 96, 136)]
 
 
 PRECS = [(B.GCN_F32, TOL_F32), (B.GCN_BF16, TOL_BF16)]
