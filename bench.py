@@ -24,6 +24,7 @@ resident in HBM.  Prints one JSON line.
 import argparse
 import hashlib
 import json
+import re
 import os
 import sys
 import time
@@ -42,11 +43,15 @@ KERNEL_SOURCES = {"gemm": ["gemm.hip", "common.h"], "spmm": ["spmm.hip", "common
 
 
 def kernel_source_hash(kernel: str) -> str:
-    """Hash of the source files the kernel class is built from."""
+    """Hash of the source files the kernel class is built from, with comments
+    and blank space left out (a comment edit does not make counters stale)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_1810_11899_amd", "csrc")
     for f in KERNEL_SOURCES["gemm" if kernel.startswith("gemm") else "spmm"]:
-        h.update(open(os.path.join(csrc, f), "rb").read())
+        text = open(os.path.join(csrc, f), encoding="utf-8").read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

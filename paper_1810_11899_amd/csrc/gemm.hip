@@ -764,9 +764,10 @@ bool al(const void *p, int b) { return ((uintptr_t)p % (uintptr_t)b) == 0; }
 // (4 x 2 v_mfma_f32_32x32x16_bf16 blocks), two wavefronts per SIMD, one block
 // per CU.  Operand tiles of 256 rows x 32 k are copied from global
 // memory straight into LDS (16-byte global_load_lds, no staging registers)
-// through a ring of kBigStages stages, so three tiles are in flight while one
-// is multiplied: a 128 x 128 x 32 tile of the smaller kernel is too short to
-// cover the load latency with a single prefetch.  Rows are 64 bytes with their 16-byte
+// through a ring of kBigStages stages, so the copies of the next two or three
+// tiles are in flight while one is multiplied: a 128 x 128 x 32 tile of the
+// smaller kernel is too short to cover the load latency with a single
+// prefetch.  Rows are 64 bytes with their 16-byte
 // chunks XOR-swizzled by row (conflict-free fragment reads); a lane's
 // global address is chosen so that the chunk it deposits lands in its
 // swizzled place.  Requires every K-segment to be a multiple of 32 and
