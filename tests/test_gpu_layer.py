@@ -223,7 +223,7 @@ def test_forced_orders_agree_with_oracle(order):
 
 
 @pytest.mark.parametrize("case", ["cfg1-f32", "cfg1-bf16", "cfg2-bf16", "dY-f32", "bce-transform-first",
-                                  "f32-odd-widths", "bf16-odd-widths"])
+                                  "f32-odd-widths", "bf16-odd-widths", "bf16-odd-wide"])
 def test_model_step_matches_separate_calls(case):
     """gcn_model_step computes what the separate calls compute: every output
     bit for bit, except that a layer whose dZ arrives from the head or from an
@@ -241,6 +241,9 @@ def test_model_step_matches_separate_calls(case):
         wl = synth.custom(2999, "rmat", 9, [(70, 51), (102, 50)], head="ce", classes=13, seed=5)
         r = StepRunner(wl, prec=B.GCN_BF16 if case.startswith("bf16") else B.GCN_F32,
                        orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
+    elif case == "bf16-odd-wide":   # masked input gradient on the large-tile kernel, 150-wide mask rows
+        wl = synth.custom(2999, "rmat", 9, [(300, 75), (150, 64)], head="ce", classes=13, seed=6)
+        r = StepRunner(wl, prec=B.GCN_BF16, orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
     else:
         wl = synth.custom(3000, "rmat", 12, [(96, 64), (128, 64)], head="bce", classes=30, seed=2)
         r = StepRunner(wl, orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
