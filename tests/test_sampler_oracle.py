@@ -241,5 +241,146 @@ def test_induce_matches_dense_submatrix(seed):
     assert np.all(np.diff(ix)[np.diff(rows) == 0] > 0)
     lens = np.diff(ip)
     assert np.all(vals == (np.float32(1) / lens[rows].astype(np.float32)))
-    X = rng.standard_normal((g.n, 5)).astype(np.float32)
-    assert np.array_equal(S.gather_rows(X, vsub), X[vsub])
+
+
+def test_gather_rows_pins():
+    """The row gather of GCN construction, pinned by what a copy of rows must
+    satisfy rather than by re-stating it: rows that carry their own index come
+    back carrying the requested index; the identity list gives X; gathering by
+    a then by b is gathering by a[b]; a permutation and its inverse cancel;
+    integer rows (labels) are copied exactly, int32 extremes included."""
+    rng = np.random.default_rng(9)
+    nX, w = 500, 7
+    X = (np.arange(nX, dtype=np.float32)[:, None] * 16 + np.arange(w, dtype=np.float32)[None, :])
+    rows = rng.integers(0, nX, 300)
+    out = S.gather_rows(X, rows)
+    assert out.shape == (300, w) and out.dtype == np.float32
+    assert np.array_equal(out[:, 0] / 16, rows.astype(np.float32))
+    assert np.array_equal(out - out[:, :1], np.broadcast_to(np.arange(w, dtype=np.float32), out.shape))
+    Y = rng.standard_normal((nX, w)).astype(np.float32)
+    assert np.array_equal(S.gather_rows(Y, np.arange(nX)).view(np.uint32), Y.view(np.uint32))
+    a, b = rng.integers(0, nX, 400), rng.integers(0, 400, 250)
+    assert np.array_equal(S.gather_rows(S.gather_rows(Y, a), b), S.gather_rows(Y, a[b]))
+    perm = rng.permutation(nX)
+    inv = np.empty_like(perm)
+    inv[perm] = np.arange(nX)
+    assert np.array_equal(S.gather_rows(S.gather_rows(Y, perm), inv), Y)
+    lab = np.array([[2 ** 31 - 1], [-2 ** 31], [0], [41]], np.int32)
+    got = S.gather_rows(lab, np.array([3, 0, 1, 1, 2]))
+    assert got.dtype == np.int32 and got[:, 0].tolist() == [41, 2 ** 31 - 1, -2 ** 31, -2 ** 31, 0]
+    assert S.gather_rows(Y, np.zeros(0, np.int64)).shape == (0, w)
+
+
+# ------------------------------------------------ draw layout, known answer ----
+# The oracle's sampler must take its random numbers exactly where the sampler
+# header says they come from (the same stream layout the GPU sampler uses, so
+# that both give the same subgraph for the same seed and run id).  The known
+# answer below is built WITHOUT the oracle: numpy's own Philox4x64-10 gives
+# the blocks, and a short re-statement of the documented run (roots, Dashboard
+# probing rounds, neighbour choice, cleanup) turns them into a vertex list.
+def _np_block(seed, sid, kind, c0, c2):
+    """Philox4x64-10 block at counter (c0, kind, c2, 0), key (seed, sid), from
+    numpy (which steps its counter by one before producing a block)."""
+    c = (int(c0) | (int(kind) << 64) | (int(c2) << 128)) - 1
+    ctr = np.array([(c >> (64 * w)) & (2 ** 64 - 1) for w in range(4)], dtype=np.uint64)
+    return np.random.Philox(key=np.array([seed, sid], np.uint64), counter=ctr).random_raw(4)
+
+
+def _np_below(word, N):
+    return (int(word) * int(N)) >> 64
+
+
+def _documented_run(indptr, indices, m, n, db_cap, ia_cap, cap, p, seed, sid):
+    """The vertex list the documented draw layout gives: root candidate t from
+    word 0 of counter (t, 1, 0, 0); probe of processor j in the run's r-th
+    probing round from word r % 4 of counter (r // 4, 2, j, 0), uniform over
+    the used Dashboard, first hitting processor wins; neighbour of step t from
+    word t % 4 of counter (t // 4, 3, 0, 0).  Dashboard entries name slots;
+    cleanup keeps live slots in order before an overflowing append."""
+    deg = np.diff(indptr)
+    w = np.minimum(deg, cap) if cap > 0 else deg
+    nV = len(deg)
+    roots, t = [], 0
+    while len(roots) < m:
+        v = _np_below(_np_block(seed, sid, 1, t, 0)[0], nV)
+        t += 1
+        if v not in roots:
+            roots.append(v)
+    slots, db = [], []                       # slot = [vertex, weight, live]
+
+    def append(v):
+        slots.append([v, int(w[v]), True])
+        db.extend([len(slots) - 1] * int(w[v]))
+
+    for v in roots:
+        append(v)
+    out, r = list(roots), 0
+    for i in range(m, n):
+        if sum(s[1] for s in slots if s[2]) == 0:
+            return out, "exhausted"
+        k = None
+        while k is None:
+            for j in range(p):
+                e = _np_below(_np_block(seed, sid, 2, r // 4, j)[r % 4], len(db))
+                if slots[db[e]][2]:
+                    k = db[e]
+                    break
+            r += 1
+        slots[k][2] = False
+        u = slots[k][0]
+        t = i - m
+        pick = _np_below(_np_block(seed, sid, 3, t // 4, 0)[t % 4], deg[u])
+        v = int(indices[indptr[u] + pick])
+        if len(db) + w[v] > db_cap or len(slots) == ia_cap:
+            live = [s for s in slots if s[2]]
+            slots.clear()
+            db.clear()
+            for s in live:
+                slots.append(s)
+                db.extend([len(slots) - 1] * s[1])
+        append(v)
+        out.append(v)
+    return out, "ok"
+
+
+@pytest.mark.parametrize("m, n, p, small_db, cap", [(2, 4, 64, False, 0), (2, 4, 1, False, 0),
+                                                   (2, 11, 3, False, 0), (2, 11, 1, True, 0),
+                                                   (3, 13, 64, True, 2)])
+def test_draw_layout_known_answer(m, n, p, small_db, cap):
+    """First roots, probes and neighbour picks of tiny runs on the 7-vertex
+    graph, from numpy's Philox and the documented layout, against the oracle.
+    n = 11 and 13 run past four neighbour steps and (with p <= 3) past four
+    probing rounds, so the word index and the counter's first word both move;
+    the small Dashboards force cleanups."""
+    ip, ix = small_graph()
+    deg = np.diff(ip)
+    wmax = int((np.minimum(deg, cap) if cap else deg).max())
+    db_cap, ia_cap = (m * wmax, m + 1) if small_db else (10 * m * wmax, 64)
+    checked = 0
+    for seed, sid in [(0, 0), (1, 0), (12345, 7), (2 ** 63 + 5, 2 ** 40 + 3)]:
+        want, wst = _documented_run(ip, ix, m, n, db_cap, ia_cap, cap, p, seed, sid)
+        got, st = S.frontier_sample(ip, ix, m, n, db_cap, ia_cap, cap=cap, p=p, seed=seed, sampler_id=sid)
+        assert st == wst and got.tolist() == want, (seed, sid, got.tolist(), want)
+        checked += len(want)
+    assert checked >= 4 * n - 4
+
+
+def test_draw_layout_known_answer_detects_a_swapped_word():
+    """The known answer has the power to see a layout mistake: taking the
+    neighbour word from word 0 of every block (instead of word t % 4) changes
+    some run of the same sizes."""
+    ip, ix = small_graph()
+    orig = _np_block
+    differs = False
+    try:
+        def word0(seed, sid, kind, c0, c2):
+            b = orig(seed, sid, kind, c0, c2)
+            return np.array([b[0]] * 4, np.uint64) if kind == 3 else b
+        globals()["_np_block"] = word0
+        for seed in range(6):
+            a, _ = _documented_run(ip, ix, 2, 11, 200, 64, 0, 64, seed, 0)
+            b, _ = S.frontier_sample(ip, ix, 2, 11, 200, 64, cap=0, p=64, seed=seed, sampler_id=0)
+            differs |= a != b.tolist()
+    finally:
+        globals()["_np_block"] = orig
+    assert differs
