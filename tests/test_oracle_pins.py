@@ -431,3 +431,104 @@ def test_bf16_relu_threshold_is_the_rounding_rule():
     bits = f32_to_bf16_bits(ys).astype(np.uint32)
     positive = ((bits & 0x8000) == 0) & (bits != 0) & ((bits & 0x7FFF) <= 0x7F80)
     assert np.array_equal(positive, ys > t)
+
+
+# ------------------------------------------------- bfloat16 kink band ----
+def _bf16_path_preactivations(wl, orders):
+    """Pre-activations of every layer as a computation that rounds each
+    product operand to bfloat16 (round to nearest even) and accumulates
+    exactly: H, both weights and the neighbour operand (A H, or H W_neigh
+    before it is aggregated) are rounded; each layer's input is the ReLU of
+    the one below.  This is the rounding model of the bfloat16 path, written
+    here with numpy and the IEEE rounding rule, not with the oracle."""
+    g = wl.graph
+    A = sp.csr_matrix((g.vals.astype(np.float64), g.indices, g.indptr), shape=(g.n, g.n))
+    r = lambda x: obf16.round_bf16(np.asarray(x, np.float32)).astype(np.float64)
+    H, Zs = wl.H, []
+    for lay, order in zip(wl.layers, orders):
+        H16, Ws, Wn = r(H), r(lay.W_self), r(lay.W_neigh)
+        S = H16 @ Ws
+        N = (r(A @ H16) @ Wn) if order == 0 else (A @ r(H16 @ Wn))
+        Z = np.concatenate([S, N], axis=1) + lay.bias.astype(np.float64)[None, :]
+        Zs.append(Z)
+        H = np.maximum(Z, 0.0).astype(np.float32)
+    return Zs
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_bf16_kink_band_covers_the_bf16_rounding_model(seed):
+    """The kink band the bfloat16 parity tests use (unit roundoff 2^-8 times
+    C_AMB times the sum of the term magnitudes) contains every pre-activation
+    deviation of the bfloat16 rounding model, over 1-3 layers, both orders
+    and ragged widths: an entry outside the band takes the oracle's ReLU
+    branch under that rounding.  Measured deviations stay below 3 units of
+    the band's scale (upstream layers' rounding included), so C_AMB = 16
+    leaves a margin of more than 5."""
+    rng = np.random.default_rng(seed)
+    L = 1 + seed % 3
+    dims, f = [], int(rng.integers(20, 90))
+    for _ in range(L):
+        h = int(rng.integers(8, 48))
+        dims.append((f, h))
+        f = 2 * h
+    wl = synth.custom(int(rng.integers(150, 600)), ["er", "rmat"][seed % 2], 8, dims, head="ce", classes=5,
+                      seed=seed)
+    for lay in wl.layers:
+        lay.bias = (rng.standard_normal(lay.bias.shape) * 0.2).astype(np.float32)
+    orders = [int(x) for x in rng.integers(0, 2, L)]
+    Zb = _bf16_path_preactivations(wl, orders)
+    H, worst = wl.H, 0.0
+    for li, lay in enumerate(wl.layers):
+        H, c = oracle.layer_fwd(wl.graph, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=True,
+                                unit=oracle.U_BF16)
+        ratio = float((np.abs(Zb[li] - c.Z) / (oracle.U_BF16 * c.mag)).max())
+        worst = max(worst, ratio)
+        assert ratio <= oracle.C_AMB / 5, (li, ratio)
+    assert worst > 0.25, worst   # the band is not vacuously wide
+
+
+def test_kink_envelope_bounds_every_branch_choice_bf16_band(monkeypatch):
+    """The brute-force envelope pin again with the bfloat16 unit roundoff
+    (the configuration of the bfloat16 chained parity tests)."""
+    import itertools
+    from oracle import gcnref
+    monkeypatch.setattr(gcnref, "C_AMB", 4.0)   # a handful of ambiguous entries per seed
+    checked = moved = 0
+    for seed in range(40):
+        wl = synth.custom(9, "er", 4, [(4, 3), (6, 2)], head="ce", classes=3, seed=seed)
+        for lay in wl.layers:
+            lay.bias = np.random.default_rng(seed).standard_normal(lay.bias.shape).astype(np.float32) * 0.05
+        res = oracle.step(wl, first_layer_dH=True, envelope=True, unit=oracle.U_BF16)
+        g = wl.graph
+        gT = synth.Graph(g.n, res.t_indptr, res.t_indices, res.t_vals)
+        H, caches = wl.H, []
+        for lay in wl.layers:
+            H, c = oracle.layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=True, unit=oracle.U_BF16)
+            caches.append(c)
+        amb = [np.argwhere(c.amb) for c in caches]
+        total = sum(a.shape[0] for a in amb)
+        if total == 0 or total > 10:
+            continue
+        attained = 0.0
+        for bits in itertools.product([0, 1], repeat=total):
+            masks = [(c.Z > 0).astype(np.float64) for c in caches]
+            k = 0
+            for li, a in enumerate(amb):
+                for (i, j) in a:
+                    masks[li][i, j] = bits[k]
+                    k += 1
+            dY = res.dHL
+            for li in range(1, -1, -1):
+                lay = wl.layers[li]
+                dWs, dWn, db, dH = oracle.layer_bwd(gT, caches[li], lay.W_self, lay.W_neigh, dY, True,
+                                                    mask=masks[li])
+                for got, ref, E in ((dWs, res.dW_self[li], res.E_dW_self[li]),
+                                    (dWn, res.dW_neigh[li], res.E_dW_neigh[li]),
+                                    (db, res.db[li], res.E_db[li]), (dH, res.dH[li], res.E_dH[li])):
+                    dev_ = np.abs(got - ref)
+                    assert np.all(dev_ <= E + 1e-12), (seed, li)
+                    attained = max(attained, float(dev_.max()))
+                dY = dH
+        moved += attained > 0.0
+        checked += 1
+    assert checked >= 2 and moved >= 2, "too few seeds with a small ambiguous set that moves a gradient"
