@@ -20,7 +20,8 @@
  *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *     Calls only enqueue work on it; outputs are valid once it is synchronised.
  *   - The library allocates no device memory on any of these paths: scratch
- *     comes from the caller's workspace `ws` of `ws_bytes` bytes, sized by the
+ *     comes from the caller's workspace `ws` of `ws_bytes` bytes (or, for
+ *     gcn_aggregate_noalloc, a static array), sized by the
  *     matching *_workspace_bytes query (any 256-byte aligned region at least
  *     that large).  Workspace contents need not be initialised and are
  *     clobbered.
@@ -31,8 +32,10 @@
  *   - Results are deterministic: the same inputs on the same device give
  *     bitwise identical outputs (no floating-point atomics; every reduction
  *     runs in a fixed order).
- *   - The library is reentrant: it keeps no device state between calls.
- *     Calls that share a workspace must be ordered on one stream.
+ *   - The library is reentrant: it keeps no device state between calls
+ *     (the one exception, gcn_aggregate_noalloc, keeps its scratch in a
+ *     static device array and says so).  Calls that share a workspace must
+ *     be ordered on one stream.
  */
 #ifndef GCN_LAYER_H_
 #define GCN_LAYER_H_
@@ -150,6 +153,27 @@ size_t gcn_aggregate_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz
 int gcn_aggregate(const gcn_csr *A, const float *X, int32_t k, int32_t ldx,
                   float *out, int32_t ldo, gcn_prec prec,
                   void *ws, size_t ws_bytes, void *stream);
+
+/* --------------------------------------------- a1, no allocation ----
+ * For callers that cannot allocate device memory or hand over a workspace:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  gcn_aggregate_noalloc computes exactly what gcn_aggregate
+ * computes (same arguments without ws / ws_bytes, same kernels, bitwise equal
+ * results), with its scratch in one file-scope device array of
+ * GCN_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until the
+ * process ends.  It allocates nothing: no hipMalloc / hipFree, no allocating
+ * library call, and no timing events (gcn_profile_* does not see its
+ * launches).  When gcn_aggregate_workspace_bytes(n_rows, n_cols, nnz, k, prec)
+ * exceeds the array it returns GCN_EUNSUPPORTED before any launch (float32
+ * fits 65,536 rows with 3.3 M edges at k = 512; the bfloat16 copy of X
+ * counts too).  Nothing in the array has to start at zero.  Every call on one
+ * GPU uses that GPU's array, which keeps the last call's contents: calls that
+ * can overlap on one GPU (other streams, other threads) race, and the caller
+ * must order them.  The stream's device (the current device for NULL) runs
+ * the work. */
+#define GCN_NOALLOC_SCRATCH_BYTES (64u << 20)
+int gcn_aggregate_noalloc(const gcn_csr *A, const float *X, int32_t k, int32_t ldx,
+                          float *out, int32_t ldo, gcn_prec prec, void *stream);
 
 /* ------------------------------------------------------------ a1 - a3 ----
  * Forward of one layer on an n-vertex subgraph (A is n x n):

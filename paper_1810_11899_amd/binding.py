@@ -20,6 +20,7 @@ GCN_F32, GCN_BF16 = 0, 1
 GCN_AGGREGATE_FIRST, GCN_TRANSFORM_FIRST = 0, 1
 GCN_SOFTMAX_CE, GCN_SIGMOID_BCE = 0, 1
 LOSS_KIND = {"ce": GCN_SOFTMAX_CE, "bce": GCN_SIGMOID_BCE}
+GCN_NOALLOC_SCRATCH_BYTES = 64 << 20      # the static scratch array of gcn_aggregate_noalloc
 PREC = {"f32": GCN_F32, "fp32": GCN_F32, "bf16": GCN_BF16}
 
 
@@ -74,6 +75,7 @@ _SIGNATURES = {
     "gcn_csr_transpose_symmetric": (ctypes.c_int, [_CSRP, _P, _P, _SZ, _P]),
     "gcn_aggregate_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, ctypes.c_int]),
     "gcn_aggregate": (ctypes.c_int, [_CSRP, _P, _I32, _I32, _P, _I32, ctypes.c_int, _P, _SZ, _P]),
+    "gcn_aggregate_noalloc": (ctypes.c_int, [_CSRP, _P, _I32, _I32, _P, _I32, ctypes.c_int, _P]),
     "gcn_layer_pick_order": (ctypes.c_int, [_I32, _I32, ctypes.c_int]),
     "gcn_layer_saved_bytes": (_SZ, [_I32, _I32, _I32, ctypes.c_int, ctypes.c_int]),
     "gcn_layer_workspace_bytes": (_SZ, [_I32, _I32, _I32, _I32, ctypes.c_int, ctypes.c_int]),
@@ -266,6 +268,16 @@ def gcn_aggregate(A: DeviceCSR, X: torch.Tensor, out: torch.Tensor, ws: Workspac
     s = A.struct()
     _check(L.gcn_aggregate(ctypes.byref(s), _ptr(X), k, _ld(X), _ptr(out), _ld(out), prec, w, wb,
                            _stream(stream)), "gcn_aggregate")
+    return out
+
+
+def gcn_aggregate_noalloc(A: DeviceCSR, X: torch.Tensor, out: torch.Tensor, prec=GCN_F32, stream=None):
+    """gcn_aggregate with the library's own static scratch (no workspace)."""
+    _dev_f32(X, "X")
+    _dev_f32(out, "out")
+    s = A.struct()
+    _check(lib().gcn_aggregate_noalloc(ctypes.byref(s), _ptr(X), int(X.shape[1]), _ld(X), _ptr(out), _ld(out),
+                                       prec, _stream(stream)), "gcn_aggregate_noalloc")
     return out
 
 

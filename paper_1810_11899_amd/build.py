@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "libgcnlayer.so")
-SOURCES = ["api.cpp", "spmm.hip", "gemm.hip", "elementwise.hip", "transpose.hip", "peaks.hip", "sampler.hip", "optim.hip"]
+SOURCES = ["api.cpp", "spmm.hip", "gemm.hip", "elementwise.hip", "transpose.hip", "peaks.hip", "sampler.hip", "optim.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -95,7 +95,12 @@ Profiler &prof() {
 }
 }  // namespace
 
+static thread_local int g_prof_suppress = 0;
+ProfSuppress::ProfSuppress() { ++g_prof_suppress; }
+ProfSuppress::~ProfSuppress() { --g_prof_suppress; }
+
 ProfScope::ProfScope(int cls, hipStream_t s, double flops, double bytes) : cls_(cls), s_(s), slot_(-1) {
+    if (g_prof_suppress) return;
     Profiler &p = prof();
     std::lock_guard<std::mutex> lk(p.mu);
     if (!p.on) return;

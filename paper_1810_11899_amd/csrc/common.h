@@ -56,6 +56,13 @@ enum KernelClass {
     K_CLASS_COUNT
 };
 const char *class_name(int cls);
+// While one of these lives on a thread, that thread's launches are not
+// timed even with profiling on (timing creates events, and the entry point
+// that promises to allocate nothing must not create any).
+struct ProfSuppress {
+    ProfSuppress();
+    ~ProfSuppress();
+};
 // Recorded around one launch when profiling is on; no-ops otherwise.
 struct ProfScope {
     ProfScope(int cls, hipStream_t s, double flops, double bytes);
