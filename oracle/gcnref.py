@@ -86,8 +86,7 @@ def set_num_threads(n: int) -> None:
 
 
 U32 = 2.0 ** -24      # unit roundoff of float32
-U_BF16 = 2.0 ** -8    # unit roundoff of bfloat16 (8 significant bits)
-C_AMB = 16.0          # safety factor on u * sum|terms| (covers upstream rounding error too)
+C_AMB = 16.0          # safety factor on u32 * sum|terms| (covers upstream float32 error too)
 
 
 def f64(a) -> np.ndarray:
@@ -139,20 +138,17 @@ class LayerCache:
     H: np.ndarray     # layer input, float64
     AGG: np.ndarray   # A H
     Z: np.ndarray     # pre-activation [S || N] + b
-    amb: Optional[np.ndarray] = None     # |Z| within rounding of 0
+    amb: Optional[np.ndarray] = None     # |Z| within float32 rounding of 0
     absAGG: Optional[np.ndarray] = None  # |A| |H|
-    mag: Optional[np.ndarray] = None     # |b| + the sum of the magnitudes of Z's terms
 
 
-def layer_fwd(g, H, W_self, W_neigh, bias, ambiguity: bool = False, unit: Optional[float] = None,
-              c_amb: Optional[float] = None):
+def layer_fwd(g, H, W_self, W_neigh, bias, ambiguity: bool = False):
     """Forward of one layer (Sec. II; Alg. 1 forward loop), float64.
 
     S = H W_self, N = (A H) W_neigh, Z = [S || N] + b, Y = max(Z, 0).
-    With ``ambiguity`` the cache also marks the ReLU kinks that the rounding
-    of the computation cannot resolve: |Z| < c_amb u (|b| + |H| |W_self|) on
-    the self half and |Z| < c_amb u (|b| + |A| |H| |W_neigh|) on the neighbour
-    half, u the unit roundoff (float32 by default) and c_amb C_AMB by default.
+    With ``ambiguity`` the cache also marks the ReLU kinks that float32 cannot
+    resolve: |Z| < C_AMB u32 (|b| + |H| |W_self|) on the self half and
+    |Z| < C_AMB u32 (|b| + |A| |H| |W_neigh|) on the neighbour half.
     """
     H = f64(H)
     AGG = aggregate(g.indptr, g.indices, g.vals, H)
@@ -163,14 +159,11 @@ def layer_fwd(g, H, W_self, W_neigh, bias, ambiguity: bool = False, unit: Option
     Y = np.maximum(Z, 0.0)
     cache = LayerCache(H, AGG, Z)
     if ambiguity:
-        u = U32 if unit is None else float(unit)
-        c = C_AMB if c_amb is None else float(c_amb)
         absAGG = aggregate(g.indptr, g.indices, np.abs(f64(g.vals)), np.abs(H))
         mag = np.concatenate([np.abs(H) @ np.abs(f64(W_self)), absAGG @ np.abs(f64(W_neigh))], axis=1)
         mag += np.abs(b)[None, :]
-        cache.amb = np.abs(Z) < c * u * mag
+        cache.amb = np.abs(Z) < C_AMB * U32 * mag
         cache.absAGG = absAGG
-        cache.mag = mag
     return Y, cache
 
 
@@ -276,15 +269,20 @@ class _CSR:
         self.indptr, self.indices, self.vals = indptr, indices, vals
 
 
-def step(wl, first_layer_dH: Optional[bool] = None, envelope: bool = False,
-         unit: Optional[float] = None) -> StepResult:
+def step(wl, first_layer_dH: Optional[bool] = None, envelope: bool = False, masks=None) -> StepResult:
     """Forward through every layer, PREDICT/LOSS (or the given dY), backward.
 
     The layer-1 input gradient is computed only for single-layer workloads
     unless ``first_layer_dH`` says otherwise (training never needs it).
-    ``envelope`` adds the ReLU-kink bounds of every gradient, for a
-    computation with unit roundoff ``unit`` (float32 by default; U_BF16 for
-    the path whose product operands are rounded to bfloat16).
+    ``envelope`` adds the ReLU-kink bounds of every gradient.
+
+    ``masks`` (one 0/1 array of Z's shape per layer) fixes the branch of every
+    activation: layer l outputs Y = Z * m_l and passes dZ = dY * m_l back,
+    the network in which each ReLU is replaced by the gate its branch choice
+    gives (exactly the ReLU network where m_l = [Z_l > 0]).  A computation
+    whose rounding decides some near-zero branches the other way computes
+    this network for its own choices; comparing on the same choices leaves
+    only the arithmetic to compare.
     """
     g = wl.graph
     L = len(wl.layers)
@@ -294,8 +292,12 @@ def step(wl, first_layer_dH: Optional[bool] = None, envelope: bool = False,
     gT = _CSR(t_indptr, t_indices, t_vals)
     H = wl.H
     caches, Ys = [], []
-    for lay in wl.layers:
-        Y, cache = layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=envelope, unit=unit)
+    if masks is not None and (envelope or len(masks) != L):
+        raise ValueError("masks: one per layer, and not together with the kink envelope")
+    for li, lay in enumerate(wl.layers):
+        Y, cache = layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=envelope)
+        if masks is not None:
+            Y = cache.Z * np.asarray(masks[li], dtype=np.float64)
         caches.append(cache)
         Ys.append(Y)
         H = Y
@@ -315,7 +317,8 @@ def step(wl, first_layer_dH: Optional[bool] = None, envelope: bool = False,
     for li in range(L - 1, -1, -1):
         lay = wl.layers[li]
         need = li > 0 or first_layer_dH
-        dWs, dWn, db, dH = layer_bwd(gT, caches[li], lay.W_self, lay.W_neigh, dY, need)
+        dWs, dWn, db, dH = layer_bwd(gT, caches[li], lay.W_self, lay.W_neigh, dY, need,
+                                     mask=None if masks is None else np.asarray(masks[li], dtype=np.float64))
         res.dW_self[li], res.dW_neigh[li], res.db[li], res.dH[li] = dWs, dWn, db, dH
         if envelope:
             e = layer_bwd_envelope(gT, caches[li], lay.W_self, lay.W_neigh, dY, E_dY, need)

@@ -433,102 +433,76 @@ def test_bf16_relu_threshold_is_the_rounding_rule():
     assert np.array_equal(positive, ys > t)
 
 
-# ------------------------------------------------- bfloat16 kink band ----
-def _bf16_path_preactivations(wl, orders):
-    """Pre-activations of every layer as a computation that rounds each
-    product operand to bfloat16 (round to nearest even) and accumulates
-    exactly: H, both weights and the neighbour operand (A H, or H W_neigh
-    before it is aggregated) are rounded; each layer's input is the ReLU of
-    the one below.  This is the rounding model of the bfloat16 path, written
-    here with numpy and the IEEE rounding rule, not with the oracle."""
-    g = wl.graph
-    A = sp.csr_matrix((g.vals.astype(np.float64), g.indices, g.indptr), shape=(g.n, g.n))
-    r = lambda x: obf16.round_bf16(np.asarray(x, np.float32)).astype(np.float64)
-    H, Zs = wl.H, []
-    for lay, order in zip(wl.layers, orders):
-        H16, Ws, Wn = r(H), r(lay.W_self), r(lay.W_neigh)
-        S = H16 @ Ws
-        N = (r(A @ H16) @ Wn) if order == 0 else (A @ r(H16 @ Wn))
-        Z = np.concatenate([S, N], axis=1) + lay.bias.astype(np.float64)[None, :]
-        Zs.append(Z)
-        H = np.maximum(Z, 0.0).astype(np.float32)
-    return Zs
+# ------------------------------------------------- given branch masks ----
+def _gated_objective(wl, masks):
+    """The network with every ReLU replaced by the fixed gate m (Y = Z * m),
+    evaluated through the oracle's forward pre-activations."""
+    H = wl.H
+    for lay, m in zip(wl.layers, masks):
+        _, c = oracle.layer_fwd(wl.graph, H, lay.W_self, lay.W_neigh, lay.bias)
+        H = c.Z * m
+    if wl.spec.head is None:
+        return float(np.sum(H * wl.dY))
+    loss, *_ = oracle.loss_grad(wl.spec.head, H, wl.W_pred, wl.b_pred, labels=wl.labels, targets=wl.targets)
+    return loss
 
 
-@pytest.mark.parametrize("seed", range(8))
-def test_bf16_kink_band_covers_the_bf16_rounding_model(seed):
-    """The kink band the bfloat16 parity tests use (unit roundoff 2^-8 times
-    C_AMB times the sum of the term magnitudes) contains every pre-activation
-    deviation of the bfloat16 rounding model, over 1-3 layers, both orders
-    and ragged widths: an entry outside the band takes the oracle's ReLU
-    branch under that rounding.  Measured deviations stay below 3 units of
-    the band's scale (upstream layers' rounding included), so C_AMB = 16
-    leaves a margin of more than 5."""
-    rng = np.random.default_rng(seed)
-    L = 1 + seed % 3
-    dims, f = [], int(rng.integers(20, 90))
-    for _ in range(L):
-        h = int(rng.integers(8, 48))
-        dims.append((f, h))
-        f = 2 * h
-    wl = synth.custom(int(rng.integers(150, 600)), ["er", "rmat"][seed % 2], 8, dims, head="ce", classes=5,
-                      seed=seed)
-    for lay in wl.layers:
-        lay.bias = (rng.standard_normal(lay.bias.shape) * 0.2).astype(np.float32)
-    orders = [int(x) for x in rng.integers(0, 2, L)]
-    Zb = _bf16_path_preactivations(wl, orders)
-    H, worst = wl.H, 0.0
+@pytest.mark.parametrize("head", ["ce", "bce", None])
+def test_step_with_masks_is_the_gradient_of_the_gated_network(head):
+    """With branch masks given, the step returns the gradient of the gated
+    network: central finite differences of that network's objective, with
+    random masks that differ from [Z > 0] in about half of the entries."""
+    wl = synth.custom(40, "er", 5, [(5, 4), (8, 3)], head=head, classes=4, seed=7)
+    rng = np.random.default_rng(3)
+    for lay in wl.layers:            # float64 parameters: the perturbations are exact
+        lay.W_self = lay.W_self.astype(np.float64)
+        lay.W_neigh = lay.W_neigh.astype(np.float64)
+        lay.bias = rng.standard_normal(lay.bias.shape) * 0.2
+    wl.H = wl.H.astype(np.float64)
+    if head is None:
+        wl.dY = rng.standard_normal((wl.n, 6))
+    else:
+        wl.W_pred = wl.W_pred.astype(np.float64)
+        wl.b_pred = rng.standard_normal(wl.b_pred.shape) * 0.1
+    masks = [(rng.random((wl.n, 2 * lay.h)) < 0.5).astype(np.float64) for lay in wl.layers]
+    r = oracle.step(wl, first_layer_dH=True, masks=masks)
+    H = wl.H
+    for li, (lay, m) in enumerate(zip(wl.layers, masks)):
+        _, c = oracle.layer_fwd(wl.graph, H, lay.W_self, lay.W_neigh, lay.bias)
+        H = c.Z * m
+        assert np.array_equal(r.Y[li], H)                     # the forward is gated too
+    checks = []
     for li, lay in enumerate(wl.layers):
-        H, c = oracle.layer_fwd(wl.graph, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=True,
-                                unit=oracle.U_BF16)
-        ratio = float((np.abs(Zb[li] - c.Z) / (oracle.U_BF16 * c.mag)).max())
-        worst = max(worst, ratio)
-        assert ratio <= oracle.C_AMB / 5, (li, ratio)
-    assert worst > 0.25, worst   # the band is not vacuously wide
+        checks += [(lay.W_self, r.dW_self[li]), (lay.W_neigh, r.dW_neigh[li]), (lay.bias, r.db[li])]
+    checks.append((wl.H, r.dH[0]))
+    if head is not None:
+        checks += [(wl.W_pred, r.dW_pred), (wl.b_pred, r.db_pred)]
+    eps = 1e-6
+    for arr, grad in checks:
+        flat = arr.reshape(-1)
+        gflat = np.asarray(grad).reshape(-1)
+        for idx in rng.choice(flat.size, size=min(8, flat.size), replace=False):
+            old = flat[idx]
+            flat[idx] = old + eps
+            jp = _gated_objective(wl, masks)
+            flat[idx] = old - eps
+            jm = _gated_objective(wl, masks)
+            flat[idx] = old
+            fd = (jp - jm) / (2 * eps)
+            assert abs(fd - gflat[idx]) <= 1e-6 * max(np.abs(gflat).max(), 1e-12) + 1e-9, (arr.shape, idx)
 
 
-def test_kink_envelope_bounds_every_branch_choice_bf16_band(monkeypatch):
-    """The brute-force envelope pin again with the bfloat16 unit roundoff
-    (the configuration of the bfloat16 chained parity tests)."""
-    import itertools
-    from oracle import gcnref
-    monkeypatch.setattr(gcnref, "C_AMB", 4.0)   # a handful of ambiguous entries per seed
-    checked = moved = 0
-    for seed in range(40):
-        wl = synth.custom(9, "er", 4, [(4, 3), (6, 2)], head="ce", classes=3, seed=seed)
-        for lay in wl.layers:
-            lay.bias = np.random.default_rng(seed).standard_normal(lay.bias.shape).astype(np.float32) * 0.05
-        res = oracle.step(wl, first_layer_dH=True, envelope=True, unit=oracle.U_BF16)
-        g = wl.graph
-        gT = synth.Graph(g.n, res.t_indptr, res.t_indices, res.t_vals)
-        H, caches = wl.H, []
-        for lay in wl.layers:
-            H, c = oracle.layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias, ambiguity=True, unit=oracle.U_BF16)
-            caches.append(c)
-        amb = [np.argwhere(c.amb) for c in caches]
-        total = sum(a.shape[0] for a in amb)
-        if total == 0 or total > 10:
-            continue
-        attained = 0.0
-        for bits in itertools.product([0, 1], repeat=total):
-            masks = [(c.Z > 0).astype(np.float64) for c in caches]
-            k = 0
-            for li, a in enumerate(amb):
-                for (i, j) in a:
-                    masks[li][i, j] = bits[k]
-                    k += 1
-            dY = res.dHL
-            for li in range(1, -1, -1):
-                lay = wl.layers[li]
-                dWs, dWn, db, dH = oracle.layer_bwd(gT, caches[li], lay.W_self, lay.W_neigh, dY, True,
-                                                    mask=masks[li])
-                for got, ref, E in ((dWs, res.dW_self[li], res.E_dW_self[li]),
-                                    (dWn, res.dW_neigh[li], res.E_dW_neigh[li]),
-                                    (db, res.db[li], res.E_db[li]), (dH, res.dH[li], res.E_dH[li])):
-                    dev_ = np.abs(got - ref)
-                    assert np.all(dev_ <= E + 1e-12), (seed, li)
-                    attained = max(attained, float(dev_.max()))
-                dY = dH
-        moved += attained > 0.0
-        checked += 1
-    assert checked >= 2 and moved >= 2, "too few seeds with a small ambiguous set that moves a gradient"
+def test_step_with_its_own_masks_is_the_relu_step():
+    """m_l = [Z_l > 0] reproduces the ReLU step exactly."""
+    wl = synth.custom(300, "rmat", 7, [(9, 6), (12, 5)], head="ce", classes=6, seed=8)
+    base = oracle.step(wl, first_layer_dH=True)
+    H, masks = wl.H, []
+    for lay in wl.layers:
+        H, c = oracle.layer_fwd(wl.graph, H, lay.W_self, lay.W_neigh, lay.bias)
+        masks.append(c.Z > 0)
+    r = oracle.step(wl, first_layer_dH=True, masks=masks)
+    for a, b in [(base.Y, r.Y), (base.dW_self, r.dW_self), (base.dW_neigh, r.dW_neigh), (base.db, r.db),
+                 (base.dH, r.dH)]:
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y)
+    assert base.loss == r.loss and np.array_equal(base.dW_pred, r.dW_pred)
