@@ -37,7 +37,8 @@ static const char *kClassNames[K_CLASS_COUNT] = {
     "spmm", "spmm_fixup", "gemm_nn", "gemm_tn", "gemm_nt", "splitk_reduce", "relu_bwd",
     "colsum", "loss_rows", "loss_reduce", "transpose_count", "transpose_scan", "transpose_scatter",
     "transpose_sort", "transpose_final", "cvt_bf16", "gemm_nn_bf16", "gemm_tn_bf16", "gemm_nt_bf16",
-    "spmm_bf16", "transpose_bf16", "frontier_sample", "induce_subgraphs", "gather_rows", "adam", "transpose_symmetric"};
+    "spmm_bf16", "transpose_bf16", "frontier_sample", "induce_subgraphs", "gather_rows", "adam", "transpose_symmetric",
+    "gemm_nt_bf16_big", "gemm_nt_bf16_big_masked"};
 
 const char *class_name(int cls) {
     return (cls >= 0 && cls < K_CLASS_COUNT) ? kClassNames[cls] : "";

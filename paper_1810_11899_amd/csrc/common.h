@@ -53,6 +53,8 @@ enum KernelClass {
     K_GATHER,
     K_ADAM,
     K_T_SYM,
+    K_GEMM_NT_BF16_BIG,         // the bfloat16 large-tile kernel
+    K_GEMM_NT_BF16_BIG_MASKED,  // the same with the ReLU-derivative epilogue
     K_CLASS_COUNT
 };
 const char *class_name(int cls);

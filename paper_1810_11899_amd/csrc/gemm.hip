@@ -1332,6 +1332,11 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     }
     int cls = layout == L_NN ? K_GEMM_NN : (layout == L_TN ? K_GEMM_TN : K_GEMM_NT);
     if (bf16) cls += K_GEMM_NN_BF16 - K_GEMM_NN;
+    if (big) {
+        bool masked = false;
+        for (int i = 0; i < nprob; ++i) masked = masked || probs[i].mask16;
+        cls = masked ? K_GEMM_NT_BF16_BIG_MASKED : K_GEMM_NT_BF16_BIG;
+    }
     {
         ProfScope ps(cls, s, flops, 0.0);
         dim3 grid((unsigned)blocks);

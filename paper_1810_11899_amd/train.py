@@ -103,10 +103,11 @@ class FlatModel:
         p = self.params.cpu().numpy()
         return [p[o:o + int(np.prod(sh))].reshape(sh)[self.f0:] for o, sh in zip(self.offsets[:2], self.shapes[:2])]
 
-    def host_tensors(self):
-        """{name: numpy array} of the current parameters (for checks), the first
-        layer's weights at their f_in rows."""
-        p = self.params.cpu().numpy()
+    def host_tensors(self, buf=None):
+        """{name: numpy array} of the current parameters (or of another buffer
+        of the same layout, such as the gradients), the first layer's weights
+        at their f_in rows (for checks)."""
+        p = (self.params if buf is None else buf).cpu().numpy()
         out = {}
         names = []
         for li in range(len(self.dims)):

@@ -34,6 +34,20 @@ def test_rmat65536_two_layer_f32_step():
     print("max relative errors beyond the kink envelope:", {k: f"{v:.1e}" for k, v in errs.items()})
 
 
+def test_rmat65536_two_layer_bf16_chained_step():
+    """The bfloat16 step the benchmark times, as one chain (the forward loop,
+    PREDICT/LOSS and the backward pass in one gcn_model_step), against the
+    float64 oracle on the unrounded inputs."""
+    from paper_1810_11899_amd import binding as B
+    from test_gpu_layer import compare_bf16_chain
+    wl = synth.config(3)
+    r = StepRunner(wl, prec=B.GCN_BF16)
+    r.step()
+    torch.cuda.synchronize()
+    errs, _ = compare_bf16_chain(r, wl)
+    print("bf16 chain:", errs)
+
+
 def test_epoch_stream_subgraphs_reuse_buffers():
     """Several subgraphs of the stream through one runner (buffers sized for
     the largest nnz, reused); each checked against the oracle."""

@@ -161,6 +161,70 @@ def compare_step(run: dict, ref: oracle.StepResult, tol=TOL_F32):
     return errs
 
 
+def check_bf16_decisions(Y_gpu, masks, wl):
+    """The forward of a bfloat16 chain against the oracle's, entry by entry:
+    |Y_gpu - max(Z, 0)| <= 16 * 2^-8 * M and every ReLU decision that differs
+    from the oracle's at an entry with |Z| <= 16 * 2^-8 * M, where M is the
+    sum of the magnitudes of Z's terms with each layer's input magnitude taken
+    as the M of the layer below (|H0| for the first).  Each layer rounds its
+    input, both weights and the neighbour operand (at most 3 units of 2^-8 of
+    M) and passes on the deviation of its input (at most the lower layer's
+    bound, carried through the same magnitudes), so 16 units hold for up to
+    five layers.  Returns the largest deviation in units of 2^-8 M and the
+    number of decisions per layer that differ from the oracle's."""
+    u, C = 2.0 ** -8, 16.0
+    g = wl.graph
+    absA = np.abs(g.vals.astype(np.float64))
+    H, Min, worst, nflip = wl.H, np.abs(wl.H.astype(np.float64)), 0.0, []
+    for li, lay in enumerate(wl.layers):
+        Yref, c = oracle.layer_fwd(g, H, lay.W_self, lay.W_neigh, lay.bias)
+        mag = np.concatenate([Min @ np.abs(lay.W_self.astype(np.float64)),
+                              oracle.aggregate(g.indptr, g.indices, absA, Min) @ np.abs(lay.W_neigh.astype(np.float64))],
+                             axis=1) + np.abs(lay.bias.astype(np.float64))[None, :]
+        band = C * u * mag
+        dev_ = np.abs(np.asarray(Y_gpu[li], np.float64) - Yref)
+        assert np.all(dev_ <= band), ("forward deviation beyond the rounding bound", li)
+        flips = np.asarray(masks[li], bool) != (c.Z > 0)
+        assert np.all(np.abs(c.Z[flips]) <= band[flips]), ("a ReLU decision rounding cannot explain", li)
+        nflip.append(int(flips.sum()))
+        worst = max(worst, float(np.divide(dev_, u * mag, out=np.zeros_like(dev_), where=mag > 0).max()))
+        H, Min = Yref, mag
+    return worst, nflip
+
+
+def compare_bf16_chain(r: StepRunner, wl, first_layer_dH=None):
+    """The bfloat16 model step as the benchmark runs it (one gcn_model_step:
+    fused masked epilogues, dZ kept as bfloat16 rows between layers) against
+    the float64 oracle on the unrounded inputs.  The bfloat16 rounding decides
+    some near-zero ReLU branches differently from float64; each such decision
+    is a correct result of the bfloat16 computation, so (a) every decision is
+    checked to be one that rounding explains, entry by entry, and (b) the
+    oracle then takes the GPU's decisions (its gated network, Y = Z * m,
+    dZ = dY * m, m = [bf16(Y) > 0], the bfloat16 path's ReLU rule) and every
+    output -- each layer's Y, the loss, every gradient -- is compared at 2e-2
+    with no allowance."""
+    from oracle import bf16 as obf16
+    got = r.results()
+    masks = [obf16.round_bf16(y) > 0 for y in got["Y"]]
+    worst, nflip = check_bf16_decisions(got["Y"], masks, wl)
+    ref = oracle.step(wl, first_layer_dH=first_layer_dH, masks=masks)
+    errs = compare_step(got, ref, tol=TOL_BF16)
+    errs["forward_units"] = worst
+    errs["decisions_differing_from_float64"] = nflip
+    return errs, ref
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_config_step_parity_bf16_chain(cfg):
+    wl = synth.config(cfg)
+    r = StepRunner(wl, prec=B.GCN_BF16)
+    print(f"bf16 chained step, workload {cfg}", flush=True)
+    r.step()
+    torch.cuda.synchronize()
+    errs, _ = compare_bf16_chain(r, wl)
+    print("bf16 chain:", errs)
+
+
 @pytest.mark.parametrize("prec", [B.GCN_F32, B.GCN_BF16])
 @pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
 def test_zero_vertex_subgraph(prec, order, ws):
@@ -250,8 +314,15 @@ def test_model_step_matches_separate_calls(case):
     print(f"model step vs calls: {case}", flush=True)
     r.step_calls()
     a = r.results()
+    B.gcn_profile_reset()
+    B.gcn_profile_enable(True)
     r.step()
+    torch.cuda.synchronize()
+    B.gcn_profile_enable(False)
+    prof = B.gcn_profile_read_all()
     b = r.results()
+    if case == "bf16-odd-wide":   # the masked input gradient really ran on the large-tile kernel
+        assert prof["gemm_nt_bf16_big_masked"][1] >= 1, prof
     inner = [t.detach().cpu().numpy() for t in ([r.dHL] if r.head is not None else []) + r.dH[1:]]
     for key in ("Y", "dW_self", "dW_neigh", "dH"):
         for i, (x, y) in enumerate(zip(a[key], b[key])):
@@ -283,7 +354,7 @@ def test_model_step_matches_separate_calls(case):
         assert same or fused, ("inter-layer gradient", i)
         if r.head is not None and i == 0:
             assert fused, "the head writes the last layer's dZ"
-        if case in ("bce-transform-first", "f32-odd-widths", "bf16-odd-widths"):
+        if case in ("bce-transform-first", "f32-odd-widths", "bf16-odd-widths", "bf16-odd-wide"):
             assert fused and not same, ("unsplit input-gradient product writes dZ", i)
 
 
@@ -310,8 +381,9 @@ def _random_model(seed):
 @pytest.mark.parametrize("seed", range(48))
 def test_model_step_random_models(seed):
     """Seeded random models through gcn_model_step (fused mask epilogues where
-    they apply, split and unsplit products, ragged tiles): float32 against the
-    oracle (kink envelope), both precisions against the separate calls.
+    they apply, split and unsplit products, ragged tiles): both precisions
+    against the oracle (float32 at 1e-4, bfloat16 chained at 2e-2, each beyond
+    the kink envelope of its unit roundoff) and against the separate calls.
     (Seed 12 found a split-K workspace that the input-gradient plan sized for
     one split too few.)"""
     wl, orders, prec = _random_model(seed)
@@ -331,6 +403,8 @@ def test_model_step_random_models(seed):
         assert rel_inf(y, x) <= 1e-6, ("db", i)
     if prec == B.GCN_F32:
         compare_step(b, oracle.step(wl, first_layer_dH=True, envelope=True))
+    else:
+        compare_bf16_chain(r, wl, first_layer_dH=True)
 
 
 @pytest.mark.parametrize("graph", ["empty", "star"])
