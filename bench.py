@@ -170,6 +170,63 @@ def measure_peaks(B, torch) -> dict:
     return out
 
 
+def measure_gather(B, torch, wl) -> dict:
+    """Measured row-gather ceilings (gcn_peak_gather): the rate at which this
+    GPU delivers gathered row bytes to the CUs, best over a few launch shapes.
+      uniform_<R>B_<size>  uniformly random rows of R bytes from an array of
+                           that size (64 MiB fits the 256 MB Infinity Cache;
+                           4 GiB does not, so most rows come from HBM)
+      csr_fp32_rows        the workload's CSR column indices in order, rows of
+                           the float32 features (k = the first layer's width)
+      csr_bf16_rows        the same with bfloat16 rows (half the bytes)
+    A 16 KiB array stays in every CU's L1, so its rate is the CU's
+    vector-memory path with every row a hit: no gather of that row size with
+    16-byte lane loads runs faster, and it is the ceiling the propagation
+    kernels are measured against.  2 MiB sits in every XCD's 4 MB L2.  The
+    csr_* cases are one aggregation pass's gathers in plain CSR order over
+    all CUs (no slice schedule, no arithmetic, no CSR or output traffic): a
+    reference point for what the kernels' schedules add, not a ceiling."""
+    stream = torch.cuda.current_stream()
+    blocks_list = (2048, 4096, 8192)
+    sink = torch.empty(max(blocks_list) * 256, dtype=torch.float32, device="cuda")
+    out = {}
+
+    def best(X, row_bytes, idx):
+        bb, best_gbs = 0, 0.0
+        for blocks in blocks_list:
+            B.gcn_peak_gather(X, row_bytes, idx, sink, blocks)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record(stream)
+            for _ in range(3):
+                B.gcn_peak_gather(X, row_bytes, idx, sink, blocks)
+            b.record(stream)
+            torch.cuda.synchronize()
+            gbs = idx.numel() * row_bytes * 3 / (a.elapsed_time(b) / 1e3) / 1e9
+            if gbs > best_gbs:
+                best_gbs, bb = gbs, blocks
+        return {"gbs": round(best_gbs, 1), "blocks": bb, "rows": int(idx.numel()), "row_bytes": row_bytes}
+
+    g = torch.Generator(device="cuda")
+    g.manual_seed(181011899)
+    for row_bytes in (256, 1024):
+        for size, tag in ((16 << 10, "16KiB"), (2 << 20, "2MiB"), (64 << 20, "64MiB"), (4 << 30, "4GiB")):
+            rows = size // row_bytes
+            X = torch.ones((rows, row_bytes // 4), dtype=torch.float32, device="cuda")
+            count = (2 << 30) // row_bytes        # 2 GiB gathered per launch
+            idx = torch.randint(0, rows, (count,), dtype=torch.int32, device="cuda", generator=g)
+            out[f"uniform_{row_bytes}B_{tag}"] = best(X, row_bytes, idx)
+            del X, idx
+    k = wl.layers[0].f_in
+    idx = torch.from_numpy(wl.graph.indices).cuda()
+    X = torch.ones((wl.n, k), dtype=torch.float32, device="cuda")
+    out["csr_order_fp32_rows"] = best(X, 4 * k, idx)
+    X16 = torch.ones((wl.n, k), dtype=torch.bfloat16, device="cuda")
+    out["csr_order_bf16_rows"] = best(X16, 2 * k, idx)
+    del X, X16
+    return out
+
+
 def chase_latency_ns(B, torch, n: int, chains: int, steps: int = 4000, seed: int = 0) -> float:
     """Latency of one dependent load, ns, over an int32 random cycle of n
     elements walked by `chains` wavefronts at once (gcn_peak_chase)."""
@@ -516,6 +573,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event timing")
     ap.add_argument("--no-peaks", action="store_true", help="skip the measured machine ceilings")
+    ap.add_argument("--no-variants", action="store_true",
+                    help="skip the bfloat16 variant that the default (float32, 65,536-vertex) run also measures")
     ap.add_argument("--workload", default="step", choices=["step", "sampler", "train", "stream"],
                     help="step: one fwd+bwd step of the layer (default); sampler: the frontier sampler; "
                          "train: the sampled-subgraph training loop")
@@ -550,7 +609,7 @@ def main():
         return
     from paper_1810_11899_amd import binding as B
     from paper_1810_11899_amd import synth
-    from paper_1810_11899_amd.runner import StepRunner, step_work
+    from paper_1810_11899_amd.runner import step_work
 
     B.lib()
     if args.workload == "sampler":
@@ -559,8 +618,66 @@ def main():
     if args.workload == "train":
         bench_train(args, B, torch)
         return
-    prec = B.PREC[args.prec]
     wl = synth.config(args.config)
+    out = bench_step(args, args.prec, wl, B, torch, synth)
+    variants = {}
+    if args.config == 3 and args.prec == "f32" and not args.no_variants:
+        # the bfloat16-operand variant of the same workload, measured the same way
+        v = bench_step(args, "bf16", wl, B, torch, synth)
+        variants["bf16"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "dtype", "gflops",
+                                               "step_ms_min_median", "host_issue_ms_per_step", "roofline",
+                                               "kernels") if k in v}
+        variants["bf16"]["config"] = {"workload": v["config"]["workload"]}
+    if variants:
+        out["variants"] = variants
+    if not args.no_peaks:
+        peaks = measure_peaks(B, torch)
+        peaks["gather"] = measure_gather(B, torch, wl)
+        out["measured_peaks"] = peaks
+        for o in [out] + list(variants.values()):
+            roof = o.get("roofline")
+            if roof is not None:
+                prec_o = "f32" if o["dtype"] == "f32" else "bf16"
+                key = "stream_read_gbs" if roof["bound"] == "hbm" else f"mfma_{prec_o}_tflops"
+                roof["measured_peak"] = peaks[key]
+                roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
+            spmm_vs_gather(o, peaks["gather"])
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.config, synth, step_work, B, min_seconds=args.cpu_seconds)
+        if args.config in (0, 1, 2):   # the serial oracle as well (small workloads only)
+            out["cpu_baseline_serial"] = cpu_baseline(args.config, synth, step_work, B,
+                                                      min_seconds=args.cpu_seconds, max_reps=5, threads=1)
+    print(json.dumps(out), flush=True)
+
+
+def spmm_vs_gather(o: dict, gather: dict):
+    """The aggregation kernels against the measured gather rates: the rate at
+    which they deliver gathered row bytes (one row of the aggregated width per
+    stored edge) over the probe's rate for random rows of the size each
+    kernel's lane groups read, from an L2-resident array (the ceiling: every
+    row an L2 hit), from one that fits only the Infinity Cache, and from one
+    that comes mostly from HBM (above 1: the kernel's locality beats random
+    rows from that level)."""
+    # the float32 kernel gathers 256-byte slices of a row per lane group
+    # (the XCD-sliced schedule), the bfloat16 one whole 1 KB rows
+    for cls, row in (("spmm", 256), ("spmm_bf16", 1024)):
+        k = o.get("kernels", {}).get(cls)
+        if not k or "gather_gbs" not in k:
+            continue
+        for tag, name in (("16KiB", "frac_of_l1_gather_ceiling"), ("2MiB", "vs_l2_gather"),
+                          ("64MiB", "vs_infinity_cache_gather"), ("4GiB", "vs_hbm_gather")):
+            ref = gather.get(f"uniform_{row}B_{tag}")
+            if ref:
+                k[name] = round(k["gather_gbs"] / ref["gbs"], 4)
+
+
+def bench_step(args, prec_name: str, wl, B, torch, synth) -> dict:
+    """Time one workload's fwd+bwd step at one precision: the whole step with
+    events around the timed steps (no per-kernel events in them), then a
+    second, profiled pass of as many steps for the per-kernel breakdown and
+    the roofline of the dominant kernel class."""
+    from paper_1810_11899_amd.runner import StepRunner
+    prec = B.PREC[prec_name]
     spec = synth.WORKLOADS[args.config]
     runner = StepRunner(wl, prec=prec)
     work = runner.work()
@@ -570,9 +687,6 @@ def main():
         runner.step()
     torch.cuda.synchronize()
 
-    # the timed steps run without the library's per-kernel events (two event
-    # records per launch would add to the step); a second, profiled pass of
-    # the same steps gives the per-kernel times and the roofline
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -602,7 +716,7 @@ def main():
 
     kernels = {}
     roof = None
-    config_name = spec.name + ("" if args.prec == "f32" else "_bf16")
+    config_name = spec.name + ("" if prec_name == "f32" else "_bf16")
     if not args.no_profile:
         prof = B.gcn_profile_read_all()
         for name, (ms, launches, flops, bytes_) in prof.items():
@@ -611,17 +725,39 @@ def main():
             e = {"ms_per_step": round(ms / args.steps, 4), "launches_per_step": launches / args.steps}
             if flops > 0 and name.startswith("gemm"):
                 e["tflops"] = round(flops / (ms / 1e3) / 1e12, 2)
+                # fraction of the time the class would take at the datasheet
+                # peaks (matrix cores or moving its bytes once, the larger)
+                t_bound = max(flops / (PEAK_TFLOPS[prec_name] * 1e12), bytes_ / (PEAK_HBM_GBS * 1e9))
+                e["roofline_time_frac"] = round(t_bound / (ms / 1e3), 4)
             if bytes_ > 0:
                 e["gbs"] = round(bytes_ / (ms / 1e3) / 1e9, 1)
             kernels[name] = e
-        dom = max(((n, v) for n, v in prof.items() if v[1] > 0), key=lambda kv: kv[1][0])
-        name, (ms, launches, flops, bytes_) = dom
+        # dominant kernel: the one with the most time (the large-tile bf16
+        # product's two classes, plain and masked epilogue, are one kernel)
+        groups = {}
+        for n, v in prof.items():
+            if v[1] == 0:
+                continue
+            key = "gemm_nt_bf16_big" if n.startswith("gemm_nt_bf16_big") else n
+            groups[key] = tuple(a + b for a, b in zip(groups.get(key, (0.0, 0, 0.0, 0.0)), v))
+        name, (ms, launches, flops, bytes_) = max(groups.items(), key=lambda kv: kv[1][0])
         per_launch_ms = ms / launches
         if name.startswith("gemm"):
-            achieved = flops / (ms / 1e3) / 1e12
-            peak = PEAK_TFLOPS[args.prec]
-            roof = {"bound": "mfma", "kernel": name, "achieved": round(achieved, 2), "peak": peak,
-                    "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+            # a product is bound by the matrix cores or by moving its operands
+            # and output once, whichever takes longer at the datasheet peaks
+            peak = PEAK_TFLOPS[prec_name]
+            t_mfma = flops / (peak * 1e12)
+            t_hbm = bytes_ / (PEAK_HBM_GBS * 1e9)
+            if t_mfma >= t_hbm:
+                achieved = flops / (ms / 1e3) / 1e12
+                roof = {"bound": "mfma", "kernel": name, "achieved": round(achieved, 2), "peak": peak,
+                        "unit": "TFLOP/s", "frac": round(achieved / peak, 4)}
+            else:
+                achieved = bytes_ / (ms / 1e3) / 1e9
+                roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
+            roof["mfma_frac"] = round(flops / (ms / 1e3) / 1e12 / peak, 4)
+            roof["hbm_frac_algorithmic"] = round(bytes_ / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
         else:
             achieved = bytes_ / (ms / 1e3) / 1e9
             roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
@@ -634,18 +770,23 @@ def main():
             if not (spm and spm[1]):
                 continue
             t_s = spm[0] / 1e3
-            kernels[cls]["hbm_frac_gather_model"] = round(spm[3] / t_s / 1e9 / PEAK_HBM_GBS, 4)
-            # compulsory model: every feature row read once, plus CSR and output
+            # bytes the aggregation delivers to the CUs under the gather model
+            # (one row of the aggregated width per stored edge, plus the CSR
+            # and the output rows): a cache-served rate, not a DRAM one
+            kernels[cls]["gather_model_gbs"] = round(spm[3] / t_s / 1e9, 1)
+            kernels[cls]["gather_gbs"] = round(work["edge_features"] * esz * args.steps / t_s / 1e9, 1)
+            # compulsory model: every feature row read once, plus CSR and
+            # output: a lower bound on DRAM traffic, as a fraction of 8 TB/s
             passes = spm[1] / args.steps
             k_sum = work["edge_features"] / max(wl.graph.nnz, 1)
             comp = args.steps * (wl.n * k_sum * (esz + 4) + passes * (8.0 * wl.graph.nnz + 4.0 * (wl.n + 1)))
             kernels[cls]["hbm_frac_compulsory_model"] = round(comp / t_s / 1e9 / PEAK_HBM_GBS, 4)
 
-    out = {
+    return {
         "metric": METRIC, "value": round(ef_per_s, 1), "unit": "edge-features/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f32" if args.prec == "f32" else "bf16",
+        "dtype": "f32" if prec_name == "f32" else "bf16",
         "data": "synthetic (seeded R-MAT subgraph, N(0,1) features, Glorot weights, uniform labels)",
         "config": {"workload": config_name, "n": wl.n, "nnz": wl.graph.nnz,
                    "layers": [list(d) for d in runner.dims],
@@ -658,19 +799,6 @@ def main():
         "edge_features_per_step": work["edge_features"], "gemm_gflop_per_step": work["gemm_flops"] / 1e9,
         "roofline": roof, "kernels": kernels,
     }
-    if not args.no_peaks:
-        peaks = measure_peaks(B, torch)
-        out["measured_peaks"] = peaks
-        if roof is not None:
-            key = "stream_read_gbs" if roof["bound"] == "hbm" else f"mfma_{args.prec}_tflops"
-            roof["measured_peak"] = peaks[key]
-            roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.config, synth, step_work, B, min_seconds=args.cpu_seconds)
-        if args.config in (0, 1, 2):   # the serial oracle as well (small workloads only)
-            out["cpu_baseline_serial"] = cpu_baseline(args.config, synth, step_work, B,
-                                                      min_seconds=args.cpu_seconds, max_reps=5, threads=1)
-    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

@@ -116,6 +116,7 @@ _SIGNATURES = {
     "gcn_peak_stream_read": (ctypes.c_int, [_P, _I64, _P, _I32, _P]),
     "gcn_peak_mfma": (ctypes.c_int, [ctypes.c_int, _I32, _I32, _P, ctypes.POINTER(ctypes.c_double), _P]),
     "gcn_peak_chase": (ctypes.c_int, [_P, _I64, _I32, _I32, _P, _P]),
+    "gcn_peak_gather": (ctypes.c_int, [_P, _I64, _I32, _I64, _P, _I64, _P, _I32, _P]),
 }
 
 
@@ -547,6 +548,17 @@ def gcn_peak_mfma(prec: int, blocks: int, iters: int, sink: torch.Tensor, stream
     _check(lib().gcn_peak_mfma(prec, blocks, iters, _ptr(sink), ctypes.byref(fl), _stream(stream)),
            "gcn_peak_mfma")
     return fl.value
+
+
+def gcn_peak_gather(X: torch.Tensor, row_bytes: int, idx: torch.Tensor, sink: torch.Tensor, blocks: int,
+                    stream=None):
+    """Enqueue the gather of the first row_bytes of rows idx of the 2-D tensor X
+    (one row per index, rows X.stride(0) elements apart)."""
+    if X.dim() != 2 or X.stride(1) != 1 or idx.dtype != torch.int32 or sink.dtype != torch.float32 \
+            or sink.numel() < blocks * 256 or row_bytes > X.shape[1] * X.element_size():
+        raise TypeError("a row-major 2-D X wide enough, int32 indices and a float32 sink of blocks*256")
+    _check(lib().gcn_peak_gather(_ptr(X), X.shape[0], int(row_bytes), X.stride(0) * X.element_size(), _ptr(idx),
+                                 idx.numel(), _ptr(sink), int(blocks), _stream(stream)), "gcn_peak_gather")
 
 
 def gcn_peak_chase(next_idx: torch.Tensor, steps: int, chains: int, sink: torch.Tensor, stream=None):

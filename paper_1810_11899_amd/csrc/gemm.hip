@@ -1290,11 +1290,17 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         return GCN_EINVAL;
     }
     bool vec = true;
-    double flops = 0.0;
+    double flops = 0.0, bytes = 0.0;
     for (int i = 0; i < nprob; ++i) {
-        vec = vec && vec_ok(layout, probs[i], bf16 ? 2 : 4);
-        flops += 2.0 * probs[i].M * probs[i].N *
-                 ((double)probs[i].seg[0].K + probs[i].seg[1].K - probs[i].k_pad);
+        const GemmProblem &g = probs[i];
+        vec = vec && vec_ok(layout, g, bf16 ? 2 : 4);
+        const double K = (double)g.seg[0].K + g.seg[1].K;
+        flops += 2.0 * g.M * g.N * (K - g.k_pad);
+        // algorithmic bytes: each operand read once, the output written once
+        // (float32 or bfloat16), the mask read once, the bias read once
+        const double esz = bf16 ? 2.0 : 4.0;
+        bytes += esz * K * ((double)g.M + g.N) + (double)g.M * g.N * (g.C16 ? 2.0 : 4.0) +
+                 (g.mask ? 4.0 * g.M * g.N : 0.0) + (g.mask16 ? 2.0 * g.M * g.N : 0.0) + (g.bias ? 4.0 * g.N : 0.0);
     }
     float *partial = nullptr;
     if (split_k > 1) {
@@ -1338,7 +1344,7 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         cls = masked ? K_GEMM_NT_BF16_BIG_MASKED : K_GEMM_NT_BF16_BIG;
     }
     {
-        ProfScope ps(cls, s, flops, 0.0);
+        ProfScope ps(cls, s, flops, bytes);
         dim3 grid((unsigned)blocks);
         if (big) hipLaunchKernelGGL(gemm_bf16_big_kernel, grid, dim3(kBigThreads), 0, s, a);
         else if (layout == L_NN) launch<L_NN>(vec, bf16 != 0, grid, s, a);
@@ -1347,10 +1353,10 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         GCN_LAUNCH_CHECK("gemm_kernel");
     }
     if (any_split) {
-        double bytes = 0.0;
+        double rbytes = 0.0;
         for (int i = 0; i < nprob; ++i)
-            bytes += (double)a.p[i].M * a.p[i].N * 4.0 * (a.p[i].split + 1);
-        ProfScope ps(K_SPLITK_REDUCE, s, 0.0, bytes);
+            rbytes += (double)a.p[i].M * a.p[i].N * 4.0 * (a.p[i].split + 1);
+        ProfScope ps(K_SPLITK_REDUCE, s, 0.0, rbytes);
         int64_t maxe = 0;
         int maxsplit = 1;
         for (int i = 0; i < nprob; ++i) {

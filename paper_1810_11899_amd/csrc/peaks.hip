@@ -1,5 +1,6 @@
-// Machine-rate probes: the streaming read bandwidth and the matrix-core rate
-// this GPU actually sustains.  They give the kernels of the layer a measured
+// Machine-rate probes: the streaming read bandwidth, the row-gather rate,
+// the matrix-core rate and the dependent-load latency this GPU actually
+// sustains.  They give the kernels of the layer a measured
 // ceiling next to the datasheet one (HBM 8 TB/s; 157.3 TFLOP/s fp32 matrix,
 // 2.5 PFLOP/s dense bf16 matrix).  Neither touches the method's data.
 #include "common.h"
@@ -85,6 +86,49 @@ __global__ __launch_bounds__(64) void chase_kernel(const int32_t *__restrict__ n
     }
 }
 
+// Row gathers, the access pattern of the feature propagation.  A wavefront
+// takes 64 consecutive indices with one coalesced load and hands them out by
+// lane shuffles; a group of G lanes reads one row of `chunks` x G x 16 bytes,
+// kGatherU rows in flight per group.  Out-of-range indices are clamped (the
+// probe never reads outside X).
+constexpr int kGatherU = 8;
+template <int CH>
+__global__ __launch_bounds__(kPeakThreads) void gather_kernel(const f4 *__restrict__ x, int64_t n_rows,
+                                                               int64_t ld4, const int32_t *__restrict__ idx,
+                                                               int64_t count, int G, float *__restrict__ sink) {
+    const int lane = threadIdx.x & 63;
+    const int gpw = 64 / G;                                   // groups per wavefront
+    const int g = lane / G, l = lane % G;
+    const int64_t wave = ((int64_t)blockIdx.x * kPeakThreads + threadIdx.x) >> 6;
+    const int64_t waves = (int64_t)gridDim.x * kPeakThreads >> 6;
+    f4 acc = {0, 0, 0, 0};
+    for (int64_t base = wave * 64; base < count; base += waves * 64) {
+        const int64_t q = base + lane;
+        int32_t mine = q < count ? idx[q] : -1;
+        mine = mine < 0 ? -1 : (mine >= n_rows ? (int32_t)(n_rows - 1) : mine);
+        // rows g, g + gpw, g + 2 gpw, ... of the batch belong to group g
+        for (int r0 = 0; r0 < 64; r0 += gpw * kGatherU) {
+            int32_t row[kGatherU];
+#pragma unroll
+            for (int u = 0; u < kGatherU; ++u) {
+                const int src = r0 + u * gpw + g;
+                row[u] = src < 64 ? __shfl(mine, src) : -1;
+            }
+            f4 v[kGatherU][CH];
+#pragma unroll
+            for (int u = 0; u < kGatherU; ++u)
+#pragma unroll
+                for (int c = 0; c < CH; ++c)
+                    v[u][c] = row[u] >= 0 ? x[(int64_t)row[u] * ld4 + c * G + l] : f4{0, 0, 0, 0};
+#pragma unroll
+            for (int u = 0; u < kGatherU; ++u)
+#pragma unroll
+                for (int c = 0; c < CH; ++c) acc += v[u][c];
+        }
+    }
+    sink[(int64_t)blockIdx.x * kPeakThreads + threadIdx.x] = (acc.x + acc.y) + (acc.z + acc.w);
+}
+
 }  // namespace
 }  // namespace gcn
 
@@ -120,6 +164,37 @@ int gcn_peak_mfma(gcn_prec prec, int32_t blocks, int32_t iters, float *sink, dou
         mfma_bf16_kernel<<<blocks, kPeakThreads, 0, s>>>(iters, sink);
     GCN_LAUNCH_CHECK("mfma_kernel");
     if (flops) *flops = per_mfma * 4.0 * iters * (blocks * (kPeakThreads / kWave));
+    return GCN_OK;
+}
+
+int gcn_peak_gather(const void *X, int64_t n_rows, int32_t row_bytes, int64_t ld_bytes, const int32_t *idx,
+                    int64_t count, float *sink, int32_t blocks, void *stream) {
+    if (!X || !idx || !sink || n_rows <= 0 || count < 0 || blocks <= 0) {
+        set_error("gcn_peak_gather: null pointer or bad size");
+        return GCN_EINVAL;
+    }
+    if (row_bytes < 16 || row_bytes > 4096 || row_bytes % 16 || ld_bytes < row_bytes || ld_bytes % 16 ||
+        ((uintptr_t)X & 15u)) {
+        set_error("gcn_peak_gather: row_bytes %d must be a multiple of 16 in [16, 4096], ld_bytes %lld a "
+                  "multiple of 16 >= row_bytes, X 16-byte aligned", row_bytes, (long long)ld_bytes);
+        return GCN_ESHAPE;
+    }
+    const int r16 = row_bytes / 16;
+    int G = 1;
+    while (G < 64 && G < r16) G *= 2;
+    if (r16 % G || !(r16 / G == 1 || r16 / G == 2 || r16 / G == 4)) {
+        set_error("gcn_peak_gather: row_bytes %d is not 16 times a power of two up to 64, 2 KB or 4 KB",
+                  row_bytes);
+        return GCN_ESHAPE;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    const int chunks = r16 / G;
+    const f4 *x4 = (const f4 *)X;
+    const int64_t ld4 = ld_bytes / 16;
+    if (chunks == 1) gather_kernel<1><<<blocks, kPeakThreads, 0, s>>>(x4, n_rows, ld4, idx, count, G, sink);
+    else if (chunks == 2) gather_kernel<2><<<blocks, kPeakThreads, 0, s>>>(x4, n_rows, ld4, idx, count, G, sink);
+    else gather_kernel<4><<<blocks, kPeakThreads, 0, s>>>(x4, n_rows, ld4, idx, count, G, sink);
+    GCN_LAUNCH_CHECK("gather_kernel");
     return GCN_OK;
 }
 
