@@ -82,7 +82,7 @@ def cpu_model() -> str:
 
 
 def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_reps: int = 20,
-                 threads: int = 0):
+                 threads: int = 0, self_loops: bool = False):
     """The CPU oracle on the same workload: whole fwd+bwd steps, repeated until
     at least `min_seconds` of CPU work have been timed (bounded by max_reps).
     threads > 0: that many threads for the oracle's aggregation and BLAS (a
@@ -97,15 +97,15 @@ def cpu_baseline(cfg: int, synth, step_work, B, min_seconds: float = 10.0, max_r
         oracle.set_num_threads(threads)
     try:
         with limit:
-            return _cpu_baseline(cfg, synth, step_work, B, min_seconds, max_reps)
+            return _cpu_baseline(cfg, synth, step_work, B, min_seconds, max_reps, self_loops)
     finally:
         if threads > 0:
             oracle.set_num_threads(prev)
 
 
-def _cpu_baseline(cfg, synth, step_work, B, min_seconds, max_reps):
+def _cpu_baseline(cfg, synth, step_work, B, min_seconds, max_reps, self_loops=False):
     import oracle
-    wl = synth.config(cfg)
+    wl = synth.config(cfg, self_loops=self_loops)
     L = len(wl.layers)
     dims = [(l.f_in, l.h) for l in wl.layers]
     need = [li > 0 for li in range(L)] if L > 1 else [True]
@@ -569,6 +569,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--prec", default="f32", choices=["f32", "bf16"])
     ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--index-bits", type=int, default=32, choices=[16, 32],
+                    help="column-index width of the subgraph's CSR (16: uint16, at most 65,536 vertices)")
+    ap.add_argument("--self-loops", action="store_true", help="add a self-connection to every vertex")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event timing")
@@ -618,16 +621,23 @@ def main():
     if args.workload == "train":
         bench_train(args, B, torch)
         return
-    wl = synth.config(args.config)
-    out = bench_step(args, args.prec, wl, B, torch, synth)
+    wl = synth.config(args.config, self_loops=args.self_loops)
+    out = bench_step(args, args.prec, wl, B, torch, synth, index_bits=args.index_bits)
     variants = {}
-    if args.config == 3 and args.prec == "f32" and not args.no_variants:
-        # the bfloat16-operand variant of the same workload, measured the same way
+    if args.config == 3 and args.prec == "f32" and args.index_bits == 32 and not args.no_variants:
+        # the bfloat16-operand variant of the same workload, and the float32
+        # step with uint16 column indices, measured the same way
+        keys = ("value", "unit", "ms_per_step", "dtype", "gflops", "step_ms_min_median", "host_issue_ms_per_step",
+                "roofline", "kernels", "csr_bytes", "index_bits")
         v = bench_step(args, "bf16", wl, B, torch, synth)
-        variants["bf16"] = {k: v[k] for k in ("value", "unit", "ms_per_step", "dtype", "gflops",
-                                               "step_ms_min_median", "host_issue_ms_per_step", "roofline",
-                                               "kernels") if k in v}
+        variants["bf16"] = {k: v[k] for k in keys if k in v}
         variants["bf16"]["config"] = {"workload": v["config"]["workload"]}
+        v = bench_step(args, "f32", wl, B, torch, synth, index_bits=16)
+        variants["uint16"] = {k: v[k] for k in keys if k in v and k != "kernels"}
+        variants["uint16"]["kernels"] = {k: v["kernels"][k] for k in ("spmm", "transpose_symmetric")
+                                         if k in v["kernels"]}
+        variants["uint16"]["config"] = {"workload": v["config"]["workload"]}
+        variants["uint16"]["csr_bytes_saved"] = out["csr_bytes"] - v["csr_bytes"]
     if variants:
         out["variants"] = variants
     if not args.no_peaks:
@@ -643,10 +653,12 @@ def main():
                 roof["frac_of_measured_peak"] = round(roof["achieved"] / peaks[key], 4)
             spmm_vs_gather(o, peaks["gather"])
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.config, synth, step_work, B, min_seconds=args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(args.config, synth, step_work, B, min_seconds=args.cpu_seconds,
+                                           self_loops=args.self_loops)
         if args.config in (0, 1, 2):   # the serial oracle as well (small workloads only)
             out["cpu_baseline_serial"] = cpu_baseline(args.config, synth, step_work, B,
-                                                      min_seconds=args.cpu_seconds, max_reps=5, threads=1)
+                                                      min_seconds=args.cpu_seconds, max_reps=5, threads=1,
+                                                      self_loops=args.self_loops)
     print(json.dumps(out), flush=True)
 
 
@@ -671,15 +683,15 @@ def spmm_vs_gather(o: dict, gather: dict):
                 k[name] = round(k["gather_gbs"] / ref["gbs"], 4)
 
 
-def bench_step(args, prec_name: str, wl, B, torch, synth) -> dict:
+def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32) -> dict:
     """Time one workload's fwd+bwd step at one precision: the whole step with
     events around the timed steps (no per-kernel events in them), then a
     second, profiled pass of as many steps for the per-kernel breakdown and
     the roofline of the dominant kernel class."""
     from paper_1810_11899_amd.runner import StepRunner
     prec = B.PREC[prec_name]
-    spec = synth.WORKLOADS[args.config]
-    runner = StepRunner(wl, prec=prec)
+    spec = wl.spec
+    runner = StepRunner(wl, prec=prec, index_bits=index_bits)
     work = runner.work()
     stream = torch.cuda.current_stream()
 
@@ -716,7 +728,7 @@ def bench_step(args, prec_name: str, wl, B, torch, synth) -> dict:
 
     kernels = {}
     roof = None
-    config_name = spec.name + ("" if prec_name == "f32" else "_bf16")
+    config_name = wl.spec.name + ("" if prec_name == "f32" else "_bf16") + ("_uint16" if index_bits == 16 else "")
     if not args.no_profile:
         prof = B.gcn_profile_read_all()
         for name, (ms, launches, flops, bytes_) in prof.items():
@@ -788,6 +800,7 @@ def bench_step(args, prec_name: str, wl, B, torch, synth) -> dict:
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32" if prec_name == "f32" else "bf16",
         "data": "synthetic (seeded R-MAT subgraph, N(0,1) features, Glorot weights, uniform labels)",
+        "csr_bytes": runner.csr_bytes(), "index_bits": index_bits,
         "config": {"workload": config_name, "n": wl.n, "nnz": wl.graph.nnz,
                    "layers": [list(d) for d in runner.dims],
                    "orders": ["aggregate_first" if o == B.GCN_AGGREGATE_FIRST else "transform_first"

@@ -76,11 +76,17 @@ typedef enum { GCN_SOFTMAX_CE = 0, GCN_SIGMOID_BCE = 1 } gcn_loss_kind;
 /* Sparse aggregation matrix A in CSR (Sec. V-B streams neighbour lists in this
  * format).  Row i = destination vertex i; its entries are the source vertices
  * j with weight vals[p] (for the mean of Sec. II, vals[p] = 1/deg(i)).
- *   indptr [n_rows+1], indptr[0] = 0, non-decreasing, indptr[n_rows] = nnz
- *   indices[nnz] in [0, n_cols)
- *   vals   [nnz]
+ *   indptr   [n_rows+1], indptr[0] = 0, non-decreasing, indptr[n_rows] = nnz
+ *   indices  [nnz] int32 in [0, n_cols), or
+ *   indices16[nnz] uint16 in [0, n_cols) for n_cols <= 65,536: the column
+ *            indices in half the bytes (the paper's subgraphs use 16-bit
+ *            indices, Sec. V-B); exactly one of the two is set when nnz > 0
+ *            (the other NULL), and every entry point that takes the CSR reads
+ *            either, with the same results bit for bit
+ *   vals     [nnz]
  * 0 <= nnz < 2^31.  Duplicated (i, j) entries add up.  Content is NOT checked
- * on the hot path; see gcn_csr_validate_host. */
+ * on the hot path; see gcn_csr_validate_host.  A struct initialised with the
+ * first six fields only has indices16 = NULL (int32 indices). */
 typedef struct {
     int32_t n_rows;
     int32_t n_cols;
@@ -88,6 +94,7 @@ typedef struct {
     const int32_t *indptr;
     const int32_t *indices;
     const float *vals;
+    const uint16_t *indices16;
 } gcn_csr;
 
 /* Message for the last non-OK return on this thread ("" if none). */
@@ -121,7 +128,8 @@ int gcn_csr_validate(const gcn_csr *A, int require_sorted, int32_t *status, void
  * CSR of A^T, the transposed aggregation used by the backward propagation
  * (Alg. 1 propagates with the transpose of the bi-adjacency matrix; the
  * backward pass of Sec. III-B applies the other orientation).
- * Output: t_indptr[n_cols+1], t_indices[nnz], t_vals[nnz]; row j of A^T holds
+ * Output: t_indptr[n_cols+1], t_indices[nnz] (int32 for either index width of
+ * A), t_vals[nnz]; row j of A^T holds
  * the rows i of A that contain column j, in ascending i (equal entries keep
  * their CSR order), with the values copied bit for bit.  The integer output is
  * unique, so it is bit-exact against any correct transpose. */

@@ -32,7 +32,8 @@ class GcnError(RuntimeError):
 
 class gcn_csr(ctypes.Structure):
     _fields_ = [("n_rows", ctypes.c_int32), ("n_cols", ctypes.c_int32), ("nnz", ctypes.c_int32),
-                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p), ("vals", ctypes.c_void_p)]
+                ("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p), ("vals", ctypes.c_void_p),
+                ("indices16", ctypes.c_void_p)]
 
 
 class gcn_sampler_params(ctypes.Structure):
@@ -185,25 +186,41 @@ class Workspace:
 
 
 class DeviceCSR:
-    """CSR arrays resident on the device (int32 indptr/indices, float32 vals)."""
+    """CSR arrays resident on the device: int32 indptr, float32 vals, and the
+    column indices as int32, or as uint16 (an int16 tensor holding the bits)
+    when the columns number at most 65,536."""
 
     def __init__(self, n_rows, n_cols, indptr, indices, vals):
         self.n_rows, self.n_cols = int(n_rows), int(n_cols)
         self.indptr, self.indices, self.vals = indptr, indices, vals
         self.nnz = int(indices.numel())
+        if indices.dtype not in (torch.int32, torch.int16):
+            raise TypeError("indices must be int32, or int16 holding uint16 bits")
+        if indices.dtype == torch.int16 and self.n_cols > 65536:
+            raise ValueError("uint16 indices need n_cols <= 65536")
+
+    @property
+    def index_bits(self) -> int:
+        return 16 if self.indices.dtype == torch.int16 else 32
 
     @classmethod
-    def from_host(cls, n_rows, n_cols, indptr, indices, vals, device="cuda"):
+    def from_host(cls, n_rows, n_cols, indptr, indices, vals, device="cuda", index_bits=32):
+        import numpy as np
         d = torch.device(device)
         ip = torch.as_tensor(indptr, dtype=torch.int32).to(d)
-        ix = torch.as_tensor(indices, dtype=torch.int32).to(d)
+        if index_bits == 16:
+            ix = torch.from_numpy(np.ascontiguousarray(np.asarray(indices, dtype=np.uint16)).view(np.int16)).to(d)
+        else:
+            ix = torch.as_tensor(indices, dtype=torch.int32).to(d)
         vv = torch.as_tensor(vals, dtype=torch.float32).to(d)
         return cls(n_rows, n_cols, ip, ix, vv)
 
     def struct(self) -> gcn_csr:
+        ix = self.indices.data_ptr() if self.nnz else None
         return gcn_csr(self.n_rows, self.n_cols, self.nnz, self.indptr.data_ptr(),
-                       self.indices.data_ptr() if self.nnz else None,
-                       self.vals.data_ptr() if self.nnz else None)
+                       ix if self.index_bits == 32 else None,
+                       self.vals.data_ptr() if self.nnz else None,
+                       ix if self.index_bits == 16 else None)
 
 
 # ------------------------------------------------------------------- calls

@@ -140,7 +140,10 @@ int check_csr(const gcn_csr *A, const char *name) {
     REQUIRE(A, GCN_EINVAL, "%s: null CSR", name);
     REQUIRE(A->n_rows >= 0 && A->n_cols >= 0 && A->nnz >= 0, GCN_ESHAPE, "%s: negative size", name);
     REQUIRE(A->n_rows == 0 || A->indptr, GCN_EINVAL, "%s: null indptr", name);
-    REQUIRE(A->nnz == 0 || (A->indices && A->vals), GCN_EINVAL, "%s: null indices/vals", name);
+    REQUIRE(!(A->indices && A->indices16), GCN_EINVAL, "%s: both indices and indices16 are set", name);
+    REQUIRE(A->nnz == 0 || ((A->indices || A->indices16) && A->vals), GCN_EINVAL, "%s: null indices/vals", name);
+    REQUIRE(!A->indices16 || A->n_cols <= 65536, GCN_ESHAPE, "%s: uint16 indices need n_cols <= 65536 (%d)", name,
+            A->n_cols);
     return GCN_OK;
 }
 
@@ -316,9 +319,11 @@ int gcn_csr_validate_host(int32_t n_rows, int32_t n_cols, int32_t nnz, const int
 int gcn_csr_validate(const gcn_csr *A, int require_sorted, int32_t *status, void *stream) {
     REQUIRE(A && status, GCN_EINVAL, "gcn_csr_validate: null argument");
     REQUIRE(A->n_rows >= 0 && A->n_cols >= 0 && A->nnz >= 0, GCN_EINVAL, "gcn_csr_validate: negative size");
-    REQUIRE(A->indptr && (A->nnz == 0 || A->indices), GCN_EINVAL, "gcn_csr_validate: null indptr or indices");
+    REQUIRE(A->indptr && (A->nnz == 0 || A->indices || A->indices16), GCN_EINVAL,
+            "gcn_csr_validate: null indptr or indices");
+    REQUIRE(!(A->indices && A->indices16), GCN_EINVAL, "gcn_csr_validate: both indices and indices16 are set");
     REQUIRE(((uintptr_t)status & 7u) == 0, GCN_EINVAL, "gcn_csr_validate: status must be 8-byte aligned");
-    return csr_validate_device(A->n_rows, A->n_cols, A->nnz, A->indptr, A->indices, require_sorted != 0, status,
+    return csr_validate_device(A->n_rows, A->n_cols, A->nnz, A->indptr, idx_of(A), require_sorted != 0, status,
                                as_stream(stream));
 }
 
@@ -336,7 +341,7 @@ int gcn_csr_transpose(const gcn_csr *A, int32_t *t_indptr, int32_t *t_indices, f
     const size_t need = transpose_workspace_bytes(A->n_rows, A->n_cols, A->nnz);
     REQUIRE(A->nnz == 0 || (ws && ws_bytes >= need), GCN_EWORKSPACE,
             "gcn_csr_transpose: workspace %zu < %zu bytes", ws_bytes, need);
-    return csr_transpose(A->n_rows, A->n_cols, A->nnz, A->indptr, A->indices, A->vals, t_indptr, t_indices,
+    return csr_transpose(A->n_rows, A->n_cols, A->nnz, A->indptr, idx_of(A), A->vals, t_indptr, t_indices,
                          t_vals, ws, ws_bytes, as_stream(stream));
 }
 
@@ -355,7 +360,7 @@ int gcn_csr_transpose_symmetric(const gcn_csr *A, float *t_vals, void *ws, size_
     REQUIRE(A->nnz == 0 || A->n_rows == 0 || (ws && ws_bytes >= need && ((uintptr_t)ws & 255u) == 0),
             GCN_EWORKSPACE, "gcn_csr_transpose_symmetric: workspace %zu < %zu bytes or misaligned", ws_bytes,
             need);
-    return csr_transpose_symmetric(A->n_rows, A->nnz, A->indptr, A->indices, A->vals, t_vals, ws, ws_bytes,
+    return csr_transpose_symmetric(A->n_rows, A->nnz, A->indptr, idx_of(A), A->vals, t_vals, ws, ws_bytes,
                                    (hipStream_t)stream);
 }
 
@@ -384,10 +389,10 @@ int gcn_aggregate(const gcn_csr *A, const float *X, int32_t k, int32_t ldx, floa
         void *w = ar.take<char>(sw);
         int rc = cvt_bf16(A->n_cols, k, X, ldx, X16, k, s);
         if (rc) return rc;
-        return spmm_bf16(A->n_rows, A->nnz, A->indptr, A->indices, A->vals, X16, k, k, out, ldo, EPI_STORE,
+        return spmm_bf16(A->n_rows, A->nnz, A->indptr, idx_of(A), A->vals, X16, k, k, out, ldo, EPI_STORE,
                          nullptr, w, sw, s);
     }
-    return spmm_f32(A->n_rows, A->nnz, A->indptr, A->indices, A->vals, X, k, ldx, out, ldo, EPI_STORE,
+    return spmm_f32(A->n_rows, A->nnz, A->indptr, idx_of(A), A->vals, X, k, ldx, out, ldo, EPI_STORE,
                     nullptr, ws, ws_bytes, s);
 }
 
@@ -457,7 +462,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         g[0].relu = 1;
         if (af) {
             void *sw = ar.take<char>(pl.fwd_spmm);
-            rc = spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, H16, f_in, f_in, AGG16, f_in,
+            rc = spmm_bf16(n, A->nnz, A->indptr, idx_of(A), A->vals, H16, f_in, f_in, AGG16, f_in,
                            EPI_STORE_BF16, nullptr, sw, pl.fwd_spmm, s, bA);
             if (rc) return rc;
             if ((rc = transpose_bf16(n, f_in, AGG16, 1, f_in, AGG16T, n, s))) return rc;
@@ -476,7 +481,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         g[1].ldc = h;
         void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
         if ((rc = gemm(L_NT, 2, g, 1, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s))) return rc;
-        return spmm_bf16(n, A->nnz, A->indptr, A->indices, A->vals, T16, h, h, Y + h, ldy, EPI_BIAS_RELU,
+        return spmm_bf16(n, A->nnz, A->indptr, idx_of(A), A->vals, T16, h, h, Y + h, ldy, EPI_BIAS_RELU,
                          bias + h, sw, pl.fwd_spmm, s, bA);
     }
 
@@ -491,7 +496,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
     if (af) {
         void *sw = ar.take<char>(pl.fwd_spmm);
         float *AGG = (float *)saved;
-        rc = spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE, nullptr, sw,
+        rc = spmm_f32(n, A->nnz, A->indptr, idx_of(A), A->vals, H, f_in, ldh, AGG, f_in, EPI_STORE, nullptr, sw,
                       pl.fwd_spmm, s, bA);
         if (rc) return rc;
         g[1].seg[0] = GemmSeg{AGG, f_in, W_neigh, h, f_in};
@@ -510,7 +515,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
     g[1].ldc = h;
     void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
     if ((rc = gemm(L_NN, 2, g, 0, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s))) return rc;
-    return spmm_f32(n, A->nnz, A->indptr, A->indices, A->vals, T, h, h, Y + h, ldy, EPI_BIAS_RELU, bias + h, sw,
+    return spmm_f32(n, A->nnz, A->indptr, idx_of(A), A->vals, T, h, h, Y + h, ldy, EPI_BIAS_RELU, bias + h, sw,
                     pl.fwd_spmm, s, bA);
 }
 
@@ -592,9 +597,9 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     }
     // G = A^T dZ_n into the second half of P
     if (pl.need_G) {
-        rc = bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)Zn, h, ldZn,
+        rc = bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, idx_of(AT), AT->vals, (const uint16_t *)Zn, h, ldZn,
                             Gp, ldG, EPI_STORE_BF16, nullptr, sw, pl.bwd_spmm, s, bAT)
-                : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)Zn, h, ldZn, Gp,
+                : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, idx_of(AT), AT->vals, (const float *)Zn, h, ldZn, Gp,
                            ldG, EPI_STORE, nullptr, sw, pl.bwd_spmm, s, bAT);
         if (rc) return rc;
     }
@@ -682,9 +687,9 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     if (bf) d[1].C16 = (uint16_t *)T2;
     else d[1].C = (float *)T2;
     if ((rc = gemm(L_NT, 2, d, bf, gemm_pick_split(2, d, false), gw, pl.bwd_gemm, s))) return rc;
-    return bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const uint16_t *)T2, f_in,
+    return bf ? spmm_bf16(AT->n_rows, AT->nnz, AT->indptr, idx_of(AT), AT->vals, (const uint16_t *)T2, f_in,
                           f_in, dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s, bAT)
-              : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, AT->indices, AT->vals, (const float *)T2, f_in, f_in,
+              : spmm_f32(AT->n_rows, AT->nnz, AT->indptr, idx_of(AT), AT->vals, (const float *)T2, f_in, f_in,
                          dH, lddh, EPI_ACCUMULATE, nullptr, sw, pl.bwd_spmm, s, bAT);
 }
 

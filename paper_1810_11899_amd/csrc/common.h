@@ -74,6 +74,18 @@ struct ProfScope {
     int slot_;
 };
 
+// ------------------------------------------------------------- CSR indices
+// The column indices of a CSR: int32, or uint16 when the columns number at
+// most 65,536 (half the index bytes; the INT16 indices of Sec. V-B).
+struct IdxRef {
+    const int32_t *i32;
+    const uint16_t *i16;
+    __host__ __device__ __forceinline__ int32_t operator[](int64_t p) const {
+        return i16 ? (int32_t)i16[p] : i32[p];
+    }
+};
+inline IdxRef idx_of(const gcn_csr *A) { return IdxRef{A->indices, A->indices16}; }
+
 // --------------------------------------------------------------- workspace
 // Bump allocator over the caller's workspace; every carve is 256-byte aligned.
 struct Arena {
@@ -106,12 +118,12 @@ size_t spmm_bounds_bytes(int32_t n_rows, int32_t nnz);
 int spmm_bounds(int32_t n_rows, int32_t nnz, const int32_t *indptr, int32_t *bounds, hipStream_t s);
 // out[i, c] (epilogue) sum_p vals[p] * X[indices[p], c].  `bounds`: the row
 // ranges from spmm_bounds for this indptr, or NULL to compute them here.
-int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
              const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s,
              const int32_t *bounds = nullptr);
 // same with bfloat16 rows of X (uint16 bits), float32 accumulation
-int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
               const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
               int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s,
               const int32_t *bounds = nullptr);
@@ -207,12 +219,12 @@ int cvt_bf16_pad(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16
 size_t transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz);
 // device-side CSR content check; status: 8-byte aligned int32[2]
 int csr_validate_device(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
-                        const int32_t *indices, int sorted, int32_t *status, hipStream_t s);
-int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+                        IdxRef indices, int sorted, int32_t *status, hipStream_t s);
+int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, IdxRef indices,
                             const float *vals, float *t_vals, void *ws, size_t ws_bytes, hipStream_t s);
 size_t transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz);
 int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
-                  const int32_t *indices, const float *vals, int32_t *t_indptr, int32_t *t_indices,
+                  IdxRef indices, const float *vals, int32_t *t_indptr, int32_t *t_indices,
                   float *t_vals, void *ws, size_t ws_bytes, hipStream_t s);
 
 }  // namespace gcn

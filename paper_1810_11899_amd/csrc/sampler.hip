@@ -608,8 +608,8 @@ int gcn_frontier_sample(const gcn_csr *G, const gcn_sampler_params *p, int64_t f
         set_error("gcn_frontier_sample: null argument or negative count");
         return GCN_EINVAL;
     }
-    if (G->n_rows != G->n_cols || G->n_rows <= 0 || !G->indptr || (G->nnz > 0 && !G->indices)) {
-        set_error("gcn_frontier_sample: G must be a square CSR with at least one vertex");
+    if (G->n_rows != G->n_cols || G->n_rows <= 0 || !G->indptr || (G->nnz > 0 && !G->indices) || G->indices16) {
+        set_error("gcn_frontier_sample: G must be a square CSR with at least one vertex and int32 indices");
         return GCN_ESHAPE;
     }
     if (p->m <= 0 || p->m > G->n_rows || p->n < p->m || p->ia_slots <= p->m || p->ia_slots > 65535 ||
@@ -663,8 +663,8 @@ int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *
         set_error("gcn_induce_subgraphs: null argument or negative size");
         return GCN_EINVAL;
     }
-    if (G->n_rows != G->n_cols || G->n_rows <= 0 || !G->indptr || (G->nnz > 0 && !G->indices)) {
-        set_error("gcn_induce_subgraphs: G must be a square CSR with at least one vertex");
+    if (G->n_rows != G->n_cols || G->n_rows <= 0 || !G->indptr || (G->nnz > 0 && !G->indices) || G->indices16) {
+        set_error("gcn_induce_subgraphs: G must be a square CSR with at least one vertex and int32 indices");
         return GCN_ESHAPE;
     }
     if (S == 0) return GCN_OK;

@@ -94,7 +94,7 @@ __device__ __forceinline__ WaveRange stage_wave(EdgeStage &st, int wv, int lane,
                                                 int ipw, int64_t items, int32_t n_rows,
                                                 const int32_t *__restrict__ bnd,
                                                 const int32_t *__restrict__ indptr,
-                                                const int32_t *__restrict__ indices,
+                                                IdxRef indices,
                                                 const float *__restrict__ vals) {
     WaveRange w{0, 0, 0, 0};
     if (live) {
@@ -238,7 +238,7 @@ __device__ __forceinline__ void store_raw(float *__restrict__ out, const float (
 template <int VEC, int CT, bool BF16>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_MAIN_WPE)))
 void spmm_main(
-    int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
+    int32_t n_rows, const int32_t *__restrict__ indptr, IdxRef indices,
     const float *__restrict__ vals, const void *__restrict__ Xv, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias, int ovec,
     int64_t items, int ipw, int64_t waves, const int32_t *__restrict__ bnd, float *__restrict__ carry,
@@ -370,7 +370,7 @@ __device__ __forceinline__ bool slice_of_block(const SliceMap &m, int64_t w, int
 
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_SLICED_WPE)))
 void spmm_sliced(
-    int32_t n_rows, const int32_t *__restrict__ indptr, const int32_t *__restrict__ indices,
+    int32_t n_rows, const int32_t *__restrict__ indptr, IdxRef indices,
     const float *__restrict__ vals, const float *__restrict__ X, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
     int64_t items, int ipw, int64_t waves, SliceMap map, const int32_t *__restrict__ bnd,
@@ -549,7 +549,7 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
 
 template <int VEC, int CT, bool BF16>
 void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr,
-                 const int32_t *indices, const float *vals, const void *X, int32_t k, int64_t ldx,
+                 IdxRef indices, const float *vals, const void *X, int32_t k, int64_t ldx,
                  void *out, int64_t ldo, int epi, const float *bias, const SpmmPlan &pl,
                  const int32_t *bnd, float *carry, int32_t *hr, int32_t *tr) {
     // the epilogue's per-lane VEC outputs as one vector store when aligned
@@ -562,7 +562,7 @@ void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr
 
 bool aligned(const void *p, int bytes) { return ((uintptr_t)p % (uintptr_t)bytes) == 0; }
 
-int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
              const float *vals, const void *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
              int epi, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
     if (n_rows <= 0 || k <= 0) return GCN_OK;
@@ -591,7 +591,7 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, cons
     const bool sliced = !bf16 && k % 4 == 0 && ldx % 4 == 0 && aligned(X, 16) && ldo % 4 == 0 &&
                         aligned(out, 16) && k >= 128;
     const double out_bytes = epi == EPI_STORE_BF16 ? 2.0 : (epi == EPI_ACCUMULATE ? 8.0 : 4.0);
-    const double bytes = (double)nnz * k * esz + (double)nnz * 8.0 + (double)(n_rows + 1) * 4.0 +
+    const double bytes = (double)nnz * k * esz + (double)nnz * (indices.i16 ? 6.0 : 8.0) + (double)(n_rows + 1) * 4.0 +
                          (double)n_rows * k * out_bytes;
     {
         ProfScope ps(bf16 ? K_SPMM_BF16 : K_SPMM, s, 2.0 * nnz * k, bytes);
@@ -682,14 +682,14 @@ int spmm_bounds(int32_t n_rows, int32_t nnz, const int32_t *indptr, int32_t *bou
     return GCN_OK;
 }
 
-int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
              const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
     return spmm_any(false, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
                     ws, ws_bytes, s, bounds);
 }
 
-int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
               const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
               int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
     return spmm_any(true, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,

@@ -25,7 +25,7 @@ constexpr int kItems = 8;           // keys per thread per tile
 constexpr int kTile = kTB * kItems; // keys per tile
 constexpr int kRadix = 256;
 
-__global__ __launch_bounds__(kTB) void iota_kernel(int32_t nnz, const int32_t *__restrict__ indices,
+__global__ __launch_bounds__(kTB) void iota_kernel(int32_t nnz, IdxRef indices,
                                                    uint32_t *__restrict__ keys, int32_t *__restrict__ vals) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < nnz; p += stride) {
@@ -251,7 +251,7 @@ __global__ __launch_bounds__(kTB) void sym_rows_kernel(int32_t n, const int32_t 
 // for j in row i.  An index outside [0, n), or a missing (i, j) found by the
 // search, gives NaN.
 __global__ __launch_bounds__(kTB) void sym_vals_kernel(int32_t n, int32_t nnz, const int32_t *__restrict__ indptr,
-                                                       const int32_t *__restrict__ indices,
+                                                       IdxRef indices,
                                                        const float *__restrict__ vals,
                                                        const uint32_t *__restrict__ rowval,
                                                        const int32_t *__restrict__ rowconst,
@@ -308,7 +308,7 @@ size_t transpose_workspace_bytes(int32_t n_rows, int32_t n_cols, int32_t nnz) {
     return b + 256;
 }
 
-int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+int csr_transpose(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr, IdxRef indices,
                   const float *vals, int32_t *t_indptr, int32_t *t_indices, float *t_vals, void *ws,
                   size_t ws_bytes, hipStream_t s) {
     if (nnz == 0) {
@@ -388,7 +388,7 @@ size_t transpose_symmetric_workspace_bytes(int32_t n, int32_t nnz) {
     return 2 * align256((size_t)n * 4) + 256;
 }
 
-int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, const int32_t *indices,
+int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, IdxRef indices,
                             const float *vals, float *t_vals, void *ws, size_t ws_bytes, hipStream_t s) {
     if (n == 0 || nnz == 0) return GCN_OK;
     Arena ar(ws, ws_bytes);
@@ -423,7 +423,7 @@ __global__ void validate_init_kernel(int64_t *key) { *key = kValidKey; }
 
 __global__ __launch_bounds__(256) void validate_rows_kernel(int32_t n_rows, int32_t n_cols, int32_t nnz,
                                                             const int32_t *__restrict__ indptr,
-                                                            const int32_t *__restrict__ indices, int sorted,
+                                                            IdxRef indices, int sorted,
                                                             int64_t *__restrict__ key) {
     const int lane = threadIdx.x & 63;
     const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -482,7 +482,7 @@ __global__ void validate_final_kernel(int32_t n_rows, int64_t *key_status) {
 }  // namespace
 
 int csr_validate_device(int32_t n_rows, int32_t n_cols, int32_t nnz, const int32_t *indptr,
-                        const int32_t *indices, int sorted, int32_t *status, hipStream_t s) {
+                        IdxRef indices, int sorted, int32_t *status, hipStream_t s) {
     int64_t *key = (int64_t *)status;
     hipLaunchKernelGGL(validate_init_kernel, dim3(1), dim3(1), 0, s, key);
     GCN_LAUNCH_CHECK("validate_init_kernel");

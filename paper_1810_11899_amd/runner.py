@@ -19,9 +19,15 @@ from . import binding as B
 class StepRunner:
     def __init__(self, wl, prec: int = B.GCN_F32, device: str = "cuda",
                  first_layer_dH: Optional[bool] = None, nnz_capacity: int = 0,
-                 orders: Optional[List[int]] = None, transpose_shortcut: bool = True):
+                 orders: Optional[List[int]] = None, transpose_shortcut: bool = True,
+                 index_bits: int = 32):
+        """index_bits = 16 keeps A's column indices as uint16 (n <= 65,536):
+        half the index bytes, the same results bit for bit."""
         self.dev = torch.device(device)
         self.prec = prec
+        if index_bits not in (16, 32) or (index_bits == 16 and wl.n > 65536):
+            raise ValueError("index_bits: 32, or 16 for at most 65,536 vertices")
+        self.index_bits = index_bits
         self.transpose_shortcut = transpose_shortcut
         self.spec = wl.spec
         self.L = len(wl.layers)
@@ -79,7 +85,7 @@ class StepRunner:
         n, d = self.n, self.dev
         self.cap = max(int(cap), 1)
         self.indptr = torch.empty(n + 1, dtype=torch.int32, device=d)
-        self.indices = torch.empty(self.cap, dtype=torch.int32, device=d)
+        self.indices = torch.empty(self.cap, dtype=torch.int16 if self.index_bits == 16 else torch.int32, device=d)
         self.vals = torch.empty(self.cap, dtype=torch.float32, device=d)
         self.t_indptr = torch.empty(n + 1, dtype=torch.int32, device=d)
         self.t_indices = torch.empty(self.cap, dtype=torch.int32, device=d)
@@ -95,7 +101,8 @@ class StepRunner:
         self.nnz = g.nnz
         self.indptr.copy_(torch.from_numpy(g.indptr), non_blocking=non_blocking)
         if g.nnz:
-            self.indices[:g.nnz].copy_(torch.from_numpy(g.indices), non_blocking=non_blocking)
+            ix = g.indices.astype(np.uint16).view(np.int16) if self.index_bits == 16 else g.indices
+            self.indices[:g.nnz].copy_(torch.from_numpy(ix), non_blocking=non_blocking)
             self.vals[:g.nnz].copy_(torch.from_numpy(g.vals), non_blocking=non_blocking)
         self.H0.copy_(torch.from_numpy(wl.H), non_blocking=non_blocking)
         if self.head is None:
@@ -152,6 +159,10 @@ class StepRunner:
         self._last = "calls"
 
     # ------------------------------------------------------------ results
+    def csr_bytes(self) -> int:
+        """Device bytes of A's CSR (row pointers, column indices, values)."""
+        return 4 * (self.n + 1) + (2 if self.index_bits == 16 else 4) * self.nnz + 4 * self.nnz
+
     def results(self) -> dict:
         """Host copies of the last step's outputs.  After ``step()`` the
         inter-layer gradient buffers (dHL, dH of layers 1..L-1) hold
@@ -161,7 +172,7 @@ class StepRunner:
         r = {"Y": [c(y) for y in self.Y], "dW_self": [c(t) for t in self.dWs],
              "dW_neigh": [c(t) for t in self.dWn], "db": [c(t) for t in self.db],
              "dH": [None if (inner and li > 0) else c(t) for li, t in enumerate(self.dH)],
-             "t_indptr": c(self.AT.indptr), "t_indices": c(self.AT.indices), "t_vals": c(self.AT.vals)}
+             "t_indptr": c(self.AT.indptr), "t_indices": _as_int32(c(self.AT.indices)), "t_vals": c(self.AT.vals)}
         if self.head is not None:
             r.update(loss=float(self.loss.item()), dW_pred=c(self.dW_pred), db_pred=c(self.db_pred),
                      dHL=None if inner else c(self.dHL))
@@ -172,6 +183,11 @@ class StepRunner:
         return step_work(self.n, self.nnz, self.dims, self.orders,
                          [d is not None for d in self.dH],
                          self.spec.classes if self.head is not None else 0)
+
+
+def _as_int32(ix: np.ndarray) -> np.ndarray:
+    """Column indices as int32 (uint16 indices are held as int16 bits)."""
+    return ix.view(np.uint16).astype(np.int32) if ix.dtype == np.int16 else ix
 
 
 def step_work(n: int, nnz: int, dims, orders, need_dH, classes: int = 0) -> dict:

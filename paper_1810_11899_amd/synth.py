@@ -91,6 +91,17 @@ def csr_from_undirected(n: int, u: np.ndarray, v: np.ndarray) -> Graph:
     return csr_from_pairs(n, np.concatenate([u, v]), np.concatenate([v, u]))
 
 
+def with_self_loops(g: Graph) -> Graph:
+    """The same graph with a self-connection added to every vertex (the
+    GraphSAGE convention Sec. V-B follows), re-normalised to the mean over
+    the row: vals = 1/(deg + 1), the vertex itself included."""
+    rows = np.repeat(np.arange(g.n, dtype=np.int64), g.degrees())
+    if g.nnz and np.any(rows == g.indices):
+        raise ValueError("the graph already has self-loops")
+    diag = np.arange(g.n, dtype=np.int64)
+    return csr_from_pairs(g.n, np.concatenate([rows, diag]), np.concatenate([g.indices.astype(np.int64), diag]))
+
+
 def _first_unique(keys: np.ndarray) -> np.ndarray:
     """Distinct keys in order of first appearance."""
     _, first = np.unique(keys, return_index=True)
@@ -202,6 +213,7 @@ class Spec:
     label_p: float = 0.1            # Bernoulli rate for BCE targets
     d_range: Optional[Tuple[int, int]] = None  # per-subgraph degree draw (epoch stream)
     subgraphs: int = 1
+    self_loops: bool = False        # add a self-connection to every vertex (Sec. V-B)
 
 
 @dataclass
@@ -273,6 +285,8 @@ def build(spec: Spec, s: int = 0, cfg_key: int = 99, n: Optional[int] = None) ->
     if spec.d_range is not None:
         d = int(rg_deg.integers(spec.d_range[0], spec.d_range[1] + 1))
     g = make_graph(spec.graph, n_eff, d, rg_graph, rg_relabel)
+    if spec.self_loops:
+        g = with_self_loops(g)
     f0 = spec.layers[0][0]
     H = rg_h.standard_normal((n_eff, f0), dtype=np.float32)
     layers = []
@@ -311,13 +325,20 @@ WORKLOADS = {
 }
 
 
-def config(cfg: int, s: int = 0, n: Optional[int] = None) -> Workload:
-    return build(WORKLOADS[cfg], s=s, cfg_key=cfg, n=n)
+def config(cfg: int, s: int = 0, n: Optional[int] = None, self_loops: bool = False) -> Workload:
+    """Workload `cfg`; with ``self_loops`` the same draw with a self-connection
+    added to every vertex of the graph."""
+    spec = WORKLOADS[cfg]
+    if self_loops:
+        import dataclasses
+        spec = dataclasses.replace(spec, name=spec.name + "_selfloops", self_loops=True)
+    return build(spec, s=s, cfg_key=cfg, n=n)
 
 
-def custom(n: int, graph: str, d: int, layers, head=None, classes=0, seed: int = 0) -> Workload:
+def custom(n: int, graph: str, d: int, layers, head=None, classes=0, seed: int = 0,
+           self_loops: bool = False) -> Workload:
     """Small workloads for tests (ragged sizes spanning several tiles)."""
-    spec = Spec(f"custom_{graph}{n}_d{d}", n, graph, d, list(layers), head, classes)
+    spec = Spec(f"custom_{graph}{n}_d{d}", n, graph, d, list(layers), head, classes, self_loops=self_loops)
     return build(spec, s=seed, cfg_key=1000)
 
 

@@ -265,3 +265,19 @@ def test_device_validate_checks_arguments_before_launch(L):
     assert "aligned" in L.gcn_last_error().decode()
     bad = B.gcn_csr(10, 10, 20, 0x1000, None, 0x3000)
     assert L.gcn_csr_validate(ctypes.byref(bad), 1, st, None) == B.GCN_EINVAL
+
+
+def test_uint16_indices_host_checks(L):
+    """uint16 indices: only for n_cols <= 65536, never together with int32
+    indices, and refused by the sampler (its G is larger); all before any launch."""
+    import ctypes
+    p = ctypes.c_void_p(256)
+    big = B.gcn_csr(70000, 70000, 10, p, None, p, p)
+    both = B.gcn_csr(100, 100, 10, p, p, p, p)
+    ok16 = B.gcn_csr(100, 100, 10, p, None, p, p)
+    X = ctypes.c_void_p(256)
+    for csr, code in ((big, B.GCN_ESHAPE), (both, B.GCN_EINVAL)):
+        assert L.gcn_aggregate(ctypes.byref(csr), X, 4, 4, X, 4, B.GCN_F32, X, 1 << 30, None) == code
+    assert L.gcn_aggregate(ctypes.byref(ok16), X, 4, 4, X, 4, B.GCN_F32, X, 0, None) == B.GCN_EWORKSPACE
+    params = B.gcn_sampler_params(2, 4, 64, 8, 0, 1)
+    assert L.gcn_frontier_sample(ctypes.byref(ok16), ctypes.byref(params), 0, 1, X, X, X, None) == B.GCN_ESHAPE

@@ -506,3 +506,38 @@ def test_step_with_its_own_masks_is_the_relu_step():
         for x, y in zip(a, b):
             assert np.array_equal(x, y)
     assert base.loss == r.loss and np.array_equal(base.dW_pred, r.dW_pred)
+
+
+# ----------------------------------------------------------- self-loops ----
+def test_self_loop_aggregation_closed_form():
+    """Sec. V-B's self-connection: with a self-loop added to every vertex the
+    mean aggregation is (H[i] + sum of the neighbours' H) / (deg(i) + 1),
+    written here from the loop-free neighbour lists; an isolated vertex keeps
+    its own row."""
+    wl0 = synth.custom(90, "rmat", 5, [(6, 3)], seed=4)
+    g0 = wl0.graph
+    g1 = synth.with_self_loops(g0)
+    H = wl0.H.astype(np.float64)
+    got = oracle.aggregate(g1.indptr, g1.indices, g1.vals, H)
+    for i in range(g0.n):
+        nb = g0.indices[g0.indptr[i]:g0.indptr[i + 1]]
+        want = (H[i] + H[nb].sum(axis=0)) / (len(nb) + 1)
+        assert np.allclose(got[i], want, rtol=1e-6, atol=1e-12), i   # vals are float32(1/(deg+1))
+    iso = np.flatnonzero(np.diff(g0.indptr) == 0)
+    assert iso.size > 0 and np.array_equal(got[iso], H[iso])
+    c = oracle.aggregate(g1.indptr, g1.indices, g1.vals, np.full((g0.n, 3), 2.5))
+    assert np.abs(c - 2.5).max() < 1e-6        # no empty rows: the constant comes back everywhere
+
+
+def test_self_loop_step_against_dense_brute_force():
+    wl = synth.custom(40, "er", 4, [(5, 3), (6, 2)], head="ce", classes=3, seed=9, self_loops=True)
+    g = wl.graph
+    A = sp.csr_matrix((g.vals.astype(np.float64), g.indices, g.indptr), shape=(g.n, g.n)).toarray()
+    assert np.allclose(np.diag(A), 1.0 / (np.count_nonzero(A, axis=1)))
+    H = wl.H.astype(np.float64)
+    r = oracle.step(wl, first_layer_dH=True)
+    for li, lay in enumerate(wl.layers):
+        Ws, Wn = lay.W_self.astype(np.float64), lay.W_neigh.astype(np.float64)
+        Z = np.concatenate([H @ Ws, A @ H @ Wn], axis=1) + lay.bias
+        H = np.maximum(Z, 0)
+        assert rel(r.Y[li], H) < 1e-12

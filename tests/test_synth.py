@@ -101,3 +101,26 @@ def test_epoch_stream_shares_model_weights():
         assert np.array_equal(la.W_self, lb.W_self) and np.array_equal(la.W_neigh, lb.W_neigh)
     assert np.array_equal(a.W_pred, b.W_pred)
     assert not np.array_equal(a.H, b.H)
+
+
+def test_with_self_loops_structure():
+    g0 = synth.custom(300, "rmat", 6, [(4, 4)], seed=2).graph
+    g1 = synth.with_self_loops(g0)
+    assert g1.nnz == g0.nnz + g0.n
+    rows = np.repeat(np.arange(g1.n), g1.degrees())
+    assert np.count_nonzero(rows == g1.indices) == g1.n            # one diagonal entry per row
+    assert np.array_equal(g1.degrees(), g0.degrees() + 1)
+    assert np.all(g1.vals == np.float32(1) / (g0.degrees() + 1).astype(np.float32)[rows])
+    ok = np.all(np.diff(g1.indices)[np.diff(rows) == 0] > 0)
+    assert ok
+    assert B_symmetric(g1)
+    with pytest.raises(ValueError):
+        synth.with_self_loops(g1)
+    wl = synth.config(1, self_loops=True, n=500)
+    assert wl.spec.self_loops and wl.graph.nnz == synth.config(1, n=500).graph.nnz + 500
+
+
+def B_symmetric(g):
+    rows = np.repeat(np.arange(g.n), g.degrees())
+    a = set(zip(rows.tolist(), g.indices.tolist()))
+    return all((j, i) in a for i, j in a)
