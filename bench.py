@@ -572,6 +572,8 @@ def main():
     ap.add_argument("--index-bits", type=int, default=32, choices=[16, 32],
                     help="column-index width of the subgraph's CSR (16: uint16, at most 65,536 vertices)")
     ap.add_argument("--self-loops", action="store_true", help="add a self-connection to every vertex")
+    ap.add_argument("--orders", default="tuned", choices=["tuned", "rule"],
+                    help="layer groupings: measured per workload (tuned) or gcn_layer_pick_order's width rule")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="minimum CPU time of the oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event timing")
@@ -632,7 +634,9 @@ def main():
         v = bench_step(args, "bf16", wl, B, torch, synth)
         variants["bf16"] = {k: v[k] for k in keys if k in v}
         variants["bf16"]["config"] = {"workload": v["config"]["workload"]}
-        v = bench_step(args, "f32", wl, B, torch, synth, index_bits=16)
+        v = bench_step(args, "f32", wl, B, torch, synth, index_bits=16,
+                       orders=[B.GCN_AGGREGATE_FIRST if o == "aggregate_first" else B.GCN_TRANSFORM_FIRST
+                               for o in out["config"]["orders"]])
         variants["uint16"] = {k: v[k] for k in keys if k in v and k != "kernels"}
         variants["uint16"]["kernels"] = {k: v["kernels"][k] for k in ("spmm", "transpose_symmetric")
                                          if k in v["kernels"]}
@@ -683,7 +687,7 @@ def spmm_vs_gather(o: dict, gather: dict):
                 k[name] = round(k["gather_gbs"] / ref["gbs"], 4)
 
 
-def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32) -> dict:
+def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32, orders=None) -> dict:
     """Time one workload's fwd+bwd step at one precision: the whole step with
     events around the timed steps (no per-kernel events in them), then a
     second, profiled pass of as many steps for the per-kernel breakdown and
@@ -691,7 +695,10 @@ def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32) 
     from paper_1810_11899_amd.runner import StepRunner
     prec = B.PREC[prec_name]
     spec = wl.spec
-    runner = StepRunner(wl, prec=prec, index_bits=index_bits)
+    if orders is None:
+        orders = None if args.orders == "rule" else "tuned"
+    runner = StepRunner(wl, prec=prec, index_bits=index_bits, orders=orders)
+    timings = getattr(runner, "order_timings", None)
     work = runner.work()
     stream = torch.cuda.current_stream()
 
@@ -805,7 +812,10 @@ def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32) 
                    "layers": [list(d) for d in runner.dims],
                    "orders": ["aggregate_first" if o == B.GCN_AGGREGATE_FIRST else "transform_first"
                               for o in runner.orders],
-                   "head": spec.head, "classes": spec.classes, "parallelism": "single GPU"},
+                   "head": spec.head, "classes": spec.classes, "parallelism": "single GPU",
+                   "order_choice": "measured" if timings else ("given" if isinstance(orders, list) else "width rule"),
+                   **({"order_step_ms": {"+".join("af" if o == B.GCN_AGGREGATE_FIRST else "tf" for o in k):
+                                         round(v, 4) for k, v in timings.items()}} if timings else {})},
         "gflops": round(gflops, 1),
         "step_ms_min_median": [round(step_ms[0], 4), round(step_ms[len(step_ms) // 2], 4)],
         "host_issue_ms_per_step": round(host * 1e3 / args.steps, 4),

@@ -22,7 +22,15 @@ class StepRunner:
                  orders: Optional[List[int]] = None, transpose_shortcut: bool = True,
                  index_bits: int = 32):
         """index_bits = 16 keeps A's column indices as uint16 (n <= 65,536):
-        half the index bytes, the same results bit for bit."""
+        half the index bytes, the same results bit for bit.  orders: one
+        gcn_order per layer, None for gcn_layer_pick_order's width rule, or
+        "tuned" for the combination tune_orders measures fastest on this
+        workload."""
+        if isinstance(orders, str):
+            if orders != "tuned":
+                raise ValueError(f"orders: a list, None or 'tuned' (got {orders!r})")
+            orders, self.order_timings = tune_orders(wl, prec=prec, device=device, first_layer_dH=first_layer_dH,
+                                                     index_bits=index_bits)
         self.dev = torch.device(device)
         self.prec = prec
         if index_bits not in (16, 32) or (index_bits == 16 and wl.n > 65536):
@@ -183,6 +191,38 @@ class StepRunner:
         return step_work(self.n, self.nnz, self.dims, self.orders,
                          [d is not None for d in self.dH],
                          self.spec.classes if self.head is not None else 0)
+
+
+def tune_orders(wl, prec: int = B.GCN_F32, device: str = "cuda", first_layer_dH: Optional[bool] = None,
+                index_bits: int = 32, warmup: int = 2, reps: int = 5):
+    """Measure the whole model step for every combination of the layers'
+    groupings (aggregate-first or transform-first, 2^L combinations) on this
+    workload's graph and widths, and return the fastest combination with the
+    per-combination median step times (ms).  The two groupings compute the
+    same layer (Alg. 1's (A H) W and A (H W)); which is faster depends on the
+    widths, the graph and which fused epilogues each grouping allows, so it
+    is measured rather than predicted."""
+    import itertools
+    L = len(wl.layers)
+    dev = torch.device(device)
+    stream = torch.cuda.current_stream(dev)
+    timings = {}
+    for combo in itertools.product((B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST), repeat=L):
+        r = StepRunner(wl, prec=prec, device=device, first_layer_dH=first_layer_dH, orders=list(combo),
+                       index_bits=index_bits)
+        for _ in range(warmup):
+            r.step()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        ev[0].record(stream)
+        for i in range(reps):
+            r.step()
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize(dev)
+        t = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(reps))
+        timings[tuple(combo)] = t[reps // 2]
+        del r
+    best = min(timings, key=timings.get)
+    return list(best), timings
 
 
 def _as_int32(ix: np.ndarray) -> np.ndarray:

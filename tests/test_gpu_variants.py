@@ -159,3 +159,17 @@ def test_self_loop_aggregation_step(prec, cfg):
         compare_step(r.results(), oracle.step(wl, envelope=True))
     else:
         compare_bf16_chain(r, wl)
+
+
+def test_measured_order_choice():
+    """orders="tuned": every grouping combination is timed on the workload and
+    the fastest is kept; the tuned step still matches the oracle."""
+    wl = synth.config(1)
+    r = StepRunner(wl, orders="tuned")
+    t = r.order_timings
+    assert len(t) == 4 and tuple(r.orders) == min(t, key=t.get)
+    assert all(v > 0 for v in t.values())
+    print("order step times (ms):", t, "chosen:", r.orders, flush=True)
+    r.step()
+    torch.cuda.synchronize()
+    compare_step(r.results(), oracle.step(wl, envelope=True))
