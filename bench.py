@@ -631,8 +631,11 @@ def main():
         # step with uint16 column indices, measured the same way
         keys = ("value", "unit", "ms_per_step", "dtype", "gflops", "step_ms_min_median", "host_issue_ms_per_step",
                 "roofline", "kernels", "csr_bytes", "index_bits")
-        v = bench_step(args, "bf16", wl, B, torch, synth)
+        # the bfloat16 step keeps activations as bfloat16 end to end (each
+        # layer's output only as the next consumer's bfloat16 operand rows)
+        v = bench_step(args, "bf16", wl, B, torch, synth, float_outputs=False)
         variants["bf16"] = {k: v[k] for k in keys if k in v}
+        variants["bf16"]["float_outputs"] = False
         variants["bf16"]["config"] = {"workload": v["config"]["workload"]}
         v = bench_step(args, "f32", wl, B, torch, synth, index_bits=16,
                        orders=[B.GCN_AGGREGATE_FIRST if o == "aggregate_first" else B.GCN_TRANSFORM_FIRST
@@ -687,7 +690,8 @@ def spmm_vs_gather(o: dict, gather: dict):
                 k[name] = round(k["gather_gbs"] / ref["gbs"], 4)
 
 
-def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32, orders=None) -> dict:
+def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32, orders=None,
+               float_outputs: bool = True) -> dict:
     """Time one workload's fwd+bwd step at one precision: the whole step with
     events around the timed steps (no per-kernel events in them), then a
     second, profiled pass of as many steps for the per-kernel breakdown and
@@ -697,7 +701,7 @@ def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32, 
     spec = wl.spec
     if orders is None:
         orders = None if args.orders == "rule" else "tuned"
-    runner = StepRunner(wl, prec=prec, index_bits=index_bits, orders=orders)
+    runner = StepRunner(wl, prec=prec, index_bits=index_bits, orders=orders, float_outputs=float_outputs)
     timings = getattr(runner, "order_timings", None)
     work = runner.work()
     stream = torch.cuda.current_stream()

@@ -262,11 +262,19 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl,
  * equals the separate calls' bit for bit, and those bias gradients equal
  * theirs up to the order of the sum.  Layer 0's dH, when given, is the
  * gradient with respect to H0 as in gcn_layer_bwd. */
+/* With GCN_BF16 a layer's Y may be NULL when its output gradient arrives
+ * masked in bfloat16 form: the last layer under a head, and layer l < L-1
+ * when layer l+1's input-gradient product runs unsplit (the products of a
+ * subgraph of tens of thousands of vertices do; GCN_EINVAL when not).  The
+ * step's product epilogues write every layer's output as bfloat16 rows (and
+ * transposed rows) for the next layer and the head anyway; a NULL Y skips the
+ * float32 copy, and the output of layer l < L-1 is then readable as the first
+ * n x 2h bfloat16 values (leading dim 2h) of layer l+1's saved buffer. */
 typedef struct {
     int32_t f_in, h;
     gcn_order order;
     const float *W_self, *W_neigh, *bias;   /* f_in x h (leading dim h), f_in x h, [2h] */
-    float *Y;                               /* n x 2h (ldy) */
+    float *Y;                               /* n x 2h (ldy); NULL allowed, see above */
     int32_t ldy;
     void *saved;                            /* gcn_layer_saved_bytes */
     size_t saved_bytes;

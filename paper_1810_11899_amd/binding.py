@@ -368,13 +368,17 @@ class ModelStep:
         self.arr = (gcn_layer_args * self.L)()
         self._keep = [layers, head]
         for i, d in enumerate(layers):
-            for nm in ("W_self", "W_neigh", "bias", "Y", "dW_self", "dW_neigh", "dbias"):
+            for nm in ("W_self", "W_neigh", "bias", "dW_self", "dW_neigh", "dbias"):
                 _dev_f32(d[nm], nm)
+            Y = d.get("Y")      # None: no float32 copy of the output (bfloat16 steps only)
+            if Y is not None:
+                _dev_f32(Y, "Y")
             f_in, h = int(d["W_self"].shape[0]), int(d["W_self"].shape[1])
             sv, dH = d.get("saved"), d.get("dH")
             self.arr[i] = gcn_layer_args(
                 f_in, h, int(d["order"]), d["W_self"].data_ptr(), d["W_neigh"].data_ptr(), d["bias"].data_ptr(),
-                d["Y"].data_ptr(), _ld(d["Y"]), None if sv is None else sv.data_ptr(),
+                None if Y is None else Y.data_ptr(), 2 * h if Y is None else _ld(Y),
+                None if sv is None else sv.data_ptr(),
                 0 if sv is None else sv.numel() * sv.element_size(), None if dH is None else dH.data_ptr(),
                 0 if dH is None else _ld(dH), d["dW_self"].data_ptr(), d["dW_neigh"].data_ptr(),
                 d["dbias"].data_ptr())

@@ -271,7 +271,7 @@ size_t saved_bytes(int32_t n, int32_t f_in, int32_t h, int order, int prec) {
 }
 
 int check_layer_common(const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh, const float *W_self,
-                       const float *W_neigh, int32_t h, int order, int prec, const char *who) {
+                       const float *W_neigh, int32_t h, int order, int prec, const char *who, bool need_H = true) {
     int rc = check_csr(A, who);
     if (rc) return rc;
     REQUIRE(A->n_rows == A->n_cols, GCN_ESHAPE, "%s: aggregation matrix must be square (%d x %d)", who,
@@ -281,7 +281,7 @@ int check_layer_common(const gcn_csr *A, const float *H, int32_t f_in, int32_t l
     REQUIRE(order == GCN_AGGREGATE_FIRST || order == GCN_TRANSFORM_FIRST, GCN_EINVAL, "%s: bad order %d",
             who, order);
     REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "%s: bad precision %d", who, prec);
-    REQUIRE(A->n_rows == 0 || (H && W_self && W_neigh), GCN_EINVAL, "%s: null H or weights", who);
+    REQUIRE(A->n_rows == 0 || ((H || !need_H) && W_self && W_neigh), GCN_EINVAL, "%s: null H or weights", who);
     return GCN_OK;
 }
 
@@ -414,18 +414,31 @@ size_t gcn_layer_workspace_bytes(int32_t n, int32_t nnz, int32_t f_in, int32_t h
     return plan_layer(n, nnz, f_in, h, order, true, prec).total;
 }
 
+// Links between the bfloat16 calls of a model step: a layer's product
+// epilogues also write its output as the bfloat16 rows and transposed rows
+// the next consumer multiplies with (the next layer's input copies in its
+// saved buffer, or the head's), and that consumer skips its conversion.
+struct Bf16Link {
+    bool in_ready = false;        // saved already holds this layer's H16 and H16^T
+    uint16_t *out16 = nullptr;    // bf16(Y) rows, n x 2h (leading dim 2h)
+    uint16_t *out16T = nullptr;   // bf16(Y)^T, 2h x n (leading dim n)
+};
+
 // launch == false: the argument checks only, nothing enqueued
 static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in, int32_t ldh,
                      const float *W_self, const float *W_neigh, const float *bias, int32_t h, float *Y, int32_t ldy,
                      void *saved, size_t saved_bytes_, gcn_order order, gcn_prec prec, void *ws, size_t ws_bytes,
-                     void *stream, const int32_t *bA = nullptr) {
+                     void *stream, const int32_t *bA = nullptr, const Bf16Link &lk = Bf16Link{}) {
     // bA: A's merge-path row ranges (spmm_bounds), or NULL
-    int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_fwd");
+    // a bfloat16 layer whose input copies are ready does not read H
+    int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_fwd",
+                                !(prec == GCN_BF16 && lk.in_ready));
     if (rc) return rc;
     const int32_t n = A->n_rows;
     REQUIRE(ldy >= 2 * h, GCN_ESHAPE, "gcn_layer_fwd: ldy=%d < 2h=%d", ldy, 2 * h);
     if (n == 0) return GCN_OK;
-    REQUIRE(Y && bias, GCN_EINVAL, "gcn_layer_fwd: null Y or bias");
+    REQUIRE(bias && (Y || (prec == GCN_BF16 && lk.out16)), GCN_EINVAL, "gcn_layer_fwd: null Y or bias");
+    REQUIRE(!lk.out16T || lk.out16, GCN_EINVAL, "gcn_layer_fwd: a transposed bfloat16 output needs the rows too");
     const size_t sneed = saved_bytes(n, f_in, h, order, prec);
     REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
             "gcn_layer_fwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
@@ -448,8 +461,8 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         uint16_t *AGG16T = af ? (uint16_t *)((char *)saved + 3 * one) : nullptr;
         uint16_t *WsT = ar.take<uint16_t>((size_t)f_in * h);
         uint16_t *WnT = ar.take<uint16_t>((size_t)f_in * h);
-        // H16T and H16 in one pass over H
-        if ((rc = transpose_bf16_copy(n, f_in, H, 0, ldh, H16T, n, H16, f_in, s))) return rc;
+        // H16T and H16 in one pass over H (unless the layer below wrote them)
+        if (!lk.in_ready && (rc = transpose_bf16_copy(n, f_in, H, 0, ldh, H16T, n, H16, f_in, s))) return rc;
         if ((rc = transpose_bf16(f_in, h, W_self, 0, h, WsT, f_in, s))) return rc;
         if ((rc = transpose_bf16(f_in, h, W_neigh, 0, h, WnT, f_in, s))) return rc;
         GemmProblem g[2] = {};
@@ -460,6 +473,18 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         g[0].ldc = ldy;
         g[0].bias = bias;
         g[0].relu = 1;
+        // the output's bfloat16 rows, per half, from the product epilogue;
+        // their transposed copy in one pass over both halves at the end
+        auto link_out = [&](GemmProblem &q, int half) {
+            if (lk.out16) {
+                q.C16 = lk.out16 + (size_t)half * h;
+                q.ldc16 = 2 * h;
+            }
+        };
+        auto link_out_t = [&]() {
+            return lk.out16T ? transpose_bf16(n, 2 * h, lk.out16, 1, 2 * h, lk.out16T, n, s) : GCN_OK;
+        };
+        link_out(g[0], 0);
         if (af) {
             void *sw = ar.take<char>(pl.fwd_spmm);
             rc = spmm_bf16(n, A->nnz, A->indptr, idx_of(A), A->vals, H16, f_in, f_in, AGG16, f_in,
@@ -467,12 +492,14 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
             if (rc) return rc;
             if ((rc = transpose_bf16(n, f_in, AGG16, 1, f_in, AGG16T, n, s))) return rc;
             g[1].seg[0] = GemmSeg{AGG16, f_in, WnT, f_in, f_in};
-            g[1].C = Y + h;
+            g[1].C = Y ? Y + h : nullptr;   // no float32 copy when Y is NULL
             g[1].ldc = ldy;
             g[1].bias = bias + h;
             g[1].relu = 1;
+            link_out(g[1], 1);
             void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
-            return gemm(L_NT, 2, g, 1, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s);
+            rc = gemm(L_NT, 2, g, 1, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s);
+            return rc ? rc : link_out_t();
         }
         uint16_t *T16 = (uint16_t *)ar.take<char>(pl.fwd_T);
         void *sw = ar.take<char>(pl.fwd_spmm);
@@ -481,8 +508,11 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         g[1].ldc = h;
         void *gw = pl.fwd_gemm ? ar.take<char>(pl.fwd_gemm) : nullptr;
         if ((rc = gemm(L_NT, 2, g, 1, gemm_pick_split(2, g, false), gw, pl.fwd_gemm, s))) return rc;
-        return spmm_bf16(n, A->nnz, A->indptr, idx_of(A), A->vals, T16, h, h, Y + h, ldy, EPI_BIAS_RELU,
-                         bias + h, sw, pl.fwd_spmm, s, bA);
+        // the neighbour half: ReLU(A T + b), and its bfloat16 rows from the
+        // same epilogue
+        rc = spmm_bf16(n, A->nnz, A->indptr, idx_of(A), A->vals, T16, h, h, Y ? Y + h : nullptr, ldy, EPI_BIAS_RELU,
+                       bias + h, sw, pl.fwd_spmm, s, bA, lk.out16 ? lk.out16 + h : nullptr, 2 * h);
+        return rc ? rc : link_out_t();
     }
 
     GemmProblem g[2] = {};
@@ -524,14 +554,23 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
                      const void *saved, size_t saved_bytes_, const float *dY, int32_t lddy, float *dH,
                      int32_t lddh, float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec,
                      void *ws, size_t ws_bytes, void *stream, bool dz_ready = false,
-                     float *below_dbias = nullptr, const int32_t *bAT = nullptr) {
+                     float *below_dbias = nullptr, const int32_t *bAT = nullptr, bool dzT_ready = false,
+                     int32_t below_tcols = 0) {
     // bAT: A^T's merge-path row ranges (spmm_bounds), or NULL
+    // dzT_ready (bfloat16, with dz_ready): the producer of dY also wrote
+    // dZ^T (2h x n, leading dim n) behind the packed dZ rows in the same
+    // buffer, at least its first h rows (all 2h for aggregate-first).
+    // below_tcols (bfloat16, with below_dbias): also write the first
+    // below_tcols columns of the layer below's dZ transposed, behind its rows
+    // in the dH buffer.
     // dz_ready: dY already holds dZ = dY * [Y > 0] (float32 with leading
     // dimension lddy, or bfloat16 n x 2h with leading dimension 2h) and dbias
     // is already written (by the producer of dY).  below_dbias: write dH
     // multiplied by [H > 0] (bfloat16 n x f_in rows with bfloat16 operands)
     // and its column sums to below_dbias (dH_mask_fusable only).
-    int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_bwd");
+    // the bfloat16 backward reads H only through its saved bfloat16 copies
+    int rc = check_layer_common(A, H, f_in, ldh, W_self, W_neigh, h, order, prec, "gcn_layer_bwd",
+                                prec == GCN_F32);
     if (rc) return rc;
     rc = check_csr(AT, "gcn_layer_bwd (transpose)");
     if (rc) return rc;
@@ -543,7 +582,8 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
             2 * h);
     REQUIRE(!dH || lddh >= f_in, GCN_ESHAPE, "gcn_layer_bwd: lddh=%d < f_in=%d", lddh, f_in);
     REQUIRE(dW_self && dW_neigh && dbias, GCN_EINVAL, "gcn_layer_bwd: null weight/bias gradient");
-    REQUIRE(n == 0 || (Y && dY), GCN_EINVAL, "gcn_layer_bwd: null Y or dY");
+    REQUIRE(n == 0 || ((Y || dz_ready) && dY), GCN_EINVAL,
+            "gcn_layer_bwd: null Y or dY (Y may be NULL only when the output gradient arrives masked)");
     const size_t sneed = saved_bytes(n, f_in, h, order, prec);
     REQUIRE(saved_bytes_ >= sneed && (sneed == 0 || saved), GCN_EWORKSPACE,
             "gcn_layer_bwd: saved buffer %zu < %zu bytes", saved_bytes_, sneed);
@@ -613,14 +653,15 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
         const uint16_t *AGG16T = af ? (const uint16_t *)((const char *)saved + 3 * one) : nullptr;
         uint16_t *PT = (uint16_t *)ar.take<char>(pl.bwd_PT);
         uint16_t *DT = pl.bwd_DT ? (uint16_t *)ar.take<char>(pl.bwd_DT) : nullptr;
+        if (dz_ready && dzT_ready) PT = (uint16_t *)const_cast<float *>(dY) + (size_t)n * 2 * h;
         if (!dz_ready) {
             if ((rc = transpose_bf16(n, 2 * h, P, 1, ldP, PT, n, s))) return rc;
             if (DT && (rc = transpose_bf16(n, h, D, 1, h, DT, n, s))) return rc;
         } else if (af) {   // PT = [dZ_s || dZ_n]^T
-            if ((rc = transpose_bf16(n, 2 * h, Zs, 1, ldZs, PT, n, s))) return rc;
+            if (!dzT_ready && (rc = transpose_bf16(n, 2 * h, Zs, 1, ldZs, PT, n, s))) return rc;
             DT = nullptr;
         } else {           // PT = [dZ_s || G]^T
-            if ((rc = transpose_bf16(n, h, Zs, 1, ldZs, PT, n, s))) return rc;
+            if (!dzT_ready && (rc = transpose_bf16(n, h, Zs, 1, ldZs, PT, n, s))) return rc;
             if ((rc = transpose_bf16(n, h, Gp, 1, ldG, PT + (size_t)h * n, n, s))) return rc;
         }
         layout = L_NT;
@@ -668,6 +709,11 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
                 d.C = nullptr;
                 d.C16 = (uint16_t *)dH;
                 d.ldc = f_in;
+                if (below_tcols > 0) {   // and its transposed rows behind them
+                    d.C16T = (uint16_t *)dH + (size_t)n * f_in;
+                    d.ldc16t = n;
+                    d.n16t = below_tcols;
+                }
             } else {
                 d.mask = H;
                 d.ldm = ldh;
@@ -734,7 +780,13 @@ size_t gcn_loss_workspace_bytes(int32_t n, int32_t f, int32_t C, gcn_prec prec) 
 static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t ldhl, const float *W_pred,
                      const float *b_pred, int32_t C, gcn_loss_kind kind, const int32_t *labels,
                      const float *targets, float *loss, float *dHL, int32_t lddhl, float *dW_pred, float *db_pred,
-                     gcn_prec prec, void *ws, size_t ws_bytes, void *stream, float *below_dbias = nullptr) {
+                     gcn_prec prec, void *ws, size_t ws_bytes, void *stream, float *below_dbias = nullptr,
+                     const uint16_t *HL16_ready = nullptr, const uint16_t *HL16T_ready = nullptr,
+                     int32_t below_tcols = 0) {
+    // HL16_ready / HL16T_ready (bfloat16): HL's bfloat16 rows and transposed
+    // rows, already written by the last layer's epilogues.  below_tcols (with
+    // below_dbias): also write the first below_tcols columns of the last
+    // layer's dZ transposed, behind its rows in the dHL buffer.
     // below_dbias: write dHL multiplied by [HL > 0] (HL is the last layer's
     // ReLU output), i.e. that layer's dZ (bfloat16 n x f rows, leading
     // dimension f, with bfloat16 operands), and its column sums to below_dbias
@@ -745,7 +797,7 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
             kind);
     REQUIRE(prec == GCN_F32 || prec == GCN_BF16, GCN_EINVAL, "gcn_loss_grad: bad precision");
     REQUIRE(W_pred && b_pred && loss && dW_pred && db_pred, GCN_EINVAL, "gcn_loss_grad: null pointer");
-    REQUIRE(n == 0 || (HL && dHL), GCN_EINVAL, "gcn_loss_grad: null HL or dHL");
+    REQUIRE(n == 0 || ((HL || HL16_ready) && dHL), GCN_EINVAL, "gcn_loss_grad: null HL or dHL");
     REQUIRE(n == 0 || (kind == GCN_SOFTMAX_CE ? labels != nullptr : targets != nullptr), GCN_EINVAL,
             "gcn_loss_grad: null labels/targets");
     const LossPlan pl = plan_loss(n, f, C, prec);
@@ -757,8 +809,12 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     const bool bf = prec == GCN_BF16;
     float *X = ar.take<float>((size_t)n * C);
     float *rows = ar.take<float>((size_t)n + 1);
-    uint16_t *HL16 = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
-    uint16_t *HL16T = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
+    const uint16_t *HL16 = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
+    const uint16_t *HL16T = bf ? ar.take<uint16_t>((size_t)n * f) : nullptr;
+    if (bf && HL16_ready) {
+        HL16 = HL16_ready;
+        HL16T = HL16T_ready;
+    }
     const int32_t Cp = pad_classes(C);
     uint16_t *Wp16 = bf ? ar.take<uint16_t>((size_t)f * Cp) : nullptr;
     uint16_t *Wp16T = bf ? ar.take<uint16_t>((size_t)f * C) : nullptr;
@@ -783,7 +839,10 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     g.bias = b_pred;
     if (bf) {
         // NT form: B = W_pred^T (C x f)
-        if ((rc = transpose_bf16_copy(n, f, HL, 0, ldhl, HL16T, n, HL16, f, s))) return rc;
+        if (!HL16_ready &&
+            (rc = transpose_bf16_copy(n, f, HL, 0, ldhl, const_cast<uint16_t *>(HL16T), n, const_cast<uint16_t *>(HL16),
+                                      f, s)))
+            return rc;
         if ((rc = cvt_bf16_pad(f, C, W_pred, C, Wp16, Cp, Cp, s))) return rc;
         if ((rc = transpose_bf16(f, C, Wp16, 1, Cp, Wp16T, f, s))) return rc;
         g.seg[0] = GemmSeg{HL16, f, Wp16T, f, f};
@@ -827,6 +886,11 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
             d.C = nullptr;
             d.C16 = (uint16_t *)dHL;
             d.ldc = f;
+            if (below_tcols > 0) {
+                d.C16T = (uint16_t *)dHL + (size_t)n * f;
+                d.ldc16t = n;
+                d.n16t = below_tcols;
+            }
         } else {
             d.mask = HL;
             d.ldm = ldhl;
@@ -903,6 +967,12 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl, const flo
 }
 
 // ------------------------------------------------------------ model step
+static size_t model_hl16_bytes(int32_t n, int32_t L, const gcn_layer_args *layers, const gcn_head_args *head,
+                               gcn_prec prec) {
+    if (prec != GCN_BF16 || !head || n <= 0) return 0;
+    return 2 * align256((size_t)n * 2 * layers[L - 1].h * 2);
+}
+
 size_t gcn_model_workspace_bytes(int32_t n, int32_t nnz, int32_t L, const gcn_layer_args *layers,
                                  const gcn_head_args *head, gcn_prec prec) {
     if (n < 0 || nnz < 0 || L < 1 || !layers) return 0;
@@ -910,7 +980,10 @@ size_t gcn_model_workspace_bytes(int32_t n, int32_t nnz, int32_t L, const gcn_la
     for (int32_t l = 0; l < L; ++l)
         b = std::max(b, plan_layer(n, nnz, layers[l].f_in, layers[l].h, layers[l].order, true, prec).total);
     if (head) b = std::max(b, plan_loss(n, 2 * layers[L - 1].h, head->C, prec).total);
-    return b + 2 * spmm_bounds_bytes(n, nnz);   // the row ranges of A and A^T, shared by the calls
+    // the row ranges of A and A^T, shared by the calls, and with bfloat16
+    // operands the last layer's output as the head's bfloat16 rows and
+    // transposed rows
+    return b + 2 * spmm_bounds_bytes(n, nnz) + model_hl16_bytes(n, L, layers, head, prec);
 }
 
 namespace {
@@ -941,16 +1014,46 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         bA = ra;
         bAT = rt;
     }
+    // bfloat16: each layer's product epilogues write its output straight into
+    // the bfloat16 copies (rows and transposed rows) the next consumer reads:
+    // the next layer's saved buffer, or the head's region below
+    const bool bf = prec == GCN_BF16;
+    uint16_t *HL16 = nullptr, *HL16T = nullptr;
+    if (const size_t hb = model_hl16_bytes(n, L, layers, head, prec)) {
+        REQUIRE(ws && ws_bytes >= hb, GCN_EWORKSPACE, "gcn_model_step: workspace %zu bytes too small", ws_bytes);
+        HL16 = (uint16_t *)ws;
+        HL16T = (uint16_t *)((char *)ws + hb / 2);
+        ws = (char *)ws + hb;
+        ws_bytes -= hb;
+    }
     const float *H = H0;  // forward: layer l reads layer l-1's output
     int32_t ldh = ldh0;
     for (int32_t l = 0; l < L; ++l) {
         const gcn_layer_args &a = layers[l];
+        Bf16Link lk;
+        if (bf && n > 0) {
+            lk.in_ready = l > 0;
+            if (l + 1 < L) {
+                const gcn_layer_args &nx = layers[l + 1];
+                lk.out16 = (uint16_t *)nx.saved;
+                lk.out16T = (uint16_t *)((char *)nx.saved + align256((size_t)n * nx.f_in * 2));
+            } else if (head) {
+                lk.out16 = HL16;
+                lk.out16T = HL16T;
+            }
+        }
         if ((rc = layer_fwd(launch, A, H, a.f_in, ldh, a.W_self, a.W_neigh, a.bias, a.h, a.Y, a.ldy, a.saved,
-                            a.saved_bytes, a.order, prec, ws, ws_bytes, stream, bA)))
+                            a.saved_bytes, a.order, prec, ws, ws_bytes, stream, bA, lk)))
             return rc;
         H = a.Y;
         ldh = a.ldy;
     }
+    // columns of a layer's dZ that its backward reads transposed: all 2h for
+    // aggregate-first (dW_self and dW_neigh), the self half for
+    // transform-first (dW_neigh takes A^T dZ_n, transposed after the SpMM)
+    auto tcols = [&](int32_t l) {
+        return bf ? (layers[l].order == GCN_AGGREGATE_FIRST ? 2 * layers[l].h : layers[l].h) : 0;
+    };
     const float *g = dY;  // PREDICT + LOSS, or the given output gradient
     int32_t ldg = lddy;
     // the head, and a layer whose input-gradient product runs unsplit, write
@@ -962,7 +1065,7 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         if ((rc = loss_grad(launch, last.Y, n, 2 * last.h, last.ldy, head->W_pred, head->b_pred, head->C,
                             head->kind, head->labels, head->targets, head->loss, head->dHL, head->lddhl,
                             head->dW_pred, head->db_pred, prec, ws, ws_bytes, stream,
-                            fuse ? last.dbias : nullptr)))
+                            fuse ? last.dbias : nullptr, HL16, HL16T, fuse ? tcols(L - 1) : 0)))
             return rc;
         g = head->dHL;
         ldg = head->lddhl;
@@ -975,7 +1078,8 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         const bool fuse = l > 0 && dH_mask_fusable(n, a.f_in, a.h, a.order, prec);
         if ((rc = layer_bwd(launch, A, AT, Hin, a.f_in, ldin, a.W_self, a.W_neigh, a.h, a.Y, a.ldy, a.saved,
                             a.saved_bytes, g, ldg, a.dH, a.lddh, a.dW_self, a.dW_neigh, a.dbias, a.order, prec, ws,
-                            ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr, bAT)))
+                            ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr, bAT, ready && bf,
+                            fuse ? tcols(l - 1) : 0)))
             return rc;
         g = a.dH;
         ldg = a.lddh;

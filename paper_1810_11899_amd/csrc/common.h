@@ -118,15 +118,17 @@ size_t spmm_bounds_bytes(int32_t n_rows, int32_t nnz);
 int spmm_bounds(int32_t n_rows, int32_t nnz, const int32_t *indptr, int32_t *bounds, hipStream_t s);
 // out[i, c] (epilogue) sum_p vals[p] * X[indices[p], c].  `bounds`: the row
 // ranges from spmm_bounds for this indptr, or NULL to compute them here.
+// out16 (EPI_STORE / EPI_BIAS_RELU): the same values also as bfloat16 rows
+// (leading dim ld16); `out` may then be NULL.
 int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
              const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s,
-             const int32_t *bounds = nullptr);
+             const int32_t *bounds = nullptr, uint16_t *out16 = nullptr, int64_t ld16 = 0);
 // same with bfloat16 rows of X (uint16 bits), float32 accumulation
 int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
               const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
               int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s,
-              const int32_t *bounds = nullptr);
+              const int32_t *bounds = nullptr, uint16_t *out16 = nullptr, int64_t ld16 = 0);
 
 // GEMM on the matrix cores -----------------------------------------------------
 // C[M x N] = sum over up to two K-segments of op(A_s) op(B_s), then epilogue.
@@ -148,7 +150,15 @@ struct GemmProblem {
     int64_t ldc;
     const float *bias;  // [N] or null
     int relu;
-    uint16_t *C16;      // when set: write bfloat16 (RNE) here instead of C (leading dim ldc)
+    // Outputs, each written when set (at least one of C, C16): C float32
+    // (leading dim ldc); C16 the same values as bfloat16 (RNE) rows (leading
+    // dim ldc16, ldc when 0); C16T bfloat16 transposed, element (i, j) at
+    // C16T[j * ldc16t + i], for the columns j < n16t only.
+    uint16_t *C16;
+    int64_t ldc16;
+    uint16_t *C16T;
+    int64_t ldc16t;
+    int32_t n16t;
     int32_t k_pad;      // trailing K columns that are zero padding (left out of the flop count)
     // float32 kernel, unsplit only: C[i][j] is kept where mask[i][j] > 0 and
     // set to 0 elsewhere (leading dim ldm), after bias and ReLU
@@ -157,7 +167,7 @@ struct GemmProblem {
     // (a bfloat16 product takes only this one, a float32 product only mask)
     const uint16_t *mask16;
     int64_t ldm;
-    // float32 kernel, unsplit only: colpart[t][j] = sum of the stored C[i][j]
+    // unsplit only: colpart[t][j] = sum of the stored C[i][j]
     // over the rows i of row tile t (gemm_colpart_rows(M) x N, leading dim N)
     float *colpart;
 };

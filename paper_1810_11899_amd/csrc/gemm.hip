@@ -16,6 +16,7 @@
 // stored k-major, so that the matrix-core operand reads (32 consecutive m or n
 // per half-wavefront) hit 32 distinct banks.  Split-K partial tiles go to the
 // workspace and a second kernel adds them in split order (no atomics).
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -52,7 +53,11 @@ struct DevProblem {
     const float *bias;
     int relu;
     float *partial;     // split x M x N when split > 1
-    uint16_t *C16;      // bfloat16 output instead of C (no split)
+    uint16_t *C16;      // bfloat16 rows of the output (ldc16), besides or instead of C
+    int64_t ldc16;
+    uint16_t *C16T;     // bfloat16 transposed output, columns < n16t (ldc16t),
+    int64_t ldc16t;     // written by a pass after the product
+    int32_t n16t;
     const float *mask;  // float32 kernel, no split: keep C where mask > 0 (leading dim ldm)
     const uint16_t *mask16;  // bfloat16 kernels: the same rule on bfloat16 bits
     int64_t ldm;
@@ -654,10 +659,8 @@ void gemm_bf16_kernel(DevArgs args) {
                         if (P.relu) v = fmaxf(v, 0.0f);
                         if (emask) v = bf16_bits_positive(emask[(int64_t)row * P.ldm + col]) ? v : 0.0f;
                         if (ecs) cs[j] += v;
-                        if (P.C16) {
-                            P.C16[(int64_t)row * P.ldc + col] = to_bf16(v);
-                            continue;
-                        }
+                        if (P.C16) P.C16[(int64_t)row * P.ldc16 + col] = to_bf16(v);
+                        if (!P.C) continue;
                     }
                     dst[(int64_t)row * ldd + col] = v;
                 }
@@ -741,9 +744,11 @@ __global__ __launch_bounds__(256) void splitk_reduce(DevArgs args, int G) {
                 if (P.relu) o[j] = fmaxf(o[j], 0.0f);
             }
             if (P.C16) {
-                uint16_t *d = P.C16 + (int64_t)row * P.ldc + col;
+                uint16_t *d = P.C16 + (int64_t)row * P.ldc16 + col;
 #pragma unroll
                 for (int j = 0; j < W; ++j) d[j] = to_bf16(o[j]);
+            }
+            if (!P.C) {
             } else if constexpr (VEC) {
                 *(float4 *)(P.C + (int64_t)row * P.ldc + col) = float4{o[0], o[1], o[2], o[3]};
             } else {
@@ -819,6 +824,14 @@ __device__ __forceinline__ void sched_reads() {
     }
 }
 
+// Output sets of the large-tile kernel, one instantiation each so that the
+// hot ones carry no code (and no registers) for outputs they never write.
+enum BigOut {
+    BIG_F32 = 0,   // float32 C (or split partials) only
+    BIG_B16 = 1,   // bfloat16 rows C16 only
+    BIG_ALL = 2    // float32 C and bfloat16 rows C16
+};
+template <int OUT>
 __global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(kBigWaves / 4)))
 void gemm_bf16_big_kernel(DevArgs args) {
     __shared__ __attribute__((aligned(16))) uint16_t lds[kBigStages][2][kBigT * kBigBK];
@@ -1007,9 +1020,10 @@ void gemm_bf16_big_kernel(DevArgs args) {
             stg[lr * kBigT + lc] = v[r];
         }
     };
-    const bool c16 = !to_partial && P.C16 != nullptr;
-    const bool vec = c16 ? (P.ldc % 4 == 0 && ((uintptr_t)P.C16 & 7) == 0)
-                         : (ldd % 4 == 0 && ((uintptr_t)dst & 15) == 0);
+    const bool c16 = OUT != BIG_F32 && !to_partial && P.C16 != nullptr;
+    const bool c32 = OUT != BIG_B16 && (to_partial || P.C != nullptr);
+    const bool vec16 = c16 && P.ldc16 % 4 == 0 && ((uintptr_t)P.C16 & 7) == 0;
+    const bool vec32 = c32 && ldd % 4 == 0 && ((uintptr_t)dst & 15) == 0;
     const int col = n0 + 4 * lane;
     float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if (!to_partial && P.bias)
@@ -1086,8 +1100,8 @@ void gemm_bf16_big_kernel(DevArgs args) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) cs[h][e] += o[e];
             if (c16) {
-                uint16_t *d = P.C16 + (int64_t)row * P.ldc + col;
-                if (vec && col + 3 <= Nlast) {
+                uint16_t *d = P.C16 + (int64_t)row * P.ldc16 + col;
+                if (vec16 && col + 3 <= Nlast) {
                     *(uint2 *)d = make_uint2((uint32_t)to_bf16(o[0]) | ((uint32_t)to_bf16(o[1]) << 16),
                                              (uint32_t)to_bf16(o[2]) | ((uint32_t)to_bf16(o[3]) << 16));
                 } else {
@@ -1095,9 +1109,10 @@ void gemm_bf16_big_kernel(DevArgs args) {
                     for (int e = 0; e < 4; ++e)
                         if (col + e <= Nlast) d[e] = to_bf16(o[e]);
                 }
-            } else {
+            }
+            if (c32) {
                 float *d = dst + (int64_t)row * ldd + col;
-                if (vec && col + 3 <= Nlast) {
+                if (vec32 && col + 3 <= Nlast) {
                     *(float4 *)d = make_float4(o[0], o[1], o[2], o[3]);
                 } else {
 #pragma unroll
@@ -1205,6 +1220,10 @@ void fill_dev(int layout, int nprob, const GemmProblem *probs, int bf16, int spl
         d.relu = g.relu;
         d.partial = nullptr;
         d.C16 = g.C16;
+        d.ldc16 = g.ldc16 ? g.ldc16 : g.ldc;
+        d.C16T = g.C16T;
+        d.ldc16t = g.ldc16t;
+        d.n16t = g.C16T ? min(g.n16t, g.N) : 0;
         d.mask = g.mask;
         d.mask16 = g.mask16;
         d.ldm = g.ldm;
@@ -1299,7 +1318,8 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         // algorithmic bytes: each operand read once, the output written once
         // (float32 or bfloat16), the mask read once, the bias read once
         const double esz = bf16 ? 2.0 : 4.0;
-        bytes += esz * K * ((double)g.M + g.N) + (double)g.M * g.N * (g.C16 ? 2.0 : 4.0) +
+        bytes += esz * K * ((double)g.M + g.N) + (double)g.M * g.N * ((g.C16 ? 2.0 : 0.0) + (g.C ? 4.0 : 0.0)) +
+                 (g.C16T ? 2.0 * g.M * std::min(g.n16t, g.N) : 0.0) +
                  (g.mask ? 4.0 * g.M * g.N : 0.0) + (g.mask16 ? 2.0 * g.M * g.N : 0.0) + (g.bias ? 4.0 * g.N : 0.0);
     }
     float *partial = nullptr;
@@ -1323,8 +1343,16 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     for (int i = 0; i < nprob; ++i) {
         any_split = any_split || a.p[i].split > 1;
         const bool masked = probs[i].mask || probs[i].mask16;
-        if ((masked || probs[i].colpart) && (a.p[i].split > 1 || (probs[i].C16 != nullptr) == (probs[i].C != nullptr))) {
-            set_error("gemm: the mask and column-sum epilogue needs an unsplit product with one output");
+        if (!probs[i].C && !probs[i].C16) {
+            set_error("gemm: no output");
+            return GCN_EINVAL;
+        }
+        if (probs[i].C16T && !bf16 && !probs[i].C) {
+            set_error("gemm: a transposed bfloat16 output needs a row output to come from");
+            return GCN_EINVAL;
+        }
+        if ((masked || probs[i].colpart) && a.p[i].split > 1) {
+            set_error("gemm: the mask and column-sum epilogue needs an unsplit product");
             return GCN_EINVAL;
         }
         if (bf16 ? probs[i].mask != nullptr : probs[i].mask16 != nullptr) {
@@ -1346,7 +1374,17 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     {
         ProfScope ps(cls, s, flops, bytes);
         dim3 grid((unsigned)blocks);
-        if (big) hipLaunchKernelGGL(gemm_bf16_big_kernel, grid, dim3(kBigThreads), 0, s, a);
+        if (big) {
+            // the output set every problem of the launch fits in
+            bool any32 = false, any16 = false;
+            for (int i = 0; i < nprob; ++i) {
+                any32 = any32 || a.p[i].split > 1 || probs[i].C;
+                any16 = any16 || (a.p[i].split == 1 && probs[i].C16);
+            }
+            if (!any16) hipLaunchKernelGGL(gemm_bf16_big_kernel<BIG_F32>, grid, dim3(kBigThreads), 0, s, a);
+            else if (!any32) hipLaunchKernelGGL(gemm_bf16_big_kernel<BIG_B16>, grid, dim3(kBigThreads), 0, s, a);
+            else hipLaunchKernelGGL(gemm_bf16_big_kernel<BIG_ALL>, grid, dim3(kBigThreads), 0, s, a);
+        }
         else if (layout == L_NN) launch<L_NN>(vec, bf16 != 0, grid, s, a);
         else if (layout == L_TN) launch<L_TN>(vec, bf16 != 0, grid, s, a);
         else launch<L_NT>(vec, bf16 != 0, grid, s, a);
@@ -1370,7 +1408,7 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         for (int i = 0; i < nprob; ++i) {
             if (r.p[i].split <= 1) { r.p[i].M = 0; }
             const DevProblem &q = r.p[i];
-            v4 = v4 && q.N % 4 == 0 && q.ldc % 4 == 0 && (q.C16 || al(q.C, 16));
+            v4 = v4 && q.N % 4 == 0 && (!q.C || (q.ldc % 4 == 0 && al(q.C, 16)));
         }
         const int64_t vecs = v4 ? maxe / 4 : maxe;
         // threads per output vector: up to 8, for about 2^18 threads in all
@@ -1382,6 +1420,20 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
         if (v4) hipLaunchKernelGGL(splitk_reduce<true>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r, G);
         else hipLaunchKernelGGL(splitk_reduce<false>, dim3((unsigned)g, (unsigned)nprob), dim3(256), 0, s, r, G);
         GCN_LAUNCH_CHECK("splitk_reduce");
+    }
+    // transposed bfloat16 outputs: one pass over the bfloat16 rows (or the
+    // float32 ones) after the product.  (Written from the large-tile epilogue
+    // instead, a tile's 256 transposed rows all land at one offset inside
+    // rows n elements apart, which puts the tile's writes in one memory
+    // channel; the separate pass spreads its blocks over the offsets.)
+    for (int i = 0; i < nprob; ++i) {
+        const GemmProblem &g = probs[i];
+        if (!g.C16T) continue;
+        const int32_t cols = std::min(g.n16t, g.N);
+        if (cols <= 0) continue;
+        const int rc = g.C16 ? transpose_bf16(g.M, cols, g.C16, 1, g.ldc16 ? g.ldc16 : g.ldc, g.C16T, g.ldc16t, s)
+                             : transpose_bf16(g.M, cols, g.C, 0, g.ldc, g.C16T, g.ldc16t, s);
+        if (rc) return rc;
     }
     return GCN_OK;
 }

@@ -179,53 +179,113 @@ __device__ __forceinline__ uint16_t to_bf16(float f) {
 }
 
 // Final value of out[r, c .. c+VEC) under the epilogue; `out` is float, or
-// bfloat16 bits for EPI_STORE_BF16 (ldo counts elements of either type).
+// bfloat16 bits for EPI_STORE_BF16 (ldo counts elements of either type), and
+// may be null when only the bfloat16 copy is wanted.  out16 (when set): the
+// same final values as bfloat16 rows (leading dim ld16), for the float32
+// epilogues other than accumulate.
 // ovec: the VEC elements are one aligned vector (ldo a multiple of VEC and
-// `out` aligned to min(16, VEC * element size) bytes), moved with 16-, 8- or
-// 4-byte accesses instead of one access per element.
+// `out` aligned to min(16, VEC * element size) bytes, and the same for
+// out16 when it is set), moved with 16-, 8- or 4-byte accesses instead of
+// one access per element.
 template <int VEC>
+__device__ __forceinline__ void store16(uint16_t *__restrict__ o, const float (&x)[VEC], bool ovec) {
+    if (VEC >= 2 && ovec) {
+        uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
+#pragma unroll
+        for (int i = 0; i < VEC / 2; ++i) w[i] = (uint32_t)to_bf16(x[2 * i]) | ((uint32_t)to_bf16(x[2 * i + 1]) << 16);
+        if constexpr (VEC == 8) *(uint4 *)o = make_uint4(w[0], w[1], w[2], w[3]);
+        else if constexpr (VEC == 4) *(uint2 *)o = make_uint2(w[0], w[1]);
+        else *(uint32_t *)o = w[0];
+        return;
+    }
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) o[v] = to_bf16(x[v]);
+}
+
+template <int VEC, int OM = 0>
 __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_t r, int c,
                                      const float (&acc)[VEC], int epi, const float *__restrict__ bias,
-                                     bool ovec) {
+                                     bool ovec, uint16_t *__restrict__ out16 = nullptr, int64_t ld16 = 0) {
     if (epi == EPI_STORE_BF16) {
-        uint16_t *o = (uint16_t *)out + r * ldo + c;
+        store16<VEC>((uint16_t *)out + r * ldo + c, acc, ovec);
+        return;
+    }
+    if constexpr (OM == 0) {   // one float32 output
+        float *o = (float *)out + r * ldo + c;
+        if (VEC >= 4 && ovec) {
+#pragma unroll
+            for (int q = 0; q < VEC / 4; ++q) {
+                float x[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
+                if (epi == EPI_BIAS_RELU) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) x[e] = fmaxf(x[e] + bias[c + 4 * q + e], 0.0f);
+                } else if (epi == EPI_ACCUMULATE) {
+                    const float4 p = *(const float4 *)(o + 4 * q);
+                    x[0] = p.x + x[0]; x[1] = p.y + x[1]; x[2] = p.z + x[2]; x[3] = p.w + x[3];
+                }
+                *(float4 *)(o + 4 * q) = make_float4(x[0], x[1], x[2], x[3]);
+            }
+            return;
+        }
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            float x = acc[v];
+            if (epi == EPI_BIAS_RELU) x = fmaxf(x + bias[c + v], 0.0f);
+            else if (epi == EPI_ACCUMULATE) x = o[v] + x;
+            o[v] = x;
+        }
+        return;
+    }
+    if constexpr (OM == 1) {   // the bfloat16 copy only: pack as the values are finished
+        uint16_t *o16 = out16 + r * ld16 + c;
+        auto fin = [&](int v) {
+            return epi == EPI_BIAS_RELU ? fmaxf(acc[v] + bias[c + v], 0.0f) : acc[v];
+        };
         if (VEC >= 2 && ovec) {
             uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
 #pragma unroll
             for (int i = 0; i < VEC / 2; ++i)
-                w[i] = (uint32_t)to_bf16(acc[2 * i]) | ((uint32_t)to_bf16(acc[2 * i + 1]) << 16);
-            if constexpr (VEC == 8) *(uint4 *)o = make_uint4(w[0], w[1], w[2], w[3]);
-            else if constexpr (VEC == 4) *(uint2 *)o = make_uint2(w[0], w[1]);
-            else *(uint32_t *)o = w[0];
-            return;
-        }
+                w[i] = (uint32_t)to_bf16(fin(2 * i)) | ((uint32_t)to_bf16(fin(2 * i + 1)) << 16);
+            if constexpr (VEC == 8) *(uint4 *)o16 = make_uint4(w[0], w[1], w[2], w[3]);
+            else if constexpr (VEC == 4) *(uint2 *)o16 = make_uint2(w[0], w[1]);
+            else *(uint32_t *)o16 = w[0];
+        } else {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) o[v] = to_bf16(acc[v]);
+            for (int v = 0; v < VEC; ++v) o16[v] = to_bf16(fin(v));
+        }
         return;
     }
-    float *o = (float *)out + r * ldo + c;
-    if (VEC >= 4 && ovec) {
+    float *o = out ? (float *)out + r * ldo + c : nullptr;
+    float x[VEC];
 #pragma unroll
-        for (int q = 0; q < VEC / 4; ++q) {
-            float x[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
-            if (epi == EPI_BIAS_RELU) {
+    for (int v = 0; v < VEC; ++v) x[v] = acc[v];
+    if (epi == EPI_BIAS_RELU) {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) x[e] = fmaxf(x[e] + bias[c + 4 * q + e], 0.0f);
-            } else if (epi == EPI_ACCUMULATE) {
+        for (int v = 0; v < VEC; ++v) x[v] = fmaxf(x[v] + bias[c + v], 0.0f);
+    } else if (epi == EPI_ACCUMULATE) {
+        if (VEC >= 4 && ovec) {
+#pragma unroll
+            for (int q = 0; q < VEC / 4; ++q) {
                 const float4 p = *(const float4 *)(o + 4 * q);
-                x[0] = p.x + x[0]; x[1] = p.y + x[1]; x[2] = p.z + x[2]; x[3] = p.w + x[3];
+                x[4 * q] = p.x + x[4 * q]; x[4 * q + 1] = p.y + x[4 * q + 1];
+                x[4 * q + 2] = p.z + x[4 * q + 2]; x[4 * q + 3] = p.w + x[4 * q + 3];
             }
-            *(float4 *)(o + 4 * q) = make_float4(x[0], x[1], x[2], x[3]);
-        }
-        return;
-    }
+        } else {
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) {
-        float x = acc[v];
-        if (epi == EPI_BIAS_RELU) x = fmaxf(x + bias[c + v], 0.0f);
-        else if (epi == EPI_ACCUMULATE) x = o[v] + x;
-        o[v] = x;
+            for (int v = 0; v < VEC; ++v) x[v] = o[v] + x[v];
+        }
     }
+    if (o) {
+        if (VEC >= 4 && ovec) {
+#pragma unroll
+            for (int q = 0; q < VEC / 4; ++q)
+                *(float4 *)(o + 4 * q) = make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]);
+        } else {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) o[v] = x[v];
+        }
+    }
+    if (out16) store16<VEC>(out16 + r * ld16 + c, x, ovec);
 }
 
 template <int VEC>
@@ -235,14 +295,17 @@ __device__ __forceinline__ void store_raw(float *__restrict__ out, const float (
 }
 
 // One wavefront = `ipw` merge items x one column slice of width 64*VEC*CT.
-template <int VEC, int CT, bool BF16>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_MAIN_WPE)))
+// OM: the epilogue's outputs, 0 `out` only, 1 the bfloat16 copy out16 only,
+// 2 both; separate instantiations, so that the common kernels carry no
+// registers for the copy.
+template <int VEC, int CT, bool BF16, int OM>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(OM == 1 && CT == 1 ? 7 : GCN_SPMM_MAIN_WPE)))
 void spmm_main(
     int32_t n_rows, const int32_t *__restrict__ indptr, IdxRef indices,
     const float *__restrict__ vals, const void *__restrict__ Xv, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias, int ovec,
     int64_t items, int ipw, int64_t waves, const int32_t *__restrict__ bnd, float *__restrict__ carry,
-    int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
+    int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row, uint16_t *__restrict__ out16, int64_t ld16) {
     using Elem = typename std::conditional<BF16, uint16_t, float>::type;
     const Elem *__restrict__ X = (const Elem *)Xv;
     const int lane = threadIdx.x & 63;
@@ -317,7 +380,7 @@ void spmm_main(
             for (int t = 0; t < CT; ++t)
                 if (cok[t]) {
                     const int c = cbase + t * 64 * VEC;
-                    emit<VEC>(out, ldo, r, c, acc[t], epi, bias, ovec != 0);
+                    emit<VEC, OM>(out, ldo, r, c, acc[t], epi, bias, ovec != 0, out16, ld16);
                 }
         } else if (complete || pe > pb) {
             // a piece of a row cut by wavefront boundaries: head (the piece
@@ -374,7 +437,8 @@ void spmm_sliced(
     const float *__restrict__ vals, const float *__restrict__ X, int32_t k, int64_t ldx,
     void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
     int64_t items, int ipw, int64_t waves, SliceMap map, const int32_t *__restrict__ bnd,
-    float *__restrict__ carry, int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row) {
+    float *__restrict__ carry, int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row,
+    uint16_t *__restrict__ out16, int64_t ld16) {
     int slice;
     int64_t chunk;
     if (!slice_of_block(map, blockIdx.x, slice, chunk)) return;
@@ -438,7 +502,7 @@ void spmm_sliced(
         const bool started = (r > r0) || (q0 == rb);
         if (g == 0 && cok) {
             if (complete && started) {
-                emit<4>(out, ldo, r, col, acc, epi, bias, true);   // ldo % 4 == 0, 16-byte aligned
+                emit<4, 2>(out, ldo, r, col, acc, epi, bias, true, out16, ld16);   // aligned (host checks)
             } else if (complete || pe > pb) {
                 const int slot = complete ? 0 : 1;
                 store_raw<4>(carry + (2 * wave + slot) * (int64_t)k + col, acc);
@@ -485,7 +549,8 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
                                                   int epi, const float *__restrict__ bias,
                                                   int64_t waves, const float *__restrict__ carry,
                                                   const int32_t *__restrict__ head_row,
-                                                  const int32_t *__restrict__ tail_row) {
+                                                  const int32_t *__restrict__ tail_row,
+                                                  uint16_t *__restrict__ out16, int64_t ld16) {
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     if (w >= waves) return;
@@ -543,7 +608,7 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
         if (c >= k) continue;
         const float hv = carry[(2 * w) * (int64_t)k + c];
         const float a[1] = {any ? acc[j] + hv : hv};
-        emit<1>(out, ldo, r, c, a, epi, bias, false);
+        emit<1, 2>(out, ldo, r, c, a, epi, bias, false, out16, ld16);
     }
 }
 
@@ -551,20 +616,32 @@ template <int VEC, int CT, bool BF16>
 void launch_main(dim3 grid, hipStream_t s, int32_t n_rows, const int32_t *indptr,
                  IdxRef indices, const float *vals, const void *X, int32_t k, int64_t ldx,
                  void *out, int64_t ldo, int epi, const float *bias, const SpmmPlan &pl,
-                 const int32_t *bnd, float *carry, int32_t *hr, int32_t *tr) {
+                 const int32_t *bnd, float *carry, int32_t *hr, int32_t *tr, uint16_t *out16, int64_t ld16) {
     // the epilogue's per-lane VEC outputs as one vector store when aligned
     const size_t chunk = std::min<size_t>(16, (size_t)VEC * (epi == EPI_STORE_BF16 ? 2 : 4));
-    const int ovec = ldo % VEC == 0 && (uintptr_t)out % chunk == 0;
-    hipLaunchKernelGGL((spmm_main<VEC, CT, BF16>), grid, dim3(256), 0, s, n_rows, indptr, indices,
-                       vals, X, k, ldx, out, ldo, epi, bias, ovec, pl.items, pl.ipw, pl.waves, bnd, carry, hr,
-                       tr);
+    const size_t chunk16 = std::min<size_t>(16, (size_t)VEC * 2);
+    const int ovec = ldo % VEC == 0 && (uintptr_t)out % chunk == 0 &&
+                     (!out16 || (ld16 % VEC == 0 && (uintptr_t)out16 % chunk16 == 0));
+    if (out16 && out)
+        hipLaunchKernelGGL((spmm_main<VEC, CT, BF16, 2>), grid, dim3(256), 0, s, n_rows, indptr, indices,
+                           vals, X, k, ldx, out, ldo, epi, bias, ovec, pl.items, pl.ipw, pl.waves, bnd, carry, hr,
+                           tr, out16, ld16);
+    else if (out16)
+        hipLaunchKernelGGL((spmm_main<VEC, CT, BF16, 1>), grid, dim3(256), 0, s, n_rows, indptr, indices,
+                           vals, X, k, ldx, nullptr, ldo, epi, bias, ovec, pl.items, pl.ipw, pl.waves, bnd, carry,
+                           hr, tr, out16, ld16);
+    else
+        hipLaunchKernelGGL((spmm_main<VEC, CT, BF16, 0>), grid, dim3(256), 0, s, n_rows, indptr, indices,
+                           vals, X, k, ldx, out, ldo, epi, bias, ovec, pl.items, pl.ipw, pl.waves, bnd, carry, hr,
+                           tr, nullptr, 0);
 }
 
 bool aligned(const void *p, int bytes) { return ((uintptr_t)p % (uintptr_t)bytes) == 0; }
 
 int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
              const float *vals, const void *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-             int epi, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
+             int epi, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds,
+             uint16_t *out16, int64_t ld16) {
     if (n_rows <= 0 || k <= 0) return GCN_OK;
     const SpmmPlan pl = spmm_plan(n_rows, nnz);
     Arena ar(ws, ws_bytes);
@@ -588,8 +665,12 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
     if (ct > 2) ct = 2;
     const int sw = 64 * vec * ct;
     dim3 grid((unsigned)((pl.waves + kWavesPerBlock - 1) / kWavesPerBlock), (unsigned)((k + sw - 1) / sw));
+    if ((out16 && (epi == EPI_ACCUMULATE || epi == EPI_STORE_BF16)) || (!out && !out16)) {
+        set_error("spmm: a bfloat16 copy goes with the store or bias+ReLU epilogue, and some output is needed");
+        return GCN_EINVAL;
+    }
     const bool sliced = !bf16 && k % 4 == 0 && ldx % 4 == 0 && aligned(X, 16) && ldo % 4 == 0 &&
-                        aligned(out, 16) && k >= 128;
+                        aligned(out, 16) && k >= 128 && (!out16 || (ld16 % 4 == 0 && aligned(out16, 8)));
     const double out_bytes = epi == EPI_STORE_BF16 ? 2.0 : (epi == EPI_ACCUMULATE ? 8.0 : 4.0);
     const double bytes = (double)nnz * k * esz + (double)nnz * (indices.i16 ? 6.0 : 8.0) + (double)(n_rows + 1) * 4.0 +
                          (double)n_rows * k * out_bytes;
@@ -606,13 +687,13 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
             const SliceMap m = make_slice_map(k, pl.waves);
             hipLaunchKernelGGL(spmm_sliced, dim3((unsigned)slice_map_blocks(m)), dim3(256), 0, s, n_rows, indptr,
                                indices, vals, (const float *)X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw,
-                               pl.waves, m, bnd, carry, hr, tr);
+                               pl.waves, m, bnd, carry, hr, tr, out16, ld16);
             GCN_LAUNCH_CHECK("spmm_sliced");
         } else
 #define GCN_SPMM_CASE(V, C, B)                                                                   \
     if (vec == V && ct == C && bf16 == B) {                                                      \
         launch_main<V, C, B>(grid, s, n_rows, indptr, indices, vals, X, k, ldx, out, ldo, epi,   \
-                             bias, pl, bnd, carry, hr, tr);                                      \
+                             bias, pl, bnd, carry, hr, tr, out16, ld16);                         \
     } else
         GCN_SPMM_CASE(4, 1, false)
         GCN_SPMM_CASE(4, 2, false)
@@ -638,7 +719,7 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
         ProfScope ps(K_SPMM_FIXUP, s, 0.0, 0.0);
         dim3 g2((unsigned)((pl.waves + kWavesPerBlock - 1) / kWavesPerBlock), (unsigned)((k + 255) / 256));
         hipLaunchKernelGGL(spmm_fixup, g2, dim3(256), 0, s, k, out, ldo, epi, bias, pl.waves, carry,
-                           hr, tr);
+                           hr, tr, out16, ld16);
         GCN_LAUNCH_CHECK("spmm_fixup");
     }
     return GCN_OK;
@@ -684,16 +765,18 @@ int spmm_bounds(int32_t n_rows, int32_t nnz, const int32_t *indptr, int32_t *bou
 
 int spmm_f32(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
              const float *vals, const float *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
+             int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds,
+             uint16_t *out16, int64_t ld16) {
     return spmm_any(false, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
-                    ws, ws_bytes, s, bounds);
+                    ws, ws_bytes, s, bounds, out16, ld16);
 }
 
 int spmm_bf16(int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxRef indices,
               const float *vals, const uint16_t *X, int32_t k, int64_t ldx, void *out, int64_t ldo,
-              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds) {
+              int epilogue, const float *bias, void *ws, size_t ws_bytes, hipStream_t s, const int32_t *bounds,
+              uint16_t *out16, int64_t ld16) {
     return spmm_any(true, n_rows, nnz, indptr, indices, vals, X, k, ldx, out, ldo, epilogue, bias,
-                    ws, ws_bytes, s, bounds);
+                    ws, ws_bytes, s, bounds, out16, ld16);
 }
 
 }  // namespace gcn

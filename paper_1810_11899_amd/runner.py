@@ -20,17 +20,23 @@ class StepRunner:
     def __init__(self, wl, prec: int = B.GCN_F32, device: str = "cuda",
                  first_layer_dH: Optional[bool] = None, nnz_capacity: int = 0,
                  orders: Optional[List[int]] = None, transpose_shortcut: bool = True,
-                 index_bits: int = 32):
+                 index_bits: int = 32, float_outputs: bool = True):
         """index_bits = 16 keeps A's column indices as uint16 (n <= 65,536):
         half the index bytes, the same results bit for bit.  orders: one
         gcn_order per layer, None for gcn_layer_pick_order's width rule, or
         "tuned" for the combination tune_orders measures fastest on this
-        workload."""
+        workload.  float_outputs=False (bfloat16 only): the model step keeps
+        the layers' outputs only as the bfloat16 copies the next consumer
+        reads, with no float32 Y (the library refuses where a layer's output
+        gradient would not arrive masked)."""
+        if not float_outputs and prec != B.GCN_BF16:
+            raise ValueError("float32 steps write their float32 outputs")
+        self.float_outputs = float_outputs
         if isinstance(orders, str):
             if orders != "tuned":
                 raise ValueError(f"orders: a list, None or 'tuned' (got {orders!r})")
             orders, self.order_timings = tune_orders(wl, prec=prec, device=device, first_layer_dH=first_layer_dH,
-                                                     index_bits=index_bits)
+                                                     index_bits=index_bits, float_outputs=float_outputs)
         self.dev = torch.device(device)
         self.prec = prec
         if index_bits not in (16, 32) or (index_bits == 16 and wl.n > 65536):
@@ -80,7 +86,8 @@ class StepRunner:
             self.dW_pred = torch.empty((hl2, C), dtype=torch.float32, device=self.dev)
             self.db_pred = torch.empty(C, dtype=torch.float32, device=self.dev)
         self.load(wl)
-        layers = [dict(W_self=Ws, W_neigh=Wn, bias=b, Y=self.Y[li], saved=self.saved[li], dH=self.dH[li],
+        layers = [dict(W_self=Ws, W_neigh=Wn, bias=b, Y=self.Y[li] if float_outputs else None, saved=self.saved[li],
+                       dH=self.dH[li],
                        dW_self=self.dWs[li], dW_neigh=self.dWn[li], dbias=self.db[li], order=self.orders[li])
                   for li, (Ws, Wn, b) in enumerate(self.W)]
         head = None if self.head is None else dict(
@@ -177,7 +184,18 @@ class StepRunner:
         intermediate values and are reported as None."""
         c = lambda t: None if t is None else t.detach().cpu().numpy()
         inner = getattr(self, "_last", "calls") == "step"
-        r = {"Y": [c(y) for y in self.Y], "dW_self": [c(t) for t in self.dWs],
+        Ys = [c(y) for y in self.Y]
+        if inner and not self.float_outputs:
+            # outputs kept as bfloat16 rows at the start of the next layer's
+            # saved buffer; the last layer's is not kept
+            for li in range(self.L):
+                if li + 1 < self.L:
+                    nb = self.n * 2 * self.dims[li][1]
+                    bits = self.saved[li + 1][:2 * nb].view(torch.int16).cpu().numpy().view(np.uint16)
+                    Ys[li] = (bits.astype(np.uint32) << 16).view(np.float32).reshape(self.n, -1)
+                else:
+                    Ys[li] = None
+        r = {"Y": Ys, "dW_self": [c(t) for t in self.dWs],
              "dW_neigh": [c(t) for t in self.dWn], "db": [c(t) for t in self.db],
              "dH": [None if (inner and li > 0) else c(t) for li, t in enumerate(self.dH)],
              "t_indptr": c(self.AT.indptr), "t_indices": _as_int32(c(self.AT.indices)), "t_vals": c(self.AT.vals)}
@@ -194,7 +212,7 @@ class StepRunner:
 
 
 def tune_orders(wl, prec: int = B.GCN_F32, device: str = "cuda", first_layer_dH: Optional[bool] = None,
-                index_bits: int = 32, warmup: int = 2, reps: int = 5):
+                index_bits: int = 32, warmup: int = 2, reps: int = 5, float_outputs: bool = True):
     """Measure the whole model step for every combination of the layers'
     groupings (aggregate-first or transform-first, 2^L combinations) on this
     workload's graph and widths, and return the fastest combination with the
@@ -209,7 +227,7 @@ def tune_orders(wl, prec: int = B.GCN_F32, device: str = "cuda", first_layer_dH:
     timings = {}
     for combo in itertools.product((B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST), repeat=L):
         r = StepRunner(wl, prec=prec, device=device, first_layer_dH=first_layer_dH, orders=list(combo),
-                       index_bits=index_bits)
+                       index_bits=index_bits, float_outputs=float_outputs)
         for _ in range(warmup):
             r.step()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]

@@ -421,3 +421,45 @@ def test_model_step_degenerate_graphs_match_oracle(graph):
     r.step()
     torch.cuda.synchronize()
     compare_step(r.results(), oracle.step(wl, first_layer_dH=True, envelope=True))
+
+
+def test_bf16_step_without_float_outputs_refused_where_needed():
+    """At 8,000 vertices layer 2's input-gradient product runs split, so
+    layer 1's output gradient arrives unmasked and its float32 Y is needed:
+    the step is refused before anything is launched."""
+    wl = synth.config(1)
+    r = StepRunner(wl, prec=B.GCN_BF16, float_outputs=False)
+    for y in r.Y:
+        y.fill_(7.0)
+    with pytest.raises(B.GcnError) as e:
+        r.step()
+    assert e.value.code == B.GCN_EINVAL and "masked" in str(e.value)
+    torch.cuda.synchronize()
+    assert all(bool((y == 7.0).all()) for y in r.Y)
+
+
+@pytest.mark.parametrize("cfg", [3])
+def test_bf16_step_without_float_outputs(cfg):
+    """The bfloat16 step with no float32 layer outputs (activations kept only
+    as the bfloat16 operand rows the next consumer reads, as the benchmark
+    runs it) gives the same loss and gradients bit for bit as the step that
+    also writes them, and its kept outputs are the bfloat16 rounding of the
+    float32 ones."""
+    from oracle import bf16 as obf16
+    wl = synth.config(cfg)
+    a = StepRunner(wl, prec=B.GCN_BF16)
+    b = StepRunner(wl, prec=B.GCN_BF16, float_outputs=False, orders=a.orders)
+    print(f"bf16 step without float outputs: workload {cfg}", flush=True)
+    a.step()
+    b.step()
+    torch.cuda.synchronize()
+    ra, rb = a.results(), b.results()
+    for key in ("dW_self", "dW_neigh", "db"):
+        for i, (x, y) in enumerate(zip(ra[key], rb[key])):
+            assert np.array_equal(x.view(np.uint32), y.view(np.uint32)), (key, i)
+    assert ra["loss"] == rb["loss"]
+    for key in ("dW_pred", "db_pred"):
+        assert np.array_equal(ra[key].view(np.uint32), rb[key].view(np.uint32)), key
+    for li in range(a.L - 1):
+        assert np.array_equal(rb["Y"][li].view(np.uint32), obf16.round_bf16(ra["Y"][li]).view(np.uint32)), li
+    assert rb["Y"][-1] is None
