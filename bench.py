@@ -447,7 +447,7 @@ PHASES = {  # the time breakdown of Sec. VI-C (Fig. 3): sampling, propagation, w
     "sampling": ("frontier_sample", "induce_subgraphs"),
     "feature_propagation": ("spmm", "spmm_fixup", "spmm_bf16"),
     "weight_application": ("gemm_nn", "gemm_tn", "gemm_nt", "splitk_reduce", "gemm_nn_bf16", "gemm_tn_bf16",
-                           "gemm_nt_bf16", "gemm_nt_bf16_big", "gemm_nt_bf16_big_masked"),
+                           "gemm_nt_bf16", "gemm_nt_bf16_big", "gemm_nt_bf16_big_masked", "gemm_tn_bf16_big"),
 }
 
 

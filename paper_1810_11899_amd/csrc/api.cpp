@@ -38,7 +38,7 @@ static const char *kClassNames[K_CLASS_COUNT] = {
     "colsum", "loss_rows", "loss_reduce", "transpose_count", "transpose_scan", "transpose_scatter",
     "transpose_sort", "transpose_final", "cvt_bf16", "gemm_nn_bf16", "gemm_tn_bf16", "gemm_nt_bf16",
     "spmm_bf16", "transpose_bf16", "frontier_sample", "induce_subgraphs", "gather_rows", "adam", "transpose_symmetric",
-    "gemm_nt_bf16_big", "gemm_nt_bf16_big_masked"};
+    "gemm_nt_bf16_big", "gemm_nt_bf16_big_masked", "gemm_tn_bf16_big"};
 
 const char *class_name(int cls) {
     return (cls >= 0 && cls < K_CLASS_COUNT) ? kClassNames[cls] : "";
@@ -155,6 +155,23 @@ struct LayerPlan {
     size_t bwd_P, bwd_PT, bwd_D, bwd_DT, bwd_T2, bwd_W16, bwd_relu, bwd_spmm, bwd_gemm, bwd_cp;
     size_t fwd_total, bwd_total, total;
 };
+
+// bfloat16 weight gradients straight from the row-major operands the layer
+// keeps (H, AGG, dZ, G: n rows): a TN product on the large-tile kernel, whose
+// k-major operand tiles are read transposed from LDS.  Then no transposed
+// copy of those operands is made.  Otherwise (shapes the large-tile kernel
+// does not take) the products run NT on transposed copies.
+bool bf16_dw_rowmajor(int32_t n, int32_t f_in, int32_t h) {
+    if (n <= 0) return false;
+    const void *p = (const void *)(uintptr_t)256;   // stands for 256-byte aligned buffers
+    GemmProblem g[2] = {};
+    for (int i = 0; i < 2; ++i) {
+        g[i].M = f_in;
+        g[i].N = h;
+        g[i].seg[0] = GemmSeg{p, f_in, p, 2 * (int64_t)h, n};
+    }
+    return gemm_bf16_big_ok(L_TN, 2, g) && h % 8 == 0;
+}
 
 bool bwd_uses_G(int order, bool dH, int32_t f_in, int32_t h) {
     return order == GCN_TRANSFORM_FIRST || (dH && h <= f_in);
@@ -461,8 +478,13 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
         uint16_t *AGG16T = af ? (uint16_t *)((char *)saved + 3 * one) : nullptr;
         uint16_t *WsT = ar.take<uint16_t>((size_t)f_in * h);
         uint16_t *WnT = ar.take<uint16_t>((size_t)f_in * h);
-        // H16T and H16 in one pass over H (unless the layer below wrote them)
-        if (!lk.in_ready && (rc = transpose_bf16_copy(n, f_in, H, 0, ldh, H16T, n, H16, f_in, s))) return rc;
+        // H16 (and H16T for the transposed weight-gradient products) in one
+        // pass over H, unless the layer below wrote them
+        const bool tnw = bf16_dw_rowmajor(n, f_in, h);
+        if (!lk.in_ready) {
+            rc = tnw ? cvt_bf16(n, f_in, H, ldh, H16, f_in, s) : transpose_bf16_copy(n, f_in, H, 0, ldh, H16T, n, H16, f_in, s);
+            if (rc) return rc;
+        }
         if ((rc = transpose_bf16(f_in, h, W_self, 0, h, WsT, f_in, s))) return rc;
         if ((rc = transpose_bf16(f_in, h, W_neigh, 0, h, WnT, f_in, s))) return rc;
         GemmProblem g[2] = {};
@@ -490,7 +512,7 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
             rc = spmm_bf16(n, A->nnz, A->indptr, idx_of(A), A->vals, H16, f_in, f_in, AGG16, f_in,
                            EPI_STORE_BF16, nullptr, sw, pl.fwd_spmm, s, bA);
             if (rc) return rc;
-            if ((rc = transpose_bf16(n, f_in, AGG16, 1, f_in, AGG16T, n, s))) return rc;
+            if (!tnw && (rc = transpose_bf16(n, f_in, AGG16, 1, f_in, AGG16T, n, s))) return rc;
             g[1].seg[0] = GemmSeg{AGG16, f_in, WnT, f_in, f_in};
             g[1].C = Y ? Y + h : nullptr;   // no float32 copy when Y is NULL
             g[1].ldc = ldy;
@@ -646,7 +668,16 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     // a7: weight gradients, K = n, split-K
     GemmProblem g[2] = {dw_problem(f_in, h, n), dw_problem(f_in, h, n)};
     int layout = L_TN;
-    if (bf) {
+    if (bf && bf16_dw_rowmajor(n, f_in, h)) {
+        // TN form on the row-major operands: dW_self = H^T dZ_s, dW_neigh =
+        // AGG^T dZ_n (aggregate-first) or H^T G (transform-first)
+        const size_t one = align256((size_t)n * f_in * 2);
+        const uint16_t *H16 = (const uint16_t *)saved;
+        layout = L_TN;
+        g[0].seg[0] = GemmSeg{H16, f_in, Zs, ldZs, n};
+        if (!af) g[1].seg[0] = GemmSeg{H16, f_in, Gp, ldG, n};
+        else g[1].seg[0] = GemmSeg{(const char *)saved + 2 * one, f_in, Zn, ldZn, n};
+    } else if (bf) {
         // NT form: dW = (H^T) (P^T)^T with H^T (f_in x n) and P^T (2h x n) contiguous along n
         const size_t one = align256((size_t)n * f_in * 2);
         const uint16_t *H16T = (const uint16_t *)((const char *)saved + one);
@@ -1036,7 +1067,8 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
             if (l + 1 < L) {
                 const gcn_layer_args &nx = layers[l + 1];
                 lk.out16 = (uint16_t *)nx.saved;
-                lk.out16T = (uint16_t *)((char *)nx.saved + align256((size_t)n * nx.f_in * 2));
+                if (!bf16_dw_rowmajor(n, nx.f_in, nx.h))   // only the transposed products read H16T
+                    lk.out16T = (uint16_t *)((char *)nx.saved + align256((size_t)n * nx.f_in * 2));
             } else if (head) {
                 lk.out16 = HL16;
                 lk.out16T = HL16T;
@@ -1052,7 +1084,8 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
     // aggregate-first (dW_self and dW_neigh), the self half for
     // transform-first (dW_neigh takes A^T dZ_n, transposed after the SpMM)
     auto tcols = [&](int32_t l) {
-        return bf ? (layers[l].order == GCN_AGGREGATE_FIRST ? 2 * layers[l].h : layers[l].h) : 0;
+        if (!bf || bf16_dw_rowmajor(n, layers[l].f_in, layers[l].h)) return 0;
+        return layers[l].order == GCN_AGGREGATE_FIRST ? 2 * layers[l].h : layers[l].h;
     };
     const float *g = dY;  // PREDICT + LOSS, or the given output gradient
     int32_t ldg = lddy;
@@ -1078,8 +1111,8 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         const bool fuse = l > 0 && dH_mask_fusable(n, a.f_in, a.h, a.order, prec);
         if ((rc = layer_bwd(launch, A, AT, Hin, a.f_in, ldin, a.W_self, a.W_neigh, a.h, a.Y, a.ldy, a.saved,
                             a.saved_bytes, g, ldg, a.dH, a.lddh, a.dW_self, a.dW_neigh, a.dbias, a.order, prec, ws,
-                            ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr, bAT, ready && bf,
-                            fuse ? tcols(l - 1) : 0)))
+                            ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr, bAT,
+                            ready && tcols(l) > 0, fuse ? tcols(l - 1) : 0)))
             return rc;
         g = a.dH;
         ldg = a.lddh;

@@ -55,6 +55,7 @@ enum KernelClass {
     K_T_SYM,
     K_GEMM_NT_BF16_BIG,         // the bfloat16 large-tile kernel
     K_GEMM_NT_BF16_BIG_MASKED,  // the same with the ReLU-derivative epilogue
+    K_GEMM_TN_BF16_BIG,         // the large-tile kernel on k-major operands (weight gradients)
     K_CLASS_COUNT
 };
 const char *class_name(int cls);
@@ -177,6 +178,9 @@ struct GemmProblem {
 int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
          void *ws, size_t ws_bytes, hipStream_t s);
 size_t gemm_workspace_bytes(int nprob, const GemmProblem *probs, int split_k);
+// whether bfloat16 products of this layout and shape run on the large-tile
+// kernel (which reads k-major operands, TN and NN, with transposing LDS reads)
+bool gemm_bf16_big_ok(int layout, int nprob, const GemmProblem *probs);
 // split-K count; k_is_rows: a weight gradient (K = vertices, few output tiles)
 int gemm_pick_split(int nprob, const GemmProblem *probs, bool k_is_rows);
 // row tiles of a float32 product with M rows (the rows of colpart)

@@ -824,6 +824,27 @@ __device__ __forceinline__ void sched_reads() {
     }
 }
 
+// k-major operand tiles (an operand stored K x rows, contiguous along its
+// rows: the K = n operands of the weight gradients, H and dZ, as the layer
+// keeps them).  A stage holds 32 k-rows of 256 elements as 32 chunks of 16
+// bytes; chunk position p of k-row kk holds the tile's chunk p ^ kmswz(kk).
+// The matrix-core fragments (8 consecutive k of one row index per lane) are
+// read with the gfx950 transposing LDS read: in each group of 16 lanes, lane
+// j addresses 4 elements of k-row kbase + j/4 at row index x0 + 4 (j%4), and
+// lane i receives element i%4 of the pieces of lanes i/4, i/4+4, i/4+8,
+// i/4+12, i.e. x0 + i at k-rows kbase .. kbase+3.  With the swizzle the 16
+// pieces of the 32 lanes of one LDS cycle fall in 16 distinct 4-bank groups.
+__device__ __forceinline__ int kmswz(int kk) { return 4 * (kk & 3); }
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ bf16x8 tr_frag(const uint16_t *tile, int off0, int off1) {
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(tile + off0));
+    const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)(tile + off1));
+    bf16x8 r;
+    __builtin_memcpy(&r, &lo, 8);
+    __builtin_memcpy((char *)&r + 8, &hi, 8);
+    return r;
+}
+
 // Output sets of the large-tile kernel, one instantiation each so that the
 // hot ones carry no code (and no registers) for outputs they never write.
 enum BigOut {
@@ -831,9 +852,12 @@ enum BigOut {
     BIG_B16 = 1,   // bfloat16 rows C16 only
     BIG_ALL = 2    // float32 C and bfloat16 rows C16
 };
-template <int OUT>
+// LAYOUT: L_NT (both operands contiguous along k), L_TN (both k-major) or
+// L_NN (A contiguous along k, B k-major).
+template <int OUT, int LAYOUT>
 __global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(kBigWaves / 4)))
 void gemm_bf16_big_kernel(DevArgs args) {
+    constexpr bool KMA = LAYOUT == L_TN, KMB = LAYOUT != L_NT;
     __shared__ __attribute__((aligned(16))) uint16_t lds[kBigStages][2][kBigT * kBigBK];
 
     BlockCoord bc;
@@ -856,14 +880,19 @@ void gemm_bf16_big_kernel(DevArgs args) {
     // Lane `lane` of load q deposits chunk position (wave*Q + q)*64 + lane of
     // the stage's operand tile: row pos/4, stored chunk pos%4, which holds
     // global chunk (pos%4) ^ swizzle(row).
-    int rowA[kBigQ], rowB[kBigQ], chk[kBigQ];
+    // A k-major operand: k-row pos/32, stored chunk pos%32, which holds the
+    // tile's chunk (pos%32) ^ kmswz(k-row), at row index x0 + 8 * chunk
+    // (clamped to the last whole chunk, rows are a multiple of 8).
+    int rowA[kBigQ], rowB[kBigQ], chk[kBigQ], kmk[kBigQ];
 #pragma unroll
     for (int q = 0; q < kBigQ; ++q) {
         const int pos = (wave * kBigQ + q) * 64 + lane;
         const int r = pos >> 2;
         chk[q] = ((pos & 3) ^ bigswz(r)) * 8;
-        rowA[q] = min(m0 + r, Mlast);
-        rowB[q] = min(n0 + r, Nlast);
+        const int kk = pos >> 5, xc = 8 * ((pos & 31) ^ kmswz(pos >> 5));
+        kmk[q] = kk;
+        rowA[q] = KMA ? min(m0 + xc, P.M - 8) : min(m0 + r, Mlast);
+        rowB[q] = KMB ? min(n0 + xc, P.N - 8) : min(n0 + r, Nlast);
     }
     auto issue = [&](int kt, int stage) {
         const bool s1 = kt >= kt0;
@@ -872,15 +901,19 @@ void gemm_bf16_big_kernel(DevArgs args) {
         const int64_t lda = s1 ? lda1 : lda0, ldb = s1 ? ldb1 : ldb0;
         const int k0 = (s1 ? kt - kt0 : kt) * kBigBK;
 #pragma unroll
-        for (int q = 0; q < kBigQ; ++q)
-            __builtin_amdgcn_global_load_lds((const void *)(A + (int64_t)rowA[q] * lda + k0 + chk[q]),
+        for (int q = 0; q < kBigQ; ++q) {
+            const uint16_t *g = KMA ? A + (int64_t)(k0 + kmk[q]) * lda + rowA[q] : A + (int64_t)rowA[q] * lda + k0 + chk[q];
+            __builtin_amdgcn_global_load_lds((const void *)g,
                                              (void __attribute__((address_space(3))) *)&lds[stage][0][(wave * kBigQ + q) * 512],
                                              16, 0, 0);
+        }
 #pragma unroll
-        for (int q = 0; q < kBigQ; ++q)
-            __builtin_amdgcn_global_load_lds((const void *)(Bm + (int64_t)rowB[q] * ldb + k0 + chk[q]),
+        for (int q = 0; q < kBigQ; ++q) {
+            const uint16_t *g = KMB ? Bm + (int64_t)(k0 + kmk[q]) * ldb + rowB[q] : Bm + (int64_t)rowB[q] * ldb + k0 + chk[q];
+            __builtin_amdgcn_global_load_lds((const void *)g,
                                              (void __attribute__((address_space(3))) *)&lds[stage][1][(wave * kBigQ + q) * 512],
                                              16, 0, 0);
+        }
     };
 
     floatx16 acc[kBigFM][kBigFN];
@@ -915,19 +948,36 @@ void gemm_bf16_big_kernel(DevArgs args) {
     static_assert(KS == 2, "the pipeline alternates two k-steps per stage");
     static_assert(kBigStages >= 3, "tile t+1 must be in flight behind tile t");
     bf16x8 fa[2][kBigFM], fb[2][kBigFN];
+    // a k-major fragment: the two transposing reads of k-rows kb .. kb+3 and
+    // kb+4 .. kb+7 (kb = 16 ks + 8 (lane / 32)) for the 32 row indices x0 ..
+    auto km_frag = [&](const uint16_t *T, int ks, int x0) {
+        const int kk = 16 * ks + 8 * (lane >> 5) + ((lane & 15) >> 2);
+        const int x = x0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+        const int off0 = kk * kBigT + ((x >> 3) ^ kmswz(kk)) * 8 + (x & 7);
+        const int off1 = (kk + 4) * kBigT + ((x >> 3) ^ kmswz(kk + 4)) * 8 + (x & 7);
+        return tr_frag(T, off0, off1);
+    };
     auto read_frags = [&](int stage, int ks, bf16x8 (&a)[kBigFM], bf16x8 (&b)[kBigFN]) {
         const uint16_t *As = lds[stage][0];
         const uint16_t *Bs = lds[stage][1];
         const int c = 2 * ks + (lane >> 5);
 #pragma unroll
         for (int i = 0; i < kBigFM; ++i) {
-            const int r = wm * kBigWTM + i * 32 + (lane & 31);
-            a[i] = *(const bf16x8 *)&As[(r * 4 + (c ^ bigswz(r))) * 8];
+            if constexpr (KMA) {
+                a[i] = km_frag(As, ks, wm * kBigWTM + i * 32);
+            } else {
+                const int r = wm * kBigWTM + i * 32 + (lane & 31);
+                a[i] = *(const bf16x8 *)&As[(r * 4 + (c ^ bigswz(r))) * 8];
+            }
         }
 #pragma unroll
         for (int j = 0; j < kBigFN; ++j) {
-            const int r = wn * kBigWTN + j * 32 + (lane & 31);
-            b[j] = *(const bf16x8 *)&Bs[(r * 4 + (c ^ bigswz(r))) * 8];
+            if constexpr (KMB) {
+                b[j] = km_frag(Bs, ks, wn * kBigWTN + j * 32);
+            } else {
+                const int r = wn * kBigWTN + j * 32 + (lane & 31);
+                b[j] = *(const bf16x8 *)&Bs[(r * 4 + (c ^ bigswz(r))) * 8];
+            }
         }
     };
     auto products = [&](const bf16x8 (&a)[kBigFM], const bf16x8 (&b)[kBigFN]) {
@@ -939,7 +989,7 @@ void gemm_bf16_big_kernel(DevArgs args) {
     };
     // the next k-step's LDS reads go out behind the first few products, so
     // they have the rest of the k-step to land
-    constexpr int kReads = kBigFM + kBigFN;
+    constexpr int kReads = (KMA ? 2 : 1) * kBigFM + (KMB ? 2 : 1) * kBigFN;   // a k-major fragment is 2 reads
     constexpr int kReadsPer = GCN_BIG_READS_PER_MFMA;
     constexpr int kReadGroups = (kReads + kReadsPer - 1) / kReadsPer;
     static_assert(kReadGroups <= kBigFM * kBigFN, "a product ahead of every read group");
@@ -1162,10 +1212,12 @@ int bk_of(int mode) { return mode == 2 ? kBigBK : (mode ? BK16 : kBK); }
 int tile_m_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBM16 : kTBM); }
 int tile_n_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBN16 : kTBN); }
 
-// The large-tile bf16 kernel takes NT products whose K-segments are multiples
-// of its k-stage, with 16-byte aligned operand rows.
+// The large-tile bf16 kernel takes NT, TN and NN products whose K-segments
+// are multiples of its k-stage, with 16-byte aligned operand rows; a k-major
+// operand (A of TN, B of TN and NN) also needs a multiple of 8 rows.
 bool big_ok(int layout, int nprob, const GemmProblem *probs) {
-    if (layout != L_NT || GCN_BF16_BIG == 0) return false;
+    if (GCN_BF16_BIG == 0) return false;
+    const bool kma = layout == L_TN, kmb = layout != L_NT;
     for (int i = 0; i < nprob; ++i) {
         if (!GCN_BIG_MASKED && probs[i].mask16) return false;
         // A side of 128 or less leaves most of a 256-wide tile idle.  Still
@@ -1180,6 +1232,7 @@ bool big_ok(int layout, int nprob, const GemmProblem *probs) {
             if (sg.K == 0) continue;
             if (sg.K % kBigBK || sg.lda % 8 || sg.ldb % 8 || !al(sg.A, 16) || !al(sg.B, 16)) return false;
         }
+        if ((kma && probs[i].M % 8) || (kmb && probs[i].N % 8)) return false;
     }
     return true;
 }
@@ -1254,6 +1307,8 @@ void launch(bool vec, bool bf16, dim3 grid, hipStream_t s, const DevArgs &a) {
 }
 
 }  // namespace
+
+bool gemm_bf16_big_ok(int layout, int nprob, const GemmProblem *probs) { return big_ok(layout, nprob, probs); }
 
 #ifndef GCN_SPLIT_MIN_TILES
 #define GCN_SPLIT_MIN_TILES 256
@@ -1369,7 +1424,7 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
     if (big) {
         bool masked = false;
         for (int i = 0; i < nprob; ++i) masked = masked || probs[i].mask16;
-        cls = masked ? K_GEMM_NT_BF16_BIG_MASKED : K_GEMM_NT_BF16_BIG;
+        cls = masked ? K_GEMM_NT_BF16_BIG_MASKED : (layout == L_NT ? K_GEMM_NT_BF16_BIG : K_GEMM_TN_BF16_BIG);
     }
     {
         ProfScope ps(cls, s, flops, bytes);
@@ -1381,9 +1436,13 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
                 any32 = any32 || a.p[i].split > 1 || probs[i].C;
                 any16 = any16 || (a.p[i].split == 1 && probs[i].C16);
             }
-            if (!any16) hipLaunchKernelGGL(gemm_bf16_big_kernel<BIG_F32>, grid, dim3(kBigThreads), 0, s, a);
-            else if (!any32) hipLaunchKernelGGL(gemm_bf16_big_kernel<BIG_B16>, grid, dim3(kBigThreads), 0, s, a);
-            else hipLaunchKernelGGL(gemm_bf16_big_kernel<BIG_ALL>, grid, dim3(kBigThreads), 0, s, a);
+            const int out = !any16 ? BIG_F32 : (!any32 ? BIG_B16 : BIG_ALL);
+#define GCN_BIG_LAUNCH(O, LY)                                                                           \
+    if (out == O && layout == LY) hipLaunchKernelGGL((gemm_bf16_big_kernel<O, LY>), grid, dim3(kBigThreads), 0, s, a);
+            GCN_BIG_LAUNCH(BIG_F32, L_NT) GCN_BIG_LAUNCH(BIG_B16, L_NT) GCN_BIG_LAUNCH(BIG_ALL, L_NT)
+            GCN_BIG_LAUNCH(BIG_F32, L_TN) GCN_BIG_LAUNCH(BIG_B16, L_TN) GCN_BIG_LAUNCH(BIG_ALL, L_TN)
+            GCN_BIG_LAUNCH(BIG_F32, L_NN) GCN_BIG_LAUNCH(BIG_B16, L_NN) GCN_BIG_LAUNCH(BIG_ALL, L_NN)
+#undef GCN_BIG_LAUNCH
         }
         else if (layout == L_NN) launch<L_NN>(vec, bf16 != 0, grid, s, a);
         else if (layout == L_TN) launch<L_TN>(vec, bf16 != 0, grid, s, a);

@@ -225,6 +225,25 @@ def test_config_step_parity_bf16_chain(cfg):
     print("bf16 chain:", errs)
 
 
+@pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
+def test_bf16_weight_gradients_from_row_major_operands(order):
+    """Weight gradients read H, AGG, dZ and G as the layer keeps them (n rows,
+    k-major for the product) on the large-tile kernel, both orders, two
+    layers; the chained step against the oracle."""
+    wl = synth.custom(4096, "rmat", 10, [(256, 256), (512, 192)], head="ce", classes=20, seed=7)
+    r = StepRunner(wl, prec=B.GCN_BF16, orders=[order, order], first_layer_dH=True)
+    print(f"bf16 row-major weight gradients, order {order}", flush=True)
+    B.gcn_profile_reset()
+    B.gcn_profile_enable(True)
+    r.step()
+    torch.cuda.synchronize()
+    B.gcn_profile_enable(False)
+    prof = B.gcn_profile_read_all()
+    assert prof["gemm_tn_bf16_big"][1] == 2, prof
+    errs, _ = compare_bf16_chain(r, wl, first_layer_dH=True)
+    print("bf16 chain:", errs)
+
+
 @pytest.mark.parametrize("prec", [B.GCN_F32, B.GCN_BF16])
 @pytest.mark.parametrize("order", [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST])
 def test_zero_vertex_subgraph(prec, order, ws):
@@ -287,7 +306,7 @@ def test_forced_orders_agree_with_oracle(order):
 
 
 @pytest.mark.parametrize("case", ["cfg1-f32", "cfg1-bf16", "cfg2-bf16", "dY-f32", "bce-transform-first",
-                                  "f32-odd-widths", "bf16-odd-widths", "bf16-odd-wide"])
+                                  "f32-odd-widths", "bf16-odd-widths", "bf16-odd-wide", "bf16-row-major-dw"])
 def test_model_step_matches_separate_calls(case):
     """gcn_model_step computes what the separate calls compute: every output
     bit for bit, except that a layer whose dZ arrives from the head or from an
@@ -305,6 +324,9 @@ def test_model_step_matches_separate_calls(case):
         wl = synth.custom(2999, "rmat", 9, [(70, 51), (102, 50)], head="ce", classes=13, seed=5)
         r = StepRunner(wl, prec=B.GCN_BF16 if case.startswith("bf16") else B.GCN_F32,
                        orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
+    elif case == "bf16-row-major-dw":   # weight gradients on k-major operands, aggregate-first
+        wl = synth.custom(4096, "rmat", 10, [(256, 256), (512, 192)], head="ce", classes=20, seed=7)
+        r = StepRunner(wl, prec=B.GCN_BF16, orders=[B.GCN_AGGREGATE_FIRST] * 2, first_layer_dH=True)
     elif case == "bf16-odd-wide":   # masked input gradient on the large-tile kernel, 150-wide mask rows
         wl = synth.custom(2999, "rmat", 9, [(300, 75), (150, 64)], head="ce", classes=13, seed=6)
         r = StepRunner(wl, prec=B.GCN_BF16, orders=[B.GCN_TRANSFORM_FIRST] * 2, first_layer_dH=True)
@@ -323,6 +345,8 @@ def test_model_step_matches_separate_calls(case):
     b = r.results()
     if case == "bf16-odd-wide":   # the masked input gradient really ran on the large-tile kernel
         assert prof["gemm_nt_bf16_big_masked"][1] >= 1, prof
+    if case == "bf16-row-major-dw":
+        assert prof["gemm_tn_bf16_big"][1] == 2, prof
     inner = [t.detach().cpu().numpy() for t in ([r.dHL] if r.head is not None else []) + r.dH[1:]]
     for key in ("Y", "dW_self", "dW_neigh", "dH"):
         for i, (x, y) in enumerate(zip(a[key], b[key])):
