@@ -396,6 +396,13 @@ class ModelStep:
         """Where the next call writes its loss (a 1-element float32 device tensor)."""
         self.head.loss = loss.data_ptr()
 
+    def set_labels(self, labels: Optional[torch.Tensor] = None, targets: Optional[torch.Tensor] = None):
+        """Where the next call reads its labels (int32, CE) or targets
+        (float32 n x C, BCE): the head of a subgraph in another input buffer."""
+        self._labels_ref = (labels, targets)
+        self.head.labels = None if labels is None else labels.data_ptr()
+        self.head.targets = None if targets is None else targets.data_ptr()
+
     def workspace_bytes(self, n: int, nnz: int) -> int:
         return int(lib().gcn_model_workspace_bytes(n, nnz, self.L, self.arr, self._head_ref, self.prec))
 

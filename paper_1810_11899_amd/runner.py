@@ -136,6 +136,25 @@ class StepRunner:
         else:
             self.AT = B.DeviceCSR(self.n, self.n, self.t_indptr, self.t_indices[:self.nnz], self.t_vals[:self.nnz])
 
+    def attach(self, slot: "InputSlot"):
+        """Run the next steps on the subgraph held in an input slot (its CSR,
+        H0 and labels), in place of the runner's own input buffers."""
+        if slot.n != self.n or slot.index_bits != self.index_bits:
+            raise ValueError("input slot built for another runner")
+        self.nnz = slot.nnz
+        self.H0 = slot.H0
+        self.A = B.DeviceCSR(self.n, self.n, slot.indptr, slot.indices[:slot.nnz], slot.vals[:slot.nnz])
+        self.symmetric = slot.symmetric
+        if self.symmetric:
+            self.AT = B.DeviceCSR(self.n, self.n, slot.indptr, slot.indices[:slot.nnz], slot.t_vals[:slot.nnz])
+        else:
+            self.AT = B.DeviceCSR(self.n, self.n, slot.t_indptr, slot.t_indices[:slot.nnz], slot.t_vals[:slot.nnz])
+        if self.head is None:
+            self.dY = slot.dY
+        else:
+            self.labels, self.targets = slot.labels, slot.targets
+            self.model.set_labels(slot.labels, slot.targets)
+
     # --------------------------------------------------------------- step
     def _transpose(self, stream):
         if self.symmetric:
@@ -274,3 +293,134 @@ def step_work(n: int, nnz: int, dims, orders, need_dH, classes: int = 0) -> dict
         f2 = 2 * dims[-1][1]
         fl += 3 * 2.0 * n * f2 * classes      # logits, dW_pred, dH_L
     return {"edge_features": float(ef), "gemm_flops": fl, "spmm_flops": 2.0 * ef}
+
+
+class InputSlot:
+    """One subgraph's inputs resident on the device (A's CSR with room for
+    A^T, H0, and the labels, targets or given output gradient), with pinned
+    host buffers of the same sizes from which they are uploaded
+    asynchronously.  Two slots double-buffer an epoch stream (EpochPipeline):
+    the next subgraph is uploaded into one while the step runs on the other.
+
+    Events order the reuse: `uploaded` is recorded on the copy stream behind
+    a slot's uploads (the host refills the pinned buffers only after it, the
+    compute stream starts the step only after it); `released` is recorded on
+    the compute stream behind the step that read the slot (the next upload
+    into the slot waits for it)."""
+
+    def __init__(self, runner: StepRunner, nnz_capacity: int):
+        n, dev = runner.n, runner.dev
+        self.n, self.index_bits, self.cap = n, runner.index_bits, max(int(nnz_capacity), 1)
+        idt = torch.int16 if runner.index_bits == 16 else torch.int32
+
+        def pair(shape, dtype):
+            return (torch.empty(shape, dtype=dtype, device=dev),
+                    torch.empty(shape, dtype=dtype, pin_memory=True))
+        self.indptr, self._h_indptr = pair(n + 1, torch.int32)
+        self.indices, self._h_indices = pair(self.cap, idt)
+        self.vals, self._h_vals = pair(self.cap, torch.float32)
+        self.t_indptr = torch.empty(n + 1, dtype=torch.int32, device=dev)
+        self.t_indices = torch.empty(self.cap, dtype=torch.int32, device=dev)
+        self.t_vals = torch.empty(self.cap, dtype=torch.float32, device=dev)
+        self.H0, self._h_H0 = pair(tuple(runner.H0.shape), torch.float32)
+        self.labels = self.targets = self.dY = None
+        self._h_labels = self._h_targets = self._h_dY = None
+        if runner.head is None:
+            self.dY, self._h_dY = pair(tuple(runner.dY.shape), torch.float32)
+        elif runner.head == "ce":
+            self.labels, self._h_labels = pair(n, torch.int32)
+        else:
+            self.targets, self._h_targets = pair((n, runner.spec.classes), torch.float32)
+        self.uploaded = torch.cuda.Event()
+        self.released = torch.cuda.Event()
+        self.nnz = 0
+        self.symmetric = False
+        self.bytes = 0
+
+    def stage(self, wl, symmetric: bool):
+        """Host side: copy subgraph `wl` into the pinned buffers, once the
+        previous upload from them has finished."""
+        g = wl.graph
+        if g.n != self.n:
+            raise ValueError("subgraph size differs from the slot")
+        if g.nnz > self.cap:
+            raise ValueError(f"subgraph has {g.nnz} entries, the slot holds {self.cap}")
+        self.uploaded.synchronize()
+        self.nnz, self.symmetric = int(g.nnz), bool(symmetric)
+        self._h_indptr.numpy()[:] = g.indptr
+        ix = self._h_indices.numpy()
+        ix[:g.nnz] = g.indices.astype(np.uint16).view(np.int16) if self.index_bits == 16 else g.indices
+        self._h_vals.numpy()[:g.nnz] = g.vals
+        self._h_H0.numpy()[:] = wl.H
+        if self._h_dY is not None:
+            self._h_dY.numpy()[:] = wl.dY
+        if self._h_labels is not None:
+            self._h_labels.numpy()[:] = wl.labels
+        if self._h_targets is not None:
+            self._h_targets.numpy()[:] = wl.targets
+
+    def upload(self, copy_stream, start_event=None):
+        """Enqueue the uploads on `copy_stream`, behind the release of the
+        slot by the last step that read it (start_event, if given, is
+        recorded once that release has been waited for)."""
+        nnz = self.nnz
+        copy_stream.wait_event(self.released)
+        if start_event is not None:
+            start_event.record(copy_stream)
+        with torch.cuda.stream(copy_stream):
+            pairs = [(self.indptr, self._h_indptr), (self.indices[:nnz], self._h_indices[:nnz]),
+                     (self.vals[:nnz], self._h_vals[:nnz]), (self.H0, self._h_H0)]
+            for d, h in ((self.dY, self._h_dY), (self.labels, self._h_labels), (self.targets, self._h_targets)):
+                if d is not None:
+                    pairs.append((d, h))
+            for d, h in pairs:
+                d.copy_(h, non_blocking=True)
+            self.uploaded.record(copy_stream)
+        self.bytes = sum(h.numel() * h.element_size() for _, h in pairs)
+
+
+class EpochPipeline:
+    """An epoch stream of independent subgraphs of one size (Alg. 5's pool
+    of sampled subgraphs, here drawn on the host): each subgraph goes through
+    pinned host buffers on a copy stream into one of `slots` device input
+    slots, and its step runs on the compute stream once its upload is done,
+    so the upload of subgraph s + 1 overlaps the step of subgraph s.  The
+    runner's weights, activations, gradients and workspace are shared by the
+    stream."""
+
+    def __init__(self, runner: StepRunner, nnz_capacity: int, slots: int = 2, compute_stream=None):
+        if slots < 1:
+            raise ValueError("at least one input slot")
+        self.runner = runner
+        self.slots = [InputSlot(runner, nnz_capacity) for _ in range(slots)]
+        self.copy_stream = torch.cuda.Stream(device=runner.dev)
+        self.compute_stream = compute_stream if compute_stream is not None else torch.cuda.current_stream(runner.dev)
+        # the workspace sized for the largest subgraph up front: no
+        # reallocation while steps are in flight
+        runner.ws.get(runner.model.workspace_bytes(runner.n, int(nnz_capacity)))
+        self.count = 0
+
+    def submit(self, wl, symmetric: Optional[bool] = None, events=None):
+        """Stage, upload and step subgraph `wl`.  events: None, or four
+        timing events (upload start, upload end, step start, step end) to
+        record around the upload on the copy stream and the step on the
+        compute stream."""
+        slot = self.slots[self.count % len(self.slots)]
+        self.count += 1
+        if symmetric is None:
+            g = wl.graph
+            symmetric = self.runner.transpose_shortcut and B.gcn_csr_pattern_symmetric_host(g.indptr, g.indices)
+        slot.stage(wl, symmetric)
+        slot.upload(self.copy_stream, None if events is None else events[0])
+        if events is not None:
+            events[1].record(self.copy_stream)
+        cs = self.compute_stream
+        cs.wait_event(slot.uploaded)
+        self.runner.attach(slot)
+        if events is not None:
+            events[2].record(cs)
+        self.runner.step(cs)
+        if events is not None:
+            events[3].record(cs)
+        slot.released.record(cs)
+        return slot

@@ -49,20 +49,81 @@ def test_rmat65536_two_layer_bf16_chained_step():
 
 
 def test_epoch_stream_subgraphs_reuse_buffers():
-    """Several subgraphs of the stream through one runner (buffers sized for
-    the largest nnz, reused); each checked against the oracle."""
+    """The oracle subset of the stream (subgraphs 0, 1, 2, 50, 100, 150, 198,
+    199) through the double-buffered upload pipeline of one runner (input
+    slots sized for the largest nnz, activations and workspace reused); each
+    checked against the oracle."""
     spec = synth.WORKLOADS[4]
     subs = [0, 1, 2, 50, 100, 150, 198, 199]
     wls = [synth.config(4, s=s) for s in subs]
-    cap = max(w.graph.nnz for w in wls)
+    cap = spec.n * spec.d_range[1]
     r = StepRunner(wls[0], nnz_capacity=cap)
-    for w in wls:
-        r.load(w)
-        r.step()
+    from paper_1810_11899_amd.runner import EpochPipeline
+    pipe = EpochPipeline(r, cap, slots=2)       # as the benchmark streams them
+    for s, w in zip(subs, wls):
+        print(f"stream subgraph {s}: nnz={w.graph.nnz}", flush=True)
+        pipe.submit(w)
         torch.cuda.synchronize()
         compare_step(r.results(), oracle.step(w, envelope=True))
     assert len({w.graph.nnz for w in wls}) > 1  # the stream really varies nnz
     assert spec.subgraphs == 200
+
+
+@pytest.mark.parametrize("prec", [0, 1])
+def test_epoch_pipeline_matches_serial_loads(prec):
+    """The double-buffered stream (pinned uploads on a copy stream into two
+    input slots, each step behind its upload, each upload behind the release
+    of its slot) computes, subgraph by subgraph, bit for bit what loading
+    each subgraph synchronously and stepping computes.  The outputs of every
+    step are copied on the compute stream behind it and compared at the end,
+    so the uploads really overlap the steps.  Subgraphs vary in nnz; one has a
+    non-symmetric pattern (general transpose), one is a BCE head's."""
+    import dataclasses
+    from paper_1810_11899_amd import binding as B
+    from paper_1810_11899_amd.runner import EpochPipeline
+    wls = [synth.custom(3000, "rmat", d, [(64, 64), (128, 32)], head="ce", classes=10, seed=s)
+           for s, d in enumerate([8, 12, 6, 10, 9, 12, 7])]
+    g = wls[3].graph
+    rows = np.repeat(np.arange(g.n), g.degrees())
+    keep = (rows + g.indices) % 3 != 0
+    wls[3] = dataclasses.replace(wls[3], graph=synth.csr_from_pairs(g.n, rows[keep], g.indices[keep]))
+    cap = max(w.graph.nnz for w in wls)
+    ref = StepRunner(wls[0], prec=prec, nnz_capacity=cap)
+    want = []
+    for w in wls:
+        ref.load(w)
+        ref.step()
+        torch.cuda.synchronize()
+        want.append([ref.loss.cpu().numpy()] + [t.cpu().numpy() for t in ref.dWs + ref.dWn + ref.db]
+                    + [ref.dW_pred.cpu().numpy(), ref.db_pred.cpu().numpy()])
+    run = StepRunner(wls[0], prec=prec, nnz_capacity=cap)
+    pipe = EpochPipeline(run, cap, slots=2)
+    got = []
+    for i, w in enumerate(wls):
+        print(f"pipelined subgraph {i} nnz={w.graph.nnz}", flush=True)
+        pipe.submit(w)
+        got.append([run.loss.clone()] + [t.clone() for t in run.dWs + run.dWn + run.db]
+                   + [run.dW_pred.clone(), run.db_pred.clone()])
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(want, got)):
+        for x, y in zip(a, b):
+            assert np.array_equal(x, y.cpu().numpy()), i
+    # a different head kind through the slots: BCE targets
+    wb = [synth.custom(2000, "er", d, [(32, 32)], head="bce", classes=6, seed=10 + d) for d in (5, 9, 7)]
+    capb = max(w.graph.nnz for w in wb)
+    refb = StepRunner(wb[0], prec=prec, nnz_capacity=capb)
+    runb = StepRunner(wb[0], prec=prec, nnz_capacity=capb)
+    pipeb = EpochPipeline(runb, capb, slots=2)
+    outs = []
+    for w in wb:
+        pipeb.submit(w)
+        outs.append((runb.loss.clone(), runb.dWs[0].clone()))
+    for w, (l, dw) in zip(wb, outs):
+        refb.load(w)
+        refb.step()
+        torch.cuda.synchronize()
+        assert np.array_equal(refb.loss.cpu().numpy(), l.cpu().numpy())
+        assert np.array_equal(refb.dWs[0].cpu().numpy(), dw.cpu().numpy())
 
 
 def _f32(a):
