@@ -112,7 +112,8 @@ int gcn_frontier_sample(const gcn_csr *G, const gcn_sampler_params *p, int64_t f
  *                                 (then no edge is written; size the arrays
  *                                 from edge_offsets[S] and call again)
  * Vertex ids outside [0, n_vertices) in `vertices` are skipped.  The
- * workspace holds an S x n_vertices int32 map. */
+ * workspace holds, per list, a membership bitmap of n_vertices bits and an
+ * int32 prefix count per 32 vertices (8 bytes per 32 vertices of G). */
 size_t gcn_induce_workspace_bytes(int32_t n_vertices, int32_t n, int32_t S);
 int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *vertices, const int32_t *counts,
                          int32_t *n_sub, int32_t *vsub, int32_t *indptr_sub, int64_t *edge_offsets,

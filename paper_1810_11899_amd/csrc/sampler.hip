@@ -21,6 +21,7 @@
 // SC 2011) keyed by (seed, sampler id); each block gives four draws.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "common.h"
 #include "gcn_sampler.h"
@@ -308,29 +309,38 @@ __global__ __launch_bounds__(kTB) void fill_i32_kernel(int32_t *__restrict__ x, 
     for (int64_t i = (int64_t)blockIdx.x * kTB + threadIdx.x; i < n; i += (int64_t)gridDim.x * kTB) x[i] = v;
 }
 
-// map[s][v] = 1 for every sampled v of subgraph s (duplicates collapse)
-__global__ __launch_bounds__(kTB) void mark_kernel(int32_t nV, int32_t n, const int32_t *__restrict__ vertices,
-                                                   const int32_t *__restrict__ counts, int32_t *__restrict__ map) {
+// The sample sets are membership bitmaps, one bit per vertex of G per list:
+// bits[s][v / 32] bit v % 32.  With wpre[s][k], the number of sampled
+// vertices in words 0 .. k-1, the local id of a sampled vertex v (its rank
+// among the list's distinct vertices in ascending order) is
+// wpre[s][v / 32] + popcount of the bits of word v / 32 below v.  A list's
+// bitmap and prefix take 8 bytes per 32 vertices of G, so the row kernels
+// hold them in LDS and look each neighbour up there (the neighbour lists of
+// G stream from memory coalesced; nothing else is read per neighbour).
+
+// bits[s][v / 32] |= bit v % 32 for every sampled v of list s (duplicates collapse)
+__global__ __launch_bounds__(kTB) void mark_kernel(int32_t nV, int32_t n, int32_t W,
+                                                   const int32_t *__restrict__ vertices,
+                                                   const int32_t *__restrict__ counts, uint32_t *__restrict__ bits) {
     const int s = blockIdx.y;
     const int32_t cnt = min(counts[s], n);
     for (int32_t i = blockIdx.x * kTB + threadIdx.x; i < cnt; i += gridDim.x * kTB) {
         const int32_t v = vertices[(int64_t)s * n + i];
-        if ((uint32_t)v < (uint32_t)nV) map[(int64_t)s * nV + v] = 1;
+        if ((uint32_t)v < (uint32_t)nV) atomicOr(&bits[(int64_t)s * W + (v >> 5)], 1u << (v & 31));
     }
 }
 
-// per (segment, tile): sum of the tile's values
-__global__ __launch_bounds__(kTB) void seg_tile_sum_kernel(const int32_t *__restrict__ x, int64_t len,
-                                                           int64_t stride, int64_t *__restrict__ tsum,
-                                                           int32_t tiles) {
+// per (list, tile of kTile words): the number of set bits in the tile
+__global__ __launch_bounds__(kTB) void popc_tile_sum_kernel(const uint32_t *__restrict__ bits, int32_t W,
+                                                            int64_t *__restrict__ tsum, int32_t tiles) {
     const int s = blockIdx.y;
     const int64_t t0 = (int64_t)blockIdx.x * kTile;
-    const int32_t *xs = x + (int64_t)s * stride;
+    const uint32_t *bs = bits + (int64_t)s * W;
     int64_t acc = 0;
 #pragma unroll
     for (int j = 0; j < kItems; ++j) {
         const int64_t i = t0 + (int64_t)threadIdx.x * kItems + j;
-        if (i < len) acc += xs[i];
+        if (i < W) acc += __popc(bs[i]);
     }
     int64_t total;
     block_excl_scan(acc, total);
@@ -354,70 +364,100 @@ __global__ __launch_bounds__(kTB) void seg_tile_scan_kernel(int64_t *__restrict_
     if (threadIdx.x == 0) seg_total[s] = carry;
 }
 
-// map[s][v] <- marked ? local id + 1 : 0;  vsub[s][local id] = v
-__global__ __launch_bounds__(kTB) void rank_kernel(int32_t nV, int32_t n, int32_t *__restrict__ map,
+// wpre[s][k] = sampled vertices in words 0 .. k-1;  vsub[s][local id] = v
+__global__ __launch_bounds__(kTB) void rank_kernel(int32_t n, int32_t W, const uint32_t *__restrict__ bits,
                                                    const int64_t *__restrict__ toff, int32_t tiles,
-                                                   int32_t *__restrict__ vsub) {
+                                                   int32_t *__restrict__ wpre, int32_t *__restrict__ vsub) {
     const int s = blockIdx.y;
     const int64_t t0 = (int64_t)blockIdx.x * kTile;
-    int32_t *ms = map + (int64_t)s * nV;
-    int32_t vals[kItems];
+    const uint32_t *bs = bits + (int64_t)s * W;
+    uint32_t words[kItems];
     int64_t acc = 0;
 #pragma unroll
     for (int j = 0; j < kItems; ++j) {
         const int64_t i = t0 + (int64_t)threadIdx.x * kItems + j;
-        vals[j] = i < nV ? ms[i] : 0;
-        acc += vals[j];
+        words[j] = i < W ? bs[i] : 0u;
+        acc += __popc(words[j]);
     }
     int64_t total;
     int64_t r = toff[(int64_t)s * tiles + blockIdx.x] + block_excl_scan(acc, total);
 #pragma unroll
     for (int j = 0; j < kItems; ++j) {
         const int64_t i = t0 + (int64_t)threadIdx.x * kItems + j;
-        if (i < nV && vals[j]) {
-            ms[i] = (int32_t)(r + 1);
-            if (r < n) vsub[(int64_t)s * n + r] = (int32_t)i;
+        if (i < W) wpre[(int64_t)s * W + i] = (int32_t)r;
+        for (uint32_t b = words[j]; b; b &= b - 1u) {
+            if (r < n) vsub[(int64_t)s * n + r] = (int32_t)(32 * i + __builtin_ctz(b));
             ++r;
         }
     }
 }
 
-// row length of every local row: neighbours of vsub[s][i] that are in the sample
-__global__ __launch_bounds__(kTB) void row_count_kernel(int32_t nV, int32_t n, const int32_t *__restrict__ indptr,
-                                                        const int32_t *__restrict__ indices,
-                                                        const int32_t *__restrict__ map,
-                                                        const int64_t *__restrict__ n_sub,
-                                                        const int32_t *__restrict__ vsub,
-                                                        int32_t *__restrict__ rowlen) {
+// Row kernels: one block of kRowThreads takes rows [b R, (b+1) R) of list s
+// (R = kRowsPerBlock), clipped to the list's distinct vertices; its
+// wavefronts take the next row from an LDS counter (hub rows of G are
+// hundreds of times longer than the median one).  TABLE_LDS: the list's
+// bitmap (and prefix) copied into LDS first; otherwise read where they are.
+constexpr int kRowThreads = 1024;
+constexpr int kRowsPerBlock = 256;
+constexpr size_t kInduceMaxLds = 128 * 1024;
+
+__device__ __forceinline__ int32_t next_row(int32_t *ctr, int lane) {
+    int32_t r = 0;
+    if (lane == 0) r = atomicAdd(ctr, 1);
+    return __shfl(r, 0);
+}
+
+// row length of every local row: neighbours of vsub[s][i] that are in the list
+template <bool TABLE_LDS>
+__global__ __launch_bounds__(kRowThreads) void row_count_kernel(int32_t nV, int32_t n, int32_t W,
+                                                                const int32_t *__restrict__ indptr,
+                                                                const int32_t *__restrict__ indices,
+                                                                const uint32_t *__restrict__ bits,
+                                                                const int64_t *__restrict__ n_sub,
+                                                                const int32_t *__restrict__ vsub,
+                                                                int32_t *__restrict__ rowlen) {
+    extern __shared__ uint32_t tab[];
+    __shared__ int32_t ctr;
     const int s = blockIdx.y;
     const int lane = threadIdx.x & 63;
-    const int32_t i = blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
-    if (i >= n) return;
-    int32_t cnt = 0;
-    if (i < n_sub[s]) {
+    const int32_t r0 = blockIdx.x * kRowsPerBlock;
+    const int32_t r1 = (int32_t)min<int64_t>((int64_t)r0 + kRowsPerBlock, min<int64_t>(n_sub[s], n));
+    if (r0 >= r1) return;
+    const uint32_t *bs = bits + (int64_t)s * W;
+    if (TABLE_LDS) {
+        for (int32_t k = threadIdx.x; k < W; k += kRowThreads) tab[k] = bs[k];
+        bs = tab;
+    }
+    if (threadIdx.x == 0) ctr = r0;
+    __syncthreads();
+    for (int32_t i = next_row(&ctr, lane); i < r1; i = next_row(&ctr, lane)) {
         const int32_t u = vsub[(int64_t)s * n + i];
-        const int32_t *ms = map + (int64_t)s * nV;
-        for (int32_t p = indptr[u] + lane; p < indptr[u + 1]; p += 64) {
+        const int32_t p1 = indptr[u + 1];
+        int32_t cnt = 0;
+        for (int32_t p = indptr[u] + lane; p < p1; p += 64) {
             const int32_t w = indices[p];
-            cnt += ((uint32_t)w < (uint32_t)nV && ms[w] > 0) ? 1 : 0;
+            cnt += ((uint32_t)w < (uint32_t)nV) ? (int32_t)((bs[w >> 5] >> (w & 31)) & 1u) : 0;
         }
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) cnt += __shfl_xor(cnt, o, 64);
+        if (lane == 0) rowlen[(int64_t)s * n + i] = cnt;
     }
-    if (lane == 0) rowlen[(int64_t)s * n + i] = cnt;
 }
 
-// per subgraph: indptr = exclusive scan of the row lengths (one block each)
+// per subgraph: indptr = exclusive scan of the row lengths (one block each);
+// rows past the list's distinct vertices are empty
 __global__ __launch_bounds__(kTB) void row_scan_kernel(int32_t n, const int32_t *__restrict__ rowlen,
+                                                       const int64_t *__restrict__ n_sub,
                                                        int32_t *__restrict__ indptr_sub,
                                                        int64_t *__restrict__ nnz_sub) {
     const int s = blockIdx.x;
     const int32_t *rl = rowlen + (int64_t)s * n;
     int32_t *ip = indptr_sub + (int64_t)s * (n + 1);
+    const int64_t ns = n_sub[s];
     int64_t carry = 0;
     for (int32_t base = 0; base < n; base += kTB) {
         const int32_t i = base + threadIdx.x;
-        const int64_t v = i < n ? rl[i] : 0;
+        const int64_t v = i < ns ? rl[i] : 0;
         int64_t total;
         const int64_t ex = block_excl_scan(v, total);
         if (i < n) ip[i] = (int32_t)(carry + ex);
@@ -449,42 +489,65 @@ __global__ __launch_bounds__(kTB) void edge_offsets_kernel(int32_t S, const int6
 }
 
 // local column ids and mean weights of every row, in neighbour order
-__global__ __launch_bounds__(kTB) void fill_rows_kernel(int32_t nV, int32_t n, const int32_t *__restrict__ indptr,
-                                                        const int32_t *__restrict__ indices,
-                                                        const int32_t *__restrict__ map,
-                                                        const int64_t *__restrict__ n_sub,
-                                                        const int32_t *__restrict__ vsub,
-                                                        const int32_t *__restrict__ indptr_sub,
-                                                        const int64_t *__restrict__ off,
-                                                        const int32_t *__restrict__ status,
-                                                        int32_t *__restrict__ sub_indices,
-                                                        float *__restrict__ sub_vals,
-                                                        float *__restrict__ sub_vals_t) {
+template <bool TABLE_LDS>
+__global__ __launch_bounds__(kRowThreads) void fill_rows_kernel(int32_t nV, int32_t n, int32_t W,
+                                                                const int32_t *__restrict__ indptr,
+                                                                const int32_t *__restrict__ indices,
+                                                                const uint32_t *__restrict__ bits,
+                                                                const int32_t *__restrict__ wpre,
+                                                                const int64_t *__restrict__ n_sub,
+                                                                const int32_t *__restrict__ vsub,
+                                                                const int32_t *__restrict__ indptr_sub,
+                                                                const int64_t *__restrict__ off,
+                                                                const int32_t *__restrict__ status,
+                                                                int32_t *__restrict__ sub_indices,
+                                                                float *__restrict__ sub_vals,
+                                                                float *__restrict__ sub_vals_t) {
+    extern __shared__ uint32_t tab[];
+    __shared__ int32_t ctr;
     const int s = blockIdx.y;
     const int lane = threadIdx.x & 63;
-    const int32_t i = blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
-    if (*status != 0 || i >= n || i >= n_sub[s]) return;
-    const int32_t u = vsub[(int64_t)s * n + i];
-    const int32_t *ms = map + (int64_t)s * nV;
+    const int32_t r0 = blockIdx.x * kRowsPerBlock;
+    const int32_t r1 = (int32_t)min<int64_t>((int64_t)r0 + kRowsPerBlock, min<int64_t>(n_sub[s], n));
+    if (*status != 0 || r0 >= r1) return;
+    const uint32_t *bs = bits + (int64_t)s * W;
+    const int32_t *ps = wpre + (int64_t)s * W;
+    if (TABLE_LDS) {
+        for (int32_t k = threadIdx.x; k < W; k += kRowThreads) {
+            tab[k] = bs[k];
+            tab[W + k] = (uint32_t)ps[k];
+        }
+        bs = tab;
+        ps = (const int32_t *)(tab + W);
+    }
+    if (threadIdx.x == 0) ctr = r0;
+    __syncthreads();
     const int32_t *ip = indptr_sub + (int64_t)s * (n + 1);
-    const int32_t len = ip[i + 1] - ip[i];
-    const float val = 1.0f / (float)len;
-    int64_t pos = off[s] + ip[i];
-    for (int32_t p0 = indptr[u]; p0 < indptr[u + 1]; p0 += 64) {
-        const int32_t p = p0 + lane;
-        int32_t loc = -1;
-        if (p < indptr[u + 1]) {
-            const int32_t w = indices[p];
-            if ((uint32_t)w < (uint32_t)nV) loc = ms[w] - 1;
+    for (int32_t i = next_row(&ctr, lane); i < r1; i = next_row(&ctr, lane)) {
+        const int32_t u = vsub[(int64_t)s * n + i];
+        const int32_t len = ip[i + 1] - ip[i];
+        const float val = 1.0f / (float)len;
+        int64_t pos = off[s] + ip[i];
+        const int32_t p1 = indptr[u + 1];
+        for (int32_t p0 = indptr[u]; p0 < p1; p0 += 64) {
+            const int32_t p = p0 + lane;
+            int32_t loc = -1;
+            if (p < p1) {
+                const int32_t w = indices[p];
+                if ((uint32_t)w < (uint32_t)nV) {
+                    const uint32_t word = bs[w >> 5], below = word & ((1u << (w & 31)) - 1u);
+                    if ((word >> (w & 31)) & 1u) loc = ps[w >> 5] + __popc(below);
+                }
+            }
+            const uint64_t mask = __ballot(loc >= 0);
+            if (loc >= 0) {
+                const int64_t q = pos + __popcll(mask & ((1ull << lane) - 1ull));
+                sub_indices[q] = loc;
+                sub_vals[q] = val;
+                if (sub_vals_t) sub_vals_t[q] = 1.0f / (float)(ip[loc + 1] - ip[loc]);
+            }
+            pos += __popcll(mask);
         }
-        const uint64_t mask = __ballot(loc >= 0);
-        if (loc >= 0) {
-            const int64_t q = pos + __popcll(mask & ((1ull << lane) - 1ull));
-            sub_indices[q] = loc;
-            sub_vals[q] = val;
-            if (sub_vals_t) sub_vals_t[q] = 1.0f / (float)(ip[loc + 1] - ip[loc]);
-        }
-        pos += __popcll(mask);
     }
 }
 
@@ -544,7 +607,8 @@ using namespace gcn;
 
 namespace {
 struct InduceWs {
-    int32_t *map;       // [S][nV]: 0, then local id + 1 of sampled vertices
+    uint32_t *bits;     // [S][W]: membership bitmap of each list (W = words of nV bits)
+    int32_t *wpre;      // [S][W]: sampled vertices in the words before each word
     int64_t *tsum;      // [S][tiles]: tile sums, then their exclusive scan
     int64_t *n_sub64;   // [S]
     int64_t *nnz_sub;   // [S]
@@ -552,8 +616,10 @@ struct InduceWs {
 };
 InduceWs carve_induce(Arena &ar, int32_t nV, int32_t n, int32_t S) {
     InduceWs w;
-    const int32_t tiles = (int32_t)((nV + kTile - 1) / kTile);
-    w.map = ar.take<int32_t>((size_t)S * nV);
+    const int32_t W = (nV + 31) / 32;
+    const int32_t tiles = (int32_t)((W + kTile - 1) / kTile);
+    w.bits = ar.take<uint32_t>((size_t)S * W);
+    w.wpre = ar.take<int32_t>((size_t)S * W);
     w.tsum = ar.take<int64_t>((size_t)S * tiles);
     w.n_sub64 = ar.take<int64_t>(S);
     w.nnz_sub = ar.take<int64_t>(S);
@@ -671,7 +737,7 @@ int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *
     const int32_t nV = G->n_rows;
     Arena ar(ws, ws_bytes);
     InduceWs w = carve_induce(ar, nV, n, S);
-    if (!w.map || !w.rowlen || ((uintptr_t)ws & 255u)) {
+    if (!w.bits || !w.rowlen || ((uintptr_t)ws & 255u)) {
         set_error("gcn_induce_subgraphs: workspace of %zu bytes is too small or misaligned (need %zu)", ws_bytes,
                   gcn_induce_workspace_bytes(nV, n, S));
         return GCN_EWORKSPACE;
@@ -682,28 +748,47 @@ int gcn_induce_subgraphs(const gcn_csr *G, int32_t S, int32_t n, const int32_t *
     }
     hipStream_t s = (hipStream_t)stream;
     ProfScope prof(K_INDUCE, s, 0.0, 0.0);
-    const int32_t tiles = (nV + kTile - 1) / kTile;
-    const int64_t mapn = (int64_t)S * nV;
-    fill_i32_kernel<<<blocks_for(mapn, kTB * 8), kTB, 0, s>>>(w.map, mapn, 0);
+    const int32_t W = (nV + 31) / 32;
+    const int32_t tiles = (W + kTile - 1) / kTile;
+    const int64_t words = (int64_t)S * W;
+    fill_i32_kernel<<<blocks_for(words, kTB * 8), kTB, 0, s>>>((int32_t *)w.bits, words, 0);
     if (n > 0) {
-        mark_kernel<<<dim3(blocks_for(n, kTB), S), kTB, 0, s>>>(nV, n, vertices, counts, w.map);
+        mark_kernel<<<dim3(blocks_for(n, kTB), S), kTB, 0, s>>>(nV, n, W, vertices, counts, w.bits);
     }
-    seg_tile_sum_kernel<<<dim3(tiles, S), kTB, 0, s>>>(w.map, nV, nV, w.tsum, tiles);
+    popc_tile_sum_kernel<<<dim3(tiles, S), kTB, 0, s>>>(w.bits, W, w.tsum, tiles);
     seg_tile_scan_kernel<<<S, kTB, 0, s>>>(w.tsum, tiles, w.n_sub64);
-    rank_kernel<<<dim3(tiles, S), kTB, 0, s>>>(nV, n, w.map, w.tsum, tiles, vsub);
+    rank_kernel<<<dim3(tiles, S), kTB, 0, s>>>(n, W, w.bits, w.tsum, tiles, w.wpre, vsub);
     copy_n_sub_kernel<<<blocks_for(S, kTB), kTB, 0, s>>>(S, w.n_sub64, n_sub);
+    // the row kernels hold a list's bitmap (and prefix) in LDS when they fit
+    const size_t count_lds = (size_t)W * 4, fill_lds = (size_t)W * 8;
+    const bool lds = fill_lds <= kInduceMaxLds;
+    static std::once_flag lds_attr;
+    std::call_once(lds_attr, [] {
+        hipFuncSetAttribute((const void *)row_count_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            kInduceMaxLds);
+        hipFuncSetAttribute((const void *)fill_rows_kernel<true>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            kInduceMaxLds);
+    });
+    const dim3 rgrid((n + kRowsPerBlock - 1) / kRowsPerBlock, S);
     if (n > 0) {
-        const int rb = (n + kTB / 64 - 1) / (kTB / 64);
-        row_count_kernel<<<dim3(rb, S), kTB, 0, s>>>(nV, n, G->indptr, G->indices, w.map, w.n_sub64, vsub,
-                                                     w.rowlen);
+        if (lds)
+            row_count_kernel<true><<<rgrid, kRowThreads, count_lds, s>>>(nV, n, W, G->indptr, G->indices, w.bits,
+                                                                        w.n_sub64, vsub, w.rowlen);
+        else
+            row_count_kernel<false><<<rgrid, kRowThreads, 0, s>>>(nV, n, W, G->indptr, G->indices, w.bits,
+                                                                 w.n_sub64, vsub, w.rowlen);
     }
-    row_scan_kernel<<<S, kTB, 0, s>>>(n, w.rowlen, indptr_sub, w.nnz_sub);
+    row_scan_kernel<<<S, kTB, 0, s>>>(n, w.rowlen, w.n_sub64, indptr_sub, w.nnz_sub);
     edge_offsets_kernel<<<1, kTB, 0, s>>>(S, w.nnz_sub, edge_offsets, edge_capacity, status);
     if (n > 0) {
-        const int rb = (n + kTB / 64 - 1) / (kTB / 64);
-        fill_rows_kernel<<<dim3(rb, S), kTB, 0, s>>>(nV, n, G->indptr, G->indices, w.map, w.n_sub64, vsub,
-                                                     indptr_sub, edge_offsets, status, sub_indices, sub_vals,
-                                                     sub_vals_t);
+        if (lds)
+            fill_rows_kernel<true><<<rgrid, kRowThreads, fill_lds, s>>>(
+                nV, n, W, G->indptr, G->indices, w.bits, w.wpre, w.n_sub64, vsub, indptr_sub, edge_offsets, status,
+                sub_indices, sub_vals, sub_vals_t);
+        else
+            fill_rows_kernel<false><<<rgrid, kRowThreads, 0, s>>>(
+                nV, n, W, G->indptr, G->indices, w.bits, w.wpre, w.n_sub64, vsub, indptr_sub, edge_offsets, status,
+                sub_indices, sub_vals, sub_vals_t);
     }
     GCN_LAUNCH_CHECK("induce kernels");
     return GCN_OK;

@@ -184,7 +184,7 @@ def test_sampler_entry_points_check_arguments_before_launch(L):
                                   0, None, None, 0, None) == B.GCN_EINVAL
     assert L.gcn_gather_rows(fake, 10, 8, 4, fake, 3, fake, 8, None) == B.GCN_ESHAPE
     assert L.gcn_gather_rows(None, 10, 8, 8, None, 0, None, 8, None) == B.GCN_OK   # nothing to do
-    assert L.gcn_induce_workspace_bytes(1000, 100, 4) >= 4 * 1000 * 4
+    assert L.gcn_induce_workspace_bytes(1000, 100, 4) >= 4 * ((1000 + 31) // 32) * 8   # bitmap + prefix per list
 
 
 def test_pattern_symmetry_check(L):

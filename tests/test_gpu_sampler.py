@@ -128,7 +128,9 @@ def check_induced(g, verts, counts, ib):
     ix = ib.indices.cpu().numpy()
     vv = ib.vals.cpu().numpy()
     for s in range(ib.S):
-        ov, oip, oix, ovals = OS.induce(g.indptr, g.indices, verts[s, :counts[s]])
+        v = verts[s, :counts[s]]
+        v = v[(v >= 0) & (v < g.n)]                 # ids outside G are skipped (gcn_sampler.h)
+        ov, oip, oix, ovals = OS.induce(g.indptr, g.indices, v)
         ns = int(n_sub[s])
         assert ns == ov.size
         assert np.array_equal(vsub[s, :ns], ov)
@@ -183,6 +185,33 @@ def test_induce_edge_cases_and_capacity(ws):
     torch.cuda.synchronize()
     assert int(ib.status.item()) == 0
     check_induced(g, verts, counts, ib)
+
+
+def test_induce_large_graph_table_outside_lds(ws):
+    """G of 600,000 vertices: a list's bitmap and prefix (8 bytes per 32
+    vertices, 150 KB) exceed what the row kernels hold in LDS, so they read
+    them from memory.  Lists: a contiguous range, one wrapping the end of the
+    vertex range, a random one with duplicates, one with out-of-range ids."""
+    nV = 600_000
+    g = synth.circulant_graph(nV, [1, 2, 3, 1000])
+    rng = np.random.default_rng(5)
+    S, n = 4, 3000
+    verts = np.empty((S, n), np.int32)
+    verts[0] = np.arange(n)
+    verts[1] = (nV - 1500 + np.arange(n)) % nV
+    verts[2] = rng.integers(nV - 40_000, nV, n)
+    verts[3] = rng.integers(0, 5000, n)
+    verts[3, ::7] = -5
+    verts[3, 3::7] = nV
+    counts = np.array([n, n, n, 2500], np.int32)
+    V, C = torch.from_numpy(verts).cuda(), torch.from_numpy(counts).cuda()
+    ib = B.InducedBatch(S, n, 200_000, "cuda", with_transpose=True)
+    print("induce: nV=600000 S=4 n=3000", flush=True)
+    B.gcn_induce_subgraphs(dcsr(g), V, C, ib, ws)
+    torch.cuda.synchronize()
+    assert int(ib.status.item()) == 0
+    check_induced(g, verts, counts, ib)
+    assert int(ib.edge_offsets[1].item()) > 0
 
 
 # ----------------------------------------------------------------- gather ----
