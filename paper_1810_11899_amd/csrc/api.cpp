@@ -173,6 +173,21 @@ bool bf16_dw_rowmajor(int32_t n, int32_t f_in, int32_t h) {
     return gemm_bf16_big_ok(L_TN, 2, g) && h % 8 == 0;
 }
 
+int32_t pad_classes(int32_t C);
+
+// The head's bfloat16 weight gradient dW_pred = HL^T G as a TN product on the
+// row-major HL and G (the class-padded bfloat16 rows the head keeps) on the
+// large-tile kernel; otherwise NT on transposed copies.
+bool head_dw_rowmajor(int32_t n, int32_t f, int32_t C) {
+    if (n <= 0) return false;
+    const void *p = (const void *)(uintptr_t)256;
+    GemmProblem g = {};
+    g.M = f;
+    g.N = C;
+    g.seg[0] = GemmSeg{p, f, p, pad_classes(C), n};
+    return gemm_bf16_big_ok(L_TN, 1, &g);
+}
+
 bool bwd_uses_G(int order, bool dH, int32_t f_in, int32_t h) {
     return order == GCN_TRANSFORM_FIRST || (dH && h <= f_in);
 }
@@ -846,6 +861,8 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
         HL16 = HL16_ready;
         HL16T = HL16T_ready;
     }
+    const bool tn_dw = bf && head_dw_rowmajor(n, f, C);   // dW_pred from the rows: no transposed copies
+    REQUIRE(!bf || !HL16_ready || tn_dw || HL16T, GCN_EINVAL, "gcn_loss_grad: transposed HL rows missing");
     const int32_t Cp = pad_classes(C);
     uint16_t *Wp16 = bf ? ar.take<uint16_t>((size_t)f * Cp) : nullptr;
     uint16_t *Wp16T = bf ? ar.take<uint16_t>((size_t)f * C) : nullptr;
@@ -871,8 +888,9 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     if (bf) {
         // NT form: B = W_pred^T (C x f)
         if (!HL16_ready &&
-            (rc = transpose_bf16_copy(n, f, HL, 0, ldhl, const_cast<uint16_t *>(HL16T), n, const_cast<uint16_t *>(HL16),
-                                      f, s)))
+            (rc = tn_dw ? cvt_bf16(n, f, HL, ldhl, const_cast<uint16_t *>(HL16), f, s)
+                        : transpose_bf16_copy(n, f, HL, 0, ldhl, const_cast<uint16_t *>(HL16T), n,
+                                              const_cast<uint16_t *>(HL16), f, s)))
             return rc;
         if ((rc = cvt_bf16_pad(f, C, W_pred, C, Wp16, Cp, Cp, s))) return rc;
         if ((rc = transpose_bf16(f, C, Wp16, 1, Cp, Wp16T, f, s))) return rc;
@@ -898,9 +916,14 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     d.ldc = lddhl;
     if (bf) {
         if ((rc = cvt_bf16_pad(n, C, X, C, G16, Cp, Cp, s))) return rc;
-        if ((rc = transpose_bf16(n, C, G16, 1, Cp, G16T, n, s))) return rc;
-        w.seg[0] = GemmSeg{HL16T, n, G16T, n, n};
-        if ((rc = gemm(L_NT, 1, &w, 1, pl.split, gw, pl.gemm, s))) return rc;
+        if (tn_dw) {
+            w.seg[0] = GemmSeg{HL16, f, G16, Cp, n};
+            if ((rc = gemm(L_TN, 1, &w, 1, pl.split, gw, pl.gemm, s))) return rc;
+        } else {
+            if ((rc = transpose_bf16(n, C, G16, 1, Cp, G16T, n, s))) return rc;
+            w.seg[0] = GemmSeg{HL16T, n, G16T, n, n};
+            if ((rc = gemm(L_NT, 1, &w, 1, pl.split, gw, pl.gemm, s))) return rc;
+        }
         d.seg[0] = GemmSeg{G16, Cp, Wp16, Cp, Cp};   // the zero columns add nothing
         d.k_pad = Cp - C;
     } else {
@@ -1071,7 +1094,7 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
                     lk.out16T = (uint16_t *)((char *)nx.saved + align256((size_t)n * nx.f_in * 2));
             } else if (head) {
                 lk.out16 = HL16;
-                lk.out16T = HL16T;
+                if (!head_dw_rowmajor(n, 2 * a.h, head->C)) lk.out16T = HL16T;   // read by an NT dW_pred only
             }
         }
         if ((rc = layer_fwd(launch, A, H, a.f_in, ldh, a.W_self, a.W_neigh, a.bias, a.h, a.Y, a.ldy, a.saved,

@@ -891,8 +891,10 @@ void gemm_bf16_big_kernel(DevArgs args) {
         chk[q] = ((pos & 3) ^ bigswz(r)) * 8;
         const int kk = pos >> 5, xc = 8 * ((pos & 31) ^ kmswz(pos >> 5));
         kmk[q] = kk;
-        rowA[q] = KMA ? min(m0 + xc, P.M - 8) : min(m0 + r, Mlast);
-        rowB[q] = KMB ? min(n0 + xc, P.N - 8) : min(n0 + r, Nlast);
+        // a k-major side reads whole 8-element chunks up to its size rounded
+        // up to 8 (the host checks the rows hold that many)
+        rowA[q] = KMA ? min(m0 + xc, ((P.M + 7) & ~7) - 8) : min(m0 + r, Mlast);
+        rowB[q] = KMB ? min(n0 + xc, ((P.N + 7) & ~7) - 8) : min(n0 + r, Nlast);
     }
     auto issue = [&](int kt, int stage) {
         const bool s1 = kt >= kt0;
@@ -1214,7 +1216,12 @@ int tile_n_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBN16 : kTBN); }
 
 // The large-tile bf16 kernel takes NT, TN and NN products whose K-segments
 // are multiples of its k-stage, with 16-byte aligned operand rows; a k-major
-// operand (A of TN, B of TN and NN) also needs a multiple of 8 rows.
+// operand (A of TN, B of TN and NN) is read in chunks of 8 along M (or N),
+// so its rows must hold M (N) rounded up to 8 (the extra columns only feed
+// outputs that are dropped).
+#ifndef GCN_BIG_NARROW_K
+#define GCN_BIG_NARROW_K 16384
+#endif
 bool big_ok(int layout, int nprob, const GemmProblem *probs) {
     if (GCN_BF16_BIG == 0) return false;
     const bool kma = layout == L_TN, kmb = layout != L_NT;
@@ -1224,15 +1231,23 @@ bool big_ok(int layout, int nprob, const GemmProblem *probs) {
         // worth it for a side of 64+ when the other one alone gives every CU
         // a tile (the logits of a large subgraph): the product is then bound
         // by its operand and output traffic, not by the idle matrix work.
+        // Also for a long-K product (a weight gradient over the subgraph's
+        // vertices), whose split-K blocks fill the GPU whatever the tiles.
         const int lo = min(probs[i].M, probs[i].N);
         const int64_t tiles = (int64_t)((probs[i].M + kBigT - 1) / kBigT) * ((probs[i].N + kBigT - 1) / kBigT);
-        if (lo <= 128 && !(lo >= 64 && tiles >= GCN_BIG_NARROW_TILES)) return false;
+        const int64_t K = (int64_t)probs[i].seg[0].K + probs[i].seg[1].K;
+        if (lo <= 128 && !(lo >= 64 && (tiles >= GCN_BIG_NARROW_TILES || K >= GCN_BIG_NARROW_K))) return false;
         for (int s = 0; s < 2; ++s) {
             const GemmSeg &sg = probs[i].seg[s];
             if (sg.K == 0) continue;
             if (sg.K % kBigBK || sg.lda % 8 || sg.ldb % 8 || !al(sg.A, 16) || !al(sg.B, 16)) return false;
         }
-        if ((kma && probs[i].M % 8) || (kmb && probs[i].N % 8)) return false;
+        const int64_t M8 = (probs[i].M + 7) & ~7, N8 = (probs[i].N + 7) & ~7;
+        for (int s = 0; s < 2; ++s) {
+            const GemmSeg &sg = probs[i].seg[s];
+            if (sg.K == 0) continue;
+            if ((kma && sg.lda < M8) || (kmb && sg.ldb < N8)) return false;
+        }
     }
     return true;
 }

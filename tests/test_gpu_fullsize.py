@@ -42,8 +42,15 @@ def test_rmat65536_two_layer_bf16_chained_step():
     from test_gpu_layer import compare_bf16_chain
     wl = synth.config(3)
     r = StepRunner(wl, prec=B.GCN_BF16)
+    B.gcn_profile_reset()
+    B.gcn_profile_enable(True)
     r.step()
     torch.cuda.synchronize()
+    B.gcn_profile_enable(False)
+    prof = B.gcn_profile_read_all()
+    # every weight gradient (both layers' and the head's, K = 65,536) reads
+    # its operands as row-major bfloat16 rows on the large-tile kernel
+    assert prof["gemm_tn_bf16_big"][1] == 3 and prof["gemm_nt_bf16"][1] == 0, prof
     errs, _ = compare_bf16_chain(r, wl)
     print("bf16 chain:", errs)
 
