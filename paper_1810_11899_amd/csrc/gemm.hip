@@ -1485,9 +1485,12 @@ int gemm(int layout, int nprob, const GemmProblem *probs, int bf16, int split_k,
             v4 = v4 && q.N % 4 == 0 && (!q.C || (q.ldc % 4 == 0 && al(q.C, 16)));
         }
         const int64_t vecs = v4 ? maxe / 4 : maxe;
-        // threads per output vector: up to 8, for about 2^18 threads in all
+        // threads per output element: up to 8, for about 2^20 elements-threads
+        // per pair of problems.  It depends on a problem's own size and split
+        // only (not on how many problems share the launch, nor on the vector
+        // width), so a product reduces to the same bits alone or grouped.
         int G = 1;
-        while (G < 8 && 2 * G <= maxsplit && vecs * nprob * G < (1 << 18)) G *= 2;
+        while (G < 8 && 2 * G <= maxsplit && maxe * 2 * G < (1 << 20)) G *= 2;
         int64_t g = (vecs + 256 / G - 1) / (256 / G);
         if (g > 4096) g = 4096;
         if (g < 1) g = 1;

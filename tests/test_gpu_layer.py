@@ -306,7 +306,8 @@ def test_forced_orders_agree_with_oracle(order):
 
 
 @pytest.mark.parametrize("case", ["cfg1-f32", "cfg1-bf16", "cfg2-bf16", "dY-f32", "bce-transform-first",
-                                  "f32-odd-widths", "bf16-odd-widths", "bf16-odd-wide", "bf16-row-major-dw"])
+                                  "f32-odd-widths", "bf16-odd-widths", "bf16-odd-wide", "bf16-row-major-dw",
+                                  "cfg3-f32", "cfg3-bf16"])
 def test_model_step_matches_separate_calls(case):
     """gcn_model_step computes what the separate calls compute: every output
     bit for bit, except that a layer whose dZ arrives from the head or from an
@@ -316,7 +317,8 @@ def test_model_step_matches_separate_calls(case):
     packed bfloat16 rows with bfloat16 operands), or that gradient itself."""
     if case.startswith("cfg"):
         wl = synth.config(int(case[3]))
-        r = StepRunner(wl, prec=B.GCN_BF16 if case.endswith("bf16") else B.GCN_F32)
+        orders = [B.GCN_AGGREGATE_FIRST, B.GCN_TRANSFORM_FIRST] if case[3] == "3" else None   # the bench's
+        r = StepRunner(wl, prec=B.GCN_BF16 if case.endswith("bf16") else B.GCN_F32, orders=orders)
     elif case == "dY-f32":
         wl = synth.custom(2500, "rmat", 10, [(64, 32), (64, 48)], head=None, seed=4)
         r = StepRunner(wl, first_layer_dH=True)
