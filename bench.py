@@ -509,6 +509,7 @@ def bench_train(args, B, torch):
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     verts = edges = 0
     host = 0.0
+    wait0 = tr.wait_s
     t0 = time.perf_counter()
     a.record(stream)
     for _ in range(args.train_iters):
@@ -558,8 +559,12 @@ def bench_train(args, B, torch):
         "edge_features_per_s": round(edges * ef / wall, 1),
         "compute_stream_ms_per_iteration": round(a.elapsed_time(b) / K, 4),
         # host time spent issuing one iteration (library calls return once
-        # their kernels are queued): near ms_per_step means the host paces the GPU
-        "host_issue_ms_per_iteration": round(host * 1e3 / K, 4),
+        # their kernels are queued), without the waits for pool refills: the
+        # host runs ahead of the GPU until the next pool is not ready yet, so
+        # those waits are the GPU's backpressure.  Near ms_per_step would mean
+        # the host paces the GPU.
+        "host_issue_ms_per_iteration": round((host - (tr.wait_s - wait0)) * 1e3 / K, 4),
+        "host_wait_for_pools_ms_per_iteration": round((tr.wait_s - wait0) * 1e3 / K, 4),
         "phases_ms_per_iteration": phases, "kernels": kernels,
         "loss_first_last": [float(losses[0]), float(losses[-1])],
     }

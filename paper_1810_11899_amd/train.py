@@ -19,6 +19,8 @@ host, which the layer calls take as sizes.
 """
 from __future__ import annotations
 
+import time
+
 from dataclasses import dataclass
 from typing import List, Optional, Tuple
 
@@ -179,6 +181,7 @@ class Trainer:
                       for _ in range(2)]
         self.cur = 0
         self.next_id = 0
+        self.wait_s = 0.0     # host time spent waiting for pool refills
         # iteration buffers, sized for the largest subgraph (n vertices)
         self.ws = B.Workspace(d)
         self.H0 = torch.empty((n, f0p), dtype=torch.float32, device=d)
@@ -236,8 +239,12 @@ class Trainer:
         p.next = -1   # filled, metadata not read yet
 
     def _open(self, p: _Pool):
-        """Wait for a refill and read its metadata on the host."""
+        """Wait for a refill and read its metadata on the host (the time the
+        host spends waiting is added to `wait_s`: with the host ahead of the
+        GPU, that is the GPU's backpressure, not issue work)."""
+        t0 = time.perf_counter()
         p.ready.synchronize()
+        self.wait_s += time.perf_counter() - t0
         if int(p.h_istatus[0]) != 0:       # edge arrays too small: grow and induce again
             need = int(p.h_off[-1])
             s = self.side
@@ -247,7 +254,9 @@ class Trainer:
                 p.h_nsub.copy_(p.batch.n_sub, non_blocking=True)
                 p.h_off.copy_(p.batch.edge_offsets, non_blocking=True)
                 p.ready.record(s)
+            t0 = time.perf_counter()
             p.ready.synchronize()
+            self.wait_s += time.perf_counter() - t0
         bad = [B.SAMPLE_STATUS[int(x)] for x in p.h_status.numpy() if int(x) not in (0, 1)]
         if bad:
             raise RuntimeError(f"sampler runs failed: {sorted(set(bad))}")
