@@ -664,7 +664,12 @@ def main():
         bench_train(args, B, torch)
         return
     wl = synth.config(args.config, self_loops=args.self_loops)
-    out = bench_step(args, args.prec, wl, B, torch, synth, index_bits=args.index_bits)
+    # a bfloat16 step keeps its activations as bfloat16 end to end (the
+    # configuration of the bfloat16 variant below), where the library allows
+    # it (an output gradient that arrives unmasked needs the float32 Y)
+    fo = args.prec == "f32" or args.config != 3
+    out = bench_step(args, args.prec, wl, B, torch, synth, index_bits=args.index_bits, float_outputs=fo)
+    out["float_outputs"] = fo
     variants = {}
     if args.config == 3 and args.prec == "f32" and args.index_bits == 32 and not args.no_variants:
         # the bfloat16-operand variant of the same workload, and the float32
