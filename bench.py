@@ -177,7 +177,8 @@ def measure_gather(B, torch, wl) -> dict:
                            that size (64 MiB fits the 256 MB Infinity Cache;
                            4 GiB does not, so most rows come from HBM)
       csr_fp32_rows        the workload's CSR column indices in order, rows of
-                           the float32 features (k = the first layer's width)
+                           the float32 features (k = the first layer's width,
+                           rounded up to a row size the probe takes)
       csr_bf16_rows        the same with bfloat16 rows (half the bytes)
     A 16 KiB array stays in every CU's L1, so its rate is the CU's
     vector-memory path with every row a hit: no gather of that row size with
@@ -219,10 +220,18 @@ def measure_gather(B, torch, wl) -> dict:
             del X, idx
     k = wl.layers[0].f_in
     idx = torch.from_numpy(wl.graph.indices).cuda()
-    X = torch.ones((wl.n, k), dtype=torch.float32, device="cuda")
-    out["csr_order_fp32_rows"] = best(X, 4 * k, idx)
-    X16 = torch.ones((wl.n, k), dtype=torch.bfloat16, device="cuda")
-    out["csr_order_bf16_rows"] = best(X16, 2 * k, idx)
+
+    def probe_row(nbytes):   # the probe's row sizes: 16 B times a power of two up to 1 KB, 2 KB, 4 KB
+        r = 16
+        while r < nbytes and r < 4096:
+            r *= 2
+        return r
+    rb = probe_row(4 * k)
+    X = torch.ones((wl.n, rb // 4), dtype=torch.float32, device="cuda")
+    out["csr_order_fp32_rows"] = best(X, rb, idx)
+    rb = probe_row(2 * k)
+    X16 = torch.ones((wl.n, rb // 2), dtype=torch.bfloat16, device="cuda")
+    out["csr_order_bf16_rows"] = best(X16, rb, idx)
     del X, X16
     return out
 
