@@ -311,7 +311,11 @@ int gcn_f32_to_bf16(const float *x, uint16_t *y, int64_t count, void *stream);
  * launches is bracketed by two hipEvents recorded on the launch stream; the
  * events are read (after the caller has synchronised) by gcn_profile_read,
  * which accumulates per kernel class.  Classes are numbered 0..count-1 with
- * stable names.  Disabled by default; costs two event records per launch. */
+ * stable names.  Disabled by default; costs two event records per launch.
+ * The switch and the accumulated times are process-wide host state (guarded
+ * by a lock): while profiling is on, the launches of every thread are
+ * counted together, so profile one workload at a time.  This is the one
+ * exception to the reentrancy above on the host side. */
 int gcn_profile_enable(int on);
 int gcn_profile_reset(void);
 int gcn_profile_class_count(void);
