@@ -778,7 +778,11 @@ bool al(const void *p, int b) { return ((uintptr_t)p % (uintptr_t)b) == 0; }
 // swizzled place.  Requires every K-segment to be a multiple of 32 and
 // 16-byte aligned rows; rows past M or N are clamped to the last row and
 // their results dropped.
-constexpr int kBigT = 256;       // block tile, M and N
+#ifndef GCN_BIG_TN
+#define GCN_BIG_TN 256
+#endif
+constexpr int kBigT = 256;       // block tile along M
+constexpr int kBigTN = GCN_BIG_TN;   // block tile along N: 256, or 128 with 4 wavefronts (two blocks per CU)
 constexpr int kBigBK = 32;       // k per stage
 #ifndef GCN_BIG_STAGES
 #define GCN_BIG_STAGES 4
@@ -803,9 +807,14 @@ constexpr int kBigWaves = GCN_BIG_WAVES;
                  // 4 (2 x 2) or 8 (2 x 4)
 constexpr int kBigThreads = 64 * kBigWaves;
 constexpr int kBigWN = kBigWaves / 2;                     // wavefronts along N
-constexpr int kBigWTM = 128, kBigWTN = kBigT / kBigWN;   // wavefront tile
+constexpr int kBigWTM = 128, kBigWTN = kBigTN / kBigWN;   // wavefront tile
 constexpr int kBigFM = kBigWTM / 32, kBigFN = kBigWTN / 32;
-constexpr int kBigQ = 16 / kBigWaves;                     // 1 KB loads per operand per wavefront
+// 1 KB (16 bytes per lane) loads per wavefront per stage, for A and for B
+constexpr int kBigQA = kBigT * kBigBK / 8 / (64 * kBigWaves);
+constexpr int kBigQB = kBigTN * kBigBK / 8 / (64 * kBigWaves);
+static_assert(kBigQA * 64 * kBigWaves * 8 == kBigT * kBigBK && kBigQB * 64 * kBigWaves * 8 == kBigTN * kBigBK,
+              "whole 16-byte chunks per lane");
+constexpr int kBigStageA = kBigT * kBigBK, kBigStageB = kBigTN * kBigBK;   // elements per stage
 __device__ __forceinline__ int bigswz(int r) { return (r >> 2) & 3; }
 
 template <int N>
@@ -855,15 +864,15 @@ enum BigOut {
 // LAYOUT: L_NT (both operands contiguous along k), L_TN (both k-major) or
 // L_NN (A contiguous along k, B k-major).
 template <int OUT, int LAYOUT>
-__global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(kBigWaves / 4)))
+__global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void gemm_bf16_big_kernel(DevArgs args) {
     constexpr bool KMA = LAYOUT == L_TN, KMB = LAYOUT != L_NT;
-    __shared__ __attribute__((aligned(16))) uint16_t lds[kBigStages][2][kBigT * kBigBK];
+    __shared__ __attribute__((aligned(16))) uint16_t lds[kBigStages][kBigStageA + kBigStageB];
 
     BlockCoord bc;
     if (!decode_block(args, bc)) return;
     const DevProblem &P = args.p[bc.pi];
-    const int m0 = bc.tm * kBigT, n0 = bc.tn * kBigT;
+    const int m0 = bc.tm * kBigT, n0 = bc.tn * kBigTN;
     const int kt_begin = bc.split * P.kt_per_split;
     const int kt_end = min(kt_begin + P.kt_per_split, P.kt_total);
     const int ntiles = kt_end - kt_begin;
@@ -883,17 +892,27 @@ void gemm_bf16_big_kernel(DevArgs args) {
     // A k-major operand: k-row pos/32, stored chunk pos%32, which holds the
     // tile's chunk (pos%32) ^ kmswz(k-row), at row index x0 + 8 * chunk
     // (clamped to the last whole chunk, rows are a multiple of 8).
-    int rowA[kBigQ], rowB[kBigQ], chk[kBigQ], kmk[kBigQ];
+    // (B's k-rows hold kBigTN / 8 chunks)
+    int rowA[kBigQA], rowB[kBigQB], chkA[kBigQA], chkB[kBigQB], kmA[kBigQA], kmB[kBigQB];
 #pragma unroll
-    for (int q = 0; q < kBigQ; ++q) {
-        const int pos = (wave * kBigQ + q) * 64 + lane;
+    for (int q = 0; q < kBigQA; ++q) {
+        const int pos = (wave * kBigQA + q) * 64 + lane;
         const int r = pos >> 2;
-        chk[q] = ((pos & 3) ^ bigswz(r)) * 8;
-        const int kk = pos >> 5, xc = 8 * ((pos & 31) ^ kmswz(pos >> 5));
-        kmk[q] = kk;
+        chkA[q] = ((pos & 3) ^ bigswz(r)) * 8;
+        const int kk = pos >> 5, xc = 8 * ((pos & 31) ^ kmswz(kk));
+        kmA[q] = kk;
         // a k-major side reads whole 8-element chunks up to its size rounded
         // up to 8 (the host checks the rows hold that many)
         rowA[q] = KMA ? min(m0 + xc, ((P.M + 7) & ~7) - 8) : min(m0 + r, Mlast);
+    }
+#pragma unroll
+    for (int q = 0; q < kBigQB; ++q) {
+        constexpr int CPR = kBigTN / 8;   // chunks per k-row of a k-major B
+        const int pos = (wave * kBigQB + q) * 64 + lane;
+        const int r = pos >> 2;
+        chkB[q] = ((pos & 3) ^ bigswz(r)) * 8;
+        const int kk = pos / CPR, xc = 8 * ((pos % CPR) ^ kmswz(kk));
+        kmB[q] = kk;
         rowB[q] = KMB ? min(n0 + xc, ((P.N + 7) & ~7) - 8) : min(n0 + r, Nlast);
     }
     auto issue = [&](int kt, int stage) {
@@ -903,17 +922,17 @@ void gemm_bf16_big_kernel(DevArgs args) {
         const int64_t lda = s1 ? lda1 : lda0, ldb = s1 ? ldb1 : ldb0;
         const int k0 = (s1 ? kt - kt0 : kt) * kBigBK;
 #pragma unroll
-        for (int q = 0; q < kBigQ; ++q) {
-            const uint16_t *g = KMA ? A + (int64_t)(k0 + kmk[q]) * lda + rowA[q] : A + (int64_t)rowA[q] * lda + k0 + chk[q];
+        for (int q = 0; q < kBigQA; ++q) {
+            const uint16_t *g = KMA ? A + (int64_t)(k0 + kmA[q]) * lda + rowA[q] : A + (int64_t)rowA[q] * lda + k0 + chkA[q];
             __builtin_amdgcn_global_load_lds((const void *)g,
-                                             (void __attribute__((address_space(3))) *)&lds[stage][0][(wave * kBigQ + q) * 512],
+                                             (void __attribute__((address_space(3))) *)&lds[stage][(wave * kBigQA + q) * 512],
                                              16, 0, 0);
         }
 #pragma unroll
-        for (int q = 0; q < kBigQ; ++q) {
-            const uint16_t *g = KMB ? Bm + (int64_t)(k0 + kmk[q]) * ldb + rowB[q] : Bm + (int64_t)rowB[q] * ldb + k0 + chk[q];
+        for (int q = 0; q < kBigQB; ++q) {
+            const uint16_t *g = KMB ? Bm + (int64_t)(k0 + kmB[q]) * ldb + rowB[q] : Bm + (int64_t)rowB[q] * ldb + k0 + chkB[q];
             __builtin_amdgcn_global_load_lds((const void *)g,
-                                             (void __attribute__((address_space(3))) *)&lds[stage][1][(wave * kBigQ + q) * 512],
+                                             (void __attribute__((address_space(3))) *)&lds[stage][kBigStageA + (wave * kBigQB + q) * 512],
                                              16, 0, 0);
         }
     };
@@ -932,7 +951,7 @@ void gemm_bf16_big_kernel(DevArgs args) {
     for (int st = 0; st < kBigStages - 1; ++st)
         if (st < ntiles) issue_tile(st);
 
-    constexpr int G = 2 * kBigQ;   // loads per tile per wavefront
+    constexpr int G = kBigQA + kBigQB;   // loads per tile per wavefront
     // Software pipeline over the two 16-k steps of a stage.  The operand
     // fragments of one k-step are read from LDS while the products of the
     // other run (the reads are interleaved with the matrix instructions), so
@@ -952,21 +971,21 @@ void gemm_bf16_big_kernel(DevArgs args) {
     bf16x8 fa[2][kBigFM], fb[2][kBigFN];
     // a k-major fragment: the two transposing reads of k-rows kb .. kb+3 and
     // kb+4 .. kb+7 (kb = 16 ks + 8 (lane / 32)) for the 32 row indices x0 ..
-    auto km_frag = [&](const uint16_t *T, int ks, int x0) {
+    auto km_frag = [&](const uint16_t *T, int RS, int ks, int x0) {   // RS: elements per k-row
         const int kk = 16 * ks + 8 * (lane >> 5) + ((lane & 15) >> 2);
         const int x = x0 + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-        const int off0 = kk * kBigT + ((x >> 3) ^ kmswz(kk)) * 8 + (x & 7);
-        const int off1 = (kk + 4) * kBigT + ((x >> 3) ^ kmswz(kk + 4)) * 8 + (x & 7);
+        const int off0 = kk * RS + ((x >> 3) ^ kmswz(kk)) * 8 + (x & 7);
+        const int off1 = (kk + 4) * RS + ((x >> 3) ^ kmswz(kk + 4)) * 8 + (x & 7);
         return tr_frag(T, off0, off1);
     };
     auto read_frags = [&](int stage, int ks, bf16x8 (&a)[kBigFM], bf16x8 (&b)[kBigFN]) {
-        const uint16_t *As = lds[stage][0];
-        const uint16_t *Bs = lds[stage][1];
+        const uint16_t *As = lds[stage];
+        const uint16_t *Bs = lds[stage] + kBigStageA;
         const int c = 2 * ks + (lane >> 5);
 #pragma unroll
         for (int i = 0; i < kBigFM; ++i) {
             if constexpr (KMA) {
-                a[i] = km_frag(As, ks, wm * kBigWTM + i * 32);
+                a[i] = km_frag(As, kBigT, ks, wm * kBigWTM + i * 32);
             } else {
                 const int r = wm * kBigWTM + i * 32 + (lane & 31);
                 a[i] = *(const bf16x8 *)&As[(r * 4 + (c ^ bigswz(r))) * 8];
@@ -975,7 +994,7 @@ void gemm_bf16_big_kernel(DevArgs args) {
 #pragma unroll
         for (int j = 0; j < kBigFN; ++j) {
             if constexpr (KMB) {
-                b[j] = km_frag(Bs, ks, wn * kBigWTN + j * 32);
+                b[j] = km_frag(Bs, kBigTN, ks, wn * kBigWTN + j * 32);
             } else {
                 const int r = wn * kBigWTN + j * 32 + (lane & 31);
                 b[j] = *(const bf16x8 *)&Bs[(r * 4 + (c ^ bigswz(r))) * 8];
@@ -1061,22 +1080,26 @@ void gemm_bf16_big_kernel(DevArgs args) {
     // idle) operand ring, then every wavefront writes whole 256-column rows,
     // 16 bytes per lane.  Accumulator blocks are moved by calls with constant
     // indices, so that they stay in registers.
-    static_assert(kBigStages >= 4, "the epilogue stages 128 x 256 floats in the operand ring");
+    static_assert(128 * kBigTN * sizeof(float) <= sizeof(lds), "the epilogue stages 128 rows of floats in the ring");
     static_assert(kBigFM == 4 && (kBigFN == 4 || kBigFN == 2), "epilogue unrolled for 4 x 4 or 4 x 2 blocks");
-    float *stg = (float *)&lds[0][0][0];
+    float *stg = (float *)&lds[0][0];
     auto put = [&](const floatx16 &v, int i, int j) {
         const int lc = wn * kBigWTN + j * 32 + (lane & 31);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int lr = i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            stg[lr * kBigT + lc] = v[r];
+            stg[lr * kBigTN + lc] = v[r];
         }
     };
+    // a row of the tile is kColLanes lanes x 4 columns; a wavefront writes
+    // kRowsPerInstr rows per instruction
+    constexpr int kColLanes = kBigTN / 4, kRowsPerInstr = 64 / kColLanes;
+    const int sub = lane / kColLanes;
     const bool c16 = OUT != BIG_F32 && !to_partial && P.C16 != nullptr;
     const bool c32 = OUT != BIG_B16 && (to_partial || P.C != nullptr);
     const bool vec16 = c16 && P.ldc16 % 4 == 0 && ((uintptr_t)P.C16 & 7) == 0;
     const bool vec32 = c32 && ldd % 4 == 0 && ((uintptr_t)dst & 15) == 0;
-    const int col = n0 + 4 * lane;
+    const int col = n0 + 4 * (lane % kColLanes);
     float bv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if (!to_partial && P.bias)
 #pragma unroll
@@ -1091,14 +1114,14 @@ void gemm_bf16_big_kernel(DevArgs args) {
     // the mask of a pass's rows is loaded in batches of kMaskBatch rows: the
     // first batch before that pass's deposit and barrier (its latency
     // overlaps them), each later one as the previous batch is used up
-    constexpr int kRowsPerWave = 128 / kBigWaves;
+    constexpr int kRowsPerWave = 128 / (kBigWaves * kRowsPerInstr);   // instructions per 128-row pass
     constexpr int kMaskBatch = GCN_BIG_MASK_PREFETCH;
     static_assert(kRowsPerWave % kMaskBatch == 0, "whole mask batches");
     uint2 mk[kMaskBatch];   // 4 bfloat16 mask values per row
     auto load_mask = [&](int h, int k0) {
 #pragma unroll
         for (int k = 0; k < kMaskBatch; ++k) {
-            const int row = m0 + h * 128 + wave + (k0 + k) * kBigWaves;
+            const int row = m0 + h * 128 + ((k0 + k) * kBigWaves + wave) * kRowsPerInstr + sub;
             mk[k] = make_uint2(0u, 0u);
             if (row <= Mlast && col <= Nlast) {
                 const uint16_t *mp = emask + (int64_t)row * P.ldm + col;
@@ -1133,10 +1156,10 @@ void gemm_bf16_big_kernel(DevArgs args) {
 #pragma unroll
         for (int k = 0; k < kRowsPerWave; ++k) {
             if (emask && k > 0 && k % kMaskBatch == 0) load_mask(h, k);
-            const int rr = wave + k * kBigWaves;
+            const int rr = (k * kBigWaves + wave) * kRowsPerInstr + sub;
             const int row = m0 + h * 128 + rr;
             if (row > Mlast || col > Nlast) continue;
-            const float4 q = *(const float4 *)&stg[rr * kBigT + 4 * lane];
+            const float4 q = *(const float4 *)&stg[rr * kBigTN + 4 * (lane % kColLanes)];
             float o[4] = {q.x + bv[0], q.y + bv[1], q.z + bv[2], q.w + bv[3]};
             if (relu)
 #pragma unroll
@@ -1178,19 +1201,29 @@ void gemm_bf16_big_kernel(DevArgs args) {
     if (ecs) {
         // per half: the 8 wavefronts' sums of each column, in order; the
         // half's rows are column-sum row 2 * tm + h (128-row tiles)
-        static_assert(16 * kBigT * sizeof(float) <= sizeof(lds), "column sums fit the ring");
-        static_assert((2 * kBigT) % kBigThreads == 0, "whole (half, column) sweeps");
+        static_assert(2 * kBigWaves * kBigTN * sizeof(float) <= sizeof(lds), "column sums fit the ring");
+        static_assert((2 * kBigTN) % kBigThreads == 0, "whole (half, column) sweeps");
+        // the rows a wavefront's two lane halves summed (when a row is half a
+        // wavefront wide), added in a fixed way
+        if constexpr (kRowsPerInstr == 2) {
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+            for (int h = 0; h < 2; ++h)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) stg[(h * kBigWaves + wave) * kBigT + 4 * lane + e] = cs[h][e];
+                for (int e = 0; e < 4; ++e) cs[h][e] += __shfl_xor(cs[h][e], 32);
+        }
+        static_assert(kRowsPerInstr == 1 || kRowsPerInstr == 2, "one or two rows per instruction");
+        if (sub == 0)
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) stg[(h * kBigWaves + wave) * kBigTN + 4 * lane + e] = cs[h][e];
         __syncthreads();
 #pragma unroll
-        for (int idx = (int)threadIdx.x; idx < 2 * kBigT; idx += kBigThreads) {
-            const int h = idx / kBigT, c = idx % kBigT;
+        for (int idx = (int)threadIdx.x; idx < 2 * kBigTN; idx += kBigThreads) {
+            const int h = idx / kBigTN, c = idx % kBigTN;
             float t = 0.0f;
 #pragma unroll
-            for (int w = 0; w < kBigWaves; ++w) t += stg[(h * kBigWaves + w) * kBigT + c];
+            for (int w = 0; w < kBigWaves; ++w) t += stg[(h * kBigWaves + w) * kBigTN + c];
             if (m0 + h * 128 <= Mlast && n0 + c <= Nlast) P.colpart[(int64_t)(2 * bc.tm + h) * P.N + n0 + c] = t;
         }
     }
@@ -1212,7 +1245,7 @@ bool vec_ok(int layout, const GemmProblem &g, int esz) {
 // mode 0: float32 kernel; 1: bf16 kernel; 2: bf16 large-tile kernel
 int bk_of(int mode) { return mode == 2 ? kBigBK : (mode ? BK16 : kBK); }
 int tile_m_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBM16 : kTBM); }
-int tile_n_of(int mode) { return mode == 2 ? kBigT : (mode ? kTBN16 : kTBN); }
+int tile_n_of(int mode) { return mode == 2 ? kBigTN : (mode ? kTBN16 : kTBN); }
 
 // The large-tile bf16 kernel takes NT, TN and NN products whose K-segments
 // are multiples of its k-stage, with 16-byte aligned operand rows; a k-major
@@ -1234,7 +1267,7 @@ bool big_ok(int layout, int nprob, const GemmProblem *probs) {
         // Also for a long-K product (a weight gradient over the subgraph's
         // vertices), whose split-K blocks fill the GPU whatever the tiles.
         const int lo = min(probs[i].M, probs[i].N);
-        const int64_t tiles = (int64_t)((probs[i].M + kBigT - 1) / kBigT) * ((probs[i].N + kBigT - 1) / kBigT);
+        const int64_t tiles = (int64_t)((probs[i].M + kBigT - 1) / kBigT) * ((probs[i].N + kBigTN - 1) / kBigTN);
         const int64_t K = (int64_t)probs[i].seg[0].K + probs[i].seg[1].K;
         if (lo <= 128 && !(lo >= 64 && (tiles >= GCN_BIG_NARROW_TILES || K >= GCN_BIG_NARROW_K))) return false;
         for (int s = 0; s < 2; ++s) {
