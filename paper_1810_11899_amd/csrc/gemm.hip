@@ -29,6 +29,13 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 constexpr int BM = 128;
 constexpr int BN = 128;
 constexpr int PAD = 4;
+#ifndef GCN_GEMM_XK
+#define GCN_GEMM_XK 1
+#endif
+#ifndef GCN_GEMM_XK_NN
+#define GCN_GEMM_XK_NN 0
+#endif
+constexpr int PAD_XK = 4;   // [x][k] tiles: rows of BK + 4 floats (conflict-free 16-byte reads and stores)
 constexpr int kThreads = 256;
 
 struct Segs {
@@ -189,6 +196,19 @@ struct TileLoader {
         for (int i = 0; i < kPer; ++i) reg[i] = *(const V *)(ptr + off[i] + kofs);
     }
 
+    // [x][k] layout (k contiguous, rows of BK + PAD_XK): an operand contiguous
+    // along k goes in as its loaded 16-byte vectors
+    template <int RS>
+    __device__ __forceinline__ void store_xk(T (*lds)[RS]) const {
+        static_assert(!KMAJOR, "the [x][k] layout takes operands contiguous along k");
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            int x, k;
+            coords(i, x, k);
+            *(V *)&lds[x][k] = reg[i];
+        }
+    }
+
     __device__ __forceinline__ void store(T (*lds)[XT + PAD]) const {
 #pragma unroll
         for (int i = 0; i < kPer; ++i) {
@@ -243,10 +263,22 @@ void gemm_kernel(DevArgs args) {
     constexpr bool B_KMAJOR = (LAYOUT != L_NT);
     constexpr int WTM = TBM / 2, WTN = TBN / 2;     // wavefront tile (2 x 2 wavefronts)
     constexpr int FM = WTM / 32, FN = WTN / 32;     // 32x32 accumulator blocks per wavefront
+    // An operand contiguous along k (A in NN and NT, B in NT) is kept [x][k]
+    // in LDS and read 4 consecutive k per lane: one ds_read_b128 feeds four
+    // products.  A k-major operand keeps the [k][x] layout (one 4-byte read
+    // per product), read in the same k order.
+    constexpr bool XKA = GCN_GEMM_XK && !A_KMAJOR && (LAYOUT == L_NT || GCN_GEMM_XK_NN);
+    constexpr bool XKB = GCN_GEMM_XK && !B_KMAJOR;
+    constexpr bool XK = XKA || XKB;
+    constexpr int RS = BK + PAD_XK;                 // [x][k] row stride
+    constexpr int kSmemA = XKA ? 2 * TBM * RS : 2 * BK * (TBM + PAD);
+    constexpr int kSmemB = XKB ? 2 * TBN * RS : 2 * BK * (TBN + PAD);
     // one LDS block: the two operand double buffers, reused by the epilogue
-    __shared__ __attribute__((aligned(16))) T smem[2 * BK * (TBM + PAD) + 2 * BK * (TBN + PAD)];
+    __shared__ __attribute__((aligned(16))) T smem[kSmemA + kSmemB];
     T(*As)[BK][TBM + PAD] = (T(*)[BK][TBM + PAD])smem;
-    T(*Bs)[BK][TBN + PAD] = (T(*)[BK][TBN + PAD])(smem + 2 * BK * (TBM + PAD));
+    T(*Bs)[BK][TBN + PAD] = (T(*)[BK][TBN + PAD])(smem + kSmemA);
+    T(*Ax)[TBM][RS] = (T(*)[TBM][RS])smem;
+    T(*Bx)[TBN][RS] = (T(*)[TBN][RS])(smem + kSmemA);
 
     // ---- which problem / split / tile
     BlockCoord bc;
@@ -307,6 +339,57 @@ void gemm_kernel(DevArgs args) {
     int buf = 0;
     const int kh = lane >> 5;
     for (int kt = kt_begin; kt < kt_end; ++kt) {
+      if constexpr (XK) {
+        if constexpr (XKA) la.template store_xk<RS>(Ax[buf]);
+        else la.store(As[buf]);
+        if constexpr (XKB) lb.template store_xk<RS>(Bx[buf]);
+        else lb.store(Bs[buf]);
+        if (kt + 1 < kt_end) load(kt + 1);
+        __syncthreads();
+        // k order shared by both operands: in group g of 8 k, lanes 0-31 take
+        // k = 8g + u and lanes 32-63 k = 8g + 4 + u for the u-th product
+        float4 a4[FM], b4[FN];
+        auto rd4 = [&](float4 *a, float4 *b, int g) {
+            const int kc = 8 * g + 4 * (lane >> 5);
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int x = wm * WTM + i * 32 + (lane & 31);
+                if constexpr (XKA) a[i] = *(const float4 *)&Ax[buf][x][kc];
+                else
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) a[i][u] = As[buf][kc + u][x ^ kswz(kc + u)];
+            }
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int x = wn * WTN + j * 32 + (lane & 31);
+                if constexpr (XKB) b[j] = *(const float4 *)&Bx[buf][x][kc];
+                else
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) b[j][u] = Bs[buf][kc + u][x ^ kswz(kc + u)];
+            }
+        };
+        auto mma4 = [&](const float4 *a, const float4 *b) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][u], b[j][u], acc[i][j], 0, 0, 0);
+        };
+        static_assert(BK % 8 == 0, "whole groups of 8 k");
+        // one group's fragments in flight (the other wavefronts on the SIMD
+        // cover the read latency): 16 registers instead of 32
+#pragma unroll
+        for (int g = 0; g < BK / 8; ++g) {
+            rd4(a4, b4, g);
+            GCN_PRIO_UP();
+            mma4(a4, b4);
+            GCN_PRIO_DOWN();
+        }
+        buf ^= 1;
+        continue;
+      }
         la.store(As[buf]);
         lb.store(Bs[buf]);
         // the staging registers are free once stored: the next tile's loads
@@ -360,7 +443,7 @@ void gemm_kernel(DevArgs args) {
     // then all four wavefronts write whole 128-column rows, 16 bytes per lane.
     static_assert(FM == 2 && FN == 2 && TBN == 128, "epilogue written for 2 x 2 blocks of a 128-wide tile");
     constexpr int SLD = 136;
-    static_assert(32 * SLD <= 2 * BK * (TBM + PAD) + 2 * BK * (TBN + PAD), "staging fits the operand buffers");
+    static_assert(32 * SLD <= kSmemA + kSmemB, "staging fits the operand buffers");
     float *stg = smem;
     const int ecol = n0 + 4 * (lane & 31);
     float ebv[4] = {0.0f, 0.0f, 0.0f, 0.0f};
