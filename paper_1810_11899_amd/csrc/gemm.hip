@@ -636,10 +636,28 @@ struct TileLoader16 {
     }
 };
 
+// float32 -> bfloat16, round to nearest even (NaN kept NaN, quiet)
 __device__ __forceinline__ uint16_t to_bf16(float f) {
     const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x0040u);
-    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+    const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    return (uint16_t)((u & 0x7FFFFFFFu) > 0x7F800000u ? ((u >> 16) | 0x0040u) : r);
+}
+
+#ifndef GCN_HW_BF16
+#define GCN_HW_BF16 1
+#endif
+typedef float gcn_float2 __attribute__((ext_vector_type(2)));
+typedef __bf16 gcn_bf16x2 __attribute__((ext_vector_type(2)));
+// two values rounded as to_bf16 does, packed (a in the low half).  gfx950
+// converts a pair in one instruction (v_cvt_pk_bf16_f32, round to nearest
+// even); it gives to_bf16's bits for every non-NaN float32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+#if GCN_HW_BF16
+    const gcn_float2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, gcn_bf16x2));
+#else
+    return (uint32_t)to_bf16(a) | ((uint32_t)to_bf16(b) << 16);
+#endif
 }
 
 // a bfloat16 value (raw bits) compares > 0 exactly when its float32 widening does
@@ -1236,47 +1254,71 @@ void gemm_bf16_big_kernel(DevArgs args) {
             }
         }
         __syncthreads();
+        // rows rr = (k * kBigWaves + wave) * kRowsPerInstr + sub of the pass;
+        // their LDS reads go out kRB at a time, ahead of the stores, and the
+        // output offsets advance by a fixed row step
+        constexpr int kRowStep = kBigWaves * kRowsPerInstr;
+        constexpr int kRB = 4;
+        static_assert(kRowsPerWave % kRB == 0 && kMaskBatch % kRB == 0, "whole row batches");
+        const int rr0 = wave * kRowsPerInstr + sub;
+        const int row0 = m0 + h * 128 + rr0;
+        const float *const srow = stg + rr0 * kBigTN + 4 * (lane % kColLanes);
+        const bool colok = col <= Nlast;
+        // whole 4-column groups on the vector paths (uniform over the launch)
+        const bool v16 = vec16 && P.N % 4 == 0, v32 = vec32 && P.N % 4 == 0;
+        // output row addresses, advanced by one row step per row
+        uint16_t *p16 = c16 ? P.C16 + (int64_t)row0 * P.ldc16 + col : nullptr;
+        float *p32 = c32 ? dst + (int64_t)row0 * ldd + col : nullptr;
+        const int64_t s16 = (int64_t)kRowStep * P.ldc16, s32 = (int64_t)kRowStep * ldd;
 #pragma unroll
-        for (int k = 0; k < kRowsPerWave; ++k) {
-            if (emask && k > 0 && k % kMaskBatch == 0) load_mask(h, k);
-            const int rr = (k * kBigWaves + wave) * kRowsPerInstr + sub;
-            const int row = m0 + h * 128 + rr;
-            if (row > Mlast || col > Nlast) continue;
-            const float4 q = *(const float4 *)&stg[rr * kBigTN + 4 * (lane % kColLanes)];
-            float o[4] = {q.x + bv[0], q.y + bv[1], q.z + bv[2], q.w + bv[3]};
-            if (relu)
+        for (int k0 = 0; k0 < kRowsPerWave; k0 += kRB) {
+            if (emask && k0 > 0 && k0 % kMaskBatch == 0) load_mask(h, k0);
+            float4 qb[kRB];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
-            if (emask) {
-                const uint2 m = mk[k % kMaskBatch];
-                o[0] = bf16_bits_positive(m.x & 0xFFFFu) ? o[0] : 0.0f;
-                o[1] = bf16_bits_positive(m.x >> 16) ? o[1] : 0.0f;
-                o[2] = bf16_bits_positive(m.y & 0xFFFFu) ? o[2] : 0.0f;
-                o[3] = bf16_bits_positive(m.y >> 16) ? o[3] : 0.0f;
-            }
-            if (ecs)
+            for (int u = 0; u < kRB; ++u) qb[u] = *(const float4 *)(srow + (k0 + u) * kRowStep * kBigTN);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) cs[h][e] += o[e];
-            if (c16) {
-                uint16_t *d = P.C16 + (int64_t)row * P.ldc16 + col;
-                if (vec16 && col + 3 <= Nlast) {
-                    *(uint2 *)d = make_uint2((uint32_t)to_bf16(o[0]) | ((uint32_t)to_bf16(o[1]) << 16),
-                                             (uint32_t)to_bf16(o[2]) | ((uint32_t)to_bf16(o[3]) << 16));
-                } else {
+            for (int u = 0; u < kRB; ++u) {
+                const int k = k0 + u;
+                const bool ok = colok && row0 + k * kRowStep <= Mlast;
+                const float4 q = qb[u];
+                float o[4] = {q.x + bv[0], q.y + bv[1], q.z + bv[2], q.w + bv[3]};
+                if (relu)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (col + e <= Nlast) d[e] = to_bf16(o[e]);
+                    for (int e = 0; e < 4; ++e) o[e] = fmaxf(o[e], 0.0f);
+                if (emask) {
+                    const uint2 m = mk[k % kMaskBatch];
+                    o[0] = bf16_bits_positive(m.x & 0xFFFFu) ? o[0] : 0.0f;
+                    o[1] = bf16_bits_positive(m.x >> 16) ? o[1] : 0.0f;
+                    o[2] = bf16_bits_positive(m.y & 0xFFFFu) ? o[2] : 0.0f;
+                    o[3] = bf16_bits_positive(m.y >> 16) ? o[3] : 0.0f;
                 }
-            }
-            if (c32) {
-                float *d = dst + (int64_t)row * ldd + col;
-                if (vec32 && col + 3 <= Nlast) {
-                    *(float4 *)d = make_float4(o[0], o[1], o[2], o[3]);
-                } else {
+                if (ok) {
+                    if (ecs)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        if (col + e <= Nlast) d[e] = o[e];
+                        for (int e = 0; e < 4; ++e) cs[h][e] += o[e];
+                    if (c16) {
+                        uint16_t *d = p16;
+                        if (v16) {
+                            *(uint2 *)d = make_uint2(pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]));
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (col + e <= Nlast) d[e] = to_bf16(o[e]);
+                        }
+                    }
+                    if (c32) {
+                        float *d = p32;
+                        if (v32) {
+                            *(float4 *)d = make_float4(o[0], o[1], o[2], o[3]);
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                if (col + e <= Nlast) d[e] = o[e];
+                        }
+                    }
                 }
+                if (c16) p16 += s16;
+                if (c32) p32 += s32;
             }
         }
         __syncthreads();
