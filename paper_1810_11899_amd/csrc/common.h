@@ -11,6 +11,30 @@ namespace gcn {
 
 constexpr int kWave = 64;  // CDNA wavefront width
 
+// ------------------------------------------------------- bfloat16 rounding
+// float32 -> bfloat16, round to nearest even; a NaN stays NaN (quiet bit set)
+__device__ __forceinline__ uint16_t to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+    return (uint16_t)((u & 0x7FFFFFFFu) > 0x7F800000u ? ((u >> 16) | 0x0040u) : r);
+}
+#ifndef GCN_HW_BF16
+#define GCN_HW_BF16 1
+#endif
+typedef float gcn_float2 __attribute__((ext_vector_type(2)));
+typedef __bf16 gcn_bf16x2 __attribute__((ext_vector_type(2)));
+// Two values rounded as to_bf16 does, packed (a in the low half).  gfx950
+// rounds a pair in one instruction (v_cvt_pk_bf16_f32, round to nearest even),
+// with to_bf16's bits on every float32 input, NaN payloads included.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+#if GCN_HW_BF16
+    const gcn_float2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, gcn_bf16x2));
+#else
+    return (uint32_t)to_bf16(a) | ((uint32_t)to_bf16(b) << 16);
+#endif
+}
+
 // ------------------------------------------------------------------ errors
 void set_error(const char *fmt, ...);
 int hip_fail(hipError_t e, const char *what);

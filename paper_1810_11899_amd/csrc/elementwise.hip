@@ -30,11 +30,6 @@ inline int32_t chunk_count(int32_t n, int32_t width) {
     return (int32_t)(((int64_t)n + r - 1) / r);
 }
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-    const uint32_t u = __float_as_uint(f);
-    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x0040u);  // NaN stays NaN
-    return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
-}
 
 // Adds the block's kRowWaves per-wavefront sums in wavefront order and writes
 // the chunk's partial row.  Every thread of the block must call it.
@@ -117,12 +112,12 @@ __global__ __launch_bounds__(256) void relu_bwd_kernel(int32_t n, int32_t h, int
             if (dst16) {
                 uint16_t *o16 = dst16 + (int64_t)r * ldd + cc;
                 if (VEC == 4) {
-                    const uint32_t lo = (uint32_t)f32_to_bf16_rne(g[0]) | ((uint32_t)f32_to_bf16_rne(g[1]) << 16);
-                    const uint32_t hi = (uint32_t)f32_to_bf16_rne(g[2]) | ((uint32_t)f32_to_bf16_rne(g[3]) << 16);
+                    const uint32_t lo = pack_bf16x2(g[0], g[1]);
+                    const uint32_t hi = pack_bf16x2(g[2], g[3]);
                     *(uint2 *)o16 = make_uint2(lo, hi);
                 } else {
 #pragma unroll
-                    for (int v = 0; v < VEC; ++v) o16[v] = f32_to_bf16_rne(g[v]);
+                    for (int v = 0; v < VEC; ++v) o16[v] = to_bf16(g[v]);
                 }
             }
         }
@@ -271,11 +266,58 @@ __global__ __launch_bounds__(256) void cvt_bf16_kernel(int64_t rows, int64_t col
         uint16_t *yr = y + r * ldy;
         if (vec4 && c + 4 <= cols) {
             const float4 v = *(const float4 *)(xr + c);
-            const uint32_t lo = (uint32_t)f32_to_bf16_rne(v.x) | ((uint32_t)f32_to_bf16_rne(v.y) << 16);
-            const uint32_t hi = (uint32_t)f32_to_bf16_rne(v.z) | ((uint32_t)f32_to_bf16_rne(v.w) << 16);
+            const uint32_t lo = pack_bf16x2(v.x, v.y);
+            const uint32_t hi = pack_bf16x2(v.z, v.w);
             *(uint2 *)(yr + c) = make_uint2(lo, hi);
         } else {
-            for (int64_t e = c; e < c + 4 && e < ycols; ++e) yr[e] = e < cols ? f32_to_bf16_rne(xr[e]) : 0;
+            for (int64_t e = c; e < c + 4 && e < ycols; ++e) yr[e] = e < cols ? to_bf16(xr[e]) : 0;
+        }
+    }
+}
+
+// The 16-byte path: a row's 4-column groups over tpr lanes (a power of two
+// covering the groups, up to 256) and 256 / tpr rows per block, rows strided
+// over the grid, kCvtRows rows' loads in flight per thread.  Columns from
+// `cols` to `ycols` are written as zeros.
+constexpr int kCvtRows = 4;
+__global__ __launch_bounds__(256) void cvt_bf16_vec_kernel(int64_t rows, int64_t cols, int64_t ycols, int tpr,
+                                                           const float *__restrict__ x, int64_t ldx,
+                                                           uint16_t *__restrict__ y, int64_t ldy) {
+    const int64_t c = ((int64_t)blockIdx.x * tpr + (threadIdx.x % tpr)) * 4;
+    if (c >= ycols) return;
+    const int64_t rstep = (int64_t)gridDim.y * (256 / tpr);
+    const bool full = c + 4 <= cols;
+    for (int64_t r0 = (int64_t)blockIdx.y * (256 / tpr) + threadIdx.x / tpr; r0 < rows; r0 += rstep * kCvtRows) {
+        float4 v[kCvtRows];
+#pragma unroll
+        for (int u = 0; u < kCvtRows; ++u) {
+            const int64_t r = r0 + u * rstep;
+            v[u] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            if (r < rows) {
+                const float *xr = x + r * ldx + c;
+                if (full) {
+                    v[u] = *(const float4 *)xr;
+                } else {
+                    if (c < cols) v[u].x = xr[0];
+                    if (c + 1 < cols) v[u].y = xr[1];
+                    if (c + 2 < cols) v[u].z = xr[2];
+                    if (c + 3 < cols) v[u].w = xr[3];
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kCvtRows; ++u) {
+            const int64_t r = r0 + u * rstep;
+            if (r < rows) {
+                uint16_t *yr = y + r * ldy + c;
+                const uint32_t lo = pack_bf16x2(v[u].x, v[u].y), hi = pack_bf16x2(v[u].z, v[u].w);
+                if (c + 4 <= ycols) {
+                    *(uint2 *)yr = make_uint2(lo, hi);
+                } else {
+                    const uint16_t h[4] = {(uint16_t)lo, (uint16_t)(lo >> 16), (uint16_t)hi, (uint16_t)(hi >> 16)};
+                    for (int e = 0; e < 4 && c + e < ycols; ++e) yr[e] = h[e];
+                }
+            }
         }
     }
 }
@@ -299,8 +341,8 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(int64_t rows, int64
             if (vec && c + 4 <= cols) {
                 if constexpr (sizeof(TIn) == 4) {
                     const float4 f = *(const float4 *)(src + r * lds_ + c);
-                    v[0] = f32_to_bf16_rne(f.x); v[1] = f32_to_bf16_rne(f.y);
-                    v[2] = f32_to_bf16_rne(f.z); v[3] = f32_to_bf16_rne(f.w);
+                    v[0] = to_bf16(f.x); v[1] = to_bf16(f.y);
+                    v[2] = to_bf16(f.z); v[3] = to_bf16(f.w);
                 } else {
                     const uint2 u = *(const uint2 *)(src + r * lds_ + c);
                     v[0] = (uint16_t)(u.x & 0xFFFF); v[1] = (uint16_t)(u.x >> 16);
@@ -310,7 +352,7 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(int64_t rows, int64
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     if (c + e < cols) {
-                        if constexpr (sizeof(TIn) == 4) v[e] = f32_to_bf16_rne(src[r * lds_ + c + e]);
+                        if constexpr (sizeof(TIn) == 4) v[e] = to_bf16(src[r * lds_ + c + e]);
                         else v[e] = (uint16_t)src[r * lds_ + c + e];
                     }
             }
@@ -516,6 +558,20 @@ int cvt_bf16_pad(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16
     int64_t gy = rows < 65535 ? rows : 65535;
     if (gx * gy > 16384) gy = (16384 + gx - 1) / gx;
     ProfScope ps(K_CVT_BF16, s, 0.0, (double)rows * cols * 4.0 + (double)rows * ycols * 2.0);
+    if (vec4) {
+        const int64_t groups = (ycols + 3) / 4;
+        int tpr = 1;
+        while (tpr < groups && tpr < 256) tpr *= 2;
+        const int64_t bx = (groups + tpr - 1) / tpr;
+        const int64_t rpb = 256 / tpr;
+        int64_t by = (rows + rpb * kCvtRows - 1) / (rpb * kCvtRows);
+        if (by > 65535) by = 65535;
+        if (bx * by > 8192) by = std::max<int64_t>(1, 8192 / bx);
+        hipLaunchKernelGGL(cvt_bf16_vec_kernel, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, s, rows, cols, ycols,
+                           tpr, x, ldx, y, ldy);
+        GCN_LAUNCH_CHECK("cvt_bf16_vec_kernel");
+        return GCN_OK;
+    }
     hipLaunchKernelGGL(cvt_bf16_kernel, dim3((unsigned)gx, (unsigned)gy), dim3(256), 0, s, rows, cols, ycols, x,
                        ldx, y, ldy, vec4);
     GCN_LAUNCH_CHECK("cvt_bf16_kernel");

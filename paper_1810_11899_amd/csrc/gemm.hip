@@ -636,30 +636,6 @@ struct TileLoader16 {
     }
 };
 
-// float32 -> bfloat16, round to nearest even (NaN kept NaN, quiet)
-__device__ __forceinline__ uint16_t to_bf16(float f) {
-    const uint32_t u = __float_as_uint(f);
-    const uint32_t r = (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-    return (uint16_t)((u & 0x7FFFFFFFu) > 0x7F800000u ? ((u >> 16) | 0x0040u) : r);
-}
-
-#ifndef GCN_HW_BF16
-#define GCN_HW_BF16 1
-#endif
-typedef float gcn_float2 __attribute__((ext_vector_type(2)));
-typedef __bf16 gcn_bf16x2 __attribute__((ext_vector_type(2)));
-// two values rounded as to_bf16 does, packed (a in the low half).  gfx950
-// converts a pair in one instruction (v_cvt_pk_bf16_f32, round to nearest
-// even); it gives to_bf16's bits for every non-NaN float32.
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-#if GCN_HW_BF16
-    const gcn_float2 v = {a, b};
-    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, gcn_bf16x2));
-#else
-    return (uint32_t)to_bf16(a) | ((uint32_t)to_bf16(b) << 16);
-#endif
-}
-
 // a bfloat16 value (raw bits) compares > 0 exactly when its float32 widening does
 __device__ __forceinline__ bool bf16_bits_positive(uint32_t b) { return __uint_as_float(b << 16) > 0.0f; }
 

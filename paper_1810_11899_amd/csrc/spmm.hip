@@ -172,7 +172,10 @@ template <int VEC> struct Row<VEC, true> {
     }
 };
 
-__device__ __forceinline__ uint16_t to_bf16(float f) {
+// float32 -> bfloat16 as to_bf16, written with the NaN case as a branch: in
+// the gather kernels this form keeps the bfloat16 variant within its 72-VGPR
+// budget (the select form and the paired hardware rounding spill there)
+__device__ __forceinline__ uint16_t bf16_round(float f) {
     const uint32_t u = __float_as_uint(f);
     if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x0040u);
     return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
@@ -192,14 +195,14 @@ __device__ __forceinline__ void store16(uint16_t *__restrict__ o, const float (&
     if (VEC >= 2 && ovec) {
         uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
 #pragma unroll
-        for (int i = 0; i < VEC / 2; ++i) w[i] = (uint32_t)to_bf16(x[2 * i]) | ((uint32_t)to_bf16(x[2 * i + 1]) << 16);
+        for (int i = 0; i < VEC / 2; ++i) w[i] = (uint32_t)bf16_round(x[2 * i]) | ((uint32_t)bf16_round(x[2 * i + 1]) << 16);
         if constexpr (VEC == 8) *(uint4 *)o = make_uint4(w[0], w[1], w[2], w[3]);
         else if constexpr (VEC == 4) *(uint2 *)o = make_uint2(w[0], w[1]);
         else *(uint32_t *)o = w[0];
         return;
     }
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) o[v] = to_bf16(x[v]);
+    for (int v = 0; v < VEC; ++v) o[v] = bf16_round(x[v]);
 }
 
 template <int VEC, int OM = 0>
@@ -245,13 +248,13 @@ __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_
             uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
 #pragma unroll
             for (int i = 0; i < VEC / 2; ++i)
-                w[i] = (uint32_t)to_bf16(fin(2 * i)) | ((uint32_t)to_bf16(fin(2 * i + 1)) << 16);
+                w[i] = (uint32_t)bf16_round(fin(2 * i)) | ((uint32_t)bf16_round(fin(2 * i + 1)) << 16);
             if constexpr (VEC == 8) *(uint4 *)o16 = make_uint4(w[0], w[1], w[2], w[3]);
             else if constexpr (VEC == 4) *(uint2 *)o16 = make_uint2(w[0], w[1]);
             else *(uint32_t *)o16 = w[0];
         } else {
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) o16[v] = to_bf16(fin(v));
+            for (int v = 0; v < VEC; ++v) o16[v] = bf16_round(fin(v));
         }
         return;
     }
