@@ -877,6 +877,9 @@ constexpr int kBigStages = GCN_BIG_STAGES;   // 3..5 (5 x 32 KB is all of the CU
 #ifndef GCN_BIG_NARROW_TILES
 #define GCN_BIG_NARROW_TILES 256
 #endif
+#ifndef GCN_BIG_COPY_SPREAD
+#define GCN_BIG_COPY_SPREAD 1
+#endif
 #ifndef GCN_BIG_READS_PER_MFMA
 #define GCN_BIG_READS_PER_MFMA 3
 #endif
@@ -907,6 +910,17 @@ __device__ __forceinline__ void sched_reads() {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, Q + 1 < NG ? PER : TOT - Q * PER, 0);
         sched_reads<Q + 1, NG, PER, TOT>();
+    }
+}
+// the same, then one global-to-LDS copy behind each of the next NC matrix
+// instructions (groups Q .. NM-1, one matrix instruction each)
+template <int Q, int NM, int NG, int PER, int TOT, int NC>
+__device__ __forceinline__ void sched_reads_copies() {
+    if constexpr (Q < NM) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if constexpr (Q < NG) __builtin_amdgcn_sched_group_barrier(0x100, Q + 1 < NG ? PER : TOT - Q * PER, 0);
+        else if constexpr (Q < NG + NC) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        sched_reads_copies<Q + 1, NM, NG, PER, TOT, NC>();
     }
 }
 
@@ -1124,6 +1138,17 @@ void gemm_bf16_big_kernel(DevArgs args) {
         products(fa[1], fb[1]);
         interleave();
     };
+    // the same, with tile t+stages-1's copies issued among the products
+    // rather than in one burst after the barrier (every wavefront of the CU
+    // issuing its copies at once stalls them all on the vector-memory queue)
+    // (the copies follow the reads in program order: the compiler keeps LDS
+    // reads and copies into LDS in order, not knowing their stages differ)
+    auto half1_copy = [&](int t) {
+        read_frags((t + 1) % kBigStages, 0, fa[0], fb[0]);
+        issue_tile(t + kBigStages - 1);
+        products(fa[1], fb[1]);
+        sched_reads_copies<0, kBigFM * kBigFN, kReadGroups, kReadsPer, kReads, G>();
+    };
     if (ntiles > 0) {
         wait_tile(min(ntiles - 1, kBigStages - 2));   // tile 0
         barrier_after_vmcnt();
@@ -1136,8 +1161,12 @@ void gemm_bf16_big_kernel(DevArgs args) {
         half0(t);
         wait_vmcnt<(kBigStages - 3) * G>();
         barrier_after_vmcnt();
-        issue_tile(t + kBigStages - 1);
-        half1(t);
+        if constexpr (GCN_BIG_COPY_SPREAD) {
+            half1_copy(t);
+        } else {
+            issue_tile(t + kBigStages - 1);
+            half1(t);
+        }
     }
     // The last tiles: nothing left to copy, fewer copies in flight.
     for (; t < ntiles; ++t) {
