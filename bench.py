@@ -707,7 +707,12 @@ def main():
         out["measured_peaks"] = peaks
         for o in [out] + list(variants.values()):
             roof = o.get("roofline")
-            if roof is not None:
+            if roof is not None and roof["bound"] == "gather":
+                ref = peaks["gather"].get(f"uniform_{roof['gather_row_bytes']}B_16KiB")
+                if ref:
+                    roof["peak"] = ref["gbs"]
+                    roof["frac"] = round(roof["achieved"] / ref["gbs"], 4)
+            elif roof is not None:
                 prec_o = "f32" if o["dtype"] == "f32" else "bf16"
                 key = "stream_read_gbs" if roof["bound"] == "hbm" else f"mfma_{prec_o}_tflops"
                 roof["measured_peak"] = peaks[key]
@@ -835,6 +840,22 @@ def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32, 
                         "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4)}
             roof["mfma_frac"] = round(flops / (ms / 1e3) / 1e12 / peak, 4)
             roof["hbm_frac_algorithmic"] = round(bytes_ / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)
+        elif name in ("spmm", "spmm_bf16"):
+            # a gather: bound by the CU's vector-memory path, which takes every
+            # gathered 16-byte lane vector wherever it hits (L2, Infinity
+            # Cache, HBM).  `achieved` is the gathered row bytes per second
+            # (one row of the aggregated width per stored edge); the peak is
+            # the measured rate of random row gathers of the size its lane
+            # groups read from an L1-resident array (filled in once the
+            # machine ceilings are measured).  The gather-model bytes over
+            # 8 TB/s are kept beside it: above 1, since the caches serve most
+            # gathers, so not a DRAM fraction.
+            esz = 4 if name == "spmm" else 2
+            achieved = work["edge_features"] * esz * args.steps / (ms / 1e3) / 1e9
+            roof = {"bound": "gather", "kernel": name, "achieved": round(achieved, 1), "peak": None,
+                    "unit": "GB/s", "frac": None, "peak_source": "measured L1-resident random-row gather",
+                    "gather_row_bytes": 256 if name == "spmm" else 1024,
+                    "hbm_frac_gather_model": round(bytes_ / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
         else:
             achieved = bytes_ / (ms / 1e3) / 1e9
             roof = {"bound": "hbm", "kernel": name, "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,

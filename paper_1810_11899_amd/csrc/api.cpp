@@ -902,7 +902,8 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     }
     if (rc) return rc;
     // row losses; X <- G in place
-    if ((rc = loss_rows(kind, n, C, X, labels, targets, rows, s))) return rc;
+    // (bfloat16: G's class-padded bfloat16 rows G16 written alongside)
+    if ((rc = loss_rows(kind, n, C, X, labels, targets, rows, G16, Cp, s))) return rc;
     const double scale = kind == GCN_SOFTMAX_CE ? 1.0 / (double)n : 1.0 / ((double)n * (double)C);
     if ((rc = loss_reduce(n, rows, scale, loss, lw, pl.red, s))) return rc;
     // a5: dW_pred = HL^T G, db_pred = sum_i G, dHL = G W_pred^T
@@ -915,7 +916,6 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
     d.C = dHL;
     d.ldc = lddhl;
     if (bf) {
-        if ((rc = cvt_bf16_pad(n, C, X, C, G16, Cp, Cp, s))) return rc;
         if (tn_dw) {
             w.seg[0] = GemmSeg{HL16, f, G16, Cp, n};
             if ((rc = gemm(L_TN, 1, &w, 1, pl.split, gw, pl.gemm, s))) return rc;

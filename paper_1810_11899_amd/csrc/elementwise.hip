@@ -214,6 +214,85 @@ __global__ __launch_bounds__(256) void loss_rows_kernel(int kind, int32_t n, int
     }
 }
 
+// The same for rows of at most R * V classes: R lanes per row, four rows per
+// wavefront for R = 16, each lane holding the V logits of columns g, g + R,
+// ... in registers (one read of the row), reductions over the R lanes by xor
+// shuffles.  G16 (optional): the gradient rows also as bfloat16, Cp wide,
+// columns C .. Cp-1 zero (the class-padded operand of the head's products).
+template <int R, int V>
+__global__ __launch_bounds__(256) void loss_group_kernel(int kind, int32_t n, int32_t C, float *__restrict__ X,
+                                                         const int32_t *__restrict__ labels,
+                                                         const float *__restrict__ targets,
+                                                         float *__restrict__ rowloss, uint16_t *__restrict__ G16,
+                                                         int32_t Cp) {
+    static_assert(64 % R == 0, "row groups inside a wavefront");
+    const int g = threadIdx.x % R;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) / R;
+    if (i >= n) return;   // whole row groups leave together
+    float *x = X + i * C;
+    auto gmax = [](float v) {
+#pragma unroll
+        for (int o = R / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, R));
+        return v;
+    };
+    auto gsum = [](float v) {
+#pragma unroll
+        for (int o = R / 2; o > 0; o >>= 1) v += __shfl_xor(v, o, R);
+        return v;
+    };
+    float v[V], gr[V];
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        const int c = g + R * k;
+        v[k] = c < C ? x[c] : 0.0f;
+    }
+    if (kind == GCN_SOFTMAX_CE) {
+        float m = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            if (g + R * k < C) m = fmaxf(m, v[k]);
+        m = gmax(m);
+        float sum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < V; ++k)
+            if (g + R * k < C) sum += expf(v[k] - m);
+        sum = gsum(sum);
+        const float lse = m + logf(sum);
+        const int y = labels[i];
+        const float inv_n = 1.0f / (float)n;
+        float xy = 0.0f;
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            const int c = g + R * k;
+            if (c == y) xy = v[k];
+            gr[k] = (expf(v[k] - lse) - (c == y ? 1.0f : 0.0f)) * inv_n;
+        }
+        xy = gsum(xy);
+        if (g == 0) rowloss[i] = lse - xy;
+    } else {
+        const float *t = targets + i * C;
+        const float inv = 1.0f / ((float)n * (float)C);
+        float sum = 0.0f;
+#pragma unroll
+        for (int k = 0; k < V; ++k) {
+            const int c = g + R * k;
+            const float tv = c < C ? t[c] : 0.0f;
+            const float e = expf(-fabsf(v[k]));
+            if (c < C) sum += fmaxf(v[k], 0.0f) - v[k] * tv + log1pf(e);
+            const float sg = v[k] >= 0.0f ? 1.0f / (1.0f + e) : e / (1.0f + e);
+            gr[k] = (sg - tv) * inv;
+        }
+        sum = gsum(sum);
+        if (g == 0) rowloss[i] = sum;
+    }
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        const int c = g + R * k;
+        if (c < C) x[c] = gr[k];
+        if (G16 && c < Cp) G16[i * Cp + c] = c < C ? to_bf16(gr[k]) : (uint16_t)0;
+    }
+}
+
 // loss = scale * sum_i rowloss[i] in fixed order.  Up to kLossOne rows: one
 // block of 1024 threads writes the loss directly.  Beyond: blocks of kLossSeg
 // rows reduce to one double each, then one block adds those.
@@ -490,13 +569,26 @@ int colsum_reduce_rows(int32_t rows, int32_t C, const float *part, float *out, h
 }
 
 int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
-              float *rowloss, hipStream_t s) {
+              float *rowloss, uint16_t *G16, int32_t Cp, hipStream_t s) {
     if (n <= 0) return GCN_OK;
-    ProfScope ps(K_LOSS_ROWS, s, 0.0, (double)n * C * 4.0 * (kind == GCN_SIGMOID_BCE ? 3.0 : 2.0));
-    hipLaunchKernelGGL(loss_rows_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, kind, n, C, X, labels,
-                       targets, rowloss);
-    GCN_LAUNCH_CHECK("loss_rows_kernel");
-    return GCN_OK;
+    constexpr int R = 16, V = 8;
+    const bool grouped = C <= R * V && (!G16 || Cp <= R * V);
+    {
+        ProfScope ps(K_LOSS_ROWS, s, 0.0,
+                     (double)n * C * 4.0 * (kind == GCN_SIGMOID_BCE ? 3.0 : 2.0) +
+                         (G16 && grouped ? (double)n * Cp * 2.0 : 0.0));
+        if (grouped) {
+            const int64_t blocks = ((int64_t)n * R + 255) / 256;
+            hipLaunchKernelGGL((loss_group_kernel<R, V>), dim3((unsigned)blocks), dim3(256), 0, s, kind, n, C, X,
+                               labels, targets, rowloss, G16, Cp);
+            GCN_LAUNCH_CHECK("loss_group_kernel");
+        } else {
+            hipLaunchKernelGGL(loss_rows_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, kind, n, C, X,
+                               labels, targets, rowloss);
+            GCN_LAUNCH_CHECK("loss_rows_kernel");
+        }
+    }
+    return G16 && !grouped ? cvt_bf16_pad(n, C, X, C, G16, Cp, Cp, s) : GCN_OK;
 }
 
 size_t loss_reduce_workspace_bytes(int32_t n) {
