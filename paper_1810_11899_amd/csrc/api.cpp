@@ -810,8 +810,13 @@ LossPlan plan_loss(int32_t n, int32_t f, int32_t C, int prec) {
     GemmProblem g = dw_problem(f, C, n);
     p.split = gemm_pick_split(1, &g, true);
     p.gemm = gemm_workspace_bytes(1, &g, p.split);
-    p.colsum = colsum_workspace_bytes(n, C);
-    p.red = loss_reduce_workspace_bytes(n);
+    if (loss_fused_ok(C)) {   // the loss and db_pred from the loss kernel's block partials
+        p.colsum = 256;
+        p.red = loss_fused_workspace_bytes(n, C);
+    } else {
+        p.colsum = colsum_workspace_bytes(n, C);
+        p.red = loss_reduce_workspace_bytes(n);
+    }
     p.cp = colpart_bytes(n, f);
     p.total = p.X + p.rows + p.HL16 + p.HL16T + p.Wp16 + p.Wp16T + p.G16 + p.G16T + p.gemm + p.colsum + p.red +
               p.cp + 3584;
@@ -901,11 +906,19 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
         rc = gemm(L_NN, 1, &g, 0, 1, nullptr, 0, s);
     }
     if (rc) return rc;
-    // row losses; X <- G in place
-    // (bfloat16: G's class-padded bfloat16 rows G16 written alongside)
-    if ((rc = loss_rows(kind, n, C, X, labels, targets, rows, G16, Cp, s))) return rc;
+    // row losses, X <- G in place (bfloat16: G's class-padded bfloat16 rows
+    // G16 alongside); up to 128 classes the same pass leaves block partials
+    // from which one more launch forms the loss and db_pred
     const double scale = kind == GCN_SOFTMAX_CE ? 1.0 / (double)n : 1.0 / ((double)n * (double)C);
-    if ((rc = loss_reduce(n, rows, scale, loss, lw, pl.red, s))) return rc;
+    const bool fused = loss_fused_ok(C);
+    if (fused) {
+        if ((rc = loss_fused(kind, n, C, X, labels, targets, scale, loss, db_pred, G16, Cp, lw, pl.red, s)))
+            return rc;
+    } else {
+        if ((rc = loss_rows(kind, n, C, X, labels, targets, rows, s))) return rc;
+        if ((rc = loss_reduce(n, rows, scale, loss, lw, pl.red, s))) return rc;
+        if (bf && (rc = cvt_bf16_pad(n, C, X, C, G16, Cp, Cp, s))) return rc;
+    }
     // a5: dW_pred = HL^T G, db_pred = sum_i G, dHL = G W_pred^T
     GemmProblem w = dw_problem(f, C, n);
     w.C = dW_pred;
@@ -931,7 +944,7 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
         if ((rc = gemm(L_TN, 1, &w, 0, pl.split, gw, pl.gemm, s))) return rc;
         d.seg[0] = GemmSeg{X, C, W_pred, C, C};
     }
-    if ((rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s))) return rc;
+    if (!fused && (rc = colsum(n, C, X, C, db_pred, cw, pl.colsum, s))) return rc;
     if (below_dbias) {
         d.colpart = cp;
         if (bf) {

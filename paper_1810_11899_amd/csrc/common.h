@@ -231,9 +231,15 @@ size_t colsum_workspace_bytes(int32_t n, int32_t C);
 int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *ws, size_t ws_bytes,
            hipStream_t s);
 // Row-wise loss on logits X (n x C, ldx == C), in place: X <- G.  rowloss[n].
-// G16 (optional): the gradient rows also as bfloat16, Cp wide, zero-padded
 int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
-              float *rowloss, uint16_t *G16, int32_t Cp, hipStream_t s);
+              float *rowloss, hipStream_t s);
+// The head for up to 128 classes in two launches: G in place (and its
+// class-padded bfloat16 rows G16 when given), the loss and db = sum_i G[i, :]
+bool loss_fused_ok(int32_t C);
+size_t loss_fused_workspace_bytes(int32_t n, int32_t C);
+int loss_fused(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
+               double scale, float *loss, float *db, uint16_t *G16, int32_t Cp, void *ws, size_t ws_bytes,
+               hipStream_t s);
 size_t loss_reduce_workspace_bytes(int32_t n);
 int loss_reduce(int32_t n, const float *rowloss, double scale, float *loss, void *ws, size_t ws_bytes,
                 hipStream_t s);

@@ -214,21 +214,29 @@ __global__ __launch_bounds__(256) void loss_rows_kernel(int kind, int32_t n, int
     }
 }
 
-// The same for rows of at most R * V classes: R lanes per row, four rows per
-// wavefront for R = 16, each lane holding the V logits of columns g, g + R,
-// ... in registers (one read of the row), reductions over the R lanes by xor
-// shuffles.  G16 (optional): the gradient rows also as bfloat16, Cp wide,
-// columns C .. Cp-1 zero (the class-padded operand of the head's products).
+// The same for rows of at most R * V classes: R lanes per row, 256 / R rows
+// per block, each lane holding the V logits of columns g, g + R, ... in
+// registers (one read of the row), reductions over the R lanes by xor
+// shuffles.  Beside G in place it writes, per block, the sum of its rows'
+// losses (double, rows in order) and the column sums of its G rows (lpart,
+// cpart: the head's loss and bias gradient finish in head_reduce_kernel).
+// G16 (optional): the gradient rows also as bfloat16, Cp wide, columns
+// C .. Cp-1 zero (the class-padded operand of the head's products).
 template <int R, int V>
 __global__ __launch_bounds__(256) void loss_group_kernel(int kind, int32_t n, int32_t C, float *__restrict__ X,
                                                          const int32_t *__restrict__ labels,
                                                          const float *__restrict__ targets,
-                                                         float *__restrict__ rowloss, uint16_t *__restrict__ G16,
-                                                         int32_t Cp) {
-    static_assert(64 % R == 0, "row groups inside a wavefront");
+                                                         double *__restrict__ lpart, float *__restrict__ cpart,
+                                                         uint16_t *__restrict__ G16, int32_t Cp) {
+    static_assert(R == 16 && V * R <= 128, "four row groups per wavefront, 128 columns at most");
+    constexpr int RPB = 256 / R;   // rows per block
+    __shared__ float sh_loss[RPB];
+    __shared__ float sh_col[4][R * V];
     const int g = threadIdx.x % R;
-    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) / R;
-    if (i >= n) return;   // whole row groups leave together
+    const int rg = threadIdx.x / R;           // row group of the block
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int64_t i = (int64_t)blockIdx.x * RPB + rg;
+    const bool live = i < n;                  // rows past n take part in the block sums as zeros
     float *x = X + i * C;
     auto gmax = [](float v) {
 #pragma unroll
@@ -244,8 +252,9 @@ __global__ __launch_bounds__(256) void loss_group_kernel(int kind, int32_t n, in
 #pragma unroll
     for (int k = 0; k < V; ++k) {
         const int c = g + R * k;
-        v[k] = c < C ? x[c] : 0.0f;
+        v[k] = live && c < C ? x[c] : 0.0f;
     }
+    float rl = 0.0f;
     if (kind == GCN_SOFTMAX_CE) {
         float m = -INFINITY;
 #pragma unroll
@@ -258,17 +267,17 @@ __global__ __launch_bounds__(256) void loss_group_kernel(int kind, int32_t n, in
             if (g + R * k < C) sum += expf(v[k] - m);
         sum = gsum(sum);
         const float lse = m + logf(sum);
-        const int y = labels[i];
+        const int y = live ? labels[i] : -1;
         const float inv_n = 1.0f / (float)n;
         float xy = 0.0f;
 #pragma unroll
         for (int k = 0; k < V; ++k) {
             const int c = g + R * k;
             if (c == y) xy = v[k];
-            gr[k] = (expf(v[k] - lse) - (c == y ? 1.0f : 0.0f)) * inv_n;
+            gr[k] = live && c < C ? (expf(v[k] - lse) - (c == y ? 1.0f : 0.0f)) * inv_n : 0.0f;
         }
         xy = gsum(xy);
-        if (g == 0) rowloss[i] = lse - xy;
+        rl = live ? lse - xy : 0.0f;
     } else {
         const float *t = targets + i * C;
         const float inv = 1.0f / ((float)n * (float)C);
@@ -276,21 +285,83 @@ __global__ __launch_bounds__(256) void loss_group_kernel(int kind, int32_t n, in
 #pragma unroll
         for (int k = 0; k < V; ++k) {
             const int c = g + R * k;
-            const float tv = c < C ? t[c] : 0.0f;
+            const bool ok = live && c < C;
+            const float tv = ok ? t[c] : 0.0f;
             const float e = expf(-fabsf(v[k]));
-            if (c < C) sum += fmaxf(v[k], 0.0f) - v[k] * tv + log1pf(e);
+            if (ok) sum += fmaxf(v[k], 0.0f) - v[k] * tv + log1pf(e);
             const float sg = v[k] >= 0.0f ? 1.0f / (1.0f + e) : e / (1.0f + e);
-            gr[k] = (sg - tv) * inv;
+            gr[k] = ok ? (sg - tv) * inv : 0.0f;
         }
-        sum = gsum(sum);
-        if (g == 0) rowloss[i] = sum;
+        rl = gsum(sum);
     }
 #pragma unroll
     for (int k = 0; k < V; ++k) {
         const int c = g + R * k;
-        if (c < C) x[c] = gr[k];
-        if (G16 && c < Cp) G16[i * Cp + c] = c < C ? to_bf16(gr[k]) : (uint16_t)0;
+        if (live && c < C) x[c] = gr[k];
+        if (live && G16 && c < Cp) G16[i * Cp + c] = c < C ? to_bf16(gr[k]) : (uint16_t)0;
     }
+    // block sums: the four row groups of a wavefront share columns (lanes
+    // g, g+16, g+32, g+48), then the four wavefronts in order
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+        float c = gr[k] + __shfl_xor(gr[k], 16);
+        c += __shfl_xor(c, 32);
+        gr[k] = c;
+    }
+    if (lane < R)
+#pragma unroll
+        for (int k = 0; k < V; ++k) sh_col[wv][g + R * k] = gr[k];
+    if (g == 0) sh_loss[rg] = rl;
+    __syncthreads();
+    if ((int)threadIdx.x < C)   // column-major: column c's block sums are contiguous
+        cpart[(int64_t)threadIdx.x * gridDim.x + blockIdx.x] =
+            ((sh_col[0][threadIdx.x] + sh_col[1][threadIdx.x]) + sh_col[2][threadIdx.x]) + sh_col[3][threadIdx.x];
+    if (threadIdx.x == 0) {
+        double t = 0.0;
+#pragma unroll
+        for (int r = 0; r < RPB; ++r) t += (double)sh_loss[r];
+        lpart[blockIdx.x] = t;
+    }
+}
+
+// The head's sums from the loss kernel's block partials, in fixed order:
+// blocks 0 .. ceil(C/4)-1 one wavefront per column (db_pred[c] = sum over
+// blocks b of cpart[c][b], read contiguously, four per lane per step), the
+// last block the loss (scale x the sum of the blocks' double loss sums).
+__global__ __launch_bounds__(256) void head_reduce_kernel(int32_t nb, int32_t C, const float *__restrict__ cpart,
+                                                          const double *__restrict__ lpart, double scale,
+                                                          float *__restrict__ loss, float *__restrict__ db) {
+    const int cblocks = (C + 3) / 4;
+    if ((int)blockIdx.x < cblocks) {
+        const int lane = threadIdx.x & 63;
+        const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
+        if (c >= C) return;
+        const float *col = cpart + (int64_t)c * nb;
+        float s0 = 0.0f, s1 = 0.0f, s2 = 0.0f, s3 = 0.0f;
+        int b = lane;
+        for (; b + 192 < nb; b += 256) {
+            s0 += col[b];
+            s1 += col[b + 64];
+            s2 += col[b + 128];
+            s3 += col[b + 192];
+        }
+        for (; b < nb; b += 64) s0 += col[b];
+        float s = (s0 + s1) + (s2 + s3);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+        if (lane == 0) db[c] = s;
+        return;
+    }
+    __shared__ double sh[256];
+    double t = 0.0;
+    for (int b = threadIdx.x; b < nb; b += 256) t += lpart[b];
+    sh[threadIdx.x] = t;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+        if ((int)threadIdx.x < o) sh[threadIdx.x] += sh[threadIdx.x + o];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = (float)(sh[0] * scale);
 }
 
 // loss = scale * sum_i rowloss[i] in fixed order.  Up to kLossOne rows: one
@@ -569,26 +640,52 @@ int colsum_reduce_rows(int32_t rows, int32_t C, const float *part, float *out, h
 }
 
 int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
-              float *rowloss, uint16_t *G16, int32_t Cp, hipStream_t s) {
+              float *rowloss, hipStream_t s) {
     if (n <= 0) return GCN_OK;
-    constexpr int R = 16, V = 8;
-    const bool grouped = C <= R * V && (!G16 || Cp <= R * V);
+    ProfScope ps(K_LOSS_ROWS, s, 0.0, (double)n * C * 4.0 * (kind == GCN_SIGMOID_BCE ? 3.0 : 2.0));
+    hipLaunchKernelGGL(loss_rows_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, kind, n, C, X, labels,
+                       targets, rowloss);
+    GCN_LAUNCH_CHECK("loss_rows_kernel");
+    return GCN_OK;
+}
+
+namespace {
+constexpr int kLossR = 16, kLossV = 8;
+int32_t loss_blocks(int32_t n) { return (int32_t)(((int64_t)n * kLossR + 255) / 256); }
+}  // namespace
+
+// (the bfloat16 head pads the classes to a multiple of 32, which stays within 128)
+bool loss_fused_ok(int32_t C) { return C >= 1 && C <= kLossR * kLossV; }
+
+size_t loss_fused_workspace_bytes(int32_t n, int32_t C) {
+    const size_t nb = (size_t)loss_blocks(n);
+    return align256(nb * sizeof(double)) + align256(nb * (size_t)C * sizeof(float)) + 512;
+}
+
+int loss_fused(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
+               double scale, float *loss, float *db, uint16_t *G16, int32_t Cp, void *ws, size_t ws_bytes,
+               hipStream_t s) {
+    if (n <= 0) return GCN_OK;
+    const int32_t nb = loss_blocks(n);
+    Arena ar(ws, ws_bytes);
+    double *lpart = ar.take<double>(nb);
+    float *cpart = ar.take<float>((size_t)nb * C);
+    if (!lpart || !cpart || !loss_fused_ok(C)) {
+        set_error("loss: workspace too small or classes > %d", kLossR * kLossV);
+        return GCN_EWORKSPACE;
+    }
     {
         ProfScope ps(K_LOSS_ROWS, s, 0.0,
-                     (double)n * C * 4.0 * (kind == GCN_SIGMOID_BCE ? 3.0 : 2.0) +
-                         (G16 && grouped ? (double)n * Cp * 2.0 : 0.0));
-        if (grouped) {
-            const int64_t blocks = ((int64_t)n * R + 255) / 256;
-            hipLaunchKernelGGL((loss_group_kernel<R, V>), dim3((unsigned)blocks), dim3(256), 0, s, kind, n, C, X,
-                               labels, targets, rowloss, G16, Cp);
-            GCN_LAUNCH_CHECK("loss_group_kernel");
-        } else {
-            hipLaunchKernelGGL(loss_rows_kernel, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, s, kind, n, C, X,
-                               labels, targets, rowloss);
-            GCN_LAUNCH_CHECK("loss_rows_kernel");
-        }
+                     (double)n * C * 4.0 * (kind == GCN_SIGMOID_BCE ? 3.0 : 2.0) + (G16 ? (double)n * Cp * 2.0 : 0.0));
+        hipLaunchKernelGGL((loss_group_kernel<kLossR, kLossV>), dim3((unsigned)nb), dim3(256), 0, s, kind, n, C, X,
+                           labels, targets, lpart, cpart, G16, Cp);
+        GCN_LAUNCH_CHECK("loss_group_kernel");
     }
-    return G16 && !grouped ? cvt_bf16_pad(n, C, X, C, G16, Cp, Cp, s) : GCN_OK;
+    ProfScope ps(K_LOSS_REDUCE, s, 0.0, (double)nb * (C * 4.0 + 8.0));
+    hipLaunchKernelGGL(head_reduce_kernel, dim3((unsigned)((C + 3) / 4 + 1)), dim3(256), 0, s, nb, C, cpart, lpart,
+                       scale, loss, db);
+    GCN_LAUNCH_CHECK("head_reduce_kernel");
+    return GCN_OK;
 }
 
 size_t loss_reduce_workspace_bytes(int32_t n) {
