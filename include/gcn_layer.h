@@ -250,8 +250,11 @@ int gcn_loss_grad(const float *HL, int32_t n, int32_t f, int32_t ldhl,
  * l = 0 only) is the output gradient of layer l-1.  With head == NULL the
  * output gradient dY [n x 2h_L] (lddy) is given instead of PREDICT/LOSS.
  * The workspace (gcn_model_workspace_bytes) holds the merge-path row ranges
- * of A and A^T, computed once for all of the step's aggregations, and the
- * scratch shared by the calls, which run in order on `stream`.  Errors are those of the calls it makes.
+ * of A and A^T, computed once for all of the step's aggregations, with
+ * GCN_BF16 the step's weight matrices as bfloat16 (each in the forms its
+ * products read, converted in one launch at the start of the step), and the
+ * scratch shared by the calls, which run in order on `stream`.  Errors are
+ * those of the calls it makes.
  * Buffers between the calls: head->dHL and the dH of layers 1..L-1 carry the
  * gradient from one call to the next, and their contents on return are
  * unspecified.  The step multiplies such a gradient by the ReLU derivative

@@ -454,6 +454,7 @@ struct Bf16Link {
     bool in_ready = false;        // saved already holds this layer's H16 and H16^T
     uint16_t *out16 = nullptr;    // bf16(Y) rows, n x 2h (leading dim 2h)
     uint16_t *out16T = nullptr;   // bf16(Y)^T, 2h x n (leading dim n)
+    const uint16_t *WsT = nullptr, *WnT = nullptr;   // bf16(W_self)^T, bf16(W_neigh)^T, already made
 };
 
 // launch == false: the argument checks only, nothing enqueued
@@ -500,8 +501,13 @@ static int layer_fwd(bool launch, const gcn_csr *A, const float *H, int32_t f_in
             rc = tnw ? cvt_bf16(n, f_in, H, ldh, H16, f_in, s) : transpose_bf16_copy(n, f_in, H, 0, ldh, H16T, n, H16, f_in, s);
             if (rc) return rc;
         }
-        if ((rc = transpose_bf16(f_in, h, W_self, 0, h, WsT, f_in, s))) return rc;
-        if ((rc = transpose_bf16(f_in, h, W_neigh, 0, h, WnT, f_in, s))) return rc;
+        if (lk.WsT) {
+            WsT = const_cast<uint16_t *>(lk.WsT);
+            WnT = const_cast<uint16_t *>(lk.WnT);
+        } else {
+            if ((rc = transpose_bf16(f_in, h, W_self, 0, h, WsT, f_in, s))) return rc;
+            if ((rc = transpose_bf16(f_in, h, W_neigh, 0, h, WnT, f_in, s))) return rc;
+        }
         GemmProblem g[2] = {};
         g[0].M = g[1].M = n;
         g[0].N = g[1].N = h;
@@ -592,7 +598,8 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
                      int32_t lddh, float *dW_self, float *dW_neigh, float *dbias, gcn_order order, gcn_prec prec,
                      void *ws, size_t ws_bytes, void *stream, bool dz_ready = false,
                      float *below_dbias = nullptr, const int32_t *bAT = nullptr, bool dzT_ready = false,
-                     int32_t below_tcols = 0) {
+                     int32_t below_tcols = 0, const uint16_t *Ws16_ready = nullptr,
+                     const uint16_t *Wn16_ready = nullptr) {
     // bAT: A^T's merge-path row ranges (spmm_bounds), or NULL
     // dzT_ready (bfloat16, with dz_ready): the producer of dY also wrote
     // dZ^T (2h x n, leading dim n) behind the packed dZ rows in the same
@@ -731,10 +738,15 @@ static int layer_bwd(bool launch, const gcn_csr *A, const gcn_csr *AT, const flo
     // a8: input gradient
     const void *Wsop = W_self, *Wnop = W_neigh;
     if (bf) {
-        if ((rc = cvt_bf16(f_in, h, W_self, h, Ws16, h, s))) return rc;
-        if ((rc = cvt_bf16(f_in, h, W_neigh, h, Wn16, h, s))) return rc;
-        Wsop = Ws16;
-        Wnop = Wn16;
+        if (Ws16_ready) {   // the model step converted the weights up front
+            Wsop = Ws16_ready;
+            Wnop = Wn16_ready;
+        } else {
+            if ((rc = cvt_bf16(f_in, h, W_self, h, Ws16, h, s))) return rc;
+            if ((rc = cvt_bf16(f_in, h, W_neigh, h, Wn16, h, s))) return rc;
+            Wsop = Ws16;
+            Wnop = Wn16;
+        }
     }
     if (pl.need_G) {
         GemmProblem d{};
@@ -833,7 +845,8 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
                      const float *targets, float *loss, float *dHL, int32_t lddhl, float *dW_pred, float *db_pred,
                      gcn_prec prec, void *ws, size_t ws_bytes, void *stream, float *below_dbias = nullptr,
                      const uint16_t *HL16_ready = nullptr, const uint16_t *HL16T_ready = nullptr,
-                     int32_t below_tcols = 0) {
+                     int32_t below_tcols = 0, const uint16_t *Wp16_ready = nullptr,
+                     const uint16_t *Wp16T_ready = nullptr) {
     // HL16_ready / HL16T_ready (bfloat16): HL's bfloat16 rows and transposed
     // rows, already written by the last layer's epilogues.  below_tcols (with
     // below_dbias): also write the first below_tcols columns of the last
@@ -897,8 +910,13 @@ static int loss_grad(bool launch, const float *HL, int32_t n, int32_t f, int32_t
                         : transpose_bf16_copy(n, f, HL, 0, ldhl, const_cast<uint16_t *>(HL16T), n,
                                               const_cast<uint16_t *>(HL16), f, s)))
             return rc;
-        if ((rc = cvt_bf16_pad(f, C, W_pred, C, Wp16, Cp, Cp, s))) return rc;
-        if ((rc = transpose_bf16(f, C, Wp16, 1, Cp, Wp16T, f, s))) return rc;
+        if (Wp16_ready) {   // the model step converted W_pred up front
+            Wp16 = const_cast<uint16_t *>(Wp16_ready);
+            Wp16T = const_cast<uint16_t *>(Wp16T_ready);
+        } else {
+            if ((rc = cvt_bf16_pad(f, C, W_pred, C, Wp16, Cp, Cp, s))) return rc;
+            if ((rc = transpose_bf16(f, C, Wp16, 1, Cp, Wp16T, f, s))) return rc;
+        }
         g.seg[0] = GemmSeg{HL16, f, Wp16T, f, f};
         rc = gemm(L_NT, 1, &g, 1, 1, nullptr, 0, s);
     } else {
@@ -1040,6 +1058,57 @@ static size_t model_hl16_bytes(int32_t n, int32_t L, const gcn_layer_args *layer
     return 2 * align256((size_t)n * 2 * layers[L - 1].h * 2);
 }
 
+// bfloat16: every weight matrix of the step in the forms its products read
+// (W^T for the forward NT products, W for the input-gradient products,
+// W_pred zero-padded to the padded classes and transposed), converted in one
+// launch at the start of the step
+struct ModelW16 {
+    const uint16_t *WsT[8] = {}, *WnT[8] = {}, *Ws16[8] = {}, *Wn16[8] = {};
+    const uint16_t *Wp16 = nullptr, *Wp16T = nullptr;
+};
+static size_t model_w16_bytes(int32_t n, int32_t L, const gcn_layer_args *layers, const gcn_head_args *head,
+                              gcn_prec prec, Bf16PrepBatch *batch = nullptr, ModelW16 *out = nullptr,
+                              char *base = nullptr) {
+    if (prec != GCN_BF16 || n <= 0 || L > 8 || 4 * L + 2 > kPrepMaxJobs) return 0;
+    size_t off = 0;
+    auto carve = [&](size_t bytes) {
+        uint16_t *p = base ? (uint16_t *)(base + off) : nullptr;
+        off += align256(bytes);
+        return p;
+    };
+    for (int32_t l = 0; l < L; ++l) {
+        const gcn_layer_args &a = layers[l];
+        const size_t one = (size_t)a.f_in * a.h * 2;
+        uint16_t *st = carve(one), *nt = carve(one);
+        if (batch) {
+            batch->add(a.W_self, a.h, a.f_in, a.h, st, a.f_in, 0, true);
+            batch->add(a.W_neigh, a.h, a.f_in, a.h, nt, a.f_in, 0, true);
+            out->WsT[l] = st;
+            out->WnT[l] = nt;
+        }
+        if (a.dH) {
+            uint16_t *sr = carve(one), *nr = carve(one);
+            if (batch) {
+                batch->add(a.W_self, a.h, a.f_in, a.h, sr, a.h, a.h, false);
+                batch->add(a.W_neigh, a.h, a.f_in, a.h, nr, a.h, a.h, false);
+                out->Ws16[l] = sr;
+                out->Wn16[l] = nr;
+            }
+        }
+    }
+    if (head) {
+        const int32_t f = 2 * layers[L - 1].h, C = head->C, Cp = pad_classes(C);
+        uint16_t *wp = carve((size_t)f * Cp * 2), *wpt = carve((size_t)f * C * 2);
+        if (batch) {
+            batch->add(head->W_pred, C, f, C, wp, Cp, Cp, false);
+            batch->add(head->W_pred, C, f, C, wpt, f, 0, true);
+            out->Wp16 = wp;
+            out->Wp16T = wpt;
+        }
+    }
+    return off;
+}
+
 size_t gcn_model_workspace_bytes(int32_t n, int32_t nnz, int32_t L, const gcn_layer_args *layers,
                                  const gcn_head_args *head, gcn_prec prec) {
     if (n < 0 || nnz < 0 || L < 1 || !layers) return 0;
@@ -1050,7 +1119,8 @@ size_t gcn_model_workspace_bytes(int32_t n, int32_t nnz, int32_t L, const gcn_la
     // the row ranges of A and A^T, shared by the calls, and with bfloat16
     // operands the last layer's output as the head's bfloat16 rows and
     // transposed rows
-    return b + 2 * spmm_bounds_bytes(n, nnz) + model_hl16_bytes(n, L, layers, head, prec);
+    return b + 2 * spmm_bounds_bytes(n, nnz) + model_hl16_bytes(n, L, layers, head, prec) +
+           model_w16_bytes(n, L, layers, head, prec);
 }
 
 namespace {
@@ -1093,6 +1163,15 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         ws = (char *)ws + hb;
         ws_bytes -= hb;
     }
+    ModelW16 w16;
+    if (const size_t wb = model_w16_bytes(n, L, layers, head, prec)) {
+        REQUIRE(ws && ws_bytes >= wb, GCN_EWORKSPACE, "gcn_model_step: workspace %zu bytes too small", ws_bytes);
+        Bf16PrepBatch batch;
+        model_w16_bytes(n, L, layers, head, prec, &batch, &w16, (char *)ws);
+        ws = (char *)ws + wb;
+        ws_bytes -= wb;
+        if (launch && (rc = prep_bf16(batch, as_stream(stream)))) return rc;
+    }
     const float *H = H0;  // forward: layer l reads layer l-1's output
     int32_t ldh = ldh0;
     for (int32_t l = 0; l < L; ++l) {
@@ -1109,6 +1188,8 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
                 lk.out16 = HL16;
                 if (!head_dw_rowmajor(n, 2 * a.h, head->C)) lk.out16T = HL16T;   // read by an NT dW_pred only
             }
+            lk.WsT = w16.WsT[l];
+            lk.WnT = w16.WnT[l];
         }
         if ((rc = layer_fwd(launch, A, H, a.f_in, ldh, a.W_self, a.W_neigh, a.bias, a.h, a.Y, a.ldy, a.saved,
                             a.saved_bytes, a.order, prec, ws, ws_bytes, stream, bA, lk)))
@@ -1134,7 +1215,8 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         if ((rc = loss_grad(launch, last.Y, n, 2 * last.h, last.ldy, head->W_pred, head->b_pred, head->C,
                             head->kind, head->labels, head->targets, head->loss, head->dHL, head->lddhl,
                             head->dW_pred, head->db_pred, prec, ws, ws_bytes, stream,
-                            fuse ? last.dbias : nullptr, HL16, HL16T, fuse ? tcols(L - 1) : 0)))
+                            fuse ? last.dbias : nullptr, HL16, HL16T, fuse ? tcols(L - 1) : 0, w16.Wp16,
+                            w16.Wp16T)))
             return rc;
         g = head->dHL;
         ldg = head->lddhl;
@@ -1148,7 +1230,7 @@ int model_step(bool launch, const gcn_csr *A, const gcn_csr *AT, const float *H0
         if ((rc = layer_bwd(launch, A, AT, Hin, a.f_in, ldin, a.W_self, a.W_neigh, a.h, a.Y, a.ldy, a.saved,
                             a.saved_bytes, g, ldg, a.dH, a.lddh, a.dW_self, a.dW_neigh, a.dbias, a.order, prec, ws,
                             ws_bytes, stream, ready, fuse ? layers[l - 1].dbias : nullptr, bAT,
-                            ready && tcols(l) > 0, fuse ? tcols(l - 1) : 0)))
+                            ready && tcols(l) > 0, fuse ? tcols(l - 1) : 0, w16.Ws16[l], w16.Wn16[l])))
             return rc;
         g = a.dH;
         ldg = a.lddh;

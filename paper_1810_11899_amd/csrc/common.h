@@ -253,6 +253,39 @@ int transpose_bf16(int64_t rows, int64_t cols, const void *src, int src_is_bf16,
 int transpose_bf16_copy(int64_t rows, int64_t cols, const void *src, int src_is_bf16, int64_t lds, uint16_t *dst,
                         int64_t ldd, uint16_t *copy, int64_t ldc, hipStream_t s);
 // float32 -> bfloat16 bits (RNE), 2-D with leading dimensions
+// A batch of small float32 -> bfloat16 conversions (plain, zero-padded to
+// dcols columns, or transposed) in one launch
+struct Bf16PrepJob {
+    const float *src;
+    int64_t lds;
+    uint16_t *dst;
+    int64_t ldd;
+    int32_t rows, cols;    // of src
+    int32_t dcols;         // plain: columns written per row (cols .. dcols-1 zero)
+    int32_t transpose;     // 1: dst (cols x rows) = bf16(src)^T
+    int32_t tiles_c;       // set by prep_bf16
+    int64_t first_block;   // set by prep_bf16
+};
+constexpr int kPrepMaxJobs = 16;
+struct Bf16PrepBatch {
+    Bf16PrepJob job[kPrepMaxJobs];
+    int32_t njobs = 0;
+    void add(const float *src, int64_t lds, int32_t rows, int32_t cols, uint16_t *dst, int64_t ldd, int32_t dcols,
+             bool transpose) {
+        Bf16PrepJob &J = job[njobs++];
+        J.src = src;
+        J.lds = lds;
+        J.dst = dst;
+        J.ldd = ldd;
+        J.rows = rows;
+        J.cols = cols;
+        J.dcols = dcols;
+        J.transpose = transpose ? 1 : 0;
+        J.tiles_c = 0;
+        J.first_block = 0;
+    }
+};
+int prep_bf16(Bf16PrepBatch &b, hipStream_t s);
 int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
              hipStream_t s);
 // the same, and columns cols .. ycols-1 of y set to zero (K padding)

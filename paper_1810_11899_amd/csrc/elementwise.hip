@@ -767,6 +767,61 @@ int cvt_bf16_pad(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16
     return GCN_OK;
 }
 
+// Several small float32 matrices (a step's weights) to bfloat16 in one
+// launch: each job is a plain copy (columns cols .. dcols-1 of a row zero)
+// or a transposed one (dst, cols x rows, = bf16(src)^T), in 32 x 32 tiles,
+// the transposed ones through LDS so that reads and writes stay coalesced.
+// Each block finds its job among the batch's block ranges.
+namespace {
+__global__ __launch_bounds__(256) void prep_bf16_kernel(Bf16PrepBatch b) {
+    int j = 0;
+    while (j + 1 < b.njobs && (int64_t)blockIdx.x >= b.job[j + 1].first_block) ++j;
+    const Bf16PrepJob &J = b.job[j];
+    const int64_t t = (int64_t)blockIdx.x - J.first_block;
+    const int tr = (int)(t / J.tiles_c), tc = (int)(t % J.tiles_c);
+    const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+    if (J.transpose) {
+        __shared__ float tile[32][33];
+#pragma unroll
+        for (int k = 0; k < 32; k += 8) {
+            const int r = tr * 32 + ty + k, c = tc * 32 + tx;
+            tile[ty + k][tx] = (r < J.rows && c < J.cols) ? J.src[(int64_t)r * J.lds + c] : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 32; k += 8) {
+            const int c = tc * 32 + ty + k, r = tr * 32 + tx;
+            if (c < J.cols && r < J.rows) J.dst[(int64_t)c * J.ldd + r] = to_bf16(tile[tx][ty + k]);
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 32; k += 8) {
+            const int r = tr * 32 + ty + k, c = tc * 32 + tx;
+            if (r < J.rows && c < J.dcols)
+                J.dst[(int64_t)r * J.ldd + c] = c < J.cols ? to_bf16(J.src[(int64_t)r * J.lds + c]) : (uint16_t)0;
+        }
+    }
+}
+}  // namespace
+
+int prep_bf16(Bf16PrepBatch &b, hipStream_t s) {
+    int64_t blocks = 0;
+    double bytes = 0.0;
+    for (int j = 0; j < b.njobs; ++j) {
+        Bf16PrepJob &J = b.job[j];
+        const int wc = J.transpose ? J.cols : J.dcols;
+        J.tiles_c = (wc + 31) / 32;
+        J.first_block = blocks;
+        blocks += (int64_t)((J.rows + 31) / 32) * J.tiles_c;
+        bytes += (double)J.rows * J.cols * 4.0 + (double)J.rows * wc * 2.0;
+    }
+    if (blocks == 0) return GCN_OK;
+    ProfScope ps(K_CVT_BF16, s, 0.0, bytes);
+    hipLaunchKernelGGL(prep_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, s, b);
+    GCN_LAUNCH_CHECK("prep_bf16_kernel");
+    return GCN_OK;
+}
+
 int cvt_bf16(int64_t rows, int64_t cols, const float *x, int64_t ldx, uint16_t *y, int64_t ldy,
              hipStream_t s) {
     return cvt_bf16_pad(rows, cols, x, ldx, y, ldy, cols, s);

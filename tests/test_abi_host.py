@@ -244,7 +244,10 @@ def test_model_workspace_is_the_largest_call(L):
     row ranges of A and A^T that it computes once for all of its SpMMs (one
     int32 per wavefront of at least 32 merge items, plus one), plus with
     bfloat16 operands the last layer's output as bfloat16 rows and transposed
-    rows for the head (2 x n x 2h bfloat16, each region 256-byte aligned)."""
+    rows for the head (2 x n x 2h bfloat16, each region 256-byte aligned) and
+    the step's weights converted up front: W_self^T and W_neigh^T of every
+    layer, W_self and W_neigh of a layer with an input gradient, W_pred padded
+    to 64 classes and W_pred^T."""
     layers = (B.gcn_layer_args * 2)(_layer_args(602, 128, dH=False), _layer_args(256, 128))
     head = B.gcn_head_args(0x4000, 0x4000, 41, B.GCN_SOFTMAX_CE, 0x4000, None, 0x4000, 0x4000, 256, 0x4000,
                            0x4000)
@@ -255,8 +258,11 @@ def test_model_workspace_is_the_largest_call(L):
         parts = [L.gcn_layer_workspace_bytes(n, nnz, 602, 128, B.GCN_AGGREGATE_FIRST, prec),
                  L.gcn_layer_workspace_bytes(n, nnz, 256, 128, B.GCN_AGGREGATE_FIRST, prec),
                  L.gcn_loss_workspace_bytes(n, 256, 41, prec)]
-        hl16 = 2 * ((n * 256 * 2 + 255) // 256 * 256) if prec == B.GCN_BF16 else 0
-        assert max(parts) + hl16 < need <= max(parts) + ranges + hl16
+        a256 = lambda b: (b + 255) // 256 * 256
+        hl16 = 2 * a256(n * 256 * 2) if prec == B.GCN_BF16 else 0
+        w16 = (2 * a256(602 * 128 * 2) + 4 * a256(256 * 128 * 2) + a256(256 * 64 * 2) + a256(256 * 41 * 2)
+               if prec == B.GCN_BF16 else 0)
+        assert max(parts) + hl16 + w16 < need <= max(parts) + ranges + hl16 + w16
 
 
 def test_device_validate_checks_arguments_before_launch(L):
