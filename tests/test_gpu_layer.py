@@ -111,7 +111,11 @@ def test_layer_backward(prec, tol, order, want_dH, shape, ws):
 
 @pytest.mark.parametrize("prec, tol", PRECS)
 @pytest.mark.parametrize("kind", ["ce", "bce"])
-@pytest.mark.parametrize("n, f, C", [(3000, 256, 41), (1001, 130, 100), (257, 64, 7)])
+# (the head's grouped row kernel takes up to 128 classes, 16 rows per block:
+# 257 and 5 rows leave part of a block empty, 128 classes fill its lanes,
+# 150 classes take the one-wavefront-per-row kernel and the separate sums)
+@pytest.mark.parametrize("n, f, C", [(3000, 256, 41), (1001, 130, 100), (257, 64, 7), (513, 96, 128), (700, 64, 150),
+                                     (5, 32, 3)])
 def test_loss_grad(prec, tol, kind, n, f, C, ws):
     rng = np.random.default_rng(n + C)
     HL = np.maximum(rng.standard_normal((n, f)), 0).astype(np.float32)
