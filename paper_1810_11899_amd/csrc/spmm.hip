@@ -189,7 +189,9 @@ __device__ __forceinline__ uint16_t bf16_round(float f) {
 // ovec: the VEC elements are one aligned vector (ldo a multiple of VEC and
 // `out` aligned to min(16, VEC * element size) bytes, and the same for
 // out16 when it is set), moved with 16-, 8- or 4-byte accesses instead of
-// one access per element.
+// one access per element.  bias (EPI_BIAS_RELU): the bias of column c, so
+// that bias[v] belongs to column c + v; the gather kernels pass their block's
+// copy in LDS, whose reads do not wait behind the row gathers in flight.
 template <int VEC>
 __device__ __forceinline__ void store16(uint16_t *__restrict__ o, const float (&x)[VEC], bool ovec) {
     if (VEC >= 2 && ovec) {
@@ -221,7 +223,7 @@ __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_
                 float x[4] = {acc[4 * q], acc[4 * q + 1], acc[4 * q + 2], acc[4 * q + 3]};
                 if (epi == EPI_BIAS_RELU) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) x[e] = fmaxf(x[e] + bias[c + 4 * q + e], 0.0f);
+                    for (int e = 0; e < 4; ++e) x[e] = fmaxf(x[e] + bias[4 * q + e], 0.0f);
                 } else if (epi == EPI_ACCUMULATE) {
                     const float4 p = *(const float4 *)(o + 4 * q);
                     x[0] = p.x + x[0]; x[1] = p.y + x[1]; x[2] = p.z + x[2]; x[3] = p.w + x[3];
@@ -233,7 +235,7 @@ __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_
 #pragma unroll
         for (int v = 0; v < VEC; ++v) {
             float x = acc[v];
-            if (epi == EPI_BIAS_RELU) x = fmaxf(x + bias[c + v], 0.0f);
+            if (epi == EPI_BIAS_RELU) x = fmaxf(x + bias[v], 0.0f);
             else if (epi == EPI_ACCUMULATE) x = o[v] + x;
             o[v] = x;
         }
@@ -242,7 +244,7 @@ __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_
     if constexpr (OM == 1) {   // the bfloat16 copy only: pack as the values are finished
         uint16_t *o16 = out16 + r * ld16 + c;
         auto fin = [&](int v) {
-            return epi == EPI_BIAS_RELU ? fmaxf(acc[v] + bias[c + v], 0.0f) : acc[v];
+            return epi == EPI_BIAS_RELU ? fmaxf(acc[v] + bias[v], 0.0f) : acc[v];
         };
         if (VEC >= 2 && ovec) {
             uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
@@ -264,7 +266,7 @@ __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_
     for (int v = 0; v < VEC; ++v) x[v] = acc[v];
     if (epi == EPI_BIAS_RELU) {
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) x[v] = fmaxf(x[v] + bias[c + v], 0.0f);
+        for (int v = 0; v < VEC; ++v) x[v] = fmaxf(x[v] + bias[v], 0.0f);
     } else if (epi == EPI_ACCUMULATE) {
         if (VEC >= 4 && ovec) {
 #pragma unroll
@@ -314,7 +316,15 @@ void spmm_main(
     const int lane = threadIdx.x & 63;
     const int wv = threadIdx.x >> 6;
     const int64_t wave = (int64_t)blockIdx.x * kWavesPerBlock + wv;
+    constexpr int SW = 64 * VEC * CT;
     __shared__ EdgeStage st;
+    // the bias of the block's column slice (published by stage_wave's barrier)
+    __shared__ float bias_s[SW];
+    if (epi == EPI_BIAS_RELU)
+        for (int i = threadIdx.x; i < SW; i += 256) {
+            const int c = blockIdx.y * SW + i;
+            bias_s[i] = c < k ? bias[c] : 0.0f;
+        }
     const bool live = wave < waves;
     const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, bnd, indptr, indices, vals);
     if (!live) return;
@@ -324,7 +334,6 @@ void spmm_main(
     const float *const e_val = st.val[wv];
     const int32_t *const r_ptr = st.ptr[wv];
 
-    constexpr int SW = 64 * VEC * CT;
     const int cbase = blockIdx.y * SW + lane * VEC;
     bool cok[CT];
 #pragma unroll
@@ -383,7 +392,7 @@ void spmm_main(
             for (int t = 0; t < CT; ++t)
                 if (cok[t]) {
                     const int c = cbase + t * 64 * VEC;
-                    emit<VEC, OM>(out, ldo, r, c, acc[t], epi, bias, ovec != 0, out16, ld16);
+                    emit<VEC, OM>(out, ldo, r, c, acc[t], epi, bias_s + lane * VEC + t * 64 * VEC, ovec != 0, out16, ld16);
                 }
         } else if (complete || pe > pb) {
             // a piece of a row cut by wavefront boundaries: head (the piece
@@ -449,6 +458,10 @@ void spmm_sliced(
     const int wv = threadIdx.x >> 6;
     const int64_t wave = chunk * kWavesPerBlock + wv;
     __shared__ EdgeStage st;
+    // the bias of the block's 64-column slice (published by stage_wave's barrier)
+    __shared__ float bias_s[64];
+    if (epi == EPI_BIAS_RELU && threadIdx.x < 64)
+        bias_s[threadIdx.x] = slice * 64 + (int)threadIdx.x < k ? bias[slice * 64 + threadIdx.x] : 0.0f;
     const bool live = wave < waves;
     const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, bnd, indptr, indices, vals);
     if (!live) return;
@@ -505,7 +518,7 @@ void spmm_sliced(
         const bool started = (r > r0) || (q0 == rb);
         if (g == 0 && cok) {
             if (complete && started) {
-                emit<4, 2>(out, ldo, r, col, acc, epi, bias, true, out16, ld16);   // aligned (host checks)
+                emit<4, 2>(out, ldo, r, col, acc, epi, bias_s + (lane & 15) * 4, true, out16, ld16);   // aligned (host checks)
             } else if (complete || pe > pb) {
                 const int slot = complete ? 0 : 1;
                 store_raw<4>(carry + (2 * wave + slot) * (int64_t)k + col, acc);
@@ -611,7 +624,7 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
         if (c >= k) continue;
         const float hv = carry[(2 * w) * (int64_t)k + c];
         const float a[1] = {any ? acc[j] + hv : hv};
-        emit<1, 2>(out, ldo, r, c, a, epi, bias, false, out16, ld16);
+        emit<1, 2>(out, ldo, r, c, a, epi, epi == EPI_BIAS_RELU ? bias + c : bias, false, out16, ld16);
     }
 }
 
@@ -670,6 +683,10 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
     dim3 grid((unsigned)((pl.waves + kWavesPerBlock - 1) / kWavesPerBlock), (unsigned)((k + sw - 1) / sw));
     if ((out16 && (epi == EPI_ACCUMULATE || epi == EPI_STORE_BF16)) || (!out && !out16)) {
         set_error("spmm: a bfloat16 copy goes with the store or bias+ReLU epilogue, and some output is needed");
+        return GCN_EINVAL;
+    }
+    if (epi == EPI_BIAS_RELU && !bias) {
+        set_error("spmm: the bias+ReLU epilogue needs a bias");
         return GCN_EINVAL;
     }
     const bool sliced = !bf16 && k % 4 == 0 && ldx % 4 == 0 && aligned(X, 16) && ldo % 4 == 0 &&
