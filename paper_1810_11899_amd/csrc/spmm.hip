@@ -570,46 +570,57 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
     const int lane = threadIdx.x & 63;
     const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     if (w >= waves) return;
+    // One round of independent loads: the head row of w, the tail rows of
+    // its 64 predecessors, w's own head piece and the tail piece of w - 1
+    // (the whole run in the common case of a row cut once; both slots are in
+    // bounds whether or not they were written), instead of four dependent
+    // rounds.
+    const int c0 = blockIdx.y * 256 + lane;
+    const int64_t q1 = w - 1 - lane;
+    const int32_t t1 = q1 >= 0 ? tail_row[q1] : -1;
     const int32_t r = head_row[w];
+    float hv[4], tv[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int c = c0 + 64 * j;
+        hv[j] = c < k ? carry[(2 * w) * (int64_t)k + c] : 0.0f;
+        tv[j] = c < k && w > 0 ? carry[(2 * w - 1) * (int64_t)k + c] : 0.0f;
+    }
     if (r < 0) return;
     // first wavefront of the run of wavefronts whose tail pieces belong to
     // row r, 64 predecessors per step (a long row spans many wavefronts)
+    uint64_t brk = __ballot(t1 != r);
     int64_t ws = w;
-    for (;;) {
+    while (brk == 0) {
+        ws -= 64;
         const int64_t q = ws - 1 - lane;
-        const bool same = q >= 0 && tail_row[q] == r;
-        const uint64_t brk = __ballot(!same);
-        if (brk == 0) {
-            ws -= 64;
-            continue;
-        }
-        ws -= __ffsll((unsigned long long)brk) - 1;
-        break;
+        brk = __ballot(!(q >= 0 && tail_row[q] == r));
     }
-    // four columns per lane; the pieces are added in wavefront order, eight
+    ws -= __ffsll((unsigned long long)brk) - 1;
+    // four columns per lane; the pieces are added in wavefront order, four
     // loads in flight per column
-    const int c0 = blockIdx.y * 256 + lane;
     float acc[4];
     bool any = false;
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[j] = 0.0f;
+    // the pieces of wavefronts ws .. w-2, then that of w-1 (loaded above)
     int64_t q = ws;
-    for (; q + 8 <= w; q += 8) {
-        float v[8][4];
+    for (; q + 4 <= w - 1; q += 4) {
+        float v[4][4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < 4; ++u)
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int c = c0 + 64 * j;
                 v[u][j] = c < k ? carry[(2 * (q + u) + 1) * (int64_t)k + c] : 0.0f;
             }
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < 4; ++u)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[j] = (any || u > 0) ? acc[j] + v[u][j] : v[u][j];
         any = true;
     }
-    for (; q < w; ++q) {
+    for (; q < w - 1; ++q) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int c = c0 + 64 * j;
@@ -618,12 +629,16 @@ __global__ __launch_bounds__(256) void spmm_fixup(int32_t k, void *__restrict__ 
         }
         any = true;
     }
+    if (ws < w) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j] = any ? acc[j] + tv[j] : tv[j];
+        any = true;
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         const int c = c0 + 64 * j;
         if (c >= k) continue;
-        const float hv = carry[(2 * w) * (int64_t)k + c];
-        const float a[1] = {any ? acc[j] + hv : hv};
+        const float a[1] = {any ? acc[j] + hv[j] : hv[j]};
         emit<1, 2>(out, ldo, r, c, a, epi, epi == EPI_BIAS_RELU ? bias + c : bias, false, out16, ld16);
     }
 }
