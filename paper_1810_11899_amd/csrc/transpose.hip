@@ -215,34 +215,66 @@ __global__ __launch_bounds__(kTB) void finalize_kernel(int32_t nnz, const int32_
 
 // Symmetric pattern: A^T has A's row pointers and indices; the value at
 // (row j, column i) is A's value at (i, j).
-// Pass 1, one wavefront per row i: whether the row's values are all the same
-// bits (true of every row of a mean aggregation matrix, Sec. II), in which
-// case that value is A(i, j) for every j.
+// Pass 1: whether row i's values are all the same bits (true of every row
+// of a mean aggregation matrix, Sec. II), in which case that value is
+// A(i, j) for every j.  A wavefront takes four rows, 16 lanes each: a row of
+// at most 64 entries is checked by its lane group with four loads per lane
+// in flight; the longer rows of the wavefront are then checked one at a time
+// by all 64 lanes with eight loads each in flight (a hub row of 14,000
+// entries is one wavefront's walk).  Four rows per wavefront, not one: the
+// pass is bound by the latency of its two dependent loads, and a quarter of
+// the wavefronts cover it in fewer rounds.
 __global__ __launch_bounds__(kTB) void sym_rows_kernel(int32_t n, const int32_t *__restrict__ indptr,
                                                        const float *__restrict__ vals,
                                                        uint32_t *__restrict__ rowval, int32_t *__restrict__ rowconst) {
-    const int64_t i = (int64_t)blockIdx.x * (kTB / 64) + (threadIdx.x >> 6);
-    if (i >= n) return;
     const int lane = threadIdx.x & 63;
-    const int32_t b = indptr[i], e = indptr[i + 1];
-    const uint32_t first = e > b ? __float_as_uint(vals[b]) : 0u;
-    bool same = true;
-    // eight loads in flight per lane: a hub row of 14,000 entries is one
-    // wavefront's serial walk
-    constexpr int U = 8;
-    int32_t p = b + lane;
-    for (; p + 64 * (U - 1) < e; p += 64 * U) {
-        uint32_t v[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = __float_as_uint(vals[p + 64 * u]);
-#pragma unroll
-        for (int u = 0; u < U; ++u) same = same && (v[u] == first);
+    const int g = lane >> 4, gl = lane & 15;
+    const int64_t i = ((int64_t)blockIdx.x * (kTB / 64) + (threadIdx.x >> 6)) * 4 + g;
+    const bool live = i < n;
+    int32_t b = 0, e = 0;
+    if (live) {
+        b = indptr[i];
+        e = indptr[i + 1];
     }
-    for (; p < e; p += 64) same = same && (__float_as_uint(vals[p]) == first);
-    const bool all_same = __all(same);
-    if (lane == 0) {
+    const bool shortrow = e - b <= 64;
+    const uint32_t first = live && e > b ? __float_as_uint(vals[b]) : 0u;
+    bool same = true;
+    if (live && shortrow) {
+        uint32_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int32_t p = b + gl + 16 * u;
+            v[u] = p < e ? __float_as_uint(vals[p]) : first;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) same = same && (v[u] == first);
+    }
+    const uint64_t bad = __ballot(!same);
+    bool row_same = ((bad >> (16 * g)) & 0xFFFFull) == 0;
+    // the long rows, one at a time (the loop is uniform over the wavefront)
+    uint64_t longs = __ballot(live && !shortrow && gl == 0);
+    while (longs) {
+        const int lg = (__ffsll((unsigned long long)longs) - 1) >> 4;
+        longs &= longs - 1;
+        const int32_t lb = __shfl(b, 16 * lg), le = __shfl(e, 16 * lg);
+        const uint32_t lf = __shfl(first, 16 * lg);
+        bool s2 = true;
+        constexpr int U = 8;
+        int32_t p = lb + lane;
+        for (; p + 64 * (U - 1) < le; p += 64 * U) {
+            uint32_t v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) v[u] = __float_as_uint(vals[p + 64 * u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) s2 = s2 && (v[u] == lf);
+        }
+        for (; p < le; p += 64) s2 = s2 && (__float_as_uint(vals[p]) == lf);
+        const bool all_same = __all(s2);
+        if (g == lg) row_same = all_same;
+    }
+    if (live && gl == 0) {
         rowval[i] = first;
-        rowconst[i] = all_same ? 1 : 0;
+        rowconst[i] = row_same ? 1 : 0;
     }
 }
 
@@ -400,7 +432,7 @@ int csr_transpose_symmetric(int32_t n, int32_t nnz, const int32_t *indptr, IdxRe
         return GCN_EWORKSPACE;
     }
     ProfScope ps(K_T_SYM, s, 0.0, (double)nnz * 12.0 + (double)n * 16.0);
-    hipLaunchKernelGGL(sym_rows_kernel, dim3((unsigned)((n + kTB / 64 - 1) / (kTB / 64))), dim3(kTB), 0, s, n,
+    hipLaunchKernelGGL(sym_rows_kernel, dim3((unsigned)((n + kTB / 16 - 1) / (kTB / 16))), dim3(kTB), 0, s, n,
                        indptr, vals, rowval, rowconst);
     unsigned g = (unsigned)std::min<int64_t>(((int64_t)nnz + kTB - 1) / kTB, 16384);
     hipLaunchKernelGGL(sym_vals_kernel, dim3(g), dim3(kTB), 0, s, n, nnz, indptr, indices, vals, rowval,
