@@ -690,7 +690,8 @@ def main():
         v = bench_step(args, "bf16", wl, B, torch, synth, float_outputs=False)
         variants["bf16"] = {k: v[k] for k in keys if k in v}
         variants["bf16"]["float_outputs"] = False
-        variants["bf16"]["config"] = {"workload": v["config"]["workload"]}
+        variants["bf16"]["config"] = {k: v["config"][k] for k in ("workload", "orders", "order_choice", "order_step_ms")
+                                      if k in v["config"]}
         v = bench_step(args, "f32", wl, B, torch, synth, index_bits=16,
                        orders=[B.GCN_AGGREGATE_FIRST if o == "aggregate_first" else B.GCN_TRANSFORM_FIRST
                                for o in out["config"]["orders"]])

@@ -46,6 +46,14 @@ constexpr int kMaxIpw = 256;   // merge items per wavefront, at most
 #ifndef GCN_SPMM_SLICED_WPE
 #define GCN_SPMM_SLICED_WPE 8
 #endif
+// bfloat16 rows on the XCD-sliced schedule (128-column slices): switch and
+// edges in flight per lane group
+#ifndef GCN_SPMM_BF16_SLICED
+#define GCN_SPMM_BF16_SLICED 1
+#endif
+#ifndef GCN_SPMM_BF16_U
+#define GCN_SPMM_BF16_U 4
+#endif
 
 
 // Smallest r in [0, n_rows] whose row-end item sits at merge position >= d,
@@ -421,7 +429,7 @@ void spmm_main(
 // gathers edges g, g+4, g+8, ... of the row (16 lanes x float4 = 64 columns),
 // and the four partial sums are combined with a fixed xor-shuffle tree.
 struct SliceMap {
-    int32_t slices;      // ceil(k / 64)
+    int32_t slices;      // ceil(k / slice width)
     int32_t chunks;      // block chunks of kWavesPerBlock wavefronts
     int32_t mode;        // 0: slice-major multiple of 8, 1: slice divides 8, 2: plain
     int32_t per_xcd;     // slices per XCD (mode 0) or XCDs per slice (mode 1)
@@ -534,9 +542,117 @@ void spmm_sliced(
     }
 }
 
-SliceMap make_slice_map(int32_t k, int64_t waves) {
+// The same schedule for bfloat16 rows: 128-column slices, so that a lane
+// group's piece of a row is again 16 lanes x 16 bytes (8 bfloat16 columns per
+// lane, kept as loaded words and widened on use) and an XCD's L2 holds 256
+// bytes of each hot row instead of the whole 1 KB row: at 512 columns each
+// slice goes to two XCDs, whose L2s then hold four times as many hot rows.
+// OM selects the epilogue's outputs as in spmm_main.
+template <int OM>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_SLICED_WPE)))
+void spmm_sliced_bf16(
+    int32_t n_rows, const int32_t *__restrict__ indptr, IdxRef indices,
+    const float *__restrict__ vals, const uint16_t *__restrict__ X, int32_t k, int64_t ldx,
+    void *__restrict__ out, int64_t ldo, int epi, const float *__restrict__ bias,
+    int64_t items, int ipw, int64_t waves, SliceMap map, const int32_t *__restrict__ bnd,
+    float *__restrict__ carry, int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row,
+    uint16_t *__restrict__ out16, int64_t ld16) {
+    constexpr int SWD = 128;
+    int slice;
+    int64_t chunk;
+    if (!slice_of_block(map, blockIdx.x, slice, chunk)) return;
+    const int lane = threadIdx.x & 63;
+    const int wv = threadIdx.x >> 6;
+    const int64_t wave = chunk * kWavesPerBlock + wv;
+    __shared__ EdgeStage st;
+    // the bias of the block's slice (published by stage_wave's barrier)
+    __shared__ float bias_s[SWD];
+    if (epi == EPI_BIAS_RELU && threadIdx.x < SWD)
+        bias_s[threadIdx.x] = slice * SWD + (int)threadIdx.x < k ? bias[slice * SWD + threadIdx.x] : 0.0f;
+    const bool live = wave < waves;
+    const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, bnd, indptr, indices, vals);
+    if (!live) return;
+    const int r0 = wr.r0, r1 = wr.r1;
+    const int64_t p0 = wr.p0, p1 = wr.p1;
+    const int32_t *const e_idx = st.idx[wv];
+    const float *const e_val = st.val[wv];
+    const int32_t *const r_ptr = st.ptr[wv];
+    const int g = lane >> 4;
+    const int col = slice * SWD + (lane & 15) * 8;
+    const bool cok = col < k;
+    constexpr int U = GCN_SPMM_BF16_U;
+
+    const int q0 = (int)p0;
+    int32_t hrow = -1, trow = -1;
+    for (int r = r0; r <= r1 && r < n_rows; ++r) {
+        const int rb = r_ptr[r - r0], re = r_ptr[r - r0 + 1];
+        const bool complete = r < r1;
+        const int pb = (q0 > rb ? q0 : rb) - q0;
+        const int pe = (complete ? re : (int)p1) - q0;
+        float a[8];
+#pragma unroll
+        for (int v = 0; v < 8; ++v) a[v] = 0.0f;
+        int p = pb + g;
+        for (; p + 4 * (U - 1) < pe; p += 4 * U) {
+            int32_t j[U];
+            float w[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + 4 * u]; w[u] = e_val[p + 4 * u]; }
+            Row<8, true> x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (cok) {
+                    x[u].load(X + (int64_t)j[u] * ldx + col);
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) x[u].w[q] = 0u;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int v = 0; v < 8; ++v) a[v] = fmaf(w[u], x[u].get(v), a[v]);
+        }
+        for (; p < pe; p += 4) {
+            const int32_t j = e_idx[p];
+            const float w = e_val[p];
+            Row<8, true> x;
+            if (cok) {
+                x.load(X + (int64_t)j * ldx + col);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) x.w[q] = 0u;
+            }
+#pragma unroll
+            for (int v = 0; v < 8; ++v) a[v] = fmaf(w, x.get(v), a[v]);
+        }
+        // groups (0,1) and (2,3), then the two pairs
+#pragma unroll
+        for (int v = 0; v < 8; ++v) a[v] += __shfl_xor(a[v], 16);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) a[v] += __shfl_xor(a[v], 32);
+        const bool started = (r > r0) || (q0 == rb);
+        if (g == 0 && cok) {
+            if (complete && started) {
+                emit<8, OM>(out, ldo, r, col, a, epi, bias_s + (lane & 15) * 8, true, out16, ld16);   // aligned (host checks)
+            } else if (complete || pe > pb) {
+                const int slot = complete ? 0 : 1;
+                store_raw<8>(carry + (2 * wave + slot) * (int64_t)k + col, a);
+            }
+        }
+        if (!(complete && started) && (complete || pe > pb)) {
+            if (complete) hrow = r; else trow = r;
+        }
+    }
+    if (slice == 0 && lane == 0) {
+        head_row[wave] = hrow;
+        tail_row[wave] = trow;
+    }
+}
+
+SliceMap make_slice_map(int32_t k, int64_t waves, int32_t width = 64) {
     SliceMap m;
-    m.slices = (k + 63) / 64;
+    m.slices = (k + width - 1) / width;
     const int64_t chunks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
     m.chunks = (int32_t)chunks;
     if (m.slices % 8 == 0) {
@@ -706,6 +822,11 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
     }
     const bool sliced = !bf16 && k % 4 == 0 && ldx % 4 == 0 && aligned(X, 16) && ldo % 4 == 0 &&
                         aligned(out, 16) && k >= 128 && (!out16 || (ld16 % 4 == 0 && aligned(out16, 8)));
+    // bfloat16 rows, 128-column slices: whole 8-column lane vectors and
+    // 16-byte aligned rows in and out
+    const bool sliced16 = GCN_SPMM_BF16_SLICED && bf16 && k >= 256 && k % 8 == 0 && ldx % 8 == 0 &&
+                          aligned(X, 16) && (!out || (ldo % 8 == 0 && aligned(out, 16))) &&
+                          (!out16 || (ld16 % 8 == 0 && aligned(out16, 16)));
     const double out_bytes = epi == EPI_STORE_BF16 ? 2.0 : (epi == EPI_ACCUMULATE ? 8.0 : 4.0);
     const double bytes = (double)nnz * k * esz + (double)nnz * (indices.i16 ? 6.0 : 8.0) + (double)(n_rows + 1) * 4.0 +
                          (double)n_rows * k * out_bytes;
@@ -724,6 +845,23 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
                                indices, vals, (const float *)X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw,
                                pl.waves, m, bnd, carry, hr, tr, out16, ld16);
             GCN_LAUNCH_CHECK("spmm_sliced");
+        } else if (sliced16) {
+            const SliceMap m = make_slice_map(k, pl.waves, 128);
+            const dim3 g16((unsigned)slice_map_blocks(m));
+            const uint16_t *X16 = (const uint16_t *)X;
+            if (out16 && out)
+                hipLaunchKernelGGL(spmm_sliced_bf16<2>, g16, dim3(256), 0, s, n_rows, indptr, indices, vals, X16, k,
+                                   ldx, out, ldo, epi, bias, pl.items, pl.ipw, pl.waves, m, bnd, carry, hr, tr, out16,
+                                   ld16);
+            else if (out16)
+                hipLaunchKernelGGL(spmm_sliced_bf16<1>, g16, dim3(256), 0, s, n_rows, indptr, indices, vals, X16, k,
+                                   ldx, nullptr, ldo, epi, bias, pl.items, pl.ipw, pl.waves, m, bnd, carry, hr, tr,
+                                   out16, ld16);
+            else
+                hipLaunchKernelGGL(spmm_sliced_bf16<0>, g16, dim3(256), 0, s, n_rows, indptr, indices, vals, X16, k,
+                                   ldx, out, ldo, epi, bias, pl.items, pl.ipw, pl.waves, m, bnd, carry, hr, tr,
+                                   nullptr, 0);
+            GCN_LAUNCH_CHECK("spmm_sliced_bf16");
         } else
 #define GCN_SPMM_CASE(V, C, B)                                                                   \
     if (vec == V && ct == C && bf16 == B) {                                                      \
