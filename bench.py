@@ -847,15 +847,16 @@ def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32, 
             # Cache, HBM).  `achieved` is the gathered row bytes per second
             # (one row of the aggregated width per stored edge); the peak is
             # the measured rate of random row gathers of the size its lane
-            # groups read from an L1-resident array (filled in once the
-            # machine ceilings are measured).  The gather-model bytes over
+            # groups read (256-byte row pieces: 64 float32 or 128 bfloat16
+            # columns on the sliced schedules) from an L1-resident array
+            # (filled in once the machine ceilings are measured).  The gather-model bytes over
             # 8 TB/s are kept beside it: above 1, since the caches serve most
             # gathers, so not a DRAM fraction.
             esz = 4 if name == "spmm" else 2
             achieved = work["edge_features"] * esz * args.steps / (ms / 1e3) / 1e9
             roof = {"bound": "gather", "kernel": name, "achieved": round(achieved, 1), "peak": None,
                     "unit": "GB/s", "frac": None, "peak_source": "measured L1-resident random-row gather",
-                    "gather_row_bytes": 256 if name == "spmm" else 1024,
+                    "gather_row_bytes": 256,
                     "hbm_frac_gather_model": round(bytes_ / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
         else:
             achieved = bytes_ / (ms / 1e3) / 1e9
