@@ -46,13 +46,22 @@ constexpr int kMaxIpw = 256;   // merge items per wavefront, at most
 #ifndef GCN_SPMM_SLICED_WPE
 #define GCN_SPMM_SLICED_WPE 8
 #endif
-// bfloat16 rows on the XCD-sliced schedule (128-column slices): switch and
-// edges in flight per lane group
+// bfloat16 rows on the XCD-sliced schedule: switch, edges in flight per lane
+// group, lanes per row piece and the occupancy target (measured at 512
+// columns: 32 lanes (256-column slices) 0.64 ms per step of three
+// aggregations, 16 lanes 0.72, 8 lanes 1.00, whole 1 KB rows unsliced 0.79;
+// 2, 6 or 8 edges in flight and 6 wavefronts per SIMD were slower)
 #ifndef GCN_SPMM_BF16_SLICED
 #define GCN_SPMM_BF16_SLICED 1
 #endif
 #ifndef GCN_SPMM_BF16_U
 #define GCN_SPMM_BF16_U 4
+#endif
+#ifndef GCN_SPMM_BF16_LP
+#define GCN_SPMM_BF16_LP 32   // lanes per row piece: 8, 16 or 32 (64, 128 or 256 columns)
+#endif
+#ifndef GCN_SPMM_BF16_WPE
+#define GCN_SPMM_BF16_WPE 8
 #endif
 
 
@@ -542,14 +551,15 @@ void spmm_sliced(
     }
 }
 
-// The same schedule for bfloat16 rows: 128-column slices, so that a lane
-// group's piece of a row is again 16 lanes x 16 bytes (8 bfloat16 columns per
-// lane, kept as loaded words and widened on use) and an XCD's L2 holds 256
-// bytes of each hot row instead of the whole 1 KB row: at 512 columns each
-// slice goes to two XCDs, whose L2s then hold four times as many hot rows.
+// The same schedule for bfloat16 rows.  A lane group of LP lanes gathers an
+// 8 * LP-column piece of a row (8 bfloat16 columns per lane, kept as loaded
+// words and widened on use), 64 / LP edges per gather instruction, and the
+// groups' sums are combined by a fixed xor-shuffle tree.  With 32 lanes at 512
+// columns there are two slices, each on four XCDs, whose L2s then hold
+// 512-byte pieces of twice as many hot rows as whole 1 KB rows would allow.
 // OM selects the epilogue's outputs as in spmm_main.
 template <int OM>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_SLICED_WPE)))
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(GCN_SPMM_BF16_WPE)))
 void spmm_sliced_bf16(
     int32_t n_rows, const int32_t *__restrict__ indptr, IdxRef indices,
     const float *__restrict__ vals, const uint16_t *__restrict__ X, int32_t k, int64_t ldx,
@@ -557,7 +567,10 @@ void spmm_sliced_bf16(
     int64_t items, int ipw, int64_t waves, SliceMap map, const int32_t *__restrict__ bnd,
     float *__restrict__ carry, int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row,
     uint16_t *__restrict__ out16, int64_t ld16) {
-    constexpr int SWD = 128;
+    constexpr int LP = GCN_SPMM_BF16_LP;   // lanes per row piece
+    constexpr int NG = 64 / LP;            // lane groups (edges per gather instruction)
+    constexpr int SWD = 8 * LP;
+    static_assert(LP == 8 || LP == 16 || LP == 32, "lane groups of 8, 16 or 32");
     int slice;
     int64_t chunk;
     if (!slice_of_block(map, blockIdx.x, slice, chunk)) return;
@@ -577,8 +590,8 @@ void spmm_sliced_bf16(
     const int32_t *const e_idx = st.idx[wv];
     const float *const e_val = st.val[wv];
     const int32_t *const r_ptr = st.ptr[wv];
-    const int g = lane >> 4;
-    const int col = slice * SWD + (lane & 15) * 8;
+    const int g = lane / LP;
+    const int col = slice * SWD + (lane % LP) * 8;
     const bool cok = col < k;
     constexpr int U = GCN_SPMM_BF16_U;
 
@@ -593,11 +606,11 @@ void spmm_sliced_bf16(
 #pragma unroll
         for (int v = 0; v < 8; ++v) a[v] = 0.0f;
         int p = pb + g;
-        for (; p + 4 * (U - 1) < pe; p += 4 * U) {
+        for (; p + NG * (U - 1) < pe; p += NG * U) {
             int32_t j[U];
             float w[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + 4 * u]; w[u] = e_val[p + 4 * u]; }
+            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + NG * u]; w[u] = e_val[p + NG * u]; }
             Row<8, true> x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -613,7 +626,7 @@ void spmm_sliced_bf16(
 #pragma unroll
                 for (int v = 0; v < 8; ++v) a[v] = fmaf(w[u], x[u].get(v), a[v]);
         }
-        for (; p < pe; p += 4) {
+        for (; p < pe; p += NG) {
             const int32_t j = e_idx[p];
             const float w = e_val[p];
             Row<8, true> x;
@@ -626,15 +639,15 @@ void spmm_sliced_bf16(
 #pragma unroll
             for (int v = 0; v < 8; ++v) a[v] = fmaf(w, x.get(v), a[v]);
         }
-        // groups (0,1) and (2,3), then the two pairs
+        // neighbouring groups, then pairs of pairs, ... (a fixed tree)
 #pragma unroll
-        for (int v = 0; v < 8; ++v) a[v] += __shfl_xor(a[v], 16);
+        for (int o = LP; o < 64; o *= 2)
 #pragma unroll
-        for (int v = 0; v < 8; ++v) a[v] += __shfl_xor(a[v], 32);
+            for (int v = 0; v < 8; ++v) a[v] += __shfl_xor(a[v], o);
         const bool started = (r > r0) || (q0 == rb);
         if (g == 0 && cok) {
             if (complete && started) {
-                emit<8, OM>(out, ldo, r, col, a, epi, bias_s + (lane & 15) * 8, true, out16, ld16);   // aligned (host checks)
+                emit<8, OM>(out, ldo, r, col, a, epi, bias_s + (lane % LP) * 8, true, out16, ld16);   // aligned (host checks)
             } else if (complete || pe > pb) {
                 const int slot = complete ? 0 : 1;
                 store_raw<8>(carry + (2 * wave + slot) * (int64_t)k + col, a);
@@ -822,7 +835,7 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
     }
     const bool sliced = !bf16 && k % 4 == 0 && ldx % 4 == 0 && aligned(X, 16) && ldo % 4 == 0 &&
                         aligned(out, 16) && k >= 128 && (!out16 || (ld16 % 4 == 0 && aligned(out16, 8)));
-    // bfloat16 rows, 128-column slices: whole 8-column lane vectors and
+    // bfloat16 rows on the sliced schedule: whole 8-column lane vectors and
     // 16-byte aligned rows in and out
     const bool sliced16 = GCN_SPMM_BF16_SLICED && bf16 && k >= 256 && k % 8 == 0 && ldx % 8 == 0 &&
                           aligned(X, 16) && (!out || (ldo % 8 == 0 && aligned(out, 16))) &&
@@ -846,7 +859,7 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
                                pl.waves, m, bnd, carry, hr, tr, out16, ld16);
             GCN_LAUNCH_CHECK("spmm_sliced");
         } else if (sliced16) {
-            const SliceMap m = make_slice_map(k, pl.waves, 128);
+            const SliceMap m = make_slice_map(k, pl.waves, 8 * GCN_SPMM_BF16_LP);
             const dim3 g16((unsigned)slice_map_blocks(m));
             const uint16_t *X16 = (const uint16_t *)X;
             if (out16 && out)
