@@ -46,6 +46,12 @@ constexpr int kMaxIpw = 256;   // merge items per wavefront, at most
 #ifndef GCN_SPMM_SLICED_WPE
 #define GCN_SPMM_SLICED_WPE 8
 #endif
+// float32 sliced kernel: lanes per row piece, 16 or 32 (64- or 128-column
+// slices; at 512 columns 32 lanes: 1.120 against 1.147 ms per step of three
+// aggregations)
+#ifndef GCN_SPMM_LP
+#define GCN_SPMM_LP 32
+#endif
 // bfloat16 rows on the XCD-sliced schedule: switch, edges in flight per lane
 // group, lanes per row piece and the occupancy target (measured at 512
 // columns: 32 lanes (256-column slices) 0.64 ms per step of three
@@ -429,14 +435,15 @@ void spmm_main(
 }
 
 // XCD-sliced variant (float32, k % 4 == 0).  The feature dimension is cut
-// into 64-column slices and workgroups are numbered so that, under the
-// round-robin workgroup-to-XCD dispatch, each XCD keeps gathering the same
-// slice: its 4 MB L2 then holds the hot rows of one slice (256 B per row)
-// instead of whole rows, which raises the hit rate on skewed graphs.  This is
-// the feature-only partitioning of Sec. V-B / Alg. 6, with the XCD L2 in the
-// role of the per-core cache.  Inside a wavefront, lane group g = lane / 16
-// gathers edges g, g+4, g+8, ... of the row (16 lanes x float4 = 64 columns),
-// and the four partial sums are combined with a fixed xor-shuffle tree.
+// into slices of 4 * LP columns (128 by default) and workgroups are numbered
+// so that, under the round-robin workgroup-to-XCD dispatch, each XCD keeps
+// gathering the same slice: its 4 MB L2 then holds the hot rows of one slice
+// (512 B per row at 128 columns) instead of whole rows, which raises the hit
+// rate on skewed graphs.  This is the feature-only partitioning of Sec. V-B /
+// Alg. 6, with the XCD L2 in the role of the per-core cache.  Inside a
+// wavefront, lane group g = lane / LP gathers edges g, g + 64/LP, ... of the
+// row (LP lanes x float4), and the groups' partial sums are combined with a
+// fixed xor-shuffle tree.
 struct SliceMap {
     int32_t slices;      // ceil(k / slice width)
     int32_t chunks;      // block chunks of kWavesPerBlock wavefronts
@@ -468,6 +475,10 @@ void spmm_sliced(
     int64_t items, int ipw, int64_t waves, SliceMap map, const int32_t *__restrict__ bnd,
     float *__restrict__ carry, int32_t *__restrict__ head_row, int32_t *__restrict__ tail_row,
     uint16_t *__restrict__ out16, int64_t ld16) {
+    constexpr int LP = GCN_SPMM_LP;   // lanes per row piece
+    constexpr int NG = 64 / LP;       // lane groups
+    constexpr int SWD = 4 * LP;       // slice width
+    static_assert(LP == 16 || LP == 32, "lane groups of 16 or 32");
     int slice;
     int64_t chunk;
     if (!slice_of_block(map, blockIdx.x, slice, chunk)) return;
@@ -475,10 +486,10 @@ void spmm_sliced(
     const int wv = threadIdx.x >> 6;
     const int64_t wave = chunk * kWavesPerBlock + wv;
     __shared__ EdgeStage st;
-    // the bias of the block's 64-column slice (published by stage_wave's barrier)
-    __shared__ float bias_s[64];
-    if (epi == EPI_BIAS_RELU && threadIdx.x < 64)
-        bias_s[threadIdx.x] = slice * 64 + (int)threadIdx.x < k ? bias[slice * 64 + threadIdx.x] : 0.0f;
+    // the bias of the block's slice (published by stage_wave's barrier)
+    __shared__ float bias_s[SWD];
+    if (epi == EPI_BIAS_RELU && threadIdx.x < SWD)
+        bias_s[threadIdx.x] = slice * SWD + (int)threadIdx.x < k ? bias[slice * SWD + threadIdx.x] : 0.0f;
     const bool live = wave < waves;
     const WaveRange wr = stage_wave(st, wv, lane, live, wave, ipw, items, n_rows, bnd, indptr, indices, vals);
     if (!live) return;
@@ -487,8 +498,8 @@ void spmm_sliced(
     const int32_t *const e_idx = st.idx[wv];
     const float *const e_val = st.val[wv];
     const int32_t *const r_ptr = st.ptr[wv];
-    const int g = lane >> 4;
-    const int col = slice * 64 + (lane & 15) * 4;
+    const int g = lane / LP;
+    const int col = slice * SWD + (lane % LP) * 4;
     const bool cok = col < k;
     constexpr int U = GCN_SPMM_U;  // edges per lane group in flight
 
@@ -502,11 +513,11 @@ void spmm_sliced(
         const int pe = (complete ? re : (int)p1) - q0;
         float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
         int p = pb + g;
-        for (; p + 4 * (U - 1) < pe; p += 4 * U) {
+        for (; p + NG * (U - 1) < pe; p += NG * U) {
             int32_t j[U];
             float w[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + 4 * u]; w[u] = e_val[p + 4 * u]; }
+            for (int u = 0; u < U; ++u) { j[u] = e_idx[p + NG * u]; w[u] = e_val[p + NG * u]; }
             float4 x[U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
@@ -519,7 +530,7 @@ void spmm_sliced(
                 a3 = fmaf(w[u], x[u].w, a3);
             }
         }
-        for (; p < pe; p += 4) {
+        for (; p < pe; p += NG) {
             const int32_t j = e_idx[p];
             const float w = e_val[p];
             const float4 x = cok ? *(const float4 *)(X + (int64_t)j * ldx + col) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -528,14 +539,16 @@ void spmm_sliced(
             a2 = fmaf(w, x.z, a2);
             a3 = fmaf(w, x.w, a3);
         }
-        // groups (0,1) and (2,3), then the two pairs
-        a0 += __shfl_xor(a0, 16); a1 += __shfl_xor(a1, 16); a2 += __shfl_xor(a2, 16); a3 += __shfl_xor(a3, 16);
-        a0 += __shfl_xor(a0, 32); a1 += __shfl_xor(a1, 32); a2 += __shfl_xor(a2, 32); a3 += __shfl_xor(a3, 32);
+        // neighbouring groups, then the pairs (a fixed tree)
+#pragma unroll
+        for (int o = LP; o < 64; o *= 2) {
+            a0 += __shfl_xor(a0, o); a1 += __shfl_xor(a1, o); a2 += __shfl_xor(a2, o); a3 += __shfl_xor(a3, o);
+        }
         const float acc[4] = {a0, a1, a2, a3};
         const bool started = (r > r0) || (q0 == rb);
         if (g == 0 && cok) {
             if (complete && started) {
-                emit<4, 2>(out, ldo, r, col, acc, epi, bias_s + (lane & 15) * 4, true, out16, ld16);   // aligned (host checks)
+                emit<4, 2>(out, ldo, r, col, acc, epi, bias_s + (lane % LP) * 4, true, out16, ld16);   // aligned (host checks)
             } else if (complete || pe > pb) {
                 const int slot = complete ? 0 : 1;
                 store_raw<4>(carry + (2 * wave + slot) * (int64_t)k + col, acc);
@@ -853,7 +866,7 @@ int spmm_any(bool bf16, int32_t n_rows, int32_t nnz, const int32_t *indptr, IdxR
             bnd = bnd_ws;
         }
         if (sliced) {
-            const SliceMap m = make_slice_map(k, pl.waves);
+            const SliceMap m = make_slice_map(k, pl.waves, 4 * GCN_SPMM_LP);
             hipLaunchKernelGGL(spmm_sliced, dim3((unsigned)slice_map_blocks(m)), dim3(256), 0, s, n_rows, indptr,
                                indices, vals, (const float *)X, k, ldx, out, ldo, epi, bias, pl.items, pl.ipw,
                                pl.waves, m, bnd, carry, hr, tr, out16, ld16);
