@@ -233,8 +233,9 @@ int colsum(int32_t n, int32_t C, const float *G, int64_t ldg, float *out, void *
 // Row-wise loss on logits X (n x C, ldx == C), in place: X <- G.  rowloss[n].
 int loss_rows(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,
               float *rowloss, hipStream_t s);
-// The head for up to 128 classes in two launches: G in place (and its
-// class-padded bfloat16 rows G16 when given), the loss and db = sum_i G[i, :]
+// The head for up to 128 classes in two launches: G in place of X, or, when
+// G16 is given, only G's class-padded bfloat16 rows G16 (X is then left as
+// the logits); the loss and db = sum_i G[i, :]
 bool loss_fused_ok(int32_t C);
 size_t loss_fused_workspace_bytes(int32_t n, int32_t C);
 int loss_fused(int kind, int32_t n, int32_t C, float *X, const int32_t *labels, const float *targets,

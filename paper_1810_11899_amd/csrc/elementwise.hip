@@ -294,10 +294,12 @@ __global__ __launch_bounds__(256) void loss_group_kernel(int kind, int32_t n, in
         }
         rl = gsum(sum);
     }
+    // G in place of the logits, or only its bfloat16 rows when those are
+    // asked for (the bfloat16 head reads nothing else)
 #pragma unroll
     for (int k = 0; k < V; ++k) {
         const int c = g + R * k;
-        if (live && c < C) x[c] = gr[k];
+        if (live && !G16 && c < C) x[c] = gr[k];
         if (live && G16 && c < Cp) G16[i * Cp + c] = c < C ? to_bf16(gr[k]) : (uint16_t)0;
     }
     // block sums: the four row groups of a wavefront share columns (lanes
