@@ -737,9 +737,9 @@ def spmm_vs_gather(o: dict, gather: dict):
     row an L2 hit), from one that fits only the Infinity Cache, and from one
     that comes mostly from HBM (above 1: the kernel's locality beats random
     rows from that level)."""
-    # per lane group on the XCD-sliced schedules, the float32 kernel gathers
-    # 256-byte pieces of a row, the bfloat16 one 512-byte pieces
-    for cls, row in (("spmm", 256), ("spmm_bf16", 512)):
+    # per lane group on the XCD-sliced schedules both kernels gather
+    # 512-byte pieces of a row (128 float32 or 256 bfloat16 columns)
+    for cls, row in (("spmm", 512), ("spmm_bf16", 512)):
         k = o.get("kernels", {}).get(cls)
         if not k or "gather_gbs" not in k:
             continue
@@ -847,17 +847,16 @@ def bench_step(args, prec_name: str, wl, B, torch, synth, index_bits: int = 32, 
             # Cache, HBM).  `achieved` is the gathered row bytes per second
             # (one row of the aggregated width per stored edge); the peak is
             # the measured rate of random row gathers of the size its lane
-            # groups read (on the sliced schedules, 256-byte pieces of 64
-            # float32 columns, 512-byte pieces of 256 bfloat16 columns) from
-            # an L1-resident array (filled in once the machine ceilings are
-            # measured).  The gather-model bytes over
+            # groups read (on the sliced schedules, 512-byte pieces: 128
+            # float32 or 256 bfloat16 columns) from an L1-resident array
+            # (filled in once the machine ceilings are measured).  The gather-model bytes over
             # 8 TB/s are kept beside it: above 1, since the caches serve most
             # gathers, so not a DRAM fraction.
             esz = 4 if name == "spmm" else 2
             achieved = work["edge_features"] * esz * args.steps / (ms / 1e3) / 1e9
             roof = {"bound": "gather", "kernel": name, "achieved": round(achieved, 1), "peak": None,
                     "unit": "GB/s", "frac": None, "peak_source": "measured L1-resident random-row gather",
-                    "gather_row_bytes": 256 if name == "spmm" else 512,
+                    "gather_row_bytes": 512,
                     "hbm_frac_gather_model": round(bytes_ / (ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
         else:
             achieved = bytes_ / (ms / 1e3) / 1e9
