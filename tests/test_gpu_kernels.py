@@ -201,6 +201,19 @@ def test_aggregate_bf16(k, ws):
     assert rel_inf(o, oracle.aggregate(g.indptr, g.indices, g.vals, obf16.round_bf16(X))) <= 1e-5
 
 
+@pytest.mark.parametrize("n, k", [(70000, 96), (70000, 512), (3, 512)])
+def test_aggregate_bf16_long_row_split_over_wavefronts(n, k, ws):
+    """A 70,000-entry hub row cut over ~270 wavefronts with bfloat16 rows: the
+    sliced schedule (512 columns) and the unsliced one (96), each against the
+    oracle on the bfloat16-rounded inputs (float32 accumulation only)."""
+    g = synth.star_graph(n)
+    X = np.random.default_rng(5).standard_normal((g.n, k)).astype(np.float32)
+    out = torch.empty((g.n, k), dtype=torch.float32, device="cuda")
+    B.gcn_aggregate(dcsr(g), dev(X), out, ws, prec=B.GCN_BF16)
+    ref = oracle.aggregate(g.indptr, g.indices, g.vals, obf16.round_bf16(X))
+    assert rel_inf(out.cpu().numpy(), ref) <= TOL_F32 / 10
+
+
 def test_bf16_conversion_bit_exact():
     rng = np.random.default_rng(0)
     x = np.concatenate([rng.standard_normal(100003).astype(np.float32) * 1e3,
