@@ -215,12 +215,16 @@ __device__ __forceinline__ uint16_t bf16_round(float f) {
 // one access per element.  bias (EPI_BIAS_RELU): the bias of column c, so
 // that bias[v] belongs to column c + v; the gather kernels pass their block's
 // copy in LDS, whose reads do not wait behind the row gathers in flight.
-template <int VEC>
+// HWR: pairs rounded by the gfx950 pair instruction (pack_bf16x2, the same
+// bits), where the kernel's register budget allows it
+template <int VEC, bool HWR = false>
 __device__ __forceinline__ void store16(uint16_t *__restrict__ o, const float (&x)[VEC], bool ovec) {
     if (VEC >= 2 && ovec) {
         uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
 #pragma unroll
-        for (int i = 0; i < VEC / 2; ++i) w[i] = (uint32_t)bf16_round(x[2 * i]) | ((uint32_t)bf16_round(x[2 * i + 1]) << 16);
+        for (int i = 0; i < VEC / 2; ++i)
+            w[i] = HWR ? pack_bf16x2(x[2 * i], x[2 * i + 1])
+                       : (uint32_t)bf16_round(x[2 * i]) | ((uint32_t)bf16_round(x[2 * i + 1]) << 16);
         if constexpr (VEC == 8) *(uint4 *)o = make_uint4(w[0], w[1], w[2], w[3]);
         else if constexpr (VEC == 4) *(uint2 *)o = make_uint2(w[0], w[1]);
         else *(uint32_t *)o = w[0];
@@ -230,12 +234,12 @@ __device__ __forceinline__ void store16(uint16_t *__restrict__ o, const float (&
     for (int v = 0; v < VEC; ++v) o[v] = bf16_round(x[v]);
 }
 
-template <int VEC, int OM = 0>
+template <int VEC, int OM = 0, bool HWR = false>
 __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_t r, int c,
                                      const float (&acc)[VEC], int epi, const float *__restrict__ bias,
                                      bool ovec, uint16_t *__restrict__ out16 = nullptr, int64_t ld16 = 0) {
     if (epi == EPI_STORE_BF16) {
-        store16<VEC>((uint16_t *)out + r * ldo + c, acc, ovec);
+        store16<VEC, HWR>((uint16_t *)out + r * ldo + c, acc, ovec);
         return;
     }
     if constexpr (OM == 0) {   // one float32 output
@@ -273,7 +277,8 @@ __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_
             uint32_t w[VEC / 2 > 0 ? VEC / 2 : 1];
 #pragma unroll
             for (int i = 0; i < VEC / 2; ++i)
-                w[i] = (uint32_t)bf16_round(fin(2 * i)) | ((uint32_t)bf16_round(fin(2 * i + 1)) << 16);
+                w[i] = HWR ? pack_bf16x2(fin(2 * i), fin(2 * i + 1))
+                           : (uint32_t)bf16_round(fin(2 * i)) | ((uint32_t)bf16_round(fin(2 * i + 1)) << 16);
             if constexpr (VEC == 8) *(uint4 *)o16 = make_uint4(w[0], w[1], w[2], w[3]);
             else if constexpr (VEC == 4) *(uint2 *)o16 = make_uint2(w[0], w[1]);
             else *(uint32_t *)o16 = w[0];
@@ -313,7 +318,7 @@ __device__ __forceinline__ void emit(void *__restrict__ out, int64_t ldo, int64_
             for (int v = 0; v < VEC; ++v) o[v] = x[v];
         }
     }
-    if (out16) store16<VEC>(out16 + r * ld16 + c, x, ovec);
+    if (out16) store16<VEC, HWR>(out16 + r * ld16 + c, x, ovec);
 }
 
 template <int VEC>
@@ -660,7 +665,7 @@ void spmm_sliced_bf16(
         const bool started = (r > r0) || (q0 == rb);
         if (g == 0 && cok) {
             if (complete && started) {
-                emit<8, OM>(out, ldo, r, col, a, epi, bias_s + (lane % LP) * 8, true, out16, ld16);   // aligned (host checks)
+                emit<8, OM, OM != 2>(out, ldo, r, col, a, epi, bias_s + (lane % LP) * 8, true, out16, ld16);   // aligned (host checks; the pair rounding where it fits the registers)
             } else if (complete || pe > pb) {
                 const int slot = complete ? 0 : 1;
                 store_raw<8>(carry + (2 * wave + slot) * (int64_t)k + col, a);
