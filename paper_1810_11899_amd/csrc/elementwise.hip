@@ -151,8 +151,18 @@ __global__ __launch_bounds__(256) void colsum_reduce_kernel(int32_t chunks, int3
     const int lane = threadIdx.x & 63;
     const int c = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (c >= C) return;
+    // a lane's chunks in order, eight loads in flight (the same sum as one
+    // load at a time)
     float s = 0.0f;
-    for (int k = lane; k < chunks; k += 64) s += part[(int64_t)k * C + c];
+    int k = lane;
+    for (; k + 64 * 7 < chunks; k += 64 * 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(k + 64 * u) * C + c];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; k < chunks; k += 64) s += part[(int64_t)k * C + c];
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
     if (lane == 0) out[c] = s;
